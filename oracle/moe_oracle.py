@@ -1,0 +1,371 @@
+"""fp64 CPU oracle for the MoE-layer hot path of Flux (federated MoE fine-tuning).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the CPU
+baseline leg of the benchmark may import this module.  The HIP library never
+calls it, and it shares no code, constant or helper with the HIP library: it is
+written from the paper's statement of the method, in plain NumPy, in float64.
+
+What each function follows:
+
+* Routing (Section 2.1, "MoE"): a gating network assigns each token to experts.
+  The paper gives no formula; the reading used here is the usual softmax gate
+  with top-k selection on the logits and renormalisation over the selected k,
+  ties broken towards the lower expert index.
+* Activation frequency (Section 2.2, Observation 2): tokens that activate an
+  expert divided by all tokens.
+* Quantisation-based profiling (Section 4.1): the same routing computed with a
+  low-bit copy of the weights.  Here the router is int8 with one symmetric scale
+  per expert row.
+* Expert merging (Section 5.3, Eq. 2): a weighted average of the weights of the
+  experts in a group, weights alpha_e normalised within the group.
+* Gate re-routing (Section 7): original experts are remapped to the slot that
+  now holds them, merged or not.
+* Tuning and non-tuning experts (Section 1, Section 3): tuning experts receive
+  weight gradients; non-tuning (merged, frozen) experts do not.
+* Expert FFN: SwiGLU, out = W_down (silu(W_gate x) * (W_up x)).
+
+Readings of silent or ambiguous points are listed in the design notes of the
+repository and restated at each function.  Every function here is pinned by
+tests that do not re-type its formula (brute force, closed forms, library
+routines on special cases, finite differences).
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+F64 = np.float64
+
+
+def _f64(a) -> np.ndarray:
+    a = np.asarray(a, dtype=F64)
+    assert np.all(np.isfinite(a)), "oracle inputs must be finite"
+    return a
+
+
+# ------------------------------------------------------------------ router --
+
+def router_logits(X, Wr, bias=None) -> np.ndarray:
+    """logit[t, e] = <X[t], Wr[e]> + bias[e], exactly (fp64, inputs exact)."""
+    X, Wr = _f64(X), _f64(Wr)
+    logits = X @ Wr.T
+    if bias is not None:
+        logits = logits + _f64(bias)[None, :]
+    return logits
+
+
+def topk_select(logits, k: int) -> np.ndarray:
+    """Indices of the k largest logits per row, in rank order.
+
+    Order is (logit descending, expert index ascending): on equal logits the
+    lower expert index ranks first.  A stable sort of the negated logits keeps
+    equal keys in index order, and -0.0 compares equal to +0.0.
+    """
+    logits = _f64(logits)
+    E = logits.shape[1]
+    assert 1 <= k <= E
+    order = np.argsort(-logits, axis=1, kind="stable")
+    return order[:, :k].astype(np.int64)
+
+
+def softmax_rows(z) -> np.ndarray:
+    z = _f64(z)
+    e = np.exp(z - z.max(axis=1, keepdims=True))
+    return e / e.sum(axis=1, keepdims=True)
+
+
+def route_topk(X, Wr, bias, k: int):
+    """Gate of one MoE layer: (idx [T,k], gate [T,k], logits [T,E]).
+
+    gate is the softmax over the k selected logits, which equals the softmax
+    over all E experts renormalised over the selected ones.
+    """
+    logits = router_logits(X, Wr, bias)
+    idx = topk_select(logits, k)
+    gate = softmax_rows(np.take_along_axis(logits, idx, axis=1))
+    return idx, gate, logits
+
+
+def topk_gap(logits, k: int) -> np.ndarray:
+    """logit_(k) - logit_(k+1) per row (inf when k == E): the selection margin."""
+    logits = _f64(logits)
+    s = -np.sort(-logits, axis=1)
+    if k >= logits.shape[1]:
+        return np.full(logits.shape[0], np.inf)
+    return s[:, k - 1] - s[:, k]
+
+
+# ------------------------------------------------------- int8 profiling ----
+
+def quantize_int8_rows(W):
+    """Per-row symmetric int8 quantisation of a router weight (Section 4.1).
+
+    s_e = max_i |W[e,i]| / 127 and q = clamp(round_half_even(W / s_e), -127, 127);
+    a zero row gets s_e = 0 and q = 0.  The division and the rounding decide an
+    integer, so they are done in float32, the precision of the kernel (W is a
+    bf16 or fp32 value, so max|W| is exact in float32 and the float32 quotient is
+    the correctly rounded one).
+    """
+    W32 = np.asarray(W, dtype=np.float32)
+    amax = np.max(np.abs(W32), axis=1)
+    s = (amax / np.float32(127.0)).astype(np.float32)
+    q = np.zeros(W32.shape, dtype=np.int8)
+    nz = s > 0
+    r = (W32[nz] / s[nz, None]).astype(np.float32)
+    q[nz] = np.clip(np.rint(r), -127, 127).astype(np.int8)
+    return q, s
+
+
+def profile_logits(X, q, s, bias=None) -> np.ndarray:
+    """Dequantised router logits: s_e * <X[t], q[e]> + bias[e] (fp64)."""
+    logits = _f64(X) @ np.asarray(q, dtype=F64).T * _f64(s)[None, :]
+    if bias is not None:
+        logits = logits + _f64(bias)[None, :]
+    return logits
+
+
+def profile_hist(X, q, s, bias, k: int):
+    """Activation histogram of the int8 profiling router: (counts [E], idx [T,k]).
+
+    counts[e] = number of tokens whose top-k set under the dequantised logits
+    contains e.  The activation frequency of Observation 2 is counts / T.
+    """
+    lg = profile_logits(X, q, s, bias)
+    idx = topk_select(lg, k)
+    counts = np.bincount(idx.ravel(), minlength=lg.shape[1]).astype(np.int64)
+    return counts, idx, lg
+
+
+# ------------------------------------------------------------ merge plan ----
+
+class MergePlan:
+    """Which slot holds which experts after merging (Sections 5.2 and 7).
+
+    kept[j]     original expert held unchanged by routed slot j (j < K)
+    groups[g]   original experts merged into routed slot K + g
+    tuning[s]   slot s receives weight gradients
+    expert_map  original expert -> routed slot (the re-routing table)
+    """
+
+    def __init__(self, E: int, kept: Sequence[int], groups: Sequence[Sequence[int]],
+                 n_tune: Optional[int] = None, tune_groups: bool = False):
+        self.E = E
+        self.kept = [int(e) for e in kept]
+        self.groups = [[int(e) for e in g] for g in groups]
+        K, G = len(self.kept), len(self.groups)
+        self.S = K + G
+        n_tune = K if n_tune is None else n_tune
+        self.tuning = np.array([j < n_tune for j in range(K)] + [tune_groups] * G)
+        self.expert_map = np.full(E, -1, dtype=np.int64)
+        for j, e in enumerate(self.kept):
+            self.expert_map[e] = j
+        for g, members in enumerate(self.groups):
+            for e in members:
+                self.expert_map[e] = K + g
+        assert np.all(self.expert_map >= 0), "every expert needs a slot"
+
+
+def frequency_merge_plan(counts, n_merge: int, group: int, n_tune: Optional[int] = None):
+    """Merge the n_merge least-activated experts, in groups of ``group``.
+
+    Experts are ranked by (count descending, index ascending).  The last n_merge
+    in that ranking are merged: walked from the least activated upwards, they
+    are cut into consecutive groups of ``group``.  Kept experts occupy the first
+    routed slots in ranking order, so the n_tune most activated kept experts are
+    slots 0..n_tune-1.  This rule stands in for the clustering of Section 5.2
+    (similar experts share a group), which is a later stage of this work.
+    """
+    counts = np.asarray(counts)
+    E = len(counts)
+    assert 0 <= n_merge <= E and n_merge % group == 0
+    rank = sorted(range(E), key=lambda e: (-int(counts[e]), e))
+    kept = rank[:E - n_merge]
+    tail = rank[E - n_merge:][::-1]
+    groups = [tail[i:i + group] for i in range(0, n_merge, group)]
+    return MergePlan(E, kept, groups, n_tune=n_tune)
+
+
+def explicit_merge_plan(E: int, groups: Sequence[Sequence[int]], tune_all: bool = True):
+    """Given groups; every other expert kept, in index order."""
+    grouped = {e for g in groups for e in g}
+    kept = [e for e in range(E) if e not in grouped]
+    return MergePlan(E, kept, groups, tune_groups=tune_all)
+
+
+# ------------------------------------------------------------------ merge ----
+
+def merge_weights(alpha, members: Sequence[int]) -> np.ndarray:
+    """Eq. 2 coefficients alpha_e / sum(alpha) over a group.
+
+    A group whose alphas sum to zero (none of its experts was activated) takes
+    the plain mean, the paper's "Avg." merging of Section 8.3.
+    """
+    a = _f64(alpha)[list(members)]
+    tot = a.sum()
+    if tot > 0:
+        return a / tot
+    return np.full(len(members), 1.0 / len(members))
+
+
+def merge_experts(W, members: Sequence[int], alpha) -> np.ndarray:
+    """Eq. 2: sum_e (alpha_e / sum alpha) W_e over the group, W stacked on axis 0."""
+    w = merge_weights(alpha, members)
+    out = np.zeros(np.shape(W)[1:], dtype=F64)
+    for coef, e in zip(w, members):
+        out += coef * _f64(W[e])
+    return out
+
+
+# ---------------------------------------------------------------- permute ----
+
+def permute_maps(idx, gate, expert_map, S_routed: int):
+    """Token -> slot buckets after gate re-routing (Section 7).
+
+    Each (token t, choice j) is mapped to slot = expert_map[idx[t, j]].  Choices
+    of one token that land on the same slot are one row of that slot, carrying
+    the sum of their gates.  Rows of a slot are ordered by token; slots are laid
+    out back to back (offsets = exclusive prefix sum of the row counts).
+
+    Returns offsets [S+1], perm_token [N], perm_gate [N] and inv [T, k] where
+    inv[t, j] = p for the choice that opened row p and -2 - p for a later choice
+    of the same token folded into row p.
+    """
+    idx = np.asarray(idx)
+    gate = _f64(gate)
+    expert_map = np.asarray(expert_map)
+    T, k = idx.shape
+    rows: List[List[tuple]] = [[] for _ in range(S_routed)]   # (t, first j)
+    owner = {}
+    for t in range(T):
+        for j in range(k):
+            s = int(expert_map[idx[t, j]])
+            assert 0 <= s < S_routed
+            if (t, s) not in owner:
+                owner[(t, s)] = j
+                rows[s].append(t)
+    counts = np.array([len(r) for r in rows], dtype=np.int64)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    N = int(offsets[-1])
+    perm_token = np.zeros(N, dtype=np.int64)
+    perm_gate = np.zeros(N, dtype=F64)
+    pos = {}
+    for s in range(S_routed):
+        for r, t in enumerate(rows[s]):
+            p = int(offsets[s]) + r
+            perm_token[p] = t
+            pos[(t, s)] = p
+    inv = np.zeros((T, k), dtype=np.int64)
+    for t in range(T):
+        for j in range(k):
+            s = int(expert_map[idx[t, j]])
+            p = pos[(t, s)]
+            perm_gate[p] += gate[t, j]
+            inv[t, j] = p if owner[(t, s)] == j else -2 - p
+    return offsets, perm_token, perm_gate, inv
+
+
+# ------------------------------------------------------------ expert FFN ----
+
+def sigmoid(z):
+    return 1.0 / (1.0 + np.exp(-z))
+
+
+def swiglu_fwd(x, Wg, Wu, Wd):
+    """One expert on rows x [n, d]: (a_g, a_u, h, o), o = h Wd^T, h = silu(a_g) a_u."""
+    x = _f64(x)
+    a_g = x @ _f64(Wg).T
+    a_u = x @ _f64(Wu).T
+    h = a_g * sigmoid(a_g) * a_u
+    o = h @ _f64(Wd).T
+    return a_g, a_u, h, o
+
+
+def swiglu_bwd(x, Wg, Wu, Wd, dO, want_dw: bool):
+    """Backward of one expert for output gradient dO [n, d].
+
+    Returns dx [n, d] and, if want_dw, (dWg [I,d], dWu [I,d], dWd [d,I]) as sums
+    over the rows (not means).
+    """
+    x, dO = _f64(x), _f64(dO)
+    a_g, a_u, h, _ = swiglu_fwd(x, Wg, Wu, Wd)
+    dh = dO @ _f64(Wd)
+    sg = sigmoid(a_g)
+    silu = a_g * sg
+    da_u = dh * silu
+    da_g = dh * a_u * sg * (1.0 + a_g * (1.0 - sg))
+    dx = da_g @ _f64(Wg) + da_u @ _f64(Wu)
+    if not want_dw:
+        return dx, None
+    return dx, (da_g.T @ x, da_u.T @ x, dO.T @ h)
+
+
+class SlotWeights:
+    """Per-slot expert weights of one layer: routed slots then shared experts."""
+
+    def __init__(self, wg, wu, wd, tuning, n_shared: int = 0):
+        self.wg, self.wu, self.wd = list(wg), list(wu), list(wd)
+        self.tuning = np.asarray(tuning, dtype=bool)
+        self.n_shared = n_shared
+        self.S = len(self.wg)
+        self.S_routed = self.S - n_shared
+        assert len(self.tuning) == self.S
+
+
+def _assignments(idx, expert_map, s):
+    slot = np.asarray(expert_map)[np.asarray(idx)]
+    return np.nonzero(slot == s)
+
+
+def moe_forward(X, idx, gate, expert_map, slots: SlotWeights):
+    """Y[t] = sum_j gate[t,j] FFN_{slot(t,j)}(X[t]) + sum_shared FFN_sh(X[t]).
+
+    Each (t, j) is its own assignment here (no folding of equal slots), which by
+    linearity equals the folded computation of the HIP path.
+    """
+    X, gate = _f64(X), _f64(gate)
+    Y = np.zeros_like(X)
+    for s in range(slots.S_routed):
+        t, j = _assignments(idx, expert_map, s)
+        if len(t) == 0:
+            continue
+        o = swiglu_fwd(X[t], slots.wg[s], slots.wu[s], slots.wd[s])[3]
+        np.add.at(Y, t, gate[t, j][:, None] * o)
+    for s in range(slots.S_routed, slots.S):
+        Y += swiglu_fwd(X, slots.wg[s], slots.wu[s], slots.wd[s])[3]
+    return Y
+
+
+def moe_backward(X, dY, idx, gate, expert_map, slots: SlotWeights):
+    """Expert-path gradients with the gates held constant.
+
+    Returns dX [T, d], dW {slot: (dWg, dWu, dWd)} for tuning slots (zero arrays
+    for a tuning slot with no rows) and dgate [T, k] = <dY[t], o_(t,j)>.
+    """
+    X, dY, gate = _f64(X), _f64(dY), _f64(gate)
+    T, d = X.shape
+    dX = np.zeros_like(X)
+    dgate = np.zeros(np.shape(idx), dtype=F64)
+    dW: Dict[int, tuple] = {}
+    for s in range(slots.S):
+        Wg, Wu, Wd = slots.wg[s], slots.wu[s], slots.wd[s]
+        I = np.shape(Wg)[0]
+        if s < slots.S_routed:
+            t, j = _assignments(idx, expert_map, s)
+            g = gate[t, j]
+        else:
+            t, j = np.arange(T), None
+            g = np.ones(T)
+        if len(t) == 0:
+            if slots.tuning[s]:
+                dW[s] = (np.zeros((I, d)), np.zeros((I, d)), np.zeros((d, I)))
+            continue
+        dO = g[:, None] * dY[t]
+        dx, dw = swiglu_bwd(X[t], Wg, Wu, Wd, dO, bool(slots.tuning[s]))
+        np.add.at(dX, t, dx)
+        if dw is not None:
+            dW[s] = dw
+        if j is not None:
+            o = swiglu_fwd(X[t], Wg, Wu, Wd)[3]
+            dgate[t, j] = np.sum(dY[t] * o, axis=1)
+    return dX, dW, dgate
