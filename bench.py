@@ -1,0 +1,212 @@
+"""Benchmark of one MoE-layer fine-tuning step on one MI355X.
+
+One step = one pass of the whole hot path over one batch:
+  int8 quantise + activation histogram -> merge plan + merge + slot tables ->
+  route -> permute -> grouped SwiGLU forward -> combine ->
+  combine backward -> grouped SwiGLU backward -> permute backward.
+Inputs are resident in HBM before timing.  Prints ONE JSON line.
+
+Default workload: the DeepSeek-MoE-16B-shaped layer (T=8192 tokens, d=2048,
+64 routed experts top-6 + 2 shared, I=1408, 32 least-activated experts merged
+into 8 groups), bf16 with fp32 accumulation, synthetic seeded data.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3        # MI355X fp32 matrix/vector
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="deepseek_moe")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-sample-tokens", type=int, default=192)
+    return p.parse_args()
+
+
+def ffn_flops(r, offsets):
+    """Algorithmic flops of the grouped SwiGLU forward and backward: 6 d I per
+    row forward; 6 d I per row backward for dX, plus 6 d I for the weight
+    gradients of tuning slots."""
+    w = r.w
+    per = 2 * w.d * w.I
+    rows = [int(offsets[s + 1] - offsets[s]) for s in range(r.S_r)] + [w.T] * w.n_shared
+    fwd = sum(3 * per * n for n in rows)
+    bwd = sum((3 + 3 * int(r.tuning[s])) * per * n for s, n in enumerate(rows))
+    return fwd, bwd
+
+
+def cpu_baseline(w, n_tok):
+    """The fp64 oracle on a bounded sample of the same workload (its first n_tok
+    tokens): routing, int8 histogram, merge plan + merge (all experts), permute
+    maps, forward and backward.  Reported in tokens/s of the sample."""
+    import numpy as np
+    import oracle as O
+    from paper_2508_19078_amd import workloads as W
+    from paper_2508_19078_amd.layer import LayerInputs
+
+    ws = W.scaled(w, T=n_tok)
+    inp = LayerInputs(ws)
+    t0 = time.perf_counter()
+    X = inp.X.f64()
+    b = inp.bias.astype(np.float64)
+    idx, gate, _ = O.route_topk(X, inp.Wr.f64(), b, w.k)
+    q, s = O.quantize_int8_rows(inp.Wr.f32())
+    counts, _, _ = O.profile_hist(X, q, s, b, w.k)
+    spec = W.layer_merge_spec(w, 0)
+    if spec is None:
+        plan = O.MergePlan(w.E, list(range(w.E)), [], n_tune=w.n_tune)
+    elif spec[0] == "groups":
+        plan = O.explicit_merge_plan(w.E, spec[1])
+    else:
+        plan = O.frequency_merge_plan(counts, spec[1], spec[2], n_tune=w.n_tune)
+    wg, wu, wd = (t.f64() for t in inp.experts)
+    alpha = counts / float(n_tok)
+    merged = [[O.merge_experts(M, g, alpha) for M in (wg, wu, wd)] for g in plan.groups]
+    sl = [[], [], []]
+    for e in plan.kept:
+        for i, M in enumerate((wg, wu, wd)):
+            sl[i].append(M[e])
+    for m in merged:
+        for i in range(3):
+            sl[i].append(m[i])
+    tuning = list(plan.tuning)
+    if w.n_shared:
+        sh = [t.f64() for t in inp.shared]
+        for j in range(w.n_shared):
+            for i in range(3):
+                sl[i].append(sh[i][j])
+            tuning.append(True)
+    slots = O.SlotWeights(sl[0], sl[1], sl[2], tuning, n_shared=w.n_shared)
+    O.permute_maps(idx, gate, plan.expert_map, plan.S)
+    O.moe_forward(X, idx, gate, plan.expert_map, slots)
+    O.moe_backward(X, inp.dY.f64(), idx, gate, plan.expert_map, slots)
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": round(n_tok / dt, 2), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n_tok} of {w.T} tokens of the same workload, full fp64 layer step "
+                      f"(route, int8 histogram, plan+merge of all experts, permute, fwd+bwd); "
+                      f"{dt:.1f} s on the host"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (this build has no multi-GPU path); got --gpus {a.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2508_19078_amd import api, workloads as W
+    from paper_2508_19078_amd.layer import LayerInputs, MoELayerRunner
+
+    if not os.path.exists(api.LIB_PATH):
+        from paper_2508_19078_amd import build
+        build.build()
+    w = W.WORKLOADS[a.workload]
+    print(f"# workload {w.name}: drawing inputs", file=sys.stderr, flush=True)
+    inp = LayerInputs(w)
+    r = MoELayerRunner(w, inp)
+    torch.cuda.synchronize()
+    print("# inputs resident; warming up", file=sys.stderr, flush=True)
+    st = torch.cuda.current_stream()
+
+    # per-entry-point events, recorded on the stream the kernels run on
+    names = ["profile", "merge", "route", "permute", "ffn_fwd", "combine", "combine_bwd", "ffn_bwd",
+             "permute_bwd"]
+
+    def timed_step(evs):
+        def mark(i):
+            evs[i].record(st)
+        mark(0); r.profile()
+        mark(1); r.merge()
+        mark(2); r.route()
+        mark(3)
+        api.moe_permute(r.X, r.idx, r.gate, r.expert_map, r.S_r, r.offsets, r.perm_token, r.perm_gate, r.inv,
+                        r.X_perm, r.ws_perm, E=w.E)
+        mark(4)
+        api.moe_grouped_swiglu_fwd(r.layer_tables, r.X, r.X_perm, r.offsets, w.T, w.k, r.A_g, r.A_u, r.H, r.O,
+                                   r.ws_fwd)
+        mark(5)
+        api.moe_unpermute(r.layer_tables, r.O, r.inv, r.perm_gate, w.T, w.k, r.Y)
+        mark(6)
+        api.moe_unpermute_bwd(r.layer_tables, r.dY, r.O, r.inv, r.offsets, r.perm_gate, w.T, w.k, r.dO, None)
+        mark(7)
+        api.moe_grouped_swiglu_bwd(r.layer_tables, r.X, r.X_perm, r.offsets, w.T, w.k, r.A_g, r.A_u, r.H, r.dO,
+                                   r.dX_perm, 0, r.ws_bwd)
+        mark(8)
+        api.moe_permute_bwd(r.layer_tables, r.dX_perm, r.inv, w.T, w.k, r.dX)
+        mark(9)
+
+    for _ in range(a.warmup):
+        r.step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(10)] for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        timed_step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = {n: float(np.mean([events[i][j].elapsed_time(events[i][j + 1]) for i in range(a.steps)]))
+           for j, n in enumerate(names)}
+    ms_step = wall * 1e3 / a.steps
+    tok_s = w.T / (ms_step / 1e3)
+
+    offsets = r.offsets.cpu().numpy()
+    fl_fwd, fl_bwd = ffn_flops(r, offsets)
+    ffn_ms = per["ffn_fwd"] + per["ffn_bwd"]
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = (fl_fwd + fl_bwd) / (ffn_ms * 1e-3) / 1e12
+    N = int(offsets[-1])
+    b = w.x_bytes
+    route_bytes = w.T * w.d * b + w.E * w.d * b + w.T * w.k * 8
+    permute_bytes = w.T * w.d * b + N * w.d * b + w.T * w.k * 8 + N * 12 + 4 * (r.S_r + 1)
+    merge_bytes = (w.E - r.K + r.G) * 3 * w.d * w.I * b if r.G else 0
+    hist_bytes = w.T * w.d * b + w.E * w.d + 12 * w.E
+    gbs = lambda by, ms: round(by / (ms * 1e-3) / 1e9, 1) if ms > 0 else None
+    out = {
+        "metric": "MoE-layer fwd+bwd tokens/sec on 1 MI355X",
+        "value": round(tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded normal draws shaped like the paper's workload; no dataset or checkpoint)",
+        "config": {"workload": f"{w.name}: T={w.T} d={w.d} E={w.E}+{w.n_shared} shared k={w.k} I={w.I}"
+                               + (f" merge={W.layer_merge_spec(w)}" if w.merge else ""),
+                   "global_batch": w.T, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "kernel": "grouped SwiGLU fwd+bwd (moe_grouped_swiglu_fwd + _bwd)",
+                     "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "flops_per_step": fl_fwd + fl_bwd, "ms": round(ffn_ms, 4)},
+        "stages_ms": {k: round(v, 4) for k, v in per.items()},
+        "hbm_kernels_GBps": {"route": gbs(route_bytes, per["route"]), "profile": gbs(hist_bytes, per["profile"]),
+                             "merge": gbs(merge_bytes, per["merge"]), "permute": gbs(permute_bytes, per["permute"])},
+    }
+    if not a.no_cpu_baseline:
+        print("# timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, a.cpu_sample_tokens)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,270 @@
+/*
+ * fluxmoe.h - C ABI of the MoE-layer hot path of Flux (federated fine-tuning of
+ * sparsely activated LLMs), hand-written HIP for MI355X (gfx950).
+ *
+ * The layer each participant runs during local fine-tuning:
+ *   route (softmax top-k gate)  ->  re-route to slots and permute into per-slot
+ *   buckets  ->  grouped SwiGLU expert FFN  ->  gate-weighted combine,
+ * and its backward; plus the two once-per-round steps that build the layer:
+ *   int8 profiling histogram (activation frequencies)  ->  expert merging.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.   Every tensor argument is caller-owned DEVICE memory, dense and
+ *           row-major, unless the comment says "host".  Tensor pointers must be
+ *           16-byte aligned (MOE_ERR_ALIGN otherwise).  The library allocates
+ *           nothing: calls that need scratch take (ws, ws_bytes), sized by the
+ *           matching *_workspace_size() function; too small -> MOE_ERR_WORKSPACE.
+ * Streams.  `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *           Every call only enqueues work on it and returns; nothing
+ *           synchronises the host.  The library keeps no state between calls.
+ * Dtypes.   MOE_F32 or MOE_BF16 for activations and weights (one dtype per
+ *           call), MOE_I8 for quantised codes.  Index arrays are int32,
+ *           gates and scales fp32.  bf16 math accumulates in fp32.
+ * Limits.   1 <= k <= min(E, 16), 1 <= E <= 256, d % 8 == 0, I % 8 == 0,
+ *           T >= 0 (T == 0 is a no-op), slot counts <= 512.  Anything else:
+ *           MOE_ERR_UNSUPPORTED or MOE_ERR_ARG.
+ * Errors.   Every function returns MOE_OK or an error code.  Arguments are
+ *           validated on the host before any HIP call, so an invalid call
+ *           enqueues nothing.  moe_last_error() gives a message for the last
+ *           failure on the calling thread.  No C++ exception crosses the ABI.
+ * Outputs.  Fully overwritten, except `counts` of moe_profile_hist (adds) and
+ *           the weight gradients of moe_grouped_swiglu_bwd when accumulate_dw.
+ */
+#ifndef FLUXMOE_H
+#define FLUXMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  MOE_OK = 0,
+  MOE_ERR_ARG = 1,          /* null required pointer, negative or inconsistent size */
+  MOE_ERR_UNSUPPORTED = 2,  /* outside the limits above, or an unsupported dtype */
+  MOE_ERR_ALIGN = 3,        /* tensor pointer not 16-byte aligned */
+  MOE_ERR_WORKSPACE = 4,    /* workspace missing or too small */
+  MOE_ERR_HIP = 5           /* a HIP launch failed (message has the HIP error) */
+};
+
+enum { MOE_F32 = 0, MOE_BF16 = 1, MOE_I8 = 2 };
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* moe_last_error(void);
+/* ABI revision of this header. */
+int moe_abi_version(void);
+#define FLUXMOE_ABI_VERSION 1
+
+/* ---------------------------------------------------------------- routing --
+ * moe_route_topk: the gating network of an MoE layer (Section 2.1, "MoE":
+ * tokens pass through a gating network that assigns them to experts).  The
+ * paper gives no formula; this is the softmax gate with top-k:
+ *   logit[t,e] = sum_i X[t,i] * Wr[e,i] + bias[e]      (fp32 accumulation)
+ *   idx[t,:]   = the k experts of largest logit, in rank order; equal logits
+ *                rank the lower expert index first (-0.0 equals +0.0)
+ *   gate[t,j]  = exp(logit[t,idx[t,j]]) / sum_j' exp(logit[t,idx[t,j']])
+ *                (= softmax over all E renormalised over the selected k)
+ * X [T,d], Wr [E,d] in `dtype`; bias [E] fp32 or NULL; idx [T,k] int32;
+ * gate [T,k] fp32; logits [T,E] fp32 or NULL (written when given).
+ */
+int moe_route_topk(const void* X, const void* Wr, int dtype, const float* bias,
+                   int T, int d, int E, int k,
+                   int32_t* idx, float* gate, float* logits, void* stream);
+
+/* ------------------------------------------------- quantisation profiling --
+ * moe_quantize_int8: the low-bit profiling copy of a weight matrix
+ * (Section 4.1, quantisation-based local profiling), one symmetric scale per
+ * row: scale[e] = max_i |W[e,i]| / 127 (fp32 division);
+ * Wq[e,i] = clamp(round_half_even(W[e,i] / scale[e]), -127, 127) with the
+ * quotient in fp32; a zero row gets scale 0 and codes 0.
+ * W [E,d] in `dtype`; Wq [E,d] int8; scale [E] fp32.  Here E is any row
+ * count >= 1 (not limited to 256).
+ */
+int moe_quantize_int8(const void* W, int dtype, int E, int d,
+                      int8_t* Wq, float* scale, void* stream);
+
+/* moe_profile_hist: expert activation histogram of the int8 profiling router
+ * (Section 4.1; the activation frequency of Section 2.2, Observation 2, is
+ * counts[e] / tokens).
+ *   logit~[t,e] = scale[e] * sum_i X[t,i] * Wq[e,i] + bias[e]
+ *   top-k of logit~ with the rule of moe_route_topk, then
+ *   counts[e] += #{t : e in top-k(t)}          (ADDS to counts; int32)
+ * X [T,d] in x_dtype (MOE_F32 / MOE_BF16); Wq [E,d] int8; scale [E] fp32;
+ * bias [E] fp32 or NULL; counts [E] int32; idx [T,k] int32 or NULL.
+ * Integer atomics only: the result does not depend on scheduling.
+ */
+int moe_profile_hist(const void* X, int x_dtype, const int8_t* Wq,
+                     const float* scale, const float* bias,
+                     int T, int d, int E, int k,
+                     int32_t* counts, int32_t* idx, void* stream);
+
+/* ---------------------------------------------------------------- merging --
+ * moe_merge_plan: which experts of one layer are merged, from its histogram
+ * (Sections 5.1-5.2 decide how many and which experts share a group; this
+ * entry point implements the frequency rule: the least-activated experts are
+ * merged).  Experts are ranked by (counts desc, index asc).  The last n_merge
+ * are merged: walked from the least activated upwards they are cut into
+ * consecutive groups of `group`.  Kept experts take routed slots 0..K-1 in
+ * rank order (K = E - n_merge), group g takes slot K + g.
+ * Outputs (device, int32 unless noted):
+ *   expert_map[E]        original expert -> routed slot (gate re-routing, Sec. 7)
+ *   slot_src[K + G]      kept slot j -> its expert; group slot K+g -> E + g
+ *   grp_ptr[grp_base .. grp_base+G]   CSR row pointers of the groups, values
+ *                        offset by member_base (entries of the whole CSR
+ *                        outside this range are not touched)
+ *   grp_member[member_base .. member_base+n_merge)  expert_base + expert id
+ *   alpha[expert_base .. expert_base+E) (fp32) = counts[e] / total_tokens,
+ *                        the activation frequency f_e
+ * Several layers write disjoint ranges of one CSR so that one
+ * moe_merge_experts call merges them all.  n_merge % group == 0, group >= 1.
+ */
+int moe_merge_plan(const int32_t* counts, int E, int n_merge, int group,
+                   float total_tokens, int expert_base, int grp_base, int member_base,
+                   int32_t* expert_map, int32_t* slot_src, int32_t* grp_ptr,
+                   int32_t* grp_member, float* alpha, void* stream);
+
+/* moe_activation_frequency: freq[e] = counts[e] / total_tokens, the activation
+ * frequency of Section 2.2 (Observation 2).  counts [E] int32, freq [E] fp32.
+ */
+int moe_activation_frequency(const int32_t* counts, int E, float total_tokens, float* freq,
+                             void* stream);
+
+/* moe_merge_experts: importance-weighted merging of grouped experts
+ * (Section 5.3, Eq. 2):  W_g = sum_{e in g} (alpha_e / sum_{e' in g} alpha_e') W_e
+ * for each of the expert's three matrices; a group whose alphas sum to 0 takes
+ * the plain mean.  fp32 accumulation, one rounding on store.
+ *   w_src: device array of 3*E_total device pointers, (gate, up, down) of
+ *          expert e at [3e, 3e+1, 3e+2]; gate/up are [I,d], down is [d,I].
+ *   grp_ptr[G+1], grp_member[grp_ptr[G]]: CSR of expert ids (into w_src/alpha).
+ *   alpha[E_total] fp32 (the paper's f_e * a_e; any non-negative weights).
+ *   w_dst: device array of 3*G device pointers, outputs in out_dtype.
+ * Groups may span layers: this is the single launch that merges every layer.
+ */
+int moe_merge_experts(const void* const* w_src, int dtype, int d, int I, int G,
+                      const int32_t* grp_ptr, const int32_t* grp_member,
+                      const float* alpha, void* const* w_dst, int out_dtype,
+                      void* stream);
+
+/* moe_slot_pointers: per-slot weight pointer tables of a layer after merging.
+ * Slot s < S reads from orig_*[slot_src[s]] when slot_src[s] < E and from
+ * merged_*[slot_src[s] - E] otherwise (stacked [E or G][rows][cols] tensors).
+ * Writes w_gate[s], w_up[s], w_down[s] (device arrays of device pointers) for
+ * s in [0, S); the caller appends shared experts after them.
+ */
+int moe_slot_pointers(const int32_t* slot_src, int S, int E, int d, int I, int dtype,
+                      const void* orig_gate, const void* orig_up, const void* orig_down,
+                      const void* merged_gate, const void* merged_up,
+                      const void* merged_down,
+                      const void** w_gate, const void** w_up, const void** w_down,
+                      void* stream);
+
+/* ------------------------------------------------------------ the layer ----
+ * A layer's slots: routed slots 0..S_routed-1 (kept experts and merged
+ * groups), then S_shared always-on shared experts (gate 1.0, every token).
+ * All pointer members are DEVICE arrays of S_routed + S_shared device pointers.
+ * Non-tuning (merged, frozen) slots have dw_* == NULL: they get dX but no dW
+ * (Section 1 and Section 3: non-tuning experts are merged and frozen).
+ *
+ * Row spaces.  For T tokens and top-k, routed rows live at [0, T*k) of every
+ * per-row buffer (X_perm, A_g, A_u, H, O, dO, dX_perm), slot s at
+ * [offsets[s], offsets[s+1]); rows from offsets[S_routed] to T*k are unused.
+ * Shared slot i owns rows [T*k + i*T, T*k + (i+1)*T), one per token.  So
+ * per-row buffers have R_tot = T*(k + S_shared) rows.
+ */
+typedef struct moe_layer {
+  int d;            /* hidden size */
+  int I;            /* expert intermediate size */
+  int dtype;        /* MOE_F32 or MOE_BF16: weights and activations */
+  int S_routed;     /* routed slots */
+  int S_shared;     /* shared experts */
+  const void* const* w_gate;   /* [S] -> [I,d] */
+  const void* const* w_up;     /* [S] -> [I,d] */
+  const void* const* w_down;   /* [S] -> [d,I] */
+  float* const* dw_gate;       /* [S] -> [I,d] fp32, NULL = frozen slot */
+  float* const* dw_up;         /* [S] -> [I,d] fp32, NULL = frozen slot */
+  float* const* dw_down;       /* [S] -> [d,I] fp32, NULL = frozen slot */
+} moe_layer;
+
+/* moe_permute: gate re-routing (Section 7) and the per-slot token subsets D^e
+ * of Section 4.1 as contiguous buckets.
+ *   slot[t,j] = expert_map[idx[t,j]]   (identity when expert_map is NULL)
+ *   choices of one token that land on the same slot form one row whose gate
+ *   is their sum (in j order); rows of a slot are ordered by token;
+ *   offsets = exclusive prefix sum of the per-slot row counts.
+ * Outputs: offsets[S_routed+1]; perm_token[T*k] (row -> token); perm_gate[T*k]
+ * fp32; inv[T,k]: p for the choice that opened row p, -2-p for a choice folded
+ * into row p; X_perm[T*k, d] with X_perm[p] = X[perm_token[p]].  Entries at or
+ * beyond offsets[S_routed] are left untouched.  idx values must be in [0, E)
+ * and expert_map values in [0, S_routed) (not checked on the device).
+ */
+int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
+                const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
+                int32_t* offsets, int32_t* perm_token, float* perm_gate,
+                int32_t* inv, void* X_perm, void* ws, size_t ws_bytes, void* stream);
+size_t moe_permute_workspace_size(int T, int k, int S_routed);
+
+/* moe_grouped_swiglu_fwd: every slot's SwiGLU expert FFN on its rows
+ * (the experts of Section 2.1; tuning and frozen slots alike):
+ *   A_g = X_s W_gate^T,  A_u = X_s W_up^T,  H = silu(A_g) * A_u,  O = H W_down^T
+ * with silu(z) = z / (1 + exp(-z)).  Routed slots read X_perm rows
+ * [offsets[s], offsets[s+1]); shared slots read X [T,d].
+ * Outputs (per-row buffers of R_tot rows, `L->dtype`): A_g, A_u, H [R_tot, I]
+ * (kept for the backward) and O [R_tot, d].
+ */
+int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const void* X_perm,
+                           const int32_t* offsets, int T, int k,
+                           void* A_g, void* A_u, void* H, void* O,
+                           void* ws, size_t ws_bytes, void* stream);
+size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int T, int k);
+
+/* moe_unpermute: the gate-weighted combine of the expert outputs
+ *   Y[t] = sum_{j: inv[t,j] >= 0} perm_gate[inv[t,j]] * O[inv[t,j]]
+ *          + sum_{shared i} O[T*k + i*T + t]              (fp32 accumulation)
+ * O [R_tot, d] and Y [T, d] in L->dtype.
+ */
+int moe_unpermute(const moe_layer* L, const void* O, const int32_t* inv,
+                  const float* perm_gate, int T, int k, void* Y, void* stream);
+
+/* moe_unpermute_bwd: backward of the combine with the gates as constants:
+ *   dO[p] = perm_gate[p] * dY[perm_token[p]]  for routed rows p < offsets[S_routed]
+ *   dO[T*k + i*T + t] = dY[t]                  for shared slot i
+ *   dgate[t,j] = <dY[t], O[row of (t,j)]>      (optional, fp32, when dgate != NULL;
+ *                folded choices read the row they were folded into)
+ */
+int moe_unpermute_bwd(const moe_layer* L, const void* dY, const void* O,
+                      const int32_t* inv, const int32_t* offsets,
+                      const float* perm_gate, int T, int k,
+                      void* dO, float* dgate, void* stream);
+
+/* moe_grouped_swiglu_bwd: backward of every slot's SwiGLU FFN:
+ *   dH   = dO W_down
+ *   dA_u = dH * silu(A_g)
+ *   dA_g = dH * A_u * s * (1 + A_g (1 - s)),  s = sigmoid(A_g)
+ *   dX_s = dA_g W_gate + dA_u W_up                 -> dX_perm rows (all slots)
+ *   tuning slots only (dw_* != NULL), sums over the slot's rows in fp32:
+ *   dW_down = dO^T H,  dW_gate = dA_g^T X_s,  dW_up = dA_u^T X_s
+ * accumulate_dw = 0 overwrites dW (a tuning slot with no rows gets zeros),
+ * 1 adds to it.  Inputs are the forward's saved A_g, A_u, H and the combine
+ * backward's dO; dX_perm [R_tot, d] in L->dtype.
+ */
+int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const void* X_perm,
+                           const int32_t* offsets, int T, int k,
+                           const void* A_g, const void* A_u, const void* H,
+                           const void* dO, void* dX_perm, int accumulate_dw,
+                           void* ws, size_t ws_bytes, void* stream);
+size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k);
+
+/* moe_permute_bwd: gradient of the permutation (a deterministic gather):
+ *   dX[t] = sum_{j: inv[t,j] >= 0} dX_perm[inv[t,j]]
+ *           + sum_{shared i} dX_perm[T*k + i*T + t]       (fp32 accumulation)
+ */
+int moe_permute_bwd(const moe_layer* L, const void* dX_perm, const int32_t* inv,
+                    int T, int k, void* dX, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FLUXMOE_H */

@@ -369,3 +369,22 @@ def moe_backward(X, dY, idx, gate, expert_map, slots: SlotWeights):
             o = swiglu_fwd(X[t], Wg, Wu, Wd)[3]
             dgate[t, j] = np.sum(dY[t] * o, axis=1)
     return dX, dW, dgate
+
+
+def expert_grad_columns(x, Wg, Wu, Wd, dO, cols):
+    """Slices of one expert's weight gradients along the intermediate index:
+    (dWg[cols, :], dWu[cols, :], dWd[:, cols]) for rows x [n, d] and output
+    gradient dO [n, d].  Column c of the intermediate layer only needs
+    a_g[:, c], a_u[:, c] and dH[:, c], so a few columns are cheap at any n.
+    """
+    x, dO = _f64(x), _f64(dO)
+    cols = list(cols)
+    Wg_c, Wu_c, Wd_c = _f64(Wg)[cols], _f64(Wu)[cols], _f64(Wd)[:, cols]
+    a_g = x @ Wg_c.T
+    a_u = x @ Wu_c.T
+    sg = sigmoid(a_g)
+    h = a_g * sg * a_u
+    dh = dO @ Wd_c
+    da_u = dh * a_g * sg
+    da_g = dh * a_u * sg * (1.0 + a_g * (1.0 - sg))
+    return da_g.T @ x, da_u.T @ x, dO.T @ h

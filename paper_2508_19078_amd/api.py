@@ -1,0 +1,283 @@
+"""Thin ctypes binding of libfluxmoe (include/fluxmoe.h).
+
+Each function has the name of the C entry point it calls and only marshals
+arguments: torch tensors become device pointers, dtypes become MOE_* codes,
+the stream defaults to torch's current stream.  No arithmetic of the method
+happens here.  If the library is not built, the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libfluxmoe.so")
+
+MOE_OK, MOE_ERR_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_ALIGN, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(6)
+MOE_F32, MOE_BF16, MOE_I8 = 0, 1, 2
+
+_c_int, _c_size, _vp, _f = ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_float
+
+
+class MoeError(RuntimeError):
+    def __init__(self, code: int, fn: str, msg: str):
+        super().__init__(f"{fn} failed with code {code}: {msg}")
+        self.code = code
+
+
+class moe_layer(ctypes.Structure):
+    _fields_ = [("d", _c_int), ("I", _c_int), ("dtype", _c_int), ("S_routed", _c_int),
+                ("S_shared", _c_int), ("w_gate", _vp), ("w_up", _vp), ("w_down", _vp),
+                ("dw_gate", _vp), ("dw_up", _vp), ("dw_down", _vp)]
+
+
+# name -> (restype, argtypes)
+_SIGS = {
+    "moe_last_error": (ctypes.c_char_p, []),
+    "moe_abi_version": (_c_int, []),
+    "moe_route_topk": (_c_int, [_vp, _vp, _c_int, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp]),
+    "moe_quantize_int8": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _vp]),
+    "moe_profile_hist": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp]),
+    "moe_merge_plan": (_c_int, [_vp, _c_int, _c_int, _c_int, _f, _c_int, _c_int, _c_int, _vp, _vp, _vp,
+                                _vp, _vp, _vp]),
+    "moe_activation_frequency": (_c_int, [_vp, _c_int, _f, _vp, _vp]),
+    "moe_merge_experts": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp, _c_int, _vp]),
+    "moe_slot_pointers": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
+                                   _vp, _vp, _vp, _vp, _vp]),
+    "moe_permute": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
+                             _vp, _vp, _vp, _vp, _c_size, _vp]),
+    "moe_permute_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
+    "moe_grouped_swiglu_fwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
+                                        _c_size, _vp]),
+    "moe_grouped_swiglu_fwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
+    "moe_unpermute": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
+    "moe_unpermute_bwd": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp]),
+    "moe_grouped_swiglu_bwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
+                                        _c_int, _vp, _c_size, _vp]),
+    "moe_grouped_swiglu_bwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
+    "moe_permute_bwd": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2508_19078_amd.build` (hipcc, gfx950)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def exported_names() -> List[str]:
+    return list(_SIGS)
+
+
+# ------------------------------------------------------------- marshalling --
+
+def dtype_code(t: torch.dtype) -> int:
+    if t == torch.bfloat16:
+        return MOE_BF16
+    if t == torch.float32:
+        return MOE_F32
+    if t == torch.int8:
+        return MOE_I8
+    raise TypeError(f"unsupported dtype {t}")
+
+
+def ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if isinstance(x, torch.Tensor):
+        return x.data_ptr()
+    if isinstance(x, ctypes.Structure):
+        return ctypes.addressof(x)
+    if hasattr(x, "struct"):
+        return ctypes.addressof(x.struct)
+    raise TypeError(type(x))
+
+
+def stream_ptr(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _call(name: str, *args) -> int:
+    rc = getattr(lib(), name)(*args)
+    if rc != MOE_OK:
+        raise MoeError(rc, name, lib().moe_last_error().decode())
+    return rc
+
+
+# --------------------------------------------------------------- routing ----
+
+def moe_route_topk(X, Wr, bias, k, idx, gate, logits=None, stream=None):
+    T, d = X.shape
+    E = Wr.shape[0]
+    return _call("moe_route_topk", ptr(X), ptr(Wr), dtype_code(X.dtype), ptr(bias), T, d, E, k,
+                 ptr(idx), ptr(gate), ptr(logits), stream_ptr(stream))
+
+
+def moe_quantize_int8(W, Wq, scale, stream=None):
+    E, d = W.shape
+    return _call("moe_quantize_int8", ptr(W), dtype_code(W.dtype), E, d, ptr(Wq), ptr(scale),
+                 stream_ptr(stream))
+
+
+def moe_profile_hist(X, Wq, scale, bias, k, counts, idx=None, stream=None):
+    T, d = X.shape
+    E = Wq.shape[0]
+    return _call("moe_profile_hist", ptr(X), dtype_code(X.dtype), ptr(Wq), ptr(scale), ptr(bias), T, d,
+                 E, k, ptr(counts), ptr(idx), stream_ptr(stream))
+
+
+# --------------------------------------------------------------- merging ----
+
+def moe_merge_plan(counts, n_merge, group, total_tokens, expert_map, slot_src, grp_ptr, grp_member,
+                   alpha, expert_base=0, grp_base=0, member_base=0, stream=None):
+    E = counts.shape[0]
+    return _call("moe_merge_plan", ptr(counts), E, n_merge, group, float(total_tokens), expert_base,
+                 grp_base, member_base, ptr(expert_map), ptr(slot_src), ptr(grp_ptr), ptr(grp_member),
+                 ptr(alpha), stream_ptr(stream))
+
+
+def moe_activation_frequency(counts, total_tokens, freq, stream=None):
+    return _call("moe_activation_frequency", ptr(counts), counts.shape[0], float(total_tokens), ptr(freq),
+                 stream_ptr(stream))
+
+
+def plan_from_groups(E: int, groups):
+    """ABI arrays of a caller-given grouping: kept experts in index order take
+    slots 0..K-1, group g takes slot K+g.  Host-side bookkeeping only."""
+    import numpy as np
+    grouped = {int(e) for g in groups for e in g}
+    kept = [e for e in range(E) if e not in grouped]
+    K = len(kept)
+    expert_map = np.zeros(E, dtype=np.int32)
+    slot_src = np.zeros(K + len(groups), dtype=np.int32)
+    for j, e in enumerate(kept):
+        expert_map[e] = j
+        slot_src[j] = e
+    grp_ptr = [0]
+    members = []
+    for g, grp in enumerate(groups):
+        for e in grp:
+            expert_map[e] = K + g
+            members.append(int(e))
+        grp_ptr.append(len(members))
+        slot_src[K + g] = E + g
+    return dict(expert_map=expert_map, slot_src=slot_src, grp_ptr=np.array(grp_ptr, dtype=np.int32),
+                grp_member=np.array(members, dtype=np.int32), K=K, G=len(groups))
+
+
+def moe_merge_experts(w_src_ptrs, dtype, d, I, G, grp_ptr, grp_member, alpha, w_dst_ptrs, out_dtype,
+                      stream=None):
+    """w_src_ptrs / w_dst_ptrs: int64 device tensors of 3 pointers per expert / group."""
+    return _call("moe_merge_experts", ptr(w_src_ptrs), dtype_code(dtype), d, I, G, ptr(grp_ptr),
+                 ptr(grp_member), ptr(alpha), ptr(w_dst_ptrs), dtype_code(out_dtype), stream_ptr(stream))
+
+
+def moe_slot_pointers(slot_src, S, E, d, I, dtype, orig, merged, w_gate, w_up, w_down, stream=None):
+    """orig / merged: (gate, up, down) stacked tensors; merged may be (None,)*3."""
+    return _call("moe_slot_pointers", ptr(slot_src), S, E, d, I, dtype_code(dtype), ptr(orig[0]),
+                 ptr(orig[1]), ptr(orig[2]), ptr(merged[0]), ptr(merged[1]), ptr(merged[2]), ptr(w_gate),
+                 ptr(w_up), ptr(w_down), stream_ptr(stream))
+
+
+# ------------------------------------------------------------- the layer ----
+
+def moe_permute_workspace_size(T, k, S_routed) -> int:
+    return lib().moe_permute_workspace_size(T, k, S_routed)
+
+
+def moe_permute(X, idx, gate, expert_map, S_routed, offsets, perm_token, perm_gate, inv, X_perm, ws,
+                E=None, stream=None):
+    T, d = X.shape
+    k = idx.shape[1]
+    E = E if E is not None else (expert_map.shape[0] if expert_map is not None else S_routed)
+    return _call("moe_permute", ptr(X), dtype_code(X.dtype), ptr(idx), ptr(gate), ptr(expert_map), T, d, E,
+                 k, S_routed, ptr(offsets), ptr(perm_token), ptr(perm_gate), ptr(inv), ptr(X_perm), ptr(ws),
+                 ws.numel() * ws.element_size() if ws is not None else 0, stream_ptr(stream))
+
+
+def moe_grouped_swiglu_fwd_workspace_size(layer, T, k) -> int:
+    return lib().moe_grouped_swiglu_fwd_workspace_size(ptr(layer), T, k)
+
+
+def moe_grouped_swiglu_bwd_workspace_size(layer, T, k) -> int:
+    return lib().moe_grouped_swiglu_bwd_workspace_size(ptr(layer), T, k)
+
+
+def moe_grouped_swiglu_fwd(layer, X, X_perm, offsets, T, k, A_g, A_u, H, O, ws, stream=None):
+    return _call("moe_grouped_swiglu_fwd", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(A_g),
+                 ptr(A_u), ptr(H), ptr(O), ptr(ws), ws.numel() * ws.element_size(), stream_ptr(stream))
+
+
+def moe_unpermute(layer, O, inv, perm_gate, T, k, Y, stream=None):
+    return _call("moe_unpermute", ptr(layer), ptr(O), ptr(inv), ptr(perm_gate), T, k, ptr(Y),
+                 stream_ptr(stream))
+
+
+def moe_unpermute_bwd(layer, dY, O, inv, offsets, perm_gate, T, k, dO, dgate=None, stream=None):
+    return _call("moe_unpermute_bwd", ptr(layer), ptr(dY), ptr(O), ptr(inv), ptr(offsets), ptr(perm_gate),
+                 T, k, ptr(dO), ptr(dgate), stream_ptr(stream))
+
+
+def moe_grouped_swiglu_bwd(layer, X, X_perm, offsets, T, k, A_g, A_u, H, dO, dX_perm, accumulate_dw, ws,
+                           stream=None):
+    return _call("moe_grouped_swiglu_bwd", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(A_g),
+                 ptr(A_u), ptr(H), ptr(dO), ptr(dX_perm), int(accumulate_dw), ptr(ws),
+                 ws.numel() * ws.element_size(), stream_ptr(stream))
+
+
+def moe_permute_bwd(layer, dX_perm, inv, T, k, dX, stream=None):
+    return _call("moe_permute_bwd", ptr(layer), ptr(dX_perm), ptr(inv), T, k, ptr(dX), stream_ptr(stream))
+
+
+# ----------------------------------------------------- layer descriptor ----
+
+class LayerTables:
+    """Device pointer tables of a layer's slots and the moe_layer struct.
+
+    w_gate/w_up/w_down: per-slot weight tensors (routed slots, then shared),
+    or pre-filled int64 device pointer tensors (e.g. written by
+    moe_slot_pointers).  dw: per-slot fp32 gradient tensors or None (frozen).
+    """
+
+    def __init__(self, d: int, I: int, dtype: torch.dtype, S_routed: int, S_shared: int,
+                 w_gate, w_up, w_down, dw_gate: Sequence = None, dw_up: Sequence = None,
+                 dw_down: Sequence = None, device="cuda"):
+        S = S_routed + S_shared
+
+        def table(x):
+            if isinstance(x, torch.Tensor) and x.dtype == torch.int64 and x.dim() == 1:
+                assert x.numel() == S
+                return x
+            vals = [0 if t is None else ptr(t) for t in x]
+            assert len(vals) == S
+            return torch.tensor(vals, dtype=torch.int64, device=device)
+
+        self.keep = [w_gate, w_up, w_down, dw_gate, dw_up, dw_down]
+        self.w_gate, self.w_up, self.w_down = table(w_gate), table(w_up), table(w_down)
+        none = [None] * S
+        self.dw_gate = table(dw_gate if dw_gate is not None else none)
+        self.dw_up = table(dw_up if dw_up is not None else none)
+        self.dw_down = table(dw_down if dw_down is not None else none)
+        self.struct = moe_layer(d, I, dtype_code(dtype), S_routed, S_shared, ptr(self.w_gate),
+                                ptr(self.w_up), ptr(self.w_down), ptr(self.dw_gate), ptr(self.dw_up),
+                                ptr(self.dw_down))

@@ -1,0 +1,476 @@
+// Gate re-routing and token permutation into per-slot buckets, the combine,
+// and their backward passes.
+//
+// Permute runs in four launches, all deterministic:
+//   count   a block of 256 tokens counts its rows per slot (LDS integer atomics)
+//   scan    one block turns the per-block counts into global row positions:
+//           a wave scan per slot over the blocks, then an exclusive scan over
+//           the slots (the bucket offsets)
+//   place   the same blocks rank their rows within each slot in token order
+//           (one wave ballot per slot) and write the maps
+//   gather  X_perm[p] = X[perm_token[p]], one wave per row, 16-byte accesses
+// Combine and the two backward gathers run one wave per token.
+#include "common.hpp"
+
+namespace fm {
+namespace {
+
+constexpr int PM_TOK = 256;   // tokens per block of count/place
+
+template <int KMAX>
+struct TokenSlots {
+  int s[KMAX];        // slot of choice j
+  bool first[KMAX];   // choice j opens its row (first choice of this slot)
+  int owner[KMAX];    // j' of the choice that opened the row of choice j
+};
+
+template <int KMAX>
+__device__ __forceinline__ void token_slots(const int32_t* __restrict__ idx,
+                                            const int32_t* __restrict__ emap, int t, int k,
+                                            TokenSlots<KMAX>& ts) {
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    ts.s[j] = -1;
+    ts.first[j] = false;
+    ts.owner[j] = j;
+    if (j < k) {
+      int e = idx[(size_t)t * k + j];
+      ts.s[j] = emap ? emap[e] : e;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    bool f = j < k;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i)
+      if (i < j && f && ts.s[i] == ts.s[j]) {
+        f = false;
+        ts.owner[j] = ts.owner[i];
+      }
+    ts.first[j] = f;
+  }
+}
+
+template <int KMAX>
+__global__ __launch_bounds__(256) void k_perm_count(const int32_t* __restrict__ idx,
+                                                    const int32_t* __restrict__ emap, int T, int k,
+                                                    int S, int32_t* __restrict__ bc, int nblk) {
+  __shared__ int cnt[512];
+  for (int s = threadIdx.x; s < S; s += blockDim.x) cnt[s] = 0;
+  __syncthreads();
+  const int t = blockIdx.x * PM_TOK + threadIdx.x;
+  if (t < T) {
+    TokenSlots<KMAX> ts;
+    token_slots<KMAX>(idx, emap, t, k, ts);
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j)
+      if (ts.first[j]) atomicAdd(&cnt[ts.s[j]], 1);
+  }
+  __syncthreads();
+  // slot-major layout: bc[s * nblk + block]
+  for (int s = threadIdx.x; s < S; s += blockDim.x) bc[(size_t)s * nblk + blockIdx.x] = cnt[s];
+}
+
+// One block of 1024 threads.
+__global__ __launch_bounds__(1024) void k_perm_scan(int32_t* __restrict__ bc, int nblk, int S,
+                                                    int32_t* __restrict__ offsets) {
+  __shared__ int tot[513];
+  const int lane = lane_id(), wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int s = wave; s < S; s += nw) {
+    int carry = 0;
+    for (int b0 = 0; b0 < nblk; b0 += 64) {
+      const int b = b0 + lane;
+      const int v = b < nblk ? bc[(size_t)s * nblk + b] : 0;
+      int x = v;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        int y = __shfl_up(x, off);
+        if (lane >= off) x += y;
+      }
+      if (b < nblk) bc[(size_t)s * nblk + b] = carry + x - v;
+      carry += __shfl(x, 63);
+    }
+    if (lane == 0) tot[s] = carry;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int s = 0; s < S; ++s) {
+      int v = tot[s];
+      tot[s] = run;
+      offsets[s] = run;
+      run += v;
+    }
+    offsets[S] = run;
+  }
+  __syncthreads();
+  for (size_t i = threadIdx.x; i < (size_t)S * nblk; i += blockDim.x) bc[i] += tot[i / nblk];
+}
+
+template <int KMAX>
+__global__ __launch_bounds__(256) void k_perm_place(const int32_t* __restrict__ idx,
+                                                    const float* __restrict__ gate,
+                                                    const int32_t* __restrict__ emap, int T, int k,
+                                                    int S, const int32_t* __restrict__ bc, int nblk,
+                                                    int32_t* __restrict__ perm_token,
+                                                    float* __restrict__ perm_gate,
+                                                    int32_t* __restrict__ inv) {
+  __shared__ int wcnt[4][512];
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
+  const int t = blockIdx.x * PM_TOK + threadIdx.x;
+  const bool valid = t < T;
+  TokenSlots<KMAX> ts;
+  if (valid) {
+    token_slots<KMAX>(idx, emap, t, k, ts);
+  } else {
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) { ts.s[j] = -1; ts.first[j] = false; ts.owner[j] = j; }
+  }
+  int rank[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) rank[j] = 0;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int s = 0; s < S; ++s) {
+    bool has = false;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) has |= ts.first[j] && ts.s[j] == s;
+    const uint64_t m = __ballot(has);
+    if (lane == 0) wcnt[wave][s] = __popcll(m);
+    const int r = __popcll(m & lt);
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j)
+      if (ts.first[j] && ts.s[j] == s) rank[j] = r;
+  }
+  __syncthreads();
+  if (!valid) return;
+  int pos[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    pos[j] = 0;
+    if (ts.first[j]) {
+      const int s = ts.s[j];
+      int base = bc[(size_t)s * nblk + blockIdx.x];
+      for (int w = 0; w < wave; ++w) base += wcnt[w][s];
+      pos[j] = base + rank[j];
+    }
+  }
+  float g[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) g[j] = j < k ? gate[(size_t)t * k + j] : 0.f;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (!ts.first[j]) continue;
+    float sum = 0.f;                 // gates of every choice folded into this row, j order
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i)
+      if (i < k && ts.s[i] == ts.s[j]) sum += g[i];
+    perm_token[pos[j]] = t;
+    perm_gate[pos[j]] = sum;
+  }
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (j >= k) continue;
+    int p = 0;
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i)
+      if (i == ts.owner[j]) p = pos[i];
+    inv[(size_t)t * k + j] = ts.first[j] ? p : -2 - p;
+  }
+}
+
+// X_perm[p] = X[perm_token[p]] for p < offsets[S]; one wave per row.
+__global__ __launch_bounds__(256) void k_gather_rows(const char* __restrict__ X,
+                                                     const int32_t* __restrict__ perm_token,
+                                                     const int32_t* __restrict__ offsets, int S,
+                                                     size_t row_bytes, char* __restrict__ Xp) {
+  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (p >= offsets[S]) return;
+  const char* src = X + (size_t)perm_token[p] * row_bytes;
+  char* dst = Xp + (size_t)p * row_bytes;
+  for (size_t c = (size_t)lane_id() * 16; c < row_bytes; c += 64 * 16) st16(dst + c, ld16(src + c));
+}
+
+__global__ void k_zero_i32(int32_t* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// Decodes inv: row of choice (t, j), folded or not.
+__device__ __forceinline__ int row_of(int v) { return v >= 0 ? v : -2 - v; }
+
+// Y[t] = sum_{first choices} perm_gate[p] O[p] + sum_shared O[shared row].
+template <typename T, int KMAX>
+__global__ __launch_bounds__(256) void k_combine(const T* __restrict__ O, const int32_t* __restrict__ inv,
+                                                 const float* __restrict__ pg, int Tn, int k, int d,
+                                                 int S_sh, T* __restrict__ Y) {
+  constexpr int V = 16 / sizeof(T);
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= Tn) return;
+  const size_t R = (size_t)Tn * k;
+  int p[KMAX];
+  float g[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    p[j] = j < k ? inv[(size_t)t * k + j] : -1;
+    g[j] = p[j] >= 0 ? pg[p[j]] : 0.f;
+  }
+  for (int c = lane_id() * V; c < d; c += 64 * V) {
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (p[j] < 0) continue;
+      float f[V];
+      unpack16(ld16(O + (size_t)p[j] * d + c), f, (T*)nullptr);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] = fmaf(g[j], f[i], acc[i]);
+    }
+    for (int sh = 0; sh < S_sh; ++sh) {
+      float f[V];
+      unpack16(ld16(O + (R + (size_t)sh * Tn + t) * d + c), f, (T*)nullptr);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] += f[i];
+    }
+    st16(Y + (size_t)t * d + c, pack16(acc, (T*)nullptr));
+  }
+}
+
+// dO[p] = perm_gate[p] dY[t]; shared rows get dY[t]; dgate[t,j] = <dY[t], O[row]>.
+template <typename T, int KMAX>
+__global__ __launch_bounds__(256) void k_combine_bwd(const T* __restrict__ dY, const T* __restrict__ O,
+                                                     const int32_t* __restrict__ inv,
+                                                     const float* __restrict__ pg, int Tn, int k,
+                                                     int d, int S_sh, T* __restrict__ dO,
+                                                     float* __restrict__ dgate) {
+  constexpr int V = 16 / sizeof(T);
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= Tn) return;
+  const size_t R = (size_t)Tn * k;
+  int p[KMAX];
+  float g[KMAX], dot[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    p[j] = j < k ? inv[(size_t)t * k + j] : -1;
+    g[j] = p[j] >= 0 ? pg[p[j]] : 0.f;
+    dot[j] = 0.f;
+  }
+  for (int c = lane_id() * V; c < d; c += 64 * V) {
+    const u32x4_t raw = ld16(dY + (size_t)t * d + c);
+    float f[V];
+    unpack16(raw, f, (T*)nullptr);
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j >= k) continue;
+      if (p[j] >= 0) {
+        float o[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) o[i] = g[j] * f[i];
+        st16(dO + (size_t)p[j] * d + c, pack16(o, (T*)nullptr));
+      }
+      if (dgate) {
+        float o[V];
+        unpack16(ld16(O + (size_t)row_of(p[j]) * d + c), o, (T*)nullptr);
+#pragma unroll
+        for (int i = 0; i < V; ++i) dot[j] = fmaf(f[i], o[i], dot[j]);
+      }
+    }
+    for (int sh = 0; sh < S_sh; ++sh) st16(dO + (R + (size_t)sh * Tn + t) * d + c, raw);
+  }
+  if (dgate) {
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j >= k) continue;
+      float v = dot[j];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+      if (lane_id() == 0) dgate[(size_t)t * k + j] = v;
+    }
+  }
+}
+
+// dX[t] = sum_{first choices} dX_perm[p] + sum_shared dX_perm[shared row].
+template <typename T, int KMAX>
+__global__ __launch_bounds__(256) void k_permute_bwd(const T* __restrict__ dXp,
+                                                     const int32_t* __restrict__ inv, int Tn, int k,
+                                                     int d, int S_sh, T* __restrict__ dX) {
+  constexpr int V = 16 / sizeof(T);
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= Tn) return;
+  const size_t R = (size_t)Tn * k;
+  int p[KMAX];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) p[j] = j < k ? inv[(size_t)t * k + j] : -1;
+  for (int c = lane_id() * V; c < d; c += 64 * V) {
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.f;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (p[j] < 0) continue;
+      float f[V];
+      unpack16(ld16(dXp + (size_t)p[j] * d + c), f, (T*)nullptr);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] += f[i];
+    }
+    for (int sh = 0; sh < S_sh; ++sh) {
+      float f[V];
+      unpack16(ld16(dXp + (R + (size_t)sh * Tn + t) * d + c), f, (T*)nullptr);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] += f[i];
+    }
+    st16(dX + (size_t)t * d + c, pack16(acc, (T*)nullptr));
+  }
+}
+
+int check_layer(const moe_layer* L) {
+  if (!L) return fail(MOE_ERR_ARG, "layer must not be NULL");
+  if (L->d <= 0 || L->I <= 0) return fail(MOE_ERR_ARG, "layer d=%d I=%d", L->d, L->I);
+  if (L->d % 8 || L->I % 8) return fail(MOE_ERR_UNSUPPORTED, "layer d=%d I=%d must be multiples of 8", L->d, L->I);
+  if (L->S_routed < 0 || L->S_shared < 0 || L->S_routed + L->S_shared < 1 || L->S_routed > 512 ||
+      L->S_shared > 512)
+    return fail(MOE_ERR_ARG, "layer S_routed=%d S_shared=%d", L->S_routed, L->S_shared);
+  return need_dtype_float(L->dtype, "layer dtype");
+}
+
+int check_tk(int T, int k) {
+  if (T < 0 || k <= 0) return fail(MOE_ERR_ARG, "T=%d k=%d", T, k);
+  if (k > 16) return fail(MOE_ERR_UNSUPPORTED, "k=%d > 16", k);
+  return MOE_OK;
+}
+
+#define FM_KSWITCH(k, MACRO)       \
+  if ((k) <= 2) { MACRO(2); }      \
+  else if ((k) <= 4) { MACRO(4); } \
+  else if ((k) <= 8) { MACRO(8); } \
+  else { MACRO(16); }
+
+}  // namespace
+}  // namespace fm
+
+using namespace fm;
+
+extern "C" size_t moe_permute_workspace_size(int T, int k, int S_routed) {
+  (void)k;
+  if (T <= 0 || S_routed <= 0) return 256;
+  const size_t nblk = (size_t)cdiv(T, PM_TOK);
+  return ((nblk * S_routed * sizeof(int32_t) + 255) / 256) * 256;
+}
+
+extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
+                           const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
+                           int32_t* offsets, int32_t* perm_token, float* perm_gate, int32_t* inv,
+                           void* X_perm, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  FM_TRY(check_tk(T, k));
+  if (d <= 0 || E <= 0 || S_routed <= 0) return fail(MOE_ERR_ARG, "d=%d E=%d S_routed=%d", d, E, S_routed);
+  if (E > 256 || k > E) return fail(MOE_ERR_UNSUPPORTED, "E=%d k=%d", E, k);
+  if (S_routed > 512) return fail(MOE_ERR_UNSUPPORTED, "S_routed=%d > 512", S_routed);
+  if (!expert_map && S_routed < E) return fail(MOE_ERR_ARG, "identity map needs S_routed >= E");
+  if (d % 8) return fail(MOE_ERR_UNSUPPORTED, "d=%d not a multiple of 8", d);
+  FM_TRY(need_dtype_float(dtype, "dtype"));
+  FM_TRY(need(offsets, "offsets"));
+  if (T > 0) {
+    FM_TRY(need(X, "X")); FM_TRY(need(idx, "idx")); FM_TRY(need(gate, "gate"));
+    FM_TRY(need(perm_token, "perm_token")); FM_TRY(need(perm_gate, "perm_gate"));
+    FM_TRY(need(inv, "inv")); FM_TRY(need(X_perm, "X_perm")); FM_TRY(need(ws, "ws"));
+  }
+  FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(X_perm, "X_perm"));
+  FM_TRY(need_aligned(offsets, "offsets")); FM_TRY(need_aligned(ws, "ws"));
+  if (ws_bytes < moe_permute_workspace_size(T, k, S_routed))
+    return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
+                moe_permute_workspace_size(T, k, S_routed));
+  hipStream_t st = as_stream(stream);
+  if (T == 0) {
+    hipLaunchKernelGGL(k_zero_i32, dim3(cdiv(S_routed + 1, 256)), dim3(256), 0, st, offsets,
+                       S_routed + 1);
+    return check_launch("moe_permute");
+  }
+  const int nblk = cdiv(T, PM_TOK);
+  int32_t* bc = (int32_t*)ws;
+#define FM_PC(KM) \
+  hipLaunchKernelGGL(k_perm_count<KM>, dim3(nblk), dim3(256), 0, st, idx, expert_map, T, k, S_routed, bc, nblk)
+  FM_KSWITCH(k, FM_PC)
+#undef FM_PC
+  hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(1024), 0, st, bc, nblk, S_routed, offsets);
+#define FM_PP(KM)                                                                                   \
+  hipLaunchKernelGGL(k_perm_place<KM>, dim3(nblk), dim3(256), 0, st, idx, gate, expert_map, T, k, \
+                     S_routed, bc, nblk, perm_token, perm_gate, inv)
+  FM_KSWITCH(k, FM_PP)
+#undef FM_PP
+  const size_t row_bytes = (size_t)d * esize(dtype);
+  hipLaunchKernelGGL(k_gather_rows, dim3(cdiv((long)T * k, 4)), dim3(256), 0, st, (const char*)X,
+                     perm_token, offsets, S_routed, row_bytes, (char*)X_perm);
+  return check_launch("moe_permute");
+}
+
+extern "C" int moe_unpermute(const moe_layer* L, const void* O, const int32_t* inv,
+                             const float* perm_gate, int T, int k, void* Y, void* stream) {
+  clear_error();
+  FM_TRY(check_layer(L));
+  FM_TRY(check_tk(T, k));
+  if (T == 0) return MOE_OK;
+  FM_TRY(need(O, "O")); FM_TRY(need(inv, "inv")); FM_TRY(need(perm_gate, "perm_gate")); FM_TRY(need(Y, "Y"));
+  FM_TRY(need_aligned(O, "O")); FM_TRY(need_aligned(Y, "Y"));
+  hipStream_t st = as_stream(stream);
+  dim3 grid(cdiv(T, 4)), block(256);
+#define FM_CB(KM)                                                                                 \
+  if (L->dtype == MOE_BF16)                                                                       \
+    hipLaunchKernelGGL((k_combine<bf16, KM>), grid, block, 0, st, (const bf16*)O, inv, perm_gate, \
+                       T, k, L->d, L->S_shared, (bf16*)Y);                                        \
+  else                                                                                            \
+    hipLaunchKernelGGL((k_combine<float, KM>), grid, block, 0, st, (const float*)O, inv,          \
+                       perm_gate, T, k, L->d, L->S_shared, (float*)Y);
+  FM_KSWITCH(k, FM_CB)
+#undef FM_CB
+  return check_launch("moe_unpermute");
+}
+
+extern "C" int moe_unpermute_bwd(const moe_layer* L, const void* dY, const void* O,
+                                 const int32_t* inv, const int32_t* offsets, const float* perm_gate,
+                                 int T, int k, void* dO, float* dgate, void* stream) {
+  clear_error();
+  FM_TRY(check_layer(L));
+  FM_TRY(check_tk(T, k));
+  if (T == 0) return MOE_OK;
+  FM_TRY(need(dY, "dY")); FM_TRY(need(inv, "inv")); FM_TRY(need(perm_gate, "perm_gate"));
+  FM_TRY(need(dO, "dO"));
+  if (dgate) FM_TRY(need(O, "O"));
+  (void)offsets;  // rows are addressed through inv; every routed row has one owner token
+  FM_TRY(need_aligned(dY, "dY")); FM_TRY(need_aligned(O, "O")); FM_TRY(need_aligned(dO, "dO"));
+  hipStream_t st = as_stream(stream);
+  dim3 grid(cdiv(T, 4)), block(256);
+#define FM_CBB(KM)                                                                                  \
+  if (L->dtype == MOE_BF16)                                                                         \
+    hipLaunchKernelGGL((k_combine_bwd<bf16, KM>), grid, block, 0, st, (const bf16*)dY,              \
+                       (const bf16*)O, inv, perm_gate, T, k, L->d, L->S_shared, (bf16*)dO, dgate); \
+  else                                                                                              \
+    hipLaunchKernelGGL((k_combine_bwd<float, KM>), grid, block, 0, st, (const float*)dY,            \
+                       (const float*)O, inv, perm_gate, T, k, L->d, L->S_shared, (float*)dO,       \
+                       dgate);
+  FM_KSWITCH(k, FM_CBB)
+#undef FM_CBB
+  return check_launch("moe_unpermute_bwd");
+}
+
+extern "C" int moe_permute_bwd(const moe_layer* L, const void* dX_perm, const int32_t* inv, int T,
+                               int k, void* dX, void* stream) {
+  clear_error();
+  FM_TRY(check_layer(L));
+  FM_TRY(check_tk(T, k));
+  if (T == 0) return MOE_OK;
+  FM_TRY(need(dX_perm, "dX_perm")); FM_TRY(need(inv, "inv")); FM_TRY(need(dX, "dX"));
+  FM_TRY(need_aligned(dX_perm, "dX_perm")); FM_TRY(need_aligned(dX, "dX"));
+  hipStream_t st = as_stream(stream);
+  dim3 grid(cdiv(T, 4)), block(256);
+#define FM_PB(KM)                                                                                  \
+  if (L->dtype == MOE_BF16)                                                                        \
+    hipLaunchKernelGGL((k_permute_bwd<bf16, KM>), grid, block, 0, st, (const bf16*)dX_perm, inv,  \
+                       T, k, L->d, L->S_shared, (bf16*)dX);                                        \
+  else                                                                                             \
+    hipLaunchKernelGGL((k_permute_bwd<float, KM>), grid, block, 0, st, (const float*)dX_perm, inv, \
+                       T, k, L->d, L->S_shared, (float*)dX);
+  FM_KSWITCH(k, FM_PB)
+#undef FM_PB
+  return check_launch("moe_permute_bwd");
+}

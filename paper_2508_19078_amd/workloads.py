@@ -97,7 +97,7 @@ def layer_merge_spec(w: LayerWorkload, layer: int = 0) -> Optional[tuple]:
         g = w.merge[1]
         m = merge_count_linear(layer, w.n_layers, max_groups=(3 * w.E // 4) // g,
                                group=g)
-        return ("frequency", m, g) if m > 0 else None
+        return ("frequency", m, g)   # m == 0 still ranks the slots by popularity
     return w.merge
 
 

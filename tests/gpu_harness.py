@@ -1,0 +1,141 @@
+"""Shared pieces of the GPU parity tests: oracle-side evaluation of a layer and
+the comparison rules.  Imports the oracle (test infrastructure) and the HIP
+binding; the two never see each other's code, only the seeded inputs."""
+from __future__ import annotations
+
+import sys
+import time
+
+import numpy as np
+import torch
+
+import oracle as O
+from paper_2508_19078_amd import workloads as W
+from paper_2508_19078_amd.layer import LayerInputs, MoELayerRunner
+
+GAP = 1e-6          # near-tie exclusion window on fp32 logits
+TOL_FFN = 2e-2      # relative Frobenius bound for Y, dX, dW (bf16 inputs, fp32 accumulation)
+TOL_MERGE = 1e-3    # merged weights vs the fp64 merge rounded to the storage type
+
+
+def log(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def rel_fro(got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref)
+    num = np.linalg.norm(got - ref)
+    return num / den if den > 0 else num
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    t = t.detach()
+    if t.dtype == torch.bfloat16:
+        return t.float().cpu().numpy().astype(np.float64)
+    return t.cpu().numpy()
+
+
+def rne_bf16(x: np.ndarray) -> np.ndarray:
+    """fp64 -> nearest-even bf16 value (as fp64), directly from fp64."""
+    m, e = np.frexp(np.asarray(x, dtype=np.float64))
+    return np.ldexp(np.rint(m * 256.0) / 256.0, e)
+
+
+def gaps_of(logits, k):
+    s = -np.sort(-np.asarray(logits, dtype=np.float64), axis=1)
+    if k >= s.shape[1]:
+        return np.full(s.shape[0], np.inf)
+    return s[:, k - 1] - s[:, k]
+
+
+def compare_topk(idx_gpu, logits_gpu, idx_ref, logits_ref, k):
+    """Bit-exact top-k sets (and rank order where adjacent logits differ by at
+    least GAP), excluding tokens whose k-th and (k+1)-th logits are within GAP
+    on either side.  Returns (n_excluded, n_mismatch)."""
+    excl = gaps_of(logits_ref, k) < GAP
+    if logits_gpu is not None:
+        excl |= gaps_of(logits_gpu, k) < GAP
+    idx_gpu, idx_ref = np.asarray(idx_gpu), np.asarray(idx_ref)
+    bad = 0
+    srt = -np.sort(-np.asarray(logits_ref), axis=1)[:, :k]
+    order_ok = np.all(np.diff(-srt, axis=1) >= GAP, axis=1) if k > 1 else np.ones(len(srt), bool)
+    for t in np.nonzero(~excl)[0]:
+        if set(idx_gpu[t]) != set(idx_ref[t]):
+            bad += 1
+        elif order_ok[t] and not np.array_equal(idx_gpu[t], idx_ref[t]):
+            bad += 1
+    return int(excl.sum()), bad
+
+
+class OracleLayer:
+    """fp64 oracle of one layer for given inputs: routing, profile, plan, merge,
+    and the slot weights the forward/backward run on."""
+
+    def __init__(self, w: W.LayerWorkload, inp: LayerInputs, layer: int = 0, with_ffn_weights: bool = True):
+        self.w = w
+        X = inp.X.f64()
+        self.X = X
+        self.bias = inp.bias.astype(np.float64)
+        self.idx, self.gate, self.logits = O.route_topk(X, inp.Wr.f64(), self.bias, w.k)
+        self.q, self.s = O.quantize_int8_rows(inp.Wr.f32())
+        self.counts, self.idx8, self.logits8 = O.profile_hist(X, self.q, self.s, self.bias, w.k)
+        spec = W.layer_merge_spec(w, layer)
+        if spec is None:
+            self.plan = O.MergePlan(w.E, list(range(w.E)), [], n_tune=w.n_tune)
+        elif spec[0] == "groups":
+            self.plan = O.explicit_merge_plan(w.E, spec[1])
+        else:
+            self.plan = O.frequency_merge_plan(self.counts, spec[1], spec[2], n_tune=w.n_tune)
+        self.alpha = self.counts / float(w.T)
+        self.dY = inp.dY.f64()
+        if not with_ffn_weights:
+            return
+        wg, wu, wd = (t.f64() for t in inp.experts)
+        self.merged = [tuple(O.merge_experts(Wm, g, self.alpha) for Wm in (wg, wu, wd))
+                       for g in self.plan.groups]
+        sg, su, sd = [], [], []
+        for e in self.plan.kept:
+            sg.append(wg[e]); su.append(wu[e]); sd.append(wd[e])
+        for m in self.merged:
+            sg.append(m[0]); su.append(m[1]); sd.append(m[2])
+        tuning = list(self.plan.tuning)
+        if w.n_shared:
+            hg, hu, hd = (t.f64() for t in inp.shared)
+            for i in range(w.n_shared):
+                sg.append(hg[i]); su.append(hu[i]); sd.append(hd[i])
+                tuning.append(True)
+        self.slots = O.SlotWeights(sg, su, sd, tuning, n_shared=w.n_shared)
+
+    def forward(self, tokens=None):
+        t = slice(None) if tokens is None else tokens
+        return O.moe_forward(self.X[t], self.idx[t], self.gate[t], self.plan.expert_map, self.slots)
+
+    def backward(self, tokens=None):
+        t = slice(None) if tokens is None else tokens
+        return O.moe_backward(self.X[t], self.dY[t], self.idx[t], self.gate[t], self.plan.expert_map,
+                              self.slots)
+
+    def slot_rows(self, s):
+        """(tokens, gate) of the rows of slot s, without folding."""
+        if s >= self.slots.S_routed:
+            return np.arange(self.w.T), np.ones(self.w.T)
+        t, j = np.nonzero(self.plan.expert_map[self.idx] == s)
+        return t, self.gate[t, j]
+
+    def grad_columns(self, s, cols):
+        t, g = self.slot_rows(s)
+        dO = g[:, None] * self.dY[t]
+        return O.expert_grad_columns(self.X[t], self.slots.wg[s], self.slots.wu[s], self.slots.wd[s], dO, cols)
+
+
+def gpu_runner(w, inp, layer=0, oracle_routing: OracleLayer = None):
+    """Runs profile + merge (+ forward/backward with the oracle's routing when
+    given, else the GPU's own) and synchronises."""
+    r = MoELayerRunner(w, inp, layer=layer)
+    r.profile()
+    r.merge()
+    r.route()
+    return r

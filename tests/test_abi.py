@@ -1,0 +1,137 @@
+"""Host-side checks of the C ABI: the library loads, exports every function the
+header declares, and rejects invalid arguments before any HIP call (so these
+run on a machine without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2508_19078_amd import api
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fluxmoe.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(api.LIB_PATH):
+        from paper_2508_19078_amd import build
+        build.build(verbose=False)
+    return api.lib()
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_function_is_exported_and_bound(L):
+    names = declared()
+    assert len(names) >= 17
+    for n in names:
+        assert hasattr(L, n), n
+        assert n in api.exported_names(), n
+    assert L.moe_abi_version() == 1
+
+
+FAKE = 0x100000          # aligned, never dereferenced: validation fails first
+MIS = FAKE + 4
+
+
+def rc_and_msg(L, name, *args):
+    rc = getattr(L, name)(*args)
+    return rc, L.moe_last_error().decode()
+
+
+def test_route_rejections(L):
+    # k > E
+    rc, msg = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_BF16, None, 16, 64, 4, 5, FAKE, FAKE, None, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED and "k=5" in msg
+    # E > 256
+    rc, _ = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_BF16, None, 16, 64, 300, 4, FAKE, FAKE, None, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    # d not a multiple of 8
+    rc, _ = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_BF16, None, 16, 60, 8, 2, FAKE, FAKE, None, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    # NULL X, NULL idx
+    rc, msg = rc_and_msg(L, "moe_route_topk", None, FAKE, api.MOE_BF16, None, 16, 64, 8, 2, FAKE, FAKE, None, None)
+    assert rc == api.MOE_ERR_ARG and "X" in msg
+    rc, _ = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_BF16, None, 16, 64, 8, 2, None, FAKE, None, None)
+    assert rc == api.MOE_ERR_ARG
+    # misaligned
+    rc, _ = rc_and_msg(L, "moe_route_topk", MIS, FAKE, api.MOE_BF16, None, 16, 64, 8, 2, FAKE, FAKE, None, None)
+    assert rc == api.MOE_ERR_ALIGN
+    # unsupported dtype (int8 activations)
+    rc, _ = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_I8, None, 16, 64, 8, 2, FAKE, FAKE, None, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    # T == 0 is a no-op that touches nothing
+    rc, _ = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_BF16, None, 0, 64, 8, 2, FAKE, FAKE, None, None)
+    assert rc == api.MOE_OK
+
+
+def test_profile_and_merge_rejections(L):
+    rc, _ = rc_and_msg(L, "moe_profile_hist", FAKE, api.MOE_BF16, FAKE, FAKE, None, 8, 64, 8, 9, FAKE, None, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    rc, _ = rc_and_msg(L, "moe_profile_hist", FAKE, api.MOE_BF16, FAKE, None, None, 8, 64, 8, 2, FAKE, None, None)
+    assert rc == api.MOE_ERR_ARG                                    # scale is required
+    rc, _ = rc_and_msg(L, "moe_merge_plan", FAKE, 64, 30, 4, ctypes.c_float(1.0), 0, 0, 0,
+                       FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert rc == api.MOE_ERR_ARG                                    # 30 % 4 != 0
+    rc, _ = rc_and_msg(L, "moe_merge_plan", FAKE, 64, 32, 4, ctypes.c_float(0.0), 0, 0, 0,
+                       FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert rc == api.MOE_ERR_ARG                                    # no tokens
+    rc, _ = rc_and_msg(L, "moe_merge_experts", FAKE, api.MOE_BF16, 2048, 1404, 8, FAKE, FAKE, FAKE, FAKE,
+                       api.MOE_BF16, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED                            # I % 8 != 0
+    rc, _ = rc_and_msg(L, "moe_merge_experts", FAKE, api.MOE_BF16, 2048, 1408, 0, FAKE, FAKE, FAKE, FAKE,
+                       api.MOE_BF16, None)
+    assert rc == api.MOE_OK                                         # no groups: nothing to do
+    rc, _ = rc_and_msg(L, "moe_quantize_int8", FAKE, api.MOE_BF16, 0, 64, FAKE, FAKE, None)
+    assert rc == api.MOE_ERR_ARG
+
+
+def test_permute_workspace_and_layer_rejections(L):
+    need = L.moe_permute_workspace_size(4096, 4, 16)
+    assert need >= (4096 // 256) * 16 * 4
+    rc, msg = rc_and_msg(L, "moe_permute", FAKE, api.MOE_BF16, FAKE, FAKE, None, 4096, 4096, 16, 4, 16,
+                         FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_size_t(need - 1), None)
+    assert rc == api.MOE_ERR_WORKSPACE and "workspace" in msg
+    rc, _ = rc_and_msg(L, "moe_permute", FAKE, api.MOE_BF16, FAKE, FAKE, None, 4096, 4096, 16, 4, 8,
+                       FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_size_t(need), None)
+    assert rc == api.MOE_ERR_ARG                                    # identity map needs S >= E
+    # a layer with an unsupported intermediate size
+    lay = api.moe_layer(2048, 1404, api.MOE_BF16, 40, 2, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    rc, _ = rc_and_msg(L, "moe_grouped_swiglu_fwd", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
+                       FAKE, FAKE, FAKE, ctypes.c_size_t(1 << 30), None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    lay = api.moe_layer(2048, 1408, api.MOE_BF16, 40, 2, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    need = L.moe_grouped_swiglu_fwd_workspace_size(ctypes.byref(lay), 8192, 6)
+    assert need > 0
+    rc, _ = rc_and_msg(L, "moe_grouped_swiglu_fwd", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
+                       FAKE, FAKE, FAKE, ctypes.c_size_t(need - 1), None)
+    assert rc == api.MOE_ERR_WORKSPACE
+    bneed = L.moe_grouped_swiglu_bwd_workspace_size(ctypes.byref(lay), 8192, 6)
+    assert bneed >= need + 2 * 8192 * 8 * 1408 * 2
+    rc, _ = rc_and_msg(L, "moe_grouped_swiglu_bwd", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
+                       FAKE, MIS, FAKE, 0, FAKE, ctypes.c_size_t(bneed), None)
+    assert rc == api.MOE_ERR_ALIGN
+    rc, _ = rc_and_msg(L, "moe_unpermute", None, FAKE, FAKE, FAKE, 8, 2, FAKE, None)
+    assert rc == api.MOE_ERR_ARG
+    rc, _ = rc_and_msg(L, "moe_permute_bwd", ctypes.byref(lay), FAKE, FAKE, 8, 17, FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED                            # k > 16
+
+
+def test_error_message_is_cleared_on_success(L):
+    rc_and_msg(L, "moe_route_topk", None, FAKE, api.MOE_BF16, None, 16, 64, 8, 2, FAKE, FAKE, None, None)
+    assert L.moe_last_error().decode() != ""
+    rc, msg = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_BF16, None, 0, 64, 8, 2, FAKE, FAKE, None, None)
+    assert rc == 0 and msg == ""
+
+
+def test_plan_from_groups_arrays():
+    pa = api.plan_from_groups(8, ((0, 1), (2, 3)))
+    assert list(pa["expert_map"]) == [4, 4, 5, 5, 0, 1, 2, 3]
+    assert list(pa["slot_src"]) == [4, 5, 6, 7, 8, 9]
+    assert list(pa["grp_ptr"]) == [0, 2, 4] and list(pa["grp_member"]) == [0, 1, 2, 3]

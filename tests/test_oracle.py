@@ -332,3 +332,16 @@ def test_empty_tuning_slot_gets_zero_dw():
     _, dW, _ = O.moe_backward(X, dY, idx, gate, emap, slots)
     for s in (1, 2):
         assert all(np.all(w == 0) for w in dW[s])
+
+
+def test_grad_columns_match_central_differences():
+    r = rng(16)
+    n, d, I = 6, 4, 7
+    x, dO = r.normal(size=(n, d)), r.normal(size=(n, d))
+    Wg, Wu, Wd = r.normal(size=(I, d)), r.normal(size=(I, d)), r.normal(size=(d, I))
+    f = lambda: float(np.sum(dO * O.swiglu_fwd(x, Wg, Wu, Wd)[3]))
+    cols = [1, 4, 6]
+    dWg, dWu, dWd = O.expert_grad_columns(x, Wg, Wu, Wd, dO, cols)
+    np.testing.assert_allclose(dWg, _fd(f, Wg)[cols], rtol=1e-7, atol=1e-8)
+    np.testing.assert_allclose(dWu, _fd(f, Wu)[cols], rtol=1e-7, atol=1e-8)
+    np.testing.assert_allclose(dWd, _fd(f, Wd)[:, cols], rtol=1e-7, atol=1e-8)

@@ -30,5 +30,5 @@ def test_linear_merge_schedule_and_biases():
     assert sorted(np.round(np.exp(-z / 1.2)).astype(int)) == list(range(1, 65))
     nb = W.router_bias(W.WORKLOADS["llama_moe"])
     assert nb.shape == (16,) and nb.std() > 0.5
-    assert W.layer_merge_spec(W.WORKLOADS["deepseek_stack"], 0) is None
+    assert W.layer_merge_spec(W.WORKLOADS["deepseek_stack"], 0) == ("frequency", 0, 4)
     assert W.layer_merge_spec(W.WORKLOADS["deepseek_stack"], 27) == ("frequency", 48, 4)
