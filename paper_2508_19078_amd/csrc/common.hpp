@@ -104,11 +104,21 @@ __device__ __forceinline__ u32x4_t pack16(const float* in, float*) {
   return v;
 }
 
+// Global-memory accesses through explicit address-space-1 pointers, so that
+// the compiler emits global_load/global_store (not flat) even for pointers
+// read from device-side tables.
+#define FM_GLOBAL __attribute__((address_space(1)))
+template <typename T> __device__ __forceinline__ const FM_GLOBAL T* gptr(const T* p) {
+  return (const FM_GLOBAL T*)(p);
+}
+template <typename T> __device__ __forceinline__ FM_GLOBAL T* gptr(T* p) {
+  return (FM_GLOBAL T*)(p);
+}
 __device__ __forceinline__ u32x4_t ld16(const void* p) {
-  return *reinterpret_cast<const u32x4_t*>(p);
+  return *(const FM_GLOBAL u32x4_t*)(p);
 }
 __device__ __forceinline__ void st16(void* p, const u32x4_t& v) {
-  *reinterpret_cast<u32x4_t*>(p) = v;
+  *(FM_GLOBAL u32x4_t*)(p) = v;
 }
 
 // Wave64 helpers.

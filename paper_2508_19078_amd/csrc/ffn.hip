@@ -13,7 +13,7 @@
 //           dx      : dX_s = dA_g W_gate + dA_u W_up            (K = 2I in two passes)
 //           dw_gu   : dW_gate = dA_g^T X_s, dW_up = dA_u^T X_s  (tuning slots)
 //           dw_d    : dW_down = dO^T H                          (tuning slots)
-#include "gemm.hpp"
+#include "gemm_bf16.hpp"
 
 namespace fm {
 namespace {
@@ -92,8 +92,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gate_up(LayerPtrs<T> W, const T* 
                                                        const int2* __restrict__ tiles, int S_r, int Tn,
                                                        int k, int d, int I, T* __restrict__ Ag,
                                                        T* __restrict__ Au, T* __restrict__ H) {
-  typedef GemmCfg<T> C;
-  __shared__ __align__(16) T lds[2 * 3 * C::TILE];
+  __shared__ __align__(16) char lds[LdsBytes<T, 1, 2>::value];
   if ((int)blockIdx.y >= tiles[0].x) return;
   const int2 tl = tiles[1 + blockIdx.y];
   const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
@@ -103,7 +102,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gate_up(LayerPtrs<T> W, const T* 
   Opnd<T> B[2] = {{W.wg[sr.s] + (size_t)n0 * d, d, I - n0, d}, {W.wu[sr.s] + (size_t)n0 * d, d, I - n0, d}};
   Acc<T, 1, 2> acc;
   acc.zero();
-  gemm_mainloop<T, true, true, 1, 2>(A, B, d, lds, acc);
+  run_gemm<T, true, true, 1, 2>(A, B, d, lds, acc);
   const size_t ob = (size_t)(sr.orow0 + sr.m0);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -128,8 +127,7 @@ __global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __r
                                                     const int32_t* __restrict__ offsets,
                                                     const int2* __restrict__ tiles, int S_r, int Tn,
                                                     int k, int d, int I, T* __restrict__ O) {
-  typedef GemmCfg<T> C;
-  __shared__ __align__(16) T lds[2 * 2 * C::TILE];
+  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
   if ((int)blockIdx.y >= tiles[0].x) return;
   const int2 tl = tiles[1 + blockIdx.y];
   const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
@@ -139,7 +137,7 @@ __global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __r
   Opnd<T> B[1] = {{W.wd[sr.s] + (size_t)n0 * I, I, d - n0, I}};
   Acc<T, 1, 1> acc;
   acc.zero();
-  gemm_mainloop<T, true, true, 1, 1>(A, B, I, lds, acc);
+  run_gemm<T, true, true, 1, 1>(A, B, I, lds, acc);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -159,8 +157,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dh(LayerPtrs<T> W, const T* __res
                                                   const int32_t* __restrict__ offsets,
                                                   const int2* __restrict__ tiles, int S_r, int Tn, int k,
                                                   int d, int I, T* __restrict__ dAg, T* __restrict__ dAu) {
-  typedef GemmCfg<T> C;
-  __shared__ __align__(16) T lds[2 * 2 * C::TILE];
+  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
   if ((int)blockIdx.y >= tiles[0].x) return;
   const int2 tl = tiles[1 + blockIdx.y];
   const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
@@ -171,7 +168,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dh(LayerPtrs<T> W, const T* __res
   Opnd<T> B[1] = {{W.wd[sr.s] + n0, I, I - n0, d}};
   Acc<T, 1, 1> acc;
   acc.zero();
-  gemm_mainloop<T, true, false, 1, 1>(A, B, d, lds, acc);
+  run_gemm<T, true, false, 1, 1>(A, B, d, lds, acc);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -199,8 +196,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dx(LayerPtrs<T> W, const T* __res
                                                   const int32_t* __restrict__ offsets,
                                                   const int2* __restrict__ tiles, int S_r, int Tn, int k,
                                                   int d, int I, T* __restrict__ dXp) {
-  typedef GemmCfg<T> C;
-  __shared__ __align__(16) T lds[2 * 2 * C::TILE];
+  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
   if ((int)blockIdx.y >= tiles[0].x) return;
   const int2 tl = tiles[1 + blockIdx.y];
   const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
@@ -211,12 +207,12 @@ __global__ __launch_bounds__(G_THREADS) void k_dx(LayerPtrs<T> W, const T* __res
   {  // B(n = hidden index, k = intermediate index) = W_gate[k][n]
     Opnd<T> A[1] = {{dAg + ob * I, I, sr.nrows - sr.m0, I}};
     Opnd<T> B[1] = {{W.wg[sr.s] + n0, d, d - n0, I}};
-    gemm_mainloop<T, true, false, 1, 1>(A, B, I, lds, acc);
+    run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
   }
   {
     Opnd<T> A[1] = {{dAu + ob * I, I, sr.nrows - sr.m0, I}};
     Opnd<T> B[1] = {{W.wu[sr.s] + n0, d, d - n0, I}};
-    gemm_mainloop<T, true, false, 1, 1>(A, B, I, lds, acc);
+    run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -230,11 +226,8 @@ __global__ __launch_bounds__(G_THREADS) void k_dx(LayerPtrs<T> W, const T* __res
 }
 
 __device__ __forceinline__ void store_dw(float* p, f32x4_t v, bool accumulate) {
-  if (accumulate) {
-    const f32x4_t o = *reinterpret_cast<const f32x4_t*>(p);
-    v = v + o;
-  }
-  *reinterpret_cast<f32x4_t*>(p) = v;
+  if (accumulate) v = v + load4(p);
+  store4(p, v);
 }
 
 // grid (d / 128 column tiles, I / 128 row tiles, slots)
@@ -244,8 +237,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_gu(LayerPtrs<T> W, const T* __
                                                      const T* __restrict__ dAu,
                                                      const int32_t* __restrict__ offsets, int S_r, int Tn,
                                                      int k, int d, int I, int accumulate) {
-  typedef GemmCfg<T> C;
-  __shared__ __align__(16) T lds[2 * 3 * C::TILE];
+  __shared__ __align__(16) char lds[LdsBytes<T, 2, 1>::value];
   const int s = blockIdx.z;
   float* dwg = W.dwg[s];
   float* dwu = W.dwu[s];
@@ -258,7 +250,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_gu(LayerPtrs<T> W, const T* __
   Opnd<T> B[1] = {{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, d, d - n0, sr.nrows}};
   Acc<T, 2, 1> acc;
   acc.zero();
-  gemm_mainloop<T, false, false, 2, 1>(A, B, sr.nrows, lds, acc);
+  run_gemm<T, false, false, 2, 1>(A, B, sr.nrows, lds, acc);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -277,8 +269,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_d(LayerPtrs<T> W, const T* __r
                                                     const T* __restrict__ H,
                                                     const int32_t* __restrict__ offsets, int S_r, int Tn,
                                                     int k, int d, int I, int accumulate) {
-  typedef GemmCfg<T> C;
-  __shared__ __align__(16) T lds[2 * 2 * C::TILE];
+  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
   const int s = blockIdx.z;
   float* dwd = W.dwd[s];
   if (!dwd) return;
@@ -289,7 +280,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_d(LayerPtrs<T> W, const T* __r
   Opnd<T> B[1] = {{H + (size_t)sr.orow0 * I + n0, I, I - n0, sr.nrows}};
   Acc<T, 1, 1> acc;
   acc.zero();
-  gemm_mainloop<T, false, false, 1, 1>(A, B, sr.nrows, lds, acc);
+  run_gemm<T, false, false, 1, 1>(A, B, sr.nrows, lds, acc);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll

@@ -87,7 +87,7 @@ template <typename T, bool KC> struct Stager {
       for (int u = 0; u < NCH; ++u) {
         const int c = tid + G_THREADS * u;
         const int r = c / (BK / V), kc = (c % (BK / V)) * V;
-        st16(lds + r * C::LDSS + kc, reg[u]);
+        *reinterpret_cast<u32x4_t*>(lds + r * C::LDSS + kc) = reg[u];   // LDS
       }
     } else {
 #pragma unroll
@@ -209,19 +209,20 @@ __device__ __forceinline__ AccCoord acc_coord(int i, int j) {
   return AccCoord{(wave & 1) * 64 + i * 16 + (lane & 15), (wave >> 1) * 64 + j * 16 + 4 * (lane >> 4)};
 }
 
-// 4 consecutive values <-> memory of T.
+// 4 consecutive values <-> global memory of T.
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void store4(bf16* p, f32x4_t v) {
-  uint2 o;
-  o.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-  o.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-  *reinterpret_cast<uint2*>(p) = o;
+  u32x2_t o;
+  o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+  o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+  *(FM_GLOBAL u32x2_t*)(p) = o;
 }
-__device__ __forceinline__ void store4(float* p, f32x4_t v) { *reinterpret_cast<f32x4_t*>(p) = v; }
+__device__ __forceinline__ void store4(float* p, f32x4_t v) { *(FM_GLOBAL f32x4_t*)(p) = v; }
 __device__ __forceinline__ f32x4_t load4(const bf16* p) {
-  const uint2 w = *reinterpret_cast<const uint2*>(p);
-  return f32x4_t{__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u),
-                 __uint_as_float(w.y << 16), __uint_as_float(w.y & 0xFFFF0000u)};
+  const u32x2_t w = *(const FM_GLOBAL u32x2_t*)(p);
+  return f32x4_t{__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xFFFF0000u),
+                 __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xFFFF0000u)};
 }
-__device__ __forceinline__ f32x4_t load4(const float* p) { return *reinterpret_cast<const f32x4_t*>(p); }
+__device__ __forceinline__ f32x4_t load4(const float* p) { return *(const FM_GLOBAL f32x4_t*)(p); }
 
 }  // namespace fm

@@ -6,10 +6,10 @@
 // into interleaved 16-byte-per-lane chunks and accumulate the token x expert
 // logits on MFMA (16x16x32 bf16, or 16x16x4 fp32 for fp32 inputs).  The four
 // partial sums are added in a fixed order in LDS, so the logits do not depend
-// on scheduling.  Then one lane per token selects the top k by
-// (logit desc, index asc) with an unrolled insertion list, and either writes
-// idx/gate or adds the selection to an LDS histogram that is flushed to the
-// global counts with one integer atomic per expert and block.
+// on scheduling.  Then 16 lanes per token select the top k by
+// (logit desc, index asc) with branch-free 64-bit key reductions, and either
+// write idx/gate or add the selection to an LDS histogram that is flushed to
+// the global counts with one integer atomic per expert and block.
 #include "common.hpp"
 
 namespace fm {
@@ -41,11 +41,12 @@ __device__ __forceinline__ f32x4_t load_w_frag(const float* p, bool ok, f32x4_t)
 }
 // int8 codes widened exactly to bf16 (|q| <= 127 has at most 7 significant bits).
 __device__ __forceinline__ bf16x8_t load_w_frag(const int8_t* p, bool ok, bf16x8_t) {
-  uint2 raw = ok ? *reinterpret_cast<const uint2*>(p) : make_uint2(0, 0);
+  typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+  u32x2_t raw = ok ? *(const FM_GLOBAL u32x2_t*)(p) : u32x2_t{0, 0};
   u32x4_t v;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    uint32_t w = i < 2 ? raw.x : raw.y;
+    uint32_t w = i < 2 ? raw[0] : raw[1];
     int sh = (i & 1) * 16;
     float lo = (float)(int8_t)((w >> sh) & 0xFF);
     float hi = (float)(int8_t)((w >> (sh + 8)) & 0xFF);
@@ -54,11 +55,35 @@ __device__ __forceinline__ bf16x8_t load_w_frag(const int8_t* p, bool ok, bf16x8
   return __builtin_bit_cast(bf16x8_t, v);
 }
 __device__ __forceinline__ f32x4_t load_w_frag(const int8_t* p, bool ok, f32x4_t) {
-  uint32_t raw = ok ? *reinterpret_cast<const uint32_t*>(p) : 0u;
+  uint32_t raw = ok ? *(const FM_GLOBAL uint32_t*)(p) : 0u;
   f32x4_t v;
 #pragma unroll
   for (int i = 0; i < 4; ++i) v[i] = (float)(int8_t)((raw >> (8 * i)) & 0xFF);
   return v;
+}
+
+// Order-preserving map of a finite fp32 (with -0.0 folded into +0.0 by the
+// caller) to uint32, and its inverse.
+__device__ __forceinline__ uint32_t ordered_key(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+// Rotation of a value within each row of 16 lanes (DPP row_ror).
+template <int N> __device__ __forceinline__ uint32_t row_ror_u(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x120 + N, 0xF, 0xF, false);
+}
+template <int N> __device__ __forceinline__ float row_ror(float x) {
+  return __uint_as_float(row_ror_u<N>(__float_as_uint(x)));
+}
+// (hi, lo) <- max((hi, lo), rotated (hi, lo)) as a 64-bit key.
+template <int N> __device__ __forceinline__ void key_max_row(uint32_t& hi, uint32_t& lo) {
+  const uint32_t h2 = row_ror_u<N>(hi), l2 = row_ror_u<N>(lo);
+  const bool tk = h2 > hi || (h2 == hi && l2 > lo);
+  hi = tk ? h2 : hi;
+  lo = tk ? l2 : lo;
 }
 
 // acc (16x16 tile) += A(16 x kc) * B(kc x 16)
@@ -101,46 +126,56 @@ __global__ __launch_bounds__(256) void k_route(
 
   const int nchunks = d / KC;
   const int tail = d - nchunks * KC;           // multiple of 8 (d % 8 == 0)
+  // Rows past T and experts past E read a clamped (valid) row: their logits
+  // are never used, so the main loop needs no predicated loads.
   const TX* xrow[2];
-  bool xok[2];
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    int t = t0 + r * 16 + r16;
-    xok[r] = t < T;
-    xrow[r] = X + (size_t)(xok[r] ? t : 0) * d;
-  }
+  for (int r = 0; r < 2; ++r) xrow[r] = X + (size_t)min(t0 + r * 16 + r16, T - 1) * d;
   const TW* wrow[NE];
-  bool wok[NE];
 #pragma unroll
-  for (int j = 0; j < NE; ++j) {
-    int e = j * 16 + r16;
-    wok[j] = e < E;
-    wrow[j] = W + (size_t)(wok[j] ? e : 0) * d;
-  }
+  for (int j = 0; j < NE; ++j) wrow[j] = W + (size_t)min(j * 16 + r16, E - 1) * d;
 
-  auto chunk = [&](int c0, bool full) {
-    int col = c0 + q4 * V;
-    bool cok = full || col < d;
+  // This wave's chunks are wave, wave + 4, ...; P of them are in flight.
+  constexpr int P = NE <= 4 ? 4 : 2;
+  const int nw = nchunks > wave ? (nchunks - wave + RT_WAVES - 1) / RT_WAVES : 0;
+  frag_t ra[P][2], rb[P][NE];
+  auto issue = [&](int u, int i) {
+    const int ci = min(i, nw - 1);
+    const int col = (wave + RT_WAVES * ci) * KC + q4 * V;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) ra[u][r] = load_x_frag(xrow[r] + col, true);
+#pragma unroll
+    for (int j = 0; j < NE; ++j) rb[u][j] = load_w_frag(wrow[j] + col, true, frag_t{});
+  };
+  if (nw > 0) {
+#pragma unroll
+    for (int u = 0; u < P; ++u) issue(u, u);
+    for (int i0 = 0; i0 < nw; i0 += P) {
+#pragma unroll
+      for (int u = 0; u < P; ++u) {
+        if (i0 + u < nw) {
+#pragma unroll
+          for (int r = 0; r < 2; ++r)
+#pragma unroll
+            for (int j = 0; j < NE; ++j) acc[r][j] = mma(ra[u][r], rb[u][j], acc[r][j]);
+        }
+        issue(u, i0 + u + P);
+      }
+    }
+  }
+  if (tail > 0 && wave == nchunks % RT_WAVES) {   // zero-filled last partial chunk
+    const int col = nchunks * KC + q4 * V;
+    const bool cok = col < d;
     frag_t a[2], b[NE];
 #pragma unroll
-    for (int r = 0; r < 2; ++r) a[r] = load_x_frag(xrow[r] + col, xok[r] && cok);
+    for (int r = 0; r < 2; ++r) a[r] = load_x_frag(xrow[r] + col, cok);
 #pragma unroll
-    for (int j = 0; j < NE; ++j) b[j] = load_w_frag(wrow[j] + col, wok[j] && cok, frag_t{});
+    for (int j = 0; j < NE; ++j) b[j] = load_w_frag(wrow[j] + col, cok, frag_t{});
 #pragma unroll
     for (int r = 0; r < 2; ++r)
 #pragma unroll
       for (int j = 0; j < NE; ++j) acc[r][j] = mma(a[r], b[j], acc[r][j]);
-  };
-
-  int c = wave;
-  for (; c + 3 * RT_WAVES < nchunks; c += 4 * RT_WAVES) {
-    chunk(c * KC, true);
-    chunk((c + RT_WAVES) * KC, true);
-    chunk((c + 2 * RT_WAVES) * KC, true);
-    chunk((c + 3 * RT_WAVES) * KC, true);
   }
-  for (; c < nchunks; c += RT_WAVES) chunk(c * KC, true);
-  if (tail > 0 && wave == nchunks % RT_WAVES) chunk(nchunks * KC, false);
 
   // fixed-order reduction of the four partial sums: ((p0 + p1) + p2) + p3
   for (int w = 0; w < RT_WAVES; ++w) {
@@ -170,48 +205,64 @@ __global__ __launch_bounds__(256) void k_route(
   }
   __syncthreads();
 
-  // one lane per token: top-k by (value desc, index asc)
-  const int tl = wave * 8 + (lane & 7);
-  if (lane < 8 && t0 + tl < T) {
-    float bv[KMAX];
-    int bi[KMAX];
+  // Top-k: 16 lanes per token, 4 tokens per wave and round.  Lane gl of the
+  // group holds experts gl, gl+16, ...  Keys order (value desc, index asc): the
+  // high word maps the fp32 value monotonically to uint32 (-0.0 == +0.0), the
+  // low word is 0xFFFF - expert.  Each of the k selection rounds takes the
+  // group maximum with four DPP row rotations; the owner lane then drops it.
+  const int grp = lane >> 4, gl = lane & 15;
 #pragma unroll
-    for (int j = 0; j < KMAX; ++j) { bv[j] = -INFINITY; bi[j] = 0x7FFFFFFF; }
-    const float* row = &red[tl * EP];
-    for (int e = 0; e < E; ++e) {
-      float v = row[e] + 0.0f;                  // -0.0 -> +0.0
-      int ie = e;
+  for (int round = 0; round < 2; ++round) {
+    const int tl = wave * 8 + round * 4 + grp;
+    const int t = t0 + tl;
+    uint32_t khi[NE], klo[NE];
 #pragma unroll
-      for (int j = 0; j < KMAX; ++j) {
-        if (j < k && ranks_before(v, ie, bv[j], bi[j])) {
-          float tv = bv[j]; int ti = bi[j];
-          bv[j] = v; bi[j] = ie;
-          v = tv; ie = ti;
+    for (int i = 0; i < NE; ++i) {
+      const int e = gl + 16 * i;
+      const float v = red[tl * EP + e] + 0.0f;
+      khi[i] = e < E ? ordered_key(v) : 0u;
+      klo[i] = e < E ? 0xFFFFu - (uint32_t)e : 0u;
+    }
+    float myv = 0.f, v0 = 0.f;
+    int mye = 0;
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k) {
+        uint32_t bh = khi[0], bl = klo[0];
+#pragma unroll
+        for (int i = 1; i < NE; ++i) {
+          const bool tk = khi[i] > bh || (khi[i] == bh && klo[i] > bl);
+          bh = tk ? khi[i] : bh;
+          bl = tk ? klo[i] : bl;
         }
+        key_max_row<8>(bh, bl);
+        key_max_row<4>(bh, bl);
+        key_max_row<2>(bh, bl);
+        key_max_row<1>(bh, bl);
+        const int e = 0xFFFF - (int)bl;
+        const float v = key_value(bh);
+        if (j == 0) v0 = v;
+        if (gl == j) { myv = v; mye = e; }
+#pragma unroll
+        for (int i = 0; i < NE; ++i)
+          if (gl + 16 * i == e) { khi[i] = 0u; klo[i] = 0u; }
       }
     }
-    const size_t t = (size_t)(t0 + tl);
+    const bool mine = gl < k && t < T;
     if (MODE == 0) {
-      float s = 0.f, g[KMAX];
-#pragma unroll
-      for (int j = 0; j < KMAX; ++j) {
-        g[j] = (j < k) ? expf(bv[j] - bv[0]) : 0.f;
-        s += g[j];
+      float g = gl < k ? expf(myv - v0) : 0.f;
+      float sum = g;
+      sum += row_ror<8>(sum);
+      sum += row_ror<4>(sum);
+      sum += row_ror<2>(sum);
+      sum += row_ror<1>(sum);
+      if (mine) {
+        idx[(size_t)t * k + gl] = mye;
+        gate[(size_t)t * k + gl] = g / sum;
       }
-      float inv = 1.0f / s;
-#pragma unroll
-      for (int j = 0; j < KMAX; ++j)
-        if (j < k) {
-          idx[t * k + j] = bi[j];
-          gate[t * k + j] = g[j] * inv;
-        }
-    } else {
-#pragma unroll
-      for (int j = 0; j < KMAX; ++j)
-        if (j < k) {
-          atomicAdd(&hist[bi[j]], 1);
-          if (idx) idx[t * k + j] = bi[j];
-        }
+    } else if (mine) {
+      atomicAdd(&hist[mye], 1);
+      if (idx) idx[(size_t)t * k + gl] = mye;
     }
   }
   if (MODE == 1) {
