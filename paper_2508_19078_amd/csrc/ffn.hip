@@ -2,10 +2,7 @@
 //
 // Rows of slot s live in the per-row buffers at the slot's row range (routed:
 // [offsets[s], offsets[s+1]) read from device memory; shared expert i:
-// [T*k + i*T, T*k + (i+1)*T)).  A one-block kernel turns the offsets into a
-// list of (slot, first row) M-tiles of 128 rows; the GEMM grids are sized by
-// the host-side upper bound of that list and surplus blocks exit at once, so
-// the host never waits for the bucket sizes.
+// [T*k + i*T, T*k + (i+1)*T)).  The host never learns the bucket sizes.
 //
 // forward   gate_up : [A_g | A_u] = X_s [W_gate | W_up]^T, epilogue H = silu(A_g) A_u
 //           down    : O = H W_down^T
@@ -13,25 +10,32 @@
 //           dx      : dX_s = dA_g W_gate + dA_u W_up            (K = 2I in two passes)
 //           dw_gu   : dW_gate = dA_g^T X_s, dW_up = dA_u^T X_s  (tuning slots)
 //           dw_d    : dW_down = dO^T H                          (tuning slots)
+//
+// Scheduling.  A one-block kernel turns the offsets into a schedule: prefix
+// sums of each slot's 128-row tiles and, for the weight gradients, of each
+// tuning slot's work (its K slabs).  The GEMM kernels are persistent, one block
+// per compute unit.  Blocks are dispatched to the 8 XCDs round-robin, so block
+// b runs on XCD b % 8; each XCD walks its own contiguous range of the tile
+// space, ordered slot-major, then in bands of row tiles (see band_order).
+// Concurrent blocks of an XCD thus share a band of one slot's activations and a
+// few weight column tiles, which stay in that XCD's L2.  The weight-gradient tile
+// space is split between XCDs by work rather than by tile count.
 #include "gemm_bf16.hpp"
 
 namespace fm {
 namespace {
 
+constexpr int N_XCD = 8;
+
 struct SlotRows {
-  int s;        // slot
-  int m0;       // first row of this tile within the slot
   int nrows;    // rows of the slot
   long orow0;   // first row of the slot in the per-row buffers
   long xrow0;   // first row of the slot's input in X_perm (routed) or X (shared)
   bool shared;
 };
 
-__device__ __forceinline__ SlotRows slot_rows(int s, int m0, const int32_t* offsets, int S_r, int Tn,
-                                              int k) {
+__device__ __forceinline__ SlotRows slot_rows(int s, const int32_t* offsets, int S_r, int Tn, int k) {
   SlotRows r;
-  r.s = s;
-  r.m0 = m0;
   if (s < S_r) {
     const int b = offsets[s];
     r.nrows = offsets[s + 1] - b;
@@ -47,24 +51,108 @@ __device__ __forceinline__ SlotRows slot_rows(int s, int m0, const int32_t* offs
   return r;
 }
 
-// tiles[0].x = number of tiles; tiles[1 + i] = (slot, first row).
-__global__ __launch_bounds__(1024) void k_build_tiles(const int32_t* __restrict__ offsets, int S_r,
-                                                      int S_sh, int Tn, int bm, int2* __restrict__ tiles) {
-  __shared__ int base[1025];
-  const int S = S_r + S_sh;
-  const int s = threadIdx.x;
+// Schedule in the workspace: mbase[0..S] (prefix of 128-row tiles per slot)
+// and wbase[0..S] (prefix of weight-gradient work per slot, 64-bit).
+struct Sched {
+  int32_t* mbase;
+  long long* wbase;
+};
+inline size_t sched_part(int S) { return ((sizeof(int32_t) * (S + 1) + 255) / 256) * 256; }
+inline size_t sched_bytes(int S) { return sched_part(S) + ((sizeof(long long) * (S + 1) + 255) / 256) * 256; }
+inline Sched sched_at(void* ws, int S) {
+  Sched s;
+  s.mbase = (int32_t*)ws;
+  s.wbase = (long long*)((char*)ws + sched_part(S));
+  return s;
+}
+
+// One block of 1024 threads (S <= 1024).  wtiles = weight-gradient tiles per
+// slot; a tuning slot's work per tile is its K slabs + 1 (so an empty tuning
+// slot still gets its zeros written); frozen slots have none.
+__global__ __launch_bounds__(1024) void k_build_sched(const int32_t* __restrict__ offsets, int S_r, int S_sh,
+                                                      int Tn, float* const* __restrict__ dw_tab, int wtiles,
+                                                      int32_t* __restrict__ mbase, long long* __restrict__ wbase) {
+  __shared__ int sm[1024];
+  __shared__ long long sw[1024];
+  const int S = S_r + S_sh, s = threadIdx.x;
   int n = 0;
   if (s < S) n = s < S_r ? offsets[s + 1] - offsets[s] : Tn;
-  const int nt = (n + bm - 1) / bm;
-  base[s + 1] = nt;
-  if (s == 0) base[0] = 0;
+  long long w = 0;
+  if (s < S && dw_tab && dw_tab[s]) w = (long long)wtiles * ((n + B16_BK - 1) / B16_BK + 1);
+  sm[s] = (n + G_BM - 1) / G_BM;
+  sw[s] = w;
   __syncthreads();
-  if (threadIdx.x == 0)
-    for (int i = 1; i <= (int)blockDim.x; ++i) base[i] += base[i - 1];
-  __syncthreads();
-  if (s < S)
-    for (int t = 0; t < nt; ++t) tiles[1 + base[s] + t] = make_int2(s, t * bm);
-  if (threadIdx.x == 0) tiles[0] = make_int2(base[blockDim.x], 0);
+  for (int off = 1; off < 1024; off <<= 1) {   // inclusive Hillis-Steele scans
+    const int a = s >= off ? sm[s - off] : 0;
+    const long long b = s >= off ? sw[s - off] : 0;
+    __syncthreads();
+    sm[s] += a;
+    sw[s] += b;
+    __syncthreads();
+  }
+  if (s <= S) {
+    mbase[s] = s == 0 ? 0 : sm[s - 1];
+    wbase[s] = s == 0 ? 0 : sw[s - 1];
+  }
+}
+
+// Largest s in [0, S) with base[s] <= v (base nondecreasing, base[0] = 0).
+template <typename B>
+__device__ __forceinline__ int find_slot(const B* base, int S, long long v) {
+  int lo = 0, hi = S - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if ((long long)base[mid] <= v) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+struct Tile {
+  int s, n, m;   // slot, output column tile, output row tile
+};
+
+// Order of the (row tile, column tile) pairs of one slot: bands of GM row
+// tiles; inside a band column tiles advance slowest and row tiles fastest.  The
+// blocks of an XCD working on one band share its GM activation tiles and a few
+// weight tiles, a working set that fits the XCD's L2.
+__device__ __forceinline__ void band_order(int loc, int mt, int NT, int GM, int& m, int& n) {
+  const int band = loc / (GM * NT);
+  const int h = min(GM, mt - band * GM);
+  const int rem = loc - band * GM * NT;
+  n = rem / h;
+  m = band * GM + rem % h;
+}
+
+constexpr int GM_ROWS = 8;   // band height of the row-tile GEMMs
+constexpr int GM_DW = 4;     // band height of the weight-gradient GEMMs
+
+// Row-tile GEMMs: tile t of [0, M_total * NT), slot-major.
+__device__ __forceinline__ Tile row_tile(const int32_t* mbase, int S, int NT, long long t) {
+  Tile r;
+  r.s = find_slot(mbase, S, t / NT);
+  const int mt = mbase[r.s + 1] - mbase[r.s];
+  band_order((int)(t - (long long)mbase[r.s] * NT), mt, NT, GM_ROWS, r.m, r.n);
+  return r;
+}
+
+// Weight-gradient tile t: tps = MT * NT tiles per slot.
+__device__ __forceinline__ Tile dw_tile(long long t, int tps, int MT) {
+  Tile r;
+  r.s = (int)(t / tps);
+  band_order((int)(t - (long long)r.s * tps), MT, tps / MT, GM_DW, r.m, r.n);
+  return r;
+}
+
+// First weight-gradient tile whose cumulative work reaches `target`.
+__device__ __forceinline__ long long tile_at_work(const long long* wbase, int S, int tps, long long target) {
+  if (target >= wbase[S]) return (long long)S * tps;
+  const int s = find_slot(wbase, S, target);
+  const long long per = (wbase[s + 1] - wbase[s]) / tps;   // work per tile of slot s
+  if (per == 0) return (long long)(s + 1) * tps;
+  long long i = (target - wbase[s] + per - 1) / per;
+  if (i > tps) i = tps;
+  return (long long)s * tps + i;
 }
 
 template <typename T> struct LayerPtrs {
@@ -83,70 +171,100 @@ template <typename T> LayerPtrs<T> layer_ptrs(const moe_layer* L) {
 
 __device__ __forceinline__ float sigm(float z) { return 1.0f / (1.0f + expf(-z)); }
 
+struct RowArgs {
+  const int32_t* offsets;
+  const int32_t* mbase;
+  int S_r, S, Tn, k, d, I;
+};
+
+struct DwArgs {
+  const int32_t* offsets;
+  const long long* wbase;
+  int S_r, S, Tn, k, d, I, accumulate;
+};
+
+// The range of the tile space handled by this block's XCD, and the block's
+// first tile and stride inside it.
+struct TileRange {
+  long long lo, hi;
+  int first, step;
+};
+__device__ __forceinline__ TileRange row_range(const RowArgs& ra, int NT) {
+  const long long total = (long long)ra.mbase[ra.S] * NT;
+  const int x = blockIdx.x % N_XCD;
+  return TileRange{total * x / N_XCD, total * (x + 1) / N_XCD, (int)(blockIdx.x / N_XCD),
+                   (int)(gridDim.x / N_XCD)};
+}
+__device__ __forceinline__ TileRange dw_range(const DwArgs& da, int tps) {
+  const long long w = da.wbase[da.S];
+  const int x = blockIdx.x % N_XCD;
+  return TileRange{tile_at_work(da.wbase, da.S, tps, w * x / N_XCD),
+                   tile_at_work(da.wbase, da.S, tps, w * (x + 1) / N_XCD), (int)(blockIdx.x / N_XCD),
+                   (int)(gridDim.x / N_XCD)};
+}
+
 // ------------------------------------------------------------- forward ----
 
 template <typename T>
 __global__ __launch_bounds__(G_THREADS) void k_gate_up(LayerPtrs<T> W, const T* __restrict__ X,
-                                                       const T* __restrict__ Xp,
-                                                       const int32_t* __restrict__ offsets,
-                                                       const int2* __restrict__ tiles, int S_r, int Tn,
-                                                       int k, int d, int I, T* __restrict__ Ag,
-                                                       T* __restrict__ Au, T* __restrict__ H) {
+                                                       const T* __restrict__ Xp, RowArgs ra,
+                                                       T* __restrict__ Ag, T* __restrict__ Au,
+                                                       T* __restrict__ H) {
   __shared__ __align__(16) char lds[LdsBytes<T, 1, 2>::value];
-  if ((int)blockIdx.y >= tiles[0].x) return;
-  const int2 tl = tiles[1 + blockIdx.y];
-  const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
-  const int n0 = blockIdx.x * G_BN;
-  const T* xs = (sr.shared ? X : Xp) + (size_t)(sr.xrow0 + sr.m0) * d;
-  Opnd<T> A[1] = {{xs, d, sr.nrows - sr.m0, d}};
-  Opnd<T> B[2] = {{W.wg[sr.s] + (size_t)n0 * d, d, I - n0, d}, {W.wu[sr.s] + (size_t)n0 * d, d, I - n0, d}};
-  Acc<T, 1, 2> acc;
-  acc.zero();
-  run_gemm<T, true, true, 1, 2>(A, B, d, lds, acc);
-  const size_t ob = (size_t)(sr.orow0 + sr.m0);
+  const int d = ra.d, I = ra.I, NT = (I + G_BN - 1) / G_BN;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
+    const T* xs = (sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d;
+    Opnd<T> A[1] = {{xs, d, sr.nrows - m0, d}};
+    Opnd<T> B[2] = {{W.wg[rt.s] + (size_t)n0 * d, d, I - n0, d}, {W.wu[rt.s] + (size_t)n0 * d, d, I - n0, d}};
+    Acc<T, 1, 2> acc;
+    acc.zero();
+    run_gemm<T, true, true, 1, 2>(A, B, d, lds, acc);
+    const size_t ob = (size_t)(sr.orow0 + m0);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const AccCoord c = acc_coord(i, j);
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = quad_coord<T>(q);
       const int n = n0 + c.col4;
-      if (c.row >= sr.nrows - sr.m0 || n >= I) continue;
-      const f32x4_t g = acc.v[0][i][j], u = acc.v[1][i][j];
+      if (c.row >= sr.nrows - m0 || n >= I) continue;
+      const f32x4_t ag = acc.quad(0, q), u = acc.quad(1, q);
       f32x4_t h;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) h[r] = g[r] * sigm(g[r]) * u[r];
+      for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm(ag[r]) * u[r];
       const size_t o = (ob + c.row) * I + n;
-      store4(Ag + o, g);
+      store4(Ag + o, ag);
       store4(Au + o, u);
       store4(H + o, h);
     }
+  }
 }
 
 template <typename T>
-__global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __restrict__ H,
-                                                    const int32_t* __restrict__ offsets,
-                                                    const int2* __restrict__ tiles, int S_r, int Tn,
-                                                    int k, int d, int I, T* __restrict__ O) {
+__global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __restrict__ H, RowArgs ra,
+                                                    T* __restrict__ O) {
   __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
-  if ((int)blockIdx.y >= tiles[0].x) return;
-  const int2 tl = tiles[1 + blockIdx.y];
-  const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
-  const int n0 = blockIdx.x * G_BN;
-  const size_t ob = (size_t)(sr.orow0 + sr.m0);
-  Opnd<T> A[1] = {{H + ob * I, I, sr.nrows - sr.m0, I}};
-  Opnd<T> B[1] = {{W.wd[sr.s] + (size_t)n0 * I, I, d - n0, I}};
-  Acc<T, 1, 1> acc;
-  acc.zero();
-  run_gemm<T, true, true, 1, 1>(A, B, I, lds, acc);
+  const int d = ra.d, I = ra.I, NT = (d + G_BN - 1) / G_BN;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    Opnd<T> A[1] = {{H + ob * I, I, sr.nrows - m0, I}};
+    Opnd<T> B[1] = {{W.wd[rt.s] + (size_t)n0 * I, I, d - n0, I}};
+    Acc<T, 1, 1> acc;
+    acc.zero();
+    run_gemm<T, true, true, 1, 1>(A, B, I, lds, acc);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const AccCoord c = acc_coord(i, j);
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = quad_coord<T>(q);
       const int n = n0 + c.col4;
-      if (c.row >= sr.nrows - sr.m0 || n >= d) continue;
-      store4(O + (ob + c.row) * d + n, acc.v[0][i][j]);
+      if (c.row >= sr.nrows - m0 || n >= d) continue;
+      store4(O + (ob + c.row) * d + n, acc.quad(0, q));
     }
+  }
 }
 
 // ------------------------------------------------------------ backward ----
@@ -154,75 +272,73 @@ __global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __r
 template <typename T>
 __global__ __launch_bounds__(G_THREADS) void k_dh(LayerPtrs<T> W, const T* __restrict__ dO,
                                                   const T* __restrict__ Ag, const T* __restrict__ Au,
-                                                  const int32_t* __restrict__ offsets,
-                                                  const int2* __restrict__ tiles, int S_r, int Tn, int k,
-                                                  int d, int I, T* __restrict__ dAg, T* __restrict__ dAu) {
+                                                  RowArgs ra, T* __restrict__ dAg, T* __restrict__ dAu) {
   __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
-  if ((int)blockIdx.y >= tiles[0].x) return;
-  const int2 tl = tiles[1 + blockIdx.y];
-  const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
-  const int n0 = blockIdx.x * G_BN;
-  const size_t ob = (size_t)(sr.orow0 + sr.m0);
-  // B(n = intermediate index, k = hidden index) = W_down[k][n]: MN-contiguous
-  Opnd<T> A[1] = {{dO + ob * d, d, sr.nrows - sr.m0, d}};
-  Opnd<T> B[1] = {{W.wd[sr.s] + n0, I, I - n0, d}};
-  Acc<T, 1, 1> acc;
-  acc.zero();
-  run_gemm<T, true, false, 1, 1>(A, B, d, lds, acc);
+  const int d = ra.d, I = ra.I, NT = (I + G_BN - 1) / G_BN;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    // B(n = intermediate index, k = hidden index) = W_down[k][n]: MN-contiguous
+    Opnd<T> A[1] = {{dO + ob * d, d, sr.nrows - m0, d}};
+    Opnd<T> B[1] = {{W.wd[rt.s] + n0, I, I - n0, d}};
+    Acc<T, 1, 1> acc;
+    acc.zero();
+    run_gemm<T, true, false, 1, 1>(A, B, d, lds, acc);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const AccCoord c = acc_coord(i, j);
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = quad_coord<T>(q);
       const int n = n0 + c.col4;
-      if (c.row >= sr.nrows - sr.m0 || n >= I) continue;
+      if (c.row >= sr.nrows - m0 || n >= I) continue;
       const size_t o = (ob + c.row) * I + n;
-      const f32x4_t dh = acc.v[0][i][j], g = load4(Ag + o), u = load4(Au + o);
+      const f32x4_t dh = acc.quad(0, q), ag = load4(Ag + o), u = load4(Au + o);
       f32x4_t dg, du;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float s = sigm(g[r]);
-        du[r] = dh[r] * g[r] * s;
-        dg[r] = dh[r] * u[r] * s * (1.0f + g[r] * (1.0f - s));
+        const float s = sigm(ag[r]);
+        du[r] = dh[r] * ag[r] * s;
+        dg[r] = dh[r] * u[r] * s * (1.0f + ag[r] * (1.0f - s));
       }
       store4(dAg + o, dg);
       store4(dAu + o, du);
     }
+  }
 }
 
 template <typename T>
 __global__ __launch_bounds__(G_THREADS) void k_dx(LayerPtrs<T> W, const T* __restrict__ dAg,
-                                                  const T* __restrict__ dAu,
-                                                  const int32_t* __restrict__ offsets,
-                                                  const int2* __restrict__ tiles, int S_r, int Tn, int k,
-                                                  int d, int I, T* __restrict__ dXp) {
+                                                  const T* __restrict__ dAu, RowArgs ra,
+                                                  T* __restrict__ dXp) {
   __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
-  if ((int)blockIdx.y >= tiles[0].x) return;
-  const int2 tl = tiles[1 + blockIdx.y];
-  const SlotRows sr = slot_rows(tl.x, tl.y, offsets, S_r, Tn, k);
-  const int n0 = blockIdx.x * G_BN;
-  const size_t ob = (size_t)(sr.orow0 + sr.m0);
-  Acc<T, 1, 1> acc;
-  acc.zero();
-  {  // B(n = hidden index, k = intermediate index) = W_gate[k][n]
-    Opnd<T> A[1] = {{dAg + ob * I, I, sr.nrows - sr.m0, I}};
-    Opnd<T> B[1] = {{W.wg[sr.s] + n0, d, d - n0, I}};
-    run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
-  }
-  {
-    Opnd<T> A[1] = {{dAu + ob * I, I, sr.nrows - sr.m0, I}};
-    Opnd<T> B[1] = {{W.wu[sr.s] + n0, d, d - n0, I}};
-    run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const AccCoord c = acc_coord(i, j);
-      const int n = n0 + c.col4;
-      if (c.row >= sr.nrows - sr.m0 || n >= d) continue;
-      store4(dXp + (ob + c.row) * d + n, acc.v[0][i][j]);
+  const int d = ra.d, I = ra.I, NT = (d + G_BN - 1) / G_BN;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    Acc<T, 1, 1> acc;
+    acc.zero();
+    {  // B(n = hidden index, k = intermediate index) = W_gate[k][n]
+      Opnd<T> A[1] = {{dAg + ob * I, I, sr.nrows - m0, I}};
+      Opnd<T> B[1] = {{W.wg[rt.s] + n0, d, d - n0, I}};
+      run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
     }
+    {
+      Opnd<T> A[1] = {{dAu + ob * I, I, sr.nrows - m0, I}};
+      Opnd<T> B[1] = {{W.wu[rt.s] + n0, d, d - n0, I}};
+      run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = quad_coord<T>(q);
+      const int n = n0 + c.col4;
+      if (c.row >= sr.nrows - m0 || n >= d) continue;
+      store4(dXp + (ob + c.row) * d + n, acc.quad(0, q));
+    }
+  }
 }
 
 __device__ __forceinline__ void store_dw(float* p, f32x4_t v, bool accumulate) {
@@ -230,66 +346,70 @@ __device__ __forceinline__ void store_dw(float* p, f32x4_t v, bool accumulate) {
   store4(p, v);
 }
 
-// grid (d / 128 column tiles, I / 128 row tiles, slots)
+// dW_gate = dA_g^T X_s, dW_up = dA_u^T X_s: rows over I, columns over d.
 template <typename T>
 __global__ __launch_bounds__(G_THREADS) void k_dw_gu(LayerPtrs<T> W, const T* __restrict__ X,
                                                      const T* __restrict__ Xp, const T* __restrict__ dAg,
-                                                     const T* __restrict__ dAu,
-                                                     const int32_t* __restrict__ offsets, int S_r, int Tn,
-                                                     int k, int d, int I, int accumulate) {
+                                                     const T* __restrict__ dAu, DwArgs da) {
   __shared__ __align__(16) char lds[LdsBytes<T, 2, 1>::value];
-  const int s = blockIdx.z;
-  float* dwg = W.dwg[s];
-  float* dwu = W.dwu[s];
-  if (!dwg || !dwu) return;
-  const SlotRows sr = slot_rows(s, 0, offsets, S_r, Tn, k);
-  const int n0 = blockIdx.x * G_BN, m0 = blockIdx.y * G_BM;
-  // A(m = intermediate index, k = row) = dA[row][m];  B(n = hidden index, k = row) = X_s[row][n]
-  Opnd<T> A[2] = {{dAg + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows},
-                  {dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows}};
-  Opnd<T> B[1] = {{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, d, d - n0, sr.nrows}};
-  Acc<T, 2, 1> acc;
-  acc.zero();
-  run_gemm<T, false, false, 2, 1>(A, B, sr.nrows, lds, acc);
+  const int d = da.d, I = da.I;
+  const int MT = (I + G_BM - 1) / G_BM, NT = (d + G_BN - 1) / G_BN;
+  const TileRange tr = dw_range(da, MT * NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = dw_tile(t, MT * NT, MT);
+    float* dwg = W.dwg[rt.s];
+    float* dwu = W.dwu[rt.s];
+    if (dwg && dwu) {
+      const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
+      const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
+      // A(m = intermediate index, k = row) = dA[row][m];  B(n = hidden index, k = row) = X_s[row][n]
+      Opnd<T> A[2] = {{dAg + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows},
+                      {dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows}};
+      Opnd<T> B[1] = {{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, d, d - n0, sr.nrows}};
+      Acc<T, 2, 1> acc;
+      acc.zero();
+      run_gemm<T, false, false, 2, 1>(A, B, sr.nrows, lds, acc);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const AccCoord c = acc_coord(i, j);
-      const int m = m0 + c.row, n = n0 + c.col4;
-      if (m >= I || n >= d) continue;
-      store_dw(dwg + (size_t)m * d + n, acc.v[0][i][j], accumulate);
-      store_dw(dwu + (size_t)m * d + n, acc.v[1][i][j], accumulate);
+      for (int q = 0; q < 16; ++q) {
+        const AccCoord c = quad_coord<T>(q);
+        const int m = m0 + c.row, n = n0 + c.col4;
+        if (m >= I || n >= d) continue;
+        store_dw(dwg + (size_t)m * d + n, acc.quad(0, q), da.accumulate);
+        store_dw(dwu + (size_t)m * d + n, acc.quad(1, q), da.accumulate);
+      }
     }
+  }
 }
 
-// grid (I / 128 column tiles, d / 128 row tiles, slots)
+// dW_down = dO^T H: rows over d, columns over I.
 template <typename T>
 __global__ __launch_bounds__(G_THREADS) void k_dw_d(LayerPtrs<T> W, const T* __restrict__ dO,
-                                                    const T* __restrict__ H,
-                                                    const int32_t* __restrict__ offsets, int S_r, int Tn,
-                                                    int k, int d, int I, int accumulate) {
+                                                    const T* __restrict__ H, DwArgs da) {
   __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
-  const int s = blockIdx.z;
-  float* dwd = W.dwd[s];
-  if (!dwd) return;
-  const SlotRows sr = slot_rows(s, 0, offsets, S_r, Tn, k);
-  const int n0 = blockIdx.x * G_BN, m0 = blockIdx.y * G_BM;
-  // A(m = hidden index, k = row) = dO[row][m];  B(n = intermediate index, k = row) = H[row][n]
-  Opnd<T> A[1] = {{dO + (size_t)sr.orow0 * d + m0, d, d - m0, sr.nrows}};
-  Opnd<T> B[1] = {{H + (size_t)sr.orow0 * I + n0, I, I - n0, sr.nrows}};
-  Acc<T, 1, 1> acc;
-  acc.zero();
-  run_gemm<T, false, false, 1, 1>(A, B, sr.nrows, lds, acc);
+  const int d = da.d, I = da.I;
+  const int MT = (d + G_BM - 1) / G_BM, NT = (I + G_BN - 1) / G_BN;
+  const TileRange tr = dw_range(da, MT * NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = dw_tile(t, MT * NT, MT);
+    float* dwd = W.dwd[rt.s];
+    if (dwd) {
+      const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
+      const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
+      // A(m = hidden index, k = row) = dO[row][m];  B(n = intermediate index, k = row) = H[row][n]
+      Opnd<T> A[1] = {{dO + (size_t)sr.orow0 * d + m0, d, d - m0, sr.nrows}};
+      Opnd<T> B[1] = {{H + (size_t)sr.orow0 * I + n0, I, I - n0, sr.nrows}};
+      Acc<T, 1, 1> acc;
+      acc.zero();
+      run_gemm<T, false, false, 1, 1>(A, B, sr.nrows, lds, acc);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const AccCoord c = acc_coord(i, j);
-      const int m = m0 + c.row, n = n0 + c.col4;
-      if (m >= d || n >= I) continue;
-      store_dw(dwd + (size_t)m * I + n, acc.v[0][i][j], accumulate);
+      for (int q = 0; q < 16; ++q) {
+        const AccCoord c = quad_coord<T>(q);
+        const int m = m0 + c.row, n = n0 + c.col4;
+        if (m >= d || n >= I) continue;
+        store_dw(dwd + (size_t)m * I + n, acc.quad(0, q), da.accumulate);
+      }
     }
+  }
 }
 
 // ------------------------------------------------------------------ host ----
@@ -300,7 +420,7 @@ int check_layer_ffn(const moe_layer* L) {
   if (L->d % 8 || L->I % 8)
     return fail(MOE_ERR_UNSUPPORTED, "layer d=%d I=%d must be multiples of 8", L->d, L->I);
   if (L->S_routed < 0 || L->S_shared < 0 || L->S_routed + L->S_shared < 1 || L->S_routed > 512 ||
-      L->S_shared > 512)
+      L->S_shared > 511)
     return fail(MOE_ERR_ARG, "layer S_routed=%d S_shared=%d", L->S_routed, L->S_shared);
   FM_TRY(need_dtype_float(L->dtype, "layer dtype"));
   FM_TRY(need(L->w_gate, "layer w_gate")); FM_TRY(need(L->w_up, "layer w_up"));
@@ -308,15 +428,19 @@ int check_layer_ffn(const moe_layer* L) {
   return MOE_OK;
 }
 
-size_t max_tiles(const moe_layer* L, int T, int k) {
-  return (size_t)cdiv((long)T * k, G_BM) + L->S_routed + (size_t)L->S_shared * cdiv(T, G_BM);
-}
-
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
-
-size_t tiles_bytes(const moe_layer* L, int T, int k) { return align256((max_tiles(L, T, k) + 1) * sizeof(int2)); }
-
 size_t rows_total(const moe_layer* L, int T, int k) { return (size_t)T * (k + L->S_shared); }
+int n_slots(const moe_layer* L) { return L->S_routed + L->S_shared; }
+
+// Persistent grid: one block per compute unit, a multiple of the XCD count.
+int persistent_blocks() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  n = (n / N_XCD) * N_XCD;
+  return n < N_XCD ? N_XCD : n;
+}
 
 }  // namespace
 }  // namespace fm
@@ -325,13 +449,13 @@ using namespace fm;
 
 extern "C" size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int T, int k) {
   if (!L || T < 0 || k <= 0) return 0;
-  return tiles_bytes(L, T, k);
+  return sched_bytes(n_slots(L));
 }
 
 extern "C" size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k) {
   if (!L || T < 0 || k <= 0) return 0;
   const size_t act = align256(rows_total(L, T, k) * L->I * esize(L->dtype));
-  return tiles_bytes(L, T, k) + 2 * act;
+  return sched_bytes(n_slots(L)) + 2 * act;
 }
 
 extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const void* X_perm,
@@ -350,19 +474,17 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
   if (ws_bytes < moe_grouped_swiglu_fwd_workspace_size(L, T, k))
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_fwd_workspace_size(L, T, k));
-  const size_t mt = max_tiles(L, T, k);
-  if (mt > 65535) return fail(MOE_ERR_UNSUPPORTED, "too many row tiles (%zu)", mt);
   hipStream_t st = as_stream(stream);
-  int2* tiles = (int2*)ws;
-  hipLaunchKernelGGL(k_build_tiles, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
-                     G_BM, tiles);
-  const int d = L->d, I = L->I;
-#define FM_FWD(TT)                                                                                   \
-  hipLaunchKernelGGL(k_gate_up<TT>, dim3(cdiv(I, G_BN), mt), dim3(G_THREADS), 0, st,               \
-                     layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, offsets, tiles, L->S_routed, \
-                     T, k, d, I, (TT*)A_g, (TT*)A_u, (TT*)H);                                       \
-  hipLaunchKernelGGL(k_down<TT>, dim3(cdiv(d, G_BN), mt), dim3(G_THREADS), 0, st, layer_ptrs<TT>(L), \
-                     (const TT*)H, offsets, tiles, L->S_routed, T, k, d, I, (TT*)O);
+  const int S = n_slots(L);
+  const Sched sc = sched_at(ws, S);
+  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
+                     (float* const*)nullptr, 0, sc.mbase, sc.wbase);
+  const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
+  const dim3 grid(persistent_blocks()), block(G_THREADS);
+#define FM_FWD(TT)                                                                                      \
+  hipLaunchKernelGGL(k_gate_up<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, \
+                     ra, (TT*)A_g, (TT*)A_u, (TT*)H);                                                   \
+  hipLaunchKernelGGL(k_down<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)H, ra, (TT*)O);
   if (L->dtype == MOE_BF16) { FM_FWD(bf16) } else { FM_FWD(float) }
 #undef FM_FWD
   return check_launch("moe_grouped_swiglu_fwd");
@@ -388,31 +510,30 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   if (ws_bytes < moe_grouped_swiglu_bwd_workspace_size(L, T, k))
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_bwd_workspace_size(L, T, k));
-  const size_t mt = max_tiles(L, T, k);
-  if (mt > 65535) return fail(MOE_ERR_UNSUPPORTED, "too many row tiles (%zu)", mt);
   hipStream_t st = as_stream(stream);
-  int2* tiles = (int2*)ws;
+  const int S = n_slots(L);
+  const Sched sc = sched_at(ws, S);
   const size_t act = align256(rows_total(L, T, k) * L->I * esize(L->dtype));
-  char* dAg = (char*)ws + tiles_bytes(L, T, k);
+  char* dAg = (char*)ws + sched_bytes(S);
   char* dAu = dAg + act;
-  const int d = L->d, I = L->I, S = L->S_routed + L->S_shared;
-  hipLaunchKernelGGL(k_build_tiles, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
-                     G_BM, tiles);
-#define FM_BWD(TT)                                                                                   \
-  if (T > 0) {                                                                                       \
-    hipLaunchKernelGGL(k_dh<TT>, dim3(cdiv(I, G_BN), mt), dim3(G_THREADS), 0, st, layer_ptrs<TT>(L), \
-                       (const TT*)dO, (const TT*)A_g, (const TT*)A_u, offsets, tiles, L->S_routed, T, \
-                       k, d, I, (TT*)dAg, (TT*)dAu);                                                \
-    hipLaunchKernelGGL(k_dx<TT>, dim3(cdiv(d, G_BN), mt), dim3(G_THREADS), 0, st, layer_ptrs<TT>(L), \
-                       (const TT*)dAg, (const TT*)dAu, offsets, tiles, L->S_routed, T, k, d, I,     \
-                       (TT*)dX_perm);                                                               \
-  }                                                                                                  \
-  hipLaunchKernelGGL(k_dw_gu<TT>, dim3(cdiv(d, G_BN), cdiv(I, G_BM), S), dim3(G_THREADS), 0, st,    \
-                     layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, (const TT*)dAg,            \
-                     (const TT*)dAu, offsets, L->S_routed, T, k, d, I, accumulate_dw);               \
-  hipLaunchKernelGGL(k_dw_d<TT>, dim3(cdiv(I, G_BN), cdiv(d, G_BM), S), dim3(G_THREADS), 0, st,     \
-                     layer_ptrs<TT>(L), (const TT*)dO, (const TT*)H, offsets, L->S_routed, T, k, d, \
-                     I, accumulate_dw);
+  const int d = L->d, I = L->I;
+  // both weight-gradient kernels have cdiv(I,128) * cdiv(d,128) tiles per slot
+  const int wtiles = cdiv(I, G_BM) * cdiv(d, G_BN);
+  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
+                     L->dw_gate, wtiles, sc.mbase, sc.wbase);
+  const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, d, I};
+  const DwArgs da{offsets, sc.wbase, L->S_routed, S, T, k, d, I, accumulate_dw};
+  const dim3 grid(persistent_blocks()), block(G_THREADS);
+#define FM_BWD(TT)                                                                                        \
+  if (T > 0) {                                                                                            \
+    hipLaunchKernelGGL(k_dh<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)A_g,    \
+                       (const TT*)A_u, ra, (TT*)dAg, (TT*)dAu);                                          \
+    hipLaunchKernelGGL(k_dx<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dAg, (const TT*)dAu,  \
+                       ra, (TT*)dX_perm);                                                                \
+  }                                                                                                       \
+  hipLaunchKernelGGL(k_dw_gu<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, \
+                     (const TT*)dAg, (const TT*)dAu, da);                                                \
+  hipLaunchKernelGGL(k_dw_d<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)H, da);
   if (L->dtype == MOE_BF16) { FM_BWD(bf16) } else { FM_BWD(float) }
 #undef FM_BWD
   return check_launch("moe_grouped_swiglu_bwd");

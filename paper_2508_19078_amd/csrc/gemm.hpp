@@ -112,7 +112,8 @@ template <typename T, bool KC> struct Stager {
   }
 };
 
-// acc[a * NB + b][i][j]: wave sub-tile (i, j) of operand pair (a, b).
+// acc[a * NB + b][i][j]: wave sub-tile (i, j) of operand pair (a, b), 16 x 16
+// MFMA tiles (the fp32 core).  The bf16 core specialises this with 32 x 32 tiles.
 template <typename T, int NA, int NB> struct Acc {
   f32x4_t v[NA * NB][4][4];
   __device__ __forceinline__ void zero() {
@@ -123,6 +124,7 @@ template <typename T, int NA, int NB> struct Acc {
 #pragma unroll
         for (int j = 0; j < 4; ++j) v[x][i][j] = f32x4_t{0, 0, 0, 0};
   }
+  __device__ __forceinline__ f32x4_t quad(int x, int g) const { return v[x][g >> 2][g & 3]; }
 };
 
 // Multiplies the staged slab in `lds` (operand tiles A0..A{NA-1}, B0..B{NB-1}).
@@ -198,6 +200,12 @@ __device__ __forceinline__ void gemm_mainloop(const Opnd<T> (&A)[NA], const Opnd
   }
 }
 
+// Epilogues walk an accumulator as 16 "quads": four consecutive output columns
+// of one row.  quad_coord<T>(g) gives the row and first column of quad g within
+// the 128 x 128 block tile; acc.quad(x, g) the four values of operand pair x.
+struct AccCoord;
+template <typename T> __device__ __forceinline__ AccCoord quad_coord(int g);
+
 // Output coordinates of accumulator element r of wave sub-tile (i, j):
 // row = wm*64 + i*16 + (lane & 15), columns col4 .. col4+3 with
 // col4 = wn*64 + j*16 + 4*(lane >> 4).
@@ -208,6 +216,7 @@ __device__ __forceinline__ AccCoord acc_coord(int i, int j) {
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   return AccCoord{(wave & 1) * 64 + i * 16 + (lane & 15), (wave >> 1) * 64 + j * 16 + 4 * (lane >> 4)};
 }
+template <> __device__ __forceinline__ AccCoord quad_coord<float>(int g) { return acc_coord(g >> 2, g & 3); }
 
 // 4 consecutive values <-> global memory of T.
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
