@@ -66,11 +66,11 @@ inline Sched sched_at(void* ws, int S) {
   return s;
 }
 
-// One block of 1024 threads (S <= 1024).  wtiles = weight-gradient tiles per
-// slot; a tuning slot's work per tile is its K slabs + 1 (so an empty tuning
-// slot still gets its zeros written); frozen slots have none.
+// One block of 1024 threads (S <= 1024).  The weight-gradient work of a tile
+// of a tuning slot is its K slabs + 1 (so an empty tuning slot still gets its
+// zeros written); frozen slots have none.
 __global__ __launch_bounds__(1024) void k_build_sched(const int32_t* __restrict__ offsets, int S_r, int S_sh,
-                                                      int Tn, float* const* __restrict__ dw_tab, int wtiles,
+                                                      int Tn, float* const* __restrict__ dw_tab,
                                                       int32_t* __restrict__ mbase, long long* __restrict__ wbase) {
   __shared__ int sm[1024];
   __shared__ long long sw[1024];
@@ -78,7 +78,7 @@ __global__ __launch_bounds__(1024) void k_build_sched(const int32_t* __restrict_
   int n = 0;
   if (s < S) n = s < S_r ? offsets[s + 1] - offsets[s] : Tn;
   long long w = 0;
-  if (s < S && dw_tab && dw_tab[s]) w = (long long)wtiles * ((n + B16_BK - 1) / B16_BK + 1);
+  if (s < S && dw_tab && dw_tab[s]) w = (n + B16_BK - 1) / B16_BK + 1;
   sm[s] = (n + G_BM - 1) / G_BM;
   sw[s] = w;
   __syncthreads();
@@ -144,13 +144,14 @@ __device__ __forceinline__ Tile dw_tile(long long t, int tps, int MT) {
   return r;
 }
 
-// First weight-gradient tile whose cumulative work reaches `target`.
+// First weight-gradient tile whose cumulative work reaches `target`; wbase
+// holds the per-tile work prefix over slots, tps tiles per slot.
 __device__ __forceinline__ long long tile_at_work(const long long* wbase, int S, int tps, long long target) {
-  if (target >= wbase[S]) return (long long)S * tps;
-  const int s = find_slot(wbase, S, target);
-  const long long per = (wbase[s + 1] - wbase[s]) / tps;   // work per tile of slot s
+  if (target >= wbase[S] * tps) return (long long)S * tps;
+  const int s = find_slot(wbase, S, target / tps);
+  const long long per = wbase[s + 1] - wbase[s];
   if (per == 0) return (long long)(s + 1) * tps;
-  long long i = (target - wbase[s] + per - 1) / per;
+  long long i = (target - wbase[s] * tps + per - 1) / per;
   if (i > tps) i = tps;
   return (long long)s * tps + i;
 }
@@ -196,21 +197,21 @@ __device__ __forceinline__ TileRange row_range(const RowArgs& ra, int NT) {
                    (int)(gridDim.x / N_XCD)};
 }
 __device__ __forceinline__ TileRange dw_range(const DwArgs& da, int tps) {
-  const long long w = da.wbase[da.S];
+  const long long w = da.wbase[da.S] * tps;
   const int x = blockIdx.x % N_XCD;
   return TileRange{tile_at_work(da.wbase, da.S, tps, w * x / N_XCD),
                    tile_at_work(da.wbase, da.S, tps, w * (x + 1) / N_XCD), (int)(blockIdx.x / N_XCD),
                    (int)(gridDim.x / N_XCD)};
 }
 
-// ------------------------------------------------------------- forward ----
+// ------------------------------------------- fp32 kernels (16x16 core) ----
 
 template <typename T>
-__global__ __launch_bounds__(G_THREADS) void k_gate_up(LayerPtrs<T> W, const T* __restrict__ X,
+__global__ __launch_bounds__(G_THREADS) void kf_gate_up(LayerPtrs<T> W, const T* __restrict__ X,
                                                        const T* __restrict__ Xp, RowArgs ra,
                                                        T* __restrict__ Ag, T* __restrict__ Au,
                                                        T* __restrict__ H) {
-  __shared__ __align__(16) char lds[LdsBytes<T, 1, 2>::value];
+  __shared__ __align__(16) char lds[2 * (1 + 2) * GemmCfg<T>::TILE * (int)sizeof(T)];
   const int d = ra.d, I = ra.I, NT = (I + G_BN - 1) / G_BN;
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
@@ -222,7 +223,7 @@ __global__ __launch_bounds__(G_THREADS) void k_gate_up(LayerPtrs<T> W, const T* 
     Opnd<T> B[2] = {{W.wg[rt.s] + (size_t)n0 * d, d, I - n0, d}, {W.wu[rt.s] + (size_t)n0 * d, d, I - n0, d}};
     Acc<T, 1, 2> acc;
     acc.zero();
-    run_gemm<T, true, true, 1, 2>(A, B, d, lds, acc);
+    gemm_mainloop<T, true, true, 1, 2>(A, B, d, (T*)lds, acc);
     const size_t ob = (size_t)(sr.orow0 + m0);
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
@@ -242,9 +243,9 @@ __global__ __launch_bounds__(G_THREADS) void k_gate_up(LayerPtrs<T> W, const T* 
 }
 
 template <typename T>
-__global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __restrict__ H, RowArgs ra,
+__global__ __launch_bounds__(G_THREADS) void kf_down(LayerPtrs<T> W, const T* __restrict__ H, RowArgs ra,
                                                     T* __restrict__ O) {
-  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
+  __shared__ __align__(16) char lds[2 * (1 + 1) * GemmCfg<T>::TILE * (int)sizeof(T)];
   const int d = ra.d, I = ra.I, NT = (d + G_BN - 1) / G_BN;
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
@@ -256,7 +257,7 @@ __global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __r
     Opnd<T> B[1] = {{W.wd[rt.s] + (size_t)n0 * I, I, d - n0, I}};
     Acc<T, 1, 1> acc;
     acc.zero();
-    run_gemm<T, true, true, 1, 1>(A, B, I, lds, acc);
+    gemm_mainloop<T, true, true, 1, 1>(A, B, I, (T*)lds, acc);
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const AccCoord c = quad_coord<T>(q);
@@ -270,10 +271,10 @@ __global__ __launch_bounds__(G_THREADS) void k_down(LayerPtrs<T> W, const T* __r
 // ------------------------------------------------------------ backward ----
 
 template <typename T>
-__global__ __launch_bounds__(G_THREADS) void k_dh(LayerPtrs<T> W, const T* __restrict__ dO,
+__global__ __launch_bounds__(G_THREADS) void kf_dh(LayerPtrs<T> W, const T* __restrict__ dO,
                                                   const T* __restrict__ Ag, const T* __restrict__ Au,
                                                   RowArgs ra, T* __restrict__ dAg, T* __restrict__ dAu) {
-  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
+  __shared__ __align__(16) char lds[2 * (1 + 1) * GemmCfg<T>::TILE * (int)sizeof(T)];
   const int d = ra.d, I = ra.I, NT = (I + G_BN - 1) / G_BN;
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
@@ -286,7 +287,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dh(LayerPtrs<T> W, const T* __res
     Opnd<T> B[1] = {{W.wd[rt.s] + n0, I, I - n0, d}};
     Acc<T, 1, 1> acc;
     acc.zero();
-    run_gemm<T, true, false, 1, 1>(A, B, d, lds, acc);
+    gemm_mainloop<T, true, false, 1, 1>(A, B, d, (T*)lds, acc);
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const AccCoord c = quad_coord<T>(q);
@@ -308,10 +309,10 @@ __global__ __launch_bounds__(G_THREADS) void k_dh(LayerPtrs<T> W, const T* __res
 }
 
 template <typename T>
-__global__ __launch_bounds__(G_THREADS) void k_dx(LayerPtrs<T> W, const T* __restrict__ dAg,
+__global__ __launch_bounds__(G_THREADS) void kf_dx(LayerPtrs<T> W, const T* __restrict__ dAg,
                                                   const T* __restrict__ dAu, RowArgs ra,
                                                   T* __restrict__ dXp) {
-  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
+  __shared__ __align__(16) char lds[2 * (1 + 1) * GemmCfg<T>::TILE * (int)sizeof(T)];
   const int d = ra.d, I = ra.I, NT = (d + G_BN - 1) / G_BN;
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
@@ -324,12 +325,12 @@ __global__ __launch_bounds__(G_THREADS) void k_dx(LayerPtrs<T> W, const T* __res
     {  // B(n = hidden index, k = intermediate index) = W_gate[k][n]
       Opnd<T> A[1] = {{dAg + ob * I, I, sr.nrows - m0, I}};
       Opnd<T> B[1] = {{W.wg[rt.s] + n0, d, d - n0, I}};
-      run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
+      gemm_mainloop<T, true, false, 1, 1>(A, B, I, (T*)lds, acc);
     }
     {
       Opnd<T> A[1] = {{dAu + ob * I, I, sr.nrows - m0, I}};
       Opnd<T> B[1] = {{W.wu[rt.s] + n0, d, d - n0, I}};
-      run_gemm<T, true, false, 1, 1>(A, B, I, lds, acc);
+      gemm_mainloop<T, true, false, 1, 1>(A, B, I, (T*)lds, acc);
     }
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
@@ -348,10 +349,10 @@ __device__ __forceinline__ void store_dw(float* p, f32x4_t v, bool accumulate) {
 
 // dW_gate = dA_g^T X_s, dW_up = dA_u^T X_s: rows over I, columns over d.
 template <typename T>
-__global__ __launch_bounds__(G_THREADS) void k_dw_gu(LayerPtrs<T> W, const T* __restrict__ X,
+__global__ __launch_bounds__(G_THREADS) void kf_dw_gu(LayerPtrs<T> W, const T* __restrict__ X,
                                                      const T* __restrict__ Xp, const T* __restrict__ dAg,
                                                      const T* __restrict__ dAu, DwArgs da) {
-  __shared__ __align__(16) char lds[LdsBytes<T, 2, 1>::value];
+  __shared__ __align__(16) char lds[2 * (2 + 1) * GemmCfg<T>::TILE * (int)sizeof(T)];
   const int d = da.d, I = da.I;
   const int MT = (I + G_BM - 1) / G_BM, NT = (d + G_BN - 1) / G_BN;
   const TileRange tr = dw_range(da, MT * NT);
@@ -368,7 +369,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_gu(LayerPtrs<T> W, const T* __
       Opnd<T> B[1] = {{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, d, d - n0, sr.nrows}};
       Acc<T, 2, 1> acc;
       acc.zero();
-      run_gemm<T, false, false, 2, 1>(A, B, sr.nrows, lds, acc);
+      gemm_mainloop<T, false, false, 2, 1>(A, B, sr.nrows, (T*)lds, acc);
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const AccCoord c = quad_coord<T>(q);
@@ -383,9 +384,9 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_gu(LayerPtrs<T> W, const T* __
 
 // dW_down = dO^T H: rows over d, columns over I.
 template <typename T>
-__global__ __launch_bounds__(G_THREADS) void k_dw_d(LayerPtrs<T> W, const T* __restrict__ dO,
+__global__ __launch_bounds__(G_THREADS) void kf_dw_d(LayerPtrs<T> W, const T* __restrict__ dO,
                                                     const T* __restrict__ H, DwArgs da) {
-  __shared__ __align__(16) char lds[LdsBytes<T, 1, 1>::value];
+  __shared__ __align__(16) char lds[2 * (1 + 1) * GemmCfg<T>::TILE * (int)sizeof(T)];
   const int d = da.d, I = da.I;
   const int MT = (d + G_BM - 1) / G_BM, NT = (I + G_BN - 1) / G_BN;
   const TileRange tr = dw_range(da, MT * NT);
@@ -400,7 +401,7 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_d(LayerPtrs<T> W, const T* __r
       Opnd<T> B[1] = {{H + (size_t)sr.orow0 * I + n0, I, I - n0, sr.nrows}};
       Acc<T, 1, 1> acc;
       acc.zero();
-      run_gemm<T, false, false, 1, 1>(A, B, sr.nrows, lds, acc);
+      gemm_mainloop<T, false, false, 1, 1>(A, B, sr.nrows, (T*)lds, acc);
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const AccCoord c = quad_coord<T>(q);
@@ -408,6 +409,196 @@ __global__ __launch_bounds__(G_THREADS) void k_dw_d(LayerPtrs<T> W, const T* __r
         if (m >= d || n >= I) continue;
         store_dw(dwd + (size_t)m * I + n, acc.quad(0, q), da.accumulate);
       }
+    }
+  }
+}
+
+// ------------------------------------------ bf16 kernels (8-wave core) ----
+
+typedef const bf16* cbp;
+
+// [A_g | A_u] = X_s [W_gate | W_up]^T, H = silu(A_g) A_u.  The B tile
+// interleaves 32-row blocks of W_gate and W_up (128 intermediate columns per
+// 256-row tile), so each wave holds gate and up of the same columns.
+__global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp X, cbp Xp, RowArgs ra,
+                                                          bf16* Ag, bf16* Au, bf16* H) {
+  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
+  const int d = ra.d, I = ra.I, NT = (I + 127) / 128;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * 128, n0 = rt.n * 128;
+    const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, sr.nrows - m0, d};
+    const B16Src B{W.wg[rt.s] + (size_t)n0 * d, W.wu[rt.s] + (size_t)n0 * d, d, I - n0, d};
+    B16Acc acc;
+    acc.zero();
+    b16_gemm<true, true, 128, 256>(A, B, d, (FM_LDS char*)lds, acc);
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    const int wn = wave_id() / 2;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      if ((q >> 2) & 1) continue;                 // j = 1 holds the up half
+      const AccCoord c = b16_quad_coord<128>(q);
+      const int n = n0 + 32 * wn + (c.col4 & 31);
+      if (c.row >= sr.nrows - m0 || n >= I) continue;
+      const f32x4_t ag = acc.quad(q), u = acc.quad(q + 4);
+      f32x4_t h;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm(ag[r]) * u[r];
+      const size_t o = (ob + c.row) * I + n;
+      store4(Ag + o, ag);
+      store4(Au + o, u);
+      store4(H + o, h);
+    }
+  }
+}
+
+// O = H W_down^T
+__global__ __launch_bounds__(B16_THREADS) void kb_down(LayerPtrs<bf16> W, cbp H, RowArgs ra, bf16* O) {
+  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
+  const int d = ra.d, I = ra.I, NT = (d + 255) / 256;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * 128, n0 = rt.n * 256;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    const B16Src A{H + ob * I, nullptr, I, sr.nrows - m0, I};
+    const B16Src B{W.wd[rt.s] + (size_t)n0 * I, nullptr, I, d - n0, I};
+    B16Acc acc;
+    acc.zero();
+    b16_gemm<true, true, 128, 256>(A, B, I, (FM_LDS char*)lds, acc);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = b16_quad_coord<128>(q);
+      const int n = n0 + c.col4;
+      if (c.row >= sr.nrows - m0 || n >= d) continue;
+      store4(O + (ob + c.row) * d + n, acc.quad(q));
+    }
+  }
+}
+
+// dH = dO W_down (B = W_down read k-major), epilogue dA_g, dA_u.
+__global__ __launch_bounds__(B16_THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, cbp Ag, cbp Au, RowArgs ra,
+                                                     bf16* dAg, bf16* dAu) {
+  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
+  const int d = ra.d, I = ra.I, NT = (I + 255) / 256;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * 128, n0 = rt.n * 256;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    // B(n = intermediate index, k = hidden index) = W_down[k][n]
+    const B16Src A{dO + ob * d, nullptr, d, sr.nrows - m0, d};
+    const B16Src B{W.wd[rt.s] + n0, nullptr, I, I - n0, d};
+    B16Acc acc;
+    acc.zero();
+    b16_gemm<true, false, 128, 256>(A, B, d, (FM_LDS char*)lds, acc);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = b16_quad_coord<128>(q);
+      const int n = n0 + c.col4;
+      if (c.row >= sr.nrows - m0 || n >= I) continue;
+      const size_t o = (ob + c.row) * I + n;
+      const f32x4_t dh = acc.quad(q), ag = load4(Ag + o), u = load4(Au + o);
+      f32x4_t dg, du;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float sg = sigm(ag[r]);
+        du[r] = dh[r] * ag[r] * sg;
+        dg[r] = dh[r] * u[r] * sg * (1.0f + ag[r] * (1.0f - sg));
+      }
+      store4(dAg + o, dg);
+      store4(dAu + o, du);
+    }
+  }
+}
+
+// dX_s = dA_g W_gate + dA_u W_up (two K passes, B read k-major).
+__global__ __launch_bounds__(B16_THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg, cbp dAu, RowArgs ra,
+                                                     bf16* dXp) {
+  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
+  const int d = ra.d, I = ra.I, NT = (d + 255) / 256;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * 128, n0 = rt.n * 256;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    B16Acc acc;
+    acc.zero();
+    // B(n = hidden index, k = intermediate index) = W_gate[k][n], then W_up
+    b16_gemm<true, false, 128, 256>(B16Src{dAg + ob * I, nullptr, I, sr.nrows - m0, I},
+                                    B16Src{W.wg[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
+    b16_gemm<true, false, 128, 256>(B16Src{dAu + ob * I, nullptr, I, sr.nrows - m0, I},
+                                    B16Src{W.wu[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = b16_quad_coord<128>(q);
+      const int n = n0 + c.col4;
+      if (c.row >= sr.nrows - m0 || n >= d) continue;
+      store4(dXp + (ob + c.row) * d + n, acc.quad(q));
+    }
+  }
+}
+
+// dW_gate = dA_g^T X_s and dW_up = dA_u^T X_s in one product: the A tile
+// interleaves 32-column blocks of dA_g and dA_u (128 intermediate rows of both
+// per 256-row tile), B = X_s; both read k-major.
+__global__ __launch_bounds__(B16_THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X, cbp Xp, cbp dAg, cbp dAu,
+                                                        DwArgs da) {
+  __shared__ __align__(16) char lds[B16Lds<256, 128>::value];
+  const int d = da.d, I = da.I;
+  const int MT = (I + 127) / 128, NT = (d + 127) / 128;
+  const TileRange tr = dw_range(da, MT * NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = dw_tile(t, MT * NT, MT);
+    float* dwg = W.dwg[rt.s];
+    float* dwu = W.dwu[rt.s];
+    if (!dwg || !dwu) continue;
+    const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
+    const int m0 = rt.m * 128, n0 = rt.n * 128;
+    const B16Src A{dAg + (size_t)sr.orow0 * I + m0, dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows};
+    const B16Src B{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, nullptr, d, d - n0, sr.nrows};
+    B16Acc acc;
+    acc.zero();
+    b16_gemm<false, false, 256, 128>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = b16_quad_coord<256>(q);
+      const int m = m0 + 32 * (c.row >> 6) + (c.row & 31), n = n0 + c.col4;
+      if (m >= I || n >= d) continue;
+      float* dst = ((c.row >> 5) & 1) ? dwu : dwg;
+      store_dw(dst + (size_t)m * d + n, acc.quad(q), da.accumulate);
+    }
+  }
+}
+
+// dW_down = dO^T H (both read k-major).
+__global__ __launch_bounds__(B16_THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO, cbp H, DwArgs da) {
+  __shared__ __align__(16) char lds[B16Lds<256, 128>::value];
+  const int d = da.d, I = da.I;
+  const int MT = (d + 255) / 256, NT = (I + 127) / 128;
+  const TileRange tr = dw_range(da, MT * NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = dw_tile(t, MT * NT, MT);
+    float* dwd = W.dwd[rt.s];
+    if (!dwd) continue;
+    const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
+    const int m0 = rt.m * 256, n0 = rt.n * 128;
+    const B16Src A{dO + (size_t)sr.orow0 * d + m0, nullptr, d, d - m0, sr.nrows};
+    const B16Src B{H + (size_t)sr.orow0 * I + n0, nullptr, I, I - n0, sr.nrows};
+    B16Acc acc;
+    acc.zero();
+    b16_gemm<false, false, 256, 128>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const AccCoord c = b16_quad_coord<256>(q);
+      const int m = m0 + c.row, n = n0 + c.col4;
+      if (m >= d || n >= I) continue;
+      store_dw(dwd + (size_t)m * I + n, acc.quad(q), da.accumulate);
     }
   }
 }
@@ -478,14 +669,21 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
   const int S = n_slots(L);
   const Sched sc = sched_at(ws, S);
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
-                     (float* const*)nullptr, 0, sc.mbase, sc.wbase);
+                     (float* const*)nullptr, sc.mbase, sc.wbase);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
   const dim3 grid(persistent_blocks()), block(G_THREADS);
 #define FM_FWD(TT)                                                                                      \
-  hipLaunchKernelGGL(k_gate_up<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, \
+  hipLaunchKernelGGL(kf_gate_up<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, \
                      ra, (TT*)A_g, (TT*)A_u, (TT*)H);                                                   \
-  hipLaunchKernelGGL(k_down<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)H, ra, (TT*)O);
-  if (L->dtype == MOE_BF16) { FM_FWD(bf16) } else { FM_FWD(float) }
+  hipLaunchKernelGGL(kf_down<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)H, ra, (TT*)O);
+  if (L->dtype == MOE_BF16) {
+    const dim3 b8(B16_THREADS);
+    hipLaunchKernelGGL(kb_gate_up, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)X, (cbp)X_perm, ra, (bf16*)A_g,
+                       (bf16*)A_u, (bf16*)H);
+    hipLaunchKernelGGL(kb_down, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)H, ra, (bf16*)O);
+  } else {
+    FM_FWD(float)
+  }
 #undef FM_FWD
   return check_launch("moe_grouped_swiglu_fwd");
 }
@@ -517,24 +715,34 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   char* dAg = (char*)ws + sched_bytes(S);
   char* dAu = dAg + act;
   const int d = L->d, I = L->I;
-  // both weight-gradient kernels have cdiv(I,128) * cdiv(d,128) tiles per slot
-  const int wtiles = cdiv(I, G_BM) * cdiv(d, G_BN);
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
-                     L->dw_gate, wtiles, sc.mbase, sc.wbase);
+                     L->dw_gate, sc.mbase, sc.wbase);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, d, I};
   const DwArgs da{offsets, sc.wbase, L->S_routed, S, T, k, d, I, accumulate_dw};
   const dim3 grid(persistent_blocks()), block(G_THREADS);
 #define FM_BWD(TT)                                                                                        \
   if (T > 0) {                                                                                            \
-    hipLaunchKernelGGL(k_dh<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)A_g,    \
+    hipLaunchKernelGGL(kf_dh<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)A_g,   \
                        (const TT*)A_u, ra, (TT*)dAg, (TT*)dAu);                                          \
-    hipLaunchKernelGGL(k_dx<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dAg, (const TT*)dAu,  \
+    hipLaunchKernelGGL(kf_dx<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dAg, (const TT*)dAu, \
                        ra, (TT*)dX_perm);                                                                \
   }                                                                                                       \
-  hipLaunchKernelGGL(k_dw_gu<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, \
+  hipLaunchKernelGGL(kf_dw_gu<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)X, (const TT*)X_perm, \
                      (const TT*)dAg, (const TT*)dAu, da);                                                \
-  hipLaunchKernelGGL(k_dw_d<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)H, da);
-  if (L->dtype == MOE_BF16) { FM_BWD(bf16) } else { FM_BWD(float) }
+  hipLaunchKernelGGL(kf_dw_d<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)H, da);
+  if (L->dtype == MOE_BF16) {
+    const dim3 b8(B16_THREADS);
+    if (T > 0) {
+      hipLaunchKernelGGL(kb_dh, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)A_g, (cbp)A_u, ra,
+                         (bf16*)dAg, (bf16*)dAu);
+      hipLaunchKernelGGL(kb_dx, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dAg, (cbp)dAu, ra, (bf16*)dX_perm);
+    }
+    hipLaunchKernelGGL(kb_dw_gu, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)X, (cbp)X_perm, (cbp)dAg,
+                       (cbp)dAu, da);
+    hipLaunchKernelGGL(kb_dw_d, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)H, da);
+  } else {
+    FM_BWD(float)
+  }
 #undef FM_BWD
   return check_launch("moe_grouped_swiglu_bwd");
 }
