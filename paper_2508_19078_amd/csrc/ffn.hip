@@ -12,7 +12,7 @@
 //           dw_d    : dW_down = dO^T H                          (tuning slots)
 //
 // Scheduling.  A one-block kernel turns the offsets into a schedule: prefix
-// sums of each slot's 128-row tiles and, for the weight gradients, of each
+// sums of each slot's row tiles and, for the weight gradients, of each
 // tuning slot's work (its K slabs).  The GEMM kernels are persistent, one block
 // per compute unit.  Blocks are dispatched to the 8 XCDs round-robin, so block
 // b runs on XCD b % 8; each XCD walks its own contiguous range of the tile
@@ -51,7 +51,7 @@ __device__ __forceinline__ SlotRows slot_rows(int s, const int32_t* offsets, int
   return r;
 }
 
-// Schedule in the workspace: mbase[0..S] (prefix of 128-row tiles per slot)
+// Schedule in the workspace: mbase[0..S] (prefix of row tiles per slot)
 // and wbase[0..S] (prefix of weight-gradient work per slot, 64-bit).
 struct Sched {
   int32_t* mbase;
@@ -67,10 +67,11 @@ inline Sched sched_at(void* ws, int S) {
 }
 
 // One block of 1024 threads (S <= 1024).  The weight-gradient work of a tile
-// of a tuning slot is its K slabs + 1 (so an empty tuning slot still gets its
-// zeros written); frozen slots have none.
+// of a tuning slot is its number of 64-row K slabs + 1 (so an empty tuning slot
+// still gets its zeros written); frozen slots have none.
+constexpr int DW_SLAB = 64;
 __global__ __launch_bounds__(1024) void k_build_sched(const int32_t* __restrict__ offsets, int S_r, int S_sh,
-                                                      int Tn, float* const* __restrict__ dw_tab,
+                                                      int Tn, int tile_rows, float* const* __restrict__ dw_tab,
                                                       int32_t* __restrict__ mbase, long long* __restrict__ wbase) {
   __shared__ int sm[1024];
   __shared__ long long sw[1024];
@@ -78,8 +79,8 @@ __global__ __launch_bounds__(1024) void k_build_sched(const int32_t* __restrict_
   int n = 0;
   if (s < S) n = s < S_r ? offsets[s + 1] - offsets[s] : Tn;
   long long w = 0;
-  if (s < S && dw_tab && dw_tab[s]) w = (n + B16_BK - 1) / B16_BK + 1;
-  sm[s] = (n + G_BM - 1) / G_BM;
+  if (s < S && dw_tab && dw_tab[s]) w = (n + DW_SLAB - 1) / DW_SLAB + 1;
+  sm[s] = (n + tile_rows - 1) / tile_rows;
   sw[s] = w;
   __syncthreads();
   for (int off = 1; off < 1024; off <<= 1) {   // inclusive Hillis-Steele scans
@@ -417,130 +418,154 @@ __global__ __launch_bounds__(G_THREADS) void kf_dw_d(LayerPtrs<T> W, const T* __
 
 typedef const bf16* cbp;
 
+// Block tile of every bf16 product: 256 x 256, waves 2 x 4 (128 x 64 each),
+// 32-deep slabs, four in the LDS ring (128 KB).
+using CB = B16Cfg<256, 256, 2, 32, 4>;
+constexpr int B16_ROWS = CB::RA;   // rows per row tile of the bf16 kernels
+
+// Physical index of logical row / column c of an operand that interleaves two
+// matrices in 32-blocks (the matrix is (c >> 5) & 1).
+__device__ __forceinline__ int deinter(int c) { return 32 * (c >> 6) + (c & 31); }
+
 // [A_g | A_u] = X_s [W_gate | W_up]^T, H = silu(A_g) A_u.  The B tile
 // interleaves 32-row blocks of W_gate and W_up (128 intermediate columns per
-// 256-row tile), so each wave holds gate and up of the same columns.
+// 256-row tile): tile j = 2jj of a wave holds gate and j = 2jj + 1 up of the
+// same columns.
 __global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp X, cbp Xp, RowArgs ra,
                                                           bf16* Ag, bf16* Au, bf16* H) {
-  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
-  const int d = ra.d, I = ra.I, NT = (I + 127) / 128;
+  __shared__ __align__(16) char lds[CB::LDS];
+  const int d = ra.d, I = ra.I, NT = (I + CB::RB / 2 - 1) / (CB::RB / 2);
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
     const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * 128, n0 = rt.n * 128;
+    const int m0 = rt.m * CB::RA, n0 = rt.n * (CB::RB / 2);
     const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, sr.nrows - m0, d};
     const B16Src B{W.wg[rt.s] + (size_t)n0 * d, W.wu[rt.s] + (size_t)n0 * d, d, I - n0, d};
-    B16Acc acc;
+    B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
-    b16_gemm<true, true, 128, 256>(A, B, d, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, true, true>(A, B, d, (FM_LDS char*)lds, acc);
     const size_t ob = (size_t)(sr.orow0 + m0);
-    const int wn = wave_id() / 2;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      if ((q >> 2) & 1) continue;                 // j = 1 holds the up half
-      const AccCoord c = b16_quad_coord<128>(q);
-      const int n = n0 + 32 * wn + (c.col4 & 31);
-      if (c.row >= sr.nrows - m0 || n >= I) continue;
-      const f32x4_t ag = acc.quad(q), u = acc.quad(q + 4);
-      f32x4_t h;
+    for (int i = 0; i < CB::MI; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm(ag[r]) * u[r];
-      const size_t o = (ob + c.row) * I + n;
-      store4(Ag + o, ag);
-      store4(Au + o, u);
-      store4(H + o, h);
-    }
+      for (int jj = 0; jj < CB::NJ / 2; ++jj)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<CB>(i, 2 * jj, q);
+          const int n = n0 + deinter(c.col4);
+          if (c.row >= sr.nrows - m0 || n >= I) continue;
+          const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
+          f32x4_t h;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm(ag[r]) * u[r];
+          const size_t o = (ob + c.row) * I + n;
+          store4(Ag + o, ag);
+          store4(Au + o, u);
+          store4(H + o, h);
+        }
   }
 }
 
 // O = H W_down^T
 __global__ __launch_bounds__(B16_THREADS) void kb_down(LayerPtrs<bf16> W, cbp H, RowArgs ra, bf16* O) {
-  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
-  const int d = ra.d, I = ra.I, NT = (d + 255) / 256;
+  __shared__ __align__(16) char lds[CB::LDS];
+  const int d = ra.d, I = ra.I, NT = (d + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
     const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * 128, n0 = rt.n * 256;
+    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
     const size_t ob = (size_t)(sr.orow0 + m0);
     const B16Src A{H + ob * I, nullptr, I, sr.nrows - m0, I};
     const B16Src B{W.wd[rt.s] + (size_t)n0 * I, nullptr, I, d - n0, I};
-    B16Acc acc;
+    B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
-    b16_gemm<true, true, 128, 256>(A, B, I, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, true, true>(A, B, I, (FM_LDS char*)lds, acc);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const AccCoord c = b16_quad_coord<128>(q);
-      const int n = n0 + c.col4;
-      if (c.row >= sr.nrows - m0 || n >= d) continue;
-      store4(O + (ob + c.row) * d + n, acc.quad(q));
-    }
+    for (int i = 0; i < CB::MI; ++i)
+#pragma unroll
+      for (int j = 0; j < CB::NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<CB>(i, j, q);
+          const int n = n0 + c.col4;
+          if (c.row >= sr.nrows - m0 || n >= d) continue;
+          store4(O + (ob + c.row) * d + n, acc.quad(i, j, q));
+        }
   }
 }
 
 // dH = dO W_down (B = W_down read k-major), epilogue dA_g, dA_u.
 __global__ __launch_bounds__(B16_THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, cbp Ag, cbp Au, RowArgs ra,
                                                      bf16* dAg, bf16* dAu) {
-  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
-  const int d = ra.d, I = ra.I, NT = (I + 255) / 256;
+  __shared__ __align__(16) char lds[CB::LDS];
+  const int d = ra.d, I = ra.I, NT = (I + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
     const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * 128, n0 = rt.n * 256;
+    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
     const size_t ob = (size_t)(sr.orow0 + m0);
     // B(n = intermediate index, k = hidden index) = W_down[k][n]
     const B16Src A{dO + ob * d, nullptr, d, sr.nrows - m0, d};
     const B16Src B{W.wd[rt.s] + n0, nullptr, I, I - n0, d};
-    B16Acc acc;
+    B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
-    b16_gemm<true, false, 128, 256>(A, B, d, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, true, false>(A, B, d, (FM_LDS char*)lds, acc);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const AccCoord c = b16_quad_coord<128>(q);
-      const int n = n0 + c.col4;
-      if (c.row >= sr.nrows - m0 || n >= I) continue;
-      const size_t o = (ob + c.row) * I + n;
-      const f32x4_t dh = acc.quad(q), ag = load4(Ag + o), u = load4(Au + o);
-      f32x4_t dg, du;
+    for (int i = 0; i < CB::MI; ++i)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float sg = sigm(ag[r]);
-        du[r] = dh[r] * ag[r] * sg;
-        dg[r] = dh[r] * u[r] * sg * (1.0f + ag[r] * (1.0f - sg));
-      }
-      store4(dAg + o, dg);
-      store4(dAu + o, du);
-    }
+      for (int j = 0; j < CB::NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<CB>(i, j, q);
+          const int n = n0 + c.col4;
+          if (c.row >= sr.nrows - m0 || n >= I) continue;
+          const size_t o = (ob + c.row) * I + n;
+          const f32x4_t dh = acc.quad(i, j, q), ag = load4(Ag + o), u = load4(Au + o);
+          f32x4_t dg, du;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float sg = sigm(ag[r]);
+            du[r] = dh[r] * ag[r] * sg;
+            dg[r] = dh[r] * u[r] * sg * (1.0f + ag[r] * (1.0f - sg));
+          }
+          store4(dAg + o, dg);
+          store4(dAu + o, du);
+        }
   }
 }
 
 // dX_s = dA_g W_gate + dA_u W_up (two K passes, B read k-major).
 __global__ __launch_bounds__(B16_THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg, cbp dAu, RowArgs ra,
                                                      bf16* dXp) {
-  __shared__ __align__(16) char lds[B16Lds<128, 256>::value];
-  const int d = ra.d, I = ra.I, NT = (d + 255) / 256;
+  __shared__ __align__(16) char lds[CB::LDS];
+  const int d = ra.d, I = ra.I, NT = (d + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
     const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * 128, n0 = rt.n * 256;
+    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
     const size_t ob = (size_t)(sr.orow0 + m0);
-    B16Acc acc;
+    B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
     // B(n = hidden index, k = intermediate index) = W_gate[k][n], then W_up
-    b16_gemm<true, false, 128, 256>(B16Src{dAg + ob * I, nullptr, I, sr.nrows - m0, I},
-                                    B16Src{W.wg[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
-    b16_gemm<true, false, 128, 256>(B16Src{dAu + ob * I, nullptr, I, sr.nrows - m0, I},
-                                    B16Src{W.wu[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, true, false>(B16Src{dAg + ob * I, nullptr, I, sr.nrows - m0, I},
+                              B16Src{W.wg[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, true, false>(B16Src{dAu + ob * I, nullptr, I, sr.nrows - m0, I},
+                              B16Src{W.wu[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const AccCoord c = b16_quad_coord<128>(q);
-      const int n = n0 + c.col4;
-      if (c.row >= sr.nrows - m0 || n >= d) continue;
-      store4(dXp + (ob + c.row) * d + n, acc.quad(q));
-    }
+    for (int i = 0; i < CB::MI; ++i)
+#pragma unroll
+      for (int j = 0; j < CB::NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<CB>(i, j, q);
+          const int n = n0 + c.col4;
+          if (c.row >= sr.nrows - m0 || n >= d) continue;
+          store4(dXp + (ob + c.row) * d + n, acc.quad(i, j, q));
+        }
   }
 }
 
@@ -549,9 +574,9 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg,
 // per 256-row tile), B = X_s; both read k-major.
 __global__ __launch_bounds__(B16_THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X, cbp Xp, cbp dAg, cbp dAu,
                                                         DwArgs da) {
-  __shared__ __align__(16) char lds[B16Lds<256, 128>::value];
+  __shared__ __align__(16) char lds[CB::LDS];
   const int d = da.d, I = da.I;
-  const int MT = (I + 127) / 128, NT = (d + 127) / 128;
+  const int MT = (I + CB::RA / 2 - 1) / (CB::RA / 2), NT = (d + CB::RB - 1) / CB::RB;
   const TileRange tr = dw_range(da, MT * NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = dw_tile(t, MT * NT, MT);
@@ -559,47 +584,55 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X
     float* dwu = W.dwu[rt.s];
     if (!dwg || !dwu) continue;
     const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
-    const int m0 = rt.m * 128, n0 = rt.n * 128;
+    const int m0 = rt.m * (CB::RA / 2), n0 = rt.n * CB::RB;
     const B16Src A{dAg + (size_t)sr.orow0 * I + m0, dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows};
     const B16Src B{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, nullptr, d, d - n0, sr.nrows};
-    B16Acc acc;
+    B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
-    b16_gemm<false, false, 256, 128>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, false, false>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const AccCoord c = b16_quad_coord<256>(q);
-      const int m = m0 + 32 * (c.row >> 6) + (c.row & 31), n = n0 + c.col4;
-      if (m >= I || n >= d) continue;
-      float* dst = ((c.row >> 5) & 1) ? dwu : dwg;
-      store_dw(dst + (size_t)m * d + n, acc.quad(q), da.accumulate);
-    }
+    for (int i = 0; i < CB::MI; ++i)
+#pragma unroll
+      for (int j = 0; j < CB::NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<CB>(i, j, q);
+          const int m = m0 + deinter(c.row), n = n0 + c.col4;
+          if (m >= I || n >= d) continue;
+          float* dst = ((c.row >> 5) & 1) ? dwu : dwg;
+          store_dw(dst + (size_t)m * d + n, acc.quad(i, j, q), da.accumulate);
+        }
   }
 }
 
 // dW_down = dO^T H (both read k-major).
 __global__ __launch_bounds__(B16_THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO, cbp H, DwArgs da) {
-  __shared__ __align__(16) char lds[B16Lds<256, 128>::value];
+  __shared__ __align__(16) char lds[CB::LDS];
   const int d = da.d, I = da.I;
-  const int MT = (d + 255) / 256, NT = (I + 127) / 128;
+  const int MT = (d + CB::RA - 1) / CB::RA, NT = (I + CB::RB - 1) / CB::RB;
   const TileRange tr = dw_range(da, MT * NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = dw_tile(t, MT * NT, MT);
     float* dwd = W.dwd[rt.s];
     if (!dwd) continue;
     const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
-    const int m0 = rt.m * 256, n0 = rt.n * 128;
+    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
     const B16Src A{dO + (size_t)sr.orow0 * d + m0, nullptr, d, d - m0, sr.nrows};
     const B16Src B{H + (size_t)sr.orow0 * I + n0, nullptr, I, I - n0, sr.nrows};
-    B16Acc acc;
+    B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
-    b16_gemm<false, false, 256, 128>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, false, false>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const AccCoord c = b16_quad_coord<256>(q);
-      const int m = m0 + c.row, n = n0 + c.col4;
-      if (m >= d || n >= I) continue;
-      store_dw(dwd + (size_t)m * I + n, acc.quad(q), da.accumulate);
-    }
+    for (int i = 0; i < CB::MI; ++i)
+#pragma unroll
+      for (int j = 0; j < CB::NJ; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<CB>(i, j, q);
+          const int m = m0 + c.row, n = n0 + c.col4;
+          if (m >= d || n >= I) continue;
+          store_dw(dwd + (size_t)m * I + n, acc.quad(i, j, q), da.accumulate);
+        }
   }
 }
 
@@ -668,7 +701,8 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
   hipStream_t st = as_stream(stream);
   const int S = n_slots(L);
   const Sched sc = sched_at(ws, S);
-  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
+  const int tile_rows = L->dtype == MOE_BF16 ? B16_ROWS : G_BM;
+  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, tile_rows,
                      (float* const*)nullptr, sc.mbase, sc.wbase);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
   const dim3 grid(persistent_blocks()), block(G_THREADS);
@@ -715,7 +749,8 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   char* dAg = (char*)ws + sched_bytes(S);
   char* dAu = dAg + act;
   const int d = L->d, I = L->I;
-  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T,
+  const int tile_rows = L->dtype == MOE_BF16 ? B16_ROWS : G_BM;
+  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, tile_rows,
                      L->dw_gate, sc.mbase, sc.wbase);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, d, I};
   const DwArgs da{offsets, sc.wbase, L->S_routed, S, T, k, d, I, accumulate_dw};

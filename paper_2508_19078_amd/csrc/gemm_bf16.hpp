@@ -1,21 +1,25 @@
-// bf16 grouped-GEMM core for gfx950: 8-wave blocks with a three-stage
-// direct-to-LDS pipeline.
+// bf16 grouped-GEMM core for gfx950: 8-wave blocks, a multi-stage
+// direct-to-LDS ring and register double-buffered MFMA fragments.
 //
 // A block of 512 threads (8 waves, two per SIMD) computes an RA x RB output
-// tile, RA, RB in {128, 256}, of C = sum_k A(r, k) B(n, k); each wave owns a
-// 64 x 64 sub-tile as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles (the bf16 shape that
-// reaches the chip's MFMA peak), operands swapped so that a lane holds groups of
-// four consecutive output columns.
+// tile of C = sum_k A(r, k) B(n, k).  The waves form a WM x WN grid; each owns
+// a TM x TN sub-tile as MI x NJ v_mfma_f32_32x32x16_bf16 tiles (the bf16 shape
+// that reaches the chip's MFMA peak), operands swapped so that a lane holds
+// groups of four consecutive output columns.
 //
 // * Tiles go straight from global memory to LDS (global_load_lds_dwordx4: each
-//   lane moves 16 bytes to LDS base + 16 * lane), three 64-deep K slabs in the
-//   ring: two are in flight while the third is multiplied.  Per-lane addresses
-//   are resolved once per tile; a slab only adds a uniform stride.
-// * K-contiguous tiles are stored [row][64 k] (128-byte rows) with the 16-byte
-//   chunk index XOR-swizzled by (row >> 1) & 7: the fragment reads of 16
+//   lane moves 16 bytes to LDS base + 16 * lane), NS slabs of BK k in a ring:
+//   up to NS - 1 slabs are in flight while one is multiplied.  Per-lane
+//   addresses are resolved once per tile; a slab only adds a uniform stride.
+// * Fragments are read one 16-k step ahead of the MFMAs that use them, into a
+//   second register set; at the end of a slab the read-ahead crosses into the
+//   next slab right after the barrier that publishes it.  LDS reads thus
+//   overlap the MFMAs of the same wave, not only those of the other wave.
+// * K-contiguous tiles are stored [row][BK k] with the 16-byte chunk index
+//   XOR-swizzled by a function of the row, so that the fragment reads of 16
 //   consecutive rows hit 16 distinct 4-bank groups.
 // * MN-contiguous tiles (weights in the NN products, both operands of the
-//   weight-gradient products) are stored k-major, [64 k][R rows], with the chunk
+//   weight-gradient products) are stored k-major, [BK k][R rows], with the chunk
 //   index XOR-swizzled by (k & 3) << 2, and read with ds_read_b64_tr_b16, which
 //   hands each lane four k-consecutive elements of one row; two such reads form
 //   a fragment, so nothing is transposed on the way in.
@@ -27,38 +31,83 @@
 //   last slab, so the clamped B data meets zeros.
 #pragma once
 
+#include <type_traits>
+
 #include "gemm.hpp"
 
 namespace fm {
 
-constexpr int B16_BK = 64;                      // k per slab
-constexpr int B16_NS = 3;                       // LDS stages
 constexpr int B16_THREADS = 512;                // 8 waves
 
 #define FM_LDS __attribute__((address_space(3)))
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
+// Tile configuration: RA x RB block tile, WM waves along RA, BK k per slab,
+// NS slabs in the LDS ring.
+template <int RA_, int RB_, int WM_, int BK_, int NS_> struct B16Cfg {
+  static constexpr int RA = RA_, RB = RB_, WM = WM_, WN = 8 / WM_, BK = BK_, NS = NS_;
+  static constexpr int TM = RA / WM, TN = RB / WN;    // wave sub-tile
+  static constexpr int MI = TM / 32, NJ = TN / 32;    // MFMA tiles per wave
+  static constexpr int KS = BK / 16;                  // MFMA k-steps per slab
+  static constexpr int A_BYTES = RA * BK * 2, STAGE = (RA + RB) * BK * 2;
+  static constexpr int LDS = NS * STAGE;
+  static constexpr int A_INS = RA * BK * 2 / 8192;    // DMA instructions per wave and slab
+  static constexpr int B_INS = RB * BK * 2 / 8192;
+  static_assert(WM * WN == 8 && TM % 32 == 0 && TN % 32 == 0, "8 waves of 32-multiples");
+  static_assert(BK == 32 || BK == 64, "slab depth");
+  static_assert(A_INS >= 1 && B_INS >= 1 && KS % 2 == 0, "whole DMA instructions per wave");
+  static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS ring");
+};
+
 // s_waitcnt with only vmcnt limited (expcnt / lgkmcnt left at their maxima).
 template <int N> __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+// s_waitcnt lgkmcnt(0) (vmcnt / expcnt left at their maxima).
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4)); }
 
 // Workgroup barrier without the memory fences of __syncthreads: the fences
 // would wait for every outstanding load, including the slabs still in flight.
-// LDS reads of the previous slab have completed (their MFMAs consumed them) and
-// this slab's DMA completion is waited for explicitly before the barrier.
+// Each wave waits for its own DMA and LDS reads explicitly before it.
 __device__ __forceinline__ void barrier_lds() { asm volatile("s_barrier" ::: "memory"); }
 
+// One global_load_lds_dwordx4: 16 bytes per lane from g to LDS l + 16 * lane
+// (l uniform, through M0).  Written as inline assembly so that the compiler's
+// wait-count bookkeeping does not see it: it would count the LDS write as an
+// out-of-order LDS event and then wait for every pending LDS read before each
+// MFMA.  The DMA's own completion is waited for explicitly (vmcnt, then a
+// barrier) before its data is read.  M0 is restored; s_nop covers the wait
+// state required between writing M0 and an LDS DMA.
 __device__ __forceinline__ void dma16(const void* g, FM_LDS void* l) {
-  __builtin_amdgcn_global_load_lds((const FM_GLOBAL void*)g, l, 16, 0, 0);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"((uint32_t)(uintptr_t)l)
+      : "memory");
 }
+
+// Keeps the instruction scheduler from moving anything across this point, so
+// that fragment reads stay ahead of the MFMAs they overlap.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // Wave index as a uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-__device__ __forceinline__ int swz_kc(int row) { return (row >> 1) & 7; }
+// K-contiguous rows hold BK / 8 chunks of 16 bytes.  A fragment read of 16
+// consecutive rows at one chunk must spread over the 16 4-bank groups of a
+// 256-byte bank period: with 128-byte rows the row parity picks the half and
+// (row >> 1) & 7 the chunk; with 64-byte rows row & 3 picks the quarter and
+// (row >> 2) & 3 the chunk.
+template <int BK> __device__ __forceinline__ int swz_kc(int row) {
+  return BK == 64 ? (row >> 1) & 7 : (row >> 2) & 3;
+}
 // A transposed read of one 16-lane group touches 4 k-rows and 2 adjacent
 // chunks; the two groups served together (rows +16) touch the next 2 chunks.
 // Moving k & 3 into bits 2-3 of the chunk position spreads the 4 x 4 chunk
@@ -88,34 +137,41 @@ __device__ __forceinline__ const bf16* b16_row(const B16Src& s, int r, int& pr) 
   return s.p;
 }
 
-// Direct-to-LDS loading of one R-row operand: the tile is R/8 blocks of 1 KB,
-// NI = R/64 of them per wave and slab.
-template <bool KC, int R> struct B16Dma {
-  static constexpr int NI = R / 64;
+// Direct-to-LDS loading of one R-row operand: a slab is R * BK * 2 / 1024
+// blocks of 1 KB, NI of them per wave.
+template <bool KC, int R, int BK, int NI> struct B16Dma {
+  static constexpr int CPK = BK / 8;   // 16-byte chunks per K-contiguous row
+  static constexpr int CPM = R / 8;    // 16-byte chunks per MN-contiguous k-row
   const char* ptr[NI];
   size_t step;
+
+  // Source of the chunk that lane `lane` moves in DMA instruction `ins` of
+  // slab 0: a = row, b = first k (KC); a = k-row, b = first row (MN).
+  __device__ __forceinline__ void chunk(int ins, int lane, int& a, int& b) const {
+    if (KC) {
+      a = ins * (64 / CPK) + lane / CPK;
+      b = 8 * ((lane % CPK) ^ swz_kc<BK>(a));
+    } else {
+      a = ins * (64 / CPM) + lane / CPM;
+      b = 8 * ((lane % CPM) ^ swz_mn(a));
+    }
+  }
 
   __device__ __forceinline__ void init(const B16Src& s) {
     const int lane = lane_id(), wave = wave_id();
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
-      const int ins = wave * NI + u;
+      int a, b, pr;
+      chunk(wave * NI + u, lane, a, b);
       if (KC) {
-        const int r = ins * 8 + (lane >> 3);            // 8 rows of 128 bytes
-        const int c = (lane & 7) ^ swz_kc(r);           // chunk this lane fetches
-        int pr;
-        const bf16* base = b16_row(s, r, pr);
-        ptr[u] = (const char*)(base + (size_t)min(pr, s.rows - 1) * s.ld + 8 * c);
+        const bf16* base = b16_row(s, a, pr);
+        ptr[u] = (const char*)(base + (size_t)min(pr, s.rows - 1) * s.ld + b);
       } else {
-        constexpr int CPR = R / 8;                       // 16-byte chunks per k-row
-        const int kr = ins * (64 / CPR) + lane / CPR;
-        const int c = (lane % CPR) ^ swz_mn(kr);
-        int pr;
-        const bf16* base = b16_row(s, 8 * c, pr);
-        ptr[u] = (const char*)(base + (size_t)kr * s.ld + min(pr, s.rows - 8));
+        const bf16* base = b16_row(s, b, pr);
+        ptr[u] = (const char*)(base + (size_t)a * s.ld + min(pr, s.rows - 8));
       }
     }
-    step = KC ? (size_t)B16_BK * 2 : (size_t)B16_BK * s.ld * 2;
+    step = KC ? (size_t)BK * 2 : (size_t)BK * s.ld * 2;
   }
 
   __device__ __forceinline__ void issue_full(int slab, FM_LDS char* tile) const {
@@ -125,46 +181,43 @@ template <bool KC, int R> struct B16Dma {
     for (int u = 0; u < NI; ++u) dma16(ptr[u] + adv, tile + (wave * NI + u) * 1024);
   }
 
+  // A slab that reaches past K: k is clamped to the last valid element.
   __device__ __forceinline__ void issue_tail(const B16Src& s, int k0, FM_LDS char* tile) const {
     const int lane = lane_id(), wave = wave_id();
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
       const int ins = wave * NI + u;
+      int a, b, pr;
+      chunk(ins, lane, a, b);
       if (KC) {
-        const int r = ins * 8 + (lane >> 3);
-        const int c = (lane & 7) ^ swz_kc(r);
-        int pr;
-        const bf16* base = b16_row(s, r, pr);
-        dma16(base + (size_t)min(pr, s.rows - 1) * s.ld + min(k0 + 8 * c, s.K - 8), tile + ins * 1024);
+        const bf16* base = b16_row(s, a, pr);
+        dma16(base + (size_t)min(pr, s.rows - 1) * s.ld + min(k0 + b, s.K - 8), tile + ins * 1024);
       } else {
-        constexpr int CPR = R / 8;
-        const int kr = ins * (64 / CPR) + lane / CPR;
-        const int c = (lane % CPR) ^ swz_mn(kr);
-        int pr;
-        const bf16* base = b16_row(s, 8 * c, pr);
-        dma16(base + (size_t)min(k0 + kr, s.K - 1) * s.ld + min(pr, s.rows - 8), tile + ins * 1024);
+        const bf16* base = b16_row(s, b, pr);
+        dma16(base + (size_t)min(k0 + a, s.K - 1) * s.ld + min(pr, s.rows - 8), tile + ins * 1024);
       }
     }
   }
 };
 
-// MFMA fragments of a wave's 64 rows (two 32-row blocks) of an R-row tile: a
-// fragment is 32 rows x 16 k, 8 k per lane: lane l holds row r0 + l % 32 and
-// k 16 ks + 8 (l / 32) + 0..7 of the slab.  Offsets are per lane, computed once.
-template <bool KC, int R> struct B16Frag {
-  uint32_t off[2][KC ? 4 : 1];   // [i][ks] for K-contiguous, [i] for MN-contiguous
+// MFMA fragments of a wave's NB 32-row blocks of an R-row tile: a fragment is
+// 32 rows x 16 k, 8 k per lane: lane l holds row r0 + l % 32 and k
+// 16 ks + 8 (l / 32) + 0..7 of the slab.  Offsets are per lane, computed once.
+template <bool KC, int R, int BK, int NB> struct B16Frag {
+  static constexpr int KS = BK / 16;
+  uint32_t off[NB][KC ? KS : 1];   // [i][ks] for K-contiguous, [i] for MN-contiguous
 
-  __device__ __forceinline__ void init(int w) {
+  __device__ __forceinline__ void init(int row0) {
     const int lane = lane_id();
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int r0 = w * 64 + i * 32;
+    for (int i = 0; i < NB; ++i) {
+      const int r0 = row0 + i * 32;
       if (KC) {
         const int r = r0 + (lane & 31);
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
+        for (int ks = 0; ks < KS; ++ks) {
           const int c = ks * 2 + (lane >> 5);
-          off[i][ks] = (uint32_t)(r * 128 + ((c ^ swz_kc(r)) << 4));
+          off[i][ks] = (uint32_t)(r * (BK * 2) + ((c ^ swz_kc<BK>(r)) << 4));
         }
       } else {
         // ds_read_b64_tr_b16: in each 16-lane group, output lane i element j
@@ -208,109 +261,146 @@ __device__ __forceinline__ bf16x8_t b16_mask_k(bf16x8_t f, int k0, int ks, int K
   return __builtin_bit_cast(bf16x8_t, w);
 }
 
-// Accumulator of a wave's 64 x 64 sub-tile: 2 x 2 MFMA tiles of 32 x 32.
-// Register r of tile (i, j) holds sub-tile row i*32 + lane % 32 and column
+// Accumulator of a wave's sub-tile: MI x NJ MFMA tiles of 32 x 32.  Register
+// r of tile (i, j) holds sub-tile row i*32 + lane % 32 and column
 // j*32 + 8 (r / 4) + 4 (lane / 32) + r % 4.
-struct B16Acc {
-  f32x16_t v[2][2];
+template <int MI, int NJ> struct B16Acc {
+  f32x16_t v[MI][NJ];
   __device__ __forceinline__ void zero() {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) v[i][j][r] = 0.f;
   }
-  // quad g = (i, j, q): i = g >> 3, j = (g >> 2) & 1, register group q = g & 3
-  __device__ __forceinline__ f32x4_t quad(int g) const {
-    const f32x16_t& t = v[g >> 3][(g >> 2) & 1];
-    const int q = g & 3;
+  // registers 4q .. 4q+3 of tile (i, j)
+  __device__ __forceinline__ f32x4_t quad(int i, int j, int q) const {
+    const f32x16_t& t = v[i][j];
     return f32x4_t{t[4 * q], t[4 * q + 1], t[4 * q + 2], t[4 * q + 3]};
   }
 };
 
-// Block-tile coordinates of quad g: the row, and the first of 4 columns.
-template <int RA> __device__ __forceinline__ AccCoord b16_quad_coord(int g) {
+// Block-tile coordinates of quad (i, j, q): the row, and the first of 4 columns.
+template <class C> __device__ __forceinline__ AccCoord b16_coord(int i, int j, int q) {
   const int lane = lane_id(), wave = wave_id();
-  const int wm = wave % (RA / 64), wn = wave / (RA / 64);
-  const int i = g >> 3, j = (g >> 2) & 1, q = g & 3;
-  return AccCoord{wm * 64 + i * 32 + (lane & 31), wn * 64 + j * 32 + 8 * q + 4 * (lane >> 5)};
+  const int wm = wave % C::WM, wn = wave / C::WM;
+  return AccCoord{wm * C::TM + i * 32 + (lane & 31), wn * C::TN + j * 32 + 8 * q + 4 * (lane >> 5)};
 }
-
-template <bool AKC, bool BKC, int RA, int RB, bool TAIL>
-__device__ __forceinline__ void b16_mma_slab(const FM_LDS char* buf, const B16Frag<AKC, RA>& fa_off,
-                                             const B16Frag<BKC, RB>& fb_off, B16Acc& acc, int k0, int K) {
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    bf16x8_t fa[2], fb[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      fa[i] = fa_off.read(buf, i, ks);
-      if (TAIL) fa[i] = b16_mask_k(fa[i], k0, ks, K);
-    }
-#pragma unroll
-    for (int j = 0; j < 2; ++j) fb[j] = fb_off.read(buf + RA * 128, j, ks);
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc.v[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc.v[i][j], 0, 0, 0);
-  }
-}
-
-// LDS bytes of the bf16 core for an RA x RB tile.
-template <int RA, int RB> struct B16Lds {
-  static constexpr int value = B16_NS * (RA + RB) * 128;
-};
 
 // k loop over [0, K), accumulating into acc.  Ends with a barrier so the LDS
 // can be reused by a following call.
-template <bool AKC, bool BKC, int RA, int RB>
+//
+// Steady state (slab kt, while slab kt + NS is still a whole slab): every
+// k-step but the last reads the next k-step's fragments, then multiplies.  The
+// last k-step multiplies half of its tiles, waits for its own LDS reads and for
+// slab kt + 1 to land, crosses the barrier that publishes slab kt + 1 and frees
+// slab kt's buffer, refills that buffer with slab kt + NS, reads the first
+// fragments of slab kt + 1 and multiplies the other half, which hides the read
+// latency.  The loop body is straight-line code, so the LDS-read wait counts
+// stay exact.  The last NS slabs (and the partial one) drain through a
+// general version of the same step.
+template <class C, bool AKC, bool BKC>
 __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K, FM_LDS char* lds,
-                                         B16Acc& acc) {
-  static_assert((RA / 64) * (RB / 64) == 8, "8 waves of 64 x 64");
-  constexpr int STAGE = (RA + RB) * 128;
-  constexpr int PER_STAGE = RA / 64 + RB / 64;   // DMA instructions per wave and stage
-  const int nk = (K + B16_BK - 1) / B16_BK;
+                                         B16Acc<C::MI, C::NJ>& acc) {
+  constexpr int BK = C::BK, NS = C::NS, KS = C::KS, MI = C::MI, NJ = C::NJ;
+  constexpr int PER = C::A_INS + C::B_INS;     // DMA instructions per wave and slab
+  const int nk = (K + BK - 1) / BK;
   if (nk <= 0) return;
-  const int nfull = K / B16_BK;                  // slabs with no k past K
+  const int nfull = K / BK;                    // slabs with no k past K
   const int wave = wave_id();
-  B16Frag<AKC, RA> fa;
-  B16Frag<BKC, RB> fb;
-  fa.init(wave % (RA / 64));
-  fb.init(wave / (RA / 64));
-  B16Dma<AKC, RA> da;
-  B16Dma<BKC, RB> db;
+  B16Frag<AKC, C::RA, BK, MI> fa;
+  B16Frag<BKC, C::RB, BK, NJ> fb;
+  fa.init((wave % C::WM) * C::TM);
+  fb.init((wave / C::WM) * C::TN);
+  B16Dma<AKC, C::RA, BK, C::A_INS> da;
+  B16Dma<BKC, C::RB, BK, C::B_INS> db;
   da.init(A);
   db.init(B);
+
   auto issue = [&](int s) {
-    FM_LDS char* buf = lds + (s % B16_NS) * STAGE;
+    FM_LDS char* buf = lds + (s % NS) * C::STAGE;
     if (s < nfull) {
       da.issue_full(s, buf);
-      db.issue_full(s, buf + RA * 128);
+      db.issue_full(s, buf + C::A_BYTES);
     } else {
-      da.issue_tail(A, s * B16_BK, buf);
-      db.issue_tail(B, s * B16_BK, buf + RA * 128);
+      da.issue_tail(A, s * BK, buf);
+      db.issue_tail(B, s * BK, buf + C::A_BYTES);
     }
   };
-  // Slab kt is ready once at most one later slab is still in flight; the
-  // barrier also tells every wave that slab kt-1's buffer is free again.
-  auto ready = [&](int kt) {
-    if (kt + 1 < nk) wait_vmcnt<PER_STAGE>();
-    else wait_vmcnt<0>();
-    barrier_lds();
-    if (kt + 2 < nk) issue(kt + 2);
+  bf16x8_t xa[2][MI], xb[2][NJ];
+  auto read = [&](int set, const FM_LDS char* buf, int ks) {
+#pragma unroll
+    for (int i = 0; i < MI; ++i) xa[set][i] = fa.read(buf, i, ks);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) xb[set][j] = fb.read(buf + C::A_BYTES, j, ks);
   };
-  issue(0);
-  if (nk > 1) issue(1);
+  // MFMAs of register set `set` for A tiles [i0, i1).
+  auto mma = [&](int set, int i0, int i1, bool tail, int k0, int ks) {
+#pragma unroll
+    for (int i = i0; i < i1; ++i) {
+      const bf16x8_t a = tail ? b16_mask_k(xa[set][i], k0, ks, K) : xa[set][i];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        acc.v[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xb[set][j], a, acc.v[i][j], 0, 0, 0);
+    }
+  };
+  constexpr int LAST = (KS - 1) & 1;           // register set of the last k-step
+  constexpr int HALF = MI / 2;
+
+  // The ring starts full: slabs 0 .. NS-1 in flight.
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    if (s < nk) issue(s);
+  if (nk >= NS) wait_vmcnt<(NS - 1) * PER>();
+  else wait_vmcnt<0>();
+  wait_lgkm0();   // no scalar loads pending: LDS-read waits in the loop can count
+  barrier_lds();
+  read(0, lds, 0);
+
   int kt = 0;
-  for (; kt < nfull; ++kt) {
-    ready(kt);
-    b16_mma_slab<AKC, BKC, RA, RB, false>(lds + (kt % B16_NS) * STAGE, fa, fb, acc, kt * B16_BK, K);
+  const int nsteady = nfull - NS;              // slab kt + NS is whole
+  for (; kt < nsteady; ++kt) {
+    const FM_LDS char* buf = lds + (kt % NS) * C::STAGE;
+#pragma unroll
+    for (int ks = 0; ks + 1 < KS; ++ks) {
+      read((ks & 1) ^ 1, buf, ks + 1);
+      sched_fence();
+      mma(ks & 1, 0, MI, false, 0, 0);
+      sched_fence();
+    }
+    mma(LAST, 0, HALF, false, 0, 0);
+    sched_fence();
+    wait_lgkm0();
+    wait_vmcnt<(NS - 2) * PER>();
+    barrier_lds();
+    FM_LDS char* nbuf = lds + ((kt + NS) % NS) * C::STAGE;
+    da.issue_full(kt + NS, nbuf);
+    db.issue_full(kt + NS, nbuf + C::A_BYTES);
+    read(LAST ^ 1, lds + ((kt + 1) % NS) * C::STAGE, 0);
+    sched_fence();
+    mma(LAST, HALF, MI, false, 0, 0);
+    sched_fence();
   }
-  if (kt < nk) {   // the partial last slab
-    ready(kt);
-    b16_mma_slab<AKC, BKC, RA, RB, true>(lds + (kt % B16_NS) * STAGE, fa, fb, acc, kt * B16_BK, K);
+  // Drain: the slabs whose refill would pass the end, and the partial slab.
+  for (; kt < nk; ++kt) {
+    const FM_LDS char* buf = lds + (kt % NS) * C::STAGE;
+    const bool tail = kt >= nfull;
+#pragma unroll
+    for (int ks = 0; ks + 1 < KS; ++ks) {
+      read((ks & 1) ^ 1, buf, ks + 1);
+      mma(ks & 1, 0, MI, tail, kt * BK, ks);
+    }
+    if (kt + 1 < nk) {
+      wait_lgkm0();
+      const int later = min(NS - 2, nk - 2 - kt);   // slabs after kt + 1 still in flight
+      if (later >= NS - 2) wait_vmcnt<(NS - 2) * PER>();
+      else wait_vmcnt<0>();
+      barrier_lds();
+      if (kt + NS < nk) issue(kt + NS);
+      read(LAST ^ 1, lds + ((kt + 1) % NS) * C::STAGE, 0);
+    }
+    mma(LAST, 0, MI, tail, kt * BK, KS - 1);
   }
   barrier_lds();
 }
