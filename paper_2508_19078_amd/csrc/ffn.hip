@@ -420,12 +420,32 @@ typedef const bf16* cbp;
 
 // Block tile of every bf16 product: 256 x 256, waves 2 x 4 (128 x 64 each),
 // 32-deep slabs, four in the LDS ring (128 KB).
-using CB = B16Cfg<256, 256, 2, 32, 4>;
+using CB = B16Cfg<256, 256, 2, 64, 2>;
 constexpr int B16_ROWS = CB::RA;   // rows per row tile of the bf16 kernels
 
 // Physical index of logical row / column c of an operand that interleaves two
 // matrices in 32-blocks (the matrix is (c >> 5) & 1).
 __device__ __forceinline__ int deinter(int c) { return 32 * (c >> 6) + (c & 31); }
+
+// Writes a whole RA x RB accumulator tile (bf16) through LDS: out points at
+// the tile origin, rows x cols of it are valid.
+template <class C>
+__device__ __forceinline__ void b16_store_staged(const B16Acc<C::MI, C::NJ>& acc, FM_LDS char* lds, bf16* out,
+                                                 size_t ld, int rows, int cols) {
+  using S = Stage<bf16, C::RB>;
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const AccCoord c = b16_coord<C>(i, j, q);
+        S::put4(lds, c.row, c.col4, acc.quad(i, j, q));
+      }
+  barrier_lds_writes();
+  S::template copy_out<C::RA>(lds, out, ld, rows, cols);
+  barrier_lds();
+}
 
 // [A_g | A_u] = X_s [W_gate | W_up]^T, H = silu(A_g) A_u.  The B tile
 // interleaves 32-row blocks of W_gate and W_up (128 intermediate columns per
@@ -444,8 +464,13 @@ __global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
     const B16Src B{W.wg[rt.s] + (size_t)n0 * d, W.wu[rt.s] + (size_t)n0 * d, d, I - n0, d};
     B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
-    b16_gemm<CB, true, true>(A, B, d, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, true, true, false, true>(A, B, d, (FM_LDS char*)lds, acc);
+    // A_g and A_u staged side by side (64 KB each), then H in the first half.
+    using SG = Stage<bf16, CB::RB / 2>;
+    FM_LDS char* sg = (FM_LDS char*)lds;
+    FM_LDS char* su = sg + CB::RA * (CB::RB / 2) * 2;
     const size_t ob = (size_t)(sr.orow0 + m0);
+    const int rows = sr.nrows - m0, cols = I - n0;
 #pragma unroll
     for (int i = 0; i < CB::MI; ++i)
 #pragma unroll
@@ -453,17 +478,29 @@ __global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const AccCoord c = b16_coord<CB>(i, 2 * jj, q);
-          const int n = n0 + deinter(c.col4);
-          if (c.row >= sr.nrows - m0 || n >= I) continue;
+          SG::put4(sg, c.row, deinter(c.col4), acc.quad(i, 2 * jj, q));
+          SG::put4(su, c.row, deinter(c.col4), acc.quad(i, 2 * jj + 1, q));
+        }
+    barrier_lds_writes();
+    SG::template copy_out<CB::RA>(sg, Ag + ob * I + n0, I, rows, cols);
+    SG::template copy_out<CB::RA>(su, Au + ob * I + n0, I, rows, cols);
+    barrier_lds();
+#pragma unroll
+    for (int i = 0; i < CB::MI; ++i)
+#pragma unroll
+      for (int jj = 0; jj < CB::NJ / 2; ++jj)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<CB>(i, 2 * jj, q);
           const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
           f32x4_t h;
 #pragma unroll
           for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm(ag[r]) * u[r];
-          const size_t o = (ob + c.row) * I + n;
-          store4(Ag + o, ag);
-          store4(Au + o, u);
-          store4(H + o, h);
+          SG::put4(sg, c.row, deinter(c.col4), h);
         }
+    barrier_lds_writes();
+    SG::template copy_out<CB::RA>(sg, H + ob * I + n0, I, rows, cols);
+    barrier_lds();
   }
 }
 
@@ -482,17 +519,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_down(LayerPtrs<bf16> W, cbp H,
     B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
     b16_gemm<CB, true, true>(A, B, I, (FM_LDS char*)lds, acc);
-#pragma unroll
-    for (int i = 0; i < CB::MI; ++i)
-#pragma unroll
-      for (int j = 0; j < CB::NJ; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const AccCoord c = b16_coord<CB>(i, j, q);
-          const int n = n0 + c.col4;
-          if (c.row >= sr.nrows - m0 || n >= d) continue;
-          store4(O + (ob + c.row) * d + n, acc.quad(i, j, q));
-        }
+    b16_store_staged<CB>(acc, (FM_LDS char*)lds, O + ob * d + n0, d, sr.nrows - m0, d - n0);
   }
 }
 
@@ -555,17 +582,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg,
                               B16Src{W.wg[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
     b16_gemm<CB, true, false>(B16Src{dAu + ob * I, nullptr, I, sr.nrows - m0, I},
                               B16Src{W.wu[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
-#pragma unroll
-    for (int i = 0; i < CB::MI; ++i)
-#pragma unroll
-      for (int j = 0; j < CB::NJ; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const AccCoord c = b16_coord<CB>(i, j, q);
-          const int n = n0 + c.col4;
-          if (c.row >= sr.nrows - m0 || n >= d) continue;
-          store4(dXp + (ob + c.row) * d + n, acc.quad(i, j, q));
-        }
+    b16_store_staged<CB>(acc, (FM_LDS char*)lds, dXp + ob * d + n0, d, sr.nrows - m0, d - n0);
   }
 }
 
@@ -589,7 +606,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X
     const B16Src B{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, nullptr, d, d - n0, sr.nrows};
     B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
-    b16_gemm<CB, false, false>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
+    b16_gemm<CB, false, false, true, false>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
 #pragma unroll
     for (int i = 0; i < CB::MI; ++i)
 #pragma unroll

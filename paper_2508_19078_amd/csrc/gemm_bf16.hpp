@@ -97,6 +97,30 @@ __device__ __forceinline__ void dma16(const void* g, FM_LDS void* l) {
 // that fragment reads stay ahead of the MFMAs they overlap.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
+// A wave-uniform pointer held in scalar registers (the compiler cannot always
+// prove that a pointer read from memory is uniform).
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+
+// The same with a uniform 64-bit base and a 32-bit per-lane byte offset.
+__device__ __forceinline__ void dma16s(const void* base, uint32_t off, FM_LDS void* l) {
+  base = uniform_ptr(base);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"((uint32_t)(uintptr_t)l)
+      : "memory");
+}
+
 // Wave index as a uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
@@ -138,37 +162,54 @@ __device__ __forceinline__ const bf16* b16_row(const B16Src& s, int r, int& pr) 
 }
 
 // Direct-to-LDS loading of one R-row operand: a slab is R * BK * 2 / 1024
-// blocks of 1 KB, NI of them per wave.
-template <bool KC, int R, int BK, int NI> struct B16Dma {
+// blocks of 1 KB, NI of them per wave.  Each instruction takes a uniform base
+// (scalar registers) plus a 32-bit per-lane offset, so a slab only advances
+// the base.  An MN-contiguous operand that interleaves two matrices mixes both
+// within one instruction and keeps full per-lane pointers instead (V64).
+template <bool KC, int R, int BK, int NI, bool INTER> struct B16Dma {
   static constexpr int CPK = BK / 8;   // 16-byte chunks per K-contiguous row
   static constexpr int CPM = R / 8;    // 16-byte chunks per MN-contiguous k-row
-  const char* ptr[NI];
+  static constexpr int RPI = 64 / CPK; // K-contiguous rows per instruction
+  static constexpr bool V64 = !KC && INTER;
+  const char* base[V64 ? 1 : NI];      // uniform
+  uint32_t off[V64 ? 1 : NI];          // per lane
+  const char* ptr[V64 ? NI : 1];       // per lane (V64)
   size_t step;
 
   // Source of the chunk that lane `lane` moves in DMA instruction `ins` of
   // slab 0: a = row, b = first k (KC); a = k-row, b = first row (MN).
   __device__ __forceinline__ void chunk(int ins, int lane, int& a, int& b) const {
     if (KC) {
-      a = ins * (64 / CPK) + lane / CPK;
+      a = ins * RPI + lane / CPK;
       b = 8 * ((lane % CPK) ^ swz_kc<BK>(a));
     } else {
       a = ins * (64 / CPM) + lane / CPM;
       b = 8 * ((lane % CPM) ^ swz_mn(a));
     }
   }
+  // Matrix of a K-contiguous instruction's rows (all in one 32-row block).
+  __device__ __forceinline__ static const bf16* kc_matrix(const B16Src& s, int ins) {
+    return (INTER && (((ins * RPI) >> 5) & 1)) ? s.p2 : s.p;
+  }
+  __device__ __forceinline__ static int phys_row(int r) { return INTER ? 32 * (r >> 6) + (r & 31) : r; }
 
   __device__ __forceinline__ void init(const B16Src& s) {
     const int lane = lane_id(), wave = wave_id();
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
-      int a, b, pr;
-      chunk(wave * NI + u, lane, a, b);
-      if (KC) {
-        const bf16* base = b16_row(s, a, pr);
-        ptr[u] = (const char*)(base + (size_t)min(pr, s.rows - 1) * s.ld + b);
+      const int ins = wave * NI + u;
+      int a, b;
+      chunk(ins, lane, a, b);
+      if (V64) {
+        int pr;
+        const bf16* m = b16_row(s, b, pr);
+        ptr[u] = (const char*)(m + (size_t)a * s.ld + min(pr, s.rows - 8));
+      } else if (KC) {
+        base[u] = (const char*)kc_matrix(s, ins);
+        off[u] = (uint32_t)(((size_t)min(phys_row(a), s.rows - 1) * s.ld + b) * 2);
       } else {
-        const bf16* base = b16_row(s, b, pr);
-        ptr[u] = (const char*)(base + (size_t)a * s.ld + min(pr, s.rows - 8));
+        base[u] = (const char*)s.p;
+        off[u] = (uint32_t)(((size_t)a * s.ld + min(b, s.rows - 8)) * 2);
       }
     }
     step = KC ? (size_t)BK * 2 : (size_t)BK * s.ld * 2;
@@ -178,7 +219,11 @@ template <bool KC, int R, int BK, int NI> struct B16Dma {
     const int wave = wave_id();
     const size_t adv = step * (size_t)slab;
 #pragma unroll
-    for (int u = 0; u < NI; ++u) dma16(ptr[u] + adv, tile + (wave * NI + u) * 1024);
+    for (int u = 0; u < NI; ++u) {
+      FM_LDS char* dst = tile + (wave * NI + u) * 1024;
+      if (V64) dma16(ptr[u] + adv, dst);
+      else dma16s(base[u] + adv, off[u], dst);
+    }
   }
 
   // A slab that reaches past K: k is clamped to the last valid element.
@@ -187,14 +232,20 @@ template <bool KC, int R, int BK, int NI> struct B16Dma {
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
       const int ins = wave * NI + u;
-      int a, b, pr;
+      FM_LDS char* dst = tile + ins * 1024;
+      int a, b;
       chunk(ins, lane, a, b);
-      if (KC) {
-        const bf16* base = b16_row(s, a, pr);
-        dma16(base + (size_t)min(pr, s.rows - 1) * s.ld + min(k0 + b, s.K - 8), tile + ins * 1024);
+      if (V64) {
+        int pr;
+        const bf16* m = b16_row(s, b, pr);
+        dma16(m + (size_t)min(k0 + a, s.K - 1) * s.ld + min(pr, s.rows - 8), dst);
+      } else if (KC) {
+        // K - 8 >= k0: both are multiples of 8 and the slab starts below K
+        const char* bt = (const char*)(kc_matrix(s, ins) + k0);
+        dma16s(bt, (uint32_t)(((size_t)min(phys_row(a), s.rows - 1) * s.ld + min(b, s.K - 8 - k0)) * 2), dst);
       } else {
-        const bf16* base = b16_row(s, b, pr);
-        dma16(base + (size_t)min(k0 + a, s.K - 1) * s.ld + min(pr, s.rows - 8), tile + ins * 1024);
+        const char* bt = (const char*)(s.p + (size_t)k0 * s.ld);
+        dma16s(bt, (uint32_t)(((size_t)min(a, s.K - 1 - k0) * s.ld + min(b, s.rows - 8)) * 2), dst);
       }
     }
   }
@@ -202,10 +253,12 @@ template <bool KC, int R, int BK, int NI> struct B16Dma {
 
 // MFMA fragments of a wave's NB 32-row blocks of an R-row tile: a fragment is
 // 32 rows x 16 k, 8 k per lane: lane l holds row r0 + l % 32 and k
-// 16 ks + 8 (l / 32) + 0..7 of the slab.  Offsets are per lane, computed once.
+// 16 ks + 8 (l / 32) + 0..7 of the slab.  Offsets are per lane, computed once:
+// for K-contiguous tiles the k-step only flips bits 5-6 of the offset (the
+// chunk index is 2 ks + l / 32 and the swizzle XORs it), for MN-contiguous
+// tiles it adds 16 k-rows.
 template <bool KC, int R, int BK, int NB> struct B16Frag {
-  static constexpr int KS = BK / 16;
-  uint32_t off[NB][KC ? KS : 1];   // [i][ks] for K-contiguous, [i] for MN-contiguous
+  uint32_t off[NB];
 
   __device__ __forceinline__ void init(int row0) {
     const int lane = lane_id();
@@ -214,11 +267,7 @@ template <bool KC, int R, int BK, int NB> struct B16Frag {
       const int r0 = row0 + i * 32;
       if (KC) {
         const int r = r0 + (lane & 31);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const int c = ks * 2 + (lane >> 5);
-          off[i][ks] = (uint32_t)(r * (BK * 2) + ((c ^ swz_kc<BK>(r)) << 4));
-        }
+        off[i] = (uint32_t)(r * (BK * 2) + (((lane >> 5) ^ swz_kc<BK>(r)) << 4));
       } else {
         // ds_read_b64_tr_b16: in each 16-lane group, output lane i element j
         // comes from the address of lane 4j + i/4, offset i % 4.  Group g covers
@@ -229,16 +278,16 @@ template <bool KC, int R, int BK, int NB> struct B16Frag {
         const int g = lane >> 4, L = lane & 15;
         const int n = r0 + 16 * (g & 1) + 4 * (L & 3);
         const int k = 8 * (g >> 1) + (L >> 2);
-        off[i][0] = (uint32_t)(k * (R * 2) + (((n >> 3) ^ swz_mn(k)) << 4) + ((n >> 2) & 1) * 8);
+        off[i] = (uint32_t)(k * (R * 2) + (((n >> 3) ^ swz_mn(k)) << 4) + ((n >> 2) & 1) * 8);
       }
     }
   }
 
   __device__ __forceinline__ bf16x8_t read(const FM_LDS char* tile, int i, int ks) const {
     if (KC) {
-      return __builtin_bit_cast(bf16x8_t, *(const FM_LDS u32x4_t*)(tile + off[i][ks]));
+      return __builtin_bit_cast(bf16x8_t, *(const FM_LDS u32x4_t*)(tile + (off[i] ^ (uint32_t)(ks << 5))));
     } else {
-      const FM_LDS char* p = tile + off[i][0] + ks * 16 * (R * 2);
+      const FM_LDS char* p = tile + off[i] + ks * 16 * (R * 2);
       const i16x4_t v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((FM_LDS i16x4_t*)p);
       const i16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((FM_LDS i16x4_t*)(p + 4 * (R * 2)));
       const u32x2_t w0 = __builtin_bit_cast(u32x2_t, v0), w1 = __builtin_bit_cast(u32x2_t, v1);
@@ -288,6 +337,60 @@ template <class C> __device__ __forceinline__ AccCoord b16_coord(int i, int j, i
   return AccCoord{wm * C::TM + i * 32 + (lane & 31), wn * C::TN + j * 32 + 8 * q + 4 * (lane >> 5)};
 }
 
+// Output staging.  Stores straight from the accumulator layout write 8 bytes
+// per lane scattered over 32 rows; instead a tile is put into LDS (row-major,
+// the 16-byte chunk index XOR-swizzled by the row) and copied out with every
+// lane storing 16 consecutive bytes and each row written whole.  T is the
+// element type of the output (bf16 or float), COLS the tile width.
+template <typename T, int COLS> struct Stage {
+  static constexpr int EPC = 16 / sizeof(T);         // elements per 16-byte chunk
+  static constexpr int CPR = COLS / EPC;             // chunks per row
+  static constexpr int ROW_BYTES = COLS * (int)sizeof(T);
+  static_assert(CPR == 16 || CPR == 32 || CPR == 64, "chunks per row");
+
+  // LDS byte offset of the 4 values at (row, col), col a multiple of 4.
+  static __device__ __forceinline__ uint32_t at(int row, int col) {
+    const int c = col / EPC;
+    return (uint32_t)(row * ROW_BYTES + ((c ^ (row & (CPR - 1))) << 4) + (col % EPC) * (int)sizeof(T));
+  }
+  static __device__ __forceinline__ void put4(FM_LDS char* lds, int row, int col, f32x4_t v) {
+    FM_LDS char* p = lds + at(row, col);
+    if (sizeof(T) == 2) {
+      *(FM_LDS u32x2_t*)p = u32x2_t{(uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
+                                    (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16)};
+    } else {
+      *(FM_LDS f32x4_t*)p = v;
+    }
+  }
+  // Copies rows [0, ROWS) of the staged tile to out[row * ld + col] for
+  // row < rows_valid and col < cols_valid (a multiple of EPC); with
+  // accumulate (float only) the values are added to what out holds.
+  template <int ROWS>
+  static __device__ __forceinline__ void copy_out(const FM_LDS char* lds, T* out, size_t ld, int rows_valid,
+                                                  int cols_valid, bool accumulate = false) {
+    constexpr int TOTAL = ROWS * CPR;
+#pragma unroll 4
+    for (int idx = threadIdx.x; idx < TOTAL; idx += B16_THREADS) {
+      const int row = idx / CPR, c = idx % CPR;
+      u32x4_t v = *(const FM_LDS u32x4_t*)(lds + row * ROW_BYTES + ((c ^ (row & (CPR - 1))) << 4));
+      if (row < rows_valid && c * EPC < cols_valid) {
+        T* dst = out + (size_t)row * ld + c * EPC;
+        if (sizeof(T) == 4 && accumulate) {
+          const f32x4_t o = *(const FM_GLOBAL f32x4_t*)dst;
+          v = __builtin_bit_cast(u32x4_t, __builtin_bit_cast(f32x4_t, v) + o);
+        }
+        st16(dst, v);
+      }
+    }
+  }
+};
+
+// Barrier that also makes this wave's LDS writes visible to the block.
+__device__ __forceinline__ void barrier_lds_writes() {
+  wait_lgkm0();
+  barrier_lds();
+}
+
 // k loop over [0, K), accumulating into acc.  Ends with a barrier so the LDS
 // can be reused by a following call.
 //
@@ -300,7 +403,7 @@ template <class C> __device__ __forceinline__ AccCoord b16_coord(int i, int j, i
 // latency.  The loop body is straight-line code, so the LDS-read wait counts
 // stay exact.  The last NS slabs (and the partial one) drain through a
 // general version of the same step.
-template <class C, bool AKC, bool BKC>
+template <class C, bool AKC, bool BKC, bool AI = false, bool BI = false>
 __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K, FM_LDS char* lds,
                                          B16Acc<C::MI, C::NJ>& acc) {
   constexpr int BK = C::BK, NS = C::NS, KS = C::KS, MI = C::MI, NJ = C::NJ;
@@ -313,8 +416,8 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
   B16Frag<BKC, C::RB, BK, NJ> fb;
   fa.init((wave % C::WM) * C::TM);
   fb.init((wave / C::WM) * C::TN);
-  B16Dma<AKC, C::RA, BK, C::A_INS> da;
-  B16Dma<BKC, C::RB, BK, C::B_INS> db;
+  B16Dma<AKC, C::RA, BK, C::A_INS, AI> da;
+  B16Dma<BKC, C::RB, BK, C::B_INS, BI> db;
   da.init(A);
   db.init(B);
 
