@@ -56,6 +56,14 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// Two fp32 -> packed bf16 (low half = a), round to nearest even, with the
+// gfx950 conversion instruction (same results as f2bf for finite inputs).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+
 template <typename T> struct elem;
 template <> struct elem<float> {
   static __device__ __forceinline__ float load(const float* p) { return *p; }
@@ -94,7 +102,7 @@ __device__ __forceinline__ u32x4_t pack16(const float* in, bf16*) {
   u32x4_t v;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    v[i] = (uint32_t)f2bf(in[2 * i]) | ((uint32_t)f2bf(in[2 * i + 1]) << 16);
+    v[i] = pk_bf16(in[2 * i], in[2 * i + 1]);
   return v;
 }
 __device__ __forceinline__ u32x4_t pack16(const float* in, float*) {

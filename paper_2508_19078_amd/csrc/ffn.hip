@@ -172,6 +172,11 @@ template <typename T> LayerPtrs<T> layer_ptrs(const moe_layer* L) {
 }
 
 __device__ __forceinline__ float sigm(float z) { return 1.0f / (1.0f + expf(-z)); }
+// Logistic function with the hardware exp2 and reciprocal (about 1 ulp each),
+// for epilogues whose results are rounded to bf16.
+__device__ __forceinline__ float sigm_fast(float z) {
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
 
 struct RowArgs {
   const int32_t* offsets;
@@ -419,7 +424,7 @@ __global__ __launch_bounds__(G_THREADS) void kf_dw_d(LayerPtrs<T> W, const T* __
 typedef const bf16* cbp;
 
 // Block tile of every bf16 product: 256 x 256, waves 2 x 4 (128 x 64 each),
-// 32-deep slabs, four in the LDS ring (128 KB).
+// 64-deep slabs, two in the LDS ring (128 KB).
 using CB = B16Cfg<256, 256, 2, 64, 2>;
 constexpr int B16_ROWS = CB::RA;   // rows per row tile of the bf16 kernels
 
@@ -495,7 +500,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
           const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
           f32x4_t h;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm(ag[r]) * u[r];
+          for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm_fast(ag[r]) * u[r];
           SG::put4(sg, c.row, deinter(c.col4), h);
         }
     barrier_lds_writes();
@@ -554,7 +559,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
           f32x4_t dg, du;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float sg = sigm(ag[r]);
+            const float sg = sigm_fast(ag[r]);
             du[r] = dh[r] * ag[r] * sg;
             dg[r] = dh[r] * u[r] * sg * (1.0f + ag[r] * (1.0f - sg));
           }

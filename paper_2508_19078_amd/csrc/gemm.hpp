@@ -222,8 +222,8 @@ template <> __device__ __forceinline__ AccCoord quad_coord<float>(int g) { retur
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void store4(bf16* p, f32x4_t v) {
   u32x2_t o;
-  o[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-  o[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+  o[0] = pk_bf16(v[0], v[1]);
+  o[1] = pk_bf16(v[2], v[3]);
   *(FM_GLOBAL u32x2_t*)(p) = o;
 }
 __device__ __forceinline__ void store4(float* p, f32x4_t v) { *(FM_GLOBAL f32x4_t*)(p) = v; }

@@ -8,24 +8,29 @@
 // groups of four consecutive output columns.
 //
 // * Tiles go straight from global memory to LDS (global_load_lds_dwordx4: each
-//   lane moves 16 bytes to LDS base + 16 * lane), NS slabs of BK k in a ring:
-//   up to NS - 1 slabs are in flight while one is multiplied.  Per-lane
-//   addresses are resolved once per tile; a slab only adds a uniform stride.
+//   lane moves 16 bytes to LDS base + 16 * lane), NS slabs of 64 k in a ring.
+//   Per-lane offsets are resolved once per tile; a slab only advances uniform
+//   bases held in scalar registers.
+// * Every DMA instruction fetches 64 bytes from each of 16 rows, and the next
+//   instruction of the same wave fetches the other 64 bytes of the same 128-byte
+//   lines.  Measured on the chip, this pairing moves about twice as many bytes
+//   per clock from L2 into LDS as instructions that fetch whole lines.
+// * K-contiguous slabs are stored as two halves [R rows][32 k] (64-byte rows),
+//   the 16-byte chunk index XOR-swizzled by (row >> 2) & 3 so that the fragment
+//   reads of 16 consecutive rows hit 16 distinct 4-bank groups.
+// * MN-contiguous slabs (weights in the NN products, both operands of the
+//   weight-gradient products) are stored as R/32 column blocks [64 k][32 rows]
+//   and read with ds_read_b64_tr_b16, which hands each lane four k-consecutive
+//   elements of one row; two such reads form a fragment, so nothing is
+//   transposed on the way in.  A 32-lane read touches four 64-byte k-rows, 32
+//   bytes of each, which already covers the 64 banks once.
 // * Fragments are read one 16-k step ahead of the MFMAs that use them, into a
 //   second register set; at the end of a slab the read-ahead crosses into the
 //   next slab right after the barrier that publishes it.  LDS reads thus
 //   overlap the MFMAs of the same wave, not only those of the other wave.
-// * K-contiguous tiles are stored [row][BK k] with the 16-byte chunk index
-//   XOR-swizzled by a function of the row, so that the fragment reads of 16
-//   consecutive rows hit 16 distinct 4-bank groups.
-// * MN-contiguous tiles (weights in the NN products, both operands of the
-//   weight-gradient products) are stored k-major, [BK k][R rows], with the chunk
-//   index XOR-swizzled by (k & 3) << 2, and read with ds_read_b64_tr_b16, which
-//   hands each lane four k-consecutive elements of one row; two such reads form
-//   a fragment, so nothing is transposed on the way in.
 // * An operand may interleave two matrices in 32-row blocks (gate and up
 //   weights; the two dSwiGLU gradients), so that the pairs the epilogue needs sit
-//   in one lane.
+//   in one lane.  A DMA instruction always stays inside one 32-row block.
 // * Rows past the operand's extent read a clamped (valid) address and only feed
 //   outputs that are never stored; k past K is zeroed in the A fragments of the
 //   last slab, so the clamped B data meets zeros.
@@ -55,7 +60,7 @@ template <int RA_, int RB_, int WM_, int BK_, int NS_> struct B16Cfg {
   static constexpr int A_INS = RA * BK * 2 / 8192;    // DMA instructions per wave and slab
   static constexpr int B_INS = RB * BK * 2 / 8192;
   static_assert(WM * WN == 8 && TM % 32 == 0 && TN % 32 == 0, "8 waves of 32-multiples");
-  static_assert(BK == 32 || BK == 64, "slab depth");
+  static_assert(BK == 64, "slab depth: two 32-k halves per slab");
   static_assert(A_INS >= 1 && B_INS >= 1 && KS % 2 == 0, "whole DMA instructions per wave");
   static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS ring");
 };
@@ -124,19 +129,9 @@ __device__ __forceinline__ void dma16s(const void* base, uint32_t off, FM_LDS vo
 // Wave index as a uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-// K-contiguous rows hold BK / 8 chunks of 16 bytes.  A fragment read of 16
-// consecutive rows at one chunk must spread over the 16 4-bank groups of a
-// 256-byte bank period: with 128-byte rows the row parity picks the half and
-// (row >> 1) & 7 the chunk; with 64-byte rows row & 3 picks the quarter and
-// (row >> 2) & 3 the chunk.
-template <int BK> __device__ __forceinline__ int swz_kc(int row) {
-  return BK == 64 ? (row >> 1) & 7 : (row >> 2) & 3;
-}
-// A transposed read of one 16-lane group touches 4 k-rows and 2 adjacent
-// chunks; the two groups served together (rows +16) touch the next 2 chunks.
-// Moving k & 3 into bits 2-3 of the chunk position spreads the 4 x 4 chunk
-// reads of the pair over 16 positions (all 64 banks).
-__device__ __forceinline__ int swz_mn(int k) { return (k & 3) << 2; }
+// Chunk swizzle of a K-contiguous half-slab row (4 chunks of 16 bytes): 16
+// consecutive rows at one logical chunk land on 16 distinct 4-bank groups.
+__device__ __forceinline__ int swz_kc(int row) { return (row >> 2) & 3; }
 
 // One operand of the bf16 core: logical [R rows][K].  Element (r, k) lives at
 // p[r * ld + k] (K-contiguous) or p[k * ld + r] (MN-contiguous), relative to
@@ -161,69 +156,75 @@ __device__ __forceinline__ const bf16* b16_row(const B16Src& s, int r, int& pr) 
   return s.p;
 }
 
-// Direct-to-LDS loading of one R-row operand: a slab is R * BK * 2 / 1024
-// blocks of 1 KB, NI of them per wave.  Each instruction takes a uniform base
-// (scalar registers) plus a 32-bit per-lane offset, so a slab only advances
-// the base.  An MN-contiguous operand that interleaves two matrices mixes both
-// within one instruction and keeps full per-lane pointers instead (V64).
-template <bool KC, int R, int BK, int NI, bool INTER> struct B16Dma {
-  static constexpr int CPK = BK / 8;   // 16-byte chunks per K-contiguous row
-  static constexpr int CPM = R / 8;    // 16-byte chunks per MN-contiguous k-row
-  static constexpr int RPI = 64 / CPK; // K-contiguous rows per instruction
-  static constexpr bool V64 = !KC && INTER;
-  const char* base[V64 ? 1 : NI];      // uniform
-  uint32_t off[V64 ? 1 : NI];          // per lane
-  const char* ptr[V64 ? NI : 1];       // per lane (V64)
+// Direct-to-LDS loading of one R-row operand: a slab is R * 128 bytes, R / 8
+// instructions of 1 KB, NI = R / 64 per wave.  Instruction `ins` moves:
+//   KC: rows 16 (ins / 2) + [0, 16), k-half ins % 2 (32 k), to half
+//       ins % 2 at row 16 (ins / 2);
+//   MN: k-rows 16 (ins / CB) + [0, 16) of a column block (32 rows), to that
+//       block's k-rows; CB = R / 32 column blocks.
+// Consecutive instructions of a wave cover the two 64-byte halves of the same
+// 16 lines.  Each takes a uniform 64-bit base plus a 32-bit per-lane offset.
+template <bool KC, int R, int NI, bool INTER> struct B16Dma {
+  static constexpr int CB = R / 32;
+  const char* base[NI];      // uniform
+  uint32_t off[NI];          // per lane
   size_t step;
 
-  // Source of the chunk that lane `lane` moves in DMA instruction `ins` of
-  // slab 0: a = row, b = first k (KC); a = k-row, b = first row (MN).
-  __device__ __forceinline__ void chunk(int ins, int lane, int& a, int& b) const {
+  // Column block of an MN instruction.  With two interleaved matrices the
+  // blocks of one matrix alternate, so consecutive instructions take blocks
+  // c and c + 2 (the two halves of the same lines): 0, 2, 1, 3, 4, 6, 5, 7, ...
+  __device__ __forceinline__ static int cblk(int ins) {
+    const int c = ins % CB;
+    return INTER ? (c & ~3) | ((c & 1) << 1) | ((c >> 1) & 1) : c;
+  }
+  // The 32-row block an instruction reads (uniform), and its matrix.
+  __device__ __forceinline__ static int block_of(int ins) { return KC ? (ins >> 1) >> 1 : cblk(ins); }
+  __device__ __forceinline__ static const bf16* matrix(const B16Src& s, int ins) {
+    return (INTER && (block_of(ins) & 1)) ? s.p2 : s.p;
+  }
+  // Physical row (within its matrix) of logical row r.
+  __device__ __forceinline__ static int phys_row(int r) { return INTER ? 32 * (r >> 6) + (r & 31) : r; }
+
+  // Lane's source in slab 0: KC (row, k), MN (k-row, first row).
+  __device__ __forceinline__ static void chunk(int ins, int lane, int& a, int& b) {
     if (KC) {
-      a = ins * RPI + lane / CPK;
-      b = 8 * ((lane % CPK) ^ swz_kc<BK>(a));
+      a = 16 * (ins >> 1) + (lane >> 2);
+      b = 32 * (ins & 1) + 8 * ((lane & 3) ^ swz_kc(a));
     } else {
-      a = ins * (64 / CPM) + lane / CPM;
-      b = 8 * ((lane % CPM) ^ swz_mn(a));
+      a = 16 * (ins / CB) + (lane >> 2);
+      b = 32 * cblk(ins) + 8 * (lane & 3);
     }
   }
-  // Matrix of a K-contiguous instruction's rows (all in one 32-row block).
-  __device__ __forceinline__ static const bf16* kc_matrix(const B16Src& s, int ins) {
-    return (INTER && (((ins * RPI) >> 5) & 1)) ? s.p2 : s.p;
+  __device__ __forceinline__ static uint32_t lane_off(const B16Src& s, int ins, int lane, int k0) {
+    int a, b;
+    chunk(ins, lane, a, b);
+    if (KC) {
+      // K - 8 >= k0: both are multiples of 8 and the slab starts below K
+      return (uint32_t)(((size_t)min(phys_row(a), s.rows - 1) * s.ld + min(b, s.K - 8 - k0)) * 2);
+    }
+    return (uint32_t)(((size_t)min(a, s.K - 1 - k0) * s.ld + min(phys_row(b), s.rows - 8)) * 2);
   }
-  __device__ __forceinline__ static int phys_row(int r) { return INTER ? 32 * (r >> 6) + (r & 31) : r; }
 
   __device__ __forceinline__ void init(const B16Src& s) {
     const int lane = lane_id(), wave = wave_id();
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
       const int ins = wave * NI + u;
-      int a, b;
-      chunk(ins, lane, a, b);
-      if (V64) {
-        int pr;
-        const bf16* m = b16_row(s, b, pr);
-        ptr[u] = (const char*)(m + (size_t)a * s.ld + min(pr, s.rows - 8));
-      } else if (KC) {
-        base[u] = (const char*)kc_matrix(s, ins);
-        off[u] = (uint32_t)(((size_t)min(phys_row(a), s.rows - 1) * s.ld + b) * 2);
-      } else {
-        base[u] = (const char*)s.p;
-        off[u] = (uint32_t)(((size_t)a * s.ld + min(b, s.rows - 8)) * 2);
-      }
+      base[u] = (const char*)matrix(s, ins);
+      off[u] = lane_off(s, ins, lane, 0);
     }
-    step = KC ? (size_t)BK * 2 : (size_t)BK * s.ld * 2;
+    step = KC ? (size_t)64 * 2 : (size_t)64 * s.ld * 2;
+  }
+
+  __device__ __forceinline__ static int lds_block(int ins) {
+    return KC ? (ins & 1) * (R / 16) + (ins >> 1) : cblk(ins) * 4 + ins / CB;
   }
 
   __device__ __forceinline__ void issue_full(int slab, FM_LDS char* tile) const {
     const int wave = wave_id();
     const size_t adv = step * (size_t)slab;
 #pragma unroll
-    for (int u = 0; u < NI; ++u) {
-      FM_LDS char* dst = tile + (wave * NI + u) * 1024;
-      if (V64) dma16(ptr[u] + adv, dst);
-      else dma16s(base[u] + adv, off[u], dst);
-    }
+    for (int u = 0; u < NI; ++u) dma16s(base[u] + adv, off[u], tile + lds_block(wave * NI + u) * 1024);
   }
 
   // A slab that reaches past K: k is clamped to the last valid element.
@@ -232,21 +233,9 @@ template <bool KC, int R, int BK, int NI, bool INTER> struct B16Dma {
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
       const int ins = wave * NI + u;
-      FM_LDS char* dst = tile + ins * 1024;
-      int a, b;
-      chunk(ins, lane, a, b);
-      if (V64) {
-        int pr;
-        const bf16* m = b16_row(s, b, pr);
-        dma16(m + (size_t)min(k0 + a, s.K - 1) * s.ld + min(pr, s.rows - 8), dst);
-      } else if (KC) {
-        // K - 8 >= k0: both are multiples of 8 and the slab starts below K
-        const char* bt = (const char*)(kc_matrix(s, ins) + k0);
-        dma16s(bt, (uint32_t)(((size_t)min(phys_row(a), s.rows - 1) * s.ld + min(b, s.K - 8 - k0)) * 2), dst);
-      } else {
-        const char* bt = (const char*)(s.p + (size_t)k0 * s.ld);
-        dma16s(bt, (uint32_t)(((size_t)min(a, s.K - 1 - k0) * s.ld + min(b, s.rows - 8)) * 2), dst);
-      }
+      const bf16* m = matrix(s, ins);
+      const char* bt = (const char*)(KC ? m + k0 : m + (size_t)k0 * s.ld);
+      dma16s(bt, lane_off(s, ins, lane, k0), tile + lds_block(ins) * 1024);
     }
   }
 };
@@ -254,10 +243,10 @@ template <bool KC, int R, int BK, int NI, bool INTER> struct B16Dma {
 // MFMA fragments of a wave's NB 32-row blocks of an R-row tile: a fragment is
 // 32 rows x 16 k, 8 k per lane: lane l holds row r0 + l % 32 and k
 // 16 ks + 8 (l / 32) + 0..7 of the slab.  Offsets are per lane, computed once:
-// for K-contiguous tiles the k-step only flips bits 5-6 of the offset (the
-// chunk index is 2 ks + l / 32 and the swizzle XORs it), for MN-contiguous
-// tiles it adds 16 k-rows.
-template <bool KC, int R, int BK, int NB> struct B16Frag {
+// for K-contiguous slabs k-step ks lies in half ks / 2 and flips bit 5 of the
+// offset (the chunk index is 2 (ks % 2) + l / 32 and the swizzle XORs it); for
+// MN-contiguous slabs it adds 16 k-rows.
+template <bool KC, int R, int NB> struct B16Frag {
   uint32_t off[NB];
 
   __device__ __forceinline__ void init(int row0) {
@@ -267,29 +256,28 @@ template <bool KC, int R, int BK, int NB> struct B16Frag {
       const int r0 = row0 + i * 32;
       if (KC) {
         const int r = r0 + (lane & 31);
-        off[i] = (uint32_t)(r * (BK * 2) + (((lane >> 5) ^ swz_kc<BK>(r)) << 4));
+        off[i] = (uint32_t)(r * 64 + (((lane >> 5) ^ swz_kc(r)) << 4));
       } else {
         // ds_read_b64_tr_b16: in each 16-lane group, output lane i element j
         // comes from the address of lane 4j + i/4, offset i % 4.  Group g covers
         // rows r0 + 16 (g & 1) + [0, 16) and k 8 (g >> 1) + [0, 8) of the k-step;
         // lane L of the group points at (k = kbase + L/4, row = rbase + 4 (L % 4)).
-        // The swizzle depends only on k & 3, which the k-step (16 ks) and the
-        // half (4 h) leave unchanged: those enter as constant offsets.
         const int g = lane >> 4, L = lane & 15;
         const int n = r0 + 16 * (g & 1) + 4 * (L & 3);
         const int k = 8 * (g >> 1) + (L >> 2);
-        off[i] = (uint32_t)(k * (R * 2) + (((n >> 3) ^ swz_mn(k)) << 4) + ((n >> 2) & 1) * 8);
+        off[i] = (uint32_t)((n >> 5) * (64 * 64) + k * 64 + (n & 31) * 2);
       }
     }
   }
 
   __device__ __forceinline__ bf16x8_t read(const FM_LDS char* tile, int i, int ks) const {
     if (KC) {
-      return __builtin_bit_cast(bf16x8_t, *(const FM_LDS u32x4_t*)(tile + (off[i] ^ (uint32_t)(ks << 5))));
+      const FM_LDS char* p = tile + (ks >> 1) * (R * 64) + (off[i] ^ (uint32_t)((ks & 1) << 5));
+      return __builtin_bit_cast(bf16x8_t, *(const FM_LDS u32x4_t*)p);
     } else {
-      const FM_LDS char* p = tile + off[i] + ks * 16 * (R * 2);
+      const FM_LDS char* p = tile + off[i] + ks * 16 * 64;
       const i16x4_t v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((FM_LDS i16x4_t*)p);
-      const i16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((FM_LDS i16x4_t*)(p + 4 * (R * 2)));
+      const i16x4_t v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((FM_LDS i16x4_t*)(p + 4 * 64));
       const u32x2_t w0 = __builtin_bit_cast(u32x2_t, v0), w1 = __builtin_bit_cast(u32x2_t, v1);
       return __builtin_bit_cast(bf16x8_t, u32x4_t{w0[0], w0[1], w1[0], w1[1]});
     }
@@ -356,8 +344,7 @@ template <typename T, int COLS> struct Stage {
   static __device__ __forceinline__ void put4(FM_LDS char* lds, int row, int col, f32x4_t v) {
     FM_LDS char* p = lds + at(row, col);
     if (sizeof(T) == 2) {
-      *(FM_LDS u32x2_t*)p = u32x2_t{(uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                                    (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16)};
+      *(FM_LDS u32x2_t*)p = u32x2_t{pk_bf16(v[0], v[1]), pk_bf16(v[2], v[3])};
     } else {
       *(FM_LDS f32x4_t*)p = v;
     }
@@ -412,12 +399,12 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
   if (nk <= 0) return;
   const int nfull = K / BK;                    // slabs with no k past K
   const int wave = wave_id();
-  B16Frag<AKC, C::RA, BK, MI> fa;
-  B16Frag<BKC, C::RB, BK, NJ> fb;
+  B16Frag<AKC, C::RA, MI> fa;
+  B16Frag<BKC, C::RB, NJ> fb;
   fa.init((wave % C::WM) * C::TM);
   fb.init((wave / C::WM) * C::TN);
-  B16Dma<AKC, C::RA, BK, C::A_INS, AI> da;
-  B16Dma<BKC, C::RB, BK, C::B_INS, BI> db;
+  B16Dma<AKC, C::RA, C::A_INS, AI> da;
+  B16Dma<BKC, C::RB, C::B_INS, BI> db;
   da.init(A);
   db.init(B);
 

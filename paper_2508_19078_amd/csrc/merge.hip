@@ -117,8 +117,8 @@ __global__ __launch_bounds__(256) void k_merge(const void* const* __restrict__ w
         st16(dst + c * 32 + 16, pack16(acc[u] + 4, (float*)nullptr));
       } else {                        // fp32 in, bf16 out: 4 values = 8 bytes
         uint2 o;
-        o.x = (uint32_t)f2bf(acc[u][0]) | ((uint32_t)f2bf(acc[u][1]) << 16);
-        o.y = (uint32_t)f2bf(acc[u][2]) | ((uint32_t)f2bf(acc[u][3]) << 16);
+        o.x = pk_bf16(acc[u][0], acc[u][1]);
+        o.y = pk_bf16(acc[u][2], acc[u][3]);
         *reinterpret_cast<uint2*>(dst + c * 8) = o;
       }
     }
