@@ -33,8 +33,30 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="deepseek_moe")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-tokens", type=int, default=192)
+    p.add_argument("--cpu-sample-tokens", type=int, default=1024)
+    p.add_argument("--calib-copy", action="store_true",
+                   help="end with a device-to-device copy of 256 MiB (counter calibration)")
     return p.parse_args()
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "grouped_swiglu_deepseek_moe_traffic.md")
+
+
+def measured_traffic(workload):
+    """HBM bytes per step of the grouped SwiGLU fwd+bwd from the committed
+    FETCH_SIZE / WRITE_SIZE summary, or None when it was taken on other kernel
+    sources or another workload."""
+    from paper_2508_19078_amd.rocprof_summary import ffn_source_hash
+    if workload != "deepseek_moe" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and line.split(":")[0] in ("source_sha256", "traffic_bytes"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != ffn_source_hash():
+        return None
+    return float(kv["traffic_bytes"]) if "traffic_bytes" in kv else None
 
 
 def ffn_flops(r, offsets):
@@ -196,12 +218,17 @@ def main():
                    "global_batch": w.T, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "kernel": "grouped SwiGLU fwd+bwd (moe_grouped_swiglu_fwd + _bwd)",
                      "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "frac": round(achieved / peak, 4), "traffic": measured_traffic(a.workload),
                      "flops_per_step": fl_fwd + fl_bwd, "ms": round(ffn_ms, 4)},
         "stages_ms": {k: round(v, 4) for k, v in per.items()},
         "hbm_kernels_GBps": {"route": gbs(route_bytes, per["route"]), "profile": gbs(hist_bytes, per["profile"]),
                              "merge": gbs(merge_bytes, per["merge"]), "permute": gbs(permute_bytes, per["permute"])},
     }
+    if a.calib_copy:
+        src = torch.ones(128 << 20, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
     if not a.no_cpu_baseline:
         print("# timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, a.cpu_sample_tokens)

@@ -1,0 +1,126 @@
+"""Text summaries of rocprofv3 CSV output, for the profiles/ folder.
+
+  python -m paper_2508_19078_amd.rocprof_summary stats STATS_CSV --cmd "..." [--top N]
+  python -m paper_2508_19078_amd.rocprof_summary traffic --fetch CSV --write CSV \
+      --cmd-fetch "..." --cmd-write "..." [--calib-bytes B]
+
+``stats`` reads a ``--kernel-trace --stats`` kernel_stats.csv and prints a table
+of the busiest kernels.  ``traffic`` reads two ``--pmc FETCH_SIZE`` /
+``--pmc WRITE_SIZE`` counter_collection.csv files of the same bench command
+(which ends with a device-to-device copy of ``calib_bytes``), scales each counter
+by what it reads for that copy, and prints the HBM bytes per step of the grouped
+SwiGLU forward + backward, with a hash of the kernel sources the counters were
+taken on (bench.py reports the traffic only while the sources still match).
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import hashlib
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+
+# The kernels of moe_grouped_swiglu_fwd + moe_grouped_swiglu_bwd (bf16 path).
+FFN_KERNELS = ("k_build_sched", "kb_gate_up", "kb_down", "kb_dh", "kb_dx", "kb_dw_gu", "kb_dw_d")
+# Sources those kernels are built from.
+FFN_SOURCES = ("csrc/ffn.hip", "csrc/gemm_bf16.hpp", "csrc/gemm.hpp", "csrc/common.hpp")
+CALIB_KERNEL = "copyBuffer"
+
+
+def ffn_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in FFN_SOURCES:
+        with open(os.path.join(PKG, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def short_name(n: str) -> str:
+    n = n.replace("fm::(anonymous namespace)::", "").replace("void ", "")
+    return n.split("(")[0]
+
+
+def stats_table(path: str, top: int) -> str:
+    rows = list(csv.DictReader(open(path)))
+    out = ["| kernel | calls | avg µs | total ms | % |", "|---|---|---|---|---|"]
+    for r in rows[:top]:
+        out.append(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                   f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['Percentage']):.1f} |")
+    ffn = [r for r in rows if short_name(r["Name"]) in FFN_KERNELS]
+    if ffn:
+        steps = max(int(r["Calls"]) for r in ffn if short_name(r["Name"]) == "kb_gate_up")
+        tot = sum(float(r["TotalDurationNs"]) for r in ffn) / steps / 1e3
+        out.append("")
+        out.append(f"grouped SwiGLU fwd+bwd kernels per step (sum of averages over {steps} steps): {tot:.1f} µs")
+    return "\n".join(out)
+
+
+def counter_per_kernel(path: str, counter: str):
+    """{kernel: [value per dispatch]} for one counter (KiB for *_SIZE)."""
+    per = collections.defaultdict(dict)
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        per[short_name(r["Kernel_Name"])][r["Dispatch_Id"]] = \
+            per[short_name(r["Kernel_Name"])].get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    return {k: list(v.values()) for k, v in per.items()}
+
+
+def traffic(fetch_csv: str, write_csv: str, calib_bytes: int):
+    res = {}
+    for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        per = counter_per_kernel(path, name)
+        calib = [v for k, vs in per.items() if CALIB_KERNEL in k for v in vs]
+        if not calib:
+            raise SystemExit(f"no {CALIB_KERNEL} dispatch in {path}")
+        kib = max(calib)
+        factor = (calib_bytes / 1024.0) / kib
+        steps = len(per.get("kb_gate_up", []))
+        raw = sum(sum(per.get(k, [])) for k in FFN_KERNELS) / max(steps, 1)
+        res[name] = {"calib_kib": kib, "factor": factor, "steps": steps, "kib_per_step": raw,
+                     "bytes_per_step": raw * 1024.0 * factor,
+                     "per_kernel_kib": {k: sum(per.get(k, [])) / max(steps, 1) for k in FFN_KERNELS}}
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="what", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    s.add_argument("--cmd", required=True)
+    s.add_argument("--top", type=int, default=16)
+    t = sub.add_parser("traffic")
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--cmd-fetch", required=True)
+    t.add_argument("--cmd-write", required=True)
+    t.add_argument("--calib-bytes", type=int, default=256 << 20)
+    a = ap.parse_args()
+    if a.what == "stats":
+        print(f"command: `{a.cmd}`\n")
+        print(stats_table(a.csv, a.top))
+        return
+    r = traffic(a.fetch, a.write, a.calib_bytes)
+    f, w = r["FETCH_SIZE"], r["WRITE_SIZE"]
+    print(f"commands:\n- `{a.cmd_fetch}`\n- `{a.cmd_write}`\n")
+    print(f"Calibration: a device-to-device copy of {a.calib_bytes} bytes reads FETCH_SIZE "
+          f"{f['calib_kib']:.0f} KiB (factor {f['factor']:.4f}) and WRITE_SIZE {w['calib_kib']:.0f} KiB "
+          f"(factor {w['factor']:.4f}).\n")
+    print("| kernel | FETCH KiB/step | WRITE KiB/step |")
+    print("|---|---|---|")
+    for k in FFN_KERNELS:
+        print(f"| {k} | {f['per_kernel_kib'][k]:.0f} | {w['per_kernel_kib'][k]:.0f} |")
+    total = f["bytes_per_step"] + w["bytes_per_step"]
+    print(f"\nHBM traffic of the grouped SwiGLU fwd+bwd per step (scaled): fetch {f['bytes_per_step']:.4g} B, "
+          f"write {w['bytes_per_step']:.4g} B, total {total:.4g} B.\n")
+    print("```")
+    print(f"source_sha256: {ffn_source_hash()}")
+    print(f"traffic_bytes: {total:.0f}")
+    print("```")
+
+
+if __name__ == "__main__":
+    main()
