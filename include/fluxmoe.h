@@ -22,7 +22,10 @@
  *           call), MOE_I8 for quantised codes.  Index arrays are int32,
  *           gates and scales fp32.  bf16 math accumulates in fp32.
  * Limits.   1 <= k <= min(E, 16), 1 <= E <= 256, d % 8 == 0, I % 8 == 0,
- *           T >= 0 (T == 0 is a no-op), routed slots <= 512, shared <= 511.  Anything else:
+ *           T >= 0, routed slots <= 512, shared <= 511.  T == 0 enqueues nothing and
+ *           per-token buffers may then be NULL (moe_permute still zeroes the
+ *           offsets; moe_grouped_swiglu_bwd still writes zero weight
+ *           gradients unless accumulating).  Anything else:
  *           MOE_ERR_UNSUPPORTED or MOE_ERR_ARG.
  * Errors.   Every function returns MOE_OK or an error code.  Arguments are
  *           validated on the host before any HIP call, so an invalid call

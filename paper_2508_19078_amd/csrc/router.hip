@@ -339,10 +339,10 @@ extern "C" int moe_route_topk(const void* X, const void* Wr, int dtype, const fl
   clear_error();
   FM_TRY(check_route_shape(T, d, E, k));
   FM_TRY(need_dtype_float(dtype, "dtype"));
+  if (T == 0) return MOE_OK;
   FM_TRY(need(X, "X")); FM_TRY(need(Wr, "Wr")); FM_TRY(need(idx, "idx")); FM_TRY(need(gate, "gate"));
   FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(Wr, "Wr")); FM_TRY(need_aligned(bias, "bias"));
   FM_TRY(need_aligned(idx, "idx")); FM_TRY(need_aligned(gate, "gate")); FM_TRY(need_aligned(logits, "logits"));
-  if (T == 0) return MOE_OK;
   hipStream_t st = as_stream(stream);
   if (dtype == MOE_BF16)
     return launch_route<bf16, bf16, 0>((const bf16*)X, (const bf16*)Wr, nullptr, bias, T, d, E, k,
@@ -374,10 +374,10 @@ extern "C" int moe_profile_hist(const void* X, int x_dtype, const int8_t* Wq, co
   clear_error();
   FM_TRY(check_route_shape(T, d, E, k));
   FM_TRY(need_dtype_float(x_dtype, "x_dtype"));
+  if (T == 0) return MOE_OK;
   FM_TRY(need(X, "X")); FM_TRY(need(Wq, "Wq")); FM_TRY(need(scale, "scale")); FM_TRY(need(counts, "counts"));
   FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(Wq, "Wq")); FM_TRY(need_aligned(scale, "scale"));
   FM_TRY(need_aligned(bias, "bias")); FM_TRY(need_aligned(counts, "counts")); FM_TRY(need_aligned(idx, "idx"));
-  if (T == 0) return MOE_OK;
   hipStream_t st = as_stream(stream);
   if (x_dtype == MOE_BF16)
     return launch_route<bf16, int8_t, 1>((const bf16*)X, Wq, scale, bias, T, d, E, k, idx, nullptr,

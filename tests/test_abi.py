@@ -66,9 +66,16 @@ def test_route_rejections(L):
     # unsupported dtype (int8 activations)
     rc, _ = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_I8, None, 16, 64, 8, 2, FAKE, FAKE, None, None)
     assert rc == api.MOE_ERR_UNSUPPORTED
-    # T == 0 is a no-op that touches nothing
+    # T == 0 is a no-op that touches nothing; per-token buffers may be NULL
     rc, _ = rc_and_msg(L, "moe_route_topk", FAKE, FAKE, api.MOE_BF16, None, 0, 64, 8, 2, FAKE, FAKE, None, None)
     assert rc == api.MOE_OK
+    rc, _ = rc_and_msg(L, "moe_route_topk", None, None, api.MOE_BF16, None, 0, 64, 8, 2, None, None, None, None)
+    assert rc == api.MOE_OK
+    rc, _ = rc_and_msg(L, "moe_profile_hist", None, api.MOE_BF16, None, None, None, 0, 64, 8, 2, None, None, None)
+    assert rc == api.MOE_OK
+    # ... but the shape is still validated
+    rc, _ = rc_and_msg(L, "moe_route_topk", None, None, api.MOE_BF16, None, 0, 64, 8, 9, None, None, None, None)
+    assert rc != api.MOE_OK
 
 
 def test_profile_and_merge_rejections(L):

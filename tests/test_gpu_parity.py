@@ -1,7 +1,7 @@
 """HIP path vs the fp64 oracle, element by element, on shapes the oracle
-finishes in seconds: several 128-row tiles, ragged row counts, N and K tails
-(I = 200 and 688), merged and frozen slots, a shared expert, and the fp32
-workload.  Everything goes through the C ABI."""
+finishes in seconds: several row tiles per slot, ragged row counts, N and K
+tails (I = 200, 384 and 688), merged and frozen slots, a shared expert, and the
+fp32 workload.  Everything goes through the C ABI."""
 import numpy as np
 import pytest
 import torch

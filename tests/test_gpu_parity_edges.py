@@ -1,0 +1,191 @@
+"""Degenerate and limit cases of the hot path against the fp64 oracle, through
+the C ABI: every token on one expert (the other slots empty), k = E, a single
+token, all logits equal (including -0.0 against +0.0), a merged group none of
+whose experts is activated (Eq. 2 falls back to the mean), the router at its
+limits (E = 256, k = 16), empty calls, and bit-for-bit determinism of a whole
+step."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2508_19078_amd import api
+from paper_2508_19078_amd import workloads as W
+from paper_2508_19078_amd.layer import LayerInputs, MoELayerRunner
+
+from gpu_harness import GAP, TOL_FFN, TOL_MERGE, OracleLayer, compare_topk, host, log, rel_fro, rne_bf16
+
+pytestmark = pytest.mark.gpu
+
+BASE = W.LayerWorkload(name="edge", cid=201, T=300, d=128, E=8, k=2, I=192, dtype="bf16",
+                       merge=("groups", ((6, 7),)))
+
+
+def with_bias(inp, bias):
+    inp.bias = np.asarray(bias, dtype=np.float32)
+    return inp
+
+
+def zero_x(inp):
+    x = inp.X
+    inp.X = W.Tensor(np.zeros_like(x.store), x.dtype, x.shape)
+    return inp
+
+
+def edge_cases():
+    E = BASE.E
+    one = np.full(E, -30.0, dtype=np.float32)
+    one[3] = 30.0
+    cold = np.zeros(E, dtype=np.float32)
+    cold[6:] = -60.0                      # experts 6 and 7 never selected
+    tie = np.zeros(E, dtype=np.float32)
+    tie[1::2] = -0.0
+    return {
+        "one_expert": (W.scaled(BASE, name="one_expert", cid=202, k=1), lambda i: with_bias(i, one)),
+        "k_equals_E": (W.scaled(BASE, name="k_equals_E", cid=203, k=E), None),
+        "single_token": (W.scaled(BASE, name="single_token", cid=204, T=1), None),
+        "all_ties": (W.scaled(BASE, name="all_ties", cid=205), lambda i: with_bias(zero_x(i), tie)),
+        "cold_group": (W.scaled(BASE, name="cold_group", cid=206, k=2), lambda i: with_bias(i, cold)),
+    }
+
+
+CASES = edge_cases()
+
+
+class EdgeRun:
+    def __init__(self, name):
+        w, mod = CASES[name]
+        log(f"edge {name}: T={w.T} d={w.d} E={w.E} k={w.k} I={w.I}")
+        inp = LayerInputs(w)
+        if mod is not None:
+            inp = mod(inp)
+        self.w, self.name = w, name
+        self.ref = ref = OracleLayer(w, inp)
+        r = MoELayerRunner(w, inp)
+        self.r = r
+        r.profile()
+        api.moe_route_topk(r.X, r.Wr, r.bias, w.k, r.idx, r.gate, r.logits)
+        self.idx_g, self.gate_g, self.logits_g = host(r.idx), host(r.gate), host(r.logits)
+        self.counts_g = host(r.counts)
+        r.merge(counts=torch.from_numpy(ref.counts.astype(np.int32)).cuda())
+        r.forward(idx=torch.from_numpy(ref.idx.astype(np.int32)).cuda(),
+                  gate=torch.from_numpy(ref.gate.astype(np.float32)).cuda())
+        r.backward(dgate=True)
+        torch.cuda.synchronize()
+
+
+_runs = {}
+
+
+@pytest.fixture(params=list(CASES))
+def run(request):
+    if request.param not in _runs:
+        _runs[request.param] = EdgeRun(request.param)
+    return _runs[request.param]
+
+
+def test_edge_routing(run):
+    ref, w = run.ref, run.w
+    if run.name == "all_ties":
+        # every logit equal: the lowest indices win, gates uniform
+        np.testing.assert_array_equal(run.idx_g, np.tile(np.arange(w.k), (w.T, 1)))
+        np.testing.assert_allclose(run.gate_g, 1.0 / w.k, rtol=1e-6)
+        np.testing.assert_array_equal(ref.idx, run.idx_g)
+        np.testing.assert_array_equal(run.counts_g, ref.counts)
+        return
+    excl, bad = compare_topk(run.idx_g, run.logits_g, ref.idx, ref.logits, w.k)
+    assert bad == 0 and excl <= 1
+    np.testing.assert_array_equal(run.counts_g, ref.counts)
+    if run.name == "k_equals_E":
+        sm = np.exp(ref.logits - ref.logits.max(1, keepdims=True))
+        sm /= sm.sum(1, keepdims=True)
+        np.testing.assert_allclose(np.take_along_axis(sm, run.idx_g, 1), run.gate_g, rtol=1e-5, atol=1e-7)
+
+
+def test_edge_merge(run):
+    ref, r = run.ref, run.r
+    np.testing.assert_array_equal(host(r.expert_map), ref.plan.expert_map)
+    for g in range(len(ref.plan.groups)):
+        for got, exact in zip((r.Mg[g], r.Mu[g], r.Md[g]), ref.merged[g]):
+            assert rel_fro(host(got), rne_bf16(exact)) <= TOL_MERGE
+    if run.name == "cold_group":
+        assert ref.counts[6] == 0 and ref.counts[7] == 0
+        mean = 0.5 * (host(r.Wg[6]) + host(r.Wg[7]))
+        assert rel_fro(host(r.Mg[0]), rne_bf16(mean)) <= TOL_MERGE
+
+
+def test_edge_forward_backward(run):
+    ref, r = run.ref, run.r
+    Y = ref.forward()
+    dX, dW, dgate = ref.backward()
+    e_y, e_dx = rel_fro(host(r.Y), Y), rel_fro(host(r.dX), dX)
+    slots = r.tuning_slots
+    got = np.concatenate([np.concatenate([host(r.dWg[i]).ravel(), host(r.dWu[i]).ravel(), host(r.dWd[i]).ravel()])
+                          for i in range(len(slots))])
+    exp = np.concatenate([np.concatenate([dW[s][0].ravel(), dW[s][1].ravel(), dW[s][2].ravel()]) for s in slots])
+    e_dw = rel_fro(got, exp)
+    log(f"{run.name}: Y {e_y:.2e} dX {e_dx:.2e} dW {e_dw:.2e}")
+    assert e_y <= TOL_FFN and e_dx <= TOL_FFN and e_dw <= TOL_FFN
+    for i, s in enumerate(slots):                 # slots without rows: exactly zero
+        if all(np.all(a == 0) for a in dW[s]):
+            assert not r.dWg[i].any() and not r.dWu[i].any() and not r.dWd[i].any()
+    if run.name == "one_expert":
+        offs = host(r.offsets)
+        assert (np.diff(offs) > 0).sum() == 1 and offs[-1] == run.w.T
+
+
+def test_router_limits():
+    """E = 256 experts, k = 16: the largest router the ABI accepts."""
+    w = W.LayerWorkload(name="router_max", cid=207, T=777, d=256, E=256, k=16, I=64, dtype="bf16",
+                        bias_kind="normal", bias_var=1.0)
+    inp = LayerInputs(w, with_experts=False)
+    ref = OracleLayer(w, inp, with_ffn_weights=False)
+    X, Wr = W.to_torch(inp.X, "cuda"), W.to_torch(inp.Wr, "cuda")
+    bias = torch.from_numpy(inp.bias).cuda()
+    idx = torch.empty(w.T, w.k, dtype=torch.int32, device="cuda")
+    gate = torch.empty(w.T, w.k, dtype=torch.float32, device="cuda")
+    logits = torch.empty(w.T, w.E, dtype=torch.float32, device="cuda")
+    api.moe_route_topk(X, Wr, bias, w.k, idx, gate, logits)
+    Wq = torch.empty(w.E, w.d, dtype=torch.int8, device="cuda")
+    sc = torch.empty(w.E, dtype=torch.float32, device="cuda")
+    counts = torch.zeros(w.E, dtype=torch.int32, device="cuda")
+    api.moe_quantize_int8(Wr, Wq, sc)
+    api.moe_profile_hist(X, Wq, sc, bias, w.k, counts)
+    excl, bad = compare_topk(host(idx), host(logits), ref.idx, ref.logits, w.k)
+    assert bad == 0 and excl <= 2
+    c = host(counts)
+    assert c.sum() == w.T * w.k
+    excl8 = O.topk_gap(ref.logits8, w.k) < GAP
+    adj = np.bincount(ref.idx8[excl8].ravel(), minlength=w.E)
+    assert np.abs(c - ref.counts).sum() <= 2 * adj.sum()
+
+
+def test_empty_calls_launch_nothing():
+    """T = 0 is a no-op for every per-token entry point (outputs untouched)."""
+    d, E, k = 64, 8, 2
+    X = torch.empty(0, d, dtype=torch.bfloat16, device="cuda")      # T = 0 (may have no storage)
+    Wr = torch.zeros(E, d, dtype=torch.bfloat16, device="cuda")
+    idx = torch.full((1, k), -7, dtype=torch.int32, device="cuda")
+    gate = torch.full((1, k), -7.0, dtype=torch.float32, device="cuda")
+    assert api.moe_route_topk(X, Wr, None, k, idx, gate, None) == 0
+    Wq = torch.zeros(E, d, dtype=torch.int8, device="cuda")
+    sc = torch.ones(E, dtype=torch.float32, device="cuda")
+    counts = torch.full((E,), 5, dtype=torch.int32, device="cuda")
+    assert api.moe_profile_hist(X, Wq, sc, None, k, counts) == 0
+    torch.cuda.synchronize()
+    assert (host(idx) == -7).all() and (host(counts) == 5).all()
+
+
+def test_step_is_deterministic():
+    """Two runs of the whole step on the same inputs agree bit for bit."""
+    w = W.scaled(W.WORKLOADS["deepseek_moe"], name="det", cid=208, T=1500, d=256, I=320)
+    inp = LayerInputs(w)
+    outs = []
+    for _ in range(2):
+        r = MoELayerRunner(w, inp)
+        r.step()
+        r.backward(dgate=True)
+        torch.cuda.synchronize()
+        outs.append([host(t) for t in (r.counts, r.idx, r.gate, r.Y, r.dX, r.dgate, r.dWg, r.dWu, r.dWd)])
+    for a, b in zip(*outs):
+        np.testing.assert_array_equal(a, b)
