@@ -424,8 +424,8 @@ __global__ __launch_bounds__(G_THREADS) void kf_dw_d(LayerPtrs<T> W, const T* __
 typedef const bf16* cbp;
 
 // Block tile of every bf16 product: 256 x 256, waves 2 x 4 (128 x 64 each),
-// 64-deep slabs, two in the LDS ring (128 KB).
-using CB = B16Cfg<256, 256, 2, 64, 2>;
+// 64-deep slabs, three of A and two of B in LDS (160 KB).
+using CB = B16Cfg<256, 256, 2, 64, 3, 2>;
 constexpr int B16_ROWS = CB::RA;   // rows per row tile of the bf16 kernels
 
 // Physical index of logical row / column c of an operand that interleaves two

@@ -8,7 +8,8 @@
 // groups of four consecutive output columns.
 //
 // * Tiles go straight from global memory to LDS (global_load_lds_dwordx4: each
-//   lane moves 16 bytes to LDS base + 16 * lane), NS slabs of 64 k in a ring.
+//   lane moves 16 bytes to LDS base + 16 * lane), 64-k slabs in two rings: NSA
+//   slabs of A, NSB = NSA - 1 of B.
 //   Per-lane offsets are resolved once per tile; a slab only advances uniform
 //   bases held in scalar registers.
 // * Every DMA instruction fetches 64 bytes from each of 16 rows, and the next
@@ -49,20 +50,22 @@ typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 // Tile configuration: RA x RB block tile, WM waves along RA, BK k per slab,
-// NS slabs in the LDS ring.
-template <int RA_, int RB_, int WM_, int BK_, int NS_> struct B16Cfg {
-  static constexpr int RA = RA_, RB = RB_, WM = WM_, WN = 8 / WM_, BK = BK_, NS = NS_;
+// separate LDS rings of NSA slabs for A and NSB slabs for B (NSA = NSB + 1: the
+// A operand, the one that streams, gets one more slab of latency tolerance).
+template <int RA_, int RB_, int WM_, int BK_, int NSA_, int NSB_> struct B16Cfg {
+  static constexpr int RA = RA_, RB = RB_, WM = WM_, WN = 8 / WM_, BK = BK_, NSA = NSA_, NSB = NSB_;
   static constexpr int TM = RA / WM, TN = RB / WN;    // wave sub-tile
   static constexpr int MI = TM / 32, NJ = TN / 32;    // MFMA tiles per wave
   static constexpr int KS = BK / 16;                  // MFMA k-steps per slab
-  static constexpr int A_BYTES = RA * BK * 2, STAGE = (RA + RB) * BK * 2;
-  static constexpr int LDS = NS * STAGE;
+  static constexpr int A_BYTES = RA * BK * 2, B_BYTES = RB * BK * 2;
+  static constexpr int B_BASE = NSA * A_BYTES;        // B ring follows the A ring
+  static constexpr int LDS = NSA * A_BYTES + NSB * B_BYTES;
   static constexpr int A_INS = RA * BK * 2 / 8192;    // DMA instructions per wave and slab
   static constexpr int B_INS = RB * BK * 2 / 8192;
   static_assert(WM * WN == 8 && TM % 32 == 0 && TN % 32 == 0, "8 waves of 32-multiples");
   static_assert(BK == 64, "slab depth: two 32-k halves per slab");
   static_assert(A_INS >= 1 && B_INS >= 1 && KS % 2 == 0, "whole DMA instructions per wave");
-  static_assert(NS >= 2 && LDS <= 160 * 1024, "LDS ring");
+  static_assert(NSB >= 2 && NSA == NSB + 1 && LDS <= 160 * 1024, "LDS rings");
 };
 
 // s_waitcnt with only vmcnt limited (expcnt / lgkmcnt left at their maxima).
@@ -124,6 +127,13 @@ __device__ __forceinline__ void dma16s(const void* base, uint32_t off, FM_LDS vo
       : "=&s"(saved)
       : "v"(off), "s"(base), "s"((uint32_t)(uintptr_t)l)
       : "memory");
+}
+
+// Lane index computed where it is used: volatile, so it cannot be hoisted.
+__device__ __forceinline__ int lane_id_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
 }
 
 // Wave index as a uniform (scalar) value.
@@ -220,16 +230,21 @@ template <bool KC, int R, int NI, bool INTER> struct B16Dma {
     return KC ? (ins & 1) * (R / 16) + (ins >> 1) : cblk(ins) * 4 + ins / CB;
   }
 
-  __device__ __forceinline__ void issue_full(int slab, FM_LDS char* tile) const {
+  __device__ __forceinline__ void issue_full(int slab, FM_LDS char* tile) const { issue_part<0, NI>(slab, tile); }
+  // Instructions [U0, U1) of a whole slab (a slab's issue can be spread out).
+  template <int U0, int U1>
+  __device__ __forceinline__ void issue_part(int slab, FM_LDS char* tile) const {
     const int wave = wave_id();
     const size_t adv = step * (size_t)slab;
 #pragma unroll
-    for (int u = 0; u < NI; ++u) dma16s(base[u] + adv, off[u], tile + lds_block(wave * NI + u) * 1024);
+    for (int u = U0; u < U1; ++u) dma16s(base[u] + adv, off[u], tile + lds_block(wave * NI + u) * 1024);
   }
 
-  // A slab that reaches past K: k is clamped to the last valid element.
+  // A slab that reaches past K: k is clamped to the last valid element.  The
+  // lane index is re-read here (opaque to the optimiser), so that these address
+  // computations are not hoisted and kept live through the main loop.
   __device__ __forceinline__ void issue_tail(const B16Src& s, int k0, FM_LDS char* tile) const {
-    const int lane = lane_id(), wave = wave_id();
+    const int lane = lane_id_here(), wave = wave_id();
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
       const int ins = wave * NI + u;
@@ -349,19 +364,20 @@ template <typename T, int COLS> struct Stage {
       *(FM_LDS f32x4_t*)p = v;
     }
   }
-  // Copies rows [0, ROWS) of the staged tile to out[row * ld + col] for
-  // row < rows_valid and col < cols_valid (a multiple of EPC); with
-  // accumulate (float only) the values are added to what out holds.
-  template <int ROWS>
-  static __device__ __forceinline__ void copy_out(const FM_LDS char* lds, T* out, size_t ld, int rows_valid,
-                                                  int cols_valid, bool accumulate = false) {
+  // Copies rows [0, ROWS) of the staged tile out: row r goes to row_ptr(r)
+  // (nullptr: not stored), columns below cols_valid (a multiple of EPC); with
+  // accumulate (float only) the values are added to what the output holds.
+  template <int ROWS, class RowPtr>
+  static __device__ __forceinline__ void copy_rows(const FM_LDS char* lds, RowPtr row_ptr, int cols_valid,
+                                                   bool accumulate = false) {
     constexpr int TOTAL = ROWS * CPR;
 #pragma unroll 4
     for (int idx = threadIdx.x; idx < TOTAL; idx += B16_THREADS) {
       const int row = idx / CPR, c = idx % CPR;
       u32x4_t v = *(const FM_LDS u32x4_t*)(lds + row * ROW_BYTES + ((c ^ (row & (CPR - 1))) << 4));
-      if (row < rows_valid && c * EPC < cols_valid) {
-        T* dst = out + (size_t)row * ld + c * EPC;
+      T* out = row_ptr(row);
+      if (out != nullptr && c * EPC < cols_valid) {
+        T* dst = out + c * EPC;
         if (sizeof(T) == 4 && accumulate) {
           const f32x4_t o = *(const FM_GLOBAL f32x4_t*)dst;
           v = __builtin_bit_cast(u32x4_t, __builtin_bit_cast(f32x4_t, v) + o);
@@ -369,6 +385,13 @@ template <typename T, int COLS> struct Stage {
         st16(dst, v);
       }
     }
+  }
+  // Rows [0, ROWS) to out[row * ld + col] for row < rows_valid.
+  template <int ROWS>
+  static __device__ __forceinline__ void copy_out(const FM_LDS char* lds, T* out, size_t ld, int rows_valid,
+                                                  int cols_valid) {
+    copy_rows<ROWS>(lds, [=](int row) { return row < rows_valid ? out + (size_t)row * ld : (T*)nullptr; },
+                    cols_valid);
   }
 };
 
@@ -381,20 +404,24 @@ __device__ __forceinline__ void barrier_lds_writes() {
 // k loop over [0, K), accumulating into acc.  Ends with a barrier so the LDS
 // can be reused by a following call.
 //
-// Steady state (slab kt, while slab kt + NS is still a whole slab): every
-// k-step but the last reads the next k-step's fragments, then multiplies.  The
-// last k-step multiplies half of its tiles, waits for its own LDS reads and for
-// slab kt + 1 to land, crosses the barrier that publishes slab kt + 1 and frees
-// slab kt's buffer, refills that buffer with slab kt + NS, reads the first
-// fragments of slab kt + 1 and multiplies the other half, which hides the read
-// latency.  The loop body is straight-line code, so the LDS-read wait counts
-// stay exact.  The last NS slabs (and the partial one) drain through a
-// general version of the same step.
+// DMA order.  At the barrier that ends slab kt the block issues B(kt + NSB),
+// then A(kt + NSA) (when they exist).  Slab kt + 1 is then complete once every
+// DMA instruction issued before A(kt + NSA - 1) has landed: the waits count the
+// A instructions issued after B(kt + 1) (s_waitcnt vmcnt is in issue order).
+//
+// Steady state (slab kt, while both refills are whole slabs): every k-step but
+// the last reads the next k-step's fragments, then multiplies.  The last k-step
+// multiplies half of its tiles, waits for its own LDS reads and for slab kt + 1,
+// crosses the barrier that publishes slab kt + 1 and frees slab kt's buffers,
+// issues the refills, reads the first fragments of slab kt + 1 and multiplies
+// the other half, which hides the read latency.  The loop body is straight-line
+// code, so the LDS-read wait counts stay exact.  The last slabs (and the partial
+// one) drain through a general version of the same step.
 template <class C, bool AKC, bool BKC, bool AI = false, bool BI = false>
 __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K, FM_LDS char* lds,
                                          B16Acc<C::MI, C::NJ>& acc) {
-  constexpr int BK = C::BK, NS = C::NS, KS = C::KS, MI = C::MI, NJ = C::NJ;
-  constexpr int PER = C::A_INS + C::B_INS;     // DMA instructions per wave and slab
+  constexpr int BK = C::BK, NSA = C::NSA, NSB = C::NSB, KS = C::KS, MI = C::MI, NJ = C::NJ;
+  constexpr int PA = C::A_INS, PB = C::B_INS;   // DMA instructions per wave and slab
   const int nk = (K + BK - 1) / BK;
   if (nk <= 0) return;
   const int nfull = K / BK;                    // slabs with no k past K
@@ -408,22 +435,24 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
   da.init(A);
   db.init(B);
 
-  auto issue = [&](int s) {
-    FM_LDS char* buf = lds + (s % NS) * C::STAGE;
-    if (s < nfull) {
-      da.issue_full(s, buf);
-      db.issue_full(s, buf + C::A_BYTES);
-    } else {
-      da.issue_tail(A, s * BK, buf);
-      db.issue_tail(B, s * BK, buf + C::A_BYTES);
-    }
+  auto abuf = [&](int s) { return lds + (s % NSA) * C::A_BYTES; };
+  auto bbuf = [&](int s) { return lds + C::B_BASE + (s % NSB) * C::B_BYTES; };
+  auto issue_a = [&](int s) {
+    if (s < nfull) da.issue_full(s, abuf(s));
+    else da.issue_tail(A, s * BK, abuf(s));
+  };
+  auto issue_b = [&](int s) {
+    if (s < nfull) db.issue_full(s, bbuf(s));
+    else db.issue_tail(B, s * BK, bbuf(s));
   };
   bf16x8_t xa[2][MI], xb[2][NJ];
-  auto read = [&](int set, const FM_LDS char* buf, int ks) {
+  auto read = [&](int set, int s, int ks) {
+    const FM_LDS char* ab = abuf(s);
+    const FM_LDS char* bb = bbuf(s);
 #pragma unroll
-    for (int i = 0; i < MI; ++i) xa[set][i] = fa.read(buf, i, ks);
+    for (int i = 0; i < MI; ++i) xa[set][i] = fa.read(ab, i, ks);
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) xb[set][j] = fb.read(buf + C::A_BYTES, j, ks);
+    for (int j = 0; j < NJ; ++j) xb[set][j] = fb.read(bb, j, ks);
   };
   // MFMAs of register set `set` for A tiles [i0, i1).
   auto mma = [&](int set, int i0, int i1, bool tail, int k0, int ks) {
@@ -438,23 +467,38 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
   constexpr int LAST = (KS - 1) & 1;           // register set of the last k-step
   constexpr int HALF = MI / 2;
 
-  // The ring starts full: slabs 0 .. NS-1 in flight.
-#pragma unroll
-  for (int s = 0; s < NS; ++s)
-    if (s < nk) issue(s);
-  if (nk >= NS) wait_vmcnt<(NS - 1) * PER>();
+  // Prologue: B(0) A(0) B(1) A(1) ... B(NSB-1) A(NSB-1) A(NSA-1).
+#pragma nounroll
+  for (int s = 0; s < NSA && s < nk; ++s) {
+    if (s < NSB) issue_b(s);
+    issue_a(s);
+  }
+  // slab 0 is complete once everything issued after A(0) is at most in flight
+  if (nk >= NSA) wait_vmcnt<(NSB - 1) * (PA + PB) + PA>();
   else wait_vmcnt<0>();
   wait_lgkm0();   // no scalar loads pending: LDS-read waits in the loop can count
   barrier_lds();
-  read(0, lds, 0);
+  read(0, 0, 0);
 
   int kt = 0;
-  const int nsteady = nfull - NS;              // slab kt + NS is whole
+  const int nsteady = nfull - NSA;             // refills A(kt + NSA), B(kt + NSB) whole
+  // The refills issued at the end of slab kt are spread over slab kt + 1: all
+  // eight waves issuing 64 KB at once stall on the address unit for about a
+  // thousand cycles.  B(kt + 2) goes out in the first half of the next slab
+  // (it is needed at its end), A(kt + 3) in the second half.
+  static_assert(KS == 4 && PA % 2 == 0 && PB % 2 == 0, "refill spread over four k-steps");
   for (; kt < nsteady; ++kt) {
-    const FM_LDS char* buf = lds + (kt % NS) * C::STAGE;
+    if (kt > 0) {
+      db.template issue_part<PB / 2, PB>(kt + NSB - 1, bbuf(kt + NSB - 1));
+    }
 #pragma unroll
     for (int ks = 0; ks + 1 < KS; ++ks) {
-      read((ks & 1) ^ 1, buf, ks + 1);
+      read((ks & 1) ^ 1, kt, ks + 1);
+      sched_fence();
+      if (kt > 0) {
+        if (ks == 0) da.template issue_part<0, PA / 2>(kt + NSA - 1, abuf(kt + NSA - 1));
+        if (ks == 1) da.template issue_part<PA / 2, PA>(kt + NSA - 1, abuf(kt + NSA - 1));
+      }
       sched_fence();
       mma(ks & 1, 0, MI, false, 0, 0);
       sched_fence();
@@ -462,33 +506,36 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
     mma(LAST, 0, HALF, false, 0, 0);
     sched_fence();
     wait_lgkm0();
-    wait_vmcnt<(NS - 2) * PER>();
+    wait_vmcnt<PA>();                          // A(kt + NSA - 1) may still be in flight
     barrier_lds();
-    FM_LDS char* nbuf = lds + ((kt + NS) % NS) * C::STAGE;
-    da.issue_full(kt + NS, nbuf);
-    db.issue_full(kt + NS, nbuf + C::A_BYTES);
-    read(LAST ^ 1, lds + ((kt + 1) % NS) * C::STAGE, 0);
+    db.template issue_part<0, PB / 2>(kt + NSB, bbuf(kt + NSB));
+    read(LAST ^ 1, kt + 1, 0);
     sched_fence();
     mma(LAST, HALF, MI, false, 0, 0);
     sched_fence();
   }
-  // Drain: the slabs whose refill would pass the end, and the partial slab.
+  // Refills still owed by the last steady slab.
+  if (kt > 0 && kt == nsteady) {
+    db.template issue_part<PB / 2, PB>(kt + NSB - 1, bbuf(kt + NSB - 1));
+    da.issue_full(kt + NSA - 1, abuf(kt + NSA - 1));
+  }
+  // Drain: the slabs whose refills pass the end, and the partial slab.
   for (; kt < nk; ++kt) {
-    const FM_LDS char* buf = lds + (kt % NS) * C::STAGE;
     const bool tail = kt >= nfull;
 #pragma unroll
     for (int ks = 0; ks + 1 < KS; ++ks) {
-      read((ks & 1) ^ 1, buf, ks + 1);
+      read((ks & 1) ^ 1, kt, ks + 1);
       mma(ks & 1, 0, MI, tail, kt * BK, ks);
     }
     if (kt + 1 < nk) {
       wait_lgkm0();
-      const int later = min(NS - 2, nk - 2 - kt);   // slabs after kt + 1 still in flight
-      if (later >= NS - 2) wait_vmcnt<(NS - 2) * PER>();
+      // A(kt + NSA - 1), issued right after B(kt + 1), may stay in flight
+      if (kt + NSA - 1 < nk) wait_vmcnt<PA>();
       else wait_vmcnt<0>();
       barrier_lds();
-      if (kt + NS < nk) issue(kt + NS);
-      read(LAST ^ 1, lds + ((kt + 1) % NS) * C::STAGE, 0);
+      if (kt + NSB < nk) issue_b(kt + NSB);
+      if (kt + NSA < nk) issue_a(kt + NSA);
+      read(LAST ^ 1, kt + 1, 0);
     }
     mma(LAST, 0, MI, tail, kt * BK, KS - 1);
   }
