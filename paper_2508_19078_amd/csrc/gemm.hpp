@@ -219,7 +219,6 @@ __device__ __forceinline__ AccCoord acc_coord(int i, int j) {
 template <> __device__ __forceinline__ AccCoord quad_coord<float>(int g) { return acc_coord(g >> 2, g & 3); }
 
 // 4 consecutive values <-> global memory of T.
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void store4(bf16* p, f32x4_t v) {
   u32x2_t o;
   o[0] = pk_bf16(v[0], v[1]);

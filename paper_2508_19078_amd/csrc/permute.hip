@@ -178,7 +178,8 @@ __global__ __launch_bounds__(256) void k_perm_place(const int32_t* __restrict__ 
   }
 }
 
-// X_perm[p] = X[perm_token[p]] for p < offsets[S]; one wave per row.
+// X_perm[p] = X[perm_token[p]] for p < offsets[S]; one wave per row, the
+// loads of four 1 KB pieces of the row issued before their stores.
 __global__ __launch_bounds__(256) void k_gather_rows(const char* __restrict__ X,
                                                      const int32_t* __restrict__ perm_token,
                                                      const int32_t* __restrict__ offsets, int S,
@@ -187,7 +188,15 @@ __global__ __launch_bounds__(256) void k_gather_rows(const char* __restrict__ X,
   if (p >= offsets[S]) return;
   const char* src = X + (size_t)perm_token[p] * row_bytes;
   char* dst = Xp + (size_t)p * row_bytes;
-  for (size_t c = (size_t)lane_id() * 16; c < row_bytes; c += 64 * 16) st16(dst + c, ld16(src + c));
+  for (size_t c0 = (size_t)lane_id() * 16; c0 < row_bytes; c0 += 4 * 64 * 16) {
+    u32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (c0 + u * 1024 < row_bytes) v[u] = ld16(src + c0 + u * 1024);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (c0 + u * 1024 < row_bytes) st16(dst + c0 + u * 1024, v[u]);
+  }
 }
 
 __global__ void k_zero_i32(int32_t* p, int n) {
@@ -198,15 +207,56 @@ __global__ void k_zero_i32(int32_t* p, int n) {
 // Decodes inv: row of choice (t, j), folded or not.
 __device__ __forceinline__ int row_of(int v) { return v >= 0 ? v : -2 - v; }
 
+// Gathers and sums up to KMAX + S_sh rows into one token's row, U 16-byte
+// chunks per lane at a time with every load of the step issued before the
+// arithmetic: out[c] = sum_j w_j src[p_j][c] (+ sum of the shared rows).
+template <typename T, int KMAX, bool WEIGHTED>
+__device__ __forceinline__ void gather_sum_row(const T* __restrict__ src, const int (&p)[KMAX],
+                                               const float (&g)[KMAX], size_t R, int Tn, int t, int d,
+                                               int S_sh, T* __restrict__ out) {
+  constexpr int V = 16 / sizeof(T), U = 2;
+  for (int c0 = lane_id() * V; c0 < d; c0 += U * 64 * V) {
+    u32x4_t raw[U][KMAX];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * 64 * V;
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j)
+        if (p[j] >= 0 && c < d) raw[u][j] = ld16(src + (size_t)p[j] * d + c);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = c0 + u * 64 * V;
+      if (c >= d) continue;
+      float acc[V];
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] = 0.f;
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j) {
+        if (p[j] < 0) continue;
+        float f[V];
+        unpack16(raw[u][j], f, (T*)nullptr);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = WEIGHTED ? fmaf(g[j], f[i], acc[i]) : acc[i] + f[i];
+      }
+      for (int sh = 0; sh < S_sh; ++sh) {
+        float f[V];
+        unpack16(ld16(src + (R + (size_t)sh * Tn + t) * d + c), f, (T*)nullptr);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] += f[i];
+      }
+      st16(out + (size_t)t * d + c, pack16(acc, (T*)nullptr));
+    }
+  }
+}
+
 // Y[t] = sum_{first choices} perm_gate[p] O[p] + sum_shared O[shared row].
 template <typename T, int KMAX>
 __global__ __launch_bounds__(256) void k_combine(const T* __restrict__ O, const int32_t* __restrict__ inv,
                                                  const float* __restrict__ pg, int Tn, int k, int d,
                                                  int S_sh, T* __restrict__ Y) {
-  constexpr int V = 16 / sizeof(T);
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= Tn) return;
-  const size_t R = (size_t)Tn * k;
   int p[KMAX];
   float g[KMAX];
 #pragma unroll
@@ -214,26 +264,7 @@ __global__ __launch_bounds__(256) void k_combine(const T* __restrict__ O, const 
     p[j] = j < k ? inv[(size_t)t * k + j] : -1;
     g[j] = p[j] >= 0 ? pg[p[j]] : 0.f;
   }
-  for (int c = lane_id() * V; c < d; c += 64 * V) {
-    float acc[V];
-#pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] = 0.f;
-#pragma unroll
-    for (int j = 0; j < KMAX; ++j) {
-      if (p[j] < 0) continue;
-      float f[V];
-      unpack16(ld16(O + (size_t)p[j] * d + c), f, (T*)nullptr);
-#pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] = fmaf(g[j], f[i], acc[i]);
-    }
-    for (int sh = 0; sh < S_sh; ++sh) {
-      float f[V];
-      unpack16(ld16(O + (R + (size_t)sh * Tn + t) * d + c), f, (T*)nullptr);
-#pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] += f[i];
-    }
-    st16(Y + (size_t)t * d + c, pack16(acc, (T*)nullptr));
-  }
+  gather_sum_row<T, KMAX, true>(O, p, g, (size_t)Tn * k, Tn, t, d, S_sh, Y);
 }
 
 // dO[p] = perm_gate[p] dY[t]; shared rows get dY[t]; dgate[t,j] = <dY[t], O[row]>.
@@ -294,33 +325,16 @@ template <typename T, int KMAX>
 __global__ __launch_bounds__(256) void k_permute_bwd(const T* __restrict__ dXp,
                                                      const int32_t* __restrict__ inv, int Tn, int k,
                                                      int d, int S_sh, T* __restrict__ dX) {
-  constexpr int V = 16 / sizeof(T);
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= Tn) return;
-  const size_t R = (size_t)Tn * k;
   int p[KMAX];
+  float g[KMAX];
 #pragma unroll
-  for (int j = 0; j < KMAX; ++j) p[j] = j < k ? inv[(size_t)t * k + j] : -1;
-  for (int c = lane_id() * V; c < d; c += 64 * V) {
-    float acc[V];
-#pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] = 0.f;
-#pragma unroll
-    for (int j = 0; j < KMAX; ++j) {
-      if (p[j] < 0) continue;
-      float f[V];
-      unpack16(ld16(dXp + (size_t)p[j] * d + c), f, (T*)nullptr);
-#pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] += f[i];
-    }
-    for (int sh = 0; sh < S_sh; ++sh) {
-      float f[V];
-      unpack16(ld16(dXp + (R + (size_t)sh * Tn + t) * d + c), f, (T*)nullptr);
-#pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] += f[i];
-    }
-    st16(dX + (size_t)t * d + c, pack16(acc, (T*)nullptr));
+  for (int j = 0; j < KMAX; ++j) {
+    p[j] = j < k ? inv[(size_t)t * k + j] : -1;
+    g[j] = 1.f;
   }
+  gather_sum_row<T, KMAX, false>(dXp, p, g, (size_t)Tn * k, Tn, t, d, S_sh, dX);
 }
 
 int check_layer(const moe_layer* L) {

@@ -2,11 +2,11 @@
 // histogram of the int8 profiling router.
 //
 // One kernel serves both the full-precision router and the int8 profiling
-// router: a block owns 32 tokens, its four waves split the hidden dimension
-// into interleaved 16-byte-per-lane chunks and accumulate the token x expert
-// logits on MFMA (16x16x32 bf16, or 16x16x4 fp32 for fp32 inputs).  The four
-// partial sums are added in a fixed order in LDS, so the logits do not depend
-// on scheduling.  Then 16 lanes per token select the top k by
+// router: a block owns 32 tokens, its waves split the hidden dimension into
+// interleaved 16-byte-per-lane chunks and accumulate the token x expert
+// logits on MFMA (16x16x32 bf16, or 16x16x4 fp32 for fp32 inputs).  The
+// sixteen partial sums are added in a fixed order in LDS (four groups of four,
+// then the groups), so the logits do not depend on scheduling.  Then 16 lanes per token select the top k by
 // (logit desc, index asc) with branch-free 64-bit key reductions, and either
 // write idx/gate or add the selection to an LDS histogram that is flushed to
 // the global counts with one integer atomic per expert and block.
@@ -16,7 +16,14 @@ namespace fm {
 namespace {
 
 constexpr int RT_TOK = 32;      // tokens per block
-constexpr int RT_WAVES = 4;     // waves per block, splitting d
+constexpr int RT_GROUPS = 4;    // partial sums reduced in RT_GROUPS fixed-order groups
+// Waves per block (splitting d) and chunks in flight per wave, by the number
+// of 16-expert column tiles: as many loads in flight per CU as the
+// accumulators leave registers for (about 200 KB for up to 64 experts).
+template <int NE> struct RtShape {
+  static constexpr int WAVES = NE <= 4 ? 16 : NE <= 8 ? 8 : 4;
+  static constexpr int P = NE <= 2 ? 4 : NE <= 8 ? 2 : 1;
+};
 
 template <int N> struct fragv;
 template <> struct fragv<8> { typedef bf16x8_t type; };   // 8 bf16 per lane
@@ -41,7 +48,6 @@ __device__ __forceinline__ f32x4_t load_w_frag(const float* p, bool ok, f32x4_t)
 }
 // int8 codes widened exactly to bf16 (|q| <= 127 has at most 7 significant bits).
 __device__ __forceinline__ bf16x8_t load_w_frag(const int8_t* p, bool ok, bf16x8_t) {
-  typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
   u32x2_t raw = ok ? *(const FM_GLOBAL u32x2_t*)(p) : u32x2_t{0, 0};
   u32x4_t v;
 #pragma unroll
@@ -98,7 +104,7 @@ __device__ __forceinline__ f32x4_t mma(f32x4_t a, f32x4_t b, f32x4_t c) {
 
 // MODE 0: write idx/gate (+logits).  MODE 1: histogram (+idx).
 template <typename TX, typename TW, int NE, int KMAX, int MODE>
-__global__ __launch_bounds__(256) void k_route(
+__global__ __launch_bounds__(RtShape<NE>::WAVES * 64) void k_route(
     const TX* __restrict__ X, const TW* __restrict__ W, const float* __restrict__ wscale,
     const float* __restrict__ bias, int T, int d, int E, int k,
     int32_t* __restrict__ idx, float* __restrict__ gate, float* __restrict__ logits,
@@ -106,8 +112,9 @@ __global__ __launch_bounds__(256) void k_route(
   constexpr int V = 16 / sizeof(TX);           // elements per lane per chunk
   constexpr int KC = 4 * V;                    // hidden columns per chunk
   constexpr int EP = NE * 16 + 1;              // padded LDS row
+  constexpr int RT_WAVES = RtShape<NE>::WAVES;
   typedef typename fragv<V>::type frag_t;
-  __shared__ float red[RT_TOK * EP];
+  __shared__ float red[RT_GROUPS][RT_TOK * EP];
   __shared__ int hist[NE * 16];
 
   const int lane = lane_id();
@@ -135,8 +142,8 @@ __global__ __launch_bounds__(256) void k_route(
 #pragma unroll
   for (int j = 0; j < NE; ++j) wrow[j] = W + (size_t)min(j * 16 + r16, E - 1) * d;
 
-  // This wave's chunks are wave, wave + 4, ...; P of them are in flight.
-  constexpr int P = NE <= 4 ? 4 : 2;
+  // This wave's chunks are wave, wave + RT_WAVES, ...; P of them are in flight.
+  constexpr int P = RtShape<NE>::P;
   const int nw = nchunks > wave ? (nchunks - wave + RT_WAVES - 1) / RT_WAVES : 0;
   frag_t ra[P][2], rb[P][NE];
   auto issue = [&](int u, int i) {
@@ -177,9 +184,12 @@ __global__ __launch_bounds__(256) void k_route(
       for (int j = 0; j < NE; ++j) acc[r][j] = mma(a[r], b[j], acc[r][j]);
   }
 
-  // fixed-order reduction of the four partial sums: ((p0 + p1) + p2) + p3
-  for (int w = 0; w < RT_WAVES; ++w) {
-    if (wave == w) {
+  // Fixed-order reduction of the partial sums: group g adds waves
+  // g, g + 4, g + 8, g + 12 in that order, then g0 + g1 + g2 + g3.
+  constexpr int PER_GROUP = RT_WAVES / RT_GROUPS;
+  const int grp_id = wave % RT_GROUPS;
+  for (int step = 0; step < PER_GROUP; ++step) {
+    if (wave / RT_GROUPS == step) {
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
@@ -187,20 +197,22 @@ __global__ __launch_bounds__(256) void k_route(
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             // MFMA output: row (token) 4*q4 + i, column (expert) r16
-            float* p = &red[(r * 16 + 4 * q4 + i) * EP + j * 16 + r16];
-            *p = (w == 0) ? acc[r][j][i] : *p + acc[r][j][i];
+            float* p = &red[grp_id][(r * 16 + 4 * q4 + i) * EP + j * 16 + r16];
+            *p = (step == 0) ? acc[r][j][i] : *p + acc[r][j][i];
           }
     }
     __syncthreads();
   }
 
-  // finalise logits: scale (int8 router) and bias
+  // finalise logits: sum of the groups, scale (int8 router) and bias
   for (int i = threadIdx.x; i < RT_TOK * E; i += blockDim.x) {
     int tl = i / E, e = i - tl * E;
-    float v = red[tl * EP + e];
+    float v = red[0][tl * EP + e];
+#pragma unroll
+    for (int g = 1; g < RT_GROUPS; ++g) v += red[g][tl * EP + e];
     if (wscale) v *= wscale[e];
     if (bias) v += bias[e];
-    red[tl * EP + e] = v;
+    red[0][tl * EP + e] = v;
     if (MODE == 0 && logits && t0 + tl < T) logits[(size_t)(t0 + tl) * E + e] = v;
   }
   __syncthreads();
@@ -210,16 +222,19 @@ __global__ __launch_bounds__(256) void k_route(
   // high word maps the fp32 value monotonically to uint32 (-0.0 == +0.0), the
   // low word is 0xFFFF - expert.  Each of the k selection rounds takes the
   // group maximum with four DPP row rotations; the owner lane then drops it.
+  // groups of 16 lanes, one token each: RT_WAVES * 4 tokens per round
   const int grp = lane >> 4, gl = lane & 15;
+  constexpr int ROUNDS = (RT_TOK + RT_WAVES * 4 - 1) / (RT_WAVES * 4);
 #pragma unroll
-  for (int round = 0; round < 2; ++round) {
-    const int tl = wave * 8 + round * 4 + grp;
+  for (int round = 0; round < ROUNDS; ++round) {
+    const int tl = round * RT_WAVES * 4 + wave * 4 + grp;
+    if (tl >= RT_TOK) continue;
     const int t = t0 + tl;
     uint32_t khi[NE], klo[NE];
 #pragma unroll
     for (int i = 0; i < NE; ++i) {
       const int e = gl + 16 * i;
-      const float v = red[tl * EP + e] + 0.0f;
+      const float v = red[0][tl * EP + e] + 0.0f;
       khi[i] = e < E ? ordered_key(v) : 0u;
       klo[i] = e < E ? 0xFFFFu - (uint32_t)e : 0u;
     }
@@ -272,27 +287,42 @@ __global__ __launch_bounds__(256) void k_route(
   }
 }
 
-// Per-row symmetric int8 quantiser: one wave per row.
+// Per-row symmetric int8 quantiser: one wave per row, 16-byte loads.
 template <typename T>
 __global__ __launch_bounds__(256) void k_quantize(const T* __restrict__ W, int E, int d,
                                                   int8_t* __restrict__ q, float* __restrict__ s) {
+  constexpr int V = 16 / sizeof(T);   // elements per 16-byte chunk (d % 8 == 0)
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = lane_id();
   if (row >= E) return;
   const T* w = W + (size_t)row * d;
   float m = 0.f;
-  for (int i = lane; i < d; i += 64) m = fmaxf(m, fabsf(to_float(w[i])));
+  for (int c = lane * V; c < d; c += 64 * V) {
+    float f[V];
+    unpack16(ld16(w + c), f, (T*)nullptr);
+#pragma unroll
+    for (int i = 0; i < V; ++i) m = fmaxf(m, fabsf(f[i]));
+  }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
   const float sc = m / 127.0f;
   if (lane == 0) s[row] = sc;
-  for (int i = lane; i < d; i += 64) {
-    int v = 0;
-    if (sc > 0.f) {
-      float r = rintf(to_float(w[i]) / sc);
-      v = (int)fminf(fmaxf(r, -127.f), 127.f);
+  for (int c = lane * V; c < d; c += 64 * V) {
+    float f[V];
+    unpack16(ld16(w + c), f, (T*)nullptr);
+    uint32_t packed[V / 4];
+#pragma unroll
+    for (int i = 0; i < V; ++i) {
+      int v = 0;
+      if (sc > 0.f) {
+        const float r = rintf(f[i] / sc);
+        v = (int)fminf(fmaxf(r, -127.f), 127.f);
+      }
+      if (i % 4 == 0) packed[i / 4] = 0;
+      packed[i / 4] |= ((uint32_t)v & 0xFFu) << (8 * (i % 4));
     }
-    q[(size_t)row * d + i] = (int8_t)v;
+    if (V == 8) *(FM_GLOBAL u32x2_t*)(q + (size_t)row * d + c) = u32x2_t{packed[0], packed[V / 4 - 1]};
+    else *(FM_GLOBAL uint32_t*)(q + (size_t)row * d + c) = packed[0];
   }
 }
 
@@ -300,11 +330,11 @@ template <typename TX, typename TW, int MODE>
 int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, int T, int d,
                  int E, int k, int32_t* idx, float* gate, float* logits, int32_t* counts,
                  hipStream_t st) {
-  dim3 grid(cdiv(T, RT_TOK)), block(256);
+  dim3 grid(cdiv(T, RT_TOK));
   const int ne = cdiv(E, 16);
-#define FM_RT(NE, KM)                                                                  \
-  hipLaunchKernelGGL((k_route<TX, TW, NE, KM, MODE>), grid, block, 0, st, X, W, ws, bias, \
-                     T, d, E, k, idx, gate, logits, counts)
+#define FM_RT(NE, KM)                                                                          \
+  hipLaunchKernelGGL((k_route<TX, TW, NE, KM, MODE>), grid, dim3(RtShape<NE>::WAVES * 64), 0, st, X, W, \
+                     ws, bias, T, d, E, k, idx, gate, logits, counts)
 #define FM_RT_K(NE)              \
   if (k <= 2) FM_RT(NE, 2);      \
   else if (k <= 4) FM_RT(NE, 4); \
