@@ -452,6 +452,70 @@ __device__ __forceinline__ void b16_store_staged(const B16Acc<C::MI, C::NJ>& acc
   barrier_lds();
 }
 
+// SwiGLU backward of a dH tile with s = logistic(a_g): dA_u = dH a_g s,
+// dA_g = dH u s (1 + a_g (1 - s)).  dH is staged through LDS rounded to bf16
+// (the precision a bf16 product would hand to the elementwise step), the
+// whole tile at once; every lane then takes 8-column chunks of a row (16-byte
+// loads of A_g, A_u and stores of dA_g, dA_u; a wave covers whole rows).  The
+// loads of the first PRE chunks are issued before the tile is staged, so their
+// latency overlaps the LDS writes.  Pointers are at the tile origin; rows x
+// cols are valid.
+template <class C>
+__device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& acc, FM_LDS char* lds,
+                                                   const bf16* Ag, const bf16* Au, bf16* dAg, bf16* dAu,
+                                                   size_t ld, int rows, int cols) {
+  using S = Stage<bf16, C::RB>;
+  constexpr int CH = C::RB / 8;                     // 8-column chunks per row
+  constexpr int PER = C::RA * CH / B16_THREADS;     // chunks per lane
+  constexpr int PRE = PER / 2;
+  static_assert(PER * B16_THREADS == C::RA * CH && C::RA * C::RB * 2 <= C::LDS, "whole chunks per lane");
+  // thread index re-read here (opaque), so that the per-chunk addresses are
+  // not hoisted out of the tile loop and kept live through the main loop
+  const int tid = wave_id() * 64 + lane_id_here();
+  u32x4_t ga[PER], ua[PER];
+  auto load = [&](int u) {
+    const int idx = tid + u * B16_THREADS, r = idx / CH, c = (idx % CH) * 8;
+    if (r < rows && c < cols) {
+      ga[u] = ld16(Ag + (size_t)r * ld + c);
+      ua[u] = ld16(Au + (size_t)r * ld + c);
+    }
+  };
+#pragma unroll
+  for (int u = 0; u < PRE; ++u) load(u);
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const AccCoord c = b16_coord<C>(i, j, q);
+        S::put4(lds, c.row, c.col4, acc.quad(i, j, q));
+      }
+  barrier_lds_writes();
+#pragma unroll
+  for (int u = PRE; u < PER; ++u) load(u);
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int idx = tid + u * B16_THREADS, r = idx / CH, c = (idx % CH) * 8;
+    if (r < rows && c < cols) {
+      float dh[8], a[8], up[8], dg[8], du[8];
+      const u32x4_t hv = *(const FM_LDS u32x4_t*)(lds + S::at(r, c));
+      unpack16(hv, dh, (bf16*)nullptr);
+      unpack16(ga[u], a, (bf16*)nullptr);
+      unpack16(ua[u], up, (bf16*)nullptr);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float sg = sigm_fast(a[e]);
+        du[e] = dh[e] * a[e] * sg;
+        dg[e] = dh[e] * up[e] * sg * (1.0f + a[e] * (1.0f - sg));
+      }
+      st16(dAg + (size_t)r * ld + c, pack16(dg, (bf16*)nullptr));
+      st16(dAu + (size_t)r * ld + c, pack16(du, (bf16*)nullptr));
+    }
+  }
+  barrier_lds();
+}
+
 // [A_g | A_u] = X_s [W_gate | W_up]^T, H = silu(A_g) A_u.  The B tile
 // interleaves 32-row blocks of W_gate and W_up (128 intermediate columns per
 // 256-row tile): tile j = 2jj of a wave holds gate and j = 2jj + 1 up of the
@@ -545,27 +609,8 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
     B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
     b16_gemm<CB, true, false>(A, B, d, (FM_LDS char*)lds, acc);
-#pragma unroll
-    for (int i = 0; i < CB::MI; ++i)
-#pragma unroll
-      for (int j = 0; j < CB::NJ; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const AccCoord c = b16_coord<CB>(i, j, q);
-          const int n = n0 + c.col4;
-          if (c.row >= sr.nrows - m0 || n >= I) continue;
-          const size_t o = (ob + c.row) * I + n;
-          const f32x4_t dh = acc.quad(i, j, q), ag = load4(Ag + o), u = load4(Au + o);
-          f32x4_t dg, du;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float sg = sigm_fast(ag[r]);
-            du[r] = dh[r] * ag[r] * sg;
-            dg[r] = dh[r] * u[r] * sg * (1.0f + ag[r] * (1.0f - sg));
-          }
-          store4(dAg + o, dg);
-          store4(dAu + o, du);
-        }
+    b16_dswiglu_staged<CB>(acc, (FM_LDS char*)lds, Ag + ob * I + n0, Au + ob * I + n0, dAg + ob * I + n0,
+                           dAu + ob * I + n0, I, sr.nrows - m0, I - n0);
   }
 }
 

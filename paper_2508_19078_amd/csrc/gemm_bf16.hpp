@@ -371,8 +371,11 @@ template <typename T, int COLS> struct Stage {
   static __device__ __forceinline__ void copy_rows(const FM_LDS char* lds, RowPtr row_ptr, int cols_valid,
                                                    bool accumulate = false) {
     constexpr int TOTAL = ROWS * CPR;
+    // thread index re-read here (opaque): per-lane addresses stay out of the
+    // registers of a surrounding tile loop
+    const int tid = wave_id() * 64 + lane_id_here();
 #pragma unroll 4
-    for (int idx = threadIdx.x; idx < TOTAL; idx += B16_THREADS) {
+    for (int idx = tid; idx < TOTAL; idx += B16_THREADS) {
       const int row = idx / CPR, c = idx % CPR;
       u32x4_t v = *(const FM_LDS u32x4_t*)(lds + row * ROW_BYTES + ((c ^ (row & (CPR - 1))) << 4));
       T* out = row_ptr(row);
