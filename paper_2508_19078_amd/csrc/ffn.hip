@@ -13,13 +13,18 @@
 //
 // Scheduling.  A one-block kernel turns the offsets into a schedule: prefix
 // sums of each slot's row tiles and, for the weight gradients, of each
-// tuning slot's work (its K slabs).  The GEMM kernels are persistent, one block
-// per compute unit.  Blocks are dispatched to the 8 XCDs round-robin, so block
-// b runs on XCD b % 8; each XCD walks its own contiguous range of the tile
-// space, ordered slot-major, then in bands of row tiles (see band_order).
-// Concurrent blocks of an XCD thus share a band of one slot's activations and a
-// few weight column tiles, which stay in that XCD's L2.  The weight-gradient tile
-// space is split between XCDs by work rather than by tile count.
+// tuning slot's work (its K slabs), and an order of the tuning slots by
+// decreasing rows.  The GEMM kernels are persistent, one block per compute
+// unit.  Blocks are dispatched to the 8 XCDs round-robin, so block b runs on
+// XCD b % 8.  Row-tile products: each XCD walks its own contiguous range of the
+// tile space, ordered slot-major, then in bands of row tiles (see band_order);
+// concurrent blocks of an XCD thus share a band of one slot's activations and a
+// few weight column tiles, which stay in that XCD's L2.  Weight-gradient
+// products (whose tiles differ in cost by up to two orders of magnitude): the
+// tiles of the tuning slots, largest slot first, are dealt to the XCDs
+// round-robin (every XCD gets an eighth of every slot), and the blocks of an XCD
+// draw its tiles from a counter, so that blocks that drew cheap tiles take more
+// (see DwQueue).
 #include "gemm_bf16.hpp"
 
 namespace fm {
@@ -51,18 +56,35 @@ __device__ __forceinline__ SlotRows slot_rows(int s, const int32_t* offsets, int
   return r;
 }
 
-// Schedule in the workspace: mbase[0..S] (prefix of row tiles per slot)
-// and wbase[0..S] (prefix of weight-gradient work per slot, 64-bit).
+// Schedule in the workspace: mbase[0..S] (prefix of row tiles per slot),
+// wbase[0..S] (prefix of weight-gradient work per slot, 64-bit), dorder[0..S]
+// (the tuning slots by decreasing rows, ties by index; dorder[S] = their
+// number) and the tile counters of the weight-gradient kernels (DW_QUEUES
+// queues of N_XCD counters, 128 bytes apart), zeroed by k_build_sched.
+constexpr int DW_QSTRIDE = 32;    // ints between two counters
+constexpr int DW_QUEUES = 2;      // dW_gate/up, dW_down
+constexpr int DW_QINTS = DW_QUEUES * N_XCD * DW_QSTRIDE;
 struct Sched {
   int32_t* mbase;
   long long* wbase;
+  int32_t* dorder;
+  int32_t* queues;
 };
-inline size_t sched_part(int S) { return ((sizeof(int32_t) * (S + 1) + 255) / 256) * 256; }
-inline size_t sched_bytes(int S) { return sched_part(S) + ((sizeof(long long) * (S + 1) + 255) / 256) * 256; }
+inline size_t round256(size_t b) { return (b + 255) / 256 * 256; }
+inline size_t sched_bytes(int S) {
+  return 2 * round256(sizeof(int32_t) * (S + 1)) + round256(sizeof(long long) * (S + 1)) +
+         round256(sizeof(int32_t) * DW_QINTS);
+}
 inline Sched sched_at(void* ws, int S) {
   Sched s;
-  s.mbase = (int32_t*)ws;
-  s.wbase = (long long*)((char*)ws + sched_part(S));
+  char* p = (char*)ws;
+  s.mbase = (int32_t*)p;
+  p += round256(sizeof(int32_t) * (S + 1));
+  s.wbase = (long long*)p;
+  p += round256(sizeof(long long) * (S + 1));
+  s.dorder = (int32_t*)p;
+  p += round256(sizeof(int32_t) * (S + 1));
+  s.queues = (int32_t*)p;
   return s;
 }
 
@@ -72,16 +94,29 @@ inline Sched sched_at(void* ws, int S) {
 constexpr int DW_SLAB = 64;
 __global__ __launch_bounds__(1024) void k_build_sched(const int32_t* __restrict__ offsets, int S_r, int S_sh,
                                                       int Tn, int tile_rows, float* const* __restrict__ dw_tab,
-                                                      int32_t* __restrict__ mbase, long long* __restrict__ wbase) {
+                                                      int32_t* __restrict__ mbase, long long* __restrict__ wbase,
+                                                      int32_t* __restrict__ dorder, int32_t* __restrict__ queues) {
   __shared__ int sm[1024];
   __shared__ long long sw[1024];
+  __shared__ int skey[1024];
   const int S = S_r + S_sh, s = threadIdx.x;
+  for (int i = s; i < DW_QINTS; i += 1024) queues[i] = 0;
   int n = 0;
   if (s < S) n = s < S_r ? offsets[s + 1] - offsets[s] : Tn;
+  const bool tune = s < S && dw_tab && dw_tab[s];
   long long w = 0;
-  if (s < S && dw_tab && dw_tab[s]) w = (n + DW_SLAB - 1) / DW_SLAB + 1;
+  if (tune) w = (n + DW_SLAB - 1) / DW_SLAB + 1;
   sm[s] = (n + tile_rows - 1) / tile_rows;
   sw[s] = w;
+  skey[s] = tune ? n : -1;
+  // tuning slots by decreasing rows (ties: lower index first)
+  const int ntune = __syncthreads_count(tune);
+  if (tune) {
+    int rank = 0;
+    for (int u = 0; u < S; ++u) rank += (skey[u] > n) || (skey[u] == n && u < s);
+    dorder[rank] = s;
+  }
+  if (s == 0) dorder[S] = ntune;
   __syncthreads();
   for (int off = 1; off < 1024; off <<= 1) {   // inclusive Hillis-Steele scans
     const int a = s >= off ? sm[s - off] : 0;
@@ -187,6 +222,8 @@ struct RowArgs {
 struct DwArgs {
   const int32_t* offsets;
   const long long* wbase;
+  const int32_t* dorder;
+  int32_t* queue;   // this kernel's N_XCD counters
   int S_r, S, Tn, k, d, I, accumulate;
 };
 
@@ -209,6 +246,37 @@ __device__ __forceinline__ TileRange dw_range(const DwArgs& da, int tps) {
                    tile_at_work(da.wbase, da.S, tps, w * (x + 1) / N_XCD), (int)(blockIdx.x / N_XCD),
                    (int)(gridDim.x / N_XCD)};
 }
+
+// Dynamic tile queue of the weight-gradient kernels.  XCD x owns tiles x,
+// x + 8, x + 16, ... of the tuning slots' tile space (slots in dorder, largest
+// first; tps tiles per slot), i.e. an eighth of every slot, so that the XCDs
+// get equal work and equal shares of the costly tiles.  Its blocks take them in
+// order, one atomic per tile, drawn by thread 0 a tile ahead; the draw reaches
+// the other waves through LDS word 0, which is free between tiles.
+struct DwQueue {
+  int32_t* ctr;
+  long long total;   // tiles of the tuning slots
+  int x;
+
+  __device__ __forceinline__ DwQueue(const DwArgs& da, int tps) {
+    x = blockIdx.x % N_XCD;
+    ctr = da.queue + x * DW_QSTRIDE;
+    total = (long long)da.dorder[da.S] * tps;
+  }
+  // Thread 0 only.
+  __device__ __forceinline__ int draw() const { return atomicAdd(ctr, 1); }
+  __device__ __forceinline__ long long tile(int j) const { return (long long)j * N_XCD + x; }
+  // Hands thread 0's draw to every thread (LDS word 0 must be free; the caller
+  // keeps it until every wave has read it).
+  __device__ __forceinline__ static int share(FM_LDS char* lds, int j) {
+    if (threadIdx.x == 0) {
+      wait_vmcnt<0>();
+      *(FM_LDS int*)lds = j;
+    }
+    barrier_lds_writes();
+    return *(const FM_LDS int*)lds;
+  }
+};
 
 // ------------------------------------------- fp32 kernels (16x16 core) ----
 
@@ -642,64 +710,85 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg,
 __global__ __launch_bounds__(B16_THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X, cbp Xp, cbp dAg, cbp dAu,
                                                         DwArgs da) {
   __shared__ __align__(16) char lds[CB::LDS];
+  FM_LDS char* const l = (FM_LDS char*)lds;
   const int d = da.d, I = da.I;
   const int MT = (I + CB::RA / 2 - 1) / (CB::RA / 2), NT = (d + CB::RB - 1) / CB::RB;
-  const TileRange tr = dw_range(da, MT * NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
-    const Tile rt = dw_tile(t, MT * NT, MT);
+  const DwQueue qu(da, MT * NT);
+  int j = DwQueue::share(l, threadIdx.x == 0 ? qu.draw() : 0);
+  barrier_lds();
+  for (long long t = qu.tile(j); t < qu.total; t = qu.tile(j)) {
+    const int next = threadIdx.x == 0 ? qu.draw() : 0;
+    Tile rt = dw_tile(t, MT * NT, MT);
+    rt.s = da.dorder[rt.s];
     float* dwg = W.dwg[rt.s];
     float* dwu = W.dwu[rt.s];
-    if (!dwg || !dwu) continue;
+    const bool run = dwg && dwu;
     const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
     const int m0 = rt.m * (CB::RA / 2), n0 = rt.n * CB::RB;
-    const B16Src A{dAg + (size_t)sr.orow0 * I + m0, dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows};
-    const B16Src B{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, nullptr, d, d - n0, sr.nrows};
     B16Acc<CB::MI, CB::NJ> acc;
-    acc.zero();
-    b16_gemm<CB, false, false, true, false>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
+    if (run) {
+      const B16Src A{dAg + (size_t)sr.orow0 * I + m0, dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows};
+      const B16Src B{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, nullptr, d, d - n0, sr.nrows};
+      acc.zero();
+      b16_gemm<CB, false, false, true, false>(A, B, sr.nrows, l, acc);
+    }
+    j = DwQueue::share(l, next);
+    if (run) {
 #pragma unroll
-    for (int i = 0; i < CB::MI; ++i)
+      for (int i = 0; i < CB::MI; ++i)
 #pragma unroll
-      for (int j = 0; j < CB::NJ; ++j)
+        for (int jj = 0; jj < CB::NJ; ++jj)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const AccCoord c = b16_coord<CB>(i, j, q);
-          const int m = m0 + deinter(c.row), n = n0 + c.col4;
-          if (m >= I || n >= d) continue;
-          float* dst = ((c.row >> 5) & 1) ? dwu : dwg;
-          store_dw(dst + (size_t)m * d + n, acc.quad(i, j, q), da.accumulate);
-        }
+          for (int q = 0; q < 4; ++q) {
+            const AccCoord c = b16_coord<CB>(i, jj, q);
+            const int m = m0 + deinter(c.row), n = n0 + c.col4;
+            if (m >= I || n >= d) continue;
+            float* dst = ((c.row >> 5) & 1) ? dwu : dwg;
+            store_dw(dst + (size_t)m * d + n, acc.quad(i, jj, q), da.accumulate);
+          }
+    }
+    barrier_lds();   // every wave has read the draw before the next tile's DMA
   }
 }
 
 // dW_down = dO^T H (both read k-major).
 __global__ __launch_bounds__(B16_THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO, cbp H, DwArgs da) {
   __shared__ __align__(16) char lds[CB::LDS];
+  FM_LDS char* const l = (FM_LDS char*)lds;
   const int d = da.d, I = da.I;
   const int MT = (d + CB::RA - 1) / CB::RA, NT = (I + CB::RB - 1) / CB::RB;
-  const TileRange tr = dw_range(da, MT * NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
-    const Tile rt = dw_tile(t, MT * NT, MT);
+  const DwQueue qu(da, MT * NT);
+  int j = DwQueue::share(l, threadIdx.x == 0 ? qu.draw() : 0);
+  barrier_lds();
+  for (long long t = qu.tile(j); t < qu.total; t = qu.tile(j)) {
+    const int next = threadIdx.x == 0 ? qu.draw() : 0;
+    Tile rt = dw_tile(t, MT * NT, MT);
+    rt.s = da.dorder[rt.s];
     float* dwd = W.dwd[rt.s];
-    if (!dwd) continue;
     const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
     const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
-    const B16Src A{dO + (size_t)sr.orow0 * d + m0, nullptr, d, d - m0, sr.nrows};
-    const B16Src B{H + (size_t)sr.orow0 * I + n0, nullptr, I, I - n0, sr.nrows};
     B16Acc<CB::MI, CB::NJ> acc;
-    acc.zero();
-    b16_gemm<CB, false, false>(A, B, sr.nrows, (FM_LDS char*)lds, acc);
+    if (dwd) {
+      const B16Src A{dO + (size_t)sr.orow0 * d + m0, nullptr, d, d - m0, sr.nrows};
+      const B16Src B{H + (size_t)sr.orow0 * I + n0, nullptr, I, I - n0, sr.nrows};
+      acc.zero();
+      b16_gemm<CB, false, false>(A, B, sr.nrows, l, acc);
+    }
+    j = DwQueue::share(l, next);
+    if (dwd) {
 #pragma unroll
-    for (int i = 0; i < CB::MI; ++i)
+      for (int i = 0; i < CB::MI; ++i)
 #pragma unroll
-      for (int j = 0; j < CB::NJ; ++j)
+        for (int jj = 0; jj < CB::NJ; ++jj)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const AccCoord c = b16_coord<CB>(i, j, q);
-          const int m = m0 + c.row, n = n0 + c.col4;
-          if (m >= d || n >= I) continue;
-          store_dw(dwd + (size_t)m * I + n, acc.quad(i, j, q), da.accumulate);
-        }
+          for (int q = 0; q < 4; ++q) {
+            const AccCoord c = b16_coord<CB>(i, jj, q);
+            const int m = m0 + c.row, n = n0 + c.col4;
+            if (m >= d || n >= I) continue;
+            store_dw(dwd + (size_t)m * I + n, acc.quad(i, jj, q), da.accumulate);
+          }
+    }
+    barrier_lds();   // every wave has read the draw before the next tile's DMA
   }
 }
 
@@ -719,7 +808,7 @@ int check_layer_ffn(const moe_layer* L) {
   return MOE_OK;
 }
 
-size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
 size_t rows_total(const moe_layer* L, int T, int k) { return (size_t)T * (k + L->S_shared); }
 int n_slots(const moe_layer* L) { return L->S_routed + L->S_shared; }
 
@@ -745,7 +834,7 @@ extern "C" size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int 
 
 extern "C" size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k) {
   if (!L || T < 0 || k <= 0) return 0;
-  const size_t act = align256(rows_total(L, T, k) * L->I * esize(L->dtype));
+  const size_t act = round256(rows_total(L, T, k) * L->I * esize(L->dtype));
   return sched_bytes(n_slots(L)) + 2 * act;
 }
 
@@ -770,7 +859,7 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
   const Sched sc = sched_at(ws, S);
   const int tile_rows = L->dtype == MOE_BF16 ? B16_ROWS : G_BM;
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, tile_rows,
-                     (float* const*)nullptr, sc.mbase, sc.wbase);
+                     (float* const*)nullptr, sc.mbase, sc.wbase, sc.dorder, sc.queues);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
   const dim3 grid(persistent_blocks()), block(G_THREADS);
 #define FM_FWD(TT)                                                                                      \
@@ -812,15 +901,17 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   hipStream_t st = as_stream(stream);
   const int S = n_slots(L);
   const Sched sc = sched_at(ws, S);
-  const size_t act = align256(rows_total(L, T, k) * L->I * esize(L->dtype));
+  const size_t act = round256(rows_total(L, T, k) * L->I * esize(L->dtype));
   char* dAg = (char*)ws + sched_bytes(S);
   char* dAu = dAg + act;
   const int d = L->d, I = L->I;
   const int tile_rows = L->dtype == MOE_BF16 ? B16_ROWS : G_BM;
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, tile_rows,
-                     L->dw_gate, sc.mbase, sc.wbase);
+                     L->dw_gate, sc.mbase, sc.wbase, sc.dorder, sc.queues);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, d, I};
-  const DwArgs da{offsets, sc.wbase, L->S_routed, S, T, k, d, I, accumulate_dw};
+  const DwArgs da{offsets, sc.wbase, sc.dorder, sc.queues, L->S_routed, S, T, k, d, I, accumulate_dw};
+  DwArgs da_d = da;
+  da_d.queue = sc.queues + N_XCD * DW_QSTRIDE;
   const dim3 grid(persistent_blocks()), block(G_THREADS);
 #define FM_BWD(TT)                                                                                        \
   if (T > 0) {                                                                                            \
@@ -841,7 +932,7 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
     }
     hipLaunchKernelGGL(kb_dw_gu, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)X, (cbp)X_perm, (cbp)dAg,
                        (cbp)dAu, da);
-    hipLaunchKernelGGL(kb_dw_d, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)H, da);
+    hipLaunchKernelGGL(kb_dw_d, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)H, da_d);
   } else {
     FM_BWD(float)
   }
