@@ -123,6 +123,12 @@ template <typename T> __device__ __forceinline__ const FM_GLOBAL T* gptr(const T
 template <typename T> __device__ __forceinline__ FM_GLOBAL T* gptr(T* p) {
   return (FM_GLOBAL T*)(p);
 }
+// Load of a wave-uniform element of a table that no thread writes while the
+// kernel runs, through the scalar cache (constant address space): it neither
+// occupies the vector-memory counter nor waits on it.
+template <typename T> __device__ __forceinline__ T ld_scalar(const T* p) {
+  return *(const __attribute__((address_space(4))) T*)(p);
+}
 __device__ __forceinline__ u32x4_t ld16(const void* p) {
   return *(const FM_GLOBAL u32x4_t*)(p);
 }

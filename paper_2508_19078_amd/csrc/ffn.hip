@@ -42,8 +42,8 @@ struct SlotRows {
 __device__ __forceinline__ SlotRows slot_rows(int s, const int32_t* offsets, int S_r, int Tn, int k) {
   SlotRows r;
   if (s < S_r) {
-    const int b = offsets[s];
-    r.nrows = offsets[s + 1] - b;
+    const int b = ld_scalar(offsets + s);
+    r.nrows = ld_scalar(offsets + s + 1) - b;
     r.orow0 = b;
     r.xrow0 = b;
     r.shared = false;
@@ -59,21 +59,25 @@ __device__ __forceinline__ SlotRows slot_rows(int s, const int32_t* offsets, int
 // Schedule in the workspace: mbase[0..S] (prefix of row tiles per slot),
 // wbase[0..S] (prefix of weight-gradient work per slot, 64-bit), dorder[0..S]
 // (the tuning slots by decreasing rows, ties by index; dorder[S] = their
-// number) and the tile counters of the weight-gradient kernels (DW_QUEUES
-// queues of N_XCD counters, 128 bytes apart), zeroed by k_build_sched.
+// number), the tile counters of the weight-gradient kernels (DW_QUEUES
+// queues of N_XCD counters, 128 bytes apart), zeroed by k_build_sched, and a
+// store sink: the weight-gradient epilogues send the stores of lanes outside
+// the output there, so that every wave issues the same number of stores.
 constexpr int DW_QSTRIDE = 32;    // ints between two counters
 constexpr int DW_QUEUES = 2;      // dW_gate/up, dW_down
 constexpr int DW_QINTS = DW_QUEUES * N_XCD * DW_QSTRIDE;
+constexpr int DW_SINK = 4096;      // 16-byte slots of the store sink
 struct Sched {
   int32_t* mbase;
   long long* wbase;
   int32_t* dorder;
   int32_t* queues;
+  float* sink;
 };
 inline size_t round256(size_t b) { return (b + 255) / 256 * 256; }
 inline size_t sched_bytes(int S) {
   return 2 * round256(sizeof(int32_t) * (S + 1)) + round256(sizeof(long long) * (S + 1)) +
-         round256(sizeof(int32_t) * DW_QINTS);
+         round256(sizeof(int32_t) * DW_QINTS) + 16 * DW_SINK;
 }
 inline Sched sched_at(void* ws, int S) {
   Sched s;
@@ -85,6 +89,8 @@ inline Sched sched_at(void* ws, int S) {
   s.dorder = (int32_t*)p;
   p += round256(sizeof(int32_t) * (S + 1));
   s.queues = (int32_t*)p;
+  p += round256(sizeof(int32_t) * DW_QINTS);
+  s.sink = (float*)p;
   return s;
 }
 
@@ -138,7 +144,7 @@ __device__ __forceinline__ int find_slot(const B* base, int S, long long v) {
   int lo = 0, hi = S - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if ((long long)base[mid] <= v) lo = mid;
+    if ((long long)ld_scalar(base + mid) <= v) lo = mid;
     else hi = mid - 1;
   }
   return lo;
@@ -167,8 +173,9 @@ constexpr int GM_DW = 4;     // band height of the weight-gradient GEMMs
 __device__ __forceinline__ Tile row_tile(const int32_t* mbase, int S, int NT, long long t) {
   Tile r;
   r.s = find_slot(mbase, S, t / NT);
-  const int mt = mbase[r.s + 1] - mbase[r.s];
-  band_order((int)(t - (long long)mbase[r.s] * NT), mt, NT, GM_ROWS, r.m, r.n);
+  const int mb = ld_scalar(mbase + r.s);
+  const int mt = ld_scalar(mbase + r.s + 1) - mb;
+  band_order((int)(t - (long long)mb * NT), mt, NT, GM_ROWS, r.m, r.n);
   return r;
 }
 
@@ -224,6 +231,7 @@ struct DwArgs {
   const long long* wbase;
   const int32_t* dorder;
   int32_t* queue;   // this kernel's N_XCD counters
+  float* sink;      // DW_SINK 16-byte slots
   int S_r, S, Tn, k, d, I, accumulate;
 };
 
@@ -234,7 +242,7 @@ struct TileRange {
   int first, step;
 };
 __device__ __forceinline__ TileRange row_range(const RowArgs& ra, int NT) {
-  const long long total = (long long)ra.mbase[ra.S] * NT;
+  const long long total = (long long)ld_scalar(ra.mbase + ra.S) * NT;
   const int x = blockIdx.x % N_XCD;
   return TileRange{total * x / N_XCD, total * (x + 1) / N_XCD, (int)(blockIdx.x / N_XCD),
                    (int)(gridDim.x / N_XCD)};
@@ -261,10 +269,17 @@ struct DwQueue {
   __device__ __forceinline__ DwQueue(const DwArgs& da, int tps) {
     x = blockIdx.x % N_XCD;
     ctr = da.queue + x * DW_QSTRIDE;
-    total = (long long)da.dorder[da.S] * tps;
+    total = (long long)ld_scalar(da.dorder + da.S) * tps;
   }
-  // Thread 0 only.
-  __device__ __forceinline__ int draw() const { return atomicAdd(ctr, 1); }
+  // Thread 0 only.  The zero offset is opaque to the compiler, so the atomic
+  // stays a plain one: on a provably uniform address it would be rewritten into
+  // a wave-aggregated form that waits for its result (and so for every load and
+  // store of the wave still in flight) right where it is issued.
+  __device__ __forceinline__ int draw() const {
+    int z;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+    return atomicAdd(ctr + z, 1);
+  }
   __device__ __forceinline__ long long tile(int j) const { return (long long)j * N_XCD + x; }
   // Hands thread 0's draw to every thread (LDS word 0 must be free; the caller
   // keeps it until every wave has read it).
@@ -294,7 +309,7 @@ __global__ __launch_bounds__(G_THREADS) void kf_gate_up(LayerPtrs<T> W, const T*
     const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
     const T* xs = (sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d;
     Opnd<T> A[1] = {{xs, d, sr.nrows - m0, d}};
-    Opnd<T> B[2] = {{W.wg[rt.s] + (size_t)n0 * d, d, I - n0, d}, {W.wu[rt.s] + (size_t)n0 * d, d, I - n0, d}};
+    Opnd<T> B[2] = {{ld_scalar(W.wg + rt.s) + (size_t)n0 * d, d, I - n0, d}, {ld_scalar(W.wu + rt.s) + (size_t)n0 * d, d, I - n0, d}};
     Acc<T, 1, 2> acc;
     acc.zero();
     gemm_mainloop<T, true, true, 1, 2>(A, B, d, (T*)lds, acc);
@@ -328,7 +343,7 @@ __global__ __launch_bounds__(G_THREADS) void kf_down(LayerPtrs<T> W, const T* __
     const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
     const size_t ob = (size_t)(sr.orow0 + m0);
     Opnd<T> A[1] = {{H + ob * I, I, sr.nrows - m0, I}};
-    Opnd<T> B[1] = {{W.wd[rt.s] + (size_t)n0 * I, I, d - n0, I}};
+    Opnd<T> B[1] = {{ld_scalar(W.wd + rt.s) + (size_t)n0 * I, I, d - n0, I}};
     Acc<T, 1, 1> acc;
     acc.zero();
     gemm_mainloop<T, true, true, 1, 1>(A, B, I, (T*)lds, acc);
@@ -358,7 +373,7 @@ __global__ __launch_bounds__(G_THREADS) void kf_dh(LayerPtrs<T> W, const T* __re
     const size_t ob = (size_t)(sr.orow0 + m0);
     // B(n = intermediate index, k = hidden index) = W_down[k][n]: MN-contiguous
     Opnd<T> A[1] = {{dO + ob * d, d, sr.nrows - m0, d}};
-    Opnd<T> B[1] = {{W.wd[rt.s] + n0, I, I - n0, d}};
+    Opnd<T> B[1] = {{ld_scalar(W.wd + rt.s) + n0, I, I - n0, d}};
     Acc<T, 1, 1> acc;
     acc.zero();
     gemm_mainloop<T, true, false, 1, 1>(A, B, d, (T*)lds, acc);
@@ -398,12 +413,12 @@ __global__ __launch_bounds__(G_THREADS) void kf_dx(LayerPtrs<T> W, const T* __re
     acc.zero();
     {  // B(n = hidden index, k = intermediate index) = W_gate[k][n]
       Opnd<T> A[1] = {{dAg + ob * I, I, sr.nrows - m0, I}};
-      Opnd<T> B[1] = {{W.wg[rt.s] + n0, d, d - n0, I}};
+      Opnd<T> B[1] = {{ld_scalar(W.wg + rt.s) + n0, d, d - n0, I}};
       gemm_mainloop<T, true, false, 1, 1>(A, B, I, (T*)lds, acc);
     }
     {
       Opnd<T> A[1] = {{dAu + ob * I, I, sr.nrows - m0, I}};
-      Opnd<T> B[1] = {{W.wu[rt.s] + n0, d, d - n0, I}};
+      Opnd<T> B[1] = {{ld_scalar(W.wu + rt.s) + n0, d, d - n0, I}};
       gemm_mainloop<T, true, false, 1, 1>(A, B, I, (T*)lds, acc);
     }
 #pragma unroll
@@ -432,8 +447,8 @@ __global__ __launch_bounds__(G_THREADS) void kf_dw_gu(LayerPtrs<T> W, const T* _
   const TileRange tr = dw_range(da, MT * NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = dw_tile(t, MT * NT, MT);
-    float* dwg = W.dwg[rt.s];
-    float* dwu = W.dwu[rt.s];
+    float* dwg = ld_scalar(W.dwg + rt.s);
+    float* dwu = ld_scalar(W.dwu + rt.s);
     if (dwg && dwu) {
       const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
       const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
@@ -466,7 +481,7 @@ __global__ __launch_bounds__(G_THREADS) void kf_dw_d(LayerPtrs<T> W, const T* __
   const TileRange tr = dw_range(da, MT * NT);
   for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
     const Tile rt = dw_tile(t, MT * NT, MT);
-    float* dwd = W.dwd[rt.s];
+    float* dwd = ld_scalar(W.dwd + rt.s);
     if (dwd) {
       const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
       const int m0 = rt.m * G_BM, n0 = rt.n * G_BN;
@@ -491,9 +506,11 @@ __global__ __launch_bounds__(G_THREADS) void kf_dw_d(LayerPtrs<T> W, const T* __
 
 typedef const bf16* cbp;
 
-// Block tile of every bf16 product: 256 x 256, waves 2 x 4 (128 x 64 each),
-// 64-deep slabs, three of A and two of B in LDS (160 KB).
-using CB = B16Cfg<256, 256, 2, 64, 3, 2>;
+// Block tile of every bf16 product: 256 x 256, waves 2 x 4 (128 x 64 each, two
+// per SIMD), 64-deep slabs, three of A and two of B in LDS (160 KB).  (One wave
+// per SIMD with 128 x 128 each reads a third less LDS but measured slower: a
+// lone wave cannot hide its own LDS-read and DMA-issue stalls.)
+using CB = B16Cfg<256, 256, 2, 4, 64, 3, 2>;
 constexpr int B16_ROWS = CB::RA;   // rows per row tile of the bf16 kernels
 
 // Physical index of logical row / column c of an operand that interleaves two
@@ -516,7 +533,7 @@ __device__ __forceinline__ void b16_store_staged(const B16Acc<C::MI, C::NJ>& acc
         S::put4(lds, c.row, c.col4, acc.quad(i, j, q));
       }
   barrier_lds_writes();
-  S::template copy_out<C::RA>(lds, out, ld, rows, cols);
+  S::template copy_out<C::RA, C::THREADS>(lds, out, ld, rows, cols);
   barrier_lds();
 }
 
@@ -525,31 +542,34 @@ __device__ __forceinline__ void b16_store_staged(const B16Acc<C::MI, C::NJ>& acc
 // (the precision a bf16 product would hand to the elementwise step), the
 // whole tile at once; every lane then takes 8-column chunks of a row (16-byte
 // loads of A_g, A_u and stores of dA_g, dA_u; a wave covers whole rows).  The
-// loads of the first PRE chunks are issued before the tile is staged, so their
-// latency overlaps the LDS writes.  Pointers are at the tile origin; rows x
-// cols are valid.
+// chunks go in groups of G per lane; the loads of the first group are issued
+// before the tile is staged, so their latency overlaps the LDS writes.
+// Pointers are at the tile origin; rows x cols are valid.
 template <class C>
 __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& acc, FM_LDS char* lds,
                                                    const bf16* Ag, const bf16* Au, bf16* dAg, bf16* dAu,
                                                    size_t ld, int rows, int cols) {
   using S = Stage<bf16, C::RB>;
   constexpr int CH = C::RB / 8;                     // 8-column chunks per row
-  constexpr int PER = C::RA * CH / B16_THREADS;     // chunks per lane
-  constexpr int PRE = PER / 2;
-  static_assert(PER * B16_THREADS == C::RA * CH && C::RA * C::RB * 2 <= C::LDS, "whole chunks per lane");
+  constexpr int PER = C::RA * CH / C::THREADS;      // chunks per lane
+  constexpr int G = 8;                              // chunks in flight per lane
+  static_assert(PER % G == 0 && PER * C::THREADS == C::RA * CH && C::RA * C::RB * 2 <= C::LDS,
+                "whole chunks per lane");
   // thread index re-read here (opaque), so that the per-chunk addresses are
   // not hoisted out of the tile loop and kept live through the main loop
   const int tid = wave_id() * 64 + lane_id_here();
-  u32x4_t ga[PER], ua[PER];
-  auto load = [&](int u) {
-    const int idx = tid + u * B16_THREADS, r = idx / CH, c = (idx % CH) * 8;
-    if (r < rows && c < cols) {
-      ga[u] = ld16(Ag + (size_t)r * ld + c);
-      ua[u] = ld16(Au + (size_t)r * ld + c);
+  u32x4_t ga[G], ua[G];
+  auto load = [&](int g) {
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const int idx = tid + (g * G + u) * C::THREADS, r = idx / CH, c = (idx % CH) * 8;
+      if (r < rows && c < cols) {
+        ga[u] = ld16(Ag + (size_t)r * ld + c);
+        ua[u] = ld16(Au + (size_t)r * ld + c);
+      }
     }
   };
-#pragma unroll
-  for (int u = 0; u < PRE; ++u) load(u);
+  load(0);
 #pragma unroll
   for (int i = 0; i < C::MI; ++i)
 #pragma unroll
@@ -561,24 +581,26 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
       }
   barrier_lds_writes();
 #pragma unroll
-  for (int u = PRE; u < PER; ++u) load(u);
+  for (int g = 0; g < PER / G; ++g) {
+    if (g > 0) load(g);
 #pragma unroll
-  for (int u = 0; u < PER; ++u) {
-    const int idx = tid + u * B16_THREADS, r = idx / CH, c = (idx % CH) * 8;
-    if (r < rows && c < cols) {
-      float dh[8], a[8], up[8], dg[8], du[8];
-      const u32x4_t hv = *(const FM_LDS u32x4_t*)(lds + S::at(r, c));
-      unpack16(hv, dh, (bf16*)nullptr);
-      unpack16(ga[u], a, (bf16*)nullptr);
-      unpack16(ua[u], up, (bf16*)nullptr);
+    for (int u = 0; u < G; ++u) {
+      const int idx = tid + (g * G + u) * C::THREADS, r = idx / CH, c = (idx % CH) * 8;
+      if (r < rows && c < cols) {
+        float dh[8], a[8], up[8], dg[8], du[8];
+        const u32x4_t hv = *(const FM_LDS u32x4_t*)(lds + S::at(r, c));
+        unpack16(hv, dh, (bf16*)nullptr);
+        unpack16(ga[u], a, (bf16*)nullptr);
+        unpack16(ua[u], up, (bf16*)nullptr);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float sg = sigm_fast(a[e]);
-        du[e] = dh[e] * a[e] * sg;
-        dg[e] = dh[e] * up[e] * sg * (1.0f + a[e] * (1.0f - sg));
+        for (int e = 0; e < 8; ++e) {
+          const float sg = sigm_fast(a[e]);
+          du[e] = dh[e] * a[e] * sg;
+          dg[e] = dh[e] * up[e] * sg * (1.0f + a[e] * (1.0f - sg));
+        }
+        st16(dAg + (size_t)r * ld + c, pack16(dg, (bf16*)nullptr));
+        st16(dAu + (size_t)r * ld + c, pack16(du, (bf16*)nullptr));
       }
-      st16(dAg + (size_t)r * ld + c, pack16(dg, (bf16*)nullptr));
-      st16(dAu + (size_t)r * ld + c, pack16(du, (bf16*)nullptr));
     }
   }
   barrier_lds();
@@ -588,7 +610,7 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
 // interleaves 32-row blocks of W_gate and W_up (128 intermediate columns per
 // 256-row tile): tile j = 2jj of a wave holds gate and j = 2jj + 1 up of the
 // same columns.
-__global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp X, cbp Xp, RowArgs ra,
+__global__ __launch_bounds__(CB::THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp X, cbp Xp, RowArgs ra,
                                                           bf16* Ag, bf16* Au, bf16* H) {
   __shared__ __align__(16) char lds[CB::LDS];
   const int d = ra.d, I = ra.I, NT = (I + CB::RB / 2 - 1) / (CB::RB / 2);
@@ -598,7 +620,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
     const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
     const int m0 = rt.m * CB::RA, n0 = rt.n * (CB::RB / 2);
     const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, sr.nrows - m0, d};
-    const B16Src B{W.wg[rt.s] + (size_t)n0 * d, W.wu[rt.s] + (size_t)n0 * d, d, I - n0, d};
+    const B16Src B{ld_scalar(W.wg + rt.s) + (size_t)n0 * d, ld_scalar(W.wu + rt.s) + (size_t)n0 * d, d, I - n0, d};
     B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
     b16_gemm<CB, true, true, false, true>(A, B, d, (FM_LDS char*)lds, acc);
@@ -619,8 +641,8 @@ __global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
           SG::put4(su, c.row, deinter(c.col4), acc.quad(i, 2 * jj + 1, q));
         }
     barrier_lds_writes();
-    SG::template copy_out<CB::RA>(sg, Ag + ob * I + n0, I, rows, cols);
-    SG::template copy_out<CB::RA>(su, Au + ob * I + n0, I, rows, cols);
+    SG::template copy_out<CB::RA, CB::THREADS>(sg, Ag + ob * I + n0, I, rows, cols);
+    SG::template copy_out<CB::RA, CB::THREADS>(su, Au + ob * I + n0, I, rows, cols);
     barrier_lds();
 #pragma unroll
     for (int i = 0; i < CB::MI; ++i)
@@ -636,13 +658,13 @@ __global__ __launch_bounds__(B16_THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
           SG::put4(sg, c.row, deinter(c.col4), h);
         }
     barrier_lds_writes();
-    SG::template copy_out<CB::RA>(sg, H + ob * I + n0, I, rows, cols);
+    SG::template copy_out<CB::RA, CB::THREADS>(sg, H + ob * I + n0, I, rows, cols);
     barrier_lds();
   }
 }
 
 // O = H W_down^T
-__global__ __launch_bounds__(B16_THREADS) void kb_down(LayerPtrs<bf16> W, cbp H, RowArgs ra, bf16* O) {
+__global__ __launch_bounds__(CB::THREADS) void kb_down(LayerPtrs<bf16> W, cbp H, RowArgs ra, bf16* O) {
   __shared__ __align__(16) char lds[CB::LDS];
   const int d = ra.d, I = ra.I, NT = (d + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
@@ -652,7 +674,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_down(LayerPtrs<bf16> W, cbp H,
     const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
     const size_t ob = (size_t)(sr.orow0 + m0);
     const B16Src A{H + ob * I, nullptr, I, sr.nrows - m0, I};
-    const B16Src B{W.wd[rt.s] + (size_t)n0 * I, nullptr, I, d - n0, I};
+    const B16Src B{ld_scalar(W.wd + rt.s) + (size_t)n0 * I, nullptr, I, d - n0, I};
     B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
     b16_gemm<CB, true, true>(A, B, I, (FM_LDS char*)lds, acc);
@@ -661,7 +683,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_down(LayerPtrs<bf16> W, cbp H,
 }
 
 // dH = dO W_down (B = W_down read k-major), epilogue dA_g, dA_u.
-__global__ __launch_bounds__(B16_THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, cbp Ag, cbp Au, RowArgs ra,
+__global__ __launch_bounds__(CB::THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, cbp Ag, cbp Au, RowArgs ra,
                                                      bf16* dAg, bf16* dAu) {
   __shared__ __align__(16) char lds[CB::LDS];
   const int d = ra.d, I = ra.I, NT = (I + CB::RB - 1) / CB::RB;
@@ -673,7 +695,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
     const size_t ob = (size_t)(sr.orow0 + m0);
     // B(n = intermediate index, k = hidden index) = W_down[k][n]
     const B16Src A{dO + ob * d, nullptr, d, sr.nrows - m0, d};
-    const B16Src B{W.wd[rt.s] + n0, nullptr, I, I - n0, d};
+    const B16Src B{ld_scalar(W.wd + rt.s) + n0, nullptr, I, I - n0, d};
     B16Acc<CB::MI, CB::NJ> acc;
     acc.zero();
     b16_gemm<CB, true, false>(A, B, d, (FM_LDS char*)lds, acc);
@@ -683,7 +705,7 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
 }
 
 // dX_s = dA_g W_gate + dA_u W_up (two K passes, B read k-major).
-__global__ __launch_bounds__(B16_THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg, cbp dAu, RowArgs ra,
+__global__ __launch_bounds__(CB::THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg, cbp dAu, RowArgs ra,
                                                      bf16* dXp) {
   __shared__ __align__(16) char lds[CB::LDS];
   const int d = ra.d, I = ra.I, NT = (d + CB::RB - 1) / CB::RB;
@@ -697,43 +719,92 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg,
     acc.zero();
     // B(n = hidden index, k = intermediate index) = W_gate[k][n], then W_up
     b16_gemm<CB, true, false>(B16Src{dAg + ob * I, nullptr, I, sr.nrows - m0, I},
-                              B16Src{W.wg[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
+                              B16Src{ld_scalar(W.wg + rt.s) + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
     b16_gemm<CB, true, false>(B16Src{dAu + ob * I, nullptr, I, sr.nrows - m0, I},
-                              B16Src{W.wu[rt.s] + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
+                              B16Src{ld_scalar(W.wu + rt.s) + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
     b16_store_staged<CB>(acc, (FM_LDS char*)lds, dXp + ob * d + n0, d, sr.nrows - m0, d - n0);
   }
+}
+
+// Weight-gradient tiles of one kernel run as a pipeline: the next tile's first
+// slabs are issued (b16_prologue) before the current tile's epilogue stores,
+// so the stores drain while those slabs land.  Every wave issues exactly
+// MI x NJ x 4 stores per tile (lanes outside the output write to the sink),
+// which the next product's first wait may leave in flight; with accumulate
+// each store is preceded by a load and the wait counts none of them.
+template <bool ACCUM> struct DwEpi {
+  static constexpr int STORES = CB::MI * CB::NJ * 4;
+  static constexpr int EXTRA = ACCUM ? 0 : STORES;
+};
+
+__device__ __forceinline__ float* dw_sink(const DwArgs& da) {
+  return da.sink + (size_t)((blockIdx.x * CB::THREADS + threadIdx.x) & (DW_SINK - 1)) * 4;
 }
 
 // dW_gate = dA_g^T X_s and dW_up = dA_u^T X_s in one product: the A tile
 // interleaves 32-column blocks of dA_g and dA_u (128 intermediate rows of both
 // per 256-row tile), B = X_s; both read k-major.
-__global__ __launch_bounds__(B16_THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X, cbp Xp, cbp dAg, cbp dAu,
+struct DwGuTile {
+  float* dwg;
+  float* dwu;
+  int m0, n0, K;
+  bool run;
+  B16Src A, B;
+  __device__ __forceinline__ void init(const LayerPtrs<bf16>& W, cbp X, cbp Xp, cbp dAg, cbp dAu, const DwArgs& da,
+                                      long long t, int MT, int NT) {
+    Tile rt = dw_tile(t, MT * NT, MT);
+    rt.s = ld_scalar(da.dorder + rt.s);
+    dwg = ld_scalar(W.dwg + rt.s);
+    dwu = ld_scalar(W.dwu + rt.s);
+    run = dwg && dwu;
+    const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
+    const int d = da.d, I = da.I;
+    m0 = rt.m * (CB::RA / 2);
+    n0 = rt.n * CB::RB;
+    K = sr.nrows;
+    A = B16Src{dAg + (size_t)sr.orow0 * I + m0, dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows};
+    B = B16Src{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, nullptr, d, d - n0, sr.nrows};
+  }
+};
+
+template <bool ACCUM>
+__global__ __launch_bounds__(CB::THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X, cbp Xp, cbp dAg, cbp dAu,
                                                         DwArgs da) {
   __shared__ __align__(16) char lds[CB::LDS];
   FM_LDS char* const l = (FM_LDS char*)lds;
   const int d = da.d, I = da.I;
   const int MT = (I + CB::RA / 2 - 1) / (CB::RA / 2), NT = (d + CB::RB - 1) / CB::RB;
   const DwQueue qu(da, MT * NT);
+  float* const sink = dw_sink(da);
   int j = DwQueue::share(l, threadIdx.x == 0 ? qu.draw() : 0);
   barrier_lds();
-  for (long long t = qu.tile(j); t < qu.total; t = qu.tile(j)) {
-    const int next = threadIdx.x == 0 ? qu.draw() : 0;
-    Tile rt = dw_tile(t, MT * NT, MT);
-    rt.s = da.dorder[rt.s];
-    float* dwg = W.dwg[rt.s];
-    float* dwu = W.dwu[rt.s];
-    const bool run = dwg && dwu;
-    const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
-    const int m0 = rt.m * (CB::RA / 2), n0 = rt.n * CB::RB;
+  long long t = qu.tile(j);
+  if (t < qu.total) {
+    DwGuTile o;
+    o.init(W, X, Xp, dAg, dAu, da, t, MT, NT);
+    if (o.run) b16_prologue<CB, false, false, true, false>(o.A, o.B, o.K, l);
+  }
+  bool stored = false;   // the previous tile's stores may be in flight
+  while (t < qu.total) {
+    int next;   // meaningful in thread 0 only
+    if (threadIdx.x == 0) next = qu.draw();
+    DwGuTile o;   // tile tables are read through the scalar cache
+    o.init(W, X, Xp, dAg, dAu, da, t, MT, NT);
     B16Acc<CB::MI, CB::NJ> acc;
-    if (run) {
-      const B16Src A{dAg + (size_t)sr.orow0 * I + m0, dAu + (size_t)sr.orow0 * I + m0, I, I - m0, sr.nrows};
-      const B16Src B{(sr.shared ? X : Xp) + (size_t)sr.xrow0 * d + n0, nullptr, d, d - n0, sr.nrows};
+    if (o.run) {
       acc.zero();
-      b16_gemm<CB, false, false, true, false>(A, B, sr.nrows, l, acc);
+      b16_gemm<CB, false, false, true, false, DwEpi<ACCUM>::EXTRA>(o.A, o.B, o.K, l, acc, stored);
     }
     j = DwQueue::share(l, next);
-    if (run) {
+    barrier_lds();   // every wave has read the draw before the next tile's DMA
+    t = qu.tile(j);
+    if (t < qu.total) {
+      DwGuTile on;
+      on.init(W, X, Xp, dAg, dAu, da, t, MT, NT);
+      if (on.run) b16_prologue<CB, false, false, true, false>(on.A, on.B, on.K, l);
+    }
+    stored = o.run;
+    if (o.run) {
 #pragma unroll
       for (int i = 0; i < CB::MI; ++i)
 #pragma unroll
@@ -741,41 +812,73 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const AccCoord c = b16_coord<CB>(i, jj, q);
-            const int m = m0 + deinter(c.row), n = n0 + c.col4;
-            if (m >= I || n >= d) continue;
-            float* dst = ((c.row >> 5) & 1) ? dwu : dwg;
-            store_dw(dst + (size_t)m * d + n, acc.quad(i, jj, q), da.accumulate);
+            const int m = o.m0 + deinter(c.row), n = o.n0 + c.col4;
+            float* dst = (m < I && n < d) ? (((c.row >> 5) & 1) ? o.dwu : o.dwg) + (size_t)m * d + n : sink;
+            store_dw(dst, acc.quad(i, jj, q), ACCUM);
           }
     }
-    barrier_lds();   // every wave has read the draw before the next tile's DMA
   }
 }
 
 // dW_down = dO^T H (both read k-major).
-__global__ __launch_bounds__(B16_THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO, cbp H, DwArgs da) {
+struct DwDTile {
+  float* dwd;
+  int m0, n0, K;
+  bool run;
+  B16Src A, B;
+  __device__ __forceinline__ void init(const LayerPtrs<bf16>& W, cbp dO, cbp H, const DwArgs& da, long long t, int MT,
+                                      int NT) {
+    Tile rt = dw_tile(t, MT * NT, MT);
+    rt.s = ld_scalar(da.dorder + rt.s);
+    dwd = ld_scalar(W.dwd + rt.s);
+    run = dwd != nullptr;
+    const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
+    const int d = da.d, I = da.I;
+    m0 = rt.m * CB::RA;
+    n0 = rt.n * CB::RB;
+    K = sr.nrows;
+    A = B16Src{dO + (size_t)sr.orow0 * d + m0, nullptr, d, d - m0, sr.nrows};
+    B = B16Src{H + (size_t)sr.orow0 * I + n0, nullptr, I, I - n0, sr.nrows};
+  }
+};
+
+template <bool ACCUM>
+__global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO, cbp H, DwArgs da) {
   __shared__ __align__(16) char lds[CB::LDS];
   FM_LDS char* const l = (FM_LDS char*)lds;
   const int d = da.d, I = da.I;
   const int MT = (d + CB::RA - 1) / CB::RA, NT = (I + CB::RB - 1) / CB::RB;
   const DwQueue qu(da, MT * NT);
+  float* const sink = dw_sink(da);
   int j = DwQueue::share(l, threadIdx.x == 0 ? qu.draw() : 0);
   barrier_lds();
-  for (long long t = qu.tile(j); t < qu.total; t = qu.tile(j)) {
-    const int next = threadIdx.x == 0 ? qu.draw() : 0;
-    Tile rt = dw_tile(t, MT * NT, MT);
-    rt.s = da.dorder[rt.s];
-    float* dwd = W.dwd[rt.s];
-    const SlotRows sr = slot_rows(rt.s, da.offsets, da.S_r, da.Tn, da.k);
-    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
+  long long t = qu.tile(j);
+  if (t < qu.total) {
+    DwDTile o;
+    o.init(W, dO, H, da, t, MT, NT);
+    if (o.run) b16_prologue<CB, false, false>(o.A, o.B, o.K, l);
+  }
+  bool stored = false;
+  while (t < qu.total) {
+    int next;   // meaningful in thread 0 only
+    if (threadIdx.x == 0) next = qu.draw();
+    DwDTile o;
+    o.init(W, dO, H, da, t, MT, NT);
     B16Acc<CB::MI, CB::NJ> acc;
-    if (dwd) {
-      const B16Src A{dO + (size_t)sr.orow0 * d + m0, nullptr, d, d - m0, sr.nrows};
-      const B16Src B{H + (size_t)sr.orow0 * I + n0, nullptr, I, I - n0, sr.nrows};
+    if (o.run) {
       acc.zero();
-      b16_gemm<CB, false, false>(A, B, sr.nrows, l, acc);
+      b16_gemm<CB, false, false, false, false, DwEpi<ACCUM>::EXTRA>(o.A, o.B, o.K, l, acc, stored);
     }
     j = DwQueue::share(l, next);
-    if (dwd) {
+    barrier_lds();
+    t = qu.tile(j);
+    if (t < qu.total) {
+      DwDTile on;
+      on.init(W, dO, H, da, t, MT, NT);
+      if (on.run) b16_prologue<CB, false, false>(on.A, on.B, on.K, l);
+    }
+    stored = o.run;
+    if (o.run) {
 #pragma unroll
       for (int i = 0; i < CB::MI; ++i)
 #pragma unroll
@@ -783,12 +886,11 @@ __global__ __launch_bounds__(B16_THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const AccCoord c = b16_coord<CB>(i, jj, q);
-            const int m = m0 + c.row, n = n0 + c.col4;
-            if (m >= d || n >= I) continue;
-            store_dw(dwd + (size_t)m * I + n, acc.quad(i, jj, q), da.accumulate);
+            const int m = o.m0 + c.row, n = o.n0 + c.col4;
+            float* dst = (m < d && n < I) ? o.dwd + (size_t)m * I + n : sink;
+            store_dw(dst, acc.quad(i, jj, q), ACCUM);
           }
     }
-    barrier_lds();   // every wave has read the draw before the next tile's DMA
   }
 }
 
@@ -867,7 +969,7 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
                      ra, (TT*)A_g, (TT*)A_u, (TT*)H);                                                   \
   hipLaunchKernelGGL(kf_down<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)H, ra, (TT*)O);
   if (L->dtype == MOE_BF16) {
-    const dim3 b8(B16_THREADS);
+    const dim3 b8(CB::THREADS);
     hipLaunchKernelGGL(kb_gate_up, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)X, (cbp)X_perm, ra, (bf16*)A_g,
                        (bf16*)A_u, (bf16*)H);
     hipLaunchKernelGGL(kb_down, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)H, ra, (bf16*)O);
@@ -909,7 +1011,7 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, tile_rows,
                      L->dw_gate, sc.mbase, sc.wbase, sc.dorder, sc.queues);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, d, I};
-  const DwArgs da{offsets, sc.wbase, sc.dorder, sc.queues, L->S_routed, S, T, k, d, I, accumulate_dw};
+  const DwArgs da{offsets, sc.wbase, sc.dorder, sc.queues, sc.sink, L->S_routed, S, T, k, d, I, accumulate_dw};
   DwArgs da_d = da;
   da_d.queue = sc.queues + N_XCD * DW_QSTRIDE;
   const dim3 grid(persistent_blocks()), block(G_THREADS);
@@ -924,15 +1026,21 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
                      (const TT*)dAg, (const TT*)dAu, da);                                                \
   hipLaunchKernelGGL(kf_dw_d<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)H, da);
   if (L->dtype == MOE_BF16) {
-    const dim3 b8(B16_THREADS);
+    const dim3 b8(CB::THREADS);
     if (T > 0) {
       hipLaunchKernelGGL(kb_dh, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)A_g, (cbp)A_u, ra,
                          (bf16*)dAg, (bf16*)dAu);
       hipLaunchKernelGGL(kb_dx, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dAg, (cbp)dAu, ra, (bf16*)dX_perm);
     }
-    hipLaunchKernelGGL(kb_dw_gu, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)X, (cbp)X_perm, (cbp)dAg,
-                       (cbp)dAu, da);
-    hipLaunchKernelGGL(kb_dw_d, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)H, da_d);
+    if (accumulate_dw) {
+      hipLaunchKernelGGL(kb_dw_gu<true>, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)X, (cbp)X_perm, (cbp)dAg,
+                         (cbp)dAu, da);
+      hipLaunchKernelGGL(kb_dw_d<true>, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)H, da_d);
+    } else {
+      hipLaunchKernelGGL(kb_dw_gu<false>, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)X, (cbp)X_perm, (cbp)dAg,
+                         (cbp)dAu, da);
+      hipLaunchKernelGGL(kb_dw_d<false>, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)H, da_d);
+    }
   } else {
     FM_BWD(float)
   }

@@ -1,8 +1,8 @@
-// bf16 grouped-GEMM core for gfx950: 8-wave blocks, a multi-stage
-// direct-to-LDS ring and register double-buffered MFMA fragments.
+// bf16 grouped-GEMM core for gfx950: persistent blocks of 4 or 8 waves, a
+// multi-stage direct-to-LDS ring and register double-buffered MFMA fragments.
 //
-// A block of 512 threads (8 waves, two per SIMD) computes an RA x RB output
-// tile of C = sum_k A(r, k) B(n, k).  The waves form a WM x WN grid; each owns
+// A block of WM x WN waves computes an RA x RB output tile of
+// C = sum_k A(r, k) B(n, k).  The waves form a WM x WN grid; each owns
 // a TM x TN sub-tile as MI x NJ v_mfma_f32_32x32x16_bf16 tiles (the bf16 shape
 // that reaches the chip's MFMA peak), operands swapped so that a lane holds
 // groups of four consecutive output columns.
@@ -43,26 +43,25 @@
 
 namespace fm {
 
-constexpr int B16_THREADS = 512;                // 8 waves
-
 #define FM_LDS __attribute__((address_space(3)))
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-// Tile configuration: RA x RB block tile, WM waves along RA, BK k per slab,
+// Tile configuration: RA x RB block tile, WM x WN waves, BK k per slab,
 // separate LDS rings of NSA slabs for A and NSB slabs for B (NSA = NSB + 1: the
 // A operand, the one that streams, gets one more slab of latency tolerance).
-template <int RA_, int RB_, int WM_, int BK_, int NSA_, int NSB_> struct B16Cfg {
-  static constexpr int RA = RA_, RB = RB_, WM = WM_, WN = 8 / WM_, BK = BK_, NSA = NSA_, NSB = NSB_;
+template <int RA_, int RB_, int WM_, int WN_, int BK_, int NSA_, int NSB_> struct B16Cfg {
+  static constexpr int RA = RA_, RB = RB_, WM = WM_, WN = WN_, BK = BK_, NSA = NSA_, NSB = NSB_;
+  static constexpr int NW = WM * WN, THREADS = 64 * NW;
   static constexpr int TM = RA / WM, TN = RB / WN;    // wave sub-tile
   static constexpr int MI = TM / 32, NJ = TN / 32;    // MFMA tiles per wave
   static constexpr int KS = BK / 16;                  // MFMA k-steps per slab
   static constexpr int A_BYTES = RA * BK * 2, B_BYTES = RB * BK * 2;
   static constexpr int B_BASE = NSA * A_BYTES;        // B ring follows the A ring
   static constexpr int LDS = NSA * A_BYTES + NSB * B_BYTES;
-  static constexpr int A_INS = RA * BK * 2 / 8192;    // DMA instructions per wave and slab
-  static constexpr int B_INS = RB * BK * 2 / 8192;
-  static_assert(WM * WN == 8 && TM % 32 == 0 && TN % 32 == 0, "8 waves of 32-multiples");
+  static constexpr int A_INS = RA * BK * 2 / 1024 / NW;   // DMA instructions per wave and slab
+  static constexpr int B_INS = RB * BK * 2 / 1024 / NW;
+  static_assert((NW == 4 || NW == 8) && TM % 32 == 0 && TN % 32 == 0, "4 or 8 waves of 32-multiples");
   static_assert(BK == 64, "slab depth: two 32-k halves per slab");
   static_assert(A_INS >= 1 && B_INS >= 1 && KS % 2 == 0, "whole DMA instructions per wave");
   static_assert(NSB >= 2 && NSA == NSB + 1 && LDS <= 160 * 1024, "LDS rings");
@@ -364,10 +363,11 @@ template <typename T, int COLS> struct Stage {
       *(FM_LDS f32x4_t*)p = v;
     }
   }
-  // Copies rows [0, ROWS) of the staged tile out: row r goes to row_ptr(r)
-  // (nullptr: not stored), columns below cols_valid (a multiple of EPC); with
-  // accumulate (float only) the values are added to what the output holds.
-  template <int ROWS, class RowPtr>
+  // Copies rows [0, ROWS) of the staged tile out with NT threads: row r goes to
+  // row_ptr(r) (nullptr: not stored), columns below cols_valid (a multiple of
+  // EPC); with accumulate (float only) the values are added to what the output
+  // holds.
+  template <int ROWS, int NT, class RowPtr>
   static __device__ __forceinline__ void copy_rows(const FM_LDS char* lds, RowPtr row_ptr, int cols_valid,
                                                    bool accumulate = false) {
     constexpr int TOTAL = ROWS * CPR;
@@ -375,7 +375,7 @@ template <typename T, int COLS> struct Stage {
     // registers of a surrounding tile loop
     const int tid = wave_id() * 64 + lane_id_here();
 #pragma unroll 4
-    for (int idx = tid; idx < TOTAL; idx += B16_THREADS) {
+    for (int idx = tid; idx < TOTAL; idx += NT) {
       const int row = idx / CPR, c = idx % CPR;
       u32x4_t v = *(const FM_LDS u32x4_t*)(lds + row * ROW_BYTES + ((c ^ (row & (CPR - 1))) << 4));
       T* out = row_ptr(row);
@@ -390,10 +390,10 @@ template <typename T, int COLS> struct Stage {
     }
   }
   // Rows [0, ROWS) to out[row * ld + col] for row < rows_valid.
-  template <int ROWS>
+  template <int ROWS, int NT>
   static __device__ __forceinline__ void copy_out(const FM_LDS char* lds, T* out, size_t ld, int rows_valid,
                                                   int cols_valid) {
-    copy_rows<ROWS>(lds, [=](int row) { return row < rows_valid ? out + (size_t)row * ld : (T*)nullptr; },
+    copy_rows<ROWS, NT>(lds, [=](int row) { return row < rows_valid ? out + (size_t)row * ld : (T*)nullptr; },
                     cols_valid);
   }
 };
@@ -420,34 +420,82 @@ __device__ __forceinline__ void barrier_lds_writes() {
 // the other half, which hides the read latency.  The loop body is straight-line
 // code, so the LDS-read wait counts stay exact.  The last slabs (and the partial
 // one) drain through a general version of the same step.
+// The DMA side of one product: slab issue into the two rings.
+template <class C, bool AKC, bool BKC, bool AI, bool BI> struct B16Pipe {
+  static constexpr int BK = C::BK, NSA = C::NSA, NSB = C::NSB;
+  B16Dma<AKC, C::RA, C::A_INS, AI> da;
+  B16Dma<BKC, C::RB, C::B_INS, BI> db;
+  const B16Src& A;
+  const B16Src& B;
+  FM_LDS char* lds;
+  int nk, nfull;
+
+  __device__ __forceinline__ B16Pipe(const B16Src& A_, const B16Src& B_, int K, FM_LDS char* lds_)
+      : A(A_), B(B_), lds(lds_) {
+    nk = (K + BK - 1) / BK;
+    nfull = K / BK;
+    if (nk > 0) {
+      da.init(A);
+      db.init(B);
+    }
+  }
+  __device__ __forceinline__ FM_LDS char* abuf(int s) const { return lds + (s % NSA) * C::A_BYTES; }
+  __device__ __forceinline__ FM_LDS char* bbuf(int s) const { return lds + C::B_BASE + (s % NSB) * C::B_BYTES; }
+  __device__ __forceinline__ void issue_a(int s) const {
+    if (s < nfull) da.issue_full(s, abuf(s));
+    else da.issue_tail(A, s * BK, abuf(s));
+  }
+  __device__ __forceinline__ void issue_b(int s) const {
+    if (s < nfull) db.issue_full(s, bbuf(s));
+    else db.issue_tail(B, s * BK, bbuf(s));
+  }
+  // B(0) A(0) B(1) A(1) ... B(NSB-1) A(NSB-1) A(NSA-1), as far as there are slabs.
+  __device__ __forceinline__ void prologue() const {
+#pragma nounroll
+    for (int s = 0; s < NSA && s < nk; ++s) {
+      if (s < NSB) issue_b(s);
+      issue_a(s);
+    }
+  }
+};
+
+// Issues the prologue of a product ahead of its b16_gemm call (which then takes
+// EXTRA >= 0): a persistent kernel starts the next tile's first slabs before the
+// previous tile's epilogue stores, so those stores drain while the slabs land.
+// The LDS rings must be free (no reads or DMA of the previous tile pending).
 template <class C, bool AKC, bool BKC, bool AI = false, bool BI = false>
+__device__ __forceinline__ void b16_prologue(const B16Src& A, const B16Src& B, int K, FM_LDS char* lds) {
+  const B16Pipe<C, AKC, BKC, AI, BI> pp(A, B, K, lds);
+  pp.prologue();
+}
+
+// EXTRA < 0: the product issues its own prologue.  EXTRA >= 0: b16_prologue
+// issued it already (same A, B, K); with extra_issued the wave has issued at
+// least EXTRA more vector-memory instructions since, which may stay in flight
+// at the first wait.
+template <class C, bool AKC, bool BKC, bool AI = false, bool BI = false, int EXTRA = -1>
 __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K, FM_LDS char* lds,
-                                         B16Acc<C::MI, C::NJ>& acc) {
+                                         B16Acc<C::MI, C::NJ>& acc, bool extra_issued = true) {
   constexpr int BK = C::BK, NSA = C::NSA, NSB = C::NSB, KS = C::KS, MI = C::MI, NJ = C::NJ;
   constexpr int PA = C::A_INS, PB = C::B_INS;   // DMA instructions per wave and slab
-  const int nk = (K + BK - 1) / BK;
+  constexpr int XW = EXTRA < 0 ? 0 : EXTRA;
+  static_assert((NSB - 1) * (PA + PB) + PA + XW < 64, "vmcnt range");
+  const B16Pipe<C, AKC, BKC, AI, BI> pp(A, B, K, lds);
+  const int nk = pp.nk;
   if (nk <= 0) return;
-  const int nfull = K / BK;                    // slabs with no k past K
+  const int nfull = pp.nfull;
   const int wave = wave_id();
   B16Frag<AKC, C::RA, MI> fa;
   B16Frag<BKC, C::RB, NJ> fb;
   fa.init((wave % C::WM) * C::TM);
   fb.init((wave / C::WM) * C::TN);
-  B16Dma<AKC, C::RA, C::A_INS, AI> da;
-  B16Dma<BKC, C::RB, C::B_INS, BI> db;
-  da.init(A);
-  db.init(B);
+  const auto& da = pp.da;
+  const auto& db = pp.db;
 
-  auto abuf = [&](int s) { return lds + (s % NSA) * C::A_BYTES; };
-  auto bbuf = [&](int s) { return lds + C::B_BASE + (s % NSB) * C::B_BYTES; };
-  auto issue_a = [&](int s) {
-    if (s < nfull) da.issue_full(s, abuf(s));
-    else da.issue_tail(A, s * BK, abuf(s));
-  };
-  auto issue_b = [&](int s) {
-    if (s < nfull) db.issue_full(s, bbuf(s));
-    else db.issue_tail(B, s * BK, bbuf(s));
-  };
+  auto abuf = [&](int s) { return pp.abuf(s); };
+  auto bbuf = [&](int s) { return pp.bbuf(s); };
+  auto issue_a = [&](int s) { pp.issue_a(s); };
+  auto issue_b = [&](int s) { pp.issue_b(s); };
   bf16x8_t xa[2][MI], xb[2][NJ];
   auto read = [&](int set, int s, int ks) {
     const FM_LDS char* ab = abuf(s);
@@ -470,15 +518,17 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
   constexpr int LAST = (KS - 1) & 1;           // register set of the last k-step
   constexpr int HALF = MI / 2;
 
-  // Prologue: B(0) A(0) B(1) A(1) ... B(NSB-1) A(NSB-1) A(NSA-1).
-#pragma nounroll
-  for (int s = 0; s < NSA && s < nk; ++s) {
-    if (s < NSB) issue_b(s);
-    issue_a(s);
-  }
+  if (EXTRA < 0) pp.prologue();
   // slab 0 is complete once everything issued after A(0) is at most in flight
-  if (nk >= NSA) wait_vmcnt<(NSB - 1) * (PA + PB) + PA>();
-  else wait_vmcnt<0>();
+  if (XW > 0 && extra_issued) {
+    if (nk >= NSA) wait_vmcnt<(NSB - 1) * (PA + PB) + PA + XW>();
+    else if (nk >= NSB) wait_vmcnt<(NSB - 1) * (PA + PB) + XW>();   // A(NSA - 1) does not exist
+    else wait_vmcnt<XW>();
+  } else {
+    if (nk >= NSA) wait_vmcnt<(NSB - 1) * (PA + PB) + PA>();
+    else if (nk >= NSB) wait_vmcnt<(NSB - 1) * (PA + PB)>();
+    else wait_vmcnt<0>();
+  }
   wait_lgkm0();   // no scalar loads pending: LDS-read waits in the loop can count
   barrier_lds();
   read(0, 0, 0);

@@ -156,3 +156,17 @@ def test_backward_outputs(run):
     for i, s in enumerate(slots):                 # empty tuning slots: exactly zero
         if all(np.all(a == 0) for a in dW[s]):
             assert not host(r.dWg[i]).any() and not host(r.dWu[i]).any() and not host(r.dWd[i]).any()
+
+
+def test_backward_accumulates_weight_gradients(run):
+    """accumulate_dw = 1 adds the step's weight gradients to what dW holds: a
+    second identical backward doubles every element exactly (fp32 x + x)."""
+    r = run.r
+    once = [host(t).copy() for t in (*r.dWg, *r.dWu, *r.dWd)]
+    r.backward(dgate=False, accumulate_dw=True)
+    torch.cuda.synchronize()
+    twice = [host(t) for t in (*r.dWg, *r.dWu, *r.dWd)]
+    r.backward(dgate=False, accumulate_dw=False)    # leave the single-pass values for other tests
+    torch.cuda.synchronize()
+    for a, b in zip(once, twice):
+        np.testing.assert_array_equal(b, 2 * a)
