@@ -42,15 +42,20 @@ def short_name(n: str) -> str:
     return n.split("(")[0]
 
 
+def base_name(n: str) -> str:
+    """Kernel name without template arguments (kb_dw_gu<false> -> kb_dw_gu)."""
+    return short_name(n).split("<")[0]
+
+
 def stats_table(path: str, top: int) -> str:
     rows = list(csv.DictReader(open(path)))
     out = ["| kernel | calls | avg µs | total ms | % |", "|---|---|---|---|---|"]
     for r in rows[:top]:
         out.append(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                    f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['Percentage']):.1f} |")
-    ffn = [r for r in rows if short_name(r["Name"]) in FFN_KERNELS]
+    ffn = [r for r in rows if base_name(r["Name"]) in FFN_KERNELS]
     if ffn:
-        steps = max(int(r["Calls"]) for r in ffn if short_name(r["Name"]) == "kb_gate_up")
+        steps = max(int(r["Calls"]) for r in ffn if base_name(r["Name"]) == "kb_gate_up")
         tot = sum(float(r["TotalDurationNs"]) for r in ffn) / steps / 1e3
         out.append("")
         out.append(f"grouped SwiGLU fwd+bwd kernels per step (sum of averages over {steps} steps): {tot:.1f} µs")
@@ -63,8 +68,8 @@ def counter_per_kernel(path: str, counter: str):
     for r in csv.DictReader(open(path)):
         if r["Counter_Name"] != counter:
             continue
-        per[short_name(r["Kernel_Name"])][r["Dispatch_Id"]] = \
-            per[short_name(r["Kernel_Name"])].get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+        per[base_name(r["Kernel_Name"])][r["Dispatch_Id"]] = \
+            per[base_name(r["Kernel_Name"])].get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
     return {k: list(v.values()) for k, v in per.items()}
 
 
