@@ -15,7 +15,7 @@
 namespace fm {
 namespace {
 
-constexpr int PM_TOK = 256;   // tokens per block of count/place
+constexpr int PM_TOK = 256;   // tokens (threads) per block of count/place
 
 template <int KMAX>
 struct TokenSlots {
@@ -52,7 +52,7 @@ __device__ __forceinline__ void token_slots(const int32_t* __restrict__ idx,
 }
 
 template <int KMAX>
-__global__ __launch_bounds__(256) void k_perm_count(const int32_t* __restrict__ idx,
+__global__ __launch_bounds__(PM_TOK) void k_perm_count(const int32_t* __restrict__ idx,
                                                     const int32_t* __restrict__ emap, int T, int k,
                                                     int S, int32_t* __restrict__ bc, int nblk) {
   __shared__ int cnt[512];
@@ -108,14 +108,14 @@ __global__ __launch_bounds__(1024) void k_perm_scan(int32_t* __restrict__ bc, in
 }
 
 template <int KMAX>
-__global__ __launch_bounds__(256) void k_perm_place(const int32_t* __restrict__ idx,
+__global__ __launch_bounds__(PM_TOK) void k_perm_place(const int32_t* __restrict__ idx,
                                                     const float* __restrict__ gate,
                                                     const int32_t* __restrict__ emap, int T, int k,
                                                     int S, const int32_t* __restrict__ bc, int nblk,
                                                     int32_t* __restrict__ perm_token,
                                                     float* __restrict__ perm_gate,
                                                     int32_t* __restrict__ inv) {
-  __shared__ int wcnt[4][512];
+  __shared__ int wcnt[PM_TOK / 64][512];
   const int lane = lane_id(), wave = threadIdx.x >> 6;
   const int t = blockIdx.x * PM_TOK + threadIdx.x;
   const bool valid = t < T;
@@ -209,20 +209,34 @@ __device__ __forceinline__ int row_of(int v) { return v >= 0 ? v : -2 - v; }
 
 // Gathers and sums up to KMAX + S_sh rows into one token's row, U 16-byte
 // chunks per lane at a time with every load of the step issued before the
-// arithmetic: out[c] = sum_j w_j src[p_j][c] (+ sum of the shared rows).
+// arithmetic: out[c] = sum_j w_j src[p_j][c] + sum of the shared rows.  The
+// first SHMAX shared rows are loaded with the routed ones; further shared rows
+// (a layer with more than SHMAX shared experts) are added one at a time.
 template <typename T, int KMAX, bool WEIGHTED>
 __device__ __forceinline__ void gather_sum_row(const T* __restrict__ src, const int (&p)[KMAX],
                                                const float (&g)[KMAX], size_t R, int Tn, int t, int d,
                                                int S_sh, T* __restrict__ out) {
-  constexpr int V = 16 / sizeof(T), U = 2;
+  constexpr int V = 16 / sizeof(T), U = 2, SHMAX = 2, NS = KMAX + SHMAX;
+  const T* rows[NS];
+  float w[NS];
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    rows[j] = p[j] >= 0 ? src + (size_t)p[j] * d : nullptr;
+    w[j] = g[j];
+  }
+#pragma unroll
+  for (int s = 0; s < SHMAX; ++s) {
+    rows[KMAX + s] = s < S_sh ? src + (R + (size_t)s * Tn + t) * d : nullptr;
+    w[KMAX + s] = 1.f;
+  }
   for (int c0 = lane_id() * V; c0 < d; c0 += U * 64 * V) {
-    u32x4_t raw[U][KMAX];
+    u32x4_t raw[U][NS];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int c = c0 + u * 64 * V;
 #pragma unroll
-      for (int j = 0; j < KMAX; ++j)
-        if (p[j] >= 0 && c < d) raw[u][j] = ld16(src + (size_t)p[j] * d + c);
+      for (int j = 0; j < NS; ++j)
+        if (rows[j] && c < d) raw[u][j] = ld16(rows[j] + c);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -232,14 +246,14 @@ __device__ __forceinline__ void gather_sum_row(const T* __restrict__ src, const 
 #pragma unroll
       for (int i = 0; i < V; ++i) acc[i] = 0.f;
 #pragma unroll
-      for (int j = 0; j < KMAX; ++j) {
-        if (p[j] < 0) continue;
+      for (int j = 0; j < NS; ++j) {
+        if (!rows[j]) continue;
         float f[V];
         unpack16(raw[u][j], f, (T*)nullptr);
 #pragma unroll
-        for (int i = 0; i < V; ++i) acc[i] = WEIGHTED ? fmaf(g[j], f[i], acc[i]) : acc[i] + f[i];
+        for (int i = 0; i < V; ++i) acc[i] = (WEIGHTED && j < KMAX) ? fmaf(w[j], f[i], acc[i]) : acc[i] + f[i];
       }
-      for (int sh = 0; sh < S_sh; ++sh) {
+      for (int sh = SHMAX; sh < S_sh; ++sh) {
         float f[V];
         unpack16(ld16(src + (R + (size_t)sh * Tn + t) * d + c), f, (T*)nullptr);
 #pragma unroll
@@ -403,12 +417,13 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
   const int nblk = cdiv(T, PM_TOK);
   int32_t* bc = (int32_t*)ws;
 #define FM_PC(KM) \
-  hipLaunchKernelGGL(k_perm_count<KM>, dim3(nblk), dim3(256), 0, st, idx, expert_map, T, k, S_routed, bc, nblk)
+  hipLaunchKernelGGL(k_perm_count<KM>, dim3(nblk), dim3(PM_TOK), 0, st, idx, expert_map, T, k, S_routed, bc, \
+                     nblk)
   FM_KSWITCH(k, FM_PC)
 #undef FM_PC
   hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(1024), 0, st, bc, nblk, S_routed, offsets);
 #define FM_PP(KM)                                                                                   \
-  hipLaunchKernelGGL(k_perm_place<KM>, dim3(nblk), dim3(256), 0, st, idx, gate, expert_map, T, k, \
+  hipLaunchKernelGGL(k_perm_place<KM>, dim3(nblk), dim3(PM_TOK), 0, st, idx, gate, expert_map, T, k, \
                      S_routed, bc, nblk, perm_token, perm_gate, inv)
   FM_KSWITCH(k, FM_PP)
 #undef FM_PP
