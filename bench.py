@@ -33,7 +33,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="deepseek_moe")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-sample-tokens", type=int, default=1024)
+    p.add_argument("--cpu-sample-tokens", type=int, default=8192)
+    p.add_argument("--no-cold", action="store_true", help="skip the cold-cache timing of the HBM-bound calls")
     p.add_argument("--calib-copy", action="store_true",
                    help="end with a device-to-device copy of 256 MiB (counter calibration)")
     return p.parse_args()
@@ -71,9 +72,69 @@ def ffn_flops(r, offsets):
     return fwd, bwd
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def cold_hbm(r, w, st, N, reps=5):
+    """The HBM-bound entry points timed one launch at a time with a cold MALL:
+    a 512 MiB scrub buffer is written before every launch (outside the timed
+    interval, which HIP events on the launch stream bracket).  Median of
+    `reps`; algorithmic bytes per launch as in the kernel table."""
+    import numpy as np
+    import torch
+    from paper_2508_19078_amd import api
+
+    b = w.x_bytes
+    Ntot = N + w.T * w.n_shared
+    calls = {
+        "route": (lambda: api.moe_route_topk(r.X, r.Wr, r.bias, w.k, r.idx, r.gate, None),
+                  w.T * w.d * b + w.E * w.d * b + w.T * w.k * 8),
+        "profile_hist": (lambda: api.moe_profile_hist(r.X, r.Wq, r.wscale, r.bias, w.k, r.counts),
+                         w.T * w.d * b + w.E * w.d + 12 * w.E),
+        "permute": (lambda: api.moe_permute(r.X, r.idx, r.gate, r.expert_map, r.S_r, r.offsets, r.perm_token,
+                                            r.perm_gate, r.inv, r.X_perm, r.ws_perm, E=w.E),
+                    w.T * w.d * b + N * w.d * b + w.T * w.k * 8 + N * 12 + 4 * (r.S_r + 1)),
+        "combine": (lambda: api.moe_unpermute(r.layer_tables, r.O, r.inv, r.perm_gate, w.T, w.k, r.Y),
+                    Ntot * w.d * b + w.T * w.d * b + w.T * w.k * 8),
+        "combine_bwd": (lambda: api.moe_unpermute_bwd(r.layer_tables, r.dY, r.O, r.inv, r.offsets, r.perm_gate,
+                                                      w.T, w.k, r.dO, None),
+                        Ntot * w.d * b + w.T * w.d * b),
+        "permute_bwd": (lambda: api.moe_permute_bwd(r.layer_tables, r.dX_perm, r.inv, w.T, w.k, r.dX),
+                        Ntot * w.d * b + w.T * w.d * b + w.T * w.k * 4),
+    }
+    if r.G:
+        calls["merge"] = (lambda: api.moe_merge_experts(r.w_src, r.dt, w.d, w.I, r.G, r.grp_ptr, r.grp_member,
+                                                        r.alpha, r.w_dst, r.dt),
+                          (w.E - r.K + r.G) * 3 * w.d * w.I * b)
+    scrub = torch.empty(256 << 20, dtype=torch.int16, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {}
+    for name, (fn, nbytes) in calls.items():
+        ts = []
+        for i in range(reps):
+            scrub.fill_(i)
+            e0.record(st)
+            fn()
+            e1.record(st)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        us = float(np.median(ts)) * 1e3
+        gbs = nbytes / (us * 1e-6) / 1e9
+        out[name] = {"us": round(us, 1), "GBps": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 3)}
+    del scrub
+    return out
+
+
 def cpu_baseline(w, n_tok):
     """The fp64 oracle on a bounded sample of the same workload (its first n_tok
-    tokens): routing, int8 histogram, merge plan + merge (all experts), permute
+    tokens; by default all of them): routing, int8 histogram, merge plan + merge (all experts), permute
     maps, forward and backward.  Reported in tokens/s of the sample."""
     import numpy as np
     import oracle as O
@@ -82,12 +143,22 @@ def cpu_baseline(w, n_tok):
 
     ws = W.scaled(w, T=n_tok)
     inp = LayerInputs(ws)
+    stages = {}
     t0 = time.perf_counter()
+    tl = [t0]
+
+    def lap(name):
+        now = time.perf_counter()
+        stages[name] = round(now - tl[0], 3)
+        tl[0] = now
+
     X = inp.X.f64()
     b = inp.bias.astype(np.float64)
     idx, gate, _ = O.route_topk(X, inp.Wr.f64(), b, w.k)
+    lap("route")
     q, s = O.quantize_int8_rows(inp.Wr.f32())
     counts, _, _ = O.profile_hist(X, q, s, b, w.k)
+    lap("profile_hist")
     spec = W.layer_merge_spec(w, 0)
     if spec is None:
         plan = O.MergePlan(w.E, list(range(w.E)), [], n_tune=w.n_tune)
@@ -98,6 +169,7 @@ def cpu_baseline(w, n_tok):
     wg, wu, wd = (t.f64() for t in inp.experts)
     alpha = counts / float(n_tok)
     merged = [[O.merge_experts(M, g, alpha) for M in (wg, wu, wd)] for g in plan.groups]
+    lap("merge")
     sl = [[], [], []]
     for e in plan.kept:
         for i, M in enumerate((wg, wu, wd)):
@@ -114,12 +186,17 @@ def cpu_baseline(w, n_tok):
             tuning.append(True)
     slots = O.SlotWeights(sl[0], sl[1], sl[2], tuning, n_shared=w.n_shared)
     O.permute_maps(idx, gate, plan.expert_map, plan.S)
+    lap("permute")
     O.moe_forward(X, idx, gate, plan.expert_map, slots)
+    lap("forward")
     O.moe_backward(X, inp.dY.f64(), idx, gate, plan.expert_map, slots)
+    lap("backward")
     dt = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": round(n_tok / dt, 2), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"first {n_tok} of {w.T} tokens of the same workload, full fp64 layer step "
+            "cpu": cpu_model(), "stages_s": stages,
+            "sample": (f"all {w.T} tokens" if n_tok >= w.T else f"first {n_tok} of {w.T} tokens")
+                      + " of the same workload, full fp64 layer step "
                       f"(route, int8 histogram, plan+merge of all experts, permute, fwd+bwd); "
                       f"{dt:.1f} s on the host"}
 
@@ -224,6 +301,9 @@ def main():
         "hbm_kernels_GBps": {"route": gbs(route_bytes, per["route"]), "profile": gbs(hist_bytes, per["profile"]),
                              "merge": gbs(merge_bytes, per["merge"]), "permute": gbs(permute_bytes, per["permute"])},
     }
+    if not a.no_cold:
+        print("# cold-cache timing of the HBM-bound entry points", file=sys.stderr, flush=True)
+        out["hbm_cold"] = cold_hbm(r, w, st, N)
     if a.calib_copy:
         src = torch.ones(128 << 20, dtype=torch.bfloat16, device="cuda")
         dst = torch.empty_like(src)

@@ -8,7 +8,7 @@
 //           the slots (the bucket offsets)
 //   place   the same blocks rank their rows within each slot in token order
 //           (one wave ballot per slot) and write the maps
-//   gather  X_perm[p] = X[perm_token[p]], one wave per row, 16-byte accesses
+//   scatter X_perm[inv[t, j]] = X[t], one wave per token, 16-byte accesses
 // Combine and the two backward gathers run one wave per token.
 #include "common.hpp"
 
@@ -178,24 +178,28 @@ __global__ __launch_bounds__(PM_TOK) void k_perm_place(const int32_t* __restrict
   }
 }
 
-// X_perm[p] = X[perm_token[p]] for p < offsets[S]; one wave per row, the
-// loads of four 1 KB pieces of the row issued before their stores.
-__global__ __launch_bounds__(256) void k_gather_rows(const char* __restrict__ X,
-                                                     const int32_t* __restrict__ perm_token,
-                                                     const int32_t* __restrict__ offsets, int S,
-                                                     size_t row_bytes, char* __restrict__ Xp) {
-  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (p >= offsets[S]) return;
-  const char* src = X + (size_t)perm_token[p] * row_bytes;
-  char* dst = Xp + (size_t)p * row_bytes;
+// X_perm[inv[t, j]] = X[t] for the rows a token opens (inv >= 0): one wave
+// per token reads its row once (four 1 KB pieces in flight) and writes it to
+// each of its rows, so X is read once instead of once per choice.
+__global__ __launch_bounds__(256) void k_scatter_rows(const char* __restrict__ X,
+                                                      const int32_t* __restrict__ inv, int T, int k,
+                                                      size_t row_bytes, char* __restrict__ Xp) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const char* src = X + (size_t)t * row_bytes;
   for (size_t c0 = (size_t)lane_id() * 16; c0 < row_bytes; c0 += 4 * 64 * 16) {
     u32x4_t v[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       if (c0 + u * 1024 < row_bytes) v[u] = ld16(src + c0 + u * 1024);
+    for (int j = 0; j < k; ++j) {
+      const int p = inv[(size_t)t * k + j];
+      if (p < 0) continue;
+      char* dst = Xp + (size_t)p * row_bytes;
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (c0 + u * 1024 < row_bytes) st16(dst + c0 + u * 1024, v[u]);
+      for (int u = 0; u < 4; ++u)
+        if (c0 + u * 1024 < row_bytes) st16(dst + c0 + u * 1024, v[u]);
+    }
   }
 }
 
@@ -428,8 +432,8 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
   FM_KSWITCH(k, FM_PP)
 #undef FM_PP
   const size_t row_bytes = (size_t)d * esize(dtype);
-  hipLaunchKernelGGL(k_gather_rows, dim3(cdiv((long)T * k, 4)), dim3(256), 0, st, (const char*)X,
-                     perm_token, offsets, S_routed, row_bytes, (char*)X_perm);
+  hipLaunchKernelGGL(k_scatter_rows, dim3(cdiv(T, 4)), dim3(256), 0, st, (const char*)X, inv, T, k, row_bytes,
+                     (char*)X_perm);
   return check_launch("moe_permute");
 }
 
