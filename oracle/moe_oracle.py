@@ -87,6 +87,26 @@ def route_topk(X, Wr, bias, k: int):
     return idx, gate, logits
 
 
+def route_topk_backward(Wr, idx, gate, dgate):
+    """Router backward with the top-k selection held fixed (the selection is a
+    piecewise-constant function of the logits).  The gate of a token is the
+    softmax of its k selected logits, so a gradient dgate [T,k] on the gates
+    gives the logits the softmax Jacobian-vector product
+        dlogit[t, idx[t,j]] = gate[t,j] * (dgate[t,j] - sum_i gate[t,i] dgate[t,i])
+    and 0 on the experts not selected; logit = X Wr^T + bias then gives
+    dX = dlogit Wr.  Returns (dlogit [T,E], dX [T,d]).  (The router itself is
+    frozen in expert-only tuning, so no weight or bias gradient is formed.)
+    """
+    Wr, gate, dgate = _f64(Wr), _f64(gate), _f64(dgate)
+    idx = np.asarray(idx, dtype=np.int64)
+    T, k = gate.shape
+    inner = np.sum(gate * dgate, axis=1, keepdims=True)
+    dsel = gate * (dgate - inner)
+    dlogit = np.zeros((T, Wr.shape[0]), dtype=F64)
+    np.put_along_axis(dlogit, idx, dsel, axis=1)
+    return dlogit, dlogit @ Wr
+
+
 def topk_gap(logits, k: int) -> np.ndarray:
     """logit_(k) - logit_(k+1) per row (inf when k == E): the selection margin."""
     logits = _f64(logits)

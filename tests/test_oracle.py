@@ -86,6 +86,55 @@ def test_router_is_expert_permutation_equivariant():
     np.testing.assert_allclose(gate_p, gate, rtol=1e-14)
 
 
+def _route_fd_setup(seed=21, T=5, d=4, E=6, k=3):
+    r = rng(seed)
+    X, Wr = r.normal(size=(T, d)), r.normal(size=(E, d))
+    bias = 3.0 * r.normal(size=E)            # wide selection margins
+    _, _, logits = O.route_topk(X, Wr, bias, k)
+    assert np.all(O.topk_gap(logits, k) > 1e-3)
+    return X, Wr, bias, r.normal(size=(T, k))
+
+
+def test_route_backward_matches_central_differences():
+    """dX of L(X) = <dgate, gate(X)> through top-k and the renormalised softmax
+    (scipy's softmax, the selection re-made at every evaluation) against the
+    closed-form router backward."""
+    X, Wr, bias, dgate = _route_fd_setup()
+    k = dgate.shape[1]
+    idx, gate, _ = O.route_topk(X, Wr, bias, k)
+
+    def loss():
+        lg = X @ Wr.T + bias
+        sel = np.argsort(-lg, axis=1, kind="stable")[:, :k]
+        return float(np.sum(dgate * scipy.special.softmax(np.take_along_axis(lg, sel, 1), axis=1)))
+
+    dlogit, dX = O.route_topk_backward(Wr, idx, gate, dgate)
+    np.testing.assert_allclose(dX, _fd(loss, X), rtol=1e-7, atol=1e-9)
+    # and with respect to the logits themselves (selection fixed by the margins)
+    lg0 = X @ Wr.T + bias
+
+    def loss_l():
+        sel = np.argsort(-lg0, axis=1, kind="stable")[:, :k]
+        return float(np.sum(dgate * scipy.special.softmax(np.take_along_axis(lg0, sel, 1), axis=1)))
+
+    np.testing.assert_allclose(dlogit, _fd(loss_l, lg0), rtol=1e-7, atol=1e-9)
+
+
+def test_route_backward_invariants():
+    """Per token the logit gradient sums to 0 (the gates sum to 1); k = 1 and a
+    dgate constant over a token's choices give no gradient."""
+    X, Wr, bias, dgate = _route_fd_setup(seed=22, T=40, d=8, E=10, k=4)
+    idx, gate, _ = O.route_topk(X, Wr, bias, 4)
+    dlogit, _ = O.route_topk_backward(Wr, idx, gate, dgate)
+    np.testing.assert_allclose(dlogit.sum(axis=1), 0.0, atol=1e-12)
+    assert np.count_nonzero(dlogit) <= dlogit.shape[0] * 4
+    const = np.repeat(dgate[:, :1], 4, axis=1)
+    assert np.all(np.abs(O.route_topk_backward(Wr, idx, gate, const)[0]) < 1e-12)
+    idx1, gate1, _ = O.route_topk(X, Wr, bias, 1)
+    dl1, dx1 = O.route_topk_backward(Wr, idx1, gate1, dgate[:, :1])
+    assert not dl1.any() and not dx1.any()
+
+
 def test_topk_gap():
     logits = np.array([[3.0, 1.0, 2.0, 2.0], [0.0, 0.0, 0.0, 5.0]])
     np.testing.assert_array_equal(O.topk_gap(logits, 2), [0.0, 0.0])
