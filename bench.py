@@ -108,6 +108,9 @@ def cold_hbm(r, w, st, N, reps=5):
                         Ntot * w.d * b + w.T * w.d * b),
         "permute_bwd": (lambda: api.moe_permute_bwd(r.layer_tables, r.dX_perm, r.inv, w.T, w.k, r.dX),
                         Ntot * w.d * b + w.T * w.d * b + w.T * w.k * 4),
+        # router backward (selection fixed), added to the layer's dX
+        "route_bwd": (lambda: api.moe_route_bwd(r.gate, r.idx, r.dgate, r.Wr, r.dX, accumulate=True),
+                      w.T * w.k * 12 + 2 * w.T * w.d * b + w.E * w.d * b),
     }
     if r.G:
         calls["merge"] = (lambda: api.moe_merge_experts(r.w_src, r.dt, w.d, w.I, r.G, r.grp_ptr, r.grp_member,

@@ -77,6 +77,22 @@ int moe_route_topk(const void* X, const void* Wr, int dtype, const float* bias,
                    int T, int d, int E, int k,
                    int32_t* idx, float* gate, float* logits, void* stream);
 
+/* moe_route_bwd: the router's backward pass with the top-k selection held
+ * fixed (the selection is piecewise constant in the logits; the gate of a
+ * token is the softmax of its selected logits, as in moe_route_topk).  From
+ * the gradient dgate of the gates (moe_unpermute_bwd's dgate):
+ *   dlogit[t,j] = gate[t,j] * (dgate[t,j] - sum_i gate[t,i] * dgate[t,i])
+ *   dX[t,:]     = (accumulate ? dX[t,:] : 0) + sum_j dlogit[t,j] * Wr[idx[t,j],:]
+ * (fp32 sums, one rounding to `dtype`).  With accumulate = 1 this adds the
+ * router's share to the expert path's dX of the same tokens.  No gradient of
+ * Wr or bias is formed: the router is frozen in expert-only tuning (Section 3).
+ * gate, dgate [T,k] fp32; idx [T,k] int32 as written by moe_route_topk
+ * (entries outside [0, E) are clamped); Wr [E,d] and dX [T,d] in `dtype`.
+ * Limits as for moe_route_topk.
+ */
+int moe_route_bwd(const float* gate, const int32_t* idx, const float* dgate, const void* Wr, int dtype,
+                  int T, int d, int E, int k, void* dX, int accumulate, void* stream);
+
 /* ------------------------------------------------- quantisation profiling --
  * moe_quantize_int8: the low-bit profiling copy of a weight matrix
  * (Section 4.1, quantisation-based local profiling), one symmetric scale per

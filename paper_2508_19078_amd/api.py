@@ -39,6 +39,7 @@ _SIGS = {
     "moe_last_error": (ctypes.c_char_p, []),
     "moe_abi_version": (_c_int, []),
     "moe_route_topk": (_c_int, [_vp, _vp, _c_int, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp]),
+    "moe_route_bwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _c_int, _vp]),
     "moe_quantize_int8": (_c_int, [_vp, _c_int, _c_int, _c_int, _vp, _vp, _vp]),
     "moe_profile_hist": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp]),
     "moe_merge_plan": (_c_int, [_vp, _c_int, _c_int, _c_int, _f, _c_int, _c_int, _c_int, _vp, _vp, _vp,
@@ -131,6 +132,13 @@ def moe_route_topk(X, Wr, bias, k, idx, gate, logits=None, stream=None):
     E = Wr.shape[0]
     return _call("moe_route_topk", ptr(X), ptr(Wr), dtype_code(X.dtype), ptr(bias), T, d, E, k,
                  ptr(idx), ptr(gate), ptr(logits), stream_ptr(stream))
+
+
+def moe_route_bwd(gate, idx, dgate, Wr, dX, accumulate=False, stream=None):
+    T, k = gate.shape
+    E, d = Wr.shape
+    return _call("moe_route_bwd", ptr(gate), ptr(idx), ptr(dgate), ptr(Wr), dtype_code(Wr.dtype), T, d, E, k,
+                 ptr(dX), int(bool(accumulate)), stream_ptr(stream))
 
 
 def moe_quantize_int8(W, Wq, scale, stream=None):

@@ -350,6 +350,69 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
   return check_launch(MODE == 0 ? "moe_route_topk" : "moe_profile_hist");
 }
 
+// Router backward with the top-k selection held fixed: for the k selected
+// experts dlogit_j = g_j (dg_j - sum_i g_i dg_i) (the softmax Jacobian-vector
+// product), and dX[t] = (accumulate ? dX[t] : 0) + sum_j dlogit_j Wr[idx_j].
+// One wave per token; the k router rows of a 16-byte column chunk are loaded
+// together (Wr stays in L2); fp32 sums in j order, one rounding to T.
+template <typename T, int KMAX>
+__global__ __launch_bounds__(256) void k_route_bwd(const float* __restrict__ gate, const int32_t* __restrict__ idx,
+                                                   const float* __restrict__ dgate, const T* __restrict__ Wr, int Tn,
+                                                   int d, int E, int k, int accumulate, T* __restrict__ dX) {
+  constexpr int V = 16 / sizeof(T);
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= Tn) return;
+  float g[KMAX], dl[KMAX];
+  const T* wrow[KMAX];
+  float inner = 0.f;
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    const bool on = j < k;
+    g[j] = on ? gate[(size_t)t * k + j] : 0.f;
+    dl[j] = on ? dgate[(size_t)t * k + j] : 0.f;
+    // an expert index outside [0, E) (a caller error) is clamped, not followed
+    wrow[j] = on ? Wr + (size_t)min(max(idx[(size_t)t * k + j], 0), E - 1) * d : nullptr;
+    inner = fmaf(g[j], dl[j], inner);
+  }
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) dl[j] = g[j] * (dl[j] - inner);
+  for (int c = lane_id() * V; c < d; c += 64 * V) {
+    u32x4_t raw[KMAX];
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j)
+      if (wrow[j]) raw[j] = ld16(wrow[j] + c);
+    float acc[V];
+    if (accumulate) {
+      unpack16(ld16(dX + (size_t)t * d + c), acc, (T*)nullptr);
+    } else {
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (!wrow[j]) continue;
+      float w[V];
+      unpack16(raw[j], w, (T*)nullptr);
+#pragma unroll
+      for (int i = 0; i < V; ++i) acc[i] = fmaf(dl[j], w[i], acc[i]);
+    }
+    st16(dX + (size_t)t * d + c, pack16(acc, (T*)nullptr));
+  }
+}
+
+template <typename T>
+void launch_route_bwd(const float* gate, const int32_t* idx, const float* dgate, const T* Wr, int Tn, int d, int E,
+                      int k, int accumulate, T* dX, hipStream_t st) {
+  const dim3 grid(cdiv(Tn, 4)), block(256);
+#define FM_RB(KM) \
+  hipLaunchKernelGGL((k_route_bwd<T, KM>), grid, block, 0, st, gate, idx, dgate, Wr, Tn, d, E, k, accumulate, dX)
+  if (k <= 2) FM_RB(2);
+  else if (k <= 4) FM_RB(4);
+  else if (k <= 8) FM_RB(8);
+  else FM_RB(16);
+#undef FM_RB
+}
+
 int check_route_shape(int T, int d, int E, int k) {
   if (T < 0 || d <= 0 || E <= 0 || k <= 0) return fail(MOE_ERR_ARG, "T=%d d=%d E=%d k=%d", T, d, E, k);
   if (E > 256) return fail(MOE_ERR_UNSUPPORTED, "E=%d > 256", E);
@@ -414,4 +477,22 @@ extern "C" int moe_profile_hist(const void* X, int x_dtype, const int8_t* Wq, co
                                          nullptr, counts, st);
   return launch_route<float, int8_t, 1>((const float*)X, Wq, scale, bias, T, d, E, k, idx, nullptr,
                                         nullptr, counts, st);
+}
+
+extern "C" int moe_route_bwd(const float* gate, const int32_t* idx, const float* dgate, const void* Wr, int dtype,
+                             int T, int d, int E, int k, void* dX, int accumulate, void* stream) {
+  clear_error();
+  FM_TRY(check_route_shape(T, d, E, k));
+  FM_TRY(need_dtype_float(dtype, "dtype"));
+  if (T == 0) return MOE_OK;
+  FM_TRY(need(gate, "gate")); FM_TRY(need(idx, "idx")); FM_TRY(need(dgate, "dgate"));
+  FM_TRY(need(Wr, "Wr")); FM_TRY(need(dX, "dX"));
+  FM_TRY(need_aligned(gate, "gate")); FM_TRY(need_aligned(idx, "idx")); FM_TRY(need_aligned(dgate, "dgate"));
+  FM_TRY(need_aligned(Wr, "Wr")); FM_TRY(need_aligned(dX, "dX"));
+  hipStream_t st = as_stream(stream);
+  if (dtype == MOE_BF16)
+    launch_route_bwd<bf16>(gate, idx, dgate, (const bf16*)Wr, T, d, E, k, accumulate != 0, (bf16*)dX, st);
+  else
+    launch_route_bwd<float>(gate, idx, dgate, (const float*)Wr, T, d, E, k, accumulate != 0, (float*)dX, st);
+  return check_launch("moe_route_bwd");
 }

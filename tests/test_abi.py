@@ -29,7 +29,7 @@ def declared():
 
 def test_every_declared_function_is_exported_and_bound(L):
     names = declared()
-    assert len(names) >= 17
+    assert len(names) >= 18
     for n in names:
         assert hasattr(L, n), n
         assert n in api.exported_names(), n
@@ -76,6 +76,24 @@ def test_route_rejections(L):
     # ... but the shape is still validated
     rc, _ = rc_and_msg(L, "moe_route_topk", None, None, api.MOE_BF16, None, 0, 64, 8, 9, None, None, None, None)
     assert rc != api.MOE_OK
+
+
+def test_route_bwd_rejections(L):
+    args = lambda **o: [o.get(n, v) for n, v in (("gate", FAKE), ("idx", FAKE), ("dgate", FAKE), ("Wr", FAKE),
+                                                 ("dtype", api.MOE_BF16), ("T", 16), ("d", 64), ("E", 8), ("k", 2),
+                                                 ("dX", FAKE), ("acc", 0), ("st", None))]
+    rc, msg = rc_and_msg(L, "moe_route_bwd", *args(k=9))
+    assert rc == api.MOE_ERR_UNSUPPORTED and "k=9" in msg
+    rc, msg = rc_and_msg(L, "moe_route_bwd", *args(dgate=None))
+    assert rc == api.MOE_ERR_ARG and "dgate" in msg
+    rc, _ = rc_and_msg(L, "moe_route_bwd", *args(dX=MIS))
+    assert rc == api.MOE_ERR_ALIGN
+    rc, _ = rc_and_msg(L, "moe_route_bwd", *args(dtype=api.MOE_I8))
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    rc, _ = rc_and_msg(L, "moe_route_bwd", *args(d=60))
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    rc, _ = rc_and_msg(L, "moe_route_bwd", *args(T=0, gate=None, idx=None, dgate=None, Wr=None, dX=None))
+    assert rc == api.MOE_OK
 
 
 def test_profile_and_merge_rejections(L):

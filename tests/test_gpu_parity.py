@@ -170,3 +170,30 @@ def test_backward_accumulates_weight_gradients(run):
     torch.cuda.synchronize()
     for a, b in zip(once, twice):
         np.testing.assert_array_equal(b, 2 * a)
+
+
+def route_bwd_check(w, r, ref, seed):
+    """moe_route_bwd (selection fixed) against the oracle on seeded dgate, alone
+    and added to the expert path's dX (accumulate = 1).  Returns the errors."""
+    rng = np.random.default_rng([w.cid, seed])
+    dgate = rng.normal(size=(w.T, w.k)).astype(np.float32)
+    gate32 = ref.gate.astype(np.float32)
+    _, dX_ref = O.route_topk_backward(host(r.Wr), ref.idx, gate32, dgate)
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
+    idx_t, gate_t, dg_t = dev(ref.idx.astype(np.int32), torch.int32), dev(gate32, torch.float32), \
+        dev(dgate, torch.float32)
+    out = torch.empty_like(r.dX)
+    from paper_2508_19078_amd import api
+    assert api.moe_route_bwd(gate_t, idx_t, dg_t, r.Wr, out, accumulate=False) == 0
+    base = r.dX.clone()
+    acc = base.clone()
+    assert api.moe_route_bwd(gate_t, idx_t, dg_t, r.Wr, acc, accumulate=True) == 0
+    torch.cuda.synchronize()
+    return rel_fro(host(out), dX_ref), rel_fro(host(acc), host(base) + dX_ref)
+
+
+def test_route_backward(run):
+    e_alone, e_acc = route_bwd_check(run.w, run.r, run.ref, 991)
+    log(f"route bwd: dX_router {e_alone:.2e}, accumulated {e_acc:.2e}")
+    tol = 1e-5 if run.w.dtype == "f32" else TOL_FFN
+    assert e_alone <= tol and e_acc <= tol

@@ -134,6 +134,14 @@ def test_edge_forward_backward(run):
         assert (np.diff(offs) > 0).sum() == 1 and offs[-1] == run.w.T
 
 
+def test_edge_route_backward(run):
+    """Router backward on the degenerate routings (k = E, one expert, ties)."""
+    from test_gpu_parity import route_bwd_check
+    e_alone, e_acc = route_bwd_check(run.w, run.r, run.ref, 993)
+    log(f"{run.name}: route bwd {e_alone:.2e} / {e_acc:.2e}")
+    assert e_alone <= TOL_FFN and e_acc <= TOL_FFN
+
+
 def test_router_limits():
     """E = 256 experts, k = 16: the largest router the ABI accepts."""
     w = W.LayerWorkload(name="router_max", cid=207, T=777, d=256, E=256, k=16, I=64, dtype="bf16",

@@ -93,6 +93,14 @@ def test_full_router(run):
     np.testing.assert_allclose(run.gate_g[keep], ref.gate[keep], rtol=1e-5, atol=1e-7)
 
 
+def test_full_route_backward(run):
+    """Router backward over every token of the full-size layer."""
+    from test_gpu_parity import route_bwd_check
+    e_alone, e_acc = route_bwd_check(run.w, run.r, run.ref, 992)
+    log(f"route bwd {run.w.name}: {e_alone:.2e} / accumulated {e_acc:.2e}")
+    assert e_alone <= TOL_FFN and e_acc <= TOL_FFN
+
+
 def test_full_quantizer_and_histogram(run):
     ref, w = run.ref, run.w
     np.testing.assert_array_equal(run.q_g, ref.q)
