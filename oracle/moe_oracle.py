@@ -391,6 +391,40 @@ def moe_backward(X, dY, idx, gate, expert_map, slots: SlotWeights):
     return dX, dW, dgate
 
 
+def expert_utility(X, dY, idx, gate, expert_map, slots: SlotWeights):
+    """Utility of each slot's expert (Section 6.1, Eq. 3).  The summand printed
+    there is garbled; read as the squared norm of the per-token gradient:
+        u_s = |D_s| * sqrt((1/|D_s|) * sum_{t in D_s} ||g_{s,t}||^2),
+    D_s the tokens that reach slot s and g_{s,t} the gradient of the slot's
+    parameters (W_gate, W_up, W_down) from token t alone; u_s = 0 for an empty
+    slot.  A token whose several choices map to the same slot reaches it once,
+    with the gates of those choices summed (the gradient of one token is what
+    its combined output contribution gives); shared experts take every token
+    with gate 1.  Computed as the explicit per-token gradients of one expert,
+    its weight gradient on a batch of one token.
+    """
+    X, dY, gate = _f64(X), _f64(dY), _f64(gate)
+    T = X.shape[0]
+    slot_of = np.asarray(expert_map)[np.asarray(idx)]
+    u = np.zeros(slots.S, dtype=F64)
+    for s in range(slots.S):
+        if s < slots.S_routed:
+            tokens = np.unique(np.nonzero(slot_of == s)[0])
+            gsum = np.array([gate[t][slot_of[t] == s].sum() for t in tokens])
+        else:
+            tokens, gsum = np.arange(T), np.ones(T)
+        if len(tokens) == 0:
+            continue
+        sq = 0.0
+        for t, g in zip(tokens, gsum):
+            _, (dWg, dWu, dWd) = swiglu_bwd(X[t:t + 1], slots.wg[s], slots.wu[s], slots.wd[s],
+                                            g * dY[t:t + 1], True)
+            sq += np.sum(dWg ** 2) + np.sum(dWu ** 2) + np.sum(dWd ** 2)
+        n = len(tokens)
+        u[s] = n * np.sqrt(sq / n)
+    return u
+
+
 def expert_grad_columns(x, Wg, Wu, Wd, dO, cols):
     """Slices of one expert's weight gradients along the intermediate index:
     (dWg[cols, :], dWu[cols, :], dWd[:, cols]) for rows x [n, d] and output

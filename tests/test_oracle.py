@@ -383,6 +383,37 @@ def test_empty_tuning_slot_gets_zero_dw():
         assert all(np.all(w == 0) for w in dW[s])
 
 
+def test_expert_utility_per_token_gradients_and_folding():
+    """Eq. 3 utility: (a) one routed expert with every token on it at gate 1:
+    u^2 / n equals the sum over tokens of the squared norms of that token's
+    weight gradient, taken by torch autograd (float64) through a dense SwiGLU
+    with torch's silu; (b) a token whose two choices reach the same slot counts
+    once, with the summed gate; (c) linear in dY; (d) an empty slot has 0."""
+    r = rng(31)
+    T, d, I = 7, 5, 6
+    X, dY = r.normal(size=(T, d)), r.normal(size=(T, d))
+    Wg, Wu, Wd = r.normal(size=(I, d)), r.normal(size=(I, d)), r.normal(size=(d, I))
+    slots = O.SlotWeights([Wg, Wg], [Wu, Wu], [Wd, Wd], [True, True])
+    emap = np.array([0, 1])
+    idx = np.zeros((T, 1), dtype=np.int64)
+    gate = np.ones((T, 1))
+    u = O.expert_utility(X, dY, idx, gate, emap, slots)
+    assert u[1] == 0.0
+    tot = 0.0
+    for t in range(T):
+        ws = [torch.tensor(w, dtype=torch.float64, requires_grad=True) for w in (Wg, Wu, Wd)]
+        x = torch.tensor(X[t], dtype=torch.float64)
+        y = ws[2] @ (torch.nn.functional.silu(ws[0] @ x) * (ws[1] @ x))
+        (y @ torch.tensor(dY[t], dtype=torch.float64)).backward()
+        tot += sum(float((w.grad ** 2).sum()) for w in ws)
+    np.testing.assert_allclose(u[0] ** 2 / T, tot, rtol=1e-12)
+    g2 = r.uniform(0.1, 0.9, size=(T, 2))
+    u2 = O.expert_utility(X, dY, np.zeros((T, 2), dtype=np.int64), g2, emap, slots)
+    u1 = O.expert_utility(X, dY, idx, g2.sum(axis=1, keepdims=True), emap, slots)
+    np.testing.assert_allclose(u2, u1, rtol=1e-12)
+    np.testing.assert_allclose(O.expert_utility(X, 3 * dY, idx, gate, emap, slots), 3 * u, rtol=1e-12)
+
+
 def test_grad_columns_match_central_differences():
     r = rng(16)
     n, d, I = 6, 4, 7
