@@ -111,7 +111,12 @@ def cold_hbm(r, w, st, N, reps=5):
         # router backward (selection fixed), added to the layer's dX
         "route_bwd": (lambda: api.moe_route_bwd(r.gate, r.idx, r.dgate, r.Wr, r.dX, accumulate=True),
                       w.T * w.k * 12 + 2 * w.T * w.d * b + w.E * w.d * b),
+        # expert utility (Eq. 3) from the backward's saved rows: x, dO, H, dA_g, dA_u of every row
+        "expert_utility": (lambda: api.moe_expert_utility(r.layer_tables, r.X, r.X_perm, r.offsets, w.T, w.k,
+                                                          r.H, r.dO, r.ws_bwd, util),
+                           Ntot * (2 * w.d + 3 * w.I) * b),
     }
+    util = torch.empty(r.S_r + w.n_shared, dtype=torch.float32, device="cuda")
     if r.G:
         calls["merge"] = (lambda: api.moe_merge_experts(r.w_src, r.dt, w.d, w.I, r.G, r.grp_ptr, r.grp_member,
                                                         r.alpha, r.w_dst, r.dt),

@@ -276,6 +276,25 @@ int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const void* X_perm
                            void* ws, size_t ws_bytes, void* stream);
 size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k);
 
+/* moe_expert_utility: the utility of each slot's expert (Section 6.1, Eq. 3),
+ * the quantity the expert role assignment ranks experts by.  Eq. 3's summand
+ * is garbled in print; read as the squared norm of the per-token gradient:
+ *   u[s] = |D_s| * sqrt((1/|D_s|) * sum_{r in D_s} ||g_r||^2),
+ * D_s the slot's rows (its tokens; a token whose choices share the slot is one
+ * row with the summed gate) and g_r the gradient of the slot's W_gate, W_up,
+ * W_down from row r alone, three rank-one products, so
+ *   ||g_r||^2 = ||dO_r||^2 ||H_r||^2 + (||dA_g,r||^2 + ||dA_u,r||^2) ||x_r||^2
+ * (per-row sums in fp32, per-slot sums in fp64, fixed order); an empty slot
+ * gets 0.  Every slot gets a utility, frozen ones included.  Call it after
+ * moe_grouped_swiglu_bwd on the same stream with that call's workspace, which
+ * still holds dA_g and dA_u, and the same layer, X, X_perm, offsets, T, k, H
+ * and dO; nothing else may use the workspace in between.  utility [S] fp32.
+ */
+int moe_expert_utility(const moe_layer* L, const void* X, const void* X_perm,
+                       const int32_t* offsets, int T, int k, const void* H,
+                       const void* dO, void* ws, size_t ws_bytes, float* utility,
+                       void* stream);
+
 /* moe_permute_bwd: gradient of the permutation (a deterministic gather):
  *   dX[t] = sum_{j: inv[t,j] >= 0} dX_perm[inv[t,j]]
  *           + sum_{shared i} dX_perm[T*k + i*T + t]       (fp32 accumulation)

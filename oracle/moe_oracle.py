@@ -391,7 +391,7 @@ def moe_backward(X, dY, idx, gate, expert_map, slots: SlotWeights):
     return dX, dW, dgate
 
 
-def expert_utility(X, dY, idx, gate, expert_map, slots: SlotWeights):
+def expert_utility(X, dY, idx, gate, expert_map, slots: SlotWeights, only: Optional[Sequence[int]] = None):
     """Utility of each slot's expert (Section 6.1, Eq. 3).  The summand printed
     there is garbled; read as the squared norm of the per-token gradient:
         u_s = |D_s| * sqrt((1/|D_s|) * sum_{t in D_s} ||g_{s,t}||^2),
@@ -401,13 +401,17 @@ def expert_utility(X, dY, idx, gate, expert_map, slots: SlotWeights):
     with the gates of those choices summed (the gradient of one token is what
     its combined output contribution gives); shared experts take every token
     with gate 1.  Computed as the explicit per-token gradients of one expert,
-    its weight gradient on a batch of one token.
+    its weight gradient on a batch of one token.  With `only`, the other slots
+    are left NaN.
     """
     X, dY, gate = _f64(X), _f64(dY), _f64(gate)
     T = X.shape[0]
     slot_of = np.asarray(expert_map)[np.asarray(idx)]
     u = np.zeros(slots.S, dtype=F64)
-    for s in range(slots.S):
+    if only is not None:
+        u[:] = np.nan
+    for s in (range(slots.S) if only is None else only):
+        u[s] = 0.0
         if s < slots.S_routed:
             tokens = np.unique(np.nonzero(slot_of == s)[0])
             gsum = np.array([gate[t][slot_of[t] == s].sum() for t in tokens])

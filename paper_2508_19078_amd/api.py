@@ -60,6 +60,7 @@ _SIGS = {
                                         _c_int, _vp, _c_size, _vp]),
     "moe_grouped_swiglu_bwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
     "moe_permute_bwd": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
+    "moe_expert_utility": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp, _vp]),
 }
 
 _lib = None
@@ -255,6 +256,12 @@ def moe_grouped_swiglu_bwd(layer, X, X_perm, offsets, T, k, A_g, A_u, H, dO, dX_
 
 def moe_permute_bwd(layer, dX_perm, inv, T, k, dX, stream=None):
     return _call("moe_permute_bwd", ptr(layer), ptr(dX_perm), ptr(inv), T, k, ptr(dX), stream_ptr(stream))
+
+
+def moe_expert_utility(layer, X, X_perm, offsets, T, k, H, dO, ws, utility, stream=None):
+    """After moe_grouped_swiglu_bwd with the same workspace `ws`."""
+    return _call("moe_expert_utility", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(H), ptr(dO),
+                 ptr(ws), ws.numel() * ws.element_size(), ptr(utility), stream_ptr(stream))
 
 
 # ----------------------------------------------------- layer descriptor ----

@@ -894,6 +894,75 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
   }
 }
 
+// ----------------------------------------- expert utility (Eq. 3) ----
+//
+// u_s = |D_s| sqrt(mean over the slot's rows of ||g_r||^2), where the weight
+// gradient of one row is three rank-one outer products, so
+//   ||g_r||^2 = ||dO_r||^2 ||h_r||^2 + (||dA_g,r||^2 + ||dA_u,r||^2) ||x_r||^2.
+// A slot's rows are its tokens after folding (a token whose choices share the
+// slot is one row with the summed gate), so |D_s| is the slot's row count.
+
+constexpr int UT_ROWS = 256;   // rows per first-pass tile
+
+// Sum of squares of n elements (n % 8 == 0) spread over a wave: every lane
+// ends with the same total (fixed butterfly order).
+template <typename T> __device__ __forceinline__ float wave_sumsq(const T* __restrict__ p, int n) {
+  constexpr int V = 16 / sizeof(T);
+  float a = 0.f;
+  for (int c = lane_id() * V; c < n; c += 64 * V) {
+    float f[V];
+    unpack16(ld16(p + c), f, (T*)nullptr);
+#pragma unroll
+    for (int i = 0; i < V; ++i) a = fmaf(f[i], f[i], a);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off);
+  return a;
+}
+
+// First pass: one block per 256-row tile of a slot (tiles as in mbase); four
+// waves take every fourth row; the tile's sum in fp64, waves added in order.
+template <typename T>
+__global__ __launch_bounds__(256) void k_utility_rows(const T* __restrict__ X, const T* __restrict__ Xp,
+                                                      const T* __restrict__ dO, const T* __restrict__ H,
+                                                      const T* __restrict__ dAg, const T* __restrict__ dAu,
+                                                      RowArgs ra, double* __restrict__ part) {
+  __shared__ double wsum[4];
+  const int b = blockIdx.x;
+  if (b >= ld_scalar(ra.mbase + ra.S)) return;
+  const int s = find_slot(ra.mbase, ra.S, b);
+  const int r0 = (b - ld_scalar(ra.mbase + s)) * UT_ROWS;
+  const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+  const int rows = min(UT_ROWS, sr.nrows - r0), wave = threadIdx.x >> 6, d = ra.d, I = ra.I;
+  double acc = 0.0;
+  for (int i = wave; i < rows; i += 4) {
+    const size_t o = (size_t)(sr.orow0 + r0 + i);
+    const T* xr = (sr.shared ? X : Xp) + (size_t)(sr.xrow0 + r0 + i) * d;
+    const float sx = wave_sumsq(xr, d), so = wave_sumsq(dO + o * d, d);
+    const float sh = wave_sumsq(H + o * I, I), sg = wave_sumsq(dAg + o * I, I), su = wave_sumsq(dAu + o * I, I);
+    acc += (double)so * sh + ((double)sg + su) * sx;
+  }
+  if (lane_id() == 0) wsum[wave] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) part[b] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+}
+
+// Second pass: thread s adds its slot's tile sums in tile order.
+__global__ __launch_bounds__(1024) void k_utility_slots(RowArgs ra, const double* __restrict__ part,
+                                                        float* __restrict__ u) {
+  const int s = threadIdx.x;
+  if (s >= ra.S) return;
+  double sum = 0.0;
+  for (int b = ld_scalar(ra.mbase + s); b < ld_scalar(ra.mbase + s + 1); ++b) sum += part[b];
+  const int n = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k).nrows;
+  u[s] = n > 0 ? (float)sqrt((double)n * sum) : 0.f;
+}
+
+__global__ void k_zero_f32(float* p, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
 // ------------------------------------------------------------------ host ----
 
 int check_layer_ffn(const moe_layer* L) {
@@ -934,10 +1003,13 @@ extern "C" size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int 
   return sched_bytes(n_slots(L));
 }
 
+// Upper bound of the utility pass's row tiles: sum_s ceil(n_s / UT_ROWS).
+static size_t utility_tiles(const moe_layer* L, int T, int k) { return rows_total(L, T, k) / UT_ROWS + n_slots(L) + 1; }
+
 extern "C" size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k) {
   if (!L || T < 0 || k <= 0) return 0;
   const size_t act = round256(rows_total(L, T, k) * L->I * esize(L->dtype));
-  return sched_bytes(n_slots(L)) + 2 * act;
+  return sched_bytes(n_slots(L)) + 2 * act + round256(sizeof(double) * utility_tiles(L, T, k));
 }
 
 extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const void* X_perm,
@@ -1046,4 +1118,44 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   }
 #undef FM_BWD
   return check_launch("moe_grouped_swiglu_bwd");
+}
+
+extern "C" int moe_expert_utility(const moe_layer* L, const void* X, const void* X_perm, const int32_t* offsets,
+                                  int T, int k, const void* H, const void* dO, void* ws, size_t ws_bytes,
+                                  float* utility, void* stream) {
+  clear_error();
+  FM_TRY(check_layer_ffn(L));
+  if (T < 0 || k <= 0 || k > 16) return fail(MOE_ERR_ARG, "T=%d k=%d", T, k);
+  FM_TRY(need(utility, "utility")); FM_TRY(need_aligned(utility, "utility"));
+  const int S = n_slots(L);
+  hipStream_t st = as_stream(stream);
+  if (T == 0) {
+    hipLaunchKernelGGL(k_zero_f32, dim3(cdiv(S, 256)), dim3(256), 0, st, utility, S);
+    return check_launch("moe_expert_utility");
+  }
+  FM_TRY(need(X, "X")); FM_TRY(need(offsets, "offsets")); FM_TRY(need(H, "H")); FM_TRY(need(dO, "dO"));
+  FM_TRY(need(ws, "ws"));
+  if (L->S_routed > 0) FM_TRY(need(X_perm, "X_perm"));
+  FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(X_perm, "X_perm")); FM_TRY(need_aligned(H, "H"));
+  FM_TRY(need_aligned(dO, "dO")); FM_TRY(need_aligned(ws, "ws"));
+  if (ws_bytes < moe_grouped_swiglu_bwd_workspace_size(L, T, k))
+    return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
+                moe_grouped_swiglu_bwd_workspace_size(L, T, k));
+  const Sched sc = sched_at(ws, S);
+  const size_t act = round256(rows_total(L, T, k) * L->I * esize(L->dtype));
+  const char* dAg = (const char*)ws + sched_bytes(S);
+  const char* dAu = dAg + act;
+  double* part = (double*)((char*)ws + sched_bytes(S) + 2 * act);
+  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, UT_ROWS,
+                     (float* const*)nullptr, sc.mbase, sc.wbase, sc.dorder, sc.queues);
+  const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
+  const dim3 grid((unsigned)utility_tiles(L, T, k));
+#define FM_UT(TT)                                                                                            \
+  hipLaunchKernelGGL(k_utility_rows<TT>, grid, dim3(256), 0, st, (const TT*)X, (const TT*)X_perm, (const TT*)dO, \
+                     (const TT*)H, (const TT*)dAg, (const TT*)dAu, ra, part)
+  if (L->dtype == MOE_BF16) FM_UT(bf16);
+  else FM_UT(float);
+#undef FM_UT
+  hipLaunchKernelGGL(k_utility_slots, dim3(1), dim3(1024), 0, st, ra, (const double*)part, utility);
+  return check_launch("moe_expert_utility");
 }

@@ -142,6 +142,13 @@ def test_permute_workspace_and_layer_rejections(L):
     rc, _ = rc_and_msg(L, "moe_grouped_swiglu_bwd", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
                        FAKE, MIS, FAKE, 0, FAKE, ctypes.c_size_t(bneed), None)
     assert rc == api.MOE_ERR_ALIGN
+    # the utility pass reads the backward's workspace: same size required
+    rc, msg = rc_and_msg(L, "moe_expert_utility", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
+                         FAKE, ctypes.c_size_t(bneed - 1), FAKE, None)
+    assert rc == api.MOE_ERR_WORKSPACE and "workspace" in msg
+    rc, msg = rc_and_msg(L, "moe_expert_utility", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
+                         FAKE, ctypes.c_size_t(bneed), None, None)
+    assert rc == api.MOE_ERR_ARG and "utility" in msg
     rc, _ = rc_and_msg(L, "moe_unpermute", None, FAKE, FAKE, FAKE, 8, 2, FAKE, None)
     assert rc == api.MOE_ERR_ARG
     rc, _ = rc_and_msg(L, "moe_permute_bwd", ctypes.byref(lay), FAKE, FAKE, 8, 17, FAKE, None)

@@ -197,3 +197,24 @@ def test_route_backward(run):
     log(f"route bwd: dX_router {e_alone:.2e}, accumulated {e_acc:.2e}")
     tol = 1e-5 if run.w.dtype == "f32" else TOL_FFN
     assert e_alone <= tol and e_acc <= tol
+
+
+def utility_check(w, r, ref, only=None):
+    """moe_expert_utility after the run's backward against the oracle (all
+    slots, or `only`).  Returns (GPU utilities, oracle utilities)."""
+    from paper_2508_19078_amd import api
+    u = torch.full((r.S_r + w.n_shared,), -1.0, dtype=torch.float32, device="cuda")
+    assert api.moe_expert_utility(r.layer_tables, r.X, r.X_perm, r.offsets, w.T, w.k, r.H, r.dO, r.ws_bwd, u) == 0
+    torch.cuda.synchronize()
+    exp = O.expert_utility(ref.X, ref.dY, ref.idx, ref.gate, ref.plan.expert_map, ref.slots, only=only)
+    return host(u), exp
+
+
+def test_expert_utility(run):
+    got, exp = utility_check(run.w, run.r, run.ref)
+    err = rel_fro(got, exp)
+    log(f"utility: rel err {err:.2e} over {len(exp)} slots")
+    assert err <= (1e-5 if run.w.dtype == "f32" else TOL_FFN)
+    np.testing.assert_array_equal(got == 0, exp == 0)      # exactly the empty slots are 0
+    rel = np.abs(got - exp) / np.maximum(exp, 1e-30)
+    assert np.all(rel[exp > 0] <= 5e-2)

@@ -101,6 +101,29 @@ def test_full_route_backward(run):
     assert e_alone <= TOL_FFN and e_acc <= TOL_FFN
 
 
+def test_full_expert_utility(run):
+    """Utility at full size: the oracle on the two smallest non-empty slots,
+    every slot non-negative and zero exactly when empty, and linear in dY
+    (a second backward with 2 dY doubles every utility)."""
+    from test_gpu_parity import utility_check
+    w, r, ref = run.w, run.r, run.ref
+    rows = np.array([len(np.unique(np.nonzero(ref.plan.expert_map[ref.idx] == s)[0])) for s in range(r.S_r)]
+                    + [w.T] * w.n_shared)
+    small = [int(s) for s in np.argsort(np.where(rows > 0, rows, 1 << 30), kind="stable")[:2]]
+    got, exp = utility_check(w, r, ref, only=small)
+    log(f"utility {w.name}: slots {small} ({rows[small]} rows) got {got[small]} oracle {exp[small]}")
+    np.testing.assert_allclose(got[small], exp[small], rtol=2e-2)
+    assert np.all(got >= 0) and np.array_equal(got == 0, rows == 0)
+    r.dY.mul_(2)
+    r.backward()
+    torch.cuda.synchronize()
+    got2, _ = utility_check(w, r, ref, only=[])
+    r.dY.div_(2)
+    r.backward()
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(got2, 2 * got, rtol=1e-5)
+
+
 def test_full_quantizer_and_histogram(run):
     ref, w = run.ref, run.w
     np.testing.assert_array_equal(run.q_g, ref.q)
