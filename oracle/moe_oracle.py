@@ -23,6 +23,10 @@ What each function follows:
 * Tuning and non-tuning experts (Section 1, Section 3): tuning experts receive
   weight gradients; non-tuning (merged, frozen) experts do not.
 * Expert FFN: SwiGLU, out = W_down (silu(W_gate x) * (W_up x)).
+* Expert utility (Section 6.1, Eq. 3): the gradient-norm utility of a slot.
+* Layer-aware merging (Section 5): the per-layer budget of Eq. 1 (Section 5.1),
+  then PCA features of the experts' parameters and K-Means with cosine
+  distance over all layers at once, cross-layer pairs masked (Section 5.2).
 
 Readings of silent or ambiguous points are listed in the design notes of the
 repository and restated at each function.  Every function here is pinned by
@@ -446,3 +450,184 @@ def expert_grad_columns(x, Wg, Wu, Wd, dO, cols):
     da_u = dh * a_g * sg
     da_g = dh * a_u * sg * (1.0 + a_g * (1.0 - sg))
     return da_g.T @ x, da_u.T @ x, dO.T @ h
+
+
+# ------------------------------------- layer-aware merging (Section 5) ----
+
+def merge_budget(counts, tuning, total_tokens, B_non: int, eps: float = 1e-12):
+    """Merging budget of each layer, Section 5.1, Eq. 1.
+
+    counts [L, E] activation counts of every layer, tuning [L, E] bool (True =
+    tuning expert), B_non the participant's total number of non-tuning slots.
+    Layer l (0-based here, the paper's l = l0 + 1) weighs
+        b_l = (L - l0) / v_l,   v_l = max(Var_e f_e, eps),   f_e = counts / T
+    (population variance over all E experts of the layer), and its share of the
+    budget is B_non * b_l / sum_k b_k.  The paper floors the share and leaves the
+    rest unassigned; here the floor is clamped to [min(1, n_l), n_l] (n_l the
+    layer's non-tuning experts: a layer with any of them needs one group, and
+    cannot have more groups than experts) and the difference to B_non is settled
+    one slot at a time: while short, +1 to the layer with the largest
+    share - B_l that is below n_l (ties: lower layer); while over, -1 to the
+    layer with the smallest share - B_l that is above its floor (ties: higher
+    layer).  With no clamp binding this is the largest-remainder rule.
+    Returns (B [L] int64, share [L] float64).
+    """
+    counts = _f64(counts)
+    tuning = np.asarray(tuning, dtype=bool)
+    L, E = counts.shape
+    f = counts / float(total_tokens)
+    v = np.maximum(f.var(axis=1), eps)
+    b = np.array([(L - l0) / v[l0] for l0 in range(L)])
+    share = B_non * b / b.sum()
+    n = (~tuning).sum(axis=1)
+    lo = np.minimum(1, n)
+    B = np.clip(np.floor(share).astype(np.int64), lo, n)
+    while B.sum() < B_non:
+        room = [l for l in range(L) if B[l] < n[l]]
+        if not room:
+            break
+        best = room[0]
+        for l in room[1:]:
+            if share[l] - B[l] > share[best] - B[best]:
+                best = l
+        B[best] += 1
+    while B.sum() > B_non:
+        room = [l for l in range(L) if B[l] > lo[l]]
+        if not room:
+            break
+        best = room[0]
+        for l in room[1:]:
+            if share[l] - B[l] <= share[best] - B[best]:
+                best = l
+        B[best] -= 1
+    return B, share
+
+
+def expert_vectors(wg, wu, wd) -> np.ndarray:
+    """Each expert's parameters as one vector: W_gate, W_up, W_down row-major,
+    concatenated in that order ([n, 3*I*d], float64)."""
+    n = np.shape(wg)[0]
+    return np.concatenate([_f64(wg).reshape(n, -1), _f64(wu).reshape(n, -1),
+                           _f64(wd).reshape(n, -1)], axis=1)
+
+
+def pca_features(vectors, r: int) -> np.ndarray:
+    """Principal-component scores of experts, Section 5.2 (first step).
+
+    The experts' parameter vectors are centred on their mean and decomposed,
+    Xc = U S V^T (thin SVD); the scores on the r leading components are
+    U[:, :r] * S[:r], components ordered by decreasing singular value.  Columns
+    beyond the rank of Xc are zero.  Returns [n, r] float64.
+    """
+    X = _f64(vectors)
+    Xc = X - X.mean(axis=0)
+    U, S, _ = np.linalg.svd(Xc, full_matrices=False)
+    n = X.shape[0]
+    Z = np.zeros((n, r), dtype=F64)
+    m = min(r, len(S))
+    Z[:, :m] = U[:, :m] * S[:m]
+    return Z
+
+
+def unit_rows(Z) -> np.ndarray:
+    """Rows scaled to unit length; a zero row stays zero."""
+    Z = _f64(Z)
+    nrm = np.sqrt(np.sum(Z * Z, axis=1))
+    out = np.zeros_like(Z)
+    nz = nrm > 0
+    out[nz] = Z[nz] / nrm[nz, None]
+    return out
+
+
+def cosine_to_centroids(Zhat, C) -> np.ndarray:
+    """cos(z, c) for unit rows z and centroids c; 0 where |c| = 0."""
+    Zhat, C = _f64(Zhat), _f64(C)
+    cn = np.sqrt(np.sum(C * C, axis=1))
+    dots = Zhat @ C.T
+    out = np.zeros_like(dots)
+    nz = cn > 0
+    out[:, nz] = dots[:, nz] / cn[nz]
+    return out
+
+
+def maximin_seeds(Z, B: int) -> List[int]:
+    """Initial centroids of one layer: experts chosen by farthest-first
+    traversal under cosine distance 1 - cos.  The first is the expert farthest
+    from the mean (largest score norm |z|); each next one is the unchosen expert
+    whose distance to its nearest chosen seed is largest.  Ties: lower index.
+    (The paper initialises the centroids without saying how.)
+    """
+    Z = _f64(Z)
+    n = Z.shape[0]
+    if B == 0 or n == 0:
+        return []
+    Zhat = unit_rows(Z)
+    nrm2 = np.sum(Z * Z, axis=1)
+    first = 0
+    for e in range(1, n):
+        if nrm2[e] > nrm2[first]:
+            first = e
+    seeds = [first]
+    mind = 1.0 - Zhat @ Zhat[first]
+    while len(seeds) < B:
+        best = -1
+        for e in range(n):
+            if e in seeds:
+                continue
+            if best < 0 or mind[e] > mind[best]:
+                best = e
+        seeds.append(best)
+        mind = np.minimum(mind, 1.0 - Zhat @ Zhat[best])
+    return seeds
+
+
+def fused_kmeans(features: Sequence, budgets: Sequence[int], max_iter: int):
+    """K-Means with cosine distance over every layer at once, Section 5.2.
+
+    features[l] [n_l, r] are the layers' expert features, budgets[l] = B_l the
+    number of clusters of layer l.  All sum_l B_l centroids are held together,
+    each labelled with its layer; one matrix of cosine similarities between all
+    experts and all centroids drives the assignment, with every expert-centroid
+    pair from different layers masked out (similarity -inf: such a centroid is
+    never chosen).  Features are compared as unit vectors; a centroid is the
+    mean of its members' unit features (an empty cluster keeps its centroid).
+    Each pass assigns every expert to its most similar centroid (ties: lower
+    centroid) and stops when no label changes or after max_iter passes.
+    Returns (labels: list of [n_l] int64 cluster ids within the layer,
+    passes: [L] int64, the pass after which each layer's labels stopped
+    changing, or max_iter).
+    """
+    L = len(features)
+    Zh = [unit_rows(z) for z in features]
+    layer_of_expert = np.concatenate([np.full(len(z), l) for l, z in enumerate(Zh)])
+    first_c = np.concatenate([[0], np.cumsum(budgets)]).astype(np.int64)
+    layer_of_centroid = np.concatenate([np.full(B, l) for l, B in enumerate(budgets)])
+    Zall = np.concatenate(Zh, axis=0) if L else np.zeros((0, 0))
+    r = Zall.shape[1] if Zall.size else 0
+    C = np.zeros((int(first_c[-1]), r), dtype=F64)
+    for l in range(L):
+        for j, e in enumerate(maximin_seeds(features[l], int(budgets[l]))):
+            C[first_c[l] + j] = Zh[l][e]
+    mask = layer_of_expert[:, None] != layer_of_centroid[None, :]
+    prev = None
+    passes = np.full(L, max_iter, dtype=np.int64)
+    it = 0
+    while True:
+        sim = cosine_to_centroids(Zall, C)
+        sim[mask] = -np.inf
+        lab = np.argmax(sim, axis=1) if sim.shape[1] else np.zeros(len(Zall), np.int64)
+        it += 1
+        if prev is not None:
+            for l in range(L):
+                sel = layer_of_expert == l
+                if passes[l] == max_iter and np.array_equal(lab[sel], prev[sel]):
+                    passes[l] = it
+        if (prev is not None and np.array_equal(lab, prev)) or it >= max_iter:
+            break
+        for c in range(C.shape[0]):
+            members = np.nonzero(lab == c)[0]
+            if len(members):
+                C[c] = Zall[members].mean(axis=0)
+        prev = lab
+    labels = [lab[layer_of_expert == l] - first_c[l] for l in range(L)]
+    return labels, passes

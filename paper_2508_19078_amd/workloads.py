@@ -28,6 +28,7 @@ import numpy as np
 
 # tensor ids of the seed key
 TID_X, TID_WR, TID_BIAS, TID_WG, TID_WU, TID_WD, TID_DY, TID_SHARED = range(8)
+TID_PROTO, TID_CLASS, TID_COUNTS = 8, 9, 10
 
 
 @dataclass(frozen=True)
@@ -213,6 +214,66 @@ def draw_experts(w: LayerWorkload, layer: int = 0,
     wd = draw_stacked([[w.cid, layer, base + TID_WD, e] for e in experts],
                       (w.d, w.I), 1.0 / np.sqrt(w.I), w.dtype)
     return wg, wu, wd
+
+
+def draw_counts(w: LayerWorkload, layer: int = 0) -> np.ndarray:
+    """Activation counts of one layer (int32 [E]): its T*k routing choices
+    spread over the experts by a multinomial draw with probabilities
+    proportional to exp(bias), the layer's router bias.  A stand-in for the
+    profiled histogram where only the counts matter (the per-layer budget)."""
+    rng = np.random.Generator(np.random.PCG64(
+        np.random.SeedSequence([w.cid, layer, TID_COUNTS])))
+    b = router_bias(w, layer).astype(np.float64)
+    p = np.exp(b - b.max())
+    return rng.multinomial(w.T * w.k, p / p.sum()).astype(np.int32)
+
+
+def expert_classes(w: LayerWorkload, layer: int, n_classes: int) -> np.ndarray:
+    """A seeded class in [0, n_classes) for each of the layer's E experts."""
+    rng = np.random.Generator(np.random.PCG64(
+        np.random.SeedSequence([w.cid, layer, TID_CLASS])))
+    return rng.integers(0, n_classes, size=w.E)
+
+
+def draw_planted_experts(w: LayerWorkload, layer: int, n_classes: int, mix: float,
+                         experts: Optional[Sequence[int]] = None):
+    """Experts with shared structure, for the similarity clustering of merging.
+
+    Expert e of class c = expert_classes(...)[e] is
+        W_e = sqrt(mix) * P_c + sqrt(1 - mix) * N_e
+    for each of its three matrices, P_c a prototype of the class drawn like an
+    expert (its own seed keys) and N_e the expert's own draw of draw_experts;
+    the sum is formed in float32 and rounded once to the storage type, so the
+    entries keep the variance of a plain expert.  mix = 0 gives draw_experts.
+    Returns (W_gate [n,I,d], W_up [n,I,d], W_down [n,d,I]).
+    """
+    if experts is None:
+        experts = range(w.E)
+    experts = list(experts)
+    cls = expert_classes(w, layer, n_classes)
+    a, b = np.float32(np.sqrt(mix)), np.float32(np.sqrt(1.0 - mix))
+    out = []
+    for tid, shape, std in ((TID_WG, (w.I, w.d), 1.0 / np.sqrt(w.d)),
+                            (TID_WU, (w.I, w.d), 1.0 / np.sqrt(w.d)),
+                            (TID_WD, (w.d, w.I), 1.0 / np.sqrt(w.I))):
+        n = int(np.prod(shape))
+        protos = {}
+        store = np.empty((len(experts), n), dtype=np.uint16 if w.dtype == "bf16" else np.float32)
+
+        def one(i):
+            e = experts[i]
+            c = int(cls[e])
+            x = _draw([w.cid, layer, tid, e], n, std, "f32")
+            x *= b
+            x += a * protos[c]
+            store[i] = round_to_bf16_bits(x) if w.dtype == "bf16" else x
+
+        for c in sorted({int(cls[e]) for e in experts}):
+            protos[c] = _draw([w.cid, layer, TID_PROTO * 16 + tid, c], n, std, "f32")
+        with ThreadPoolExecutor(_threads()) as ex:
+            list(ex.map(one, range(len(experts))))
+        out.append(Tensor(store.reshape(-1), w.dtype, (len(experts),) + shape))
+    return tuple(out)
 
 
 def to_torch(t: Tensor, device="cpu"):
