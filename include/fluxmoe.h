@@ -180,6 +180,63 @@ int moe_slot_pointers(const int32_t* slot_src, int S, int E, int d, int I, int d
                       const void** w_gate, const void** w_up, const void** w_down,
                       void* stream);
 
+/* ------------------------------------------------- layer-aware merging ----
+ * moe_merge_budget: how many groups each layer's non-tuning experts are
+ * merged into (Section 5.1, Eq. 1).  For layer l = 0..L-1 (the paper's l + 1):
+ *   f_e = counts[l, e] / total_tokens,  v_l = max(population variance of f
+ *   over the layer's E experts, eps),   b_l = (L - l) / v_l,
+ *   share_l = B_non * b_l / sum_k b_k   (fp64; sum in layer order).
+ * budget_l = floor(share_l) clamped to [min(1, n_l), n_l], n_l the layer's
+ * non-tuning experts; then, while the total is below B_non, +1 to the layer
+ * with the largest share_l - budget_l that is below n_l (ties: lower layer);
+ * while above, -1 to the layer with the smallest share_l - budget_l above its
+ * floor (ties: higher layer).  The total equals B_non whenever
+ * sum min(1, n_l) <= B_non <= sum n_l.
+ *   counts [L, E] int32 (device), tuning [L, E] uint8 (device, 1 = tuning
+ *   expert), budget [L] int32 (device, written).  1 <= L <= 1024.
+ */
+int moe_merge_budget(const int32_t* counts, const uint8_t* tuning, int L, int E,
+                     float total_tokens, int B_non, double eps, int32_t* budget,
+                     void* stream);
+
+/* moe_cluster_experts: which non-tuning experts of each layer share a group
+ * (Section 5.2), for all L layers in one call.
+ *   Features: the parameters of expert (l, e) form one vector, W_gate, W_up and
+ *   W_down row-major in that order (D = 3 I d values).  Over the layer's n_l
+ *   non-tuning experts the vectors are centred on their mean; the features are
+ *   the scores on the r leading principal components (U sqrt(lambda) of the
+ *   centred n_l x n_l Gram matrix, eigenvalues descending, ties lower index;
+ *   components past the rank score 0), scaled to unit length (a zero vector
+ *   stays zero).  The Gram matrix accumulates the stored values' products in
+ *   fp32 per 32768-parameter chunk and sums chunks in fp64; the
+ *   eigen-decomposition (cyclic Jacobi) and all that follows are fp64.
+ *   K-Means with cosine similarity: B_l = clamp(budget[l], 1, n_l) centroids
+ *   per layer, seeded by farthest-first traversal under 1 - cos (first the
+ *   expert with the largest score norm, then the unchosen expert farthest from
+ *   its nearest seed; ties lower index).  Each pass assigns every expert to the
+ *   most similar centroid of its own layer (ties: lower centroid), then sets
+ *   each centroid to the mean of its members' unit features (an empty cluster
+ *   keeps its centroid).  A layer stops at the first pass that changes none of
+ *   its labels, or after max_iter passes.
+ *   w_src   device array of 3*L*E device pointers, (gate, up, down) of expert
+ *           (l, e) at 3*(l*E + e) + {0, 1, 2}; gate/up [I, d], down [d, I],
+ *           16-byte aligned, in dtype (MOE_BF16 or MOE_F32).
+ *   tuning  [L, E] uint8 (device), 1 = tuning expert (not clustered).
+ *   budget  [L] int32 (device), e.g. from moe_merge_budget.
+ *   labels  [L, E] int32 (device, written): cluster in [0, B_l) for non-tuning
+ *           experts, -1 for tuning ones.
+ *   features  optional [L, E, r] fp32 (device): the unit features, 0 for
+ *           tuning experts.   iters  optional [L] int32: passes run.
+ *   ws      device workspace of moe_cluster_workspace_size(L, E, d, I) bytes.
+ * Limits: E <= 64, 1 <= r <= 32, I*d*element size a multiple of 16 bytes,
+ * max_iter >= 1.
+ */
+size_t moe_cluster_workspace_size(int L, int E, int d, int I);
+int moe_cluster_experts(const void* const* w_src, int dtype, int L, int E, int d, int I,
+                        const uint8_t* tuning, const int32_t* budget, int r, int max_iter,
+                        void* ws, size_t ws_bytes, int32_t* labels, float* features,
+                        int32_t* iters, void* stream);
+
 /* ------------------------------------------------------------ the layer ----
  * A layer's slots: routed slots 0..S_routed-1 (kept experts and merged
  * groups), then S_shared always-on shared experts (gate 1.0, every token).

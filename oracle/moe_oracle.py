@@ -506,9 +506,9 @@ def merge_budget(counts, tuning, total_tokens, B_non: int, eps: float = 1e-12):
 def expert_vectors(wg, wu, wd) -> np.ndarray:
     """Each expert's parameters as one vector: W_gate, W_up, W_down row-major,
     concatenated in that order ([n, 3*I*d], float64)."""
-    n = np.shape(wg)[0]
-    return np.concatenate([_f64(wg).reshape(n, -1), _f64(wu).reshape(n, -1),
-                           _f64(wd).reshape(n, -1)], axis=1)
+    mats = [_f64(m) for m in (wg, wu, wd)]
+    n = mats[0].shape[0]
+    return np.concatenate([m.reshape(n, int(np.prod(m.shape[1:]))) for m in mats], axis=1)
 
 
 def pca_features(vectors, r: int) -> np.ndarray:

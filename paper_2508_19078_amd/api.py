@@ -61,6 +61,10 @@ _SIGS = {
     "moe_grouped_swiglu_bwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
     "moe_permute_bwd": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
     "moe_expert_utility": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp, _vp]),
+    "moe_merge_budget": (_c_int, [_vp, _vp, _c_int, _c_int, _f, _c_int, ctypes.c_double, _vp, _vp]),
+    "moe_cluster_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
+    "moe_cluster_experts": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int,
+                                     _vp, _c_size, _vp, _vp, _vp, _vp]),
 }
 
 _lib = None
@@ -206,6 +210,27 @@ def moe_slot_pointers(slot_src, S, E, d, I, dtype, orig, merged, w_gate, w_up, w
     return _call("moe_slot_pointers", ptr(slot_src), S, E, d, I, dtype_code(dtype), ptr(orig[0]),
                  ptr(orig[1]), ptr(orig[2]), ptr(merged[0]), ptr(merged[1]), ptr(merged[2]), ptr(w_gate),
                  ptr(w_up), ptr(w_down), stream_ptr(stream))
+
+
+# --------------------------------------------------- layer-aware merging ----
+
+def moe_merge_budget(counts, tuning, total_tokens, B_non, budget, eps=1e-12, stream=None):
+    """counts [L, E] int32, tuning [L, E] uint8 (1 = tuning), budget [L] int32."""
+    L, E = counts.shape
+    return _call("moe_merge_budget", ptr(counts), ptr(tuning), L, E, float(total_tokens), int(B_non),
+                 float(eps), ptr(budget), stream_ptr(stream))
+
+
+def moe_cluster_workspace_size(L, E, d, I) -> int:
+    return lib().moe_cluster_workspace_size(L, E, d, I)
+
+
+def moe_cluster_experts(w_src_ptrs, dtype, L, E, d, I, tuning, budget, r, max_iter, ws, labels,
+                        features=None, iters=None, stream=None):
+    """w_src_ptrs: int64 device tensor of 3 pointers per expert (layer-major)."""
+    return _call("moe_cluster_experts", ptr(w_src_ptrs), dtype_code(dtype), L, E, d, I, ptr(tuning),
+                 ptr(budget), int(r), int(max_iter), ptr(ws), ws.numel() * ws.element_size(), ptr(labels),
+                 ptr(features), ptr(iters), stream_ptr(stream))
 
 
 # ------------------------------------------------------------- the layer ----

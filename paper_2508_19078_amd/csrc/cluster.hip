@@ -1,0 +1,685 @@
+// Layer-aware merging of the non-tuning experts (Section 5): the merging
+// budget of each layer (Section 5.1, Eq. 1) and the similarity clustering that
+// decides which experts share a group (Section 5.2): PCA features of the
+// experts' parameters, then K-Means with cosine distance over every layer in
+// one launch.
+//
+// PCA of n experts with D = 3 I d parameters each goes through the n x n Gram
+// matrix of the parameter vectors (the scores are U sqrt(lambda) from the
+// eigen-decomposition of the centred Gram matrix), so the only pass over the
+// weights is the Gram product: an HBM-bound MFMA contraction over D, split
+// into chunks of 32768 parameters, one block per (chunk, layer).  The
+// per-layer eigen-decomposition (parallel cyclic Jacobi in fp64) and K-Means
+// run in one block per layer; a centroid only ever meets experts of its own
+// layer, which is the paper's masking of cross-layer distances.
+#include "common.hpp"
+#include "gemm_bf16.hpp"
+
+namespace fm {
+namespace {
+
+constexpr int CL_NMAX = 64;        // experts per layer
+constexpr int CL_RMAX = 32;        // feature dimension
+constexpr int GR_ROWB = 512;       // bytes of one expert's parameters per slab
+constexpr int GR_NS = 4;           // slabs in the LDS ring (3 in flight)
+constexpr long GR_KC = 32768;      // parameters per chunk
+constexpr int CL_MAXL = 1024;      // layers of one budget call
+constexpr int JAC_SWEEPS = 40;
+
+// ------------------------------------------------------------ Eq. 1 ------
+
+// One block.  Thread l computes layer l's variance and weight; thread 0 sums
+// the weights in layer order and settles the integer budgets serially.
+__global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict__ counts,
+                                                      const uint8_t* __restrict__ tuning, int L,
+                                                      int E, double total, int B_non, double eps,
+                                                      int32_t* __restrict__ budget) {
+  __shared__ double sh[CL_MAXL];
+  __shared__ int sB[CL_MAXL], sn[CL_MAXL];
+  __shared__ double s_sum;
+  for (int l = threadIdx.x; l < L; l += blockDim.x) {
+    const int32_t* c = counts + (size_t)l * E;
+    double mean = 0.0;
+    for (int e = 0; e < E; ++e) mean += (double)c[e] / total;
+    mean /= E;
+    double v = 0.0;
+    int n = 0;
+    for (int e = 0; e < E; ++e) {
+      const double dl = (double)c[e] / total - mean;
+      v += dl * dl;
+      n += tuning[(size_t)l * E + e] == 0;
+    }
+    v = fmax(v / E, eps);
+    sh[l] = (double)(L - l) / v;       // the paper's (L - l + 1) with l counted from 1
+    sn[l] = n;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double s = 0.0;
+    for (int l = 0; l < L; ++l) s += sh[l];
+    s_sum = s;
+  }
+  __syncthreads();
+  for (int l = threadIdx.x; l < L; l += blockDim.x) {
+    const double share = (double)B_non * sh[l] / s_sum;
+    sh[l] = share;
+    const int lo = min(1, sn[l]);
+    sB[l] = (int)fmin(fmax(floor(share), (double)lo), (double)sn[l]);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long tot = 0;
+    for (int l = 0; l < L; ++l) tot += sB[l];
+    while (tot < B_non) {              // short: the largest share - B_l with room
+      int best = -1;
+      for (int l = 0; l < L; ++l)
+        if (sB[l] < sn[l] && (best < 0 || sh[l] - sB[l] > sh[best] - sB[best])) best = l;
+      if (best < 0) break;
+      ++sB[best];
+      ++tot;
+    }
+    while (tot > B_non) {              // over: the smallest share - B_l above its floor
+      int best = -1;
+      for (int l = 0; l < L; ++l)
+        if (sB[l] > min(1, sn[l]) && (best < 0 || sh[l] - sB[l] <= sh[best] - sB[best])) best = l;
+      if (best < 0) break;
+      --sB[best];
+      --tot;
+    }
+  }
+  __syncthreads();
+  for (int l = threadIdx.x; l < L; l += blockDim.x) budget[l] = sB[l];
+}
+
+// -------------------------------------------------------- Gram product ----
+
+// Wave 0 lists the layer's non-tuning experts in index order (E <= 64).
+__device__ __forceinline__ int list_members(const uint8_t* tuning, int l, int E, int* mem) {
+  __shared__ int s_n;
+  if (threadIdx.x < 64) {
+    const int e = threadIdx.x;
+    const bool non = e < E && tuning[(size_t)l * E + e] == 0;
+    const uint64_t m = __ballot(non);
+    if (non) mem[__popcll(m & ((1ull << e) - 1ull))] = e;
+    if (e == 0) s_n = __popcll(m);
+  }
+  __syncthreads();
+  return s_n;
+}
+
+struct GramArgs {
+  const void* const* w_src;   // [3 * L * E]: (gate, up, down) of expert (l, e)
+  const uint8_t* tuning;      // [L * E]
+  float* part;                // [L][nchunk][NT][32][32]
+  long P;                     // parameters per matrix, I * d
+  int E, cpm;                 // experts per layer, chunks per matrix
+};
+
+// Slab layout in LDS: [row group g (16 rows)][128-byte line m][64-byte half h]
+// blocks of [16 rows][4 chunks of 16 bytes], one DMA instruction each, the
+// chunk index XOR-swizzled by (row >> 2) & 3.  Wave w reads line w of every
+// row (its four 16-parameter k-steps), so the waves split each slab's k range.
+template <typename T> struct GramFrag;
+template <> struct GramFrag<bf16> {
+  typedef bf16x8_t frag;
+  static __device__ __forceinline__ frag load(const FM_LDS char* p) { return *(const FM_LDS bf16x8_t*)p; }
+  static __device__ __forceinline__ frag zero() { return frag{}; }
+  static __device__ __forceinline__ f32x16_t mma(const frag& a, const frag& b, const f32x16_t& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct GramFrag<float> {
+  typedef f32x4_t frag;
+  static __device__ __forceinline__ frag load(const FM_LDS char* p) { return *(const FM_LDS f32x4_t*)p; }
+  static __device__ __forceinline__ frag zero() { return frag{0.f, 0.f, 0.f, 0.f}; }
+  static __device__ __forceinline__ f32x16_t mma(const frag& a, const frag& b, f32x16_t c) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[e], b[e], c, 0, 0, 0);
+    return c;
+  }
+};
+
+template <int INS> __device__ __forceinline__ void gram_wait(int ahead) {
+  if (ahead >= 2) wait_vmcnt<2 * INS>();
+  else if (ahead == 1) wait_vmcnt<INS>();
+  else wait_vmcnt<0>();
+}
+
+// NG groups of 16 rows hold the n experts (rows past n repeat row n - 1).
+template <typename T, int NB, int NG>
+__device__ __forceinline__ void gram_chunk(const GramArgs& a, const int* mem, int n, int l, int mat,
+                                           long k0, long klen, FM_LDS char* lds, f32x16_t* acc) {
+  constexpr int ROWS = NB * 32, SLAB = ROWS * GR_ROWB;
+  constexpr int EPS = GR_ROWB / (int)sizeof(T);       // parameters per row and slab
+  constexpr int EPC = 16 / (int)sizeof(T);            // parameters per 16-byte chunk
+  constexpr int INS = 2 * NG;                         // DMA instructions per wave and slab
+  constexpr int NT = NB * (NB + 1) / 2;
+  static_assert(NG >= 1 && NG <= 2 * NB, "row groups");
+  typedef GramFrag<T> F;
+  const int lane = lane_id_here(), wave = wave_id();
+  const int nslab = (int)((klen + EPS - 1) / EPS);
+  const int tail_chunks = (int)((klen - (long)(nslab - 1) * EPS) / EPC);
+
+  // DMA plan: instruction u = wave * INS + q moves line m, half h of group g.
+  const char* gp[INS];
+  int cix[INS];
+  uint32_t dst[INS];
+#pragma unroll
+  for (int q = 0; q < INS; ++q) {
+    const int u = wave * INS + q, g = u >> 3, m = (u >> 1) & 3, h = u & 1;
+    const int rr = lane >> 2, row = g * 16 + rr;
+    const int chunk = m * 8 + h * 4 + ((lane & 3) ^ ((rr >> 2) & 3));
+    const int e = mem[min(row, n - 1)];
+    const char* base = (const char*)a.w_src[3 * ((size_t)l * a.E + e) + mat];
+    gp[q] = base + (k0 * (long)sizeof(T)) + chunk * 16;
+    cix[q] = chunk;
+    dst[q] = (uint32_t)(((g * 4 + m) * 2 + h) * 1024);
+  }
+  auto issue = [&](int s) {
+    FM_LDS char* slab = lds + (s % GR_NS) * SLAB;
+    const bool last = s == nslab - 1;
+#pragma unroll
+    for (int q = 0; q < INS; ++q) {
+      const char* src = gp[q] + (long)s * GR_ROWB;
+      if (last && cix[q] >= tail_chunks) src -= cix[q] * 16;   // any valid address: masked below
+      dma16(src, slab + dst[q]);
+    }
+  };
+
+  const int pre = min(GR_NS - 1, nslab);
+  for (int s = 0; s < pre; ++s) issue(s);
+
+  // fragment addresses: lane (i, hf) reads row 32 b + i, k-steps j = 0..3 of line `wave`
+  const int i = lane & 31, hf = lane >> 5;
+  for (int s = 0; s < nslab; ++s) {
+    gram_wait<INS>(min(GR_NS - 2, nslab - 1 - s));
+    barrier_lds();
+    if (s + GR_NS - 1 < nslab) issue(s + GR_NS - 1);
+    const FM_LDS char* slab = lds + (s % GR_NS) * SLAB;
+    const bool last = s == nslab - 1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int cc = 2 * j + hf, h = cc >> 2, q = cc & 3;
+      typename F::frag fr[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int R = 32 * b + i, g = R >> 4, rr = R & 15;
+        fr[b] = F::load(slab + ((g * 4 + wave) * 2 + h) * 1024 + rr * 64 + ((q ^ ((rr >> 2) & 3)) << 4));
+      }
+      if (last && wave * 8 + cc >= tail_chunks) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) fr[b] = F::zero();
+      }
+      int t = 0;
+#pragma unroll
+      for (int b1 = 0; b1 < NB; ++b1)
+#pragma unroll
+        for (int b2 = b1; b2 < NB; ++b2) acc[t] = F::mma(fr[b1], fr[b2], acc[t]), ++t;
+    }
+  }
+  (void)NT;
+}
+
+// Partial Gram matrix of one chunk of one matrix (gate, up or down) of the
+// layer's non-tuning experts: tiles (b1 <= b2) of 32 x 32, the four waves'
+// k-subranges summed in wave order.  Register r of a tile's lane L holds
+// G[32 b1 + 8 (r / 4) + 4 (L / 32) + r % 4][32 b2 + L % 32].
+template <typename T, int NB>
+__global__ __launch_bounds__(256) void k_gram(GramArgs a) {
+  constexpr int NT = NB * (NB + 1) / 2;
+  __shared__ __align__(1024) char lds_raw[GR_NS * NB * 32 * GR_ROWB];
+  __shared__ int mem[CL_NMAX];
+  FM_LDS char* lds = (FM_LDS char*)lds_raw;
+  const int l = blockIdx.y, c = blockIdx.x, nchunk = gridDim.x;
+  const int n = list_members(a.tuning, l, a.E, mem);
+  const int mat = c / a.cpm;
+  const long k0 = (long)(c % a.cpm) * GR_KC;
+  const long klen = a.P - k0 < GR_KC ? a.P - k0 : GR_KC;
+
+  f32x16_t acc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
+  const int ng = (n + 15) >> 4;
+  if (ng == 1) gram_chunk<T, NB, 1>(a, mem, n, l, mat, k0, klen, lds, acc);
+  else if (ng == 2) gram_chunk<T, NB, 2>(a, mem, n, l, mat, k0, klen, lds, acc);
+  if constexpr (NB == 2) {
+    if (ng == 3) gram_chunk<T, NB, 3>(a, mem, n, l, mat, k0, klen, lds, acc);
+    else if (ng == 4) gram_chunk<T, NB, 4>(a, mem, n, l, mat, k0, klen, lds, acc);
+  }
+  __syncthreads();
+
+  // sum the four waves' accumulators in wave order
+  float* red = (float*)lds_raw;                        // [wave][t][r][lane]
+  const int lane = lane_id(), wave = wave_id();
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[((wave * NT + t) * 16 + r) * 64 + lane] = acc[t][r];
+  __syncthreads();
+  float* out = a.part + ((size_t)l * nchunk + c) * NT * 1024;
+  for (int x = threadIdx.x; x < NT * 1024; x += blockDim.x) {
+    const int t = x >> 10, r = (x >> 6) & 15, L = x & 63;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) s += red[((w * NT + t) * 16 + r) * 64 + L];
+    const int p = 8 * (r >> 2) + 4 * (L >> 5) + (r & 3), q = L & 31;
+    out[t * 1024 + p * 32 + q] = s;
+  }
+}
+
+// G[l][t][p][q] = sum over chunks (in chunk order, fp64) of the partials.
+__global__ __launch_bounds__(256) void k_gram_sum(const float* __restrict__ part, int nchunk, int NT,
+                                                  double* __restrict__ G) {
+  const int l = blockIdx.y, x = blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= NT * 1024) return;
+  const float* p = part + (size_t)l * nchunk * NT * 1024 + x;
+  double s = 0.0;
+  for (int c = 0; c < nchunk; ++c) s += (double)p[(size_t)c * NT * 1024];
+  G[(size_t)l * NT * 1024 + x] = s;
+}
+
+// ------------------------------------------- PCA and K-Means per layer ----
+
+constexpr int LDA = CL_NMAX + 1;
+constexpr int LDZ = CL_RMAX + 1;
+
+struct ClusterLds {
+  double A[CL_NMAX * LDA];      // centred Gram matrix, rotated to diagonal
+  double V[CL_NMAX * LDA];      // eigenvectors (columns)
+  double Z[CL_NMAX * LDZ];      // unit features
+  double C[CL_NMAX * LDZ];      // centroids
+  double rc[CL_NMAX / 2], rs[CL_NMAX / 2];
+  double rho[CL_NMAX], nrm2[CL_NMAX], mind[CL_NMAX], cn[CL_NMAX];
+  double red[2][256];
+  double bsim[4][CL_NMAX];
+  int bj[4][CL_NMAX];
+  int mem[CL_NMAX], comp[CL_RMAX], lab[CL_NMAX], chosen[CL_NMAX];
+  int flag;
+};
+
+// Round-robin pairing of m indices (m even): m / 2 disjoint pairs per round,
+// every pair once over m - 1 rounds.
+__device__ __forceinline__ void rr_pair(int round, int k, int m, int& p, int& q) {
+  int x, y;
+  if (k == 0) {
+    x = m - 1;
+    y = round;
+  } else {
+    x = (round + k) % (m - 1);
+    y = (round - k + (m - 1)) % (m - 1);
+  }
+  p = min(x, y);
+  q = max(x, y);
+}
+
+// Wave-wide (value desc, index asc) maximum.
+__device__ __forceinline__ void wave_argmax(double& v, int& idx) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const double ov = __shfl_xor(v, o);
+    const int oi = __shfl_xor(idx, o);
+    if (ov > v || (ov == v && oi < idx)) {
+      v = ov;
+      idx = oi;
+    }
+  }
+}
+
+struct ClusterArgs {
+  const double* G;            // [L][NT][32][32]
+  const uint8_t* tuning;
+  const int32_t* budget;
+  int32_t* labels;            // [L * E]
+  float* features;            // [L * E * r] or nullptr
+  int32_t* iters;             // [L] or nullptr
+  int E, NB, r, max_iter;
+};
+
+__global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
+  __shared__ ClusterLds S;
+  const int l = blockIdx.x, tid = threadIdx.x, lane = lane_id(), wave = wave_id();
+  const int E = a.E, r = a.r;
+  const int n = list_members(a.tuning, l, E, S.mem);
+  const int NT = a.NB * (a.NB + 1) / 2;
+
+  // outputs of tuning experts
+  for (int e = tid; e < E; e += blockDim.x) {
+    if (a.tuning[(size_t)l * E + e] != 0) {
+      a.labels[(size_t)l * E + e] = -1;
+      if (a.features)
+        for (int j = 0; j < r; ++j) a.features[((size_t)l * E + e) * r + j] = 0.f;
+    }
+  }
+  if (n == 0) {
+    if (a.iters && tid == 0) a.iters[l] = 0;
+    return;
+  }
+  const int B = min(max(a.budget[l], 1), n);
+  const int m = n + (n & 1);
+
+  // 1. Gram matrix (symmetrised), centred on the experts' mean.
+  const double* G = a.G + (size_t)l * NT * 1024;
+  auto g_at = [&](int i, int j) {
+    const int b1 = i >> 5, b2 = j >> 5;
+    const int t = b1 * a.NB - b1 * (b1 - 1) / 2 + (b2 - b1);
+    return G[t * 1024 + (i & 31) * 32 + (j & 31)];
+  };
+  for (int x = tid; x < m * m; x += blockDim.x) {
+    const int i = x / m, j = x % m;
+    double v = 0.0;
+    if (i < n && j < n) {
+      if ((i >> 5) < (j >> 5)) v = g_at(i, j);
+      else if ((i >> 5) > (j >> 5)) v = g_at(j, i);
+      else v = 0.5 * (g_at(i, j) + g_at(j, i));
+    }
+    S.A[i * LDA + j] = v;
+    S.V[i * LDA + j] = i == j ? 1.0 : 0.0;
+  }
+  __syncthreads();
+  if (tid < n) {
+    double s = 0.0;
+    for (int j = 0; j < n; ++j) s += S.A[tid * LDA + j];
+    S.rho[tid] = s / n;
+  }
+  __syncthreads();
+  {
+    double mu = 0.0;
+    for (int i = 0; i < n; ++i) mu += S.rho[i];
+    mu /= n;
+    for (int x = tid; x < n * n; x += blockDim.x) {
+      const int i = x / n, j = x % n;
+      S.A[i * LDA + j] = S.A[i * LDA + j] - S.rho[i] - S.rho[j] + mu;
+    }
+  }
+  __syncthreads();
+
+  // 2. Eigen-decomposition: parallel cyclic Jacobi, A <- J^T A J, V <- V J.
+  for (int sweep = 0; sweep < JAC_SWEEPS; ++sweep) {
+    double off = 0.0, tot = 0.0;
+    for (int x = tid; x < m * m; x += blockDim.x) {
+      const int i = x / m, j = x % m;
+      const double v = S.A[i * LDA + j] * S.A[i * LDA + j];
+      tot += v;
+      if (i != j) off += v;
+    }
+    S.red[0][tid] = off;
+    S.red[1][tid] = tot;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+      if (tid < h) {
+        S.red[0][tid] += S.red[0][tid + h];
+        S.red[1][tid] += S.red[1][tid + h];
+      }
+      __syncthreads();
+    }
+    const bool done = S.red[0][0] <= 1e-28 * S.red[1][0];
+    __syncthreads();
+    if (done) break;
+    for (int round = 0; round < m - 1; ++round) {
+      if (tid < m / 2) {
+        int p, q;
+        rr_pair(round, tid, m, p, q);
+        const double apq = S.A[p * LDA + q];
+        double c = 1.0, s = 0.0;
+        if (apq != 0.0) {
+          const double tau = (S.A[q * LDA + q] - S.A[p * LDA + p]) / (2.0 * apq);
+          const double t = fabs(tau) > 1e150 ? 0.5 / tau
+                                              : (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+          c = 1.0 / sqrt(1.0 + t * t);
+          s = t * c;
+        }
+        S.rc[tid] = c;
+        S.rs[tid] = s;
+      }
+      __syncthreads();
+      for (int x = tid; x < (m / 2) * m; x += blockDim.x) {
+        const int k = x / m, j = x % m;
+        int p, q;
+        rr_pair(round, k, m, p, q);
+        const double c = S.rc[k], s = S.rs[k];
+        const double ap = S.A[p * LDA + j], aq = S.A[q * LDA + j];
+        S.A[p * LDA + j] = c * ap - s * aq;
+        S.A[q * LDA + j] = s * ap + c * aq;
+      }
+      __syncthreads();
+      for (int x = tid; x < (m / 2) * m; x += blockDim.x) {
+        const int k = x / m, i = x % m;
+        int p, q;
+        rr_pair(round, k, m, p, q);
+        const double c = S.rc[k], s = S.rs[k];
+        const double ap = S.A[i * LDA + p], aq = S.A[i * LDA + q];
+        S.A[i * LDA + p] = c * ap - s * aq;
+        S.A[i * LDA + q] = s * ap + c * aq;
+        const double vp = S.V[i * LDA + p], vq = S.V[i * LDA + q];
+        S.V[i * LDA + p] = c * vp - s * vq;
+        S.V[i * LDA + q] = s * vp + c * vq;
+      }
+      __syncthreads();
+    }
+  }
+
+  // 3. Features: scores on the r leading components (eigenvalue desc, ties
+  // lower index), then scaled to unit length.
+  if (tid < r) S.comp[tid] = -1;
+  __syncthreads();
+  if (tid < n) {
+    const double li = S.A[tid * LDA + tid];
+    int rank = 0;
+    for (int q = 0; q < n; ++q) {
+      const double lq = S.A[q * LDA + q];
+      rank += (lq > li) || (lq == li && q < tid);
+    }
+    if (rank < r) S.comp[rank] = tid;
+  }
+  __syncthreads();
+  for (int x = tid; x < n * r; x += blockDim.x) {
+    const int e = x / r, j = x % r, p = S.comp[j];
+    S.Z[e * LDZ + j] = p < 0 ? 0.0 : sqrt(fmax(S.A[p * LDA + p], 0.0)) * S.V[e * LDA + p];
+  }
+  __syncthreads();
+  if (tid < n) {
+    double s = 0.0;
+    for (int j = 0; j < r; ++j) s += S.Z[tid * LDZ + j] * S.Z[tid * LDZ + j];
+    S.nrm2[tid] = s;
+  }
+  __syncthreads();
+  for (int x = tid; x < n * r; x += blockDim.x) {
+    const int e = x / r, j = x % r;
+    const double nr = sqrt(S.nrm2[e]);
+    S.Z[e * LDZ + j] = nr > 0.0 ? S.Z[e * LDZ + j] / nr : 0.0;
+  }
+  __syncthreads();
+  if (a.features)
+    for (int x = tid; x < n * r; x += blockDim.x) {
+      const int i = x / r, j = x % r;
+      a.features[((size_t)l * E + S.mem[i]) * r + j] = (float)S.Z[i * LDZ + j];
+    }
+
+  // 4. Seeds: farthest-first traversal under 1 - cos, from the largest score.
+  if (wave == 0) {
+    const int e = lane;
+    double v = e < n ? S.nrm2[e] : -1.0;
+    int idx = e < n ? e : 1 << 30;
+    wave_argmax(v, idx);
+    int seed = idx;
+    bool mine_chosen = e == seed;
+    auto dist = [&](int s) {
+      double d = 0.0;
+      for (int j = 0; j < r; ++j) d += S.Z[e * LDZ + j] * S.Z[s * LDZ + j];
+      return 1.0 - d;
+    };
+    double md = e < n ? dist(seed) : 0.0;
+    if (e < r) S.C[0 * LDZ + e] = S.Z[seed * LDZ + e];
+    for (int c = 1; c < B; ++c) {
+      double cv = (e < n && !mine_chosen) ? md : -1.0;
+      int ci = (e < n && !mine_chosen) ? e : 1 << 30;
+      wave_argmax(cv, ci);
+      seed = ci;
+      mine_chosen = mine_chosen || e == seed;
+      if (e < n) md = fmin(md, dist(seed));
+      if (e < r) S.C[c * LDZ + e] = S.Z[seed * LDZ + e];
+    }
+  }
+  __syncthreads();
+  if (tid < B) {
+    double s = 0.0;
+    for (int j = 0; j < r; ++j) s += S.C[tid * LDZ + j] * S.C[tid * LDZ + j];
+    S.cn[tid] = sqrt(s);
+  }
+  if (tid < n) S.lab[tid] = -1;
+  __syncthreads();
+
+  // 5. Lloyd passes: thread (e, w) scans centroids w, w + 4, ...
+  int pass = 0;
+  for (;;) {
+    ++pass;
+    {
+      const int e = tid & 63, w = tid >> 6;
+      double bs = -INFINITY;
+      int bj = 1 << 30;
+      if (e < n)
+        for (int c = w; c < B; c += 4) {
+          double d = 0.0;
+          for (int j = 0; j < r; ++j) d += S.Z[e * LDZ + j] * S.C[c * LDZ + j];
+          const double sim = S.cn[c] > 0.0 ? d / S.cn[c] : 0.0;
+          if (sim > bs) {        // c increases: ties keep the lower centroid
+            bs = sim;
+            bj = c;
+          }
+        }
+      S.bsim[w][e] = bs;
+      S.bj[w][e] = bj;
+    }
+    if (tid == 0) S.flag = 0;
+    __syncthreads();
+    if (tid < n) {
+      double bs = S.bsim[0][tid];
+      int bj = S.bj[0][tid];
+      for (int w = 1; w < 4; ++w) {
+        const double v = S.bsim[w][tid];
+        const int j = S.bj[w][tid];
+        if (v > bs || (v == bs && j < bj)) {
+          bs = v;
+          bj = j;
+        }
+      }
+      if (S.lab[tid] != bj) S.flag = 1;
+      S.lab[tid] = bj;
+    }
+    __syncthreads();
+    const bool changed = S.flag != 0;
+    if ((pass > 1 && !changed) || pass >= a.max_iter) break;
+    for (int x = tid; x < B * r; x += blockDim.x) {
+      const int c = x / r, j = x % r;
+      double s = 0.0;
+      int cnt = 0;
+      for (int e = 0; e < n; ++e)
+        if (S.lab[e] == c) {
+          s += S.Z[e * LDZ + j];
+          ++cnt;
+        }
+      if (cnt) S.C[c * LDZ + j] = s / cnt;
+    }
+    __syncthreads();
+    if (tid < B) {
+      double s = 0.0;
+      for (int j = 0; j < r; ++j) s += S.C[tid * LDZ + j] * S.C[tid * LDZ + j];
+      S.cn[tid] = sqrt(s);
+    }
+    __syncthreads();
+  }
+  if (tid < n) a.labels[(size_t)l * E + S.mem[tid]] = S.lab[tid];
+  if (a.iters && tid == 0) a.iters[l] = pass;
+}
+
+size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct ClusterSizes {
+  int NB, NT, cpm, nchunk;
+  size_t g_bytes, part_bytes;
+};
+
+ClusterSizes cluster_sizes(int L, int E, int d, int I) {
+  ClusterSizes z;
+  z.NB = E <= 32 ? 1 : 2;
+  z.NT = z.NB * (z.NB + 1) / 2;
+  const long P = (long)I * d;
+  z.cpm = (int)((P + GR_KC - 1) / GR_KC);
+  z.nchunk = 3 * z.cpm;
+  z.g_bytes = round256((size_t)L * z.NT * 1024 * sizeof(double));
+  z.part_bytes = round256((size_t)L * z.nchunk * z.NT * 1024 * sizeof(float));
+  return z;
+}
+
+}  // namespace
+}  // namespace fm
+
+using namespace fm;
+
+extern "C" int moe_merge_budget(const int32_t* counts, const uint8_t* tuning, int L, int E,
+                                float total_tokens, int B_non, double eps, int32_t* budget,
+                                void* stream) {
+  clear_error();
+  FM_TRY(need(counts, "counts"));
+  FM_TRY(need(tuning, "tuning"));
+  FM_TRY(need(budget, "budget"));
+  if (L < 1 || L > CL_MAXL) return fail(MOE_ERR_UNSUPPORTED, "L=%d: 1..%d layers", L, CL_MAXL);
+  if (E < 1) return fail(MOE_ERR_ARG, "E=%d", E);
+  if (!(total_tokens > 0.f)) return fail(MOE_ERR_ARG, "total_tokens must be positive");
+  if (B_non < 0) return fail(MOE_ERR_ARG, "B_non=%d", B_non);
+  if (!(eps > 0.0)) return fail(MOE_ERR_ARG, "eps must be positive");
+  hipLaunchKernelGGL(k_merge_budget, dim3(1), dim3(256), 0, as_stream(stream), counts, tuning, L, E,
+                     (double)total_tokens, B_non, eps, budget);
+  return check_launch("moe_merge_budget");
+}
+
+extern "C" size_t moe_cluster_workspace_size(int L, int E, int d, int I) {
+  if (L < 1 || E < 1 || E > CL_NMAX || d < 1 || I < 1) return 0;
+  const ClusterSizes z = cluster_sizes(L, E, d, I);
+  return z.g_bytes + z.part_bytes;
+}
+
+extern "C" int moe_cluster_experts(const void* const* w_src, int dtype, int L, int E, int d, int I,
+                                   const uint8_t* tuning, const int32_t* budget, int r,
+                                   int max_iter, void* ws, size_t ws_bytes, int32_t* labels,
+                                   float* features, int32_t* iters, void* stream) {
+  clear_error();
+  FM_TRY(need(w_src, "w_src"));
+  FM_TRY(need(tuning, "tuning"));
+  FM_TRY(need(budget, "budget"));
+  FM_TRY(need(labels, "labels"));
+  FM_TRY(need_dtype_float(dtype, "dtype"));
+  if (!ws) return fail(MOE_ERR_WORKSPACE, "workspace is NULL");
+  FM_TRY(need_aligned(ws, "ws"));
+  if (L < 1 || L > 65535) return fail(MOE_ERR_UNSUPPORTED, "L=%d: 1..65535 layers", L);
+  if (E < 1 || E > CL_NMAX) return fail(MOE_ERR_UNSUPPORTED, "E=%d: at most %d experts per layer", E, CL_NMAX);
+  if (d < 1 || I < 1) return fail(MOE_ERR_ARG, "d=%d I=%d", d, I);
+  if (((size_t)I * d * esize(dtype)) % 16 != 0)
+    return fail(MOE_ERR_UNSUPPORTED, "I*d*element size must be a multiple of 16 bytes");
+  if (r < 1 || r > CL_RMAX) return fail(MOE_ERR_UNSUPPORTED, "r=%d: 1..%d components", r, CL_RMAX);
+  if (max_iter < 1) return fail(MOE_ERR_ARG, "max_iter=%d", max_iter);
+  const ClusterSizes z = cluster_sizes(L, E, d, I);
+  if (ws_bytes < z.g_bytes + z.part_bytes)
+    return fail(MOE_ERR_WORKSPACE, "workspace of %zu bytes < %zu", ws_bytes, z.g_bytes + z.part_bytes);
+  hipStream_t st = as_stream(stream);
+  double* G = (double*)ws;
+  float* part = (float*)((char*)ws + z.g_bytes);
+  GramArgs ga{w_src, tuning, part, (long)I * d, E, z.cpm};
+  const dim3 grid(z.nchunk, L);
+  if (dtype == MOE_BF16) {
+    if (z.NB == 1) hipLaunchKernelGGL((k_gram<bf16, 1>), grid, dim3(256), 0, st, ga);
+    else hipLaunchKernelGGL((k_gram<bf16, 2>), grid, dim3(256), 0, st, ga);
+  } else {
+    if (z.NB == 1) hipLaunchKernelGGL((k_gram<float, 1>), grid, dim3(256), 0, st, ga);
+    else hipLaunchKernelGGL((k_gram<float, 2>), grid, dim3(256), 0, st, ga);
+  }
+  FM_TRY(check_launch("moe_cluster_experts (Gram)"));
+  hipLaunchKernelGGL(k_gram_sum, dim3(cdiv(z.NT * 1024, 256), L), dim3(256), 0, st, part, z.nchunk,
+                     z.NT, G);
+  FM_TRY(check_launch("moe_cluster_experts (Gram sum)"));
+  ClusterArgs ca{G, tuning, budget, labels, features, iters, E, z.NB, r, max_iter};
+  hipLaunchKernelGGL(k_cluster, dim3(L), dim3(256), 0, st, ca);
+  return check_launch("moe_cluster_experts (PCA, K-Means)");
+}

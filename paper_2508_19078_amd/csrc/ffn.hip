@@ -786,8 +786,11 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X
   }
   bool stored = false;   // the previous tile's stores may be in flight
   while (t < qu.total) {
-    int next;   // meaningful in thread 0 only
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Wsometimes-uninitialized"
+    int next;   // meaningful in thread 0 only (no default: it would cost a wait on the atomic)
     if (threadIdx.x == 0) next = qu.draw();
+#pragma clang diagnostic pop
     DwGuTile o;   // tile tables are read through the scalar cache
     o.init(W, X, Xp, dAg, dAu, da, t, MT, NT);
     B16Acc<CB::MI, CB::NJ> acc;
@@ -860,8 +863,11 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
   }
   bool stored = false;
   while (t < qu.total) {
-    int next;   // meaningful in thread 0 only
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Wsometimes-uninitialized"
+    int next;   // meaningful in thread 0 only (no default: it would cost a wait on the atomic)
     if (threadIdx.x == 0) next = qu.draw();
+#pragma clang diagnostic pop
     DwDTile o;
     o.init(W, dO, H, da, t, MT, NT);
     B16Acc<CB::MI, CB::NJ> acc;

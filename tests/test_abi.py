@@ -167,3 +167,41 @@ def test_plan_from_groups_arrays():
     assert list(pa["expert_map"]) == [4, 4, 5, 5, 0, 1, 2, 3]
     assert list(pa["slot_src"]) == [4, 5, 6, 7, 8, 9]
     assert list(pa["grp_ptr"]) == [0, 2, 4] and list(pa["grp_member"]) == [0, 1, 2, 3]
+
+
+def test_merge_budget_and_cluster_rejections(L):
+    dbl = ctypes.c_double
+    rc, msg = rc_and_msg(L, "moe_merge_budget", FAKE, FAKE, 0, 8, ctypes.c_float(10.0), 4, dbl(1e-12), FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED and "L=0" in msg
+    rc, _ = rc_and_msg(L, "moe_merge_budget", FAKE, FAKE, 2000, 8, ctypes.c_float(10.0), 4, dbl(1e-12), FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    rc, msg = rc_and_msg(L, "moe_merge_budget", FAKE, None, 4, 8, ctypes.c_float(10.0), 4, dbl(1e-12), FAKE, None)
+    assert rc == api.MOE_ERR_ARG and "tuning" in msg
+    rc, _ = rc_and_msg(L, "moe_merge_budget", FAKE, FAKE, 4, 8, ctypes.c_float(0.0), 4, dbl(1e-12), FAKE, None)
+    assert rc == api.MOE_ERR_ARG
+    rc, _ = rc_and_msg(L, "moe_merge_budget", FAKE, FAKE, 4, 8, ctypes.c_float(10.0), -1, dbl(1e-12), FAKE, None)
+    assert rc == api.MOE_ERR_ARG
+    rc, _ = rc_and_msg(L, "moe_merge_budget", FAKE, FAKE, 4, 8, ctypes.c_float(10.0), 4, dbl(0.0), FAKE, None)
+    assert rc == api.MOE_ERR_ARG
+
+    need = L.moe_cluster_workspace_size(28, 64, 2048, 1408)
+    # Gram partials of 264 chunks per layer (3 tiles) and the fp64 sums
+    assert need >= 28 * 264 * 3 * 1024 * 4 + 28 * 3 * 1024 * 8
+    assert L.moe_cluster_workspace_size(28, 65, 2048, 1408) == 0
+
+    def call(E=64, d=2048, I=1408, r=16, it=50, ws=FAKE, nbytes=need, dtype=api.MOE_BF16, labels=FAKE):
+        return rc_and_msg(L, "moe_cluster_experts", FAKE, dtype, 28, E, d, I, FAKE, FAKE, r, it, ws,
+                          ctypes.c_size_t(nbytes), labels, None, None, None)
+    rc, msg = call(E=65)
+    assert rc == api.MOE_ERR_UNSUPPORTED and "E=65" in msg
+    assert call(r=0)[0] == api.MOE_ERR_UNSUPPORTED
+    assert call(r=33)[0] == api.MOE_ERR_UNSUPPORTED
+    assert call(it=0)[0] == api.MOE_ERR_ARG
+    assert call(d=3, I=5)[0] == api.MOE_ERR_UNSUPPORTED       # 15 bf16 values: not whole 16-byte chunks
+    assert call(dtype=api.MOE_I8)[0] == api.MOE_ERR_UNSUPPORTED
+    rc, msg = call(nbytes=need - 1)
+    assert rc == api.MOE_ERR_WORKSPACE and "workspace" in msg
+    assert call(ws=None)[0] == api.MOE_ERR_WORKSPACE
+    assert call(ws=MIS)[0] == api.MOE_ERR_ALIGN
+    rc, msg = call(labels=None)
+    assert rc == api.MOE_ERR_ARG and "labels" in msg

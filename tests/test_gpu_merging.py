@@ -1,0 +1,251 @@
+"""GPU parity of layer-aware merging (Section 5): the Eq. 1 budget and the
+fused PCA + K-Means clustering, through the C ABI, against the fp64 oracle.
+
+Budgets are integers decided by fp64 arithmetic on both sides: they must match
+exactly, on inputs whose shares and settlement margins are not within 1e-9 of
+a tie (checked on the oracle's values).  The clustering is compared through
+what is unique: the features' cosine matrix (the sign of a principal
+component is arbitrary) within TOL_COS, and the labels exactly, on experts
+with planted class structure whose leading components are well separated.
+On unstructured experts, where near-degenerate components make the features
+themselves non-unique, the labels are checked for validity instead: in range,
+and a fixed point of the assignment under the GPU's own features."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2508_19078_amd import api
+from paper_2508_19078_amd import workloads as W
+
+from gpu_harness import log
+
+pytestmark = pytest.mark.gpu
+
+TOL_COS = 2e-3      # |cos_gpu - cos_oracle| of feature pairs (fp32 Gram chunks, fp64 after)
+
+
+def tuning_mask(counts, n_tune):
+    """Top n_tune experts by (count desc, index asc) tune."""
+    m = np.zeros(len(counts), dtype=np.uint8)
+    order = sorted(range(len(counts)), key=lambda e: (-int(counts[e]), e))
+    m[order[:n_tune]] = 1
+    return m
+
+
+def budget_margin(share, B):
+    """Distance of the oracle's decisions from a tie: fractional parts from 0
+    and 1, and gaps between distinct deficits share - B."""
+    fr = share - np.floor(share)
+    m = float(np.min(np.minimum(fr, 1 - fr)))
+    d = np.sort(share - B)
+    if len(d) > 1:
+        m = min(m, float(np.min(np.diff(d))))
+    return m
+
+
+def run_budget(counts, tuning, T, B_non, eps=1e-12):
+    dev = torch.device("cuda")
+    c = torch.from_numpy(np.ascontiguousarray(counts, dtype=np.int32)).to(dev)
+    t = torch.from_numpy(np.ascontiguousarray(tuning, dtype=np.uint8)).to(dev)
+    out = torch.full((counts.shape[0],), -7, dtype=torch.int32, device=dev)
+    api.moe_merge_budget(c, t, T, B_non, out, eps=eps)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def stack_counts(w, layers):
+    return np.stack([W.draw_counts(w, l) for l in layers])
+
+
+def test_merge_budget_deepseek_stack():
+    """28 layers of 64 experts, top-16 tuning, 840 non-tuning slots (the
+    number the linear merge schedule keeps), plus tight and loose totals."""
+    w = W.WORKLOADS["deepseek_stack"]
+    counts = stack_counts(w, range(w.n_layers))
+    tuning = np.stack([tuning_mask(c, w.n_tune) for c in counts])
+    compared = 0
+    for B_non in (840, 28, 29, 100, 1343, 1344, 2000, 0):
+        ref, share = O.merge_budget(counts, tuning.astype(bool), w.T, B_non)
+        # B_non = 0: every share is exactly 0 on both sides, no decision is close
+        if B_non > 0 and budget_margin(share, ref) < 1e-9:
+            log(f"budget B_non={B_non}: excluded, oracle decision within 1e-9 of a tie")
+            continue
+        got = run_budget(counts, tuning, w.T, B_non)
+        log(f"budget B_non={B_non}: {got.tolist()}")
+        assert np.array_equal(got, ref), (B_non, got, ref)
+        compared += 1
+    assert compared >= 6
+
+
+def test_merge_budget_edges():
+    rng = np.random.default_rng(11)
+    L, E = 9, 20
+    counts = rng.integers(0, 500, size=(L, E)).astype(np.int32)
+    counts[3] = 25                       # flat layer: variance 0 -> eps floor
+    tuning = (rng.random((L, E)) < 0.25).astype(np.uint8)
+    tuning[5] = 1                        # a layer with no non-tuning expert
+    tuning[6] = 1
+    tuning[6, 7] = 0                     # a layer with one
+    for B_non in (0, 3, 8, 40, 117, 400):
+        ref, share = O.merge_budget(counts, tuning.astype(bool), 1000.0, B_non)
+        got = run_budget(counts, tuning, 1000.0, B_non)
+        assert got[5] == 0 and 0 <= got[6] <= 1
+        assert np.array_equal(got, ref), (B_non, got, ref)
+    # one layer; many layers
+    c1 = counts[:1]
+    assert np.array_equal(run_budget(c1, tuning[:1], 1000.0, 7),
+                          O.merge_budget(c1, tuning[:1].astype(bool), 1000.0, 7)[0])
+    big = rng.integers(0, 50, size=(700, 8)).astype(np.int32)
+    tb = np.zeros((700, 8), dtype=np.uint8)
+    ref, share = O.merge_budget(big, tb.astype(bool), 100.0, 3000)
+    if budget_margin(share, ref) >= 1e-9:
+        assert np.array_equal(run_budget(big, tb, 100.0, 3000), ref)
+
+
+# ---------------------------------------------------------------- clustering --
+
+class Stack:
+    """Expert weights of several layers on the GPU with their pointer table."""
+
+    def __init__(self, w, layers, tuning, n_classes=0, mix=0.0):
+        dev = torch.device("cuda")
+        self.w, self.L, self.E = w, len(layers), w.E
+        self.host = []
+        self.dev = []
+        ptrs = []
+        for li, l in enumerate(layers):
+            if n_classes:
+                mats = W.draw_planted_experts(w, l, n_classes, mix)
+            else:
+                mats = W.draw_experts(w, l)
+            self.host.append(mats)
+            tens = [W.to_torch(m, dev) for m in mats]
+            self.dev.append(tens)
+            esz = tens[0].element_size()
+            for e in range(w.E):
+                for t in tens:
+                    ptrs.append(t.data_ptr() + e * t[0].numel() * esz)
+        self.w_src = torch.tensor(ptrs, dtype=torch.int64, device=dev)
+        self.tuning = np.ascontiguousarray(tuning, dtype=np.uint8)
+        self.dtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+    def run(self, budget, r, max_iter):
+        dev = torch.device("cuda")
+        w = self.w
+        L, E = self.L, self.E
+        ws = torch.empty(api.moe_cluster_workspace_size(L, E, w.d, w.I), dtype=torch.uint8, device=dev)
+        labels = torch.full((L, E), -9, dtype=torch.int32, device=dev)
+        feats = torch.full((L, E, r), 7.0, dtype=torch.float32, device=dev)
+        iters = torch.full((L,), -9, dtype=torch.int32, device=dev)
+        tun = torch.from_numpy(self.tuning).to(dev)
+        bud = torch.from_numpy(np.ascontiguousarray(budget, dtype=np.int32)).to(dev)
+        api.moe_cluster_experts(self.w_src, self.dtype, L, E, w.d, w.I, tun, bud, r, max_iter, ws, labels,
+                                feats, iters)
+        torch.cuda.synchronize()
+        return labels.cpu().numpy(), feats.cpu().numpy(), iters.cpu().numpy()
+
+    def oracle(self, budget, r, max_iter):
+        feats, Bs, mems = [], [], []
+        for li in range(self.L):
+            mem = np.nonzero(self.tuning[li] == 0)[0]
+            if len(mem) == 0:
+                feats.append(np.zeros((0, r)))
+            else:
+                wg, wu, wd = (m.f64() for m in self.host[li])
+                feats.append(O.pca_features(O.expert_vectors(wg[mem], wu[mem], wd[mem]), r))
+            Bs.append(min(max(int(budget[li]), 1), len(mem)) if len(mem) else 0)
+            mems.append(mem)
+        labels, passes = O.fused_kmeans(feats, Bs, max_iter)
+        return feats, labels, passes, mems, Bs
+
+
+def check_clusters(st, budget, r, max_iter, exact=True):
+    got_lab, got_f, got_it = st.run(budget, r, max_iter)
+    feats, labels, passes, mems, Bs = st.oracle(budget, r, max_iter)
+    for li in range(st.L):
+        mem = mems[li]
+        tun = st.tuning[li] != 0
+        assert np.all(got_lab[li][tun] == -1) and np.all(got_f[li][tun] == 0.0)
+        if len(mem) == 0:
+            assert got_it[li] == 0
+            continue
+        gl = got_lab[li][mem]
+        assert np.all((gl >= 0) & (gl < Bs[li])), (li, gl, Bs[li])
+        Zg = got_f[li][mem].astype(np.float64)
+        Zo = O.unit_rows(feats[li])
+        if exact:
+            err = np.max(np.abs(Zg @ Zg.T - Zo @ Zo.T))
+            log(f"layer {li}: n={len(mem)} B={Bs[li]} cos err {err:.2e} passes gpu {got_it[li]} "
+                f"oracle {passes[li]}")
+            assert err <= TOL_COS, (li, err)
+            assert np.array_equal(gl, labels[li]), (li, gl, labels[li])
+            assert got_it[li] == passes[li]
+        else:
+            # validity: unit (or zero) features and a fixed point of the assignment
+            nr = np.linalg.norm(Zg, axis=1)
+            assert np.all((np.abs(nr - 1) < 1e-5) | (nr == 0))
+            assert 1 <= got_it[li] <= max_iter
+            if got_it[li] < max_iter:
+                cents = np.zeros((Bs[li], Zg.shape[1]))
+                for c in np.unique(gl):
+                    cents[c] = Zg[gl == c].mean(0)
+                cn = np.linalg.norm(cents, axis=1)
+                present = np.unique(gl)
+                sims = Zg @ cents[present].T / cn[present]
+                own = sims[np.arange(len(gl)), np.searchsorted(present, gl)]
+                assert np.all(own >= sims.max(1) - 1e-5), li
+    return got_lab, got_it
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_cluster_planted_small(dtype):
+    """Several layers, member counts that fill 1 to 4 row groups of 16, a ragged
+    last slab (I*d = 7200), planted classes with r = classes - 1."""
+    w = W.scaled(W.WORKLOADS["deepseek_stack"], d=72, I=100, E=64, dtype=dtype)
+    K = 6
+    layers = [0, 1, 2, 3, 4]
+    n_tune = [0, 16, 34, 52, 60]            # n = 64, 48, 30, 12, 4
+    tun = []
+    for l, nt in zip(layers, n_tune):
+        tun.append(tuning_mask(W.draw_counts(w, l), nt))
+    st = Stack(w, layers, np.stack(tun), n_classes=K, mix=0.7)
+    budget = [K, K, K, 5, 3]
+    log(f"planted small {dtype}: n_tune {n_tune}")
+    check_clusters(st, budget, K - 1, 50)
+
+
+def test_cluster_planted_sixteen_experts_multi_chunk():
+    """E = 16 (one 32-row block), I*d = 44032 (two chunks per matrix)."""
+    w = W.scaled(W.WORKLOADS["deepseek_stack"], d=128, I=344, E=16)
+    K = 4
+    layers = [0, 1, 2]
+    tun = np.stack([tuning_mask(W.draw_counts(w, l), nt) for l, nt in zip(layers, (0, 4, 9))])
+    st = Stack(w, layers, tun, n_classes=K, mix=0.7)
+    check_clusters(st, [K, K, 3], K - 1, 50)
+
+
+def test_cluster_edges():
+    """Odd member counts, one member, no member, B = n, B = 1, budgets outside
+    [1, n] (clamped), max_iter = 1."""
+    w = W.scaled(W.WORKLOADS["deepseek_stack"], d=64, I=96, E=24)
+    layers = [0, 1, 2, 3, 4, 5]
+    tun = np.zeros((6, 24), dtype=np.uint8)
+    tun[1, :] = 1                 # none
+    tun[2, 1:] = 1                # one
+    tun[3, :7] = 1                # 17 (odd)
+    tun[4, ::2] = 1               # 12
+    st = Stack(w, layers, tun, n_classes=5, mix=0.7)
+    check_clusters(st, [24, 3, 1, 0, 12, 99], 4, 40)
+    check_clusters(st, [5, 3, 1, 5, 5, 5], 4, 1)
+
+
+def test_cluster_unstructured_validity():
+    """Plain random experts: the leading components are near-degenerate, so
+    only validity is checked (labels in range, converged labels a fixed point
+    under the GPU's own features)."""
+    w = W.scaled(W.WORKLOADS["deepseek_stack"], d=64, I=96, E=64)
+    layers = list(range(6))
+    tun = np.stack([tuning_mask(W.draw_counts(w, l), 16) for l in layers])
+    st = Stack(w, layers, tun)
+    check_clusters(st, [30, 20, 10, 5, 2, 1], 16, 100, exact=False)
