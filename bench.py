@@ -35,6 +35,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-sample-tokens", type=int, default=8192)
     p.add_argument("--no-cold", action="store_true", help="skip the cold-cache timing of the HBM-bound calls")
+    p.add_argument("--no-merging", action="store_true", help="skip the layer-aware merging (Section 5) timing")
     p.add_argument("--calib-copy", action="store_true",
                    help="end with a device-to-device copy of 256 MiB (counter calibration)")
     return p.parse_args()
@@ -209,6 +210,77 @@ def cpu_baseline(w, n_tok):
                       f"{dt:.1f} s on the host"}
 
 
+def layer_merging(reps=3, B_non=840, r=16, n_classes=32, mix=0.6, max_iter=100):
+    """Layer-aware merging of Section 5 over the 28-layer DeepSeek-MoE stack
+    (64 experts per layer, d = 2048, I = 1408, top-16 tuning): the Eq. 1 budget
+    and the fused PCA + K-Means clustering of the 48 non-tuning experts of every
+    layer.  Expert weights are drawn on the GPU (torch's seeded generator) with
+    n_classes planted classes per layer, W = sqrt(mix) P_class + sqrt(1 - mix) N;
+    the counts come from the seeded counts generator.  The clustering call's
+    algorithmic bytes are the non-tuning experts' parameters, read once."""
+    import numpy as np
+    import torch
+    from paper_2508_19078_amd import api, workloads as W
+
+    w = W.WORKLOADS["deepseek_stack"]
+    dev = torch.device("cuda")
+    L, E, d, I = w.n_layers, w.E, w.d, w.I
+    g = torch.Generator(device=dev)
+    g.manual_seed(2508190780)
+    mats, ptrs = [], []
+    for l in range(L):
+        cls = torch.randint(0, n_classes, (E,), generator=g, device=dev)
+        layer = []
+        for shape, std in (((I, d), d ** -0.5), ((I, d), d ** -0.5), ((d, I), I ** -0.5)):
+            proto = torch.randn((n_classes,) + shape, generator=g, device=dev)
+            m = torch.randn((E,) + shape, generator=g, device=dev)
+            m.mul_((1 - mix) ** 0.5).add_(proto[cls], alpha=mix ** 0.5).mul_(std)
+            layer.append(m.to(torch.bfloat16))
+            del proto, m
+        mats.append(layer)
+        for e in range(E):
+            for t in layer:
+                ptrs.append(t[e].data_ptr())
+    w_src = torch.tensor(ptrs, dtype=torch.int64, device=dev)
+    counts = np.stack([W.draw_counts(w, l) for l in range(L)])
+    tun = np.zeros((L, E), dtype=np.uint8)
+    for l in range(L):
+        tun[l, sorted(range(E), key=lambda e: (-int(counts[l, e]), e))[:w.n_tune]] = 1
+    counts_d = torch.from_numpy(counts).to(dev)
+    tun_d = torch.from_numpy(tun).to(dev)
+    budget = torch.empty(L, dtype=torch.int32, device=dev)
+    labels = torch.empty((L, E), dtype=torch.int32, device=dev)
+    iters = torch.empty(L, dtype=torch.int32, device=dev)
+    ws = torch.empty(api.moe_cluster_workspace_size(L, E, d, I), dtype=torch.uint8, device=dev)
+    st = torch.cuda.current_stream()
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    tb, tc = [], []
+    for i in range(reps + 1):
+        e0.record(st)
+        api.moe_merge_budget(counts_d, tun_d, w.T, B_non, budget)
+        e1.record(st)
+        api.moe_cluster_experts(w_src, torch.bfloat16, L, E, d, I, tun_d, budget, r, max_iter, ws, labels,
+                                None, iters)
+        e2.record(st)
+        torch.cuda.synchronize()
+        if i:
+            tb.append(e0.elapsed_time(e1))
+            tc.append(e1.elapsed_time(e2))
+    n_non = int((tun == 0).sum())
+    nbytes = n_non * 3 * d * I * 2
+    ms = float(np.median(tc))
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    out = {"workload": f"deepseek_stack: {L} layers x {E} experts, d={d} I={I}, {w.n_tune} tuning per layer, "
+                       f"B_non={B_non}, r={r}, {n_classes} planted classes, mix={mix}",
+           "budget_us": round(float(np.median(tb)) * 1e3, 1),
+           "cluster_ms": round(ms, 4), "bytes": nbytes, "GBps": round(gbs, 1),
+           "frac_hbm": round(gbs / PEAK_HBM_GBS, 3), "groups": int(budget.sum().item()),
+           "kmeans_passes": iters.cpu().tolist()}
+    del mats, w_src, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -312,6 +384,9 @@ def main():
     if not a.no_cold:
         print("# cold-cache timing of the HBM-bound entry points", file=sys.stderr, flush=True)
         out["hbm_cold"] = cold_hbm(r, w, st, N)
+    if not a.no_merging:
+        print("# layer-aware merging over the 28-layer stack", file=sys.stderr, flush=True)
+        out["layer_merging"] = layer_merging()
     if a.calib_copy:
         src = torch.ones(128 << 20, dtype=torch.bfloat16, device="cuda")
         dst = torch.empty_like(src)

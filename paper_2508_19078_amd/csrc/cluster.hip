@@ -28,67 +28,102 @@ constexpr int JAC_SWEEPS = 40;
 
 // ------------------------------------------------------------ Eq. 1 ------
 
-// One block.  Thread l computes layer l's variance and weight; thread 0 sums
-// the weights in layer order and settles the integer budgets serially.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Wave-wide (value desc, index asc) maximum.
+__device__ __forceinline__ void wave_argmax(double& v, int& idx) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const double ov = __shfl_xor(v, o);
+    const int oi = __shfl_xor(idx, o);
+    if (ov > v || (ov == v && oi < idx)) {
+      v = ov;
+      idx = oi;
+    }
+  }
+}
+
+// One block.  Wave w takes layers w, w + 4, ...: mean and variance of the
+// frequencies by wave reductions.  Wave 0 then sums the weights and settles the
+// integer budgets one slot at a time, each step a wave-wide arg-max over the
+// layers (lane i holds layers i, i + 64, ...).
 __global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict__ counts,
                                                       const uint8_t* __restrict__ tuning, int L,
                                                       int E, double total, int B_non, double eps,
                                                       int32_t* __restrict__ budget) {
   __shared__ double sh[CL_MAXL];
   __shared__ int sB[CL_MAXL], sn[CL_MAXL];
-  __shared__ double s_sum;
-  for (int l = threadIdx.x; l < L; l += blockDim.x) {
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
+  for (int l = wave; l < L; l += 4) {
     const int32_t* c = counts + (size_t)l * E;
-    double mean = 0.0;
-    for (int e = 0; e < E; ++e) mean += (double)c[e] / total;
-    mean /= E;
-    double v = 0.0;
+    double s = 0.0;
     int n = 0;
-    for (int e = 0; e < E; ++e) {
-      const double dl = (double)c[e] / total - mean;
-      v += dl * dl;
+    for (int e = lane; e < E; e += 64) {
+      s += (double)c[e] / total;
       n += tuning[(size_t)l * E + e] == 0;
     }
-    v = fmax(v / E, eps);
-    sh[l] = (double)(L - l) / v;       // the paper's (L - l + 1) with l counted from 1
-    sn[l] = n;
+    const double mean = wave_sum(s) / E;
+    double v = 0.0;
+    for (int e = lane; e < E; e += 64) {
+      const double dl = (double)c[e] / total - mean;
+      v += dl * dl;
+    }
+    v = wave_sum(v);
+    n = wave_sum(n);
+    if (lane == 0) {
+      sh[l] = (double)(L - l) / fmax(v / E, eps);   // the paper's (L - l + 1) with l counted from 1
+      sn[l] = n;
+    }
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    double s = 0.0;
-    for (int l = 0; l < L; ++l) s += sh[l];
-    s_sum = s;
-  }
-  __syncthreads();
-  for (int l = threadIdx.x; l < L; l += blockDim.x) {
-    const double share = (double)B_non * sh[l] / s_sum;
+  if (wave != 0) return;
+  double part = 0.0;
+  for (int l = lane; l < L; l += 64) part += sh[l];
+  const double sum = wave_sum(part);
+  long tot = 0;
+  for (int l = lane; l < L; l += 64) {
+    const double share = (double)B_non * sh[l] / sum;
     sh[l] = share;
-    const int lo = min(1, sn[l]);
-    sB[l] = (int)fmin(fmax(floor(share), (double)lo), (double)sn[l]);
+    sB[l] = (int)fmin(fmax(floor(share), (double)min(1, sn[l])), (double)sn[l]);
+    tot += sB[l];
   }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    long tot = 0;
-    for (int l = 0; l < L; ++l) tot += sB[l];
-    while (tot < B_non) {              // short: the largest share - B_l with room
-      int best = -1;
-      for (int l = 0; l < L; ++l)
-        if (sB[l] < sn[l] && (best < 0 || sh[l] - sB[l] > sh[best] - sB[best])) best = l;
-      if (best < 0) break;
-      ++sB[best];
-      ++tot;
-    }
-    while (tot > B_non) {              // over: the smallest share - B_l above its floor
-      int best = -1;
-      for (int l = 0; l < L; ++l)
-        if (sB[l] > min(1, sn[l]) && (best < 0 || sh[l] - sB[l] <= sh[best] - sB[best])) best = l;
-      if (best < 0) break;
-      --sB[best];
-      --tot;
-    }
+  for (int o = 32; o >= 1; o >>= 1) tot += __shfl_xor(tot, o);
+  while (tot < B_non) {            // short: +1 to the largest share - B_l with room (ties: lower layer)
+    double bv = -INFINITY;
+    int bl = 1 << 30;
+    for (int l = lane; l < L; l += 64)
+      if (sB[l] < sn[l] && sh[l] - sB[l] > bv) {
+        bv = sh[l] - sB[l];
+        bl = l;
+      }
+    wave_argmax(bv, bl);
+    if (bl >= L) break;
+    if (lane == 0) ++sB[bl];
+    ++tot;
   }
-  __syncthreads();
-  for (int l = threadIdx.x; l < L; l += blockDim.x) budget[l] = sB[l];
+  while (tot > B_non) {            // over: -1 to the smallest share - B_l above its floor (ties: higher layer)
+    double bv = -INFINITY;
+    int bl = 1 << 30;
+    for (int l = lane; l < L; l += 64)
+      if (sB[l] > min(1, sn[l]) && -(sh[l] - sB[l]) >= bv) {
+        bv = -(sh[l] - sB[l]);
+        bl = -l;
+      }
+    wave_argmax(bv, bl);
+    if (bl > 0) break;
+    if (lane == 0) --sB[-bl];
+    --tot;
+  }
+  for (int l = lane; l < L; l += 64) budget[l] = sB[l];
 }
 
 // -------------------------------------------------------- Gram product ----
@@ -275,8 +310,17 @@ __global__ __launch_bounds__(256) void k_gram_sum(const float* __restrict__ part
   const int l = blockIdx.y, x = blockIdx.x * blockDim.x + threadIdx.x;
   if (x >= NT * 1024) return;
   const float* p = part + (size_t)l * nchunk * NT * 1024 + x;
+  const size_t st = (size_t)NT * 1024;
   double s = 0.0;
-  for (int c = 0; c < nchunk; ++c) s += (double)p[(size_t)c * NT * 1024];
+  int c = 0;
+  for (; c + 16 <= nchunk; c += 16) {      // loads batched, sums kept in chunk order
+    float v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = p[(size_t)(c + u) * st];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) s += (double)v[u];
+  }
+  for (; c < nchunk; ++c) s += (double)p[(size_t)c * st];
   G[(size_t)l * NT * 1024 + x] = s;
 }
 
@@ -291,6 +335,9 @@ struct ClusterLds {
   double Z[CL_NMAX * LDZ];      // unit features
   double C[CL_NMAX * LDZ];      // centroids
   double rc[CL_NMAX / 2], rs[CL_NMAX / 2];
+  int rp[CL_NMAX / 2], rq[CL_NMAX / 2];
+  uint16_t tri[CL_NMAX / 2 * (CL_NMAX / 2 + 1) / 2];   // pair blocks k1 <= k2
+  uint16_t pairs[(CL_NMAX - 1) * (CL_NMAX / 2)];        // round-robin (p << 8 | q) per round
   double rho[CL_NMAX], nrm2[CL_NMAX], mind[CL_NMAX], cn[CL_NMAX];
   double red[2][256];
   double bsim[4][CL_NMAX];
@@ -312,19 +359,6 @@ __device__ __forceinline__ void rr_pair(int round, int k, int m, int& p, int& q)
   }
   p = min(x, y);
   q = max(x, y);
-}
-
-// Wave-wide (value desc, index asc) maximum.
-__device__ __forceinline__ void wave_argmax(double& v, int& idx) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const double ov = __shfl_xor(v, o);
-    const int oi = __shfl_xor(idx, o);
-    if (ov > v || (ov == v && oi < idx)) {
-      v = ov;
-      idx = oi;
-    }
-  }
 }
 
 struct ClusterArgs {
@@ -380,6 +414,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
   __syncthreads();
   if (tid < n) {
     double s = 0.0;
+#pragma unroll 8
     for (int j = 0; j < n; ++j) s += S.A[tid * LDA + j];
     S.rho[tid] = s / n;
   }
@@ -396,31 +431,47 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
   __syncthreads();
 
   // 2. Eigen-decomposition: parallel cyclic Jacobi, A <- J^T A J, V <- V J.
+  // J rotates the m / 2 disjoint pairs of a round at once, so every 2 x 2
+  // block (pair k1 rows, pair k2 columns) of A and every (row, pair) of V is
+  // updated from its own old values: one update phase per round.
+  const int h = m / 2, ntri = h * (h + 1) / 2;
+  if (tid == 0) {
+    int x = 0;
+    for (int k1 = 0; k1 < h; ++k1)
+      for (int k2 = k1; k2 < h; ++k2) S.tri[x++] = (uint16_t)(k1 << 8 | k2);
+  }
+  for (int x = tid; x < (m - 1) * h; x += blockDim.x) {
+    int p, q;
+    rr_pair(x / h, x % h, m, p, q);
+    S.pairs[x] = (uint16_t)(p << 8 | q);
+  }
+  __syncthreads();
   for (int sweep = 0; sweep < JAC_SWEEPS; ++sweep) {
     double off = 0.0, tot = 0.0;
-    for (int x = tid; x < m * m; x += blockDim.x) {
-      const int i = x / m, j = x % m;
-      const double v = S.A[i * LDA + j] * S.A[i * LDA + j];
-      tot += v;
-      if (i != j) off += v;
+    for (int x = tid; x < CL_NMAX * CL_NMAX; x += blockDim.x) {
+      const int i = x >> 6, j = x & 63;
+      if (i < m && j < m) {
+        const double v = S.A[i * LDA + j] * S.A[i * LDA + j];
+        tot += v;
+        if (i != j) off += v;
+      }
     }
     S.red[0][tid] = off;
     S.red[1][tid] = tot;
     __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
-      if (tid < h) {
-        S.red[0][tid] += S.red[0][tid + h];
-        S.red[1][tid] += S.red[1][tid + h];
+    for (int hh = 128; hh > 0; hh >>= 1) {
+      if (tid < hh) {
+        S.red[0][tid] += S.red[0][tid + hh];
+        S.red[1][tid] += S.red[1][tid + hh];
       }
       __syncthreads();
     }
-    const bool done = S.red[0][0] <= 1e-28 * S.red[1][0];
+    const bool done = S.red[0][0] <= 1e-18 * S.red[1][0];
     __syncthreads();
     if (done) break;
     for (int round = 0; round < m - 1; ++round) {
-      if (tid < m / 2) {
-        int p, q;
-        rr_pair(round, tid, m, p, q);
+      if (tid < h) {
+        const int pq = S.pairs[round * h + tid], p = pq >> 8, q = pq & 255;
         const double apq = S.A[p * LDA + q];
         double c = 1.0, s = 0.0;
         if (apq != 0.0) {
@@ -432,29 +483,74 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
         }
         S.rc[tid] = c;
         S.rs[tid] = s;
+        S.rp[tid] = p;
+        S.rq[tid] = q;
       }
       __syncthreads();
-      for (int x = tid; x < (m / 2) * m; x += blockDim.x) {
-        const int k = x / m, j = x % m;
-        int p, q;
-        rr_pair(round, k, m, p, q);
-        const double c = S.rc[k], s = S.rs[k];
-        const double ap = S.A[p * LDA + j], aq = S.A[q * LDA + j];
-        S.A[p * LDA + j] = c * ap - s * aq;
-        S.A[q * LDA + j] = s * ap + c * aq;
-      }
-      __syncthreads();
-      for (int x = tid; x < (m / 2) * m; x += blockDim.x) {
-        const int k = x / m, i = x % m;
-        int p, q;
-        rr_pair(round, k, m, p, q);
-        const double c = S.rc[k], s = S.rs[k];
-        const double ap = S.A[i * LDA + p], aq = S.A[i * LDA + q];
-        S.A[i * LDA + p] = c * ap - s * aq;
-        S.A[i * LDA + q] = s * ap + c * aq;
-        const double vp = S.V[i * LDA + p], vq = S.V[i * LDA + q];
-        S.V[i * LDA + p] = c * vp - s * vq;
-        S.V[i * LDA + q] = s * vp + c * vq;
+      // A is symmetric: blocks k1 <= k2 are computed and stored with their
+      // mirror.  Every item's loads are issued before any store, so that the
+      // stores (which may alias in the compiler's view) do not serialise them.
+      constexpr int NTRI = (CL_NMAX / 2 * (CL_NMAX / 2 + 1) / 2 + 255) / 256;
+      {
+        double va[NTRI][4];
+        int ip[NTRI][4];
+        double rot[NTRI][4];
+#pragma unroll
+        for (int u = 0; u < NTRI; ++u) {
+          const int x = min(tid + 256 * u, ntri - 1);
+          const int k1 = S.tri[x] >> 8, k2 = S.tri[x] & 255;
+          ip[u][0] = S.rp[k1]; ip[u][1] = S.rq[k1]; ip[u][2] = S.rp[k2]; ip[u][3] = S.rq[k2];
+          rot[u][0] = S.rc[k1]; rot[u][1] = S.rs[k1]; rot[u][2] = S.rc[k2]; rot[u][3] = S.rs[k2];
+          va[u][0] = S.A[ip[u][0] * LDA + ip[u][2]];
+          va[u][1] = S.A[ip[u][0] * LDA + ip[u][3]];
+          va[u][2] = S.A[ip[u][1] * LDA + ip[u][2]];
+          va[u][3] = S.A[ip[u][1] * LDA + ip[u][3]];
+        }
+        // V: thread owns pair k = tid % 32 and rows tid / 32 + 8 j
+        const int k = tid & 31;
+        const bool kv = k < h;
+        const int kk = kv ? k : 0;
+        const int vp_ = S.rp[kk], vq_ = S.rq[kk];
+        const double vc = S.rc[kk], vs = S.rs[kk];
+        double vv[CL_NMAX / 8][2];
+#pragma unroll
+        for (int j = 0; j < CL_NMAX / 8; ++j) {
+          const int i = min((tid >> 5) + 8 * j, m - 1);
+          vv[j][0] = S.V[i * LDA + vp_];
+          vv[j][1] = S.V[i * LDA + vq_];
+        }
+#pragma unroll
+        for (int u = 0; u < NTRI; ++u) {
+          if (tid + 256 * u < ntri) {
+            const double c1 = rot[u][0], s1 = rot[u][1], c2 = rot[u][2], s2 = rot[u][3];
+            const double a = va[u][0], b = va[u][1], c = va[u][2], d = va[u][3];
+            const double ra = c1 * a - s1 * c, rb = c1 * b - s1 * d;     // rows (pair k1)
+            const double rc = s1 * a + c1 * c, rd = s1 * b + c1 * d;
+            const double na = c2 * ra - s2 * rb, nb = s2 * ra + c2 * rb;  // columns (pair k2)
+            const double nc = c2 * rc - s2 * rd, nd = s2 * rc + c2 * rd;
+            const int p1 = ip[u][0], q1 = ip[u][1], p2 = ip[u][2], q2 = ip[u][3];
+            S.A[p1 * LDA + p2] = na;
+            S.A[p1 * LDA + q2] = nb;
+            S.A[q1 * LDA + p2] = nc;
+            S.A[q1 * LDA + q2] = nd;
+            if (p1 != p2) {
+              S.A[p2 * LDA + p1] = na;
+              S.A[q2 * LDA + p1] = nb;
+              S.A[p2 * LDA + q1] = nc;
+              S.A[q2 * LDA + q1] = nd;
+            }
+          }
+        }
+        if (kv) {
+#pragma unroll
+          for (int j = 0; j < CL_NMAX / 8; ++j) {
+            const int i = (tid >> 5) + 8 * j;
+            if (i < m) {
+              S.V[i * LDA + vp_] = vc * vv[j][0] - vs * vv[j][1];
+              S.V[i * LDA + vq_] = vs * vv[j][0] + vc * vv[j][1];
+            }
+          }
+        }
       }
       __syncthreads();
     }
@@ -467,6 +563,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
   if (tid < n) {
     const double li = S.A[tid * LDA + tid];
     int rank = 0;
+#pragma unroll 8
     for (int q = 0; q < n; ++q) {
       const double lq = S.A[q * LDA + q];
       rank += (lq > li) || (lq == li && q < tid);
@@ -481,6 +578,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
   __syncthreads();
   if (tid < n) {
     double s = 0.0;
+#pragma unroll 8
     for (int j = 0; j < r; ++j) s += S.Z[tid * LDZ + j] * S.Z[tid * LDZ + j];
     S.nrm2[tid] = s;
   }
@@ -507,6 +605,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
     bool mine_chosen = e == seed;
     auto dist = [&](int s) {
       double d = 0.0;
+#pragma unroll 8
       for (int j = 0; j < r; ++j) d += S.Z[e * LDZ + j] * S.Z[s * LDZ + j];
       return 1.0 - d;
     };
@@ -525,6 +624,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
   __syncthreads();
   if (tid < B) {
     double s = 0.0;
+#pragma unroll 8
     for (int j = 0; j < r; ++j) s += S.C[tid * LDZ + j] * S.C[tid * LDZ + j];
     S.cn[tid] = sqrt(s);
   }
@@ -542,6 +642,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
       if (e < n)
         for (int c = w; c < B; c += 4) {
           double d = 0.0;
+#pragma unroll 8
           for (int j = 0; j < r; ++j) d += S.Z[e * LDZ + j] * S.C[c * LDZ + j];
           const double sim = S.cn[c] > 0.0 ? d / S.cn[c] : 0.0;
           if (sim > bs) {        // c increases: ties keep the lower centroid
@@ -575,6 +676,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
       const int c = x / r, j = x % r;
       double s = 0.0;
       int cnt = 0;
+#pragma unroll 8
       for (int e = 0; e < n; ++e)
         if (S.lab[e] == c) {
           s += S.Z[e * LDZ + j];
@@ -585,6 +687,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
     __syncthreads();
     if (tid < B) {
       double s = 0.0;
+#pragma unroll 8
       for (int j = 0; j < r; ++j) s += S.C[tid * LDZ + j] * S.C[tid * LDZ + j];
       S.cn[tid] = sqrt(s);
     }

@@ -249,3 +249,27 @@ def test_cluster_unstructured_validity():
     tun = np.stack([tuning_mask(W.draw_counts(w, l), 16) for l in layers])
     st = Stack(w, layers, tun)
     check_clusters(st, [30, 20, 10, 5, 2, 1], 16, 100, exact=False)
+
+
+def test_cluster_full_size_layers():
+    """Two layers at the DeepSeek-MoE stack shape (64 experts, d = 2048,
+    I = 1408, top-16 tuning, so 48 clustered experts and 264 Gram chunks per
+    layer), the launch configuration the benchmark times on 28 layers.  Planted
+    classes: exact cosine matrix and labels with budget = classes present and
+    r = classes - 1; then the layers' Eq. 1 budgets (840 slots over 28
+    layers) with r = 16, checked for validity."""
+    w = W.WORKLOADS["deepseek_stack"]
+    K = 8
+    layers = [0, 27]
+    counts_all = stack_counts(w, range(w.n_layers))
+    tun_all = np.stack([tuning_mask(c, w.n_tune) for c in counts_all])
+    tun = tun_all[layers]
+    log("full size: drawing 2 layers of planted experts")
+    st = Stack(w, layers, tun, n_classes=K, mix=0.6)
+    present = [len(set(W.expert_classes(w, l, K)[tun[i] == 0].tolist())) for i, l in enumerate(layers)]
+    assert present == [K, K], present
+    log("full size: exact check")
+    check_clusters(st, [K, K], K - 1, 100)
+    B, _ = O.merge_budget(counts_all, tun_all.astype(bool), w.T, 840)
+    log(f"full size: Eq. 1 budgets {B[layers].tolist()}")
+    check_clusters(st, B[layers], 16, 100, exact=False)
