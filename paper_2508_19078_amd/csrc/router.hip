@@ -5,12 +5,13 @@
 // router: a block owns 32 tokens, its waves split the hidden dimension into
 // interleaved 16-byte-per-lane chunks and accumulate the token x expert
 // logits on MFMA (16x16x32 bf16, or 16x16x4 fp32 for fp32 inputs).  The
-// sixteen partial sums are added in a fixed order in LDS (four groups of four,
+// waves' partial sums are added in a fixed order in LDS (four groups of four,
 // then the groups), so the logits do not depend on scheduling.  Then 16 lanes per token select the top k by
 // (logit desc, index asc) with branch-free 64-bit key reductions, and either
 // write idx/gate or add the selection to an LDS histogram that is flushed to
 // the global counts with one integer atomic per expert and block.
 #include "common.hpp"
+#include "gemm_bf16.hpp"
 
 namespace fm {
 namespace {
@@ -102,6 +103,119 @@ __device__ __forceinline__ f32x4_t mma(f32x4_t a, f32x4_t b, f32x4_t c) {
   return c;
 }
 
+// Top-k selection and outputs for the block's RT_TOK tokens starting at t0,
+// WAVES waves.  The logit of (token tl, expert e) is the sum, in order, of
+// NPART partials part[p * PSTRIDE + tl * EP + e], times scale[e] and plus
+// bias[e] when those are given (LDS arrays); with logits != nullptr (MODE 0)
+// the logits are also written out.
+//
+// 16 lanes per token: lane gl of the group holds experts gl, gl+16, ...  Keys
+// order (value desc, index asc): the high word maps the fp32 value
+// monotonically to uint32 (-0.0 == +0.0), the low word is 0xFFFF - expert.
+// Each of the k selection rounds takes the group maximum with four DPP row
+// rotations; the owner lane then drops it.  A group handles TPL tokens at once
+// (independent chains for the scheduler to interleave).
+template <int NE, int KMAX, int MODE, int WAVES, int NPART>
+__device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int EP, const float* scale,
+                                             const float* bias, int t0, int T, int E, int k,
+                                             int32_t* __restrict__ idx, float* __restrict__ gate,
+                                             float* __restrict__ logits, int32_t* __restrict__ counts,
+                                             int* hist) {
+  constexpr int TPL = (RT_TOK + WAVES * 4 - 1) / (WAVES * 4);
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int grp = lane >> 4, gl = lane & 15;
+  uint32_t khi[TPL][NE], klo[TPL][NE];
+  int tl[TPL];
+#pragma unroll
+  for (int u = 0; u < TPL; ++u) {
+    tl[u] = u * WAVES * 4 + wave * 4 + grp;
+    const bool on = tl[u] < RT_TOK;
+    const int tc = on ? tl[u] : 0;
+#pragma unroll
+    for (int i = 0; i < NE; ++i) {
+      const int e = gl + 16 * i;
+      float v = 0.f;
+      if (e < E) {
+        v = part[tc * EP + e];
+#pragma unroll
+        for (int p = 1; p < NPART; ++p) v += part[p * PSTRIDE + tc * EP + e];
+        if (scale) v *= scale[e];
+        if (bias) v += bias[e];
+        if (MODE == 0 && logits && on && t0 + tc < T) logits[(size_t)(t0 + tc) * E + e] = v;
+      }
+      v += 0.0f;
+      khi[u][i] = (on && e < E) ? ordered_key(v) : 0u;
+      klo[u][i] = (on && e < E) ? 0xFFFFu - (uint32_t)e : 0u;
+    }
+  }
+  float myv[TPL], v0[TPL];
+  int mye[TPL];
+#pragma unroll
+  for (int u = 0; u < TPL; ++u) {
+    myv[u] = 0.f;
+    v0[u] = 0.f;
+    mye[u] = 0;
+  }
+#pragma unroll
+  for (int j = 0; j < KMAX; ++j) {
+    if (j < k) {
+#pragma unroll
+      for (int u = 0; u < TPL; ++u) {
+        uint32_t bh = khi[u][0], bl = klo[u][0];
+#pragma unroll
+        for (int i = 1; i < NE; ++i) {
+          const bool tk = khi[u][i] > bh || (khi[u][i] == bh && klo[u][i] > bl);
+          bh = tk ? khi[u][i] : bh;
+          bl = tk ? klo[u][i] : bl;
+        }
+        key_max_row<8>(bh, bl);
+        key_max_row<4>(bh, bl);
+        key_max_row<2>(bh, bl);
+        key_max_row<1>(bh, bl);
+        const int e = 0xFFFF - (int)bl;
+        const float v = key_value(bh);
+        if (j == 0) v0[u] = v;
+        if (gl == j) {
+          myv[u] = v;
+          mye[u] = e;
+        }
+#pragma unroll
+        for (int i = 0; i < NE; ++i)
+          if (gl + 16 * i == e) {
+            khi[u][i] = 0u;
+            klo[u][i] = 0u;
+          }
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < TPL; ++u) {
+    const int t = t0 + tl[u];
+    const bool mine = gl < k && tl[u] < RT_TOK && t < T;
+    if (MODE == 0) {
+      float g = gl < k ? expf(myv[u] - v0[u]) : 0.f;
+      float sum = g;
+      sum += row_ror<8>(sum);
+      sum += row_ror<4>(sum);
+      sum += row_ror<2>(sum);
+      sum += row_ror<1>(sum);
+      if (mine) {
+        idx[(size_t)t * k + gl] = mye[u];
+        gate[(size_t)t * k + gl] = g / sum;
+      }
+    } else if (mine) {
+      atomicAdd(&hist[mye[u]], 1);
+      if (idx) idx[(size_t)t * k + gl] = mye[u];
+    }
+  }
+  if (MODE == 1) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x)
+      if (hist[e]) atomicAdd(&counts[e], hist[e]);
+  }
+}
+
 // MODE 0: write idx/gate (+logits).  MODE 1: histogram (+idx).
 template <typename TX, typename TW, int NE, int KMAX, int MODE>
 __global__ __launch_bounds__(RtShape<NE>::WAVES * 64) void k_route(
@@ -142,46 +256,62 @@ __global__ __launch_bounds__(RtShape<NE>::WAVES * 64) void k_route(
 #pragma unroll
   for (int j = 0; j < NE; ++j) wrow[j] = W + (size_t)min(j * 16 + r16, E - 1) * d;
 
-  // This wave's chunks are wave, wave + RT_WAVES, ...; P of them are in flight.
-  constexpr int P = RtShape<NE>::P;
-  const int nw = nchunks > wave ? (nchunks - wave + RT_WAVES - 1) / RT_WAVES : 0;
-  frag_t ra[P][2], rb[P][NE];
+  // Chunks go in pairs: chunks 2u and 2u + 1 are the two 64-byte halves of
+  // the same 128-byte lines of every row, and their loads are issued back to
+  // back (the CU moves about twice the bytes per clock from L2 that way).
+  // This wave's pairs are wave, wave + RT_WAVES, ...; PU of them in flight.
+  constexpr int PU = RtShape<NE>::P > 1 ? RtShape<NE>::P / 2 : 1;
+  const int npairs = nchunks / 2;
+  const int nw = npairs > wave ? (npairs - wave + RT_WAVES - 1) / RT_WAVES : 0;
+  frag_t ra[PU][2][2], rb[PU][2][NE];
   auto issue = [&](int u, int i) {
-    const int ci = min(i, nw - 1);
-    const int col = (wave + RT_WAVES * ci) * KC + q4 * V;
+    const int pi = min(i, nw - 1);
+    const int col = (wave + RT_WAVES * pi) * 2 * KC + q4 * V;
 #pragma unroll
-    for (int r = 0; r < 2; ++r) ra[u][r] = load_x_frag(xrow[r] + col, true);
+    for (int r = 0; r < 2; ++r) {
+      ra[u][0][r] = load_x_frag(xrow[r] + col, true);
+      ra[u][1][r] = load_x_frag(xrow[r] + col + KC, true);
+    }
 #pragma unroll
-    for (int j = 0; j < NE; ++j) rb[u][j] = load_w_frag(wrow[j] + col, true, frag_t{});
+    for (int j = 0; j < NE; ++j) {
+      rb[u][0][j] = load_w_frag(wrow[j] + col, true, frag_t{});
+      rb[u][1][j] = load_w_frag(wrow[j] + col + KC, true, frag_t{});
+    }
   };
   if (nw > 0) {
 #pragma unroll
-    for (int u = 0; u < P; ++u) issue(u, u);
-    for (int i0 = 0; i0 < nw; i0 += P) {
+    for (int u = 0; u < PU; ++u) issue(u, u);
+    for (int i0 = 0; i0 < nw; i0 += PU) {
 #pragma unroll
-      for (int u = 0; u < P; ++u) {
+      for (int u = 0; u < PU; ++u) {
         if (i0 + u < nw) {
 #pragma unroll
-          for (int r = 0; r < 2; ++r)
+          for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int j = 0; j < NE; ++j) acc[r][j] = mma(ra[u][r], rb[u][j], acc[r][j]);
+            for (int r = 0; r < 2; ++r)
+#pragma unroll
+              for (int j = 0; j < NE; ++j) acc[r][j] = mma(ra[u][h][r], rb[u][h][j], acc[r][j]);
         }
-        issue(u, i0 + u + P);
+        issue(u, i0 + u + PU);
       }
     }
   }
-  if (tail > 0 && wave == nchunks % RT_WAVES) {   // zero-filled last partial chunk
-    const int col = nchunks * KC + q4 * V;
-    const bool cok = col < d;
-    frag_t a[2], b[NE];
+  // An odd last whole chunk and the zero-filled partial chunk, if any, go to
+  // the wave next in the round-robin.
+  if (wave == npairs % RT_WAVES) {
+    for (int c = 2 * npairs; c < nchunks + (tail > 0); ++c) {
+      const int col = c * KC + q4 * V;
+      const bool cok = col < d;
+      frag_t a[2], b[NE];
 #pragma unroll
-    for (int r = 0; r < 2; ++r) a[r] = load_x_frag(xrow[r] + col, cok);
+      for (int r = 0; r < 2; ++r) a[r] = load_x_frag(xrow[r] + col, cok);
 #pragma unroll
-    for (int j = 0; j < NE; ++j) b[j] = load_w_frag(wrow[j] + col, cok, frag_t{});
+      for (int j = 0; j < NE; ++j) b[j] = load_w_frag(wrow[j] + col, cok, frag_t{});
 #pragma unroll
-    for (int r = 0; r < 2; ++r)
+      for (int r = 0; r < 2; ++r)
 #pragma unroll
-      for (int j = 0; j < NE; ++j) acc[r][j] = mma(a[r], b[j], acc[r][j]);
+        for (int j = 0; j < NE; ++j) acc[r][j] = mma(a[r], b[j], acc[r][j]);
+    }
   }
 
   // Fixed-order reduction of the partial sums: group g adds waves
@@ -217,74 +347,161 @@ __global__ __launch_bounds__(RtShape<NE>::WAVES * 64) void k_route(
   }
   __syncthreads();
 
-  // Top-k: 16 lanes per token, 4 tokens per wave and round.  Lane gl of the
-  // group holds experts gl, gl+16, ...  Keys order (value desc, index asc): the
-  // high word maps the fp32 value monotonically to uint32 (-0.0 == +0.0), the
-  // low word is 0xFFFF - expert.  Each of the k selection rounds takes the
-  // group maximum with four DPP row rotations; the owner lane then drops it.
-  // groups of 16 lanes, one token each: RT_WAVES * 4 tokens per round
-  const int grp = lane >> 4, gl = lane & 15;
-  constexpr int ROUNDS = (RT_TOK + RT_WAVES * 4 - 1) / (RT_WAVES * 4);
+  route_select<NE, KMAX, MODE, RT_WAVES, 1>(red[0], 0, EP, nullptr, nullptr, t0, T, E, k, idx, gate, nullptr,
+                                           counts, hist);
+}
+
+// The same router for bf16 activations with E <= 64 and d a multiple of 256,
+// with its operands staged through LDS: every block needs all of W for its 32
+// tokens, which makes the per-CU load path (not HBM) the limit of the
+// register-fed kernel above.  Slabs of 256 columns of the block's 32 X rows
+// and of W's rows move global -> LDS with global_load_lds_dwordx4, each
+// instruction 64 bytes of 16 rows and the same wave's next one the other
+// halves of those lines (the pairing that doubles the CU's L2 -> LDS rate),
+// chunk index XOR-swizzled by (row >> 2) & 3; a ring of three slabs, two in
+// flight.  Wave w multiplies columns [64 w, 64 w + 64) of each slab with
+// v_mfma_f32_32x32x16_bf16 (int8 W widened exactly to bf16 on the way in);
+// the four partial sums are added in wave order.
+template <typename TW> struct RtLds;
+template <> struct RtLds<bf16> {
+  static constexpr int WB = 512;                     // bytes of a W row per slab
+  static __device__ __forceinline__ bf16x8_t frag(const FM_LDS char* blk, int rr, int w, int cc) {
+    // line w, chunk cc of the row
+    const int h = cc >> 2, q = cc & 3;
+    return *(const FM_LDS bf16x8_t*)(blk + ((w * 2 + h) * 1024) + rr * 64 + ((q ^ ((rr >> 2) & 3)) << 4));
+  }
+};
+template <> struct RtLds<int8_t> {
+  static constexpr int WB = 256;
+  static __device__ __forceinline__ bf16x8_t frag(const FM_LDS char* blk, int rr, int w, int cc) {
+    // columns 64 w + 8 cc .. +8 are bytes 64 w + 8 cc of the 256-byte row:
+    // line w / 2, half w % 2, 16-byte chunk cc / 2, 8 bytes at (cc % 2) * 8
+    const int q = cc >> 1;
+    const u32x2_t raw = *(const FM_LDS u32x2_t*)(blk + (((w >> 1) * 2 + (w & 1)) * 1024) + rr * 64 +
+                                                 ((q ^ ((rr >> 2) & 3)) << 4) + (cc & 1) * 8);
+    u32x4_t v;
 #pragma unroll
-  for (int round = 0; round < ROUNDS; ++round) {
-    const int tl = round * RT_WAVES * 4 + wave * 4 + grp;
-    if (tl >= RT_TOK) continue;
-    const int t = t0 + tl;
-    uint32_t khi[NE], klo[NE];
-#pragma unroll
-    for (int i = 0; i < NE; ++i) {
-      const int e = gl + 16 * i;
-      const float v = red[0][tl * EP + e] + 0.0f;
-      khi[i] = e < E ? ordered_key(v) : 0u;
-      klo[i] = e < E ? 0xFFFFu - (uint32_t)e : 0u;
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t x = raw[i >> 1];
+      const int sh = (i & 1) * 16;
+      const float lo = (float)(int8_t)((x >> sh) & 0xFF);
+      const float hi = (float)(int8_t)((x >> (sh + 8)) & 0xFF);
+      v[i] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
     }
-    float myv = 0.f, v0 = 0.f;
-    int mye = 0;
+    return __builtin_bit_cast(bf16x8_t, v);
+  }
+};
+
+constexpr int RL_COLS = 256, RL_XB = 512, RL_NS = 3;
+
+template <typename TW, int NB, int KMAX, int MODE>
+__global__ __launch_bounds__(256) void k_route_lds(const bf16* __restrict__ X, const TW* __restrict__ W,
+                                                   const float* __restrict__ wscale, const float* __restrict__ bias,
+                                                   int T, int d, int E, int k, int32_t* __restrict__ idx,
+                                                   float* __restrict__ gate, float* __restrict__ logits,
+                                                   int32_t* __restrict__ counts) {
+  constexpr int WB = RtLds<TW>::WB;
+  constexpr int WLINES = WB / 128;                   // 128-byte lines of a W row per slab
+  constexpr int XBYTES = RT_TOK * RL_XB;             // 16 KB
+  constexpr int SLAB = XBYTES + NB * 32 * WB;
+  constexpr int NIX = 2 * 4 * 2;                     // X: 2 row groups x 4 lines x 2 halves
+  constexpr int NIW = 2 * NB * WLINES * 2;           // W: 2 NB row groups x lines x 2 halves
+  constexpr int INS = (NIX + NIW) / 4;               // DMA instructions per wave and slab
+  static_assert((NIX + NIW) % 4 == 0, "whole instructions per wave");
+  constexpr int EP = NB * 32 + 1;
+  static_assert(RL_NS * SLAB <= 160 * 1024 && 4 * RT_TOK * EP * 4 <= RL_NS * SLAB, "LDS");
+  __shared__ __align__(1024) char lds_raw[RL_NS * SLAB];
+  __shared__ int hist[NB * 32];
+  __shared__ float s_scale[NB * 32], s_bias[NB * 32];
+  FM_LDS char* lds = (FM_LDS char*)lds_raw;
+  const int lane = lane_id_here(), wave = wave_id();
+  const int t0 = blockIdx.x * RT_TOK;
+  if (MODE == 1)
+    for (int e = threadIdx.x; e < NB * 32; e += blockDim.x) hist[e] = 0;
+  // the epilogue's per-expert scale and bias, fetched while the slabs stream
+  if (threadIdx.x < E) {
+    s_scale[threadIdx.x] = wscale ? wscale[threadIdx.x] : 1.f;
+    s_bias[threadIdx.x] = bias ? bias[threadIdx.x] : 0.f;
+  }
+
+  // DMA plan: instruction u = wave * INS + q; X instructions first.
+  const char* gp[INS];
+  uint32_t dst[INS];
 #pragma unroll
-    for (int j = 0; j < KMAX; ++j) {
-      if (j < k) {
-        uint32_t bh = khi[0], bl = klo[0];
-#pragma unroll
-        for (int i = 1; i < NE; ++i) {
-          const bool tk = khi[i] > bh || (khi[i] == bh && klo[i] > bl);
-          bh = tk ? khi[i] : bh;
-          bl = tk ? klo[i] : bl;
-        }
-        key_max_row<8>(bh, bl);
-        key_max_row<4>(bh, bl);
-        key_max_row<2>(bh, bl);
-        key_max_row<1>(bh, bl);
-        const int e = 0xFFFF - (int)bl;
-        const float v = key_value(bh);
-        if (j == 0) v0 = v;
-        if (gl == j) { myv = v; mye = e; }
-#pragma unroll
-        for (int i = 0; i < NE; ++i)
-          if (gl + 16 * i == e) { khi[i] = 0u; klo[i] = 0u; }
-      }
-    }
-    const bool mine = gl < k && t < T;
-    if (MODE == 0) {
-      float g = gl < k ? expf(myv - v0) : 0.f;
-      float sum = g;
-      sum += row_ror<8>(sum);
-      sum += row_ror<4>(sum);
-      sum += row_ror<2>(sum);
-      sum += row_ror<1>(sum);
-      if (mine) {
-        idx[(size_t)t * k + gl] = mye;
-        gate[(size_t)t * k + gl] = g / sum;
-      }
-    } else if (mine) {
-      atomicAdd(&hist[mye], 1);
-      if (idx) idx[(size_t)t * k + gl] = mye;
+  for (int q = 0; q < INS; ++q) {
+    const int u = wave * INS + q;
+    const int rr = lane >> 2;
+    if (u < NIX) {
+      const int g = u >> 3, m = (u >> 1) & 3, h = u & 1;
+      const int row = min(t0 + g * 16 + rr, T - 1);
+      gp[q] = (const char*)(X + (size_t)row * d) + m * 128 + h * 64 + (((lane & 3) ^ ((rr >> 2) & 3)) << 4);
+      dst[q] = (uint32_t)(((g * 4 + m) * 2 + h) * 1024);
+    } else {
+      const int v = u - NIX, g = v / (WLINES * 2), m = (v >> 1) % WLINES, h = v & 1;
+      const int row = min(g * 16 + rr, E - 1);
+      gp[q] = (const char*)(W + (size_t)row * d) + m * 128 + h * 64 + (((lane & 3) ^ ((rr >> 2) & 3)) << 4);
+      dst[q] = (uint32_t)(XBYTES + ((g * WLINES + m) * 2 + h) * 1024);
     }
   }
-  if (MODE == 1) {
-    __syncthreads();
-    for (int e = threadIdx.x; e < E; e += blockDim.x)
-      if (hist[e]) atomicAdd(&counts[e], hist[e]);
+  const int nslab = d / RL_COLS;
+  // Blocks start at different slabs (their rank within the XCD), so that the
+  // CUs sharing an L2 do not all ask for the same lines of W at once.
+  const int s_off = (int)(blockIdx.x >> 3) % nslab;
+  auto issue = [&](int s) {
+    FM_LDS char* slab = lds + (s % RL_NS) * SLAB;
+    int sg = s + s_off;
+    sg -= sg >= nslab ? nslab : 0;
+#pragma unroll
+    for (int q = 0; q < INS; ++q) {
+      const bool isx = wave * INS + q < NIX;
+      dma16(gp[q] + (size_t)sg * (isx ? RL_XB : WB), slab + dst[q]);
+    }
+  };
+  f32x16_t acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[b][r] = 0.f;
+
+  const int pre = min(RL_NS - 1, nslab);
+  for (int s = 0; s < pre; ++s) issue(s);
+  const int i = lane & 31, hf = lane >> 5;
+  for (int s = 0; s < nslab; ++s) {
+    if (s + 1 < nslab) wait_vmcnt<INS>();
+    else wait_vmcnt<0>();
+    barrier_lds();
+    if (s + RL_NS - 1 < nslab) issue(s + RL_NS - 1);
+    const FM_LDS char* slab = lds + (s % RL_NS) * SLAB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int cc = 2 * j + hf;
+      // X row i: group i >> 4, row i & 15 of that group's blocks
+      const bf16x8_t xa = RtLds<bf16>::frag(slab + (i >> 4) * 8 * 1024, i & 15, wave, cc);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int R = 32 * b + i;
+        const bf16x8_t wb = RtLds<TW>::frag(slab + XBYTES + (R >> 4) * WLINES * 2 * 1024, R & 15, wave, cc);
+        acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa, wb, acc[b], 0, 0, 0);
+      }
+    }
   }
+  __syncthreads();
+
+  // partial sums of the four waves, added in wave order; then scale and bias.
+  // Register r of lane L holds token 8 (r / 4) + 4 (L / 32) + r % 4, expert 32 b + L % 32.
+  float* red = (float*)lds_raw;                      // [wave][token][EP]
+  {
+    const int L = lane_id();
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[(wave * RT_TOK + 8 * (r >> 2) + 4 * (L >> 5) + (r & 3)) * EP + 32 * b + (L & 31)] = acc[b][r];
+  }
+  __syncthreads();
+  route_select<(NB * 32 + 15) / 16, KMAX, MODE, 4, 4>(red, RT_TOK * EP, EP, wscale ? s_scale : nullptr,
+                                                     bias ? s_bias : nullptr, t0, T, E, k, idx, gate, logits,
+                                                     counts, hist);
 }
 
 // Per-row symmetric int8 quantiser: one wave per row, 16-byte loads.
@@ -331,6 +548,23 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
                  int E, int k, int32_t* idx, float* gate, float* logits, int32_t* counts,
                  hipStream_t st) {
   dim3 grid(cdiv(T, RT_TOK));
+  if constexpr (std::is_same<TX, bf16>::value) {
+    if (E <= 64 && d % RL_COLS == 0) {
+#define FM_RL(NB, KM)                                                                          \
+  hipLaunchKernelGGL((k_route_lds<TW, NB, KM, MODE>), grid, dim3(256), 0, st, X, W, ws, bias, T, d, E, k, \
+                     idx, gate, logits, counts)
+#define FM_RL_K(NB)              \
+  if (k <= 2) FM_RL(NB, 2);      \
+  else if (k <= 4) FM_RL(NB, 4); \
+  else if (k <= 8) FM_RL(NB, 8); \
+  else FM_RL(NB, 16);
+      if (E <= 32) { FM_RL_K(1) }
+      else { FM_RL_K(2) }
+#undef FM_RL_K
+#undef FM_RL
+      return check_launch(MODE == 0 ? "moe_route_topk" : "moe_profile_hist");
+    }
+  }
   const int ne = cdiv(E, 16);
 #define FM_RT(NE, KM)                                                                          \
   hipLaunchKernelGGL((k_route<TX, TW, NE, KM, MODE>), grid, dim3(RtShape<NE>::WAVES * 64), 0, st, X, W, \
