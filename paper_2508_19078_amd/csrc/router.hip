@@ -2,14 +2,16 @@
 // histogram of the int8 profiling router.
 //
 // One kernel serves both the full-precision router and the int8 profiling
-// router: a block owns 32 tokens, its waves split the hidden dimension into
-// interleaved 16-byte-per-lane chunks and accumulate the token x expert
-// logits on MFMA (16x16x32 bf16, or 16x16x4 fp32 for fp32 inputs).  The
-// waves' partial sums are added in a fixed order in LDS (four groups of four,
-// then the groups), so the logits do not depend on scheduling.  Then 16 lanes per token select the top k by
-// (logit desc, index asc) with branch-free 64-bit key reductions, and either
-// write idx/gate or add the selection to an LDS histogram that is flushed to
-// the global counts with one integer atomic per expert and block.
+// router: a block owns 32 tokens and accumulates the token x expert logits on
+// MFMA.  For bf16 activations with at most 64 experts and d a multiple of 256
+// (every bf16 workload here) the operands stream through an LDS ring
+// (k_route_lds); otherwise (fp32, wider routers) the waves split the hidden
+// dimension into 16-byte-per-lane register chunks (k_route).  The waves'
+// partial sums are added in a fixed order, so the logits do not depend on
+// scheduling.  Then 16 lanes per token select the top k by (logit desc, index
+// asc) with branch-free 64-bit key reductions, and either write idx/gate or
+// add the selection to an LDS histogram that is flushed to the global counts
+// with one integer atomic per expert and block.
 #include "common.hpp"
 #include "gemm_bf16.hpp"
 
