@@ -49,8 +49,10 @@ def base_name(n: str) -> str:
 
 def stats_table(path: str, top: int) -> str:
     rows = list(csv.DictReader(open(path)))
-    out = ["| kernel | calls | avg µs | total ms | % |", "|---|---|---|---|---|"]
-    for r in rows[:top]:
+    # PyTorch's own kernels (input generation, fills) are left out of the table
+    lib = [r for r in rows if not short_name(r["Name"]).startswith("at::")]
+    out = ["| kernel | calls | avg µs | total ms | % of all GPU time |", "|---|---|---|---|---|"]
+    for r in lib[:top]:
         out.append(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                    f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['Percentage']):.1f} |")
     ffn = [r for r in rows if base_name(r["Name"]) in FFN_KERNELS]
@@ -86,7 +88,10 @@ def traffic(fetch_csv: str, write_csv: str, calib_bytes: int):
         raw = sum(sum(per.get(k, [])) for k in FFN_KERNELS) / max(steps, 1)
         res[name] = {"calib_kib": kib, "factor": factor, "steps": steps, "kib_per_step": raw,
                      "bytes_per_step": raw * 1024.0 * factor,
-                     "per_kernel_kib": {k: sum(per.get(k, [])) / max(steps, 1) for k in FFN_KERNELS}}
+                     "per_kernel_kib": {k: sum(per.get(k, [])) / max(steps, 1) for k in FFN_KERNELS},
+                     # the library's other kernels: scaled bytes per dispatch (mean)
+                     "other_bytes": {k: sum(vs) / len(vs) * 1024.0 * factor for k, vs in per.items()
+                                     if k.startswith("k_") and k not in FFN_KERNELS}}
     return res
 
 
@@ -118,6 +123,13 @@ def main():
     print("|---|---|---|")
     for k in FFN_KERNELS:
         print(f"| {k} | {f['per_kernel_kib'][k]:.0f} | {w['per_kernel_kib'][k]:.0f} |")
+    others = sorted(set(f["other_bytes"]) | set(w["other_bytes"]))
+    if others:
+        print("\nOther kernels of the library, scaled HBM bytes per dispatch (mean over dispatches):\n")
+        print("| kernel | fetch MB | write MB |")
+        print("|---|---|---|")
+        for k in others:
+            print(f"| {k} | {f['other_bytes'].get(k, 0) / 1e6:.2f} | {w['other_bytes'].get(k, 0) / 1e6:.2f} |")
     total = f["bytes_per_step"] + w["bytes_per_step"]
     print(f"\nHBM traffic of the grouped SwiGLU fwd+bwd per step (scaled): fetch {f['bytes_per_step']:.4g} B, "
           f"write {w['bytes_per_step']:.4g} B, total {total:.4g} B.\n")
