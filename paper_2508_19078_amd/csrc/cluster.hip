@@ -25,6 +25,8 @@ constexpr int GR_NS = 4;           // slabs in the LDS ring (3 in flight)
 constexpr long GR_KC = 32768;      // parameters per chunk
 constexpr int CL_MAXL = 1024;      // layers of one budget call
 constexpr int JAC_SWEEPS = 40;
+constexpr int CL_TH = 1024;       // threads of the per-layer PCA / K-Means block
+constexpr int CL_W = CL_TH / 64;
 
 // ------------------------------------------------------------ Eq. 1 ------
 
@@ -54,8 +56,8 @@ __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
 
 // One block.  Wave w takes layers w, w + 4, ...: mean and variance of the
 // frequencies by wave reductions.  Wave 0 then sums the weights and settles the
-// integer budgets one slot at a time, each step a wave-wide arg-max over the
-// layers (lane i holds layers i, i + 64, ...).
+// integer budgets with wave-wide arg-max steps over the layers (lane i holds
+// layers i, i + 64, ...).
 __global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict__ counts,
                                                       const uint8_t* __restrict__ tuning, int L,
                                                       int E, double total, int B_non, double eps,
@@ -97,9 +99,14 @@ __global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict_
     tot += sB[l];
   }
   for (int o = 32; o >= 1; o >>= 1) tot += __shfl_xor(tot, o);
-  while (tot < B_non) {            // short: +1 to the largest share - B_l with room (ties: lower layer)
-    double bv = -INFINITY;
-    int bl = 1 << 30;
+  // The slots go one at a time to the layer with the largest share - B_l
+  // that has room (ties: lower layer).  A layer that wins keeps winning until
+  // its share - (B_l + j) falls below the best other layer's, so each step
+  // hands it that whole run at once (the same result, in at most a few steps
+  // per layer).
+  while (tot < B_non) {
+    double bv = -INFINITY, cv = -INFINITY;
+    int bl = 1 << 30, cl = 1 << 30;
     for (int l = lane; l < L; l += 64)
       if (sB[l] < sn[l] && sh[l] - sB[l] > bv) {
         bv = sh[l] - sB[l];
@@ -107,12 +114,35 @@ __global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict_
       }
     wave_argmax(bv, bl);
     if (bl >= L) break;
-    if (lane == 0) ++sB[bl];
-    ++tot;
+    for (int l = lane; l < L; l += 64)
+      if (l != bl && sB[l] < sn[l] && sh[l] - sB[l] > cv) {
+        cv = sh[l] - sB[l];
+        cl = l;
+      }
+    wave_argmax(cv, cl);
+    const int b0 = sB[bl];
+    const long lim = min((long)(sn[bl] - b0), (long)B_non - tot);
+    auto wins = [&](long j) {
+      const double dj = sh[bl] - (double)(b0 + j);
+      return dj > cv || (dj == cv && bl < cl);
+    };
+    long j = 0;                      // wins(0) holds; find the last winning j
+    if (cl >= L) {
+      j = lim - 1;
+    } else {
+      j = (long)fmax(0.0, fmin((double)(lim - 1), floor(bv - cv)));
+      while (j + 1 < lim && wins(j + 1)) ++j;
+      while (j > 0 && !wins(j)) --j;
+    }
+    if (lane == 0) sB[bl] = b0 + (int)(j + 1);
+    tot += j + 1;
   }
-  while (tot > B_non) {            // over: -1 to the smallest share - B_l above its floor (ties: higher layer)
-    double bv = -INFINITY;
-    int bl = 1 << 30;
+  // Over the total: slots are taken back one at a time from the layer with
+  // the smallest share - B_l above its floor (ties: higher layer), in runs
+  // the same way.  Values are negated so that the arg-max picks them.
+  while (tot > B_non) {
+    double bv = -INFINITY, cv = -INFINITY;
+    int bl = 1 << 30, cl = 1 << 30;
     for (int l = lane; l < L; l += 64)
       if (sB[l] > min(1, sn[l]) && -(sh[l] - sB[l]) >= bv) {
         bv = -(sh[l] - sB[l]);
@@ -120,8 +150,29 @@ __global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict_
       }
     wave_argmax(bv, bl);
     if (bl > 0) break;
-    if (lane == 0) --sB[-bl];
-    --tot;
+    const int lb = -bl;
+    for (int l = lane; l < L; l += 64)
+      if (l != lb && sB[l] > min(1, sn[l]) && -(sh[l] - sB[l]) >= cv) {
+        cv = -(sh[l] - sB[l]);
+        cl = -l;
+      }
+    wave_argmax(cv, cl);
+    const int b0 = sB[lb];
+    const long lim = min((long)(b0 - min(1, sn[lb])), tot - (long)B_non);
+    auto wins = [&](long j) {
+      const double nj = -(sh[lb] - (double)(b0 - j));
+      return nj > cv || (nj == cv && bl < cl);
+    };
+    long j = 0;
+    if (cl > 0) {
+      j = lim - 1;
+    } else {
+      j = (long)fmax(0.0, fmin((double)(lim - 1), floor(bv - cv)));
+      while (j + 1 < lim && wins(j + 1)) ++j;
+      while (j > 0 && !wins(j)) --j;
+    }
+    if (lane == 0) sB[lb] = b0 - (int)(j + 1);
+    tot -= j + 1;
   }
   for (int l = lane; l < L; l += 64) budget[l] = sB[l];
 }
@@ -339,9 +390,9 @@ struct ClusterLds {
   uint16_t tri[CL_NMAX / 2 * (CL_NMAX / 2 + 1) / 2];   // pair blocks k1 <= k2
   uint16_t pairs[(CL_NMAX - 1) * (CL_NMAX / 2)];        // round-robin (p << 8 | q) per round
   double rho[CL_NMAX], nrm2[CL_NMAX], mind[CL_NMAX], cn[CL_NMAX];
-  double red[2][256];
-  double bsim[4][CL_NMAX];
-  int bj[4][CL_NMAX];
+  double red[2][CL_TH];
+  double bsim[CL_W][CL_NMAX];
+  int bj[CL_W][CL_NMAX];
   int mem[CL_NMAX], comp[CL_RMAX], lab[CL_NMAX], chosen[CL_NMAX];
   int flag;
 };
@@ -371,7 +422,7 @@ struct ClusterArgs {
   int E, NB, r, max_iter;
 };
 
-__global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
+__global__ __launch_bounds__(CL_TH) void k_cluster(ClusterArgs a) {
   __shared__ ClusterLds S;
   const int l = blockIdx.x, tid = threadIdx.x, lane = lane_id(), wave = wave_id();
   const int E = a.E, r = a.r;
@@ -459,7 +510,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
     S.red[0][tid] = off;
     S.red[1][tid] = tot;
     __syncthreads();
-    for (int hh = 128; hh > 0; hh >>= 1) {
+    for (int hh = CL_TH / 2; hh > 0; hh >>= 1) {
       if (tid < hh) {
         S.red[0][tid] += S.red[0][tid + hh];
         S.red[1][tid] += S.red[1][tid + hh];
@@ -490,14 +541,14 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
       // A is symmetric: blocks k1 <= k2 are computed and stored with their
       // mirror.  Every item's loads are issued before any store, so that the
       // stores (which may alias in the compiler's view) do not serialise them.
-      constexpr int NTRI = (CL_NMAX / 2 * (CL_NMAX / 2 + 1) / 2 + 255) / 256;
+      constexpr int NTRI = (CL_NMAX / 2 * (CL_NMAX / 2 + 1) / 2 + CL_TH - 1) / CL_TH;
       {
         double va[NTRI][4];
         int ip[NTRI][4];
         double rot[NTRI][4];
 #pragma unroll
         for (int u = 0; u < NTRI; ++u) {
-          const int x = min(tid + 256 * u, ntri - 1);
+          const int x = min(tid + CL_TH * u, ntri - 1);
           const int k1 = S.tri[x] >> 8, k2 = S.tri[x] & 255;
           ip[u][0] = S.rp[k1]; ip[u][1] = S.rq[k1]; ip[u][2] = S.rp[k2]; ip[u][3] = S.rq[k2];
           rot[u][0] = S.rc[k1]; rot[u][1] = S.rs[k1]; rot[u][2] = S.rc[k2]; rot[u][3] = S.rs[k2];
@@ -506,22 +557,23 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
           va[u][2] = S.A[ip[u][1] * LDA + ip[u][2]];
           va[u][3] = S.A[ip[u][1] * LDA + ip[u][3]];
         }
-        // V: thread owns pair k = tid % 32 and rows tid / 32 + 8 j
+        // V: thread owns pair k = tid % 32 and rows tid / 32 + (CL_TH / 32) j
         const int k = tid & 31;
         const bool kv = k < h;
         const int kk = kv ? k : 0;
         const int vp_ = S.rp[kk], vq_ = S.rq[kk];
         const double vc = S.rc[kk], vs = S.rs[kk];
-        double vv[CL_NMAX / 8][2];
+        constexpr int VR = (CL_NMAX + CL_TH / 32 - 1) / (CL_TH / 32);
+        double vv[VR][2];
 #pragma unroll
-        for (int j = 0; j < CL_NMAX / 8; ++j) {
-          const int i = min((tid >> 5) + 8 * j, m - 1);
+        for (int j = 0; j < VR; ++j) {
+          const int i = min((tid >> 5) + (CL_TH / 32) * j, m - 1);
           vv[j][0] = S.V[i * LDA + vp_];
           vv[j][1] = S.V[i * LDA + vq_];
         }
 #pragma unroll
         for (int u = 0; u < NTRI; ++u) {
-          if (tid + 256 * u < ntri) {
+          if (tid + CL_TH * u < ntri) {
             const double c1 = rot[u][0], s1 = rot[u][1], c2 = rot[u][2], s2 = rot[u][3];
             const double a = va[u][0], b = va[u][1], c = va[u][2], d = va[u][3];
             const double ra = c1 * a - s1 * c, rb = c1 * b - s1 * d;     // rows (pair k1)
@@ -543,8 +595,8 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
         }
         if (kv) {
 #pragma unroll
-          for (int j = 0; j < CL_NMAX / 8; ++j) {
-            const int i = (tid >> 5) + 8 * j;
+          for (int j = 0; j < VR; ++j) {
+            const int i = (tid >> 5) + (CL_TH / 32) * j;
             if (i < m) {
               S.V[i * LDA + vp_] = vc * vv[j][0] - vs * vv[j][1];
               S.V[i * LDA + vq_] = vs * vv[j][0] + vc * vv[j][1];
@@ -631,7 +683,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
   if (tid < n) S.lab[tid] = -1;
   __syncthreads();
 
-  // 5. Lloyd passes: thread (e, w) scans centroids w, w + 4, ...
+  // 5. Lloyd passes: thread (e, w) scans centroids w, w + CL_W, ...
   int pass = 0;
   for (;;) {
     ++pass;
@@ -640,7 +692,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
       double bs = -INFINITY;
       int bj = 1 << 30;
       if (e < n)
-        for (int c = w; c < B; c += 4) {
+        for (int c = w; c < B; c += CL_W) {
           double d = 0.0;
 #pragma unroll 8
           for (int j = 0; j < r; ++j) d += S.Z[e * LDZ + j] * S.C[c * LDZ + j];
@@ -658,7 +710,7 @@ __global__ __launch_bounds__(256) void k_cluster(ClusterArgs a) {
     if (tid < n) {
       double bs = S.bsim[0][tid];
       int bj = S.bj[0][tid];
-      for (int w = 1; w < 4; ++w) {
+      for (int w = 1; w < CL_W; ++w) {
         const double v = S.bsim[w][tid];
         const int j = S.bj[w][tid];
         if (v > bs || (v == bs && j < bj)) {
@@ -783,6 +835,6 @@ extern "C" int moe_cluster_experts(const void* const* w_src, int dtype, int L, i
                      z.NT, G);
   FM_TRY(check_launch("moe_cluster_experts (Gram sum)"));
   ClusterArgs ca{G, tuning, budget, labels, features, iters, E, z.NB, r, max_iter};
-  hipLaunchKernelGGL(k_cluster, dim3(L), dim3(256), 0, st, ca);
+  hipLaunchKernelGGL(k_cluster, dim3(L), dim3(CL_TH), 0, st, ca);
   return check_launch("moe_cluster_experts (PCA, K-Means)");
 }
