@@ -908,13 +908,14 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
 // A slot's rows are its tokens after folding (a token whose choices share the
 // slot is one row with the summed gate), so |D_s| is the slot's row count.
 
-constexpr int UT_ROWS = 256;   // rows per first-pass tile
+constexpr int UT_ROWS = 64;    // rows per first-pass tile (several blocks per CU keep loads in flight)
 
 // Sum of squares of n elements (n % 8 == 0) spread over a wave: every lane
 // ends with the same total (fixed butterfly order).
 template <typename T> __device__ __forceinline__ float wave_sumsq(const T* __restrict__ p, int n) {
   constexpr int V = 16 / sizeof(T);
   float a = 0.f;
+#pragma unroll 4
   for (int c = lane_id() * V; c < n; c += 64 * V) {
     float f[V];
     unpack16(ld16(p + c), f, (T*)nullptr);
@@ -926,7 +927,7 @@ template <typename T> __device__ __forceinline__ float wave_sumsq(const T* __res
   return a;
 }
 
-// First pass: one block per 256-row tile of a slot (tiles as in mbase); four
+// First pass: one block per 64-row tile of a slot (tiles as in mbase); four
 // waves take every fourth row; the tile's sum in fp64, waves added in order.
 template <typename T>
 __global__ __launch_bounds__(256) void k_utility_rows(const T* __restrict__ X, const T* __restrict__ Xp,

@@ -103,6 +103,26 @@ def test_merge_budget_edges():
         assert np.array_equal(run_budget(big, tb, 100.0, 3000), ref)
 
 
+def test_merge_budget_random_totals():
+    """Random layers, tuning masks and totals, many with capped or floored
+    layers, so that the settlement runs long stretches for one layer."""
+    rng = np.random.default_rng(12)
+    checked = 0
+    for trial in range(60):
+        L, E = int(rng.integers(1, 40)), int(rng.integers(2, 64))
+        counts = rng.integers(0, int(rng.integers(1, 400)), size=(L, E)).astype(np.int32)
+        tuning = (rng.random((L, E)) < rng.random()).astype(np.uint8)
+        n_non = int((tuning == 0).sum())
+        for B_non in rng.integers(0, n_non + 5, size=3):
+            ref, share = O.merge_budget(counts, tuning.astype(bool), 300.0, int(B_non))
+            if B_non > 0 and budget_margin(share, ref) < 1e-9:
+                continue
+            got = run_budget(counts, tuning, 300.0, int(B_non))
+            assert np.array_equal(got, ref), (trial, int(B_non), got, ref)
+            checked += 1
+    assert checked >= 120
+
+
 # ---------------------------------------------------------------- clustering --
 
 class Stack:
