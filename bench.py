@@ -85,7 +85,7 @@ def cpu_model():
 
 def cold_hbm(r, w, st, N, reps=5):
     """The HBM-bound entry points timed one launch at a time with a cold MALL:
-    a 512 MiB scrub buffer is written before every launch (outside the timed
+    a 512 MiB scrub buffer is read before every launch (outside the timed
     interval, which HIP events on the launch stream bracket).  Median of
     `reps`; algorithmic bytes per launch as in the kernel table."""
     import numpy as np
@@ -122,13 +122,16 @@ def cold_hbm(r, w, st, N, reps=5):
         calls["merge"] = (lambda: api.moe_merge_experts(r.w_src, r.dt, w.d, w.I, r.G, r.grp_ptr, r.grp_member,
                                                         r.alpha, r.w_dst, r.dt),
                           (w.E - r.K + r.G) * 3 * w.d * w.I * b)
-    scrub = torch.empty(256 << 20, dtype=torch.int16, device="cuda")
+    # read, not written: dirty scrub lines would be written back to HBM while
+    # the timed kernel evicts them
+    scrub = torch.ones(256 << 20, dtype=torch.int16, device="cuda")
+    sink = torch.empty((), dtype=torch.int64, device="cuda")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     out = {}
     for name, (fn, nbytes) in calls.items():
         ts = []
         for i in range(reps):
-            scrub.fill_(i)
+            torch.sum(scrub, dim=0, dtype=torch.int64, out=sink)
             e0.record(st)
             fn()
             e1.record(st)
@@ -137,7 +140,7 @@ def cold_hbm(r, w, st, N, reps=5):
         us = float(np.median(ts)) * 1e3
         gbs = nbytes / (us * 1e-6) / 1e9
         out[name] = {"us": round(us, 1), "GBps": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 3)}
-    del scrub
+    del scrub, sink
     return out
 
 
