@@ -397,6 +397,15 @@ struct ClusterLds {
   int flag;
 };
 
+// 1 / sqrt(x) for x > 0: the hardware estimate refined by two Newton steps.
+__device__ __forceinline__ double rsqrt_f64(double x) {
+  double y = __builtin_amdgcn_rsq(x);
+  const double hx = 0.5 * x;
+  y = y * (1.5 - hx * y * y);
+  y = y * (1.5 - hx * y * y);
+  return y;
+}
+
 // Round-robin pairing of m indices (m even): m / 2 disjoint pairs per round,
 // every pair once over m - 1 rounds.
 __device__ __forceinline__ void rr_pair(int round, int k, int m, int& p, int& q) {
@@ -526,11 +535,21 @@ __global__ __launch_bounds__(CL_TH) void k_cluster(ClusterArgs a) {
         const double apq = S.A[p * LDA + q];
         double c = 1.0, s = 0.0;
         if (apq != 0.0) {
-          const double tau = (S.A[q * LDA + q] - S.A[p * LDA + p]) / (2.0 * apq);
-          const double t = fabs(tau) > 1e150 ? 0.5 / tau
-                                              : (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-          c = 1.0 / sqrt(1.0 + t * t);
-          s = t * c;
+          // tan of the angle t = sgn(tau) / (|tau| + sqrt(1 + tau^2)), tau =
+          // dd / e2, written without divisions: with hyp = sqrt(dd^2 + e2^2)
+          // and w = |dd| + hyp, c = w / sqrt(2 hyp w), s = sgn(tau) |e2| / sqrt(2 hyp w).
+          double dd = S.A[q * LDA + q] - S.A[p * LDA + p], e2 = 2.0 * apq;
+          const double sg = (dd == 0.0 || (dd > 0.0) == (e2 > 0.0)) ? 1.0 : -1.0;
+          const double mx = fmax(fabs(dd), fabs(e2));
+          if (mx > 1e100 || mx < 1e-100) {   // c and s depend on the ratio only
+            dd /= mx;
+            e2 /= mx;
+          }
+          const double hyp = sqrt(dd * dd + e2 * e2);
+          const double w = fabs(dd) + hyp;
+          const double r = rsqrt_f64(2.0 * hyp * w);
+          c = w * r;
+          s = sg * fabs(e2) * r;
         }
         S.rc[tid] = c;
         S.rs[tid] = s;
