@@ -21,7 +21,7 @@ namespace {
 constexpr int CL_NMAX = 64;        // experts per layer
 constexpr int CL_RMAX = 32;        // feature dimension
 constexpr int GR_ROWB = 512;       // bytes of one expert's parameters per slab
-constexpr int GR_NS = 4;           // slabs in the LDS ring (3 in flight)
+constexpr int GR_LDS = 144 * 1024; // LDS of the slab ring
 constexpr long GR_KC = 32768;      // parameters per chunk
 constexpr int CL_MAXL = 1024;      // layers of one budget call
 constexpr int JAC_SWEEPS = 40;
@@ -99,6 +99,60 @@ __global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict_
     tot += sB[l];
   }
   for (int o = 32; o >= 1; o >>= 1) tot += __shfl_xor(tot, o);
+  // Bulk of a shortfall.  Slot j of layer l beyond B_l has the value
+  // share_l - (B_l + j); the settlement below takes slots in decreasing value,
+  // so every slot whose value exceeds a threshold tau with at most `need` such
+  // slots is taken for sure.  A bisection finds such a tau close to the
+  // shortfall; the few slots left go through the settlement steps.
+  if (tot < B_non) {
+    const long need = (long)B_non - tot;
+    auto above = [&](double tau, int l) -> int {      // #{j < room : share - (B + j) > tau}
+      const int room = sn[l] - sB[l];
+      if (room <= 0) return 0;
+      const double x = sh[l] - sB[l] - tau;
+      int j = x <= 0.0 ? 0 : (x >= room ? room : (int)ceil(x));
+      while (j > 0 && !(sh[l] - (double)(sB[l] + j - 1) > tau)) --j;
+      while (j < room && sh[l] - (double)(sB[l] + j) > tau) ++j;
+      return j;
+    };
+    auto count = [&](double tau) {
+      long c = 0;
+      for (int l = lane; l < L; l += 64) c += above(tau, l);
+      for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
+      return c;
+    };
+    double hi = -INFINITY, lo = INFINITY;            // the largest and smallest slot values
+    for (int l = lane; l < L; l += 64)
+      if (sB[l] < sn[l]) {
+        hi = fmax(hi, sh[l] - sB[l]);
+        lo = fmin(lo, sh[l] - (double)(sn[l] - 1));
+      }
+    for (int o = 32; o >= 1; o >>= 1) {
+      hi = fmax(hi, __shfl_xor(hi, o));
+      lo = fmin(lo, __shfl_xor(lo, o));
+    }
+    if (hi > -INFINITY) {
+      lo -= 1.0;                                      // every slot lies above lo
+      if (count(lo) <= need) {
+        hi = lo;
+      } else {
+        for (int it = 0; it < 200; ++it) {           // count(hi) <= need < count(lo)
+          const double mid = 0.5 * (lo + hi);
+          if (!(mid > lo && mid < hi)) break;
+          if (count(mid) <= need) hi = mid;
+          else lo = mid;
+        }
+      }
+      long got = 0;
+      for (int l = lane; l < L; l += 64) {
+        const int g = above(hi, l);
+        sB[l] += g;
+        got += g;
+      }
+      for (int o = 32; o >= 1; o >>= 1) got += __shfl_xor(got, o);
+      tot += got;
+    }
+  }
   // The slots go one at a time to the layer with the largest share - B_l
   // that has room (ties: lower layer).  A layer that wins keeps winning until
   // its share - (B_l + j) falls below the best other layer's, so each step
@@ -136,6 +190,58 @@ __global__ __launch_bounds__(256) void k_merge_budget(const int32_t* __restrict_
     }
     if (lane == 0) sB[bl] = b0 + (int)(j + 1);
     tot += j + 1;
+  }
+  // Bulk of an excess, the same way: the j-th slot taken back from layer l has
+  // the key share_l - (B_l - j), keys are taken in increasing order, and every
+  // key below a threshold with at most `need` such keys goes for sure.
+  if (tot > B_non) {
+    const long need = tot - (long)B_non;
+    auto below = [&](double tau, int l) -> int {      // #{j < cap : share - (B - j) < tau}
+      const int cap = sB[l] - min(1, sn[l]);
+      if (cap <= 0) return 0;
+      const double x = tau - (sh[l] - sB[l]);
+      int j = x <= 0.0 ? 0 : (x >= cap ? cap : (int)ceil(x));
+      while (j > 0 && !(sh[l] - (double)(sB[l] - (j - 1)) < tau)) --j;
+      while (j < cap && sh[l] - (double)(sB[l] - j) < tau) ++j;
+      return j;
+    };
+    auto count = [&](double tau) {
+      long c = 0;
+      for (int l = lane; l < L; l += 64) c += below(tau, l);
+      for (int o = 32; o >= 1; o >>= 1) c += __shfl_xor(c, o);
+      return c;
+    };
+    double lo = INFINITY, hi = -INFINITY;            // the smallest and largest keys
+    for (int l = lane; l < L; l += 64)
+      if (sB[l] > min(1, sn[l])) {
+        lo = fmin(lo, sh[l] - sB[l]);
+        hi = fmax(hi, sh[l] - (double)(min(1, sn[l]) + 1));
+      }
+    for (int o = 32; o >= 1; o >>= 1) {
+      hi = fmax(hi, __shfl_xor(hi, o));
+      lo = fmin(lo, __shfl_xor(lo, o));
+    }
+    if (lo < INFINITY) {
+      hi += 1.0;                                      // every key lies below hi
+      if (count(hi) <= need) {
+        lo = hi;
+      } else {
+        for (int it = 0; it < 200; ++it) {           // count(lo) <= need < count(hi)
+          const double mid = 0.5 * (lo + hi);
+          if (!(mid > lo && mid < hi)) break;
+          if (count(mid) <= need) lo = mid;
+          else hi = mid;
+        }
+      }
+      long got = 0;
+      for (int l = lane; l < L; l += 64) {
+        const int g = below(lo, l);
+        sB[l] -= g;
+        got += g;
+      }
+      for (int o = 32; o >= 1; o >>= 1) got += __shfl_xor(got, o);
+      tot -= got;
+    }
   }
   // Over the total: slots are taken back one at a time from the layer with
   // the smallest share - B_l above its floor (ties: higher layer), in runs
@@ -225,17 +331,30 @@ template <> struct GramFrag<float> {
   }
 };
 
-template <int INS> __device__ __forceinline__ void gram_wait(int ahead) {
-  if (ahead >= 2) wait_vmcnt<2 * INS>();
-  else if (ahead == 1) wait_vmcnt<INS>();
-  else wait_vmcnt<0>();
+// Waits for this wave's DMA of the slab being consumed, leaving the `ahead`
+// later slabs' INS instructions each in flight (A = the most there can be).
+template <int INS, int A> __device__ __forceinline__ void gram_wait(int ahead) {
+  if constexpr (A == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= A) wait_vmcnt<A * INS>();
+    else gram_wait<INS, A - 1>(ahead);
+  }
 }
+
+// The slab ring of NG row groups: as many slabs as fit in GR_LDS (at most 16),
+// so that fewer rows mean more slabs in flight.
+template <int NG> struct GramRing {
+  static constexpr int SLAB = NG * 16 * GR_ROWB;
+  static constexpr int NS = GR_LDS / SLAB < 16 ? GR_LDS / SLAB : 16;
+  static_assert(NS >= 3, "ring depth");
+};
 
 // NG groups of 16 rows hold the n experts (rows past n repeat row n - 1).
 template <typename T, int NB, int NG>
 __device__ __forceinline__ void gram_chunk(const GramArgs& a, const int* mem, int n, int l, int mat,
                                            long k0, long klen, FM_LDS char* lds, f32x16_t* acc) {
-  constexpr int ROWS = NB * 32, SLAB = ROWS * GR_ROWB;
+  constexpr int SLAB = GramRing<NG>::SLAB, NS = GramRing<NG>::NS;
   constexpr int EPS = GR_ROWB / (int)sizeof(T);       // parameters per row and slab
   constexpr int EPC = 16 / (int)sizeof(T);            // parameters per 16-byte chunk
   constexpr int INS = 2 * NG;                         // DMA instructions per wave and slab
@@ -262,7 +381,7 @@ __device__ __forceinline__ void gram_chunk(const GramArgs& a, const int* mem, in
     dst[q] = (uint32_t)(((g * 4 + m) * 2 + h) * 1024);
   }
   auto issue = [&](int s) {
-    FM_LDS char* slab = lds + (s % GR_NS) * SLAB;
+    FM_LDS char* slab = lds + (s % NS) * SLAB;
     const bool last = s == nslab - 1;
 #pragma unroll
     for (int q = 0; q < INS; ++q) {
@@ -272,16 +391,16 @@ __device__ __forceinline__ void gram_chunk(const GramArgs& a, const int* mem, in
     }
   };
 
-  const int pre = min(GR_NS - 1, nslab);
+  const int pre = min(NS - 1, nslab);
   for (int s = 0; s < pre; ++s) issue(s);
 
   // fragment addresses: lane (i, hf) reads row 32 b + i, k-steps j = 0..3 of line `wave`
   const int i = lane & 31, hf = lane >> 5;
   for (int s = 0; s < nslab; ++s) {
-    gram_wait<INS>(min(GR_NS - 2, nslab - 1 - s));
+    gram_wait<INS, NS - 2>(min(NS - 2, nslab - 1 - s));
     barrier_lds();
-    if (s + GR_NS - 1 < nslab) issue(s + GR_NS - 1);
-    const FM_LDS char* slab = lds + (s % GR_NS) * SLAB;
+    if (s + NS - 1 < nslab) issue(s + NS - 1);
+    const FM_LDS char* slab = lds + (s % NS) * SLAB;
     const bool last = s == nslab - 1;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -289,7 +408,9 @@ __device__ __forceinline__ void gram_chunk(const GramArgs& a, const int* mem, in
       typename F::frag fr[NB];
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        const int R = 32 * b + i, g = R >> 4, rr = R & 15;
+        // rows past the NG loaded groups feed only outputs that are not used:
+        // they read the last group
+        const int R = 32 * b + i, g = min(R >> 4, NG - 1), rr = R & 15;
         fr[b] = F::load(slab + ((g * 4 + wave) * 2 + h) * 1024 + rr * 64 + ((q ^ ((rr >> 2) & 3)) << 4));
       }
       if (last && wave * 8 + cc >= tail_chunks) {
@@ -313,7 +434,7 @@ __device__ __forceinline__ void gram_chunk(const GramArgs& a, const int* mem, in
 template <typename T, int NB>
 __global__ __launch_bounds__(256) void k_gram(GramArgs a) {
   constexpr int NT = NB * (NB + 1) / 2;
-  __shared__ __align__(1024) char lds_raw[GR_NS * NB * 32 * GR_ROWB];
+  __shared__ __align__(1024) char lds_raw[GR_LDS];
   __shared__ int mem[CL_NMAX];
   FM_LDS char* lds = (FM_LDS char*)lds_raw;
   const int l = blockIdx.y, c = blockIdx.x, nchunk = gridDim.x;
