@@ -24,6 +24,8 @@ What each function follows:
   weight gradients; non-tuning (merged, frozen) experts do not.
 * Expert FFN: SwiGLU, out = W_down (silu(W_gate x) * (W_up x)).
 * Expert utility (Section 6.1, Eq. 3): the gradient-norm utility of a slot.
+* Quantised profiling of a layer stack (Section 4.1): int8 router and experts,
+  layers coupled by a residual stream.
 * Layer-aware merging (Section 5): the per-layer budget of Eq. 1 (Section 5.1),
   then PCA features of the experts' parameters and K-Means with cosine
   distance over all layers at once, cross-layer pairs masked (Section 5.2).
@@ -631,3 +633,56 @@ def fused_kmeans(features: Sequence, budgets: Sequence[int], max_iter: int):
         prev = lab
     labels = [lab[layer_of_expert == l] - first_c[l] for l in range(L)]
     return labels, passes
+
+
+# ------------------------------- quantised profiling of a layer stack ----
+
+def dequantize_rows(q, s) -> np.ndarray:
+    """q [..., rows, cols] int8 codes times their row scale s [..., rows]."""
+    return _f64(q) * _f64(s)[..., None]
+
+
+def quantized_stack_profile(X0, layers: Sequence[Dict], k: int):
+    """Profiling pass of Section 4.1 with a low-bit copy of a stack of MoE
+    layers: each layer's router and expert matrices are quantised per row to
+    int8 (quantize_int8_rows), and the layer runs on them — the int8 router's
+    top-k and softmax gate, every routed expert (unmerged) with its dequantised
+    weights q * s, and shared experts with gate 1.  The histogram of layer l
+    counts its top-k selections.  Layers are coupled by a residual stream,
+    X_{l+1} = X_l + Y_l (the synthetic stack has no other sublayers).
+    layers[l]: dict with Wr [E,d], bias [E] or None, wg [E,I,d], wu [E,I,d],
+    wd [E,d,I] and optionally sg, su, sd (shared experts).
+    Returns (counts [L][E] int64, idx [L][T,k], gate [L][T,k], X [L+1][T,d]).
+    """
+    X = _f64(X0)
+    counts, idxs, gates, Xs = [], [], [], [X]
+    for lay in layers:
+        q, s = quantize_int8_rows(lay["Wr"])
+        lg = profile_logits(X, q, s, lay.get("bias"))
+        idx = topk_select(lg, k)
+        sel = np.take_along_axis(lg, idx, axis=1)
+        gate = softmax_rows(sel)
+        E = lg.shape[1]
+        counts.append(np.bincount(idx.ravel(), minlength=E).astype(np.int64))
+
+        def deq(W):
+            W = np.asarray(W)
+            n = W.shape[0]
+            qq, ss = quantize_int8_rows(W.reshape(-1, W.shape[-1]))
+            return dequantize_rows(qq, ss).reshape(W.shape) if n else W
+
+        wg, wu, wd = deq(lay["wg"]), deq(lay["wu"]), deq(lay["wd"])
+        n_sh = 0
+        if lay.get("sg") is not None:
+            sgq, suq, sdq = deq(lay["sg"]), deq(lay["su"]), deq(lay["sd"])
+            n_sh = len(sgq)
+            wg = list(wg) + list(sgq)
+            wu = list(wu) + list(suq)
+            wd = list(wd) + list(sdq)
+        slots = SlotWeights(wg, wu, wd, [False] * (E + n_sh), n_shared=n_sh)
+        Y = moe_forward(X, idx, gate, np.arange(E), slots)
+        X = X + Y
+        idxs.append(idx)
+        gates.append(gate)
+        Xs.append(X)
+    return counts, idxs, gates, Xs
