@@ -31,7 +31,8 @@
  *           validated on the host before any HIP call, so an invalid call
  *           enqueues nothing.  moe_last_error() gives a message for the last
  *           failure on the calling thread.  No C++ exception crosses the ABI.
- * Outputs.  Fully overwritten, except `counts` of moe_profile_hist (adds) and
+ * Outputs.  Fully overwritten, except `counts` of moe_profile_hist and
+ *           moe_profile_route (adds) and
  *           the weight gradients of moe_grouped_swiglu_bwd when accumulate_dw.
  */
 #ifndef FLUXMOE_H
@@ -119,6 +120,34 @@ int moe_profile_hist(const void* X, int x_dtype, const int8_t* Wq,
                      const float* scale, const float* bias,
                      int T, int d, int E, int k,
                      int32_t* counts, int32_t* idx, void* stream);
+
+/* moe_profile_route: the int8 profiling router of moe_profile_hist that also
+ * hands its routing to the profiling forward (Section 4.1: the low-bit copy
+ * of the model is run, not only its routers): counts[e] += the histogram as
+ * in moe_profile_hist, and idx [T,k] int32 (rank order) and gate [T,k] fp32
+ * (softmax over the k selected int8 logits~, as moe_route_topk does over its
+ * logits) are written.  idx and gate are required.
+ */
+int moe_profile_route(const void* X, int x_dtype, const int8_t* Wq,
+                      const float* scale, const float* bias,
+                      int T, int d, int E, int k,
+                      int32_t* counts, int32_t* idx, float* gate, void* stream);
+
+/* moe_dequant_int8: the matrices the profiling forward runs on (Section 4.1):
+ *   out[r, c] = q[r, c] * scale[r]   (fp32 product, one rounding to out_dtype)
+ * q [rows, cols] int8 (e.g. every expert's W_gate rows stacked: rows = E*I),
+ * scale [rows] fp32 from moe_quantize_int8, out [rows, cols] in out_dtype
+ * (MOE_BF16 or MOE_F32).  cols % 8 == 0.
+ */
+int moe_dequant_int8(const int8_t* q, const float* scale, long rows, int cols,
+                     int out_dtype, void* out, void* stream);
+
+/* moe_residual_add: out = X + Y elementwise (fp32 add, one rounding), the
+ * residual stream that carries one layer's output into the next layer of the
+ * profiling stack.  X, Y, out [T,d] in dtype; out may alias X.  d % 8 == 0.
+ */
+int moe_residual_add(const void* X, const void* Y, int T, int d, int dtype,
+                     void* out, void* stream);
 
 /* ---------------------------------------------------------------- merging --
  * moe_merge_plan: which experts of one layer are merged, from its histogram

@@ -61,6 +61,10 @@ _SIGS = {
     "moe_grouped_swiglu_bwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
     "moe_permute_bwd": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
     "moe_expert_utility": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp, _vp]),
+    "moe_profile_route": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp,
+                                   _vp]),
+    "moe_dequant_int8": (_c_int, [_vp, _vp, ctypes.c_long, _c_int, _c_int, _vp, _vp]),
+    "moe_residual_add": (_c_int, [_vp, _vp, _c_int, _c_int, _c_int, _vp, _vp]),
     "moe_merge_budget": (_c_int, [_vp, _vp, _c_int, _c_int, _f, _c_int, ctypes.c_double, _vp, _vp]),
     "moe_cluster_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
     "moe_cluster_experts": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int,
@@ -160,6 +164,26 @@ def moe_profile_hist(X, Wq, scale, bias, k, counts, idx=None, stream=None):
 
 
 # --------------------------------------------------------------- merging ----
+
+def moe_profile_route(X, Wq, scale, bias, k, counts, idx, gate, stream=None):
+    T, d = X.shape
+    E = Wq.shape[0]
+    return _call("moe_profile_route", ptr(X), dtype_code(X.dtype), ptr(Wq), ptr(scale), ptr(bias), T, d, E, k,
+                 ptr(counts), ptr(idx), ptr(gate), stream_ptr(stream))
+
+
+def moe_dequant_int8(q, scale, out, stream=None):
+    """q [..., cols] int8 with one scale per row of the flattened [rows, cols]."""
+    cols = q.shape[-1]
+    rows = q.numel() // cols
+    return _call("moe_dequant_int8", ptr(q), ptr(scale), rows, cols, dtype_code(out.dtype), ptr(out),
+                 stream_ptr(stream))
+
+
+def moe_residual_add(X, Y, out, stream=None):
+    T, d = X.shape
+    return _call("moe_residual_add", ptr(X), ptr(Y), T, d, dtype_code(X.dtype), ptr(out), stream_ptr(stream))
+
 
 def moe_merge_plan(counts, n_merge, group, total_tokens, expert_map, slot_src, grp_ptr, grp_member,
                    alpha, expert_base=0, grp_base=0, member_base=0, stream=None):

@@ -195,7 +195,7 @@ __device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int
   for (int u = 0; u < TPL; ++u) {
     const int t = t0 + tl[u];
     const bool mine = gl < k && tl[u] < RT_TOK && t < T;
-    if (MODE == 0) {
+    if (MODE != 1) {                 // idx and the softmax gate over the k selected
       float g = gl < k ? expf(myv[u] - v0[u]) : 0.f;
       float sum = g;
       sum += row_ror<8>(sum);
@@ -206,19 +206,21 @@ __device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int
         idx[(size_t)t * k + gl] = mye[u];
         gate[(size_t)t * k + gl] = g / sum;
       }
-    } else if (mine) {
+    }
+    if (MODE != 0 && mine) {         // histogram (+ idx alone in MODE 1)
       atomicAdd(&hist[mye[u]], 1);
-      if (idx) idx[(size_t)t * k + gl] = mye[u];
+      if (MODE == 1 && idx) idx[(size_t)t * k + gl] = mye[u];
     }
   }
-  if (MODE == 1) {
+  if (MODE != 0) {
     __syncthreads();
     for (int e = threadIdx.x; e < E; e += blockDim.x)
       if (hist[e]) atomicAdd(&counts[e], hist[e]);
   }
 }
 
-// MODE 0: write idx/gate (+logits).  MODE 1: histogram (+idx).
+// MODE 0: write idx/gate (+logits).  MODE 1: histogram (+idx).  MODE 2:
+// histogram, idx and gate.
 template <typename TX, typename TW, int NE, int KMAX, int MODE>
 __global__ __launch_bounds__(RtShape<NE>::WAVES * 64) void k_route(
     const TX* __restrict__ X, const TW* __restrict__ W, const float* __restrict__ wscale,
@@ -238,7 +240,7 @@ __global__ __launch_bounds__(RtShape<NE>::WAVES * 64) void k_route(
   const int t0 = blockIdx.x * RT_TOK;
   const int r16 = lane & 15, q4 = lane >> 4;
 
-  if (MODE == 1)
+  if (MODE != 0)
     for (int e = threadIdx.x; e < NE * 16; e += blockDim.x) hist[e] = 0;
 
   f32x4_t acc[2][NE];
@@ -418,7 +420,7 @@ __global__ __launch_bounds__(256) void k_route_lds(const bf16* __restrict__ X, c
   FM_LDS char* lds = (FM_LDS char*)lds_raw;
   const int lane = lane_id_here(), wave = wave_id();
   const int t0 = blockIdx.x * RT_TOK;
-  if (MODE == 1)
+  if (MODE != 0)
     for (int e = threadIdx.x; e < NB * 32; e += blockDim.x) hist[e] = 0;
   // the epilogue's per-expert scale and bias, fetched while the slabs stream
   if (threadIdx.x < E) {
@@ -564,7 +566,7 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
       else { FM_RL_K(2) }
 #undef FM_RL_K
 #undef FM_RL
-      return check_launch(MODE == 0 ? "moe_route_topk" : "moe_profile_hist");
+      return check_launch(MODE == 0 ? "moe_route_topk" : MODE == 1 ? "moe_profile_hist" : "moe_profile_route");
     }
   }
   const int ne = cdiv(E, 16);
@@ -583,7 +585,7 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
   else { FM_RT_K(16) }
 #undef FM_RT_K
 #undef FM_RT
-  return check_launch(MODE == 0 ? "moe_route_topk" : "moe_profile_hist");
+  return check_launch(MODE == 0 ? "moe_route_topk" : MODE == 1 ? "moe_profile_hist" : "moe_profile_route");
 }
 
 // Router backward with the top-k selection held fixed: for the k selected
@@ -713,6 +715,26 @@ extern "C" int moe_profile_hist(const void* X, int x_dtype, const int8_t* Wq, co
                                          nullptr, counts, st);
   return launch_route<float, int8_t, 1>((const float*)X, Wq, scale, bias, T, d, E, k, idx, nullptr,
                                         nullptr, counts, st);
+}
+
+extern "C" int moe_profile_route(const void* X, int x_dtype, const int8_t* Wq, const float* scale,
+                                 const float* bias, int T, int d, int E, int k, int32_t* counts,
+                                 int32_t* idx, float* gate, void* stream) {
+  clear_error();
+  FM_TRY(check_route_shape(T, d, E, k));
+  FM_TRY(need_dtype_float(x_dtype, "x_dtype"));
+  if (T == 0) return MOE_OK;
+  FM_TRY(need(X, "X")); FM_TRY(need(Wq, "Wq")); FM_TRY(need(scale, "scale")); FM_TRY(need(counts, "counts"));
+  FM_TRY(need(idx, "idx")); FM_TRY(need(gate, "gate"));
+  FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(Wq, "Wq")); FM_TRY(need_aligned(scale, "scale"));
+  FM_TRY(need_aligned(bias, "bias")); FM_TRY(need_aligned(counts, "counts")); FM_TRY(need_aligned(idx, "idx"));
+  FM_TRY(need_aligned(gate, "gate"));
+  hipStream_t st = as_stream(stream);
+  if (x_dtype == MOE_BF16)
+    return launch_route<bf16, int8_t, 2>((const bf16*)X, Wq, scale, bias, T, d, E, k, idx, gate, nullptr,
+                                         counts, st);
+  return launch_route<float, int8_t, 2>((const float*)X, Wq, scale, bias, T, d, E, k, idx, gate, nullptr,
+                                        counts, st);
 }
 
 extern "C" int moe_route_bwd(const float* gate, const int32_t* idx, const float* dgate, const void* Wr, int dtype,

@@ -205,3 +205,29 @@ def test_merge_budget_and_cluster_rejections(L):
     assert call(ws=MIS)[0] == api.MOE_ERR_ALIGN
     rc, msg = call(labels=None)
     assert rc == api.MOE_ERR_ARG and "labels" in msg
+
+
+def test_profiling_stack_rejections(L):
+    f = ctypes.c_float
+    rc, msg = rc_and_msg(L, "moe_profile_route", FAKE, api.MOE_BF16, FAKE, FAKE, None, 16, 64, 8, 2, FAKE, FAKE,
+                         None, None)
+    assert rc == api.MOE_ERR_ARG and "gate" in msg
+    rc, msg = rc_and_msg(L, "moe_profile_route", FAKE, api.MOE_BF16, FAKE, FAKE, None, 16, 64, 8, 2, FAKE, None,
+                         FAKE, None)
+    assert rc == api.MOE_ERR_ARG and "idx" in msg
+    rc, _ = rc_and_msg(L, "moe_profile_route", FAKE, api.MOE_BF16, FAKE, FAKE, None, 16, 64, 8, 9, FAKE, FAKE,
+                       FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED                              # k > E
+    rc, _ = rc_and_msg(L, "moe_dequant_int8", FAKE, FAKE, 10, 12, api.MOE_BF16, FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED                              # cols % 8
+    rc, _ = rc_and_msg(L, "moe_dequant_int8", FAKE, FAKE, 10, 16, api.MOE_I8, FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    rc, _ = rc_and_msg(L, "moe_dequant_int8", FAKE, FAKE, -1, 16, api.MOE_BF16, FAKE, None)
+    assert rc == api.MOE_ERR_ARG
+    rc, _ = rc_and_msg(L, "moe_dequant_int8", FAKE, MIS, 10, 16, api.MOE_BF16, FAKE, None)
+    assert rc == api.MOE_ERR_ALIGN
+    rc, _ = rc_and_msg(L, "moe_residual_add", FAKE, FAKE, 16, 12, api.MOE_BF16, FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED
+    rc, msg = rc_and_msg(L, "moe_residual_add", FAKE, None, 16, 16, api.MOE_BF16, FAKE, None)
+    assert rc == api.MOE_ERR_ARG and "Y" in msg
+    assert L.moe_residual_add(None, None, 0, 16, api.MOE_BF16, None, None) == 0   # T = 0: nothing to do
