@@ -36,6 +36,8 @@ def parse():
     p.add_argument("--cpu-sample-tokens", type=int, default=8192)
     p.add_argument("--no-cold", action="store_true", help="skip the cold-cache timing of the HBM-bound calls")
     p.add_argument("--no-merging", action="store_true", help="skip the layer-aware merging (Section 5) timing")
+    p.add_argument("--no-profiling", action="store_true",
+                   help="skip the quantised profiling pass over the layer stack (Section 4.1)")
     p.add_argument("--calib-copy", action="store_true",
                    help="end with a device-to-device copy of 256 MiB (counter calibration)")
     return p.parse_args()
@@ -284,6 +286,71 @@ def layer_merging(reps=3, B_non=840, r=16, n_classes=32, mix=0.6, max_iter=100):
     return out
 
 
+def profiling_stack(reps=3):
+    """The quantised profiling pass of Section 4.1 over the 28-layer
+    DeepSeek-MoE stack (64 experts, d = 2048, I = 1408, top-6, T = 4096 tokens):
+    per layer int8 routing with the histogram, the layer's experts dequantised
+    from int8, permute, grouped SwiGLU forward, combine and the residual.  The
+    weights are drawn on the GPU (torch's seeded generator, the workload's
+    distributions) and quantised once; the pass is timed with HIP events per
+    stage, median over `reps` passes after one warm-up."""
+    import numpy as np
+    import torch
+    from paper_2508_19078_amd import workloads as W
+    from paper_2508_19078_amd.profiling import QuantizedStack
+
+    w = W.WORKLOADS["deepseek_stack"]
+    dev = torch.device("cuda")
+    L, E, d, I, T, k = w.n_layers, w.E, w.d, w.I, w.T, w.k
+    g = torch.Generator(device=dev)
+    g.manual_seed(2508190781)
+    layers = []
+    for l in range(L):
+        rn = lambda *shape, std: (torch.randn(*shape, generator=g, device=dev) * std).to(torch.bfloat16)
+        layers.append(dict(Wr=rn(E, d, std=d ** -0.5), bias=torch.from_numpy(W.router_bias(w, l)).to(dev),
+                           wg=rn(E, I, d, std=d ** -0.5), wu=rn(E, I, d, std=d ** -0.5),
+                           wd=rn(E, d, I, std=I ** -0.5)))
+    X0 = torch.randn(T, d, generator=g, device=dev).to(torch.bfloat16)
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    qs = QuantizedStack(layers, T, k)
+    e1.record(st)
+    torch.cuda.synchronize()
+    quant_ms = e0.elapsed_time(e1)
+    del layers
+    torch.cuda.empty_cache()
+    passes = []
+    for rep in range(reps + 1):
+        evs = [torch.cuda.Event(enable_timing=True)]
+        names = []
+        evs[0].record(st)
+
+        def mark(name):
+            ev = torch.cuda.Event(enable_timing=True)
+            ev.record(st)
+            evs.append(ev)
+            names.append(name)
+        qs.run(X0, mark)
+        torch.cuda.synchronize()
+        stages = {}
+        for i, nm in enumerate(names):
+            stages[nm] = stages.get(nm, 0.0) + evs[i].elapsed_time(evs[i + 1])
+        passes.append((evs[0].elapsed_time(evs[-1]), stages))
+    total = float(np.median([p[0] for p in passes[1:]]))
+    stages = {nm: round(float(np.median([p[1][nm] for p in passes[1:]])), 3) for nm in passes[1][1]}
+    counts = qs.counts.cpu().numpy()
+    out = {"workload": f"deepseek_stack: {L} layers x {E} experts, d={d} I={I}, T={T}, top-{k}, int8 router "
+                       "and experts (per-row scales), residual stream",
+           "pass_ms": round(total, 3), "tokens_per_s": round(T / (total * 1e-3), 1),
+           "stages_ms": stages, "quantise_ms": round(quant_ms, 3),
+           "int8_weight_bytes": int(sum(q[n][0].numel() for q in qs.q for n in ("wg", "wu", "wd", "Wr"))),
+           "hist_ok": bool((counts.sum(axis=1) == T * k).all())}
+    del qs
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -390,6 +457,9 @@ def main():
     if not a.no_merging:
         print("# layer-aware merging over the 28-layer stack", file=sys.stderr, flush=True)
         out["layer_merging"] = layer_merging()
+    if not a.no_profiling:
+        print("# quantised profiling pass over the 28-layer stack", file=sys.stderr, flush=True)
+        out["profiling_stack"] = profiling_stack()
     if a.calib_copy:
         src = torch.ones(128 << 20, dtype=torch.bfloat16, device="cuda")
         dst = torch.empty_like(src)

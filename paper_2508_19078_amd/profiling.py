@@ -82,9 +82,11 @@ class QuantizedStack:
                                   dtype=torch.uint8, device=dev)
         self.trace: List[dict] = []
 
-    def run(self, X0: torch.Tensor) -> torch.Tensor:
+    def run(self, X0: torch.Tensor, mark=None) -> torch.Tensor:
         """The stack on the batch X0 [T,d]; per-layer histograms land in
-        self.counts [L,E]; returns the last layer's output stream."""
+        self.counts [L,E]; returns the last layer's output stream.  mark(name),
+        if given, is called after each stage (e.g. to record a HIP event)."""
+        mark = mark if mark is not None else (lambda name: None)
         T, k = self.T, self.k
         self.counts.zero_()
         self.trace = []
@@ -98,14 +100,19 @@ class QuantizedStack:
                 api.moe_dequant_int8(ql["sg"][0], ql["sg"][1], self.Sg)
                 api.moe_dequant_int8(ql["su"][0], ql["su"][1], self.Su)
                 api.moe_dequant_int8(ql["sd"][0], ql["sd"][1], self.Sd)
+            mark("dequant")
             Wq, ws = ql["Wr"]
             api.moe_profile_route(X, Wq, ws, ql["bias"], k, self.counts[l], self.idx, self.gate)
+            mark("route")
             api.moe_permute(X, self.idx, self.gate, None, self.E, self.offsets, self.perm_token, self.perm_gate,
                             self.inv, self.X_perm, self.ws_perm, E=self.E)
+            mark("permute")
             api.moe_grouped_swiglu_fwd(self.tables, X, self.X_perm, self.offsets, T, k, self.A_g, self.A_u,
                                        self.H, self.O, self.ws_fwd)
+            mark("ffn_fwd")
             api.moe_unpermute(self.tables, self.O, self.inv, self.perm_gate, T, k, self.Y)
             api.moe_residual_add(X, self.Y, Xn)
+            mark("combine")
             if self.record:
                 self.trace.append({"idx": self.idx.clone(), "gate": self.gate.clone(), "X": X.clone()})
             X, Xn = Xn, X
