@@ -38,6 +38,8 @@ def parse():
     p.add_argument("--no-merging", action="store_true", help="skip the layer-aware merging (Section 5) timing")
     p.add_argument("--no-profiling", action="store_true",
                    help="skip the quantised profiling pass over the layer stack (Section 4.1)")
+    p.add_argument("--part", choices=("all", "merging", "profiling"), default="all",
+                   help="merging / profiling: time only that once-per-round pass and print its JSON")
     p.add_argument("--calib-copy", action="store_true",
                    help="end with a device-to-device copy of 256 MiB (counter calibration)")
     return p.parse_args()
@@ -365,6 +367,9 @@ def main():
     if not os.path.exists(api.LIB_PATH):
         from paper_2508_19078_amd import build
         build.build()
+    if a.part != "all":
+        print(json.dumps(layer_merging() if a.part == "merging" else profiling_stack()))
+        return
     w = W.WORKLOADS[a.workload]
     print(f"# workload {w.name}: drawing inputs", file=sys.stderr, flush=True)
     inp = LayerInputs(w)
