@@ -1,14 +1,17 @@
 // Gate re-routing and token permutation into per-slot buckets, the combine,
 // and their backward passes.
 //
-// Permute runs in four launches, all deterministic:
-//   count   a block of 256 tokens counts its rows per slot (LDS integer atomics)
-//   scan    one block turns the per-block counts into global row positions:
-//           a wave scan per slot over the blocks, then an exclusive scan over
-//           the slots (the bucket offsets)
-//   place   the same blocks rank their rows within each slot in token order
-//           (one wave ballot per slot) and write the maps
-//   scatter X_perm[inv[t, j]] = X[t], one wave per token, 16-byte accesses
+// Permute runs in two launches (three when slots x count blocks exceed 16384),
+// all deterministic:
+//   count          a block of 256 tokens counts its rows per slot (LDS integer
+//                  atomics)
+//   [scan]         for large tables, one block turns the per-block counts into
+//                  global row positions: a wave scan per slot over the blocks,
+//                  then an exclusive scan over the slots (the bucket offsets)
+//   place+scatter  a block of 32 tokens ranks its rows within each slot in
+//                  token order, writes the maps and copies X[t] to every row t
+//                  opens (16-byte accesses, the row loads issued first); for
+//                  small tables it sums the count table itself
 // Combine and the two backward gathers run one wave per token.
 #include "common.hpp"
 
@@ -16,6 +19,10 @@ namespace fm {
 namespace {
 
 constexpr int PM_TOK = 256;   // tokens (threads) per block of count/place
+constexpr int PM_SMAX = 512;  // slots count and place support
+constexpr int PM_FUSE = 16384;  // place sums the count table itself up to this many entries
+constexpr int PS_TOK = 32;      // tokens per block of place + scatter
+constexpr int PS_THREADS = 512;
 
 template <int KMAX>
 struct TokenSlots {
@@ -55,7 +62,7 @@ template <int KMAX>
 __global__ __launch_bounds__(PM_TOK) void k_perm_count(const int32_t* __restrict__ idx,
                                                     const int32_t* __restrict__ emap, int T, int k,
                                                     int S, int32_t* __restrict__ bc, int nblk) {
-  __shared__ int cnt[512];
+  __shared__ int cnt[PM_SMAX];
   for (int s = threadIdx.x; s < S; s += blockDim.x) cnt[s] = 0;
   __syncthreads();
   const int t = blockIdx.x * PM_TOK + threadIdx.x;
@@ -107,98 +114,189 @@ __global__ __launch_bounds__(1024) void k_perm_scan(int32_t* __restrict__ bc, in
   for (size_t i = threadIdx.x; i < (size_t)S * nblk; i += blockDim.x) bc[i] += tot[i / nblk];
 }
 
-template <int KMAX>
-__global__ __launch_bounds__(PM_TOK) void k_perm_place(const int32_t* __restrict__ idx,
-                                                    const float* __restrict__ gate,
-                                                    const int32_t* __restrict__ emap, int T, int k,
-                                                    int S, const int32_t* __restrict__ bc, int nblk,
-                                                    int32_t* __restrict__ perm_token,
-                                                    float* __restrict__ perm_gate,
-                                                    int32_t* __restrict__ inv) {
-  __shared__ int wcnt[PM_TOK / 64][512];
-  const int lane = lane_id(), wave = threadIdx.x >> 6;
-  const int t = blockIdx.x * PM_TOK + threadIdx.x;
-  const bool valid = t < T;
+// Places the rows of 32 tokens and copies them: block = 8 waves, wave w owns
+// tokens t0 + 4w .. t0 + 4w + 3.
+//   1. every wave starts loading the first 4 KB of its four rows (they do not
+//      depend on the maps), while the first 256 threads take the slots of the
+//      count block's tokens up to the end of this block;
+//   2. the rows the count block's earlier tokens open are counted per slot (LDS
+//      integer atomics); this block's own tokens OR their bit into one 64-bit
+//      mask per slot, so a row's rank among them is a popcount (order-free);
+//      with SCAN the block also folds the count table into the slot totals and
+//      the rows of the count blocks before its own (and block 0 writes the
+//      bucket offsets), otherwise bc already holds those positions;
+//   3. the maps are written and each row is stored at every position its token
+//      opens.
+template <int KMAX, bool SCAN>
+__global__ __launch_bounds__(PS_THREADS) void k_place_scatter(
+    const int32_t* __restrict__ idx, const float* __restrict__ gate, const int32_t* __restrict__ emap,
+    int T, int k, int S, const int32_t* __restrict__ bc, int nblk, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ perm_token, float* __restrict__ perm_gate, int32_t* __restrict__ inv,
+    const char* __restrict__ X, int row_bytes, char* __restrict__ Xp) {
+  constexpr int NTW = PS_TOK / (PS_THREADS / 64);   // tokens per wave
+  constexpr int U = 4;                              // 16-byte chunks per lane and row per pass
+  __shared__ unsigned long long msk[PM_SMAX];       // this block's tokens, one bit each, per slot
+  __shared__ int pre[PM_SMAX];                      // rows of the count block's earlier tokens
+  __shared__ int base[PM_SMAX];                     // this block's first row in each slot
+  __shared__ int tot[SCAN ? PM_SMAX : 1];           // rows of each slot over all tokens
+  __shared__ int posl[PS_TOK][KMAX];                // row of each choice that opens one, else -1
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
+  const int t0 = blockIdx.x * PS_TOK;
+  const int grp = t0 / PM_TOK;
+  // 1. first pass of this wave's rows
+  u32x4_t v[NTW][U];
+#pragma unroll
+  for (int x = 0; x < NTW; ++x) {
+    const int t = t0 + wave * NTW + x;
+    const char* src = X + (size_t)t * row_bytes;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int c = (lane + 64 * u) * 16;
+      if (t < T && c < row_bytes) v[x][u] = ld16(src + c);
+    }
+  }
+  const int tg = grp * PM_TOK + tid;
+  const bool mine = tid < PM_TOK && tg >= t0 && tg < t0 + PS_TOK && tg < T;
+  const bool earlier = tid < PM_TOK && tg < t0;
   TokenSlots<KMAX> ts;
-  if (valid) {
-    token_slots<KMAX>(idx, emap, t, k, ts);
+  if (mine || earlier) {
+    token_slots<KMAX>(idx, emap, tg, k, ts);
   } else {
 #pragma unroll
     for (int j = 0; j < KMAX; ++j) { ts.s[j] = -1; ts.first[j] = false; ts.owner[j] = j; }
   }
-  int rank[KMAX];
-#pragma unroll
-  for (int j = 0; j < KMAX; ++j) rank[j] = 0;
-  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int s = 0; s < S; ++s) {
-    bool has = false;
-#pragma unroll
-    for (int j = 0; j < KMAX; ++j) has |= ts.first[j] && ts.s[j] == s;
-    const uint64_t m = __ballot(has);
-    if (lane == 0) wcnt[wave][s] = __popcll(m);
-    const int r = __popcll(m & lt);
-#pragma unroll
-    for (int j = 0; j < KMAX; ++j)
-      if (ts.first[j] && ts.s[j] == s) rank[j] = r;
-  }
-  __syncthreads();
-  if (!valid) return;
-  int pos[KMAX];
-#pragma unroll
-  for (int j = 0; j < KMAX; ++j) {
-    pos[j] = 0;
-    if (ts.first[j]) {
-      const int s = ts.s[j];
-      int base = bc[(size_t)s * nblk + blockIdx.x];
-      for (int w = 0; w < wave; ++w) base += wcnt[w][s];
-      pos[j] = base + rank[j];
-    }
-  }
   float g[KMAX];
 #pragma unroll
-  for (int j = 0; j < KMAX; ++j) g[j] = j < k ? gate[(size_t)t * k + j] : 0.f;
+  for (int j = 0; j < KMAX; ++j) g[j] = (mine && j < k) ? gate[(size_t)tg * k + j] : 0.f;
+  const int n = SCAN ? S * nblk : 0;
+  int cv[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = u * PS_THREADS + tid;
+    cv[u] = i < n ? bc[i] : 0;
+  }
+  for (int s = tid; s < S; s += PS_THREADS) {
+    msk[s] = 0ull;
+    pre[s] = 0;
+    if (SCAN) tot[s] = 0;
+    base[s] = SCAN ? 0 : bc[(size_t)s * nblk + grp];
+  }
+  __syncthreads();
+  // 2. counts and masks
+  const int me = tg - t0;
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) {
     if (!ts.first[j]) continue;
-    float sum = 0.f;                 // gates of every choice folded into this row, j order
-#pragma unroll
-    for (int i = 0; i < KMAX; ++i)
-      if (i < k && ts.s[i] == ts.s[j]) sum += g[i];
-    perm_token[pos[j]] = t;
-    perm_gate[pos[j]] = sum;
+    if (earlier) atomicAdd(&pre[ts.s[j]], 1);
+    else atomicOr(&msk[ts.s[j]], 1ull << me);
   }
+  for (int i0 = 0; i0 < n; i0 += 4 * PS_THREADS) {
+    if (i0 > 0) {
 #pragma unroll
-  for (int j = 0; j < KMAX; ++j) {
-    if (j >= k) continue;
-    int p = 0;
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * PS_THREADS + tid;
+        cv[u] = i < n ? bc[i] : 0;
+      }
+    }
 #pragma unroll
-    for (int i = 0; i < KMAX; ++i)
-      if (i == ts.owner[j]) p = pos[i];
-    inv[(size_t)t * k + j] = ts.first[j] ? p : -2 - p;
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * PS_THREADS + tid;
+      if (i < n && cv[u]) {
+        const int s = i / nblk;
+        atomicAdd(&tot[s], cv[u]);
+        if (i - s * nblk < grp) atomicAdd(&base[s], cv[u]);
+      }
+    }
   }
-}
-
-// X_perm[inv[t, j]] = X[t] for the rows a token opens (inv >= 0): one wave
-// per token reads its row once (four 1 KB pieces in flight) and writes it to
-// each of its rows, so X is read once instead of once per choice.
-__global__ __launch_bounds__(256) void k_scatter_rows(const char* __restrict__ X,
-                                                      const int32_t* __restrict__ inv, int T, int k,
-                                                      size_t row_bytes, char* __restrict__ Xp) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
-  const char* src = X + (size_t)t * row_bytes;
-  for (size_t c0 = (size_t)lane_id() * 16; c0 < row_bytes; c0 += 4 * 64 * 16) {
-    u32x4_t v[4];
+  __syncthreads();
+  if (SCAN) {
+    if (wave == 0) {
+      // exclusive scan of the slot totals: lane l takes a run of consecutive slots
+      const int per = (S + 63) / 64, s0 = min(S, lane * per), s1 = min(S, s0 + per);
+      int loc = 0;
+      for (int s = s0; s < s1; ++s) loc += tot[s];
+      int inc = loc;
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (c0 + u * 1024 < row_bytes) v[u] = ld16(src + c0 + u * 1024);
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(inc, off);
+        if (lane >= off) inc += y;
+      }
+      int run = inc - loc;
+      for (int s = s0; s < s1; ++s) {
+        base[s] += run + pre[s];
+        if (blockIdx.x == 0) offsets[s] = run;
+        run += tot[s];
+      }
+      if (blockIdx.x == 0 && lane == 63) offsets[S] = inc;
+    }
+  } else {
+    for (int s = tid; s < S; s += PS_THREADS) base[s] += pre[s];
+  }
+  __syncthreads();
+  // 3. maps, then rows
+  if (mine) {
+    const unsigned long long lt = (1ull << me) - 1ull;
+    int pos[KMAX];
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      pos[j] = 0;
+      if (ts.first[j]) pos[j] = base[ts.s[j]] + __popcll(msk[ts.s[j]] & lt);
+    }
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (!ts.first[j]) continue;
+      float sum = 0.f;                 // gates of every choice folded into this row, j order
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i)
+        if (i < k && ts.s[i] == ts.s[j]) sum += g[i];
+      perm_token[pos[j]] = tg;
+      perm_gate[pos[j]] = sum;
+    }
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      posl[me][j] = ts.first[j] ? pos[j] : -1;
+      if (j >= k) continue;
+      int p = 0;
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i)
+        if (i == ts.owner[j]) p = pos[i];
+      inv[(size_t)tg * k + j] = ts.first[j] ? p : -2 - p;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < NTW; ++x) {
+    const int tl = wave * NTW + x, t = t0 + tl;
+    if (t >= T) break;
     for (int j = 0; j < k; ++j) {
-      const int p = inv[(size_t)t * k + j];
+      const int p = posl[tl][j];
       if (p < 0) continue;
       char* dst = Xp + (size_t)p * row_bytes;
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (c0 + u * 1024 < row_bytes) st16(dst + c0 + u * 1024, v[u]);
+      for (int u = 0; u < U; ++u) {
+        const int c = (lane + 64 * u) * 16;
+        if (c < row_bytes) st16(dst + c, v[x][u]);
+      }
+    }
+    // rows longer than one pass
+    const char* src = X + (size_t)t * row_bytes;
+    for (int c0 = 64 * U * 16; c0 < row_bytes; c0 += 64 * U * 16) {
+      u32x4_t w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = c0 + (lane + 64 * u) * 16;
+        if (c < row_bytes) w[u] = ld16(src + c);
+      }
+      for (int j = 0; j < k; ++j) {
+        const int p = posl[tl][j];
+        if (p < 0) continue;
+        char* dst = Xp + (size_t)p * row_bytes;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int c = c0 + (lane + 64 * u) * 16;
+          if (c < row_bytes) st16(dst + c, w[u]);
+        }
+      }
     }
   }
 }
@@ -425,15 +523,20 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
                      nblk)
   FM_KSWITCH(k, FM_PC)
 #undef FM_PC
-  hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(1024), 0, st, bc, nblk, S_routed, offsets);
-#define FM_PP(KM)                                                                                   \
-  hipLaunchKernelGGL(k_perm_place<KM>, dim3(nblk), dim3(PM_TOK), 0, st, idx, gate, expert_map, T, k, \
-                     S_routed, bc, nblk, perm_token, perm_gate, inv)
+  const bool fuse = (long long)nblk * S_routed <= PM_FUSE;
+  if (!fuse) hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(1024), 0, st, bc, nblk, S_routed, offsets);
+  const int row_bytes = d * esize(dtype);
+#define FM_PP(KM)                                                                                          \
+  if (fuse)                                                                                                \
+    hipLaunchKernelGGL((k_place_scatter<KM, true>), dim3(cdiv(T, PS_TOK)), dim3(PS_THREADS), 0, st, idx,   \
+                       gate, expert_map, T, k, S_routed, bc, nblk, offsets, perm_token, perm_gate, inv,    \
+                       (const char*)X, row_bytes, (char*)X_perm);                                          \
+  else                                                                                                     \
+    hipLaunchKernelGGL((k_place_scatter<KM, false>), dim3(cdiv(T, PS_TOK)), dim3(PS_THREADS), 0, st, idx,  \
+                       gate, expert_map, T, k, S_routed, bc, nblk, offsets, perm_token, perm_gate, inv,    \
+                       (const char*)X, row_bytes, (char*)X_perm)
   FM_KSWITCH(k, FM_PP)
 #undef FM_PP
-  const size_t row_bytes = (size_t)d * esize(dtype);
-  hipLaunchKernelGGL(k_scatter_rows, dim3(cdiv(T, 4)), dim3(256), 0, st, (const char*)X, inv, T, k, row_bytes,
-                     (char*)X_perm);
   return check_launch("moe_permute");
 }
 
