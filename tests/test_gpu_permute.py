@@ -1,8 +1,8 @@
 """Gate re-routing and permutation (Section 7) alone, through the C ABI, against
 the oracle's maps, bit-exact: offsets, perm_token and inv exactly, perm_gate to
 fp32 summation order, X_perm rows bit for bit.  The shapes reach both ways the
-entry point builds the maps (each block summing the per-block count table
-itself up to 256 blocks of 256 tokens, a separate scan launch beyond), the
+entry point builds the maps (each block summing the slots x count-blocks table
+itself up to 16384 entries, a separate scan launch beyond), the
 largest slot count (512), slot maps that fold several experts into one slot (a
 token's choices merged into one row), maps that leave slots empty, and the
 largest k."""
