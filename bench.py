@@ -291,8 +291,8 @@ def layer_merging(reps=3, B_non=840, r=16, n_classes=32, mix=0.6, max_iter=100):
 def profiling_stack(reps=3):
     """The quantised profiling pass of Section 4.1 over the 28-layer
     DeepSeek-MoE stack (64 experts, d = 2048, I = 1408, top-6, T = 4096 tokens):
-    per layer int8 routing with the histogram, the layer's experts dequantised
-    from int8, permute, grouped SwiGLU forward, combine and the residual.  The
+    per layer int8 routing with the histogram, permute, the grouped SwiGLU
+    forward straight from the int8 expert codes, combine and the residual.  The
     weights are drawn on the GPU (torch's seeded generator, the workload's
     distributions) and quantised once; the pass is timed with HIP events per
     stage, median over `reps` passes after one warm-up."""

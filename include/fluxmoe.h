@@ -325,6 +325,37 @@ int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const void* X_perm
                            void* ws, size_t ws_bytes, void* stream);
 size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int T, int k);
 
+/* moe_grouped_swiglu_fwd_q8: the forward of the quantised profiling model
+ * (Section 4.1: a low-bit copy of the experts decides nothing but which
+ * experts the next layers see).  Expert weights are int8 codes with one fp32
+ * scale per row, W = diag(s) Q as moe_quantize_int8 writes them; activations
+ * are bf16.  Per slot, with the scales applied to the fp32 products:
+ *   H = silu(s_g * (X_s Q_gate^T)) * (s_u * (X_s Q_up^T)),  O = s_d * (H Q_down^T)
+ * (s_* scale output columns).  The codes are widened exactly to bf16 inside the
+ * GEMM; no dequantised copy of the weights is made.  Rows, offsets, X, X_perm,
+ * H [R_tot, I] and O [R_tot, d] as in moe_grouped_swiglu_fwd (bf16); A_g and
+ * A_u are not written.  Limits: d and I multiples of 16; the struct's tables
+ * are DEVICE arrays of S_routed + S_shared device pointers:
+ *   q_gate, q_up [S] -> [I,d] int8;  q_down [S] -> [d,I] int8;
+ *   s_gate, s_up [S] -> [I] fp32;    s_down [S] -> [d] fp32.
+ */
+typedef struct moe_layer_q8 {
+  int d;
+  int I;
+  int S_routed;
+  int S_shared;
+  const int8_t* const* q_gate;
+  const int8_t* const* q_up;
+  const int8_t* const* q_down;
+  const float* const* s_gate;
+  const float* const* s_up;
+  const float* const* s_down;
+} moe_layer_q8;
+int moe_grouped_swiglu_fwd_q8(const moe_layer_q8* L, const void* X, const void* X_perm,
+                              const int32_t* offsets, int T, int k, void* H, void* O,
+                              void* ws, size_t ws_bytes, void* stream);
+size_t moe_grouped_swiglu_fwd_q8_workspace_size(const moe_layer_q8* L, int T, int k);
+
 /* moe_unpermute: the gate-weighted combine of the expert outputs
  *   Y[t] = sum_{j: inv[t,j] >= 0} perm_gate[inv[t,j]] * O[inv[t,j]]
  *          + sum_{shared i} O[T*k + i*T + t]              (fp32 accumulation)

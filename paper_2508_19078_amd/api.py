@@ -34,6 +34,12 @@ class moe_layer(ctypes.Structure):
                 ("dw_gate", _vp), ("dw_up", _vp), ("dw_down", _vp)]
 
 
+class moe_layer_q8(ctypes.Structure):
+    _fields_ = [("d", _c_int), ("I", _c_int), ("S_routed", _c_int), ("S_shared", _c_int),
+                ("q_gate", _vp), ("q_up", _vp), ("q_down", _vp), ("s_gate", _vp), ("s_up", _vp),
+                ("s_down", _vp)]
+
+
 # name -> (restype, argtypes)
 _SIGS = {
     "moe_last_error": (ctypes.c_char_p, []),
@@ -54,6 +60,8 @@ _SIGS = {
     "moe_grouped_swiglu_fwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
                                         _c_size, _vp]),
     "moe_grouped_swiglu_fwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
+    "moe_grouped_swiglu_fwd_q8": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp]),
+    "moe_grouped_swiglu_fwd_q8_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
     "moe_unpermute": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
     "moe_unpermute_bwd": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp]),
     "moe_grouped_swiglu_bwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
@@ -286,6 +294,15 @@ def moe_grouped_swiglu_fwd(layer, X, X_perm, offsets, T, k, A_g, A_u, H, O, ws, 
                  ptr(A_u), ptr(H), ptr(O), ptr(ws), ws.numel() * ws.element_size(), stream_ptr(stream))
 
 
+def moe_grouped_swiglu_fwd_q8_workspace_size(layer, T, k) -> int:
+    return lib().moe_grouped_swiglu_fwd_q8_workspace_size(ptr(layer), T, k)
+
+
+def moe_grouped_swiglu_fwd_q8(layer, X, X_perm, offsets, T, k, H, O, ws, stream=None):
+    return _call("moe_grouped_swiglu_fwd_q8", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(H),
+                 ptr(O), ptr(ws), ws.numel() * ws.element_size(), stream_ptr(stream))
+
+
 def moe_unpermute(layer, O, inv, perm_gate, T, k, Y, stream=None):
     return _call("moe_unpermute", ptr(layer), ptr(O), ptr(inv), ptr(perm_gate), T, k, ptr(Y),
                  stream_ptr(stream))
@@ -345,3 +362,22 @@ class LayerTables:
         self.struct = moe_layer(d, I, dtype_code(dtype), S_routed, S_shared, ptr(self.w_gate),
                                 ptr(self.w_up), ptr(self.w_down), ptr(self.dw_gate), ptr(self.dw_up),
                                 ptr(self.dw_down))
+
+
+class LayerTablesQ8:
+    """Device pointer tables of a layer's int8 experts and the moe_layer_q8
+    struct.  q_*: per-slot int8 code tensors (routed slots, then shared);
+    s_*: the matching per-row fp32 scales."""
+
+    def __init__(self, d: int, I: int, S_routed: int, S_shared: int, q_gate, q_up, q_down, s_gate, s_up,
+                 s_down, device="cuda"):
+        S = S_routed + S_shared
+
+        def table(x):
+            vals = [ptr(t) for t in x]
+            assert len(vals) == S and all(v for v in vals)
+            return torch.tensor(vals, dtype=torch.int64, device=device)
+
+        self.keep = [q_gate, q_up, q_down, s_gate, s_up, s_down]
+        self.tabs = [table(x) for x in self.keep]
+        self.struct = moe_layer_q8(d, I, S_routed, S_shared, *[ptr(t) for t in self.tabs])

@@ -663,6 +663,106 @@ __global__ __launch_bounds__(CB::THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
   }
 }
 
+// ------------------------------ quantised forward (int8 weights, bf16 X) ----
+
+struct Q8Ptrs {
+  const int8_t* const* qg;
+  const int8_t* const* qu;
+  const int8_t* const* qd;
+  const float* const* sg;
+  const float* const* su;
+  const float* const* sd;
+};
+
+// The bf16 tile shape with int8 B slabs (16 KB instead of 32 KB each).
+using CQ = B16Cfg<256, 256, 2, 4, 64, 3, 2, 1>;
+
+// Four consecutive row scales from col (clamped so that the four stay inside
+// the row count n, n >= 4; columns past n are never stored).
+__device__ __forceinline__ f32x4_t scale4(const float* s, int col, int n) {
+  const int c = min(col, n - 4);
+  return f32x4_t{s[c], s[c + 1], s[c + 2], s[c + 3]};
+}
+
+// H = silu(s_g (X_s Q_g^T)) (s_u (X_s Q_u^T)) with int8 Q_g, Q_u interleaved
+// in 32-row blocks as in kb_gate_up; the row scales of the weights scale the
+// output columns.  Only H is written (no backward follows this forward).
+__global__ __launch_bounds__(CQ::THREADS) void kq_gate_up(Q8Ptrs W, cbp X, cbp Xp, RowArgs ra, bf16* H) {
+  __shared__ __align__(16) char lds[CQ::LDS];
+  const int d = ra.d, I = ra.I, NT = (I + CQ::RB / 2 - 1) / (CQ::RB / 2);
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * CQ::RA, n0 = rt.n * (CQ::RB / 2);
+    const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, sr.nrows - m0, d};
+    // byte pointers in the B16Src fields: ld and K count bytes
+    const B16Src B{(cbp)(ld_scalar(W.qg + rt.s) + (size_t)n0 * d), (cbp)(ld_scalar(W.qu + rt.s) + (size_t)n0 * d),
+                   d, I - n0, d};
+    B16Acc<CQ::MI, CQ::NJ> acc;
+    acc.zero();
+    b16_gemm<CQ, true, true, false, true>(A, B, d, (FM_LDS char*)lds, acc);
+    const float* sgp = ld_scalar(W.sg + rt.s) + n0;
+    const float* sup = ld_scalar(W.su + rt.s) + n0;
+    using SG = Stage<bf16, CQ::RB / 2>;
+    FM_LDS char* sg = (FM_LDS char*)lds;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    const int rows = sr.nrows - m0, cols = I - n0;
+#pragma unroll
+    for (int jj = 0; jj < CQ::NJ / 2; ++jj)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = deinter(b16_coord<CQ>(0, 2 * jj, q).col4);
+        const f32x4_t cg = scale4(sgp, col, cols), cu = scale4(sup, col, cols);
+#pragma unroll
+        for (int i = 0; i < CQ::MI; ++i) {
+          const AccCoord c = b16_coord<CQ>(i, 2 * jj, q);
+          const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
+          f32x4_t h;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float a = ag[r] * cg[r];
+            h[r] = a * sigm_fast(a) * (u[r] * cu[r]);
+          }
+          SG::put4(sg, c.row, col, h);
+        }
+      }
+    barrier_lds_writes();
+    SG::template copy_out<CQ::RA, CQ::THREADS>(sg, H + ob * I + n0, I, rows, cols);
+    barrier_lds();
+  }
+}
+
+// O = s_d (H Q_d^T) with int8 Q_d.
+__global__ __launch_bounds__(CQ::THREADS) void kq_down(Q8Ptrs W, cbp H, RowArgs ra, bf16* O) {
+  __shared__ __align__(16) char lds[CQ::LDS];
+  const int d = ra.d, I = ra.I, NT = (d + CQ::RB - 1) / CQ::RB;
+  const TileRange tr = row_range(ra, NT);
+  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
+    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+    const int m0 = rt.m * CQ::RA, n0 = rt.n * CQ::RB;
+    const size_t ob = (size_t)(sr.orow0 + m0);
+    const B16Src A{H + ob * I, nullptr, I, sr.nrows - m0, I};
+    const B16Src B{(cbp)(ld_scalar(W.qd + rt.s) + (size_t)n0 * I), nullptr, I, d - n0, I};
+    B16Acc<CQ::MI, CQ::NJ> acc;
+    acc.zero();
+    b16_gemm<CQ, true, true>(A, B, I, (FM_LDS char*)lds, acc);
+    const float* sdp = ld_scalar(W.sd + rt.s) + n0;
+#pragma unroll
+    for (int j = 0; j < CQ::NJ; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f32x4_t c4 = scale4(sdp, b16_coord<CQ>(0, j, q).col4, d - n0);
+#pragma unroll
+        for (int i = 0; i < CQ::MI; ++i)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) acc.v[i][j][4 * q + r] *= c4[r];
+      }
+    b16_store_staged<CQ>(acc, (FM_LDS char*)lds, O + ob * d + n0, d, sr.nrows - m0, d - n0);
+  }
+}
+
 // O = H W_down^T
 __global__ __launch_bounds__(CB::THREADS) void kb_down(LayerPtrs<bf16> W, cbp H, RowArgs ra, bf16* O) {
   __shared__ __align__(16) char lds[CB::LDS];
@@ -1057,6 +1157,48 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
   }
 #undef FM_FWD
   return check_launch("moe_grouped_swiglu_fwd");
+}
+
+extern "C" size_t moe_grouped_swiglu_fwd_q8_workspace_size(const moe_layer_q8* L, int T, int k) {
+  if (!L || T < 0 || k <= 0) return 0;
+  return sched_bytes(L->S_routed + L->S_shared);
+}
+
+extern "C" int moe_grouped_swiglu_fwd_q8(const moe_layer_q8* L, const void* X, const void* X_perm,
+                                         const int32_t* offsets, int T, int k, void* H, void* O, void* ws,
+                                         size_t ws_bytes, void* stream) {
+  clear_error();
+  if (!L) return fail(MOE_ERR_ARG, "layer must not be NULL");
+  if (L->d <= 0 || L->I <= 0) return fail(MOE_ERR_ARG, "layer d=%d I=%d", L->d, L->I);
+  if (L->d % 16 || L->I % 16)
+    return fail(MOE_ERR_UNSUPPORTED, "int8 layer d=%d I=%d must be multiples of 16", L->d, L->I);
+  if (L->S_routed < 0 || L->S_shared < 0 || L->S_routed + L->S_shared < 1 || L->S_routed > 512 ||
+      L->S_shared > 511)
+    return fail(MOE_ERR_ARG, "layer S_routed=%d S_shared=%d", L->S_routed, L->S_shared);
+  FM_TRY(need(L->q_gate, "layer q_gate")); FM_TRY(need(L->q_up, "layer q_up"));
+  FM_TRY(need(L->q_down, "layer q_down")); FM_TRY(need(L->s_gate, "layer s_gate"));
+  FM_TRY(need(L->s_up, "layer s_up")); FM_TRY(need(L->s_down, "layer s_down"));
+  if (T < 0 || k <= 0 || k > 16) return fail(MOE_ERR_ARG, "T=%d k=%d", T, k);
+  if (T == 0) return MOE_OK;
+  FM_TRY(need(X, "X")); FM_TRY(need(offsets, "offsets")); FM_TRY(need(H, "H")); FM_TRY(need(O, "O"));
+  FM_TRY(need(ws, "ws"));
+  if (L->S_routed > 0) FM_TRY(need(X_perm, "X_perm"));
+  FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(X_perm, "X_perm")); FM_TRY(need_aligned(H, "H"));
+  FM_TRY(need_aligned(O, "O")); FM_TRY(need_aligned(ws, "ws"));
+  if (ws_bytes < moe_grouped_swiglu_fwd_q8_workspace_size(L, T, k))
+    return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
+                moe_grouped_swiglu_fwd_q8_workspace_size(L, T, k));
+  hipStream_t st = as_stream(stream);
+  const int S = L->S_routed + L->S_shared;
+  const Sched sc = sched_at(ws, S);
+  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, CQ::RA,
+                     (float* const*)nullptr, sc.mbase, sc.wbase, sc.dorder, sc.queues);
+  const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
+  const Q8Ptrs W{L->q_gate, L->q_up, L->q_down, L->s_gate, L->s_up, L->s_down};
+  const dim3 grid(persistent_blocks()), block(CQ::THREADS);
+  hipLaunchKernelGGL(kq_gate_up, grid, block, 0, st, W, (cbp)X, (cbp)X_perm, ra, (bf16*)H);
+  hipLaunchKernelGGL(kq_down, grid, block, 0, st, W, (cbp)H, ra, (bf16*)O);
+  return check_launch("moe_grouped_swiglu_fwd_q8");
 }
 
 extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const void* X_perm,

@@ -50,17 +50,20 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // Tile configuration: RA x RB block tile, WM x WN waves, BK k per slab,
 // separate LDS rings of NSA slabs for A and NSB slabs for B (NSA = NSB + 1: the
 // A operand, the one that streams, gets one more slab of latency tolerance).
-template <int RA_, int RB_, int WM_, int WN_, int BK_, int NSA_, int NSB_> struct B16Cfg {
-  static constexpr int RA = RA_, RB = RB_, WM = WM_, WN = WN_, BK = BK_, NSA = NSA_, NSB = NSB_;
+// BE = bytes per B element: 2 (bf16) or 1 (int8 codes, K-contiguous only,
+// widened exactly to bf16 as fragments are read).
+template <int RA_, int RB_, int WM_, int WN_, int BK_, int NSA_, int NSB_, int BE_ = 2> struct B16Cfg {
+  static constexpr int RA = RA_, RB = RB_, WM = WM_, WN = WN_, BK = BK_, NSA = NSA_, NSB = NSB_, BE = BE_;
   static constexpr int NW = WM * WN, THREADS = 64 * NW;
   static constexpr int TM = RA / WM, TN = RB / WN;    // wave sub-tile
   static constexpr int MI = TM / 32, NJ = TN / 32;    // MFMA tiles per wave
   static constexpr int KS = BK / 16;                  // MFMA k-steps per slab
-  static constexpr int A_BYTES = RA * BK * 2, B_BYTES = RB * BK * 2;
+  static constexpr int A_BYTES = RA * BK * 2, B_BYTES = RB * BK * BE;
   static constexpr int B_BASE = NSA * A_BYTES;        // B ring follows the A ring
   static constexpr int LDS = NSA * A_BYTES + NSB * B_BYTES;
   static constexpr int A_INS = RA * BK * 2 / 1024 / NW;   // DMA instructions per wave and slab
-  static constexpr int B_INS = RB * BK * 2 / 1024 / NW;
+  static constexpr int B_INS = RB * BK * BE / 1024 / NW;
+  static_assert(BE == 1 || BE == 2, "bf16 or int8 B");
   static_assert((NW == 4 || NW == 8) && TM % 32 == 0 && TN % 32 == 0, "4 or 8 waves of 32-multiples");
   static_assert(BK == 64, "slab depth: two 32-k halves per slab");
   static_assert(A_INS >= 1 && B_INS >= 1 && KS % 2 == 0, "whole DMA instructions per wave");
@@ -298,6 +301,87 @@ template <bool KC, int R, int NB> struct B16Frag {
   }
 };
 
+// int8 K-contiguous operand (the weights of the quantised forward), logical
+// [R rows][K] bytes with the same row / interleave conventions as B16Src (ld
+// and K in bytes; the pointers are byte pointers).  A slab is R rows x 64 k =
+// 64 bytes per row, stored [R][64 B] with the 16-byte chunk index XOR-swizzled
+// by (row >> 2) & 3; instruction ins moves rows 16 ins + [0, 16), 64 bytes of
+// each (half of a 128-byte line: the other half belongs to the next slab).
+template <int R, int NI, bool INTER> struct I8Dma {
+  const char* base[NI];      // uniform
+  uint32_t off[NI];          // per lane
+  size_t step;
+
+  __device__ __forceinline__ static const char* matrix(const B16Src& s, int ins) {
+    return (const char*)((INTER && ((ins >> 1) & 1)) ? s.p2 : s.p);   // 32-row block ins / 2
+  }
+  __device__ __forceinline__ static int phys_row(int r) { return INTER ? 32 * (r >> 6) + (r & 31) : r; }
+  __device__ __forceinline__ static uint32_t lane_off(const B16Src& s, int ins, int lane, int k0) {
+    const int a = 16 * ins + (lane >> 2);
+    const int b = 16 * ((lane & 3) ^ swz_kc(a));
+    // K - 16 >= k0: K is a multiple of 16 and the slab starts below K
+    return (uint32_t)((size_t)min(phys_row(a), s.rows - 1) * s.ld + min(b, s.K - 16 - k0));
+  }
+  __device__ __forceinline__ void init(const B16Src& s) {
+    const int lane = lane_id(), wave = wave_id();
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+      const int ins = wave * NI + u;
+      base[u] = matrix(s, ins);
+      off[u] = lane_off(s, ins, lane, 0);
+    }
+    step = 64;
+  }
+  __device__ __forceinline__ void issue_full(int slab, FM_LDS char* tile) const { issue_part<0, NI>(slab, tile); }
+  template <int U0, int U1>
+  __device__ __forceinline__ void issue_part(int slab, FM_LDS char* tile) const {
+    const int wave = wave_id();
+    const size_t adv = step * (size_t)slab;
+#pragma unroll
+    for (int u = U0; u < U1; ++u) dma16s(base[u] + adv, off[u], tile + (wave * NI + u) * 1024);
+  }
+  __device__ __forceinline__ void issue_tail(const B16Src& s, int k0, FM_LDS char* tile) const {
+    const int lane = lane_id_here(), wave = wave_id();
+#pragma unroll
+    for (int u = 0; u < NI; ++u) {
+      const int ins = wave * NI + u;
+      dma16s(matrix(s, ins) + k0, lane_off(s, ins, lane, k0), tile + ins * 1024);
+    }
+  }
+};
+
+// Eight int8 codes -> eight bf16 (exact: |q| <= 128 has at most 8 significant bits).
+__device__ __forceinline__ bf16x8_t widen_i8x8(u32x2_t raw) {
+  u32x4_t v;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t x = raw[i >> 1];
+    const int sh = (i & 1) * 16;
+    const float lo = (float)(int8_t)((x >> sh) & 0xFF);
+    const float hi = (float)(int8_t)((x >> (sh + 8)) & 0xFF);
+    v[i] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+  }
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// Fragments of an int8 slab: lane l holds row r0 + l % 32 and k 16 ks +
+// 8 (l / 32) + 0..7, i.e. 8 bytes of chunk ks (swizzled), widened to bf16.
+// Sixteen consecutive rows read 16 distinct 2-bank groups.
+template <int R, int NB> struct I8Frag {
+  uint32_t off[NB];
+  __device__ __forceinline__ void init(int row0) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int r = row0 + i * 32 + (lane & 31);
+      off[i] = (uint32_t)(r * 64 + (swz_kc(r) << 4) + 8 * (lane >> 5));
+    }
+  }
+  __device__ __forceinline__ bf16x8_t read(const FM_LDS char* tile, int i, int ks) const {
+    return widen_i8x8(*(const FM_LDS u32x2_t*)(tile + (off[i] ^ (uint32_t)(ks << 4))));
+  }
+};
+
 // Zeroes the k >= K elements of an A fragment (k-step ks of the slab at k0).
 __device__ __forceinline__ bf16x8_t b16_mask_k(bf16x8_t f, int k0, int ks, int K) {
   const int kf = k0 + ks * 16 + 8 * (lane_id() >> 5);
@@ -423,8 +507,10 @@ __device__ __forceinline__ void barrier_lds_writes() {
 // The DMA side of one product: slab issue into the two rings.
 template <class C, bool AKC, bool BKC, bool AI, bool BI> struct B16Pipe {
   static constexpr int BK = C::BK, NSA = C::NSA, NSB = C::NSB;
+  static_assert(C::BE == 2 || BKC, "int8 B is K-contiguous");
+  using DmaB = std::conditional_t<C::BE == 1, I8Dma<C::RB, C::B_INS, BI>, B16Dma<BKC, C::RB, C::B_INS, BI>>;
   B16Dma<AKC, C::RA, C::A_INS, AI> da;
-  B16Dma<BKC, C::RB, C::B_INS, BI> db;
+  DmaB db;
   const B16Src& A;
   const B16Src& B;
   FM_LDS char* lds;
@@ -486,7 +572,7 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
   const int nfull = pp.nfull;
   const int wave = wave_id();
   B16Frag<AKC, C::RA, MI> fa;
-  B16Frag<BKC, C::RB, NJ> fb;
+  std::conditional_t<C::BE == 1, I8Frag<C::RB, NJ>, B16Frag<BKC, C::RB, NJ>> fb;
   fa.init((wave % C::WM) * C::TM);
   fb.init((wave / C::WM) * C::TN);
   const auto& da = pp.da;

@@ -8,9 +8,12 @@ scales resident.  ``run`` then passes a batch through the stack, layer by
 layer, on one stream:
 
   moe_profile_route   int8 routing: histogram, top-k indices and gates
-  moe_dequant_int8    the layer's experts, dequantised into one reused buffer
-  moe_permute -> moe_grouped_swiglu_fwd -> moe_unpermute   the layer's output
-  moe_residual_add    X_{l+1} = X_l + Y_l
+  moe_permute         the layer's rows into per-expert buckets
+  moe_grouped_swiglu_fwd_q8   the experts straight from their int8 codes
+                      (bf16 activations, d and I multiples of 16); otherwise
+                      moe_dequant_int8 into one reused buffer and
+                      moe_grouped_swiglu_fwd
+  moe_unpermute, moe_residual_add   Y_l and X_{l+1} = X_l + Y_l
 
 Every value is computed by libfluxmoe; this module only owns buffers and
 orders the calls.
@@ -30,7 +33,7 @@ class QuantizedStack:
     one float dtype.  Only the int8 codes and fp32 scales are kept."""
 
     def __init__(self, layers: Sequence[dict], T: int, k: int, device: str = "cuda",
-                 record: bool = False):
+                 record: bool = False, fused: Optional[bool] = None):
         L0 = layers[0]
         self.dt = L0["wg"].dtype
         self.E, self.I, self.d = L0["wg"].shape
@@ -55,15 +58,43 @@ class QuantizedStack:
                     ql[name] = quant(lay[name])
             self.q.append(ql)
 
-        # one layer's dequantised experts, reused by every layer
+        can_fuse = self.dt == torch.bfloat16 and d % 16 == 0 and I % 16 == 0
+        self.fused = can_fuse if fused is None else bool(fused)
+        if self.fused and not can_fuse:
+            raise ValueError("the int8 forward needs bf16 activations and d, I multiples of 16")
         z = lambda *shape, dtype=self.dt: torch.empty(*shape, dtype=dtype, device=dev)
-        self.Dg, self.Du, self.Dd = z(E, I, d), z(E, I, d), z(E, d, I)
-        if n_sh:
-            self.Sg, self.Su, self.Sd = z(n_sh, I, d), z(n_sh, I, d), z(n_sh, d, I)
-        wg = [self.Dg[e] for e in range(E)] + ([self.Sg[i] for i in range(n_sh)] if n_sh else [])
-        wu = [self.Du[e] for e in range(E)] + ([self.Su[i] for i in range(n_sh)] if n_sh else [])
-        wd = [self.Dd[e] for e in range(E)] + ([self.Sd[i] for i in range(n_sh)] if n_sh else [])
-        self.tables = api.LayerTables(d, I, self.dt, E, n_sh, wg, wu, wd, device=dev)
+
+        def per_slot(ql, name, sname, rows):
+            """Per-slot codes and scales of one matrix: routed slots, then shared."""
+            out_q, out_s = [], []
+            for nm, n in ((name, E), (sname, n_sh)):
+                if n == 0:
+                    continue
+                q, sc = ql[nm]
+                out_q += [q[e] for e in range(n)]
+                out_s += [sc[e * rows:(e + 1) * rows] for e in range(n)]
+            return out_q, out_s
+        if self.fused:
+            # per-layer tables of the int8 codes and their row scales
+            self.qtables = []
+            for ql in self.q:
+                gq, gs = per_slot(ql, "wg", "sg", I)
+                uq, us = per_slot(ql, "wu", "su", I)
+                dq, ds = per_slot(ql, "wd", "sd", d)
+                self.qtables.append(api.LayerTablesQ8(d, I, E, n_sh, gq, uq, dq, gs, us, ds, device=dev))
+            # the combine reads only the layer's shape
+            self.layer = api.moe_layer(d, I, api.dtype_code(self.dt), E, n_sh, None, None, None, None, None, None)
+            ws_fwd = api.moe_grouped_swiglu_fwd_q8_workspace_size(self.qtables[0], T, k)
+        else:
+            # one layer's dequantised experts, reused by every layer
+            self.Dg, self.Du, self.Dd = z(E, I, d), z(E, I, d), z(E, d, I)
+            if n_sh:
+                self.Sg, self.Su, self.Sd = z(n_sh, I, d), z(n_sh, I, d), z(n_sh, d, I)
+            wg = [self.Dg[e] for e in range(E)] + ([self.Sg[i] for i in range(n_sh)] if n_sh else [])
+            wu = [self.Du[e] for e in range(E)] + ([self.Su[i] for i in range(n_sh)] if n_sh else [])
+            wd = [self.Dd[e] for e in range(E)] + ([self.Sd[i] for i in range(n_sh)] if n_sh else [])
+            self.layer = api.LayerTables(d, I, self.dt, E, n_sh, wg, wu, wd, device=dev)
+            ws_fwd = api.moe_grouped_swiglu_fwd_workspace_size(self.layer, T, k)
 
         R, Rt = T * k, T * (k + n_sh)
         zi = lambda *shape: torch.zeros(*shape, dtype=torch.int32, device=dev)
@@ -75,11 +106,12 @@ class QuantizedStack:
         self.perm_gate = z(R, dtype=torch.float32)
         self.X_perm = z(R, d)
         self.ws_perm = torch.empty(api.moe_permute_workspace_size(T, k, E), dtype=torch.uint8, device=dev)
-        self.A_g, self.A_u, self.H, self.O = z(Rt, I), z(Rt, I), z(Rt, I), z(Rt, d)
+        if not self.fused:
+            self.A_g, self.A_u = z(Rt, I), z(Rt, I)
+        self.H, self.O = z(Rt, I), z(Rt, d)
         self.Y = z(T, d)
         self.Xa, self.Xb = z(T, d), z(T, d)
-        self.ws_fwd = torch.empty(api.moe_grouped_swiglu_fwd_workspace_size(self.tables, T, k),
-                                  dtype=torch.uint8, device=dev)
+        self.ws_fwd = torch.empty(ws_fwd, dtype=torch.uint8, device=dev)
         self.trace: List[dict] = []
 
     def run(self, X0: torch.Tensor, mark=None) -> torch.Tensor:
@@ -93,24 +125,29 @@ class QuantizedStack:
         self.Xa.copy_(X0)
         X, Xn = self.Xa, self.Xb
         for l, ql in enumerate(self.q):
-            api.moe_dequant_int8(ql["wg"][0], ql["wg"][1], self.Dg)
-            api.moe_dequant_int8(ql["wu"][0], ql["wu"][1], self.Du)
-            api.moe_dequant_int8(ql["wd"][0], ql["wd"][1], self.Dd)
-            if self.n_sh:
-                api.moe_dequant_int8(ql["sg"][0], ql["sg"][1], self.Sg)
-                api.moe_dequant_int8(ql["su"][0], ql["su"][1], self.Su)
-                api.moe_dequant_int8(ql["sd"][0], ql["sd"][1], self.Sd)
-            mark("dequant")
+            if not self.fused:
+                api.moe_dequant_int8(ql["wg"][0], ql["wg"][1], self.Dg)
+                api.moe_dequant_int8(ql["wu"][0], ql["wu"][1], self.Du)
+                api.moe_dequant_int8(ql["wd"][0], ql["wd"][1], self.Dd)
+                if self.n_sh:
+                    api.moe_dequant_int8(ql["sg"][0], ql["sg"][1], self.Sg)
+                    api.moe_dequant_int8(ql["su"][0], ql["su"][1], self.Su)
+                    api.moe_dequant_int8(ql["sd"][0], ql["sd"][1], self.Sd)
+                mark("dequant")
             Wq, ws = ql["Wr"]
             api.moe_profile_route(X, Wq, ws, ql["bias"], k, self.counts[l], self.idx, self.gate)
             mark("route")
             api.moe_permute(X, self.idx, self.gate, None, self.E, self.offsets, self.perm_token, self.perm_gate,
                             self.inv, self.X_perm, self.ws_perm, E=self.E)
             mark("permute")
-            api.moe_grouped_swiglu_fwd(self.tables, X, self.X_perm, self.offsets, T, k, self.A_g, self.A_u,
-                                       self.H, self.O, self.ws_fwd)
+            if self.fused:
+                api.moe_grouped_swiglu_fwd_q8(self.qtables[l], X, self.X_perm, self.offsets, T, k, self.H, self.O,
+                                              self.ws_fwd)
+            else:
+                api.moe_grouped_swiglu_fwd(self.layer, X, self.X_perm, self.offsets, T, k, self.A_g, self.A_u,
+                                           self.H, self.O, self.ws_fwd)
             mark("ffn_fwd")
-            api.moe_unpermute(self.tables, self.O, self.inv, self.perm_gate, T, k, self.Y)
+            api.moe_unpermute(self.layer, self.O, self.inv, self.perm_gate, T, k, self.Y)
             api.moe_residual_add(X, self.Y, Xn)
             mark("combine")
             if self.record:

@@ -231,3 +231,31 @@ def test_profiling_stack_rejections(L):
     rc, msg = rc_and_msg(L, "moe_residual_add", FAKE, None, 16, 16, api.MOE_BF16, FAKE, None)
     assert rc == api.MOE_ERR_ARG and "Y" in msg
     assert L.moe_residual_add(None, None, 0, 16, api.MOE_BF16, None, None) == 0   # T = 0: nothing to do
+
+
+def test_quantised_forward_rejections(L):
+    def lay(d=2048, I=1408, S_r=64, S_sh=0, tabs=(FAKE,) * 6):
+        return api.moe_layer_q8(d, I, S_r, S_sh, *tabs)
+
+    def call(layer, T=4096, k=6, X=FAKE, Xp=FAKE, off=FAKE, H=FAKE, O=FAKE, ws=FAKE, ws_bytes=None):
+        if ws_bytes is None:
+            ws_bytes = L.moe_grouped_swiglu_fwd_q8_workspace_size(ctypes.byref(layer), T, k)
+        return rc_and_msg(L, "moe_grouped_swiglu_fwd_q8", ctypes.byref(layer), X, Xp, off, T, k, H, O, ws,
+                          ctypes.c_size_t(ws_bytes), None)
+
+    assert L.moe_grouped_swiglu_fwd_q8_workspace_size(ctypes.byref(lay()), 4096, 6) > 0
+    assert L.moe_grouped_swiglu_fwd_q8_workspace_size(None, 4096, 6) == 0
+    assert rc_and_msg(L, "moe_grouped_swiglu_fwd_q8", None, FAKE, FAKE, FAKE, 16, 2, FAKE, FAKE, FAKE,
+                      ctypes.c_size_t(1 << 20), None)[0] == api.MOE_ERR_ARG
+    assert call(lay(d=2040))[0] == api.MOE_ERR_UNSUPPORTED          # d % 16
+    assert call(lay(I=1400))[0] == api.MOE_ERR_UNSUPPORTED          # I % 16
+    assert call(lay(S_r=0, S_sh=0))[0] == api.MOE_ERR_ARG
+    rc, msg = call(lay(tabs=(FAKE, FAKE, FAKE, FAKE, None, FAKE)))
+    assert rc == api.MOE_ERR_ARG and "s_up" in msg
+    assert call(lay(), k=17)[0] == api.MOE_ERR_ARG
+    rc, msg = call(lay(), H=None)
+    assert rc == api.MOE_ERR_ARG and "H" in msg
+    assert call(lay(), O=MIS)[0] == api.MOE_ERR_ALIGN
+    need = L.moe_grouped_swiglu_fwd_q8_workspace_size(ctypes.byref(lay()), 4096, 6)
+    assert call(lay(), ws_bytes=need - 1)[0] == api.MOE_ERR_WORKSPACE
+    assert call(lay(), T=0, X=None, Xp=None, off=None, H=None, O=None, ws=None)[0] == api.MOE_OK   # nothing to do
