@@ -32,6 +32,9 @@
 // * An operand may interleave two matrices in 32-row blocks (gate and up
 //   weights; the two dSwiGLU gradients), so that the pairs the epilogue needs sit
 //   in one lane.  A DMA instruction always stays inside one 32-row block.
+// * With BE = 1 the B operand is int8 (the quantised forward's weight codes,
+//   K-contiguous): 64-byte slab rows, one DMA instruction per 16 rows, and each
+//   lane widens its 8 codes to bf16 (exactly) as it reads the fragment.
 // * Rows past the operand's extent read a clamped (valid) address and only feed
 //   outputs that are never stored; k past K is zeroed in the A fragments of the
 //   last slab, so the clamped B data meets zeros.
