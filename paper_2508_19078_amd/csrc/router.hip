@@ -592,7 +592,10 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
 // experts dlogit_j = g_j (dg_j - sum_i g_i dg_i) (the softmax Jacobian-vector
 // product), and dX[t] = (accumulate ? dX[t] : 0) + sum_j dlogit_j Wr[idx_j].
 // One wave per token; the k router rows of a 16-byte column chunk are loaded
-// together (Wr stays in L2); fp32 sums in j order, one rounding to T.
+// together (Wr stays in L2); fp32 sums in j order, one rounding to T.  (Staging
+// the router in LDS per 32-token block cuts the L2 reads threefold but left one
+// block of four waves per CU waiting on a serial chain of chunks: measured
+// slower.)
 template <typename T, int KMAX>
 __global__ __launch_bounds__(256) void k_route_bwd(const float* __restrict__ gate, const int32_t* __restrict__ idx,
                                                    const float* __restrict__ dgate, const T* __restrict__ Wr, int Tn,
@@ -614,27 +617,50 @@ __global__ __launch_bounds__(256) void k_route_bwd(const float* __restrict__ gat
   }
 #pragma unroll
   for (int j = 0; j < KMAX; ++j) dl[j] = g[j] * (dl[j] - inner);
-  for (int c = lane_id() * V; c < d; c += 64 * V) {
-    u32x4_t raw[KMAX];
+  // The row in groups of G 16-byte chunks per lane: the group's dX chunks (from
+  // HBM) are all requested first, and the router rows of chunk u + 1 (from L2)
+  // before chunk u is summed, so a wave waits for one HBM round trip per group
+  // instead of one per chunk.
+  constexpr int G = 4;
+  const int lane = lane_id();
+  T* xrow = dX + (size_t)t * d;
+  for (int c0 = lane * V; c0 < d; c0 += G * 64 * V) {
+    u32x4_t xr[G];
+    if (accumulate) {
+#pragma unroll
+      for (int u = 0; u < G; ++u)
+        if (c0 + u * 64 * V < d) xr[u] = ld16(xrow + c0 + u * 64 * V);
+    }
+    u32x4_t raw[2][KMAX];
 #pragma unroll
     for (int j = 0; j < KMAX; ++j)
-      if (wrow[j]) raw[j] = ld16(wrow[j] + c);
-    float acc[V];
-    if (accumulate) {
-      unpack16(ld16(dX + (size_t)t * d + c), acc, (T*)nullptr);
-    } else {
+      if (wrow[j]) raw[0][j] = ld16(wrow[j] + c0);
 #pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] = 0.f;
+    for (int u = 0; u < G; ++u) {
+      const int c = c0 + u * 64 * V;
+      if (c >= d) break;
+      if (u + 1 < G && c + 64 * V < d) {
+#pragma unroll
+        for (int j = 0; j < KMAX; ++j)
+          if (wrow[j]) raw[(u + 1) & 1][j] = ld16(wrow[j] + c + 64 * V);
+      }
+      float acc[V];
+      if (accumulate) {
+        unpack16(xr[u], acc, (T*)nullptr);
+      } else {
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j) {
+        if (!wrow[j]) continue;
+        float w[V];
+        unpack16(raw[u & 1][j], w, (T*)nullptr);
+#pragma unroll
+        for (int i = 0; i < V; ++i) acc[i] = fmaf(dl[j], w[i], acc[i]);
+      }
+      st16(xrow + c, pack16(acc, (T*)nullptr));
     }
-#pragma unroll
-    for (int j = 0; j < KMAX; ++j) {
-      if (!wrow[j]) continue;
-      float w[V];
-      unpack16(raw[j], w, (T*)nullptr);
-#pragma unroll
-      for (int i = 0; i < V; ++i) acc[i] = fmaf(dl[j], w[i], acc[i]);
-    }
-    st16(dX + (size_t)t * d + c, pack16(acc, (T*)nullptr));
   }
 }
 

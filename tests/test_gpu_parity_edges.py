@@ -197,3 +197,42 @@ def test_step_is_deterministic():
         outs.append([host(t) for t in (r.counts, r.idx, r.gate, r.Y, r.dX, r.dgate, r.dWg, r.dWu, r.dWd)])
     for a, b in zip(*outs):
         np.testing.assert_array_equal(a, b)
+
+
+RB_SHAPES = {
+    # name: (T, d, E, k, dtype): k up to 16, E up to 256, partial column groups
+    "k16_partial_group": (500, 1032, 64, 16, torch.bfloat16),
+    "fp32_odd_tokens": (97, 520, 40, 3, torch.float32),
+    "E256_k16": (777, 256, 256, 16, torch.bfloat16),
+    "E65_short_rows": (33, 64, 65, 2, torch.bfloat16),
+}
+
+
+@pytest.mark.parametrize("name", list(RB_SHAPES))
+def test_route_backward_shapes(name):
+    """moe_route_bwd on shapes the layer workloads do not reach: k = 16, E up
+    to 256, rows that end inside a group of column chunks (d = 1032 bf16,
+    d = 520 fp32, d = 64), an odd token count.  Inputs: selection and gates as
+    the forward would hand them over (distinct experts per token, softmax
+    gates), dgate ~ N(0, 1)."""
+    T, d, E, k, dt = RB_SHAPES[name]
+    rng = np.random.default_rng([995, T, d, E, k])
+    Wr = torch.from_numpy((rng.standard_normal((E, d)) / np.sqrt(d)).astype(np.float32)).to(dt)
+    idx = np.argsort(rng.random((T, E)), axis=1)[:, :k].astype(np.int32)
+    z = rng.standard_normal((T, k))
+    gate = (np.exp(z) / np.exp(z).sum(1, keepdims=True)).astype(np.float32)
+    dgate = rng.standard_normal((T, k)).astype(np.float32)
+    base = torch.from_numpy(rng.standard_normal((T, d)).astype(np.float32)).to(dt).cuda()
+    log(f"route bwd {name}: T={T} d={d} E={E} k={k} {dt}")
+    g_t, i_t, dg_t, W_t = (torch.from_numpy(gate).cuda(), torch.from_numpy(idx).cuda(),
+                           torch.from_numpy(dgate).cuda(), Wr.cuda())
+    out = torch.full((T, d), float("nan"), dtype=dt, device="cuda")
+    acc = base.clone()
+    assert api.moe_route_bwd(g_t, i_t, dg_t, W_t, out, accumulate=False) == 0
+    assert api.moe_route_bwd(g_t, i_t, dg_t, W_t, acc, accumulate=True) == 0
+    torch.cuda.synchronize()
+    _, ref = O.route_topk_backward(host(W_t), idx, gate, dgate)
+    e1, e2 = rel_fro(host(out), ref), rel_fro(host(acc), host(base) + ref)
+    log(f"  dX {e1:.2e}, accumulated {e2:.2e}")
+    tol = 1e-5 if dt == torch.float32 else TOL_FFN
+    assert e1 <= tol and e2 <= tol
