@@ -56,11 +56,19 @@ def stats_table(path: str, top: int) -> str:
         out.append(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                    f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['Percentage']):.1f} |")
     ffn = [r for r in rows if base_name(r["Name"]) in FFN_KERNELS]
-    if ffn:
-        steps = max(int(r["Calls"]) for r in ffn if base_name(r["Name"]) == "kb_gate_up")
+    calls = [int(r["Calls"]) for r in ffn if base_name(r["Name"]) == "kb_gate_up"]
+    if calls:
+        steps = max(calls)
         tot = sum(float(r["TotalDurationNs"]) for r in ffn) / steps / 1e3
         out.append("")
         out.append(f"grouped SwiGLU fwd+bwd kernels per step (sum of averages over {steps} steps): {tot:.1f} µs")
+    q8 = [r for r in rows if base_name(r["Name"]) in ("kq_gate_up", "kq_down")]
+    if q8:
+        layers = max(int(r["Calls"]) for r in q8)
+        tot = sum(float(r["TotalDurationNs"]) for r in q8) / layers / 1e3
+        out.append("")
+        out.append(f"int8-code grouped forward kernels per layer (sum of averages over {layers} layer passes): "
+                   f"{tot:.1f} µs")
     return "\n".join(out)
 
 
