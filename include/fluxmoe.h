@@ -269,7 +269,9 @@ int moe_cluster_experts(const void* const* w_src, int dtype, int L, int E, int d
 /* ------------------------------------------------------------ the layer ----
  * A layer's slots: routed slots 0..S_routed-1 (kept experts and merged
  * groups), then S_shared always-on shared experts (gate 1.0, every token).
- * All pointer members are DEVICE arrays of S_routed + S_shared device pointers.
+ * All pointer members are DEVICE arrays of S_routed + S_shared device pointers;
+ * the matrices they point to must be 16-byte aligned (read on the device only,
+ * not checked).
  * Non-tuning (merged, frozen) slots have dw_* == NULL: they get dX but no dW
  * (Section 1 and Section 3: non-tuning experts are merged and frozen).
  *
@@ -338,6 +340,8 @@ size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int T, int k);
  * are DEVICE arrays of S_routed + S_shared device pointers:
  *   q_gate, q_up [S] -> [I,d] int8;  q_down [S] -> [d,I] int8;
  *   s_gate, s_up [S] -> [I] fp32;    s_down [S] -> [d] fp32.
+ * The pointers in the tables are read on the device only: each code matrix
+ * must be 16-byte aligned and each scale array 4-byte aligned (not checked).
  */
 typedef struct moe_layer_q8 {
   int d;
