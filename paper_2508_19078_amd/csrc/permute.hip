@@ -8,7 +8,7 @@
 //   [scan]         for large tables, one block turns the per-block counts into
 //                  global row positions: a wave scan per slot over the blocks,
 //                  then an exclusive scan over the slots (the bucket offsets)
-//   place+scatter  a block of 32 tokens ranks its rows within each slot in
+//   place+scatter  a block of 16 or 32 tokens ranks its rows within each slot in
 //                  token order, writes the maps and copies X[t] to every row t
 //                  opens (16-byte accesses, the row loads issued first); for
 //                  small tables it sums the count table itself
@@ -21,8 +21,7 @@ namespace {
 constexpr int PM_TOK = 256;   // tokens (threads) per block of count/place
 constexpr int PM_SMAX = 512;  // slots count and place support
 constexpr int PM_FUSE = 16384;  // place sums the count table itself up to this many entries
-constexpr int PS_TOK = 32;      // tokens per block of place + scatter
-constexpr int PS_THREADS = 512;
+constexpr int PS_THREADS = 512;  // place + scatter: 8 waves of 16 or 32 tokens per block
 
 template <int KMAX>
 struct TokenSlots {
@@ -114,8 +113,9 @@ __global__ __launch_bounds__(1024) void k_perm_scan(int32_t* __restrict__ bc, in
   for (size_t i = threadIdx.x; i < (size_t)S * nblk; i += blockDim.x) bc[i] += tot[i / nblk];
 }
 
-// Places the rows of 32 tokens and copies them: block = 8 waves, wave w owns
-// tokens t0 + 4w .. t0 + 4w + 3.
+// Places the rows of PS_TOK (16 or 32) tokens and copies them: block = 8 waves,
+// wave w owns tokens t0 + w * PS_TOK / 8 onwards.  (16-token blocks when
+// 32-token ones would leave compute units idle.)
 //   1. every wave starts loading the first 4 KB of its four rows (they do not
 //      depend on the maps), while the first 256 threads take the slots of the
 //      count block's tokens up to the end of this block;
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(1024) void k_perm_scan(int32_t* __restrict__ bc, in
 //      bucket offsets), otherwise bc already holds those positions;
 //   3. the maps are written and each row is stored at every position its token
 //      opens.
-template <int KMAX, bool SCAN>
+template <int KMAX, bool SCAN, int PS_TOK>
 __global__ __launch_bounds__(PS_THREADS) void k_place_scatter(
     const int32_t* __restrict__ idx, const float* __restrict__ gate, const int32_t* __restrict__ emap,
     int T, int k, int S, const int32_t* __restrict__ bc, int nblk, int32_t* __restrict__ offsets,
@@ -475,6 +475,15 @@ int check_tk(int T, int k) {
   else if ((k) <= 8) { MACRO(8); } \
   else { MACRO(16); }
 
+// Compute units of the current device (256 on MI355X when the query fails).
+int cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  return n;
+}
+
 }  // namespace
 }  // namespace fm
 
@@ -526,17 +535,20 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
   const bool fuse = (long long)nblk * S_routed <= PM_FUSE;
   if (!fuse) hipLaunchKernelGGL(k_perm_scan, dim3(1), dim3(1024), 0, st, bc, nblk, S_routed, offsets);
   const int row_bytes = d * esize(dtype);
-#define FM_PP(KM)                                                                                          \
-  if (fuse)                                                                                                \
-    hipLaunchKernelGGL((k_place_scatter<KM, true>), dim3(cdiv(T, PS_TOK)), dim3(PS_THREADS), 0, st, idx,   \
-                       gate, expert_map, T, k, S_routed, bc, nblk, offsets, perm_token, perm_gate, inv,    \
-                       (const char*)X, row_bytes, (char*)X_perm);                                          \
-  else                                                                                                     \
-    hipLaunchKernelGGL((k_place_scatter<KM, false>), dim3(cdiv(T, PS_TOK)), dim3(PS_THREADS), 0, st, idx,  \
-                       gate, expert_map, T, k, S_routed, bc, nblk, offsets, perm_token, perm_gate, inv,    \
-                       (const char*)X, row_bytes, (char*)X_perm)
+  // 32-token blocks once they fill every compute unit, else 16-token ones
+  const bool wide = cdiv(T, 32) >= cu_count();
+#define FM_PS(KM, SC, TOK)                                                                                  \
+  hipLaunchKernelGGL((k_place_scatter<KM, SC, TOK>), dim3(cdiv(T, TOK)), dim3(PS_THREADS), 0, st, idx, gate, \
+                     expert_map, T, k, S_routed, bc, nblk, offsets, perm_token, perm_gate, inv,             \
+                     (const char*)X, row_bytes, (char*)X_perm)
+#define FM_PP(KM)                       \
+  if (fuse && wide) FM_PS(KM, true, 32);  \
+  else if (fuse) FM_PS(KM, true, 16);     \
+  else if (wide) FM_PS(KM, false, 32);    \
+  else FM_PS(KM, false, 16)
   FM_KSWITCH(k, FM_PP)
 #undef FM_PP
+#undef FM_PS
   return check_launch("moe_permute");
 }
 
