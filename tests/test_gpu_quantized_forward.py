@@ -6,9 +6,10 @@ the whole int8 range (-128 included) and fed to both sides as inputs.
 H and O must be within the 2e-2 relative Frobenius bar of the bf16 products
 (each shape is reported).  Shapes: K tails inside a slab (d = 272, I = 208),
 intermediate and hidden sizes below one tile (I = 48, d = 64), an empty slot, a
-shared expert, and a full-size DeepSeek-stack layer (T = 4096, d = 2048, 64
-experts, top-6, I = 1408) in the launch configuration of the profiling pass,
-compared on a seeded sample of rows."""
+shared expert, a layer of shared experts only (no routed slot), and a
+full-size DeepSeek-stack layer (T = 4096, d = 2048, 64 experts, top-6,
+I = 1408) in the launch configuration of the profiling pass, compared on a
+seeded sample of rows."""
 import numpy as np
 import pytest
 import torch
@@ -24,6 +25,7 @@ CASES = {
     # name: (T, d, E, k, I, n_shared, experts drawn from, sampled rows or None)
     "ragged_tails_empty_slot": (300, 272, 8, 2, 208, 1, 7, None),
     "below_one_tile": (5, 64, 4, 2, 48, 0, 4, None),
+    "shared_experts_only": (77, 128, 0, 1, 96, 2, 0, None),
     "full_deepseek_stack_layer": (4096, 2048, 64, 6, 1408, 0, 64, 384),
 }
 
@@ -37,7 +39,7 @@ def draw_case(name):
     rng = np.random.default_rng([4242, T, d, E, I])
     S = E + n_sh
     Xb = bf16_values(rng.standard_normal((T, d)))
-    idx = np.argsort(rng.random((T, E_drawn)), axis=1)[:, :k].astype(np.int32)
+    idx = (np.argsort(rng.random((T, E_drawn)), axis=1)[:, :k] if E else np.zeros((T, k))).astype(np.int32)
     gate = np.full((T, k), 1.0 / k, dtype=np.float32)
     q = {
         "g": rng.integers(-128, 128, size=(S, I, d), dtype=np.int8),
@@ -56,11 +58,15 @@ def draw_case(name):
 def run_gpu(c):
     T, d, E, k, I, n_sh, S = (c[x] for x in ("T", "d", "E", "k", "I", "n_sh", "S"))
     dev = "cuda"
-    offsets, ptok, _, _ = O.permute_maps(c["idx"], c["gate"], np.arange(E), E)
+    if E:
+        offsets, ptok, _, _ = O.permute_maps(c["idx"], c["gate"], np.arange(E), E)
+    else:                                   # no routed slot: no permuted rows
+        offsets, ptok = np.zeros(1, dtype=np.int64), np.zeros(0, dtype=np.int64)
     N = int(offsets[-1])
     X = c["Xb"].to(dev)
     Xp = torch.zeros((T * k, d), dtype=torch.bfloat16, device=dev)
-    Xp[:N] = X[torch.from_numpy(ptok).to(dev)]
+    if N:
+        Xp[:N] = X[torch.from_numpy(ptok).to(dev)]
     qd = {m: torch.from_numpy(c["q"][m]).to(dev) for m in "gud"}
     sd = {m: torch.from_numpy(c["s"][m]).to(dev) for m in "gud"}
     tab = api.LayerTablesQ8(d, I, E, n_sh, [qd["g"][i] for i in range(S)], [qd["u"][i] for i in range(S)],
