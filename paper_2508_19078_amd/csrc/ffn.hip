@@ -1008,7 +1008,11 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
 // A slot's rows are its tokens after folding (a token whose choices share the
 // slot is one row with the summed gate), so |D_s| is the slot's row count.
 
-constexpr int UT_ROWS = 64;    // rows per first-pass tile (several blocks per CU keep loads in flight)
+// Rows per first-pass tile: 64, or 32 when 64-row tiles would give fewer than
+// two blocks per CU (several blocks per CU keep loads in flight; at the
+// DeepSeek shape 64 measured best, at T = 4096 with 16 experts 32 took the pass
+// from 129 to 94 us).
+constexpr int UT_ROWS = 64, UT_ROWS_MIN = 32;
 
 // Sum of squares of n elements (n % 8 == 0) spread over a wave: every lane
 // ends with the same total (fixed butterfly order).
@@ -1027,20 +1031,20 @@ template <typename T> __device__ __forceinline__ float wave_sumsq(const T* __res
   return a;
 }
 
-// First pass: one block per 64-row tile of a slot (tiles as in mbase); four
+// First pass: one block per tile of tile_rows rows of a slot (tiles as in mbase); four
 // waves take every fourth row; the tile's sum in fp64, waves added in order.
 template <typename T>
 __global__ __launch_bounds__(256) void k_utility_rows(const T* __restrict__ X, const T* __restrict__ Xp,
                                                       const T* __restrict__ dO, const T* __restrict__ H,
                                                       const T* __restrict__ dAg, const T* __restrict__ dAu,
-                                                      RowArgs ra, double* __restrict__ part) {
+                                                      RowArgs ra, int tile_rows, double* __restrict__ part) {
   __shared__ double wsum[4];
   const int b = blockIdx.x;
   if (b >= ld_scalar(ra.mbase + ra.S)) return;
   const int s = find_slot(ra.mbase, ra.S, b);
-  const int r0 = (b - ld_scalar(ra.mbase + s)) * UT_ROWS;
+  const int r0 = (b - ld_scalar(ra.mbase + s)) * tile_rows;
   const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-  const int rows = min(UT_ROWS, sr.nrows - r0), wave = threadIdx.x >> 6, d = ra.d, I = ra.I;
+  const int rows = min(tile_rows, sr.nrows - r0), wave = threadIdx.x >> 6, d = ra.d, I = ra.I;
   double acc = 0.0;
   for (int i = wave; i < rows; i += 4) {
     const size_t o = (size_t)(sr.orow0 + r0 + i);
@@ -1110,8 +1114,13 @@ extern "C" size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int 
   return sched_bytes(n_slots(L));
 }
 
-// Upper bound of the utility pass's row tiles: sum_s ceil(n_s / UT_ROWS).
-static size_t utility_tiles(const moe_layer* L, int T, int k) { return rows_total(L, T, k) / UT_ROWS + n_slots(L) + 1; }
+// Upper bound of the utility pass's row tiles at tile height `rows`: sum_s ceil(n_s / rows).
+static size_t utility_tiles(const moe_layer* L, int T, int k, int rows = UT_ROWS_MIN) {
+  return rows_total(L, T, k) / rows + n_slots(L) + 1;
+}
+static int utility_tile_rows(const moe_layer* L, int T, int k) {
+  return rows_total(L, T, k) / UT_ROWS >= 2 * (size_t)persistent_blocks() ? UT_ROWS : UT_ROWS_MIN;
+}
 
 extern "C" size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k) {
   if (!L || T < 0 || k <= 0) return 0;
@@ -1295,13 +1304,14 @@ extern "C" int moe_expert_utility(const moe_layer* L, const void* X, const void*
   const char* dAg = (const char*)ws + sched_bytes(S);
   const char* dAu = dAg + act;
   double* part = (double*)((char*)ws + sched_bytes(S) + 2 * act);
-  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, UT_ROWS,
+  const int ut_rows = utility_tile_rows(L, T, k);
+  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, ut_rows,
                      (float* const*)nullptr, sc.mbase, sc.wbase, sc.dorder, sc.queues);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
-  const dim3 grid((unsigned)utility_tiles(L, T, k));
+  const dim3 grid((unsigned)utility_tiles(L, T, k, ut_rows));
 #define FM_UT(TT)                                                                                            \
   hipLaunchKernelGGL(k_utility_rows<TT>, grid, dim3(256), 0, st, (const TT*)X, (const TT*)X_perm, (const TT*)dO, \
-                     (const TT*)H, (const TT*)dAg, (const TT*)dAu, ra, part)
+                     (const TT*)H, (const TT*)dAg, (const TT*)dAu, ra, ut_rows, part)
   if (L->dtype == MOE_BF16) FM_UT(bf16);
   else FM_UT(float);
 #undef FM_UT
