@@ -46,10 +46,12 @@ def stack_inputs(w, L):
     return dev, ora, W.draw_x(w, 0)
 
 
-def check_stack(w, L, max_excluded=0.25):
+def check_stack(w, L, max_excluded=0.25, fused=None):
     dev, ora, X0 = stack_inputs(w, L)
-    log(f"stack {w.name}: L={L} T={w.T} d={w.d} E={w.E}+{w.n_shared} k={w.k} I={w.I}")
-    st = QuantizedStack(dev, w.T, w.k, record=True)
+    log(f"stack {w.name}: L={L} T={w.T} d={w.d} E={w.E}+{w.n_shared} k={w.k} I={w.I} fused={fused}")
+    st = QuantizedStack(dev, w.T, w.k, record=True, fused=fused)
+    if fused is not None:
+        assert st.fused == fused
     out = st.run(W.to_torch(X0, "cuda"))
     torch.cuda.synchronize()
     counts_o, idx_o, gate_o, X_o = O.quantized_stack_profile(X0.f64(), ora, w.k)
@@ -98,6 +100,13 @@ def test_profiling_stack_small():
 def test_profiling_stack_shared_experts():
     w = W.scaled(W.WORKLOADS["deepseek_moe"], T=256, d=256, E=16, k=4, I=128)
     check_stack(w, 2)
+
+
+def test_profiling_stack_dequantising_path():
+    """bf16 with the experts dequantised to bf16 (moe_dequant_int8) before the
+    bf16 grouped forward: the path for shapes the int8-code GEMM does not take."""
+    w = W.scaled(W.WORKLOADS["deepseek_moe"], T=256, d=256, E=16, k=4, I=128)
+    check_stack(w, 2, fused=False)
 
 
 def test_profiling_stack_fp32_and_narrow():

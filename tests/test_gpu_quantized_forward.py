@@ -126,3 +126,24 @@ def test_quantised_forward(name):
     log(f"  {len(got_o)} rows compared: H rel err {eh:.2e}, O rel err {eo:.2e}")
     assert np.isfinite(got_h).all() and np.isfinite(got_o).all()
     assert eh <= TOL_FFN and eo <= TOL_FFN
+
+
+@pytest.mark.parametrize("out_dtype", [torch.bfloat16, torch.float32])
+def test_dequantise_rows(out_dtype):
+    """moe_dequant_int8 against the exact q * s (oracle dequantize_rows), element
+    by element: fp32 output within fp32 rounding of the product, bf16 output
+    within half a bf16 step (one rounding of the fp32 product); codes over the
+    whole int8 range, scales over six decades, a row count that is not a
+    multiple of the kernel's rows per block."""
+    rng = np.random.default_rng([4243])
+    rows, cols = 1037, 272
+    q = rng.integers(-128, 128, size=(rows, cols), dtype=np.int8)
+    sc = (10.0 ** rng.uniform(-5, 1, size=rows)).astype(np.float32)
+    out = torch.empty((rows, cols), dtype=out_dtype, device="cuda")
+    api.moe_dequant_int8(torch.from_numpy(q).cuda(), torch.from_numpy(sc).cuda(), out)
+    torch.cuda.synchronize()
+    exact = O.dequantize_rows(q, sc)
+    got = host(out)
+    # bf16 keeps 8 significant bits: a rounding is within 2^-8 of the value
+    rel = 2.0 ** -24 if out_dtype == torch.float32 else 2.0 ** -8 + 2.0 ** -23
+    assert np.all(np.abs(got - exact) <= rel * np.abs(exact)), np.max(np.abs(got - exact) / np.maximum(np.abs(exact), 1e-30))
