@@ -147,3 +147,21 @@ def test_dequantise_rows(out_dtype):
     # bf16 keeps 8 significant bits: a rounding is within 2^-8 of the value
     rel = 2.0 ** -24 if out_dtype == torch.float32 else 2.0 ** -8 + 2.0 ** -23
     assert np.all(np.abs(got - exact) <= rel * np.abs(exact)), np.max(np.abs(got - exact) / np.maximum(np.abs(exact), 1e-30))
+
+
+@pytest.mark.parametrize("dt", [torch.bfloat16, torch.float32])
+def test_residual_add(dt):
+    """moe_residual_add (the stack's X_{l+1} = X_l + Y_l) element by element
+    against the exact sum: one rounding of the fp32 sum to the stream's type;
+    an odd row count and rows of 8 + 16 k elements."""
+    rng = np.random.default_rng([4244])
+    T, d = 333, 264
+    Xh = rng.standard_normal((T, d)).astype(np.float32)
+    Yh = (rng.standard_normal((T, d)) * 10.0 ** rng.uniform(-3, 1, size=(T, 1))).astype(np.float32)
+    X, Y = torch.from_numpy(Xh).to(dt).cuda(), torch.from_numpy(Yh).to(dt).cuda()
+    out = torch.empty_like(X)
+    api.moe_residual_add(X, Y, out)
+    torch.cuda.synchronize()
+    exact = host(X) + host(Y)
+    rel = 2.0 ** -24 if dt == torch.float32 else 2.0 ** -8 + 2.0 ** -23
+    assert np.all(np.abs(host(out) - exact) <= rel * np.abs(exact))
