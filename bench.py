@@ -342,10 +342,14 @@ def profiling_stack(reps=3):
     total = float(np.median([p[0] for p in passes[1:]]))
     stages = {nm: round(float(np.median([p[1][nm] for p in passes[1:]])), 3) for nm in passes[1][1]}
     counts = qs.counts.cpu().numpy()
+    # the grouped forward's algorithmic flops: 6 d I per routed row (T k rows per layer; no shared experts)
+    ffn_flops = 6.0 * d * I * T * k * L
     out = {"workload": f"deepseek_stack: {L} layers x {E} experts, d={d} I={I}, T={T}, top-{k}, int8 router "
                        "and experts (per-row scales), residual stream",
            "pass_ms": round(total, 3), "tokens_per_s": round(T / (total * 1e-3), 1),
            "stages_ms": stages, "quantise_ms": round(quant_ms, 3),
+           "ffn_fwd_TFLOPs": round(ffn_flops / (stages["ffn_fwd"] * 1e-3) / 1e12, 1),
+           "ffn_fwd_frac_bf16_peak": round(ffn_flops / (stages["ffn_fwd"] * 1e-3) / 2.5e15, 4),
            "int8_weight_bytes": int(sum(q[n][0].numel() for q in qs.q for n in ("wg", "wu", "wd", "Wr"))),
            "hist_ok": bool((counts.sum(axis=1) == T * k).all())}
     del qs
