@@ -360,7 +360,7 @@ def profiling_stack(reps=3):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (this build has no multi-GPU path); got --gpus {a.gpus}",
+        print(f"bench.py measures one GPU only (the multi-GPU path is not implemented); got --gpus {a.gpus}",
               file=sys.stderr)
         sys.exit(2)
     import numpy as np
