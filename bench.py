@@ -208,9 +208,31 @@ def cpu_baseline(w, n_tok):
     O.moe_backward(X, inp.dY.f64(), idx, gate, plan.expert_map, slots)
     lap("backward")
     dt = time.perf_counter() - t0
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    # the thread pools NumPy's BLAS and OpenMP actually run with, and the
+    # router, histogram and permute stages again on one thread
+    pools, one_thread = None, {}
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+    except ImportError:
+        threadpool_info = threadpool_limits = None
+    if threadpool_info is not None:
+        pools = [{"api": i.get("internal_api"), "user_api": i.get("user_api"), "threads": i.get("num_threads")}
+                 for i in threadpool_info()]
+        with threadpool_limits(limits=1):
+            t1 = time.perf_counter()
+            O.route_topk(X, inp.Wr.f64(), b, w.k)
+            t2 = time.perf_counter()
+            O.profile_hist(X, q, s, b, w.k)
+            t3 = time.perf_counter()
+            O.permute_maps(idx, gate, plan.expert_map, plan.S)
+            t4 = time.perf_counter()
+        one_thread = {"route": round(t2 - t1, 3), "profile_hist": round(t3 - t2, 3), "permute": round(t4 - t3, 3)}
+    blas_threads = [p["threads"] for p in (pools or []) if p["user_api"] == "blas"]
+    cores = max(blas_threads) if blas_threads else int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": round(n_tok / dt, 2), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "cpu": cpu_model(), "stages_s": stages,
+            "cpu": cpu_model(), "cpu_count": os.cpu_count(), "thread_pools": pools,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS"), "stages_s": stages,
+            "stages_1_thread_s": one_thread,
             "sample": (f"all {w.T} tokens" if n_tok >= w.T else f"first {n_tok} of {w.T} tokens")
                       + " of the same workload, full fp64 layer step "
                       f"(route, int8 histogram, plan+merge of all experts, permute, fwd+bwd); "

@@ -305,13 +305,26 @@ typedef struct moe_layer {
  * fp32; inv[T,k]: p for the choice that opened row p, -2-p for a choice folded
  * into row p; X_perm[T*k, d] with X_perm[p] = X[perm_token[p]].  Entries at or
  * beyond offsets[S_routed] are left untouched.  idx values must be in [0, E)
- * and expert_map values in [0, S_routed) (not checked on the device).
+ * and expert_map values in [0, S_routed) (not checked on the device; see
+ * moe_validate_routing and FLUXMOE_DEBUG_CHECKS).
  */
 int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
                 const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
                 int32_t* offsets, int32_t* perm_token, float* perm_gate,
                 int32_t* inv, void* X_perm, void* ws, size_t ws_bytes, void* stream);
 size_t moe_permute_workspace_size(int T, int k, int S_routed);
+
+/* moe_validate_routing: range check of moe_permute's index inputs, for
+ * debugging a caller (the routing it hands over must name experts that exist
+ * and slots that exist, Section 7's re-routing table included).  idx [T,k] and
+ * expert_map [E] (or NULL = identity, which needs S_routed >= E) are HOST
+ * arrays.  Returns MOE_OK, or MOE_ERR_ARG naming the first entry outside
+ * [0, E) resp. [0, S_routed).  With the environment variable
+ * FLUXMOE_DEBUG_CHECKS set (to anything but "0"), moe_permute itself copies
+ * idx and expert_map to the host, waits for `stream`, and runs this check
+ * before it enqueues anything (slow: debugging only).
+ */
+int moe_validate_routing(const int32_t* idx, const int32_t* expert_map, int T, int E, int k, int S_routed);
 
 /* moe_grouped_swiglu_fwd: every slot's SwiGLU expert FFN on its rows
  * (the experts of Section 2.1; tuning and frozen slots alike):
@@ -360,7 +373,10 @@ int moe_grouped_swiglu_fwd_q8(const moe_layer_q8* L, const void* X, const void* 
                               void* ws, size_t ws_bytes, void* stream);
 size_t moe_grouped_swiglu_fwd_q8_workspace_size(const moe_layer_q8* L, int T, int k);
 
-/* moe_unpermute: the gate-weighted combine of the expert outputs
+/* moe_unpermute: the gate-weighted combine of the expert outputs, the output
+ * of the MoE layer of Section 2.1 (each token's output is the sum of its
+ * selected experts' outputs weighted by the gating network's gates; shared
+ * experts add with gate 1):
  *   Y[t] = sum_{j: inv[t,j] >= 0} perm_gate[inv[t,j]] * O[inv[t,j]]
  *          + sum_{shared i} O[T*k + i*T + t]              (fp32 accumulation)
  * O [R_tot, d] and Y [T, d] in L->dtype.
@@ -368,7 +384,10 @@ size_t moe_grouped_swiglu_fwd_q8_workspace_size(const moe_layer_q8* L, int T, in
 int moe_unpermute(const moe_layer* L, const void* O, const int32_t* inv,
                   const float* perm_gate, int T, int k, void* Y, void* stream);
 
-/* moe_unpermute_bwd: backward of the combine with the gates as constants:
+/* moe_unpermute_bwd: backward of the combine of moe_unpermute (the MoE layer
+ * output of Section 2.1) with the gates as constants: the experts are what is
+ * fine-tuned (Sections 1 and 3), so the expert path's gradient holds the
+ * routing fixed; dgate hands the gates' share to moe_route_bwd:
  *   dO[p] = perm_gate[p] * dY[perm_token[p]]  for routed rows p < offsets[S_routed]
  *   dO[T*k + i*T + t] = dY[t]                  for shared slot i
  *   dgate[t,j] = <dY[t], O[row of (t,j)]>      (optional, fp32, when dgate != NULL;
@@ -379,7 +398,11 @@ int moe_unpermute_bwd(const moe_layer* L, const void* dY, const void* O,
                       const float* perm_gate, int T, int k,
                       void* dO, float* dgate, void* stream);
 
-/* moe_grouped_swiglu_bwd: backward of every slot's SwiGLU FFN:
+/* moe_grouped_swiglu_bwd: backward of every slot's SwiGLU FFN.  Only tuning
+ * experts are updated during local fine-tuning; non-tuning experts are merged
+ * and frozen (Section 1; Section 3, the tuning / non-tuning roles), so weight
+ * gradients are formed for tuning slots only, while every slot passes dX on to
+ * earlier layers:
  *   dH   = dO W_down
  *   dA_u = dH * silu(A_g)
  *   dA_g = dH * A_u * s * (1 + A_g (1 - s)),  s = sigmoid(A_g)
@@ -416,7 +439,10 @@ int moe_expert_utility(const moe_layer* L, const void* X, const void* X_perm,
                        const void* dO, void* ws, size_t ws_bytes, float* utility,
                        void* stream);
 
-/* moe_permute_bwd: gradient of the permutation (a deterministic gather):
+/* moe_permute_bwd: gradient of moe_permute's gather of each token into the
+ * buckets of the slots it is re-routed to (the token subsets D^e of
+ * Section 4.1 after the gate re-routing of Section 7): every row a token
+ * opened sends its gradient back to that token (a deterministic gather):
  *   dX[t] = sum_{j: inv[t,j] >= 0} dX_perm[inv[t,j]]
  *           + sum_{shared i} dX_perm[T*k + i*T + t]       (fp32 accumulation)
  */

@@ -435,6 +435,44 @@ def expert_utility(X, dY, idx, gate, expert_map, slots: SlotWeights, only: Optio
     return u
 
 
+def expert_utility_rank_one(X, dY, idx, gate, expert_map, slots: SlotWeights):
+    """The utility of expert_utility (Eq. 3, same reading, same token sets and
+    summed gates) without forming the per-token gradients: each of them is a
+    sum of three rank-one matrices, dW_down = dO_t h_t^T, dW_gate = da_g,t x_t^T,
+    dW_up = da_u,t x_t^T, and the Frobenius norm of an outer product a b^T is
+    ||a|| ||b||, so ||g_t||^2 = ||dO_t||^2 ||h_t||^2 + (||da_g,t||^2 +
+    ||da_u,t||^2) ||x_t||^2.  One batched pass per slot; for full-size layers,
+    where forming T * k gradients of size 3 I d is out of reach.
+    """
+    X, dY, gate = _f64(X), _f64(dY), _f64(gate)
+    T = X.shape[0]
+    slot_of = np.asarray(expert_map)[np.asarray(idx)]
+    u = np.zeros(slots.S, dtype=F64)
+    for s in range(slots.S):
+        if s < slots.S_routed:
+            t_all, j_all = np.nonzero(slot_of == s)
+            tokens = np.unique(t_all)
+            gsum = np.zeros(T)
+            np.add.at(gsum, t_all, gate[t_all, j_all])
+            gsum = gsum[tokens]
+        else:
+            tokens, gsum = np.arange(T), np.ones(T)
+        n = len(tokens)
+        if n == 0:
+            continue
+        x = X[tokens]
+        dO = gsum[:, None] * dY[tokens]
+        a_g, a_u, h, _ = swiglu_fwd(x, slots.wg[s], slots.wu[s], slots.wd[s])
+        dh = dO @ _f64(slots.wd[s])
+        sg = sigmoid(a_g)
+        da_u = dh * a_g * sg
+        da_g = dh * a_u * sg * (1.0 + a_g * (1.0 - sg))
+        sq = (np.sum(dO ** 2, axis=1) * np.sum(h ** 2, axis=1)
+              + (np.sum(da_g ** 2, axis=1) + np.sum(da_u ** 2, axis=1)) * np.sum(x ** 2, axis=1))
+        u[s] = n * np.sqrt(np.sum(sq) / n)
+    return u
+
+
 def expert_grad_columns(x, Wg, Wu, Wd, dO, cols):
     """Slices of one expert's weight gradients along the intermediate index:
     (dWg[cols, :], dWu[cols, :], dWd[:, cols]) for rows x [n, d] and output

@@ -57,6 +57,7 @@ _SIGS = {
     "moe_permute": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
                              _vp, _vp, _vp, _vp, _c_size, _vp]),
     "moe_permute_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
+    "moe_validate_routing": (_c_int, [_vp, _vp, _c_int, _c_int, _c_int, _c_int]),
     "moe_grouped_swiglu_fwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
                                         _c_size, _vp]),
     "moe_grouped_swiglu_fwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
@@ -113,12 +114,28 @@ def dtype_code(t: torch.dtype) -> int:
     raise TypeError(f"unsupported dtype {t}")
 
 
-def ptr(x) -> Optional[int]:
+I32, F32, I64, U8, I8 = torch.int32, torch.float32, torch.int64, torch.uint8, torch.int8
+FLOAT = (torch.float32, torch.bfloat16)
+
+
+def ptr(x, dt=None) -> Optional[int]:
+    """Device address of a tensor argument (ints, structs and None pass through).
+
+    A tensor must be dense (contiguous), on a GPU, and of dtype `dt` when one is
+    given (a dtype or a tuple of them): the library reads raw memory with the
+    layout and element type its header states, so an int64 index tensor or a
+    strided view would otherwise be misread silently."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
     if isinstance(x, torch.Tensor):
+        if not x.is_contiguous():
+            raise ValueError(f"tensor argument of shape {tuple(x.shape)} is not contiguous")
+        if x.device.type != "cuda":
+            raise ValueError(f"tensor argument is on {x.device}, the library reads device memory")
+        if dt is not None and x.dtype not in (dt if isinstance(dt, tuple) else (dt,)):
+            raise TypeError(f"tensor argument has dtype {x.dtype}, expected {dt}")
         return x.data_ptr()
     if isinstance(x, ctypes.Structure):
         return ctypes.addressof(x)
@@ -147,28 +164,28 @@ def _call(name: str, *args) -> int:
 def moe_route_topk(X, Wr, bias, k, idx, gate, logits=None, stream=None):
     T, d = X.shape
     E = Wr.shape[0]
-    return _call("moe_route_topk", ptr(X), ptr(Wr), dtype_code(X.dtype), ptr(bias), T, d, E, k,
-                 ptr(idx), ptr(gate), ptr(logits), stream_ptr(stream))
+    return _call("moe_route_topk", ptr(X, FLOAT), ptr(Wr, X.dtype), dtype_code(X.dtype), ptr(bias, F32), T, d,
+                 E, k, ptr(idx, I32), ptr(gate, F32), ptr(logits, F32), stream_ptr(stream))
 
 
 def moe_route_bwd(gate, idx, dgate, Wr, dX, accumulate=False, stream=None):
     T, k = gate.shape
     E, d = Wr.shape
-    return _call("moe_route_bwd", ptr(gate), ptr(idx), ptr(dgate), ptr(Wr), dtype_code(Wr.dtype), T, d, E, k,
-                 ptr(dX), int(bool(accumulate)), stream_ptr(stream))
+    return _call("moe_route_bwd", ptr(gate, F32), ptr(idx, I32), ptr(dgate, F32), ptr(Wr, FLOAT),
+                 dtype_code(Wr.dtype), T, d, E, k, ptr(dX, Wr.dtype), int(bool(accumulate)), stream_ptr(stream))
 
 
 def moe_quantize_int8(W, Wq, scale, stream=None):
     E, d = W.shape
-    return _call("moe_quantize_int8", ptr(W), dtype_code(W.dtype), E, d, ptr(Wq), ptr(scale),
+    return _call("moe_quantize_int8", ptr(W, FLOAT), dtype_code(W.dtype), E, d, ptr(Wq, I8), ptr(scale, F32),
                  stream_ptr(stream))
 
 
 def moe_profile_hist(X, Wq, scale, bias, k, counts, idx=None, stream=None):
     T, d = X.shape
     E = Wq.shape[0]
-    return _call("moe_profile_hist", ptr(X), dtype_code(X.dtype), ptr(Wq), ptr(scale), ptr(bias), T, d,
-                 E, k, ptr(counts), ptr(idx), stream_ptr(stream))
+    return _call("moe_profile_hist", ptr(X, FLOAT), dtype_code(X.dtype), ptr(Wq, I8), ptr(scale, F32),
+                 ptr(bias, F32), T, d, E, k, ptr(counts, I32), ptr(idx, I32), stream_ptr(stream))
 
 
 # --------------------------------------------------------------- merging ----
@@ -176,34 +193,35 @@ def moe_profile_hist(X, Wq, scale, bias, k, counts, idx=None, stream=None):
 def moe_profile_route(X, Wq, scale, bias, k, counts, idx, gate, stream=None):
     T, d = X.shape
     E = Wq.shape[0]
-    return _call("moe_profile_route", ptr(X), dtype_code(X.dtype), ptr(Wq), ptr(scale), ptr(bias), T, d, E, k,
-                 ptr(counts), ptr(idx), ptr(gate), stream_ptr(stream))
+    return _call("moe_profile_route", ptr(X, FLOAT), dtype_code(X.dtype), ptr(Wq, I8), ptr(scale, F32),
+                 ptr(bias, F32), T, d, E, k, ptr(counts, I32), ptr(idx, I32), ptr(gate, F32), stream_ptr(stream))
 
 
 def moe_dequant_int8(q, scale, out, stream=None):
     """q [..., cols] int8 with one scale per row of the flattened [rows, cols]."""
     cols = q.shape[-1]
     rows = q.numel() // cols
-    return _call("moe_dequant_int8", ptr(q), ptr(scale), rows, cols, dtype_code(out.dtype), ptr(out),
-                 stream_ptr(stream))
+    return _call("moe_dequant_int8", ptr(q, I8), ptr(scale, F32), rows, cols, dtype_code(out.dtype),
+                 ptr(out, FLOAT), stream_ptr(stream))
 
 
 def moe_residual_add(X, Y, out, stream=None):
     T, d = X.shape
-    return _call("moe_residual_add", ptr(X), ptr(Y), T, d, dtype_code(X.dtype), ptr(out), stream_ptr(stream))
+    return _call("moe_residual_add", ptr(X, FLOAT), ptr(Y, X.dtype), T, d, dtype_code(X.dtype), ptr(out, X.dtype),
+                 stream_ptr(stream))
 
 
 def moe_merge_plan(counts, n_merge, group, total_tokens, expert_map, slot_src, grp_ptr, grp_member,
                    alpha, expert_base=0, grp_base=0, member_base=0, stream=None):
     E = counts.shape[0]
-    return _call("moe_merge_plan", ptr(counts), E, n_merge, group, float(total_tokens), expert_base,
-                 grp_base, member_base, ptr(expert_map), ptr(slot_src), ptr(grp_ptr), ptr(grp_member),
-                 ptr(alpha), stream_ptr(stream))
+    return _call("moe_merge_plan", ptr(counts, I32), E, n_merge, group, float(total_tokens), expert_base,
+                 grp_base, member_base, ptr(expert_map, I32), ptr(slot_src, I32), ptr(grp_ptr, I32),
+                 ptr(grp_member, I32), ptr(alpha, F32), stream_ptr(stream))
 
 
 def moe_activation_frequency(counts, total_tokens, freq, stream=None):
-    return _call("moe_activation_frequency", ptr(counts), counts.shape[0], float(total_tokens), ptr(freq),
-                 stream_ptr(stream))
+    return _call("moe_activation_frequency", ptr(counts, I32), counts.shape[0], float(total_tokens),
+                 ptr(freq, F32), stream_ptr(stream))
 
 
 def plan_from_groups(E: int, groups):
@@ -233,15 +251,16 @@ def plan_from_groups(E: int, groups):
 def moe_merge_experts(w_src_ptrs, dtype, d, I, G, grp_ptr, grp_member, alpha, w_dst_ptrs, out_dtype,
                       stream=None):
     """w_src_ptrs / w_dst_ptrs: int64 device tensors of 3 pointers per expert / group."""
-    return _call("moe_merge_experts", ptr(w_src_ptrs), dtype_code(dtype), d, I, G, ptr(grp_ptr),
-                 ptr(grp_member), ptr(alpha), ptr(w_dst_ptrs), dtype_code(out_dtype), stream_ptr(stream))
+    return _call("moe_merge_experts", ptr(w_src_ptrs, I64), dtype_code(dtype), d, I, G, ptr(grp_ptr, I32),
+                 ptr(grp_member, I32), ptr(alpha, F32), ptr(w_dst_ptrs, I64), dtype_code(out_dtype),
+                 stream_ptr(stream))
 
 
 def moe_slot_pointers(slot_src, S, E, d, I, dtype, orig, merged, w_gate, w_up, w_down, stream=None):
     """orig / merged: (gate, up, down) stacked tensors; merged may be (None,)*3."""
-    return _call("moe_slot_pointers", ptr(slot_src), S, E, d, I, dtype_code(dtype), ptr(orig[0]),
-                 ptr(orig[1]), ptr(orig[2]), ptr(merged[0]), ptr(merged[1]), ptr(merged[2]), ptr(w_gate),
-                 ptr(w_up), ptr(w_down), stream_ptr(stream))
+    return _call("moe_slot_pointers", ptr(slot_src, I32), S, E, d, I, dtype_code(dtype), ptr(orig[0], dtype),
+                 ptr(orig[1], dtype), ptr(orig[2], dtype), ptr(merged[0], dtype), ptr(merged[1], dtype),
+                 ptr(merged[2], dtype), ptr(w_gate, I64), ptr(w_up, I64), ptr(w_down, I64), stream_ptr(stream))
 
 
 # --------------------------------------------------- layer-aware merging ----
@@ -249,8 +268,8 @@ def moe_slot_pointers(slot_src, S, E, d, I, dtype, orig, merged, w_gate, w_up, w
 def moe_merge_budget(counts, tuning, total_tokens, B_non, budget, eps=1e-12, stream=None):
     """counts [L, E] int32, tuning [L, E] uint8 (1 = tuning), budget [L] int32."""
     L, E = counts.shape
-    return _call("moe_merge_budget", ptr(counts), ptr(tuning), L, E, float(total_tokens), int(B_non),
-                 float(eps), ptr(budget), stream_ptr(stream))
+    return _call("moe_merge_budget", ptr(counts, I32), ptr(tuning, U8), L, E, float(total_tokens), int(B_non),
+                 float(eps), ptr(budget, I32), stream_ptr(stream))
 
 
 def moe_cluster_workspace_size(L, E, d, I) -> int:
@@ -260,9 +279,9 @@ def moe_cluster_workspace_size(L, E, d, I) -> int:
 def moe_cluster_experts(w_src_ptrs, dtype, L, E, d, I, tuning, budget, r, max_iter, ws, labels,
                         features=None, iters=None, stream=None):
     """w_src_ptrs: int64 device tensor of 3 pointers per expert (layer-major)."""
-    return _call("moe_cluster_experts", ptr(w_src_ptrs), dtype_code(dtype), L, E, d, I, ptr(tuning),
-                 ptr(budget), int(r), int(max_iter), ptr(ws), ws.numel() * ws.element_size(), ptr(labels),
-                 ptr(features), ptr(iters), stream_ptr(stream))
+    return _call("moe_cluster_experts", ptr(w_src_ptrs, I64), dtype_code(dtype), L, E, d, I, ptr(tuning, U8),
+                 ptr(budget, I32), int(r), int(max_iter), ptr(ws), ws.numel() * ws.element_size(),
+                 ptr(labels, I32), ptr(features, F32), ptr(iters, I32), stream_ptr(stream))
 
 
 # ------------------------------------------------------------- the layer ----
@@ -276,9 +295,25 @@ def moe_permute(X, idx, gate, expert_map, S_routed, offsets, perm_token, perm_ga
     T, d = X.shape
     k = idx.shape[1]
     E = E if E is not None else (expert_map.shape[0] if expert_map is not None else S_routed)
-    return _call("moe_permute", ptr(X), dtype_code(X.dtype), ptr(idx), ptr(gate), ptr(expert_map), T, d, E,
-                 k, S_routed, ptr(offsets), ptr(perm_token), ptr(perm_gate), ptr(inv), ptr(X_perm), ptr(ws),
+    return _call("moe_permute", ptr(X, FLOAT), dtype_code(X.dtype), ptr(idx, I32), ptr(gate, F32),
+                 ptr(expert_map, I32), T, d, E, k, S_routed, ptr(offsets, I32), ptr(perm_token, I32),
+                 ptr(perm_gate, F32), ptr(inv, I32), ptr(X_perm, X.dtype), ptr(ws),
                  ws.numel() * ws.element_size() if ws is not None else 0, stream_ptr(stream))
+
+
+def moe_validate_routing(idx, expert_map, S_routed, E=None):
+    """Host-side range check of a routing (idx [T,k], expert_map [E] or None),
+    given as CPU tensors or NumPy arrays (copied to int32 host arrays here)."""
+    import numpy as np
+    hi = np.ascontiguousarray(np.asarray(idx.cpu() if isinstance(idx, torch.Tensor) else idx), dtype=np.int32)
+    T, k = hi.shape
+    hm = None
+    if expert_map is not None:
+        hm = np.ascontiguousarray(np.asarray(expert_map.cpu() if isinstance(expert_map, torch.Tensor)
+                                             else expert_map), dtype=np.int32)
+    E = E if E is not None else (len(hm) if hm is not None else S_routed)
+    return _call("moe_validate_routing", hi.ctypes.data if hi.size else None,
+                 hm.ctypes.data if hm is not None else None, T, E, k, S_routed)
 
 
 def moe_grouped_swiglu_fwd_workspace_size(layer, T, k) -> int:
@@ -290,8 +325,9 @@ def moe_grouped_swiglu_bwd_workspace_size(layer, T, k) -> int:
 
 
 def moe_grouped_swiglu_fwd(layer, X, X_perm, offsets, T, k, A_g, A_u, H, O, ws, stream=None):
-    return _call("moe_grouped_swiglu_fwd", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(A_g),
-                 ptr(A_u), ptr(H), ptr(O), ptr(ws), ws.numel() * ws.element_size(), stream_ptr(stream))
+    return _call("moe_grouped_swiglu_fwd", ptr(layer), ptr(X, FLOAT), ptr(X_perm, FLOAT), ptr(offsets, I32), T,
+                 k, ptr(A_g, FLOAT), ptr(A_u, FLOAT), ptr(H, FLOAT), ptr(O, FLOAT), ptr(ws),
+                 ws.numel() * ws.element_size(), stream_ptr(stream))
 
 
 def moe_grouped_swiglu_fwd_q8_workspace_size(layer, T, k) -> int:
@@ -299,35 +335,37 @@ def moe_grouped_swiglu_fwd_q8_workspace_size(layer, T, k) -> int:
 
 
 def moe_grouped_swiglu_fwd_q8(layer, X, X_perm, offsets, T, k, H, O, ws, stream=None):
-    return _call("moe_grouped_swiglu_fwd_q8", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(H),
-                 ptr(O), ptr(ws), ws.numel() * ws.element_size(), stream_ptr(stream))
+    return _call("moe_grouped_swiglu_fwd_q8", ptr(layer), ptr(X, FLOAT), ptr(X_perm, FLOAT), ptr(offsets, I32),
+                 T, k, ptr(H, FLOAT), ptr(O, FLOAT), ptr(ws), ws.numel() * ws.element_size(), stream_ptr(stream))
 
 
 def moe_unpermute(layer, O, inv, perm_gate, T, k, Y, stream=None):
-    return _call("moe_unpermute", ptr(layer), ptr(O), ptr(inv), ptr(perm_gate), T, k, ptr(Y),
-                 stream_ptr(stream))
+    return _call("moe_unpermute", ptr(layer), ptr(O, FLOAT), ptr(inv, I32), ptr(perm_gate, F32), T, k,
+                 ptr(Y, FLOAT), stream_ptr(stream))
 
 
 def moe_unpermute_bwd(layer, dY, O, inv, offsets, perm_gate, T, k, dO, dgate=None, stream=None):
-    return _call("moe_unpermute_bwd", ptr(layer), ptr(dY), ptr(O), ptr(inv), ptr(offsets), ptr(perm_gate),
-                 T, k, ptr(dO), ptr(dgate), stream_ptr(stream))
+    return _call("moe_unpermute_bwd", ptr(layer), ptr(dY, FLOAT), ptr(O, FLOAT), ptr(inv, I32), ptr(offsets, I32),
+                 ptr(perm_gate, F32), T, k, ptr(dO, FLOAT), ptr(dgate, F32), stream_ptr(stream))
 
 
 def moe_grouped_swiglu_bwd(layer, X, X_perm, offsets, T, k, A_g, A_u, H, dO, dX_perm, accumulate_dw, ws,
                            stream=None):
-    return _call("moe_grouped_swiglu_bwd", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(A_g),
-                 ptr(A_u), ptr(H), ptr(dO), ptr(dX_perm), int(accumulate_dw), ptr(ws),
-                 ws.numel() * ws.element_size(), stream_ptr(stream))
+    return _call("moe_grouped_swiglu_bwd", ptr(layer), ptr(X, FLOAT), ptr(X_perm, FLOAT), ptr(offsets, I32), T,
+                 k, ptr(A_g, FLOAT), ptr(A_u, FLOAT), ptr(H, FLOAT), ptr(dO, FLOAT), ptr(dX_perm, FLOAT),
+                 int(accumulate_dw), ptr(ws), ws.numel() * ws.element_size(), stream_ptr(stream))
 
 
 def moe_permute_bwd(layer, dX_perm, inv, T, k, dX, stream=None):
-    return _call("moe_permute_bwd", ptr(layer), ptr(dX_perm), ptr(inv), T, k, ptr(dX), stream_ptr(stream))
+    return _call("moe_permute_bwd", ptr(layer), ptr(dX_perm, FLOAT), ptr(inv, I32), T, k, ptr(dX, FLOAT),
+                 stream_ptr(stream))
 
 
 def moe_expert_utility(layer, X, X_perm, offsets, T, k, H, dO, ws, utility, stream=None):
     """After moe_grouped_swiglu_bwd with the same workspace `ws`."""
-    return _call("moe_expert_utility", ptr(layer), ptr(X), ptr(X_perm), ptr(offsets), T, k, ptr(H), ptr(dO),
-                 ptr(ws), ws.numel() * ws.element_size(), ptr(utility), stream_ptr(stream))
+    return _call("moe_expert_utility", ptr(layer), ptr(X, FLOAT), ptr(X_perm, FLOAT), ptr(offsets, I32), T, k,
+                 ptr(H, FLOAT), ptr(dO, FLOAT), ptr(ws), ws.numel() * ws.element_size(), ptr(utility, F32),
+                 stream_ptr(stream))
 
 
 # ----------------------------------------------------- layer descriptor ----

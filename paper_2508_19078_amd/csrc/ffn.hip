@@ -1220,10 +1220,14 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   FM_TRY(need(L->dw_gate, "layer dw_gate")); FM_TRY(need(L->dw_up, "layer dw_up"));
   FM_TRY(need(L->dw_down, "layer dw_down"));
   if (T == 0 && accumulate_dw) return MOE_OK;
-  FM_TRY(need(X, "X")); FM_TRY(need(offsets, "offsets")); FM_TRY(need(A_g, "A_g"));
-  FM_TRY(need(A_u, "A_u")); FM_TRY(need(H, "H")); FM_TRY(need(dO, "dO"));
-  FM_TRY(need(dX_perm, "dX_perm")); FM_TRY(need(ws, "ws"));
-  if (L->S_routed > 0) FM_TRY(need(X_perm, "X_perm"));
+  // With no tokens only the zeroing of the weight gradients runs: it reads the
+  // offsets and the schedule workspace, no per-token buffer (those may be NULL).
+  FM_TRY(need(offsets, "offsets")); FM_TRY(need(ws, "ws"));
+  if (T > 0) {
+    FM_TRY(need(X, "X")); FM_TRY(need(A_g, "A_g")); FM_TRY(need(A_u, "A_u")); FM_TRY(need(H, "H"));
+    FM_TRY(need(dO, "dO")); FM_TRY(need(dX_perm, "dX_perm"));
+    if (L->S_routed > 0) FM_TRY(need(X_perm, "X_perm"));
+  }
   FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(X_perm, "X_perm")); FM_TRY(need_aligned(A_g, "A_g"));
   FM_TRY(need_aligned(A_u, "A_u")); FM_TRY(need_aligned(H, "H")); FM_TRY(need_aligned(dO, "dO"));
   FM_TRY(need_aligned(dX_perm, "dX_perm")); FM_TRY(need_aligned(ws, "ws"));

@@ -13,6 +13,10 @@
 //                  opens (16-byte accesses, the row loads issued first); for
 //                  small tables it sums the count table itself
 // Combine and the two backward gathers run one wave per token.
+#include <stdlib.h>
+
+#include <vector>
+
 #include "common.hpp"
 
 namespace fm {
@@ -489,6 +493,49 @@ int cu_count() {
 
 using namespace fm;
 
+extern "C" int moe_validate_routing(const int32_t* idx, const int32_t* expert_map, int T, int E, int k,
+                                    int S_routed) {
+  clear_error();
+  if (T < 0 || k <= 0 || E <= 0 || S_routed <= 0) return fail(MOE_ERR_ARG, "T=%d k=%d E=%d S_routed=%d", T, k, E,
+                                                               S_routed);
+  if (T > 0 && !idx) return fail(MOE_ERR_ARG, "idx must not be NULL");
+  if (expert_map) {
+    for (int e = 0; e < E; ++e)
+      if (expert_map[e] < 0 || expert_map[e] >= S_routed)
+        return fail(MOE_ERR_ARG, "expert_map[%d]=%d outside [0, %d)", e, expert_map[e], S_routed);
+  } else if (S_routed < E) {
+    return fail(MOE_ERR_ARG, "identity map needs S_routed >= E");
+  }
+  for (long i = 0; i < (long)T * k; ++i)
+    if (idx[i] < 0 || idx[i] >= E)
+      return fail(MOE_ERR_ARG, "idx[%ld][%ld]=%d outside [0, %d)", i / k, i % k, idx[i], E);
+  return MOE_OK;
+}
+
+namespace fm {
+namespace {
+// FLUXMOE_DEBUG_CHECKS set (and not "0"): moe_permute copies idx and
+// expert_map to the host, waits for the stream, and range-checks them before
+// launching anything.  Slow; for debugging callers.
+bool debug_checks() {
+  const char* v = getenv("FLUXMOE_DEBUG_CHECKS");
+  return v && v[0] && !(v[0] == '0' && v[1] == '\0');
+}
+
+int debug_check_routing(const int32_t* idx, const int32_t* expert_map, int T, int E, int k, int S_routed,
+                        hipStream_t st) {
+  std::vector<int32_t> hi((size_t)T * k), hm(expert_map ? E : 0);
+  if (T > 0 && hipMemcpyAsync(hi.data(), idx, hi.size() * sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return fail(MOE_ERR_HIP, "debug check: copy of idx failed");
+  if (expert_map &&
+      hipMemcpyAsync(hm.data(), expert_map, hm.size() * sizeof(int32_t), hipMemcpyDeviceToHost, st) != hipSuccess)
+    return fail(MOE_ERR_HIP, "debug check: copy of expert_map failed");
+  if (hipStreamSynchronize(st) != hipSuccess) return fail(MOE_ERR_HIP, "debug check: stream synchronisation failed");
+  return moe_validate_routing(hi.data(), expert_map ? hm.data() : nullptr, T, E, k, S_routed);
+}
+}  // namespace
+}  // namespace fm
+
 extern "C" size_t moe_permute_workspace_size(int T, int k, int S_routed) {
   (void)k;
   if (T <= 0 || S_routed <= 0) return 256;
@@ -525,6 +572,7 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
                        S_routed + 1);
     return check_launch("moe_permute");
   }
+  if (debug_checks()) FM_TRY(debug_check_routing(idx, expert_map, T, E, k, S_routed, st));
   const int nblk = cdiv(T, PM_TOK);
   int32_t* bc = (int32_t*)ws;
 #define FM_PC(KM) \

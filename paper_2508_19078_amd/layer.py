@@ -163,11 +163,12 @@ class MoELayerRunner:
                                   dtype=torch.uint8, device=device)
 
     # ------------------------------------------------------------ stages --
-    def profile(self):
+    def profile(self, idx8: Optional[torch.Tensor] = None):
+        """idx8 [T,k] int32, if given, receives the int8 router's top-k sets."""
         w = self.w
         api.moe_quantize_int8(self.Wr, self.Wq, self.wscale)
         self.counts.zero_()
-        api.moe_profile_hist(self.X, self.Wq, self.wscale, self.bias, w.k, self.counts)
+        api.moe_profile_hist(self.X, self.Wq, self.wscale, self.bias, w.k, self.counts, idx8)
 
     def merge(self, counts: Optional[torch.Tensor] = None):
         """Plan from `counts` (default: this layer's histogram), merge, slot tables."""

@@ -151,6 +151,7 @@ class QuantizedStack:
             api.moe_residual_add(X, self.Y, Xn)
             mark("combine")
             if self.record:
-                self.trace.append({"idx": self.idx.clone(), "gate": self.gate.clone(), "X": X.clone()})
+                self.trace.append({"idx": self.idx.clone(), "gate": self.gate.clone(), "X": X.clone(),
+                                   "Y": self.Y.clone()})
             X, Xn = Xn, X
         return X

@@ -70,6 +70,22 @@ def compare_topk(idx_gpu, logits_gpu, idx_ref, logits_ref, k):
     return int(excl.sum()), bad
 
 
+def compare_hist(counts_g, idx8_g, ref, k, E):
+    """The int8 profiling histogram, bit-exact outside the near-tie window: the
+    GPU's per-token top-k sets (moe_profile_hist's idx) against the oracle's on
+    its int8 logits (compare_topk), then both histograms with the choices of
+    the excluded tokens removed must be equal.  Returns the excluded count."""
+    excl_n, bad = compare_topk(idx8_g, None, ref.idx8, ref.logits8, k)
+    assert bad == 0, f"{bad} tokens outside the tie window take another int8 top-k set"
+    excl = O.topk_gap(ref.logits8, k) < GAP
+    idx8_g = np.asarray(idx8_g)
+    g_adj = np.asarray(counts_g) - np.bincount(idx8_g[excl].ravel(), minlength=E)
+    r_adj = np.asarray(ref.counts) - np.bincount(np.asarray(ref.idx8)[excl].ravel(), minlength=E)
+    np.testing.assert_array_equal(g_adj, r_adj)
+    assert int(np.sum(counts_g)) == idx8_g.size
+    return excl_n
+
+
 class OracleLayer:
     """fp64 oracle of one layer for given inputs: routing, profile, plan, merge,
     and the slot weights the forward/backward run on."""

@@ -259,3 +259,55 @@ def test_quantised_forward_rejections(L):
     need = L.moe_grouped_swiglu_fwd_q8_workspace_size(ctypes.byref(lay()), 4096, 6)
     assert call(lay(), ws_bytes=need - 1)[0] == api.MOE_ERR_WORKSPACE
     assert call(lay(), T=0, X=None, Xp=None, off=None, H=None, O=None, ws=None)[0] == api.MOE_OK   # nothing to do
+
+
+def test_validate_routing_rejects_out_of_range_maps(L):
+    """The debug-only range check of moe_permute's idx and expert_map (host arrays)."""
+    import numpy as np
+    idx = np.array([[0, 3], [2, 1], [3, 0]], dtype=np.int32)
+    emap = np.array([1, 0, 2, 2], dtype=np.int32)
+    assert api.moe_validate_routing(idx, emap, 3) == api.MOE_OK
+    assert api.moe_validate_routing(idx, None, 4) == api.MOE_OK        # identity map, S >= E
+    bad = idx.copy(); bad[1, 1] = 4
+    with pytest.raises(api.MoeError) as e:
+        api.moe_validate_routing(bad, emap, 3)
+    assert e.value.code == api.MOE_ERR_ARG and "idx[1][1]=4" in str(e.value)
+    bad[1, 1] = -1
+    with pytest.raises(api.MoeError):
+        api.moe_validate_routing(bad, emap, 3)
+    bmap = emap.copy(); bmap[3] = 3                                      # slot 3 of 3 slots
+    with pytest.raises(api.MoeError) as e:
+        api.moe_validate_routing(idx, bmap, 3)
+    assert "expert_map[3]=3" in str(e.value)
+    with pytest.raises(api.MoeError):
+        api.moe_validate_routing(idx, None, 3)                           # identity map needs S >= E
+    assert api.moe_validate_routing(np.zeros((0, 2), np.int32), emap, 3) == api.MOE_OK
+
+
+def test_backward_without_tokens_needs_only_offsets_and_workspace(L):
+    """T = 0: the per-token buffers may be NULL; offsets and the workspace are
+    what the zeroing of the weight gradients reads, so they stay required."""
+    lay = api.moe_layer(2048, 1408, api.MOE_BF16, 40, 2, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+    need = ctypes.c_size_t(L.moe_grouped_swiglu_bwd_workspace_size(ctypes.byref(lay), 0, 6))
+    rc, msg = rc_and_msg(L, "moe_grouped_swiglu_bwd", ctypes.byref(lay), None, None, None, 0, 6, None, None, None,
+                         None, None, 0, FAKE, need, None)
+    assert rc == api.MOE_ERR_ARG and "offsets" in msg
+    rc, msg = rc_and_msg(L, "moe_grouped_swiglu_bwd", ctypes.byref(lay), None, None, FAKE, 0, 6, None, None, None,
+                         None, None, 0, None, need, None)
+    assert rc == api.MOE_ERR_ARG and "ws" in msg
+    # accumulating into dW with no rows: nothing to do, every pointer may be NULL
+    rc, _ = rc_and_msg(L, "moe_grouped_swiglu_bwd", ctypes.byref(lay), None, None, None, 0, 6, None, None, None,
+                       None, None, 1, None, ctypes.c_size_t(0), None)
+    assert rc == api.MOE_OK
+
+
+def test_binding_rejects_misdescribed_tensors():
+    """The binding refuses tensors whose dtype, layout or device the library
+    would misread (checked before any library call)."""
+    import torch
+    i64 = torch.zeros(4, 2, dtype=torch.int64)
+    with pytest.raises(ValueError):                                      # host tensor
+        api.ptr(i64)
+    with pytest.raises(ValueError):                                      # strided view
+        api.ptr(torch.zeros(4, 4)[:, ::2])
+    assert api.ptr(None) is None and api.ptr(1 << 20) == 1 << 20

@@ -293,3 +293,59 @@ def test_cluster_full_size_layers():
     B, _ = O.merge_budget(counts_all, tun_all.astype(bool), w.T, 840)
     log(f"full size: Eq. 1 budgets {B[layers].tolist()}")
     check_clusters(st, B[layers], 16, 100, exact=False)
+
+
+def pair_agreement(a, b):
+    """Share of expert pairs that both labelings place alike (together in both,
+    or apart in both): label values themselves are arbitrary."""
+    a, b = np.asarray(a), np.asarray(b)
+    sa, sb = a[:, None] == a[None, :], b[:, None] == b[None, :]
+    iu = np.triu_indices(len(a), 1)
+    return float(np.mean(sa[iu] == sb[iu])) if len(a) > 1 else 1.0
+
+
+@pytest.mark.timeout(900)
+def test_cluster_benchmark_configuration():
+    """The benchmark's clustering configuration on layers 0, 9, 18 and 27 of the
+    DeepSeek-MoE stack: 32 planted classes, mix 0.6, top-16 tuning (48
+    clustered experts per layer), r = 16 and the Eq. 1 budgets of 840 slots over
+    the 28 layers.  With r below the number of classes the r-th and (r+1)-th
+    principal components can be close, and then the features are not unique.
+    The cosine matrix of the features is compared wherever the oracle's
+    relative eigengap (lambda_r - lambda_{r+1}) / lambda_1 is at least 1e-3: the
+    GPU's Gram entries carry fp32 rounding of about 1e-6 of lambda_1, which then
+    moves the projected Gram matrix by at most about 1e-3.  Labels are checked
+    for validity (in range, converged labels a fixed point under the GPU's own
+    features), and their agreement with the oracle's labels (share of expert
+    pairs placed alike) is reported."""
+    w = W.WORKLOADS["deepseek_stack"]
+    K, mix, r, max_iter = 32, 0.6, 16, 100
+    layers = [0, 9, 18, 27]
+    counts_all = stack_counts(w, range(w.n_layers))
+    tun_all = np.stack([tuning_mask(c, w.n_tune) for c in counts_all])
+    B, _ = O.merge_budget(counts_all, tun_all.astype(bool), w.T, 840)
+    budget = B[layers]
+    log(f"benchmark clustering: layers {layers}, Eq. 1 budgets {budget.tolist()}; drawing planted experts")
+    st = Stack(w, layers, tun_all[layers], n_classes=K, mix=mix)
+    got_lab, got_f, got_it = check_clusters(st, budget, r, max_iter, exact=False)
+    feats, labels, passes, mems, Bs = st.oracle(budget, r, max_iter)
+    compared = 0
+    for li, l in enumerate(layers):
+        mem = mems[li]
+        wg, wu, wd = (m.f64() for m in st.host[li])
+        V = O.expert_vectors(wg[mem], wu[mem], wd[mem])
+        V = V - V.mean(axis=0)
+        lam = np.sort(np.linalg.eigvalsh(V @ V.T))[::-1]
+        gap = (lam[r - 1] - lam[r]) / lam[0]
+        Zg = got_f[li][mem].astype(np.float64)
+        Zo = O.unit_rows(feats[li])
+        err = np.max(np.abs(Zg @ Zg.T - Zo @ Zo.T))
+        agree = pair_agreement(got_lab[li][mem], labels[li])
+        log(f"layer {l}: n={len(mem)} B={Bs[li]} relative eigengap {gap:.2e} cos err {err:.2e} "
+            f"label pair agreement {agree:.4f} (labels equal: {np.array_equal(got_lab[li][mem], labels[li])}) "
+            f"passes gpu {got_it[li]} oracle {passes[li]}")
+        if gap >= 1e-3:
+            assert err <= TOL_COS, (l, gap, err)
+            compared += 1
+        del V, wg, wu, wd
+    log(f"benchmark clustering: cosine matrices compared on {compared} of {len(layers)} layers")

@@ -13,7 +13,7 @@ from paper_2508_19078_amd import api
 from paper_2508_19078_amd import workloads as W
 from paper_2508_19078_amd.layer import LayerInputs, MoELayerRunner
 
-from gpu_harness import GAP, TOL_FFN, TOL_MERGE, OracleLayer, compare_topk, host, log, rel_fro, rne_bf16
+from gpu_harness import GAP, TOL_FFN, TOL_MERGE, OracleLayer, compare_hist, compare_topk, host, log, rel_fro, rne_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -63,10 +63,11 @@ class EdgeRun:
         self.ref = ref = OracleLayer(w, inp)
         r = MoELayerRunner(w, inp)
         self.r = r
-        r.profile()
+        idx8 = torch.full((w.T, w.k), -1, dtype=torch.int32, device="cuda")
+        r.profile(idx8=idx8)
         api.moe_route_topk(r.X, r.Wr, r.bias, w.k, r.idx, r.gate, r.logits)
         self.idx_g, self.gate_g, self.logits_g = host(r.idx), host(r.gate), host(r.logits)
-        self.counts_g = host(r.counts)
+        self.counts_g, self.idx8_g = host(r.counts), host(idx8)
         r.merge(counts=torch.from_numpy(ref.counts.astype(np.int32)).cuda())
         r.forward(idx=torch.from_numpy(ref.idx.astype(np.int32)).cuda(),
                   gate=torch.from_numpy(ref.gate.astype(np.float32)).cuda())
@@ -95,6 +96,7 @@ def test_edge_routing(run):
         return
     excl, bad = compare_topk(run.idx_g, run.logits_g, ref.idx, ref.logits, w.k)
     assert bad == 0 and excl <= 1
+    assert compare_hist(run.counts_g, run.idx8_g, ref, w.k, w.E) <= 1
     np.testing.assert_array_equal(run.counts_g, ref.counts)
     if run.name == "k_equals_E":
         sm = np.exp(ref.logits - ref.logits.max(1, keepdims=True))
@@ -158,14 +160,14 @@ def test_router_limits():
     sc = torch.empty(w.E, dtype=torch.float32, device="cuda")
     counts = torch.zeros(w.E, dtype=torch.int32, device="cuda")
     api.moe_quantize_int8(Wr, Wq, sc)
-    api.moe_profile_hist(X, Wq, sc, bias, w.k, counts)
+    idx8 = torch.full((w.T, w.k), -1, dtype=torch.int32, device="cuda")
+    api.moe_profile_hist(X, Wq, sc, bias, w.k, counts, idx8)
     excl, bad = compare_topk(host(idx), host(logits), ref.idx, ref.logits, w.k)
     assert bad == 0 and excl <= 2
     c = host(counts)
     assert c.sum() == w.T * w.k
-    excl8 = O.topk_gap(ref.logits8, w.k) < GAP
-    adj = np.bincount(ref.idx8[excl8].ravel(), minlength=w.E)
-    assert np.abs(c - ref.counts).sum() <= 2 * adj.sum()
+    excl8 = compare_hist(c, host(idx8), ref, w.k, w.E)
+    log(f"router limits: {excl} / {excl8} tokens in the tie windows")
 
 
 def test_empty_calls_launch_nothing():
@@ -182,6 +184,55 @@ def test_empty_calls_launch_nothing():
     assert api.moe_profile_hist(X, Wq, sc, None, k, counts) == 0
     torch.cuda.synchronize()
     assert (host(idx) == -7).all() and (host(counts) == 5).all()
+
+
+def test_backward_without_tokens_zeroes_weight_gradients():
+    """T = 0 with every per-token buffer NULL: a non-accumulating backward
+    writes zero weight gradients (only offsets and the workspace are read);
+    an accumulating one leaves them as they are."""
+    d, I, S_r, n_sh, k = 128, 64, 3, 1, 2
+    dt = torch.bfloat16
+    S = S_r + n_sh
+    Wg = torch.randn(S, I, d, device="cuda").to(dt)
+    Wu = torch.randn(S, I, d, device="cuda").to(dt)
+    Wd = torch.randn(S, d, I, device="cuda").to(dt)
+    dWg = torch.full((S, I, d), 3.0, device="cuda")
+    dWu = torch.full((S, I, d), 3.0, device="cuda")
+    dWd = torch.full((S, d, I), 3.0, device="cuda")
+    tun = [0, 2, 3]                                    # slot 1 frozen
+    dw = lambda t: [t[s] if s in tun else None for s in range(S)]
+    lay = api.LayerTables(d, I, dt, S_r, n_sh, list(Wg), list(Wu), list(Wd), dw(dWg), dw(dWu), dw(dWd))
+    offsets = torch.zeros(S_r + 1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(api.moe_grouped_swiglu_bwd_workspace_size(lay, 0, k), dtype=torch.uint8, device="cuda")
+    assert api.moe_grouped_swiglu_bwd(lay, None, None, offsets, 0, k, None, None, None, None, None, True, ws) == 0
+    torch.cuda.synchronize()
+    assert bool((dWg == 3).all() and (dWu == 3).all() and (dWd == 3).all())
+    assert api.moe_grouped_swiglu_bwd(lay, None, None, offsets, 0, k, None, None, None, None, None, False, ws) == 0
+    torch.cuda.synchronize()
+    for t in (dWg, dWu, dWd):
+        for s in range(S):
+            assert bool((t[s] == 0).all()) == (s in tun), s
+        assert bool((t[1] == 3).all())
+
+
+def test_permute_with_debug_range_checks(monkeypatch):
+    """FLUXMOE_DEBUG_CHECKS: moe_permute copies idx and expert_map to the host
+    and range-checks them before launching; valid maps give the same result as
+    without the checks (the rejection of invalid maps is a host-only test)."""
+    w = W.scaled(W.WORKLOADS["deepseek_moe"], name="dbg", cid=209, T=300, d=64, I=64)
+    inp = LayerInputs(w)
+    r = MoELayerRunner(w, inp)
+    r.profile()
+    r.merge()
+    r.route()
+    r.forward()
+    torch.cuda.synchronize()
+    plain = [host(t).copy() for t in (r.offsets, r.perm_token, r.inv, r.X_perm)]
+    monkeypatch.setenv("FLUXMOE_DEBUG_CHECKS", "1")
+    r.forward()
+    torch.cuda.synchronize()
+    for a, t in zip(plain, (r.offsets, r.perm_token, r.inv, r.X_perm)):
+        np.testing.assert_array_equal(a, host(t))
 
 
 def test_step_is_deterministic():

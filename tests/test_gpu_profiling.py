@@ -2,7 +2,7 @@
 against the fp64 oracle.
 
 Layer 0 sees the same input on both sides: its top-k sets and histogram must
-match bit-exactly outside a 1e-5 near-tie window, its gates to fp32
+match bit-exactly outside the 1e-6 near-tie window, its gates to fp32
 precision.  Deeper layers see the stream the layers before them produced, which
 the GPU carries in bf16.  A token that took another expert set in an earlier
 layer (only possible at a near tie) has a legitimately different stream from
@@ -10,9 +10,14 @@ then on; over the other tokens the stream must stay within the 2e-2 relative
 Frobenius bar.  A token's top-k set must match wherever the oracle's gap
 between its k-th and (k+1)-th logit exceeds twice the largest change the
 difference of the two streams makes to one of its logits (s_e <dX_t, q_e>,
-computed here from the two streams) plus a 1e-5 window for fp32 accumulation;
-the histograms are compared after removing the excluded tokens' choices from
-both sides.  The excluded share is reported and bounded."""
+computed here from the two streams) plus the 1e-6 window; the histograms are
+compared after removing the excluded tokens' choices from both sides.  The
+excluded share is reported and bounded.
+
+The teacher-forced check removes the drift: the oracle routes each layer on
+the GPU's own bf16 input to that layer, so every layer of the 28-layer stack
+must give bit-exact top-k sets and histograms outside the 1e-6 window, and the
+layer output Y within the 2e-2 bar."""
 import numpy as np
 import pytest
 import torch
@@ -26,7 +31,12 @@ from gpu_harness import gaps_of, host, log, rel_fro
 pytestmark = pytest.mark.gpu
 
 TOL_X = 2e-2
-WIN = 1e-5          # fp32 accumulation of the GPU's logits
+WIN = 1e-6          # the near-tie window of the routing bar
+# Share of tokens a chained layer may exclude: its window grows with the
+# difference between the GPU's bf16 stream and the oracle's fp64 one.  Measured:
+# 7.6 % at the second full-size DeepSeek-stack layer, 4.1-4.3 % on the small
+# stacks; the bound leaves half as much again.
+MAX_EXCLUDED = 0.12
 
 
 def stack_inputs(w, L):
@@ -46,7 +56,7 @@ def stack_inputs(w, L):
     return dev, ora, W.draw_x(w, 0)
 
 
-def check_stack(w, L, max_excluded=0.25, fused=None):
+def check_stack(w, L, max_excluded=MAX_EXCLUDED, fused=None):
     dev, ora, X0 = stack_inputs(w, L)
     log(f"stack {w.name}: L={L} T={w.T} d={w.d} E={w.E}+{w.n_shared} k={w.k} I={w.I} fused={fused}")
     st = QuantizedStack(dev, w.T, w.k, record=True, fused=fused)
@@ -121,3 +131,94 @@ def test_profiling_stack_full_size_layers():
     28-layer pass."""
     w = W.WORKLOADS["deepseek_stack"]
     check_stack(w, 2)
+
+
+def test_profiling_stack_llama_moe_layers():
+    """Two layers at the LLaMA-MoE shape (T = 4096, d = 4096, 16 experts,
+    top-4, I = 688): the int8 router and int8 experts this workload profiles
+    with, I = 688 ending inside a column tile and a K slab."""
+    w = W.WORKLOADS["llama_moe"]
+    check_stack(w, 2)
+
+
+def draw_stack_on_gpu(w, L, seed):
+    """The stack's weights drawn on the GPU with torch's seeded generator (the
+    28 layers hold 31 GB of bf16 experts): router N(0, 1/d), the workload's
+    router bias, W_gate, W_up ~ N(0, 1/d), W_down ~ N(0, 1/I); X0 ~ N(0, 1)."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    E, d, I, T = w.E, w.d, w.I, w.T
+    rn = lambda *shape, std: (torch.randn(*shape, generator=g, device="cuda") * std).to(torch.bfloat16)
+    layers = []
+    for l in range(L):
+        layers.append(dict(Wr=rn(E, d, std=d ** -0.5), bias=torch.from_numpy(W.router_bias(w, l)).cuda(),
+                           wg=rn(E, I, d, std=d ** -0.5), wu=rn(E, I, d, std=d ** -0.5),
+                           wd=rn(E, d, I, std=I ** -0.5)))
+    X0 = torch.randn(T, d, generator=g, device="cuda").to(torch.bfloat16)
+    return layers, X0
+
+
+def f64_of(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.timeout(900)
+def test_profiling_stack_teacher_forced_all_layers():
+    """All 28 layers of the DeepSeek-MoE stack (T = 4096, d = 2048, 64 experts,
+    top-6, I = 1408) in the launch configuration of the benchmark's profiling
+    pass.  Per layer, the oracle's int8 router runs on the GPU's own bf16 input
+    to that layer: top-k sets and histogram bit-exact outside the 1e-6 window,
+    gates to 1e-5.  On layers 0, 9, 18 and 27 the oracle also runs the layer's
+    dequantised experts on that input: Y within the 2e-2 bar over the tokens
+    routed alike."""
+    w = W.WORKLOADS["deepseek_stack"]
+    L, k, E = w.n_layers, w.k, w.E
+    torch.cuda.empty_cache()
+    log(f"teacher-forced stack: drawing {L} layers on the GPU")
+    layers, X0 = draw_stack_on_gpu(w, L, 2508190782)
+    st = QuantizedStack(layers, w.T, k, record=True)
+    assert st.fused
+    Y_checked = (0, 9, 18, 27)
+    ora_layers = {l: dict(Wr=f64_of(layers[l]["Wr"]), bias=layers[l]["bias"].cpu().numpy(),
+                          wg=f64_of(layers[l]["wg"]), wu=f64_of(layers[l]["wu"]), wd=f64_of(layers[l]["wd"]))
+                  for l in Y_checked}
+    routers = [(f64_of(lay["Wr"]), lay["bias"].cpu().numpy()) for lay in layers]
+    del layers
+    torch.cuda.empty_cache()
+    st.run(X0)
+    torch.cuda.synchronize()
+    counts_g = st.counts.cpu().numpy()
+    total_excl = 0
+    for l in range(L):
+        tr = st.trace[l]
+        Xg = host(tr["X"])
+        ig, gg = tr["idx"].cpu().numpy(), tr["gate"].cpu().numpy()
+        Wr, bias = routers[l]
+        q, s = O.quantize_int8_rows(Wr)
+        lg = O.profile_logits(Xg, q, s, bias)
+        io = O.topk_select(lg, k)
+        go = O.softmax_rows(np.take_along_axis(lg, io, axis=1))
+        excl = gaps_of(lg, k) < WIN
+        keep = ~excl
+        bad = sum(set(ig[t]) != set(io[t]) for t in np.nonzero(keep)[0])
+        cg = counts_g[l] - np.bincount(ig[excl].ravel(), minlength=E)
+        co = np.bincount(io[keep].ravel(), minlength=E)
+        total_excl += int(excl.sum())
+        log(f"  layer {l}: {excl.sum()} of {w.T} tokens in the tie window, {bad} mismatched")
+        assert bad == 0, l
+        np.testing.assert_array_equal(cg, co, err_msg=f"layer {l}")
+        assert counts_g[l].sum() == w.T * k
+        # gates of the kept tokens, matched by expert
+        o_by = np.zeros((w.T, E))
+        np.put_along_axis(o_by, io, go, axis=1)
+        g_match = np.take_along_axis(o_by, ig.astype(np.int64), axis=1)
+        np.testing.assert_allclose(gg[keep], g_match[keep], rtol=0, atol=1e-5)
+        if l in Y_checked:
+            _, idx_o, _, Xs = O.quantized_stack_profile(Xg, [ora_layers[l]], k)
+            assert np.array_equal(idx_o[0], io)
+            same = np.array([set(ig[t]) == set(io[t]) for t in range(w.T)])
+            err = rel_fro(host(tr["Y"])[same], (Xs[1] - Xg)[same])
+            log(f"  layer {l}: Y rel err {err:.2e} over {same.sum()} tokens routed alike")
+            assert err <= TOL_X, (l, err)
+    log(f"teacher-forced stack: {total_excl} of {L * w.T} token-layers in the tie window")
+    assert total_excl <= L * w.T // 1000

@@ -6,10 +6,11 @@ the whole int8 range (-128 included) and fed to both sides as inputs.
 H and O must be within the 2e-2 relative Frobenius bar of the bf16 products
 (each shape is reported).  Shapes: K tails inside a slab (d = 272, I = 208),
 intermediate and hidden sizes below one tile (I = 48, d = 64), an empty slot, a
-shared expert, a layer of shared experts only (no routed slot), and a
-full-size DeepSeek-stack layer (T = 4096, d = 2048, 64 experts, top-6,
-I = 1408) in the launch configuration of the profiling pass, compared on a
-seeded sample of rows."""
+shared expert, a layer of shared experts only (no routed slot), and
+full-size layers in the launch configuration of the profiling pass, every row
+compared: a DeepSeek-stack layer (T = 4096, d = 2048, 64 experts, top-6,
+I = 1408) and a LLaMA-MoE layer (T = 4096, d = 4096, 16 experts, top-4,
+I = 688: a partial column tile and a partial K slab)."""
 import numpy as np
 import pytest
 import torch
@@ -26,7 +27,8 @@ CASES = {
     "ragged_tails_empty_slot": (300, 272, 8, 2, 208, 1, 7, None),
     "below_one_tile": (5, 64, 4, 2, 48, 0, 4, None),
     "shared_experts_only": (77, 128, 0, 1, 96, 2, 0, None),
-    "full_deepseek_stack_layer": (4096, 2048, 64, 6, 1408, 0, 64, 384),
+    "full_deepseek_stack_layer": (4096, 2048, 64, 6, 1408, 0, 64, None),
+    "full_llama_moe_layer": (4096, 4096, 16, 4, 688, 0, 16, None),
 }
 
 

@@ -206,6 +206,17 @@ def test_frequency_plan_golden():
                                g["alpha_equals_counts_merge_coefficients"]["group1"])
 
 
+def test_explicit_plan_golden():
+    g = json.load(open(os.path.join(GOLD, "explicit_merge_plan_example.json")))
+    for c in g["cases"]:
+        plan = O.explicit_merge_plan(c["E"], c["groups"], tune_all=c["tune_all"])
+        assert plan.kept == c["kept"], c["note"]
+        assert plan.groups == c["groups"], c["note"]
+        assert plan.S == c["S"], c["note"]
+        np.testing.assert_array_equal(plan.expert_map, c["expert_map"], err_msg=c["note"])
+        np.testing.assert_array_equal(plan.tuning, c["tuning"], err_msg=c["note"])
+
+
 def test_frequency_plan_properties():
     r = rng(8)
     counts = r.integers(0, 50, size=64)
@@ -425,3 +436,35 @@ def test_grad_columns_match_central_differences():
     np.testing.assert_allclose(dWg, _fd(f, Wg)[cols], rtol=1e-7, atol=1e-8)
     np.testing.assert_allclose(dWu, _fd(f, Wu)[cols], rtol=1e-7, atol=1e-8)
     np.testing.assert_allclose(dWd, _fd(f, Wd)[:, cols], rtol=1e-7, atol=1e-8)
+
+
+def test_expert_utility_rank_one_route_equals_per_token_gradients():
+    """The batched utility (norms of rank-one products) against the explicit
+    per-token gradients of expert_utility, which the autograd test above pins:
+    several routed slots with folded choices (two experts of a token in one
+    merged slot), an empty slot, a frozen slot, two shared experts and unequal
+    gates; then a random layer with ties of slots across many tokens."""
+    r = rng(33)
+    T, d, I, E, k = 40, 6, 7, 6, 3
+    X, dY = r.normal(size=(T, d)), r.normal(size=(T, d))
+    S_r, n_sh = 5, 2
+    mats = [(r.normal(size=(I, d)), r.normal(size=(I, d)), r.normal(size=(d, I))) for _ in range(S_r + n_sh)]
+    slots = O.SlotWeights([m[0] for m in mats], [m[1] for m in mats], [m[2] for m in mats],
+                          [True, False, True, True, True, True, True], n_shared=n_sh)
+    emap = np.array([0, 1, 2, 2, 0, 4])           # experts 2 and 3 share slot 2, 0 and 4 share slot 0
+    idx = np.stack([r.choice(E, size=k, replace=False) for _ in range(T)])
+    idx[idx == 5] = 4                            # nothing reaches slot 4... through expert 5
+    idx[:, 0] = np.where(idx[:, 0] == 4, 1, idx[:, 0])
+    z = r.normal(size=(T, k))
+    gate = np.exp(z) / np.exp(z).sum(1, keepdims=True)
+    u_ref = O.expert_utility(X, dY, idx, gate, emap, slots)
+    u = O.expert_utility_rank_one(X, dY, idx, gate, emap, slots)
+    folded = sum(len(set(emap[idx[t]])) < k for t in range(T))
+    assert folded > 0
+    np.testing.assert_allclose(u, u_ref, rtol=1e-12, atol=0)
+    assert np.array_equal(u == 0, u_ref == 0)
+    # a plain random layer
+    idx2 = np.stack([r.choice(E, size=k, replace=False) for _ in range(T)])
+    emap2 = np.array([0, 1, 2, 3, 4, 4])
+    np.testing.assert_allclose(O.expert_utility_rank_one(X, dY, idx2, gate, emap2, slots),
+                               O.expert_utility(X, dY, idx2, gate, emap2, slots), rtol=1e-12)
