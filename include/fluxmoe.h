@@ -314,6 +314,26 @@ int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
                 int32_t* inv, void* X_perm, void* ws, size_t ws_bytes, void* stream);
 size_t moe_permute_workspace_size(int T, int k, int S_routed);
 
+/* moe_permute_noalloc: moe_permute for callers that cannot allocate device
+ * memory or hand over a workspace (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, outputs and
+ * errors as moe_permute, without (ws, ws_bytes): the count table lives in a
+ * device array of the library, moe_permute_noalloc_max_bytes() bytes (1 MiB)
+ * on each device it runs on, held until the process ends.  Calls whose table,
+ * moe_permute_workspace_size(T, k, S_routed), exceeds that are rejected with
+ * MOE_ERR_UNSUPPORTED before anything is enqueued (e.g. T <= 131072 tokens at
+ * 512 slots, T <= 1048576 at 64).  Every call on a device shares the array:
+ * calls that overlap on one device (several streams or threads) race and must
+ * be serialised by the caller.  Calls no allocating routine; the first call on
+ * a device looks the array's address up (hipGetSymbolAddress).  The debug
+ * range check of FLUXMOE_DEBUG_CHECKS is not run by this variant.
+ */
+int moe_permute_noalloc(const void* X, int dtype, const int32_t* idx, const float* gate,
+                        const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
+                        int32_t* offsets, int32_t* perm_token, float* perm_gate,
+                        int32_t* inv, void* X_perm, void* stream);
+size_t moe_permute_noalloc_max_bytes(void);
+
 /* moe_validate_routing: range check of moe_permute's index inputs, for
  * debugging a caller (the routing it hands over must name experts that exist
  * and slots that exist, Section 7's re-routing table included).  idx [T,k] and

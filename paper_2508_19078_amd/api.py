@@ -58,6 +58,9 @@ _SIGS = {
                              _vp, _vp, _vp, _vp, _c_size, _vp]),
     "moe_permute_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
     "moe_validate_routing": (_c_int, [_vp, _vp, _c_int, _c_int, _c_int, _c_int]),
+    "moe_permute_noalloc": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp,
+                                     _vp, _vp, _vp, _vp, _vp]),
+    "moe_permute_noalloc_max_bytes": (_c_size, []),
     "moe_grouped_swiglu_fwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
                                         _c_size, _vp]),
     "moe_grouped_swiglu_fwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
@@ -299,6 +302,21 @@ def moe_permute(X, idx, gate, expert_map, S_routed, offsets, perm_token, perm_ga
                  ptr(expert_map, I32), T, d, E, k, S_routed, ptr(offsets, I32), ptr(perm_token, I32),
                  ptr(perm_gate, F32), ptr(inv, I32), ptr(X_perm, X.dtype), ptr(ws),
                  ws.numel() * ws.element_size() if ws is not None else 0, stream_ptr(stream))
+
+
+def moe_permute_noalloc(X, idx, gate, expert_map, S_routed, offsets, perm_token, perm_gate, inv, X_perm, E=None,
+                        stream=None):
+    """moe_permute without a workspace (the library's own device scratch)."""
+    T, d = X.shape
+    k = idx.shape[1]
+    E = E if E is not None else (expert_map.shape[0] if expert_map is not None else S_routed)
+    return _call("moe_permute_noalloc", ptr(X, FLOAT), dtype_code(X.dtype), ptr(idx, I32), ptr(gate, F32),
+                 ptr(expert_map, I32), T, d, E, k, S_routed, ptr(offsets, I32), ptr(perm_token, I32),
+                 ptr(perm_gate, F32), ptr(inv, I32), ptr(X_perm, X.dtype), stream_ptr(stream))
+
+
+def moe_permute_noalloc_max_bytes() -> int:
+    return lib().moe_permute_noalloc_max_bytes()
 
 
 def moe_validate_routing(idx, expert_map, S_routed, E=None):

@@ -15,6 +15,7 @@
 // Combine and the two backward gathers run one wave per token.
 #include <stdlib.h>
 
+#include <mutex>
 #include <vector>
 
 #include "common.hpp"
@@ -543,11 +544,13 @@ extern "C" size_t moe_permute_workspace_size(int T, int k, int S_routed) {
   return ((nblk * S_routed * sizeof(int32_t) + 255) / 256) * 256;
 }
 
-extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
-                           const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
-                           int32_t* offsets, int32_t* perm_token, float* perm_gate, int32_t* inv,
-                           void* X_perm, void* ws, size_t ws_bytes, void* stream) {
-  clear_error();
+namespace fm {
+namespace {
+
+// Validation of moe_permute's arguments other than the workspace.
+int permute_check(const void* X, int dtype, const int32_t* idx, const float* gate, const int32_t* expert_map,
+                  int T, int d, int E, int k, int S_routed, const int32_t* offsets, const int32_t* perm_token,
+                  const float* perm_gate, const int32_t* inv, const void* X_perm) {
   FM_TRY(check_tk(T, k));
   if (d <= 0 || E <= 0 || S_routed <= 0) return fail(MOE_ERR_ARG, "d=%d E=%d S_routed=%d", d, E, S_routed);
   if (E > 256 || k > E) return fail(MOE_ERR_UNSUPPORTED, "E=%d k=%d", E, k);
@@ -559,22 +562,25 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
   if (T > 0) {
     FM_TRY(need(X, "X")); FM_TRY(need(idx, "idx")); FM_TRY(need(gate, "gate"));
     FM_TRY(need(perm_token, "perm_token")); FM_TRY(need(perm_gate, "perm_gate"));
-    FM_TRY(need(inv, "inv")); FM_TRY(need(X_perm, "X_perm")); FM_TRY(need(ws, "ws"));
+    FM_TRY(need(inv, "inv")); FM_TRY(need(X_perm, "X_perm"));
   }
   FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(X_perm, "X_perm"));
-  FM_TRY(need_aligned(offsets, "offsets")); FM_TRY(need_aligned(ws, "ws"));
-  if (ws_bytes < moe_permute_workspace_size(T, k, S_routed))
-    return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
-                moe_permute_workspace_size(T, k, S_routed));
-  hipStream_t st = as_stream(stream);
+  FM_TRY(need_aligned(offsets, "offsets"));
+  return MOE_OK;
+}
+
+// The launches of a validated permute; bc = the count table (workspace).
+int permute_launch(const void* X, int dtype, const int32_t* idx, const float* gate, const int32_t* expert_map,
+                   int T, int d, int E, int k, int S_routed, int32_t* offsets, int32_t* perm_token,
+                   float* perm_gate, int32_t* inv, void* X_perm, int32_t* bc, hipStream_t st, const char* what,
+                   bool allow_debug) {
   if (T == 0) {
     hipLaunchKernelGGL(k_zero_i32, dim3(cdiv(S_routed + 1, 256)), dim3(256), 0, st, offsets,
                        S_routed + 1);
-    return check_launch("moe_permute");
+    return check_launch(what);
   }
-  if (debug_checks()) FM_TRY(debug_check_routing(idx, expert_map, T, E, k, S_routed, st));
+  if (allow_debug && debug_checks()) FM_TRY(debug_check_routing(idx, expert_map, T, E, k, S_routed, st));
   const int nblk = cdiv(T, PM_TOK);
-  int32_t* bc = (int32_t*)ws;
 #define FM_PC(KM) \
   hipLaunchKernelGGL(k_perm_count<KM>, dim3(nblk), dim3(PM_TOK), 0, st, idx, expert_map, T, k, S_routed, bc, \
                      nblk)
@@ -597,7 +603,92 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
   FM_KSWITCH(k, FM_PP)
 #undef FM_PP
 #undef FM_PS
-  return check_launch("moe_permute");
+  return check_launch(what);
+}
+
+}  // namespace
+}  // namespace fm
+
+extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
+                           const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
+                           int32_t* offsets, int32_t* perm_token, float* perm_gate, int32_t* inv,
+                           void* X_perm, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  FM_TRY(permute_check(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
+                       X_perm));
+  if (T > 0) FM_TRY(need(ws, "ws"));
+  FM_TRY(need_aligned(ws, "ws"));
+  if (ws_bytes < moe_permute_workspace_size(T, k, S_routed))
+    return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
+                moe_permute_workspace_size(T, k, S_routed));
+  return permute_launch(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
+                        X_perm, (int32_t*)ws, as_stream(stream), "moe_permute", true);
+}
+
+// ------------------------------------------------- no-allocation variant ----
+//
+// moe_permute_noalloc keeps its count table in a file-scope device array
+// instead of a caller workspace.  In host code `scratch` names a host-side
+// stand-in, not device memory: its device address is looked up per device
+// (hipGetSymbolAddress, on the first call on that device) and only that
+// address is handed to kernels.  Every call on a device shares the array, so
+// calls that overlap on one device race; each call overwrites every entry of
+// the table it reads (the count kernel stores all of them), so nothing has to
+// be cleared between calls.  The debug range check of moe_permute (a host copy
+// and a stream synchronisation) is not run here.
+namespace fm {
+namespace {
+constexpr size_t PERM_SCRATCH_BYTES = size_t(1) << 20;   // count tables of up to 262144 entries
+}  // namespace
+}  // namespace fm
+
+static __device__ __align__(256) char scratch[fm::PERM_SCRATCH_BYTES];
+
+namespace fm {
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[MAX_DEVICES] = {};
+
+// Device address of `scratch` on the current device.
+int scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(MOE_ERR_HIP, "moe_permute_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(MOE_ERR_UNSUPPORTED, "moe_permute_noalloc: device %d", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(MOE_ERR_HIP, "moe_permute_noalloc: hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return MOE_OK;
+}
+}  // namespace
+}  // namespace fm
+
+extern "C" size_t moe_permute_noalloc_max_bytes(void) { return PERM_SCRATCH_BYTES; }
+
+extern "C" int moe_permute_noalloc(const void* X, int dtype, const int32_t* idx, const float* gate,
+                                   const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
+                                   int32_t* offsets, int32_t* perm_token, float* perm_gate, int32_t* inv,
+                                   void* X_perm, void* stream) {
+  clear_error();
+  FM_TRY(permute_check(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
+                       X_perm));
+  const size_t need = moe_permute_workspace_size(T, k, S_routed);
+  if (need > PERM_SCRATCH_BYTES)
+    return fail(MOE_ERR_UNSUPPORTED,
+                "moe_permute_noalloc: T=%d tokens over S_routed=%d slots need a %zu-byte count table, above its "
+                "%zu-byte scratch; use moe_permute with a workspace",
+                T, S_routed, need, PERM_SCRATCH_BYTES);
+  void* p = nullptr;
+  FM_TRY(scratch_address(&p));
+  return permute_launch(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
+                        X_perm, (int32_t*)p, as_stream(stream), "moe_permute_noalloc", false);
 }
 
 extern "C" int moe_unpermute(const moe_layer* L, const void* O, const int32_t* inv,

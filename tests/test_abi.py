@@ -311,3 +311,17 @@ def test_binding_rejects_misdescribed_tensors():
     with pytest.raises(ValueError):                                      # strided view
         api.ptr(torch.zeros(4, 4)[:, ::2])
     assert api.ptr(None) is None and api.ptr(1 << 20) == 1 << 20
+
+
+def test_noalloc_permute_rejects_tables_above_its_scratch(L):
+    """The no-allocation permute refuses, on the host, a count table larger
+    than its fixed device scratch (1 MiB)."""
+    assert L.moe_permute_noalloc_max_bytes() == 1 << 20
+    T, S = 140000, 512
+    assert L.moe_permute_workspace_size(T, 8, S) > 1 << 20
+    rc, msg = rc_and_msg(L, "moe_permute_noalloc", FAKE, api.MOE_BF16, FAKE, FAKE, FAKE, T, 256, 256, 8, S, FAKE,
+                         FAKE, FAKE, FAKE, FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED and "scratch" in msg
+    rc, msg = rc_and_msg(L, "moe_permute_noalloc", FAKE, api.MOE_BF16, FAKE, FAKE, FAKE, 64, 256, 256, 17, S, FAKE,
+                         FAKE, FAKE, FAKE, FAKE, None)
+    assert rc == api.MOE_ERR_UNSUPPORTED                             # k > 16: validated as moe_permute does
