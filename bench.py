@@ -313,8 +313,9 @@ def layer_merging(reps=3, B_non=840, r=16, n_classes=32, mix=0.6, max_iter=100):
 def profiling_stack(reps=3):
     """The quantised profiling pass of Section 4.1 over the 28-layer
     DeepSeek-MoE stack (64 experts, d = 2048, I = 1408, top-6, T = 4096 tokens):
-    per layer int8 routing with the histogram, permute, the grouped SwiGLU
-    forward straight from the int8 expert codes, combine and the residual.  The
+    per layer int8 routing with the histogram on the RMS-normalised stream,
+    permute, the grouped SwiGLU forward straight from the int8 expert codes,
+    combine, and the residual add fused with the next layer's normalisation.  The
     weights are drawn on the GPU (torch's seeded generator, the workload's
     distributions) and quantised once; the pass is timed with HIP events per
     stage, median over `reps` passes after one warm-up."""
@@ -355,7 +356,7 @@ def profiling_stack(reps=3):
             ev.record(st)
             evs.append(ev)
             names.append(name)
-        qs.run(X0, mark)
+        Xout = qs.run(X0, mark)
         torch.cuda.synchronize()
         stages = {}
         for i, nm in enumerate(names):
@@ -367,13 +368,15 @@ def profiling_stack(reps=3):
     # the grouped forward's algorithmic flops: 6 d I per routed row (T k rows per layer; no shared experts)
     ffn_flops = 6.0 * d * I * T * k * L
     out = {"workload": f"deepseek_stack: {L} layers x {E} experts, d={d} I={I}, T={T}, top-{k}, int8 router "
-                       "and experts (per-row scales), residual stream",
+                       "and experts (per-row scales), RMS-normalised layer inputs, residual stream",
            "pass_ms": round(total, 3), "tokens_per_s": round(T / (total * 1e-3), 1),
            "stages_ms": stages, "quantise_ms": round(quant_ms, 3),
            "ffn_fwd_TFLOPs": round(ffn_flops / (stages["ffn_fwd"] * 1e-3) / 1e12, 1),
            "ffn_fwd_frac_bf16_peak": round(ffn_flops / (stages["ffn_fwd"] * 1e-3) / 2.5e15, 4),
            "int8_weight_bytes": int(sum(q[n][0].numel() for q in qs.q for n in ("wg", "wu", "wd", "Wr"))),
-           "hist_ok": bool((counts.sum(axis=1) == T * k).all())}
+           "hist_ok": bool((counts.sum(axis=1) == T * k).all()),
+           "stream_out_rms": round(float(Xout.float().pow(2).mean().sqrt()), 3),
+           "stream_finite": bool(torch.isfinite(Xout.float()).all())}
     del qs
     torch.cuda.empty_cache()
     return out

@@ -149,6 +149,20 @@ int moe_dequant_int8(const int8_t* q, const float* scale, long rows, int cols,
 int moe_residual_add(const void* X, const void* Y, int T, int d, int dtype,
                      void* out, void* stream);
 
+/* moe_rms_norm: the input of a layer of the profiling stack (Section 4.1 runs
+ * the low-bit copy of the paper's models, pre-norm transformers whose MoE
+ * layers read the RMS-normalised residual stream), optionally fused with the
+ * residual add that produces that stream:
+ *   S        = X + Y (fp32 add, one rounding to dtype), or S = X when Y is NULL
+ *   out_sum  = S                                   (when out_sum != NULL)
+ *   out_norm = S / sqrt(mean_i S[t,i]^2 + eps)     (per row, from the rounded S,
+ *              fp32, one rounding; unit gain; a zero row stays zero)
+ * X, Y, out_sum, out_norm [T,d] in dtype.  out_sum may alias X or Y; out_norm
+ * aliases none of them (MOE_ERR_ARG).  eps finite and >= 0; d % 8 == 0.
+ */
+int moe_rms_norm(const void* X, const void* Y, int T, int d, int dtype, float eps,
+                 void* out_sum, void* out_norm, void* stream);
+
 /* ---------------------------------------------------------------- merging --
  * moe_merge_plan: which experts of one layer are merged, from its histogram
  * (Sections 5.1-5.2 decide how many and which experts share a group; this

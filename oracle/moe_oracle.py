@@ -25,7 +25,8 @@ What each function follows:
 * Expert FFN: SwiGLU, out = W_down (silu(W_gate x) * (W_up x)).
 * Expert utility (Section 6.1, Eq. 3): the gradient-norm utility of a slot.
 * Quantised profiling of a layer stack (Section 4.1): int8 router and experts,
-  layers coupled by a residual stream.
+  each layer reading the RMS-normalised stream (the pre-norm of the paper's
+  models), layers coupled by a residual stream.
 * Layer-aware merging (Section 5): the per-layer budget of Eq. 1 (Section 5.1),
   then PCA features of the experts' parameters and K-Means with cosine
   distance over all layers at once, cross-layer pairs masked (Section 5.2).
@@ -680,14 +681,27 @@ def dequantize_rows(q, s) -> np.ndarray:
     return _f64(q) * _f64(s)[..., None]
 
 
-def quantized_stack_profile(X0, layers: Sequence[Dict], k: int):
+def rms_norm_rows(X, eps: float = 1e-6) -> np.ndarray:
+    """The normalisation in front of every MoE layer of the paper's models
+    (LLaMA-MoE and DeepSeek-MoE are pre-norm transformers with RMSNorm): each
+    row divided by its root mean square, X / sqrt(mean(X^2) + eps), unit gain;
+    a zero row stays zero (also with eps = 0)."""
+    X = _f64(X)
+    den = np.sqrt(np.mean(X * X, axis=1, keepdims=True) + eps)
+    return X / np.where(den > 0, den, 1.0)
+
+
+def quantized_stack_profile(X0, layers: Sequence[Dict], k: int, eps: float = 1e-6):
     """Profiling pass of Section 4.1 with a low-bit copy of a stack of MoE
     layers: each layer's router and expert matrices are quantised per row to
     int8 (quantize_int8_rows), and the layer runs on them — the int8 router's
     top-k and softmax gate, every routed expert (unmerged) with its dequantised
     weights q * s, and shared experts with gate 1.  The histogram of layer l
-    counts its top-k selections.  Layers are coupled by a residual stream,
-    X_{l+1} = X_l + Y_l (the synthetic stack has no other sublayers).
+    counts its top-k selections.  A layer reads the RMS-normalised stream
+    (rms_norm_rows), and layers are coupled by a residual stream,
+    X_{l+1} = X_l + Y_l(rms_norm(X_l)) (the synthetic stack has no attention or
+    other sublayers; without the normalisation the SwiGLU experts, quadratic in
+    their input, make the stream grow without bound over a deep stack).
     layers[l]: dict with Wr [E,d], bias [E] or None, wg [E,I,d], wu [E,I,d],
     wd [E,d,I] and optionally sg, su, sd (shared experts).
     Returns (counts [L][E] int64, idx [L][T,k], gate [L][T,k], X [L+1][T,d]).
@@ -695,8 +709,9 @@ def quantized_stack_profile(X0, layers: Sequence[Dict], k: int):
     X = _f64(X0)
     counts, idxs, gates, Xs = [], [], [], [X]
     for lay in layers:
+        Xn = rms_norm_rows(X, eps)
         q, s = quantize_int8_rows(lay["Wr"])
-        lg = profile_logits(X, q, s, lay.get("bias"))
+        lg = profile_logits(Xn, q, s, lay.get("bias"))
         idx = topk_select(lg, k)
         sel = np.take_along_axis(lg, idx, axis=1)
         gate = softmax_rows(sel)
@@ -718,7 +733,7 @@ def quantized_stack_profile(X0, layers: Sequence[Dict], k: int):
             wu = list(wu) + list(suq)
             wd = list(wd) + list(sdq)
         slots = SlotWeights(wg, wu, wd, [False] * (E + n_sh), n_shared=n_sh)
-        Y = moe_forward(X, idx, gate, np.arange(E), slots)
+        Y = moe_forward(Xn, idx, gate, np.arange(E), slots)
         X = X + Y
         idxs.append(idx)
         gates.append(gate)

@@ -77,6 +77,7 @@ _SIGS = {
                                    _vp]),
     "moe_dequant_int8": (_c_int, [_vp, _vp, ctypes.c_long, _c_int, _c_int, _vp, _vp]),
     "moe_residual_add": (_c_int, [_vp, _vp, _c_int, _c_int, _c_int, _vp, _vp]),
+    "moe_rms_norm": (_c_int, [_vp, _vp, _c_int, _c_int, _c_int, _f, _vp, _vp, _vp]),
     "moe_merge_budget": (_c_int, [_vp, _vp, _c_int, _c_int, _f, _c_int, ctypes.c_double, _vp, _vp]),
     "moe_cluster_workspace_size": (_c_size, [_c_int, _c_int, _c_int, _c_int]),
     "moe_cluster_experts": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _c_int, _c_int,
@@ -212,6 +213,13 @@ def moe_residual_add(X, Y, out, stream=None):
     T, d = X.shape
     return _call("moe_residual_add", ptr(X, FLOAT), ptr(Y, X.dtype), T, d, dtype_code(X.dtype), ptr(out, X.dtype),
                  stream_ptr(stream))
+
+
+def moe_rms_norm(X, Y, out_norm, out_sum=None, eps=1e-6, stream=None):
+    """out_norm = RMS-normalised (X + Y) (or X when Y is None); out_sum = X + Y."""
+    T, d = X.shape
+    return _call("moe_rms_norm", ptr(X, FLOAT), ptr(Y, X.dtype), T, d, dtype_code(X.dtype), float(eps),
+                 ptr(out_sum, X.dtype), ptr(out_norm, X.dtype), stream_ptr(stream))
 
 
 def moe_merge_plan(counts, n_merge, group, total_tokens, expert_map, slot_src, grp_ptr, grp_member,

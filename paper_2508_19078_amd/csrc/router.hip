@@ -117,12 +117,16 @@ __device__ __forceinline__ f32x4_t mma(f32x4_t a, f32x4_t b, f32x4_t c) {
 // Each of the k selection rounds takes the group maximum with four DPP row
 // rotations; the owner lane then drops it.  A group handles TPL tokens at once
 // (independent chains for the scheduler to interleave).
-template <int NE, int KMAX, int MODE, int WAVES, int NPART>
+// TT tokens (RT_TOK by default).  With FLUSH the LDS histogram is added to the
+// global counts at the end (MODE != 0); a persistent kernel passes false and
+// flushes once after its last tile.
+template <int NE, int KMAX, int MODE, int WAVES, int NPART, int TT = RT_TOK, bool FLUSH = true>
 __device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int EP, const float* scale,
                                              const float* bias, int t0, int T, int E, int k,
                                              int32_t* __restrict__ idx, float* __restrict__ gate,
                                              float* __restrict__ logits, int32_t* __restrict__ counts,
                                              int* hist) {
+  constexpr int RT_TOK = TT;
   constexpr int TPL = (RT_TOK + WAVES * 4 - 1) / (WAVES * 4);
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
@@ -212,7 +216,7 @@ __device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int
       if (MODE == 1 && idx) idx[(size_t)t * k + gl] = mye[u];
     }
   }
-  if (MODE != 0) {
+  if (MODE != 0 && FLUSH) {
     __syncthreads();
     for (int e = threadIdx.x; e < E; e += blockDim.x)
       if (hist[e]) atomicAdd(&counts[e], hist[e]);
@@ -508,6 +512,244 @@ __global__ __launch_bounds__(256) void k_route_lds(const bf16* __restrict__ X, c
                                                      counts, hist);
 }
 
+// Persistent router for bf16 activations, E <= 64 and d a multiple of the slab
+// width (256 columns for 32-token tiles, 128 for 64-token tiles).
+// A block owns tiles of TT tokens (32, or 64 once every compute unit gets a
+// whole 64-token tile) and walks tiles blockIdx.x, blockIdx.x + gridDim.x, ...
+// Slabs of the tile's X rows and of the router's rows (padded to
+// NEG * 32, rows past E clamped) stream global -> LDS through a ring of NS slabs
+// with paired-half DMA (each instruction 64 bytes of 16 rows, the same wave's
+// next one the other halves of those lines; 16-byte chunks XOR-swizzled by
+// (row >> 2) & 3).  The four waves split the work as expert groups of 32 x
+// NKS parts of each slab's eight 16-column k-steps; each wave keeps a 32 x 32
+// accumulator per 32 tokens of the tile (v_mfma_f32_32x32x16_bf16), so every
+// router fragment is read, and int8 codes widened exactly to bf16, by one wave
+// only; the NKS partial sums meet in LDS in a fixed order.  With 64-token tiles each router row read from L2 serves twice
+// the tokens.  Once a tile's last slab is read, the next tile's first NS - 1
+// slabs are issued, and the selection of the finished tile (a separate LDS
+// region) overlaps their latency.  The LDS histogram of MODE 1 and 2 is
+// flushed to `counts` once, after the block's last tile.
+template <typename TW> struct RpW;
+template <> struct RpW<bf16> {
+  static __device__ __forceinline__ bf16x8_t frag(const FM_LDS char* grp, int rr, int ks, int hf) {
+    // columns 16 ks + 8 hf .. + 8 (bytes 32 ks + 16 hf of the 256-byte slab row)
+    const int m = ks >> 2, h = (ks >> 1) & 1, q = ((ks & 1) << 1) | hf;
+    return *(const FM_LDS bf16x8_t*)(grp + (m * 2 + h) * 1024 + rr * 64 + ((q ^ ((rr >> 2) & 3)) << 4));
+  }
+};
+template <> struct RpW<int8_t> {
+  static __device__ __forceinline__ bf16x8_t frag(const FM_LDS char* grp, int rr, int ks, int hf) {
+    // codes 16 ks + 8 hf .. + 8: bytes 16 ks + 8 hf of the slab row (line ks / 8)
+    const int m = ks >> 3, h = (ks >> 2) & 1, q = ks & 3;
+    const u32x2_t raw =
+        *(const FM_LDS u32x2_t*)(grp + (m * 2 + h) * 1024 + rr * 64 + ((q ^ ((rr >> 2) & 3)) << 4) + hf * 8);
+    u32x4_t v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t x = raw[i >> 1];
+      const int sh = (i & 1) * 16;
+      const float lo = (float)(int8_t)((x >> sh) & 0xFF);
+      const float hi = (float)(int8_t)((x >> (sh + 8)) & 0xFF);
+      v[i] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xFFFF0000u);
+    }
+    return __builtin_bit_cast(bf16x8_t, v);
+  }
+};
+
+// Slabs of COLS hidden columns: 256 for 32-token tiles (half the slab steps),
+// 128 for 64-token tiles (measured faster than 256 with int8 codes, and a
+// 256-column bf16 slab would leave room for two in the ring).  The selection's
+// staging area lives in ring slot NS - 1, which is free while the next tile's
+// first NS - 1 slabs land.
+template <typename TW, int TT, int NEG> struct RpCfg {
+  static constexpr int COLS = TT == 32 ? 256 : 128;
+  static constexpr int NTG = TT / 32;                          // token groups (accumulators per wave)
+  static constexpr int NKS = 4 / NEG;                          // parts of a slab's k-steps
+  static constexpr int KSTEPS = COLS / 16;                     // 16-column MFMA k-steps per slab
+  static constexpr int KSP = KSTEPS / NKS;                     // k-steps per part
+  static constexpr int XROW = COLS * 2;                        // bytes of an X row per slab
+  static constexpr int WB = COLS * (int)sizeof(TW);            // bytes of a router row per slab
+  static constexpr int XLINES = XROW / 128, WLINES = WB / 128; // 128-byte lines per slab row
+  static constexpr int XBYTES = TT * XROW;
+  static constexpr int SLAB = XBYTES + NEG * 32 * WB;
+  static constexpr int NIX = (TT / 16) * XLINES * 2;           // X: row groups x lines x halves
+  static constexpr int NIW = NEG * 2 * WLINES * 2;             // W: row groups x lines x halves
+  static constexpr int INS = (NIX + NIW) / 4;                  // DMA instructions per wave and slab
+  static constexpr int EP = NEG * 32 + 1;                      // padded logit row
+  static constexpr int STAGE = TT * EP * 4;
+  static constexpr int NS0 = (159 * 1024) / SLAB;
+  static constexpr int NS = NS0 > 6 ? 6 : NS0;                 // ring depth
+  static_assert(NEG * NKS == 4 && (NIX + NIW) % 4 == 0 && NS >= 3, "router tile");
+  static_assert(STAGE <= SLAB && NS * SLAB + 3 * NEG * 32 * 4 <= 160 * 1024, "LDS");
+  static_assert((NS - 2) * INS < 64, "vmcnt range");
+};
+
+template <int N> __device__ __forceinline__ void wait_vm_upto(int n) {
+  // s_waitcnt vmcnt(n * N) for a small runtime n (0..5)
+  switch (n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<N>(); break;
+    case 2: wait_vmcnt<2 * N>(); break;
+    case 3: wait_vmcnt<3 * N>(); break;
+    case 4: wait_vmcnt<4 * N>(); break;
+    default: wait_vmcnt<5 * N>(); break;
+  }
+}
+
+template <typename TW, int TT, int NEG, int KMAX, int MODE>
+__global__ __launch_bounds__(256) void k_route_p(const bf16* __restrict__ X, const TW* __restrict__ W,
+                                                 const float* __restrict__ wscale, const float* __restrict__ bias,
+                                                 int T, int d, int E, int k, int32_t* __restrict__ idx,
+                                                 float* __restrict__ gate, float* __restrict__ logits,
+                                                 int32_t* __restrict__ counts) {
+  using C = RpCfg<TW, TT, NEG>;
+  constexpr int NS = C::NS, INS = C::INS, EP = C::EP;
+  __shared__ __align__(1024) char lds_raw[NS * C::SLAB];
+  float* const stage = (float*)(lds_raw + (NS - 1) * C::SLAB);   // ring slot NS - 1
+  __shared__ int hist[NEG * 32];
+  __shared__ float s_scale[NEG * 32], s_bias[NEG * 32];
+  FM_LDS char* ring = (FM_LDS char*)lds_raw;
+  const int lane = lane_id_here(), wave = wave_id();
+  const int ntiles = (T + TT - 1) / TT;
+  if (MODE != 0)
+    for (int e = threadIdx.x; e < NEG * 32; e += blockDim.x) hist[e] = 0;
+  if (threadIdx.x < E) {
+    s_scale[threadIdx.x] = wscale ? wscale[threadIdx.x] : 1.f;
+    s_bias[threadIdx.x] = bias ? bias[threadIdx.x] : 0.f;
+  }
+  // This wave's DMA instructions: u = wave * INS + q, X ones first.  Per lane:
+  // the row within the 16-row group and the swizzled 16-byte chunk.
+  const int rr = lane >> 2;
+  const uint32_t cb = (uint32_t)(((lane & 3) ^ ((rr >> 2) & 3)) << 4);
+  const char* gp[INS];
+  uint32_t dst[INS];
+  bool isx[INS];
+  const int nslab = d / C::COLS;
+  auto plan = [&](int t0) {
+#pragma unroll
+    for (int q = 0; q < INS; ++q) {
+      const int u = wave * INS + q;
+      isx[q] = u < C::NIX;
+      if (u < C::NIX) {
+        const int h = u & 1, m = (u >> 1) % C::XLINES, g = (u >> 1) / C::XLINES;
+        const int row = min(t0 + g * 16 + rr, T - 1);
+        gp[q] = (const char*)(X + (size_t)row * d) + m * 128 + h * 64 + cb;
+        dst[q] = (uint32_t)(((g * C::XLINES + m) * 2 + h) * 1024);
+      } else {
+        const int v = u - C::NIX, h = v & 1, m = (v >> 1) % C::WLINES, g = (v >> 1) / C::WLINES;
+        const int row = min(g * 16 + rr, E - 1);
+        gp[q] = (const char*)(W + (size_t)row * d) + m * 128 + h * 64 + cb;
+        dst[q] = (uint32_t)(C::XBYTES + ((g * C::WLINES + m) * 2 + h) * 1024);
+      }
+    }
+  };
+  // Blocks of one XCD start at different slabs (their rank within the XCD), so
+  // that the CUs sharing an L2 do not all ask for the same router lines at once.
+  const int s_off = (int)(blockIdx.x >> 3) % nslab;
+  auto issue = [&](int s) {
+    FM_LDS char* slab = ring + (s % NS) * C::SLAB;
+    int sg = s + s_off;
+    sg -= sg >= nslab ? nslab : 0;
+#pragma unroll
+    for (int q = 0; q < INS; ++q) dma16(gp[q] + (size_t)sg * (isx[q] ? C::XROW : C::WB), slab + dst[q]);
+  };
+  // this wave's share: an expert group and a part of every slab's k-steps, for
+  // all TT tokens (NTG accumulators), so that every router fragment is read,
+  // and for int8 widened, by one wave only
+  const int eg = wave % NEG, kp = wave / NEG;
+  const int i = lane & 31, hf = lane >> 5;
+  const int wr = eg * 32 + i;
+
+  int tile = blockIdx.x;
+  if (tile < ntiles) {
+    plan(tile * TT);
+    for (int s = 0; s < NS - 1 && s < nslab; ++s) issue(s);
+  }
+  bool first = true;
+  while (tile < ntiles) {
+    const int t0 = tile * TT;
+    // two independent accumulator chains per wave (token groups, or even and
+    // odd k-steps of a single token group), so consecutive MFMAs do not wait on
+    // each other's results
+    constexpr int NCH = C::NTG == 1 ? 2 : 1;
+    f32x16_t acc[C::NTG][NCH];
+#pragma unroll
+    for (int g = 0; g < C::NTG; ++g)
+#pragma unroll
+      for (int c = 0; c < NCH; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[g][c][r] = 0.f;
+    for (int s = 0; s < nslab; ++s) {
+      // slabs issued after s and possibly still in flight: min(NS - 2, nslab - 1 - s);
+      // the first slab of a later tile also waits for the epilogue's stores
+      const int after = min(NS - 2, nslab - 1 - s);
+      if (s == 0 && !first) wait_vmcnt<0>();
+      else wait_vm_upto<INS>(after);
+      barrier_lds();
+      const FM_LDS char* slab = ring + (s % NS) * C::SLAB;
+      const FM_LDS char* wg = slab + C::XBYTES + (wr >> 4) * C::WLINES * 2 * 1024;
+      // all of this part's fragments are requested at once, then the refill is
+      // issued while they land, then the MFMAs run (they retire while the wave
+      // waits for the next slab)
+      bf16x8_t xa[C::KSP][C::NTG], wb[C::KSP];
+#pragma unroll
+      for (int j = 0; j < C::KSP; ++j) {
+        const int ks = kp * C::KSP + j;
+        wb[j] = RpW<TW>::frag(wg, wr & 15, ks, hf);
+#pragma unroll
+        for (int g = 0; g < C::NTG; ++g) {
+          const int xr = g * 32 + i;
+          xa[j][g] = RpW<bf16>::frag(slab + (xr >> 4) * C::XLINES * 2 * 1024, xr & 15, ks, hf);
+        }
+      }
+      sched_fence();
+      if (s + NS - 1 < nslab) issue(s + NS - 1);
+      sched_fence();
+#pragma unroll
+      for (int j = 0; j < C::KSP; ++j)
+#pragma unroll
+        for (int g = 0; g < C::NTG; ++g)
+          acc[g][j % NCH] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xa[j][g], wb[j], acc[g][j % NCH], 0, 0, 0);
+    }
+    if (NCH == 2)
+#pragma unroll
+      for (int g = 0; g < C::NTG; ++g) acc[g][0] += acc[g][NCH - 1];
+    first = false;
+    // every wave is done with the ring: start the next tile's first slabs
+    barrier_lds();
+    const int next = tile + gridDim.x;
+    if (next < ntiles) {
+      plan(next * TT);
+      for (int s = 0; s < NS - 1 && s < nslab; ++s) issue(s);
+    }
+    // the parts' partial sums meet in the stage, the last part first and part 0
+    // last (a fixed order): register r of lane L is token 32 g + 8 (r / 4) +
+    // 4 (L / 32) + r % 4, expert 32 eg + L % 32
+    for (int p = C::NKS - 1; p >= 0; --p) {
+      if (kp == p) {
+#pragma unroll
+        for (int g = 0; g < C::NTG; ++g)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            float* q = &stage[(g * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)) * EP + eg * 32 + i];
+            *q = (p == C::NKS - 1) ? acc[g][0][r] : *q + acc[g][0][r];
+          }
+      }
+      __syncthreads();
+    }
+    route_select<(NEG * 32 + 15) / 16, KMAX, MODE, 4, 1, TT, false>(
+        stage, 0, EP, wscale ? s_scale : nullptr, bias ? s_bias : nullptr, t0, T, E, k, idx, gate, logits,
+        counts, hist);
+    __syncthreads();   // the stage is free again
+    tile = next;
+  }
+  if (MODE != 0) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x)
+      if (hist[e]) atomicAdd(&counts[e], hist[e]);
+  }
+}
+
 // Per-row symmetric int8 quantiser: one wave per row, 16-byte loads.
 template <typename T>
 __global__ __launch_bounds__(256) void k_quantize(const T* __restrict__ W, int E, int d,
@@ -547,12 +789,45 @@ __global__ __launch_bounds__(256) void k_quantize(const T* __restrict__ W, int E
   }
 }
 
+int route_cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+    n = 256;
+  return n;
+}
+
 template <typename TX, typename TW, int MODE>
 int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, int T, int d,
                  int E, int k, int32_t* idx, float* gate, float* logits, int32_t* counts,
                  hipStream_t st) {
   dim3 grid(cdiv(T, RT_TOK));
   if constexpr (std::is_same<TX, bf16>::value) {
+    const int ncu = route_cu_count();
+    const bool wide = T >= 64 * ncu;
+    // the int8 profiling router keeps the 32-token kernel below when tiles are
+    // 32 tokens (measured faster there: 20.3 against 22.7 us at T = 8192, d = 2048)
+    if (E <= 64 && d % (wide ? 128 : 256) == 0 && (MODE == 0 || wide)) {
+      // 64-token tiles once every compute unit gets one, else 32; one block per CU
+      const int tiles = wide ? cdiv(T, 64) : cdiv(T, 32);
+      const dim3 pg(tiles < ncu ? tiles : ncu);
+#define FM_RP(TT, NEG, KM)                                                                                \
+  hipLaunchKernelGGL((k_route_p<TW, TT, NEG, KM, MODE>), pg, dim3(256), 0, st, X, W, ws, bias, T, d, E, k, \
+                     idx, gate, logits, counts)
+#define FM_RP_K(TT, NEG)             \
+  if (k <= 2) FM_RP(TT, NEG, 2);      \
+  else if (k <= 4) FM_RP(TT, NEG, 4); \
+  else if (k <= 8) FM_RP(TT, NEG, 8); \
+  else FM_RP(TT, NEG, 16);
+      if (wide) {
+        if (E <= 32) { FM_RP_K(64, 1) } else { FM_RP_K(64, 2) }
+      } else {
+        if (E <= 32) { FM_RP_K(32, 1) } else { FM_RP_K(32, 2) }
+      }
+#undef FM_RP_K
+#undef FM_RP
+      return check_launch(MODE == 0 ? "moe_route_topk" : MODE == 1 ? "moe_profile_hist" : "moe_profile_route");
+    }
     if (E <= 64 && d % RL_COLS == 0) {
 #define FM_RL(NB, KM)                                                                          \
   hipLaunchKernelGGL((k_route_lds<TW, NB, KM, MODE>), grid, dim3(256), 0, st, X, W, ws, bias, T, d, E, k, \

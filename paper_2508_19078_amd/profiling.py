@@ -7,13 +7,17 @@ with one scale per row (``moe_quantize_int8``) and keeps only the codes and
 scales resident.  ``run`` then passes a batch through the stack, layer by
 layer, on one stream:
 
+  moe_rms_norm        the layer's input: the RMS-normalised stream (fused with
+                      the previous layer's residual add)
   moe_profile_route   int8 routing: histogram, top-k indices and gates
   moe_permute         the layer's rows into per-expert buckets
   moe_grouped_swiglu_fwd_q8   the experts straight from their int8 codes
                       (bf16 activations, d and I multiples of 16); otherwise
                       moe_dequant_int8 into one reused buffer and
                       moe_grouped_swiglu_fwd
-  moe_unpermute, moe_residual_add   Y_l and X_{l+1} = X_l + Y_l
+  moe_unpermute       Y_l, then X_{l+1} = X_l + Y_l (moe_rms_norm, which also
+                      normalises X_{l+1} for the next layer; moe_residual_add
+                      after the last layer)
 
 Every value is computed by libfluxmoe; this module only owns buffers and
 orders the calls.
@@ -33,13 +37,14 @@ class QuantizedStack:
     one float dtype.  Only the int8 codes and fp32 scales are kept."""
 
     def __init__(self, layers: Sequence[dict], T: int, k: int, device: str = "cuda",
-                 record: bool = False, fused: Optional[bool] = None):
+                 record: bool = False, fused: Optional[bool] = None, eps: float = 1e-6):
         L0 = layers[0]
         self.dt = L0["wg"].dtype
         self.E, self.I, self.d = L0["wg"].shape
         self.n_sh = 0 if L0.get("sg") is None else L0["sg"].shape[0]
         self.T, self.k, self.L = T, k, len(layers)
         self.record = record
+        self.eps = eps
         E, I, d, n_sh = self.E, self.I, self.d, self.n_sh
         dev = device
 
@@ -110,7 +115,7 @@ class QuantizedStack:
             self.A_g, self.A_u = z(Rt, I), z(Rt, I)
         self.H, self.O = z(Rt, I), z(Rt, d)
         self.Y = z(T, d)
-        self.Xa, self.Xb = z(T, d), z(T, d)
+        self.Xa, self.Xb, self.Xn = z(T, d), z(T, d), z(T, d)
         self.ws_fwd = torch.empty(ws_fwd, dtype=torch.uint8, device=dev)
         self.trace: List[dict] = []
 
@@ -123,7 +128,9 @@ class QuantizedStack:
         self.counts.zero_()
         self.trace = []
         self.Xa.copy_(X0)
-        X, Xn = self.Xa, self.Xb
+        X, Xnext, Xn = self.Xa, self.Xb, self.Xn
+        api.moe_rms_norm(X, None, Xn, eps=self.eps)
+        mark("norm")
         for l, ql in enumerate(self.q):
             if not self.fused:
                 api.moe_dequant_int8(ql["wg"][0], ql["wg"][1], self.Dg)
@@ -135,23 +142,26 @@ class QuantizedStack:
                     api.moe_dequant_int8(ql["sd"][0], ql["sd"][1], self.Sd)
                 mark("dequant")
             Wq, ws = ql["Wr"]
-            api.moe_profile_route(X, Wq, ws, ql["bias"], k, self.counts[l], self.idx, self.gate)
+            api.moe_profile_route(Xn, Wq, ws, ql["bias"], k, self.counts[l], self.idx, self.gate)
             mark("route")
-            api.moe_permute(X, self.idx, self.gate, None, self.E, self.offsets, self.perm_token, self.perm_gate,
+            api.moe_permute(Xn, self.idx, self.gate, None, self.E, self.offsets, self.perm_token, self.perm_gate,
                             self.inv, self.X_perm, self.ws_perm, E=self.E)
             mark("permute")
             if self.fused:
-                api.moe_grouped_swiglu_fwd_q8(self.qtables[l], X, self.X_perm, self.offsets, T, k, self.H, self.O,
+                api.moe_grouped_swiglu_fwd_q8(self.qtables[l], Xn, self.X_perm, self.offsets, T, k, self.H, self.O,
                                               self.ws_fwd)
             else:
-                api.moe_grouped_swiglu_fwd(self.layer, X, self.X_perm, self.offsets, T, k, self.A_g, self.A_u,
+                api.moe_grouped_swiglu_fwd(self.layer, Xn, self.X_perm, self.offsets, T, k, self.A_g, self.A_u,
                                            self.H, self.O, self.ws_fwd)
             mark("ffn_fwd")
             api.moe_unpermute(self.layer, self.O, self.inv, self.perm_gate, T, k, self.Y)
-            api.moe_residual_add(X, self.Y, Xn)
-            mark("combine")
             if self.record:
                 self.trace.append({"idx": self.idx.clone(), "gate": self.gate.clone(), "X": X.clone(),
-                                   "Y": self.Y.clone()})
-            X, Xn = Xn, X
+                                   "Xn": Xn.clone(), "Y": self.Y.clone()})
+            if l + 1 < self.L:
+                api.moe_rms_norm(X, self.Y, Xn, out_sum=Xnext, eps=self.eps)
+            else:
+                api.moe_residual_add(X, self.Y, Xnext)
+            mark("combine")
+            X, Xnext = Xnext, X
         return X

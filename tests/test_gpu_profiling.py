@@ -1,23 +1,24 @@
 """GPU parity of the quantised profiling pass over a layer stack (Section 4.1)
 against the fp64 oracle.
 
-Layer 0 sees the same input on both sides: its top-k sets and histogram must
-match bit-exactly outside the 1e-6 near-tie window, its gates to fp32
-precision.  Deeper layers see the stream the layers before them produced, which
+Every layer reads the RMS-normalised stream, which the GPU rounds to bf16, so
+even the first layer routes on an input within one bf16 rounding of the
+oracle's.  Deeper layers see the stream the layers before them produced, which
 the GPU carries in bf16.  A token that took another expert set in an earlier
 layer (only possible at a near tie) has a legitimately different stream from
 then on; over the other tokens the stream must stay within the 2e-2 relative
 Frobenius bar.  A token's top-k set must match wherever the oracle's gap
 between its k-th and (k+1)-th logit exceeds twice the largest change the
-difference of the two streams makes to one of its logits (s_e <dX_t, q_e>,
-computed here from the two streams) plus the 1e-6 window; the histograms are
-compared after removing the excluded tokens' choices from both sides.  The
-excluded share is reported and bounded.
+difference of the two routers' inputs makes to one of its logits
+(s_e <dXn_t, q_e>, computed here from the two normalised streams) plus the
+1e-6 window; the histograms are compared after removing the excluded tokens'
+choices from both sides.  The excluded share is reported and bounded.
 
-The teacher-forced check removes the drift: the oracle routes each layer on
-the GPU's own bf16 input to that layer, so every layer of the 28-layer stack
-must give bit-exact top-k sets and histograms outside the 1e-6 window, and the
-layer output Y within the 2e-2 bar."""
+The teacher-forced check removes the drift: the oracle routes each
+layer on the GPU's own bf16 input to that layer's router, so every layer of the
+28-layer stack must give bit-exact top-k sets and histograms outside the 1e-6
+window; the GPU's normalisation must be within one bf16 rounding of the exact
+one, and the layer output Y within the 2e-2 bar."""
 import numpy as np
 import pytest
 import torch
@@ -76,9 +77,10 @@ def check_stack(w, L, max_excluded=MAX_EXCLUDED, fused=None):
             log(f"  layer {l}: input stream rel err {err:.2e} over {same.sum()} tokens routed alike so far")
             assert err <= TOL_X, (l, err)
         q, s = O.quantize_int8_rows(ora[l]["Wr"])
-        lg = O.profile_logits(Xo, q, s, ora[l]["bias"])
-        # the largest change of one of token t's logits due to the stream difference
-        delta = np.max(np.abs((Xg - Xo) @ O.dequantize_rows(q, s).T), axis=1) * (1 + 1e-6)
+        Xno, Xng = O.rms_norm_rows(Xo), host(tr["Xn"])      # the router's inputs
+        lg = O.profile_logits(Xno, q, s, ora[l]["bias"])
+        # the largest change of one of token t's logits due to the input difference
+        delta = np.max(np.abs((Xng - Xno) @ O.dequantize_rows(q, s).T), axis=1) * (1 + 1e-6)
         excl = gaps_of(lg, w.k) < 2 * delta + WIN
         ig, gg = tr["idx"].cpu().numpy(), tr["gate"].cpu().numpy()
         same &= np.array([set(ig[t]) == set(idx_o[l][t]) for t in range(w.T)])
@@ -86,7 +88,9 @@ def check_stack(w, L, max_excluded=MAX_EXCLUDED, fused=None):
         bad = sum(set(ig[t]) != set(idx_o[l][t]) for t in np.nonzero(keep)[0])
         log(f"  layer {l}: excluded {excl.sum()} of {w.T} tokens, mismatched {bad}")
         assert bad == 0
-        assert excl.mean() <= (1e-3 if l == 0 else max_excluded), excl.mean()
+        # every layer, the first included, reads the GPU's bf16 rounding of its
+        # normalised input, so every layer may exclude up to the same share
+        assert excl.mean() <= max_excluded, (l, excl.mean())
         # histogram without the excluded tokens' choices
         cg = counts_g[l] - np.bincount(ig[excl].ravel(), minlength=w.E)
         co = counts_o[l] - np.bincount(idx_o[l][excl].ravel(), minlength=w.E)
@@ -168,7 +172,7 @@ def test_profiling_stack_teacher_forced_all_layers():
     top-6, I = 1408) in the launch configuration of the benchmark's profiling
     pass.  Per layer, the oracle's int8 router runs on the GPU's own bf16 input
     to that layer: top-k sets and histogram bit-exact outside the 1e-6 window,
-    gates to 1e-5.  On layers 0, 9, 18 and 27 the oracle also runs the layer's
+    gates to 1e-5 at the first layer's logit scale.  On layers 0, 9, 18 and 27 the oracle also runs the layer's
     dequantised experts on that input: Y within the 2e-2 bar over the tokens
     routed alike."""
     w = W.WORKLOADS["deepseek_stack"]
@@ -189,13 +193,19 @@ def test_profiling_stack_teacher_forced_all_layers():
     torch.cuda.synchronize()
     counts_g = st.counts.cpu().numpy()
     total_excl = 0
+    scale0 = None
     for l in range(L):
         tr = st.trace[l]
-        Xg = host(tr["X"])
+        Xg, Xng = host(tr["X"]), host(tr["Xn"])
+        # the layer's input: the GPU's stream RMS-normalised, within one bf16
+        # rounding (unit roundoff 2^-8) of the exact normalisation of that stream,
+        # plus the fp32 rounding of the row's scale
+        ex = O.rms_norm_rows(Xg)
+        assert np.all(np.abs(Xng - ex) <= (2.0 ** -8 + 1e-5) * np.abs(ex)), l
         ig, gg = tr["idx"].cpu().numpy(), tr["gate"].cpu().numpy()
         Wr, bias = routers[l]
         q, s = O.quantize_int8_rows(Wr)
-        lg = O.profile_logits(Xg, q, s, bias)
+        lg = O.profile_logits(Xng, q, s, bias)        # routed on exactly what the GPU routed on
         io = O.topk_select(lg, k)
         go = O.softmax_rows(np.take_along_axis(lg, io, axis=1))
         excl = gaps_of(lg, k) < WIN
@@ -208,17 +218,24 @@ def test_profiling_stack_teacher_forced_all_layers():
         assert bad == 0, l
         np.testing.assert_array_equal(cg, co, err_msg=f"layer {l}")
         assert counts_g[l].sum() == w.T * k
-        # gates of the kept tokens, matched by expert
+        # gates of the kept tokens, matched by expert: 1e-5 at the first layer's
+        # logit scale; the GPU's fp32 logits carry rounding in proportion to their
+        # size, which grows along the residual stream
+        scale = float(np.sqrt(np.mean(lg ** 2)))
+        scale0 = scale if scale0 is None else scale0
+        tol = 1e-5 * max(1.0, scale / scale0)
         o_by = np.zeros((w.T, E))
         np.put_along_axis(o_by, io, go, axis=1)
         g_match = np.take_along_axis(o_by, ig.astype(np.int64), axis=1)
-        np.testing.assert_allclose(gg[keep], g_match[keep], rtol=0, atol=1e-5)
+        gerr = float(np.max(np.abs(gg[keep] - g_match[keep]))) if keep.any() else 0.0
+        log(f"  layer {l}: logit rms {scale:.3f}, gate max abs err {gerr:.2e} (tolerance {tol:.2e})")
+        assert gerr <= tol, (l, gerr, tol)
         if l in Y_checked:
+            # the oracle's layer on the GPU's stream (normalised in fp64)
             _, idx_o, _, Xs = O.quantized_stack_profile(Xg, [ora_layers[l]], k)
-            assert np.array_equal(idx_o[0], io)
-            same = np.array([set(ig[t]) == set(io[t]) for t in range(w.T)])
+            same = np.array([set(ig[t]) == set(idx_o[0][t]) for t in range(w.T)])
             err = rel_fro(host(tr["Y"])[same], (Xs[1] - Xg)[same])
             log(f"  layer {l}: Y rel err {err:.2e} over {same.sum()} tokens routed alike")
-            assert err <= TOL_X, (l, err)
+            assert err <= TOL_X and same.mean() >= 0.99, (l, err, same.mean())
     log(f"teacher-forced stack: {total_excl} of {L * w.T} token-layers in the tie window")
     assert total_excl <= L * w.T // 1000

@@ -167,3 +167,46 @@ def test_residual_add(dt):
     exact = host(X) + host(Y)
     rel = 2.0 ** -24 if dt == torch.float32 else 2.0 ** -8 + 2.0 ** -23
     assert np.all(np.abs(host(out) - exact) <= rel * np.abs(exact))
+
+
+RN_CASES = {
+    # name: (T, d, dtype, with Y, out_sum aliasing X)
+    "bf16_residual_in_place": (333, 2048, torch.bfloat16, True, True),
+    "bf16_norm_only": (97, 264, torch.bfloat16, False, False),
+    "bf16_rows_past_the_register_cache": (45, 8456, torch.bfloat16, True, False),
+    "fp32_residual": (130, 1032, torch.float32, True, False),
+    "fp32_rows_past_the_register_cache": (17, 4104, torch.float32, True, True),
+}
+
+
+@pytest.mark.parametrize("name", list(RN_CASES))
+def test_rms_norm(name):
+    """moe_rms_norm (the profiling stack's layer input, fused with the residual
+    add) element by element against the oracle's rms_norm_rows of the exact
+    X + Y: out_sum within one rounding of the exact sum, out_norm within three
+    roundings to the stream's type (the sum, the scale computed from the
+    rounded sum, the output); a zero row stays zero; rows of many scales."""
+    T, d, dt, with_y, alias = RN_CASES[name]
+    rng = np.random.default_rng([4245, T, d])
+    Xh = (rng.standard_normal((T, d)) * 10.0 ** rng.uniform(-2, 2, size=(T, 1))).astype(np.float32)
+    Yh = (rng.standard_normal((T, d)) * 10.0 ** rng.uniform(-2, 2, size=(T, 1))).astype(np.float32)
+    Xh[3] = 0.0
+    Yh[3] = 0.0
+    X, Y = torch.from_numpy(Xh).to(dt).cuda(), torch.from_numpy(Yh).to(dt).cuda()
+    Xv, Yv = host(X), host(Y)
+    exact_sum = Xv + Yv if with_y else Xv
+    out_norm = torch.full_like(X, float("nan"))
+    out_sum = X if alias else torch.full_like(X, float("nan"))
+    api.moe_rms_norm(X, Y if with_y else None, out_norm, out_sum=out_sum if with_y else None, eps=1e-6)
+    torch.cuda.synchronize()
+    u = 2.0 ** -24 if dt == torch.float32 else 2.0 ** -8      # unit roundoff of the stream's type
+    if with_y:
+        got_s = host(out_sum)
+        assert np.all(np.abs(got_s - exact_sum) <= 2 * u * np.abs(exact_sum))
+    exact = O.rms_norm_rows(exact_sum, eps=1e-6)
+    got = host(out_norm)
+    tol = 3 * u + 1e-6
+    bad = np.abs(got - exact) > tol * np.abs(exact)
+    log(f"rms norm {name}: max rel err {np.max(np.abs(got - exact) / np.maximum(np.abs(exact), 1e-30)):.2e}")
+    assert not bad.any(), np.argwhere(bad)[:5]
+    assert np.all(got[3] == 0)
