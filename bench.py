@@ -116,10 +116,11 @@ def cold_hbm(r, w, st, N, reps=5):
         # router backward (selection fixed), added to the layer's dX
         "route_bwd": (lambda: api.moe_route_bwd(r.gate, r.idx, r.dgate, r.Wr, r.dX, accumulate=True),
                       w.T * w.k * 12 + 2 * w.T * w.d * b + w.E * w.d * b),
-        # expert utility (Eq. 3) from the backward's saved rows: x, dO, H, dA_g, dA_u of every row
-        "expert_utility": (lambda: api.moe_expert_utility(r.layer_tables, r.X, r.X_perm, r.offsets, w.T, w.k,
-                                                          r.H, r.dO, r.ws_bwd, util),
-                           Ntot * (2 * w.d + 3 * w.I) * b),
+        # expert utility (Eq. 3): the tokens' X and dY rows, the rows' maps and the
+        # per-row norm partials the backward left (8 bytes per row and dH column tile)
+        "expert_utility": (lambda: api.moe_expert_utility(r.layer_tables, r.X, r.dY, r.perm_token, r.perm_gate,
+                                                          r.offsets, w.T, w.k, r.ws_bwd, util),
+                           2 * w.T * w.d * b + N * 8 + Ntot * 8 * -(-w.I // 256)),
     }
     util = torch.empty(r.S_r + w.n_shared, dtype=torch.float32, device="cuda")
     if r.G:

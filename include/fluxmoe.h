@@ -60,7 +60,7 @@ enum { MOE_F32 = 0, MOE_BF16 = 1, MOE_I8 = 2 };
 const char* moe_last_error(void);
 /* ABI revision of this header. */
 int moe_abi_version(void);
-#define FLUXMOE_ABI_VERSION 1
+#define FLUXMOE_ABI_VERSION 2
 
 /* ---------------------------------------------------------------- routing --
  * moe_route_topk: the gating network of an MoE layer (Section 2.1, "MoE":
@@ -461,17 +461,23 @@ size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k);
  * D_s the slot's rows (its tokens; a token whose choices share the slot is one
  * row with the summed gate) and g_r the gradient of the slot's W_gate, W_up,
  * W_down from row r alone, three rank-one products, so
- *   ||g_r||^2 = ||dO_r||^2 ||H_r||^2 + (||dA_g,r||^2 + ||dA_u,r||^2) ||x_r||^2
- * (per-row sums in fp32, per-slot sums in fp64, fixed order); an empty slot
- * gets 0.  Every slot gets a utility, frozen ones included.  Call it after
- * moe_grouped_swiglu_bwd on the same stream with that call's workspace, which
- * still holds dA_g and dA_u, and the same layer, X, X_perm, offsets, T, k, H
- * and dO; nothing else may use the workspace in between.  utility [S] fp32.
+ *   ||g_r||^2 = ||dO_r||^2 ||h_r||^2 + (||dA_g,r||^2 + ||dA_u,r||^2) ||x_r||^2
+ * with x_r = X[t] and dO_r = gate_r dY[t] for the row's token t (gate 1 on a
+ * shared slot).  The sums of squares of dA_g, dA_u and h = silu(a_g) a_u over
+ * each row are left in the workspace by moe_grouped_swiglu_bwd (its dH step,
+ * h recomputed from the saved A_g, A_u); this call adds ||X[t]||^2 and
+ * ||dY[t]||^2 per token and reduces per slot (per-row and per-token sums in
+ * fp32, per-slot sums in fp64, fixed order); an empty slot gets 0.  Every slot
+ * gets a utility, frozen ones included.  Call it after moe_grouped_swiglu_bwd
+ * on the same stream with that call's workspace and the same layer, offsets,
+ * T and k; nothing else may use the workspace in between.
+ * X, dY [T,d] in L->dtype; perm_token, perm_gate: moe_permute's maps (may be
+ * NULL when S_routed == 0); utility [S] fp32.
  */
-int moe_expert_utility(const moe_layer* L, const void* X, const void* X_perm,
-                       const int32_t* offsets, int T, int k, const void* H,
-                       const void* dO, void* ws, size_t ws_bytes, float* utility,
-                       void* stream);
+int moe_expert_utility(const moe_layer* L, const void* X, const void* dY,
+                       const int32_t* perm_token, const float* perm_gate,
+                       const int32_t* offsets, int T, int k, void* ws, size_t ws_bytes,
+                       float* utility, void* stream);
 
 /* moe_permute_bwd: gradient of moe_permute's gather of each token into the
  * buckets of the slots it is re-routed to (the token subsets D^e of

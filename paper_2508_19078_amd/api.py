@@ -72,7 +72,7 @@ _SIGS = {
                                         _c_int, _vp, _c_size, _vp]),
     "moe_grouped_swiglu_bwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
     "moe_permute_bwd": (_c_int, [_vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
-    "moe_expert_utility": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp, _vp]),
+    "moe_expert_utility": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _c_size, _vp, _vp]),
     "moe_profile_route": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp,
                                    _vp]),
     "moe_dequant_int8": (_c_int, [_vp, _vp, ctypes.c_long, _c_int, _c_int, _vp, _vp]),
@@ -387,11 +387,11 @@ def moe_permute_bwd(layer, dX_perm, inv, T, k, dX, stream=None):
                  stream_ptr(stream))
 
 
-def moe_expert_utility(layer, X, X_perm, offsets, T, k, H, dO, ws, utility, stream=None):
+def moe_expert_utility(layer, X, dY, perm_token, perm_gate, offsets, T, k, ws, utility, stream=None):
     """After moe_grouped_swiglu_bwd with the same workspace `ws`."""
-    return _call("moe_expert_utility", ptr(layer), ptr(X, FLOAT), ptr(X_perm, FLOAT), ptr(offsets, I32), T, k,
-                 ptr(H, FLOAT), ptr(dO, FLOAT), ptr(ws), ws.numel() * ws.element_size(), ptr(utility, F32),
-                 stream_ptr(stream))
+    return _call("moe_expert_utility", ptr(layer), ptr(X, FLOAT), ptr(dY, FLOAT), ptr(perm_token, I32),
+                 ptr(perm_gate, F32), ptr(offsets, I32), T, k, ptr(ws), ws.numel() * ws.element_size(),
+                 ptr(utility, F32), stream_ptr(stream))
 
 
 # ----------------------------------------------------- layer descriptor ----

@@ -359,10 +359,14 @@ __global__ __launch_bounds__(G_THREADS) void kf_down(LayerPtrs<T> W, const T* __
 
 // ------------------------------------------------------------ backward ----
 
+// Also leaves per-row partial sums of dA_g^2 + dA_u^2 and h^2 (h = silu(a_g) a_u)
+// for the expert utility: per column tile, one pair per wave column (two),
+// at norms[row * 2 NT + 2 tile + wave column].
 template <typename T>
 __global__ __launch_bounds__(G_THREADS) void kf_dh(LayerPtrs<T> W, const T* __restrict__ dO,
                                                   const T* __restrict__ Ag, const T* __restrict__ Au,
-                                                  RowArgs ra, T* __restrict__ dAg, T* __restrict__ dAu) {
+                                                  RowArgs ra, T* __restrict__ dAg, T* __restrict__ dAu,
+                                                  float2* __restrict__ norms) {
   __shared__ __align__(16) char lds[2 * (1 + 1) * GemmCfg<T>::TILE * (int)sizeof(T)];
   const int d = ra.d, I = ra.I, NT = (I + G_BN - 1) / G_BN;
   const TileRange tr = row_range(ra, NT);
@@ -377,6 +381,7 @@ __global__ __launch_bounds__(G_THREADS) void kf_dh(LayerPtrs<T> W, const T* __re
     Acc<T, 1, 1> acc;
     acc.zero();
     gemm_mainloop<T, true, false, 1, 1>(A, B, d, (T*)lds, acc);
+    float sa[4] = {0.f, 0.f, 0.f, 0.f}, sh[4] = {0.f, 0.f, 0.f, 0.f};   // per row block i of the wave
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const AccCoord c = quad_coord<T>(q);
@@ -390,9 +395,26 @@ __global__ __launch_bounds__(G_THREADS) void kf_dh(LayerPtrs<T> W, const T* __re
         const float s = sigm(ag[r]);
         du[r] = dh[r] * ag[r] * s;
         dg[r] = dh[r] * u[r] * s * (1.0f + ag[r] * (1.0f - s));
+        const float h = ag[r] * s * u[r];
+        sa[q >> 2] = fmaf(dg[r], dg[r], fmaf(du[r], du[r], sa[q >> 2]));
+        sh[q >> 2] = fmaf(h, h, sh[q >> 2]);
       }
       store4(dAg + o, dg);
       store4(dAu + o, du);
+    }
+    // quad (i, j) of lane L covers row 64 wm + 16 i + L % 16: add over the
+    // four lanes L / 16 of that row, then one pair per row and wave column
+    const int lane = lane_id(), wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float a = sa[i], h = sh[i];
+      a += __shfl_xor(a, 16);
+      h += __shfl_xor(h, 16);
+      a += __shfl_xor(a, 32);
+      h += __shfl_xor(h, 32);
+      const int row = (wave & 1) * 64 + i * 16 + (lane & 15);
+      if (lane < 16 && row < sr.nrows - m0)
+        norms[(ob + row) * (2 * NT) + 2 * rt.n + (wave >> 1)] = make_float2(a, h);
     }
   }
 }
@@ -545,16 +567,22 @@ __device__ __forceinline__ void b16_store_staged(const B16Acc<C::MI, C::NJ>& acc
 // chunks go in groups of G per lane; the loads of the first group are issued
 // before the tile is staged, so their latency overlaps the LDS writes.
 // Pointers are at the tile origin; rows x cols are valid.
+//
+// The same pass leaves, per row of the tile, the sums over its columns of
+// dA_g^2 + dA_u^2 and of h^2 with h = silu(a_g) a_u recomputed from the stored
+// A_g, A_u (the factors of the expert utility, Eq. 3): the 32 lanes that share
+// a row add their values by a fixed butterfly and one of them stores the pair
+// at norms[row * P] (P partials per row, this column tile's slot).
 template <class C>
 __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& acc, FM_LDS char* lds,
                                                    const bf16* Ag, const bf16* Au, bf16* dAg, bf16* dAu,
-                                                   size_t ld, int rows, int cols) {
+                                                   size_t ld, int rows, int cols, float2* norms, int P) {
   using S = Stage<bf16, C::RB>;
   constexpr int CH = C::RB / 8;                     // 8-column chunks per row
   constexpr int PER = C::RA * CH / C::THREADS;      // chunks per lane
   constexpr int G = 8;                              // chunks in flight per lane
-  static_assert(PER % G == 0 && PER * C::THREADS == C::RA * CH && C::RA * C::RB * 2 <= C::LDS,
-                "whole chunks per lane");
+  static_assert(PER % G == 0 && PER * C::THREADS == C::RA * CH && C::RA * C::RB * 2 <= C::LDS && CH == 32,
+                "whole chunks per lane, a row per half-wave");
   // thread index re-read here (opaque), so that the per-chunk addresses are
   // not hoisted out of the tile loop and kept live through the main loop
   const int tid = wave_id() * 64 + lane_id_here();
@@ -586,6 +614,7 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
 #pragma unroll
     for (int u = 0; u < G; ++u) {
       const int idx = tid + (g * G + u) * C::THREADS, r = idx / CH, c = (idx % CH) * 8;
+      float sa = 0.f, sh = 0.f;
       if (r < rows && c < cols) {
         float dh[8], a[8], up[8], dg[8], du[8];
         const u32x4_t hv = *(const FM_LDS u32x4_t*)(lds + S::at(r, c));
@@ -595,12 +624,23 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float sg = sigm_fast(a[e]);
-          du[e] = dh[e] * a[e] * sg;
+          const float silu = a[e] * sg;
+          du[e] = dh[e] * silu;
           dg[e] = dh[e] * up[e] * sg * (1.0f + a[e] * (1.0f - sg));
+          const float h = silu * up[e];
+          sa = fmaf(dg[e], dg[e], fmaf(du[e], du[e], sa));
+          sh = fmaf(h, h, sh);
         }
         st16(dAg + (size_t)r * ld + c, pack16(dg, (bf16*)nullptr));
         st16(dAu + (size_t)r * ld + c, pack16(du, (bf16*)nullptr));
       }
+      // the 32 lanes of this row (one half of the wave, CH = 32 chunks)
+#pragma unroll
+      for (int off = 16; off > 0; off >>= 1) {
+        sa += __shfl_xor(sa, off);
+        sh += __shfl_xor(sh, off);
+      }
+      if ((tid & 31) == 0 && r < rows) norms[(size_t)r * P] = make_float2(sa, sh);
     }
   }
   barrier_lds();
@@ -784,7 +824,7 @@ __global__ __launch_bounds__(CB::THREADS) void kb_down(LayerPtrs<bf16> W, cbp H,
 
 // dH = dO W_down (B = W_down read k-major), epilogue dA_g, dA_u.
 __global__ __launch_bounds__(CB::THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, cbp Ag, cbp Au, RowArgs ra,
-                                                     bf16* dAg, bf16* dAu) {
+                                                     bf16* dAg, bf16* dAu, float2* norms) {
   __shared__ __align__(16) char lds[CB::LDS];
   const int d = ra.d, I = ra.I, NT = (I + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
@@ -800,7 +840,7 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
     acc.zero();
     b16_gemm<CB, true, false>(A, B, d, (FM_LDS char*)lds, acc);
     b16_dswiglu_staged<CB>(acc, (FM_LDS char*)lds, Ag + ob * I + n0, Au + ob * I + n0, dAg + ob * I + n0,
-                           dAu + ob * I + n0, I, sr.nrows - m0, I - n0);
+                           dAu + ob * I + n0, I, sr.nrows - m0, I - n0, norms + ob * NT + rt.n, NT);
   }
 }
 
@@ -1007,55 +1047,89 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
 //   ||g_r||^2 = ||dO_r||^2 ||h_r||^2 + (||dA_g,r||^2 + ||dA_u,r||^2) ||x_r||^2.
 // A slot's rows are its tokens after folding (a token whose choices share the
 // slot is one row with the summed gate), so |D_s| is the slot's row count.
+// The backward's dH epilogue leaves per row the partial sums of dA_g^2 + dA_u^2
+// and h^2 over its column tiles; a row's x is its token's input and its dO the
+// token's output gradient times the row's gate, so the rest needs only one
+// pass over the tokens: ||x_t||^2 and ||dY_t||^2.
 
-// Rows per first-pass tile: 64, or 32 when 64-row tiles would give fewer than
-// two blocks per CU (several blocks per CU keep loads in flight; at the
-// DeepSeek shape 64 measured best, at T = 4096 with 16 experts 32 took the pass
-// from 129 to 94 us).
-constexpr int UT_ROWS = 64, UT_ROWS_MIN = 32;
+constexpr int UT_THREADS = 256;   // threads of the per-row pass: one row each (tiles of up to 256 rows)
+static_assert(B16_ROWS <= UT_THREADS && G_BM <= UT_THREADS, "a row tile per block of the utility pass");
 
-// Sum of squares of n elements (n % 8 == 0) spread over a wave: every lane
-// ends with the same total (fixed butterfly order).
-template <typename T> __device__ __forceinline__ float wave_sumsq(const T* __restrict__ p, int n) {
+// ||X_t||^2 and ||dY_t||^2, one wave per token (fp32 lane sums, fixed butterfly).
+template <typename T>
+__global__ __launch_bounds__(256) void k_token_norms(const T* __restrict__ X, const T* __restrict__ dY, int Tn,
+                                                     int d, float2* __restrict__ tn) {
   constexpr int V = 16 / sizeof(T);
-  float a = 0.f;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= Tn) return;
+  float sx = 0.f, sy = 0.f;
+  const T* xr = X + (size_t)t * d;
+  const T* yr = dY + (size_t)t * d;
 #pragma unroll 4
-  for (int c = lane_id() * V; c < n; c += 64 * V) {
-    float f[V];
-    unpack16(ld16(p + c), f, (T*)nullptr);
+  for (int c = lane_id() * V; c < d; c += 64 * V) {
+    float a[V], b[V];
+    unpack16(ld16(xr + c), a, (T*)nullptr);
+    unpack16(ld16(yr + c), b, (T*)nullptr);
 #pragma unroll
-    for (int i = 0; i < V; ++i) a = fmaf(f[i], f[i], a);
+    for (int i = 0; i < V; ++i) {
+      sx = fmaf(a[i], a[i], sx);
+      sy = fmaf(b[i], b[i], sy);
+    }
   }
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off);
-  return a;
+  for (int off = 32; off > 0; off >>= 1) {
+    sx += __shfl_xor(sx, off);
+    sy += __shfl_xor(sy, off);
+  }
+  if (lane_id() == 0) tn[t] = make_float2(sx, sy);
 }
 
-// First pass: one block per tile of tile_rows rows of a slot (tiles as in mbase); four
-// waves take every fourth row; the tile's sum in fp64, waves added in order.
-template <typename T>
-__global__ __launch_bounds__(256) void k_utility_rows(const T* __restrict__ X, const T* __restrict__ Xp,
-                                                      const T* __restrict__ dO, const T* __restrict__ H,
-                                                      const T* __restrict__ dAg, const T* __restrict__ dAu,
-                                                      RowArgs ra, int tile_rows, double* __restrict__ part) {
-  __shared__ double wsum[4];
+// One block per row tile of a slot, the backward's own row tiles (its
+// schedule, tile_rows <= UT_THREADS rows, is still in the workspace): a thread
+// takes one row, ||g_r||^2 in fp64 from its token's norms, its gate and the P
+// partials of the row (in order); the block adds its rows by a fixed tree.
+__global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, int tile_rows,
+                                                             const int32_t* __restrict__ perm_token,
+                                                             const float* __restrict__ perm_gate,
+                                                             const float2* __restrict__ tn,
+                                                             const float2* __restrict__ norms, int P,
+                                                             double* __restrict__ part) {
+  __shared__ double red[UT_THREADS];
   const int b = blockIdx.x;
   if (b >= ld_scalar(ra.mbase + ra.S)) return;
   const int s = find_slot(ra.mbase, ra.S, b);
   const int r0 = (b - ld_scalar(ra.mbase + s)) * tile_rows;
   const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-  const int rows = min(tile_rows, sr.nrows - r0), wave = threadIdx.x >> 6, d = ra.d, I = ra.I;
-  double acc = 0.0;
-  for (int i = wave; i < rows; i += 4) {
-    const size_t o = (size_t)(sr.orow0 + r0 + i);
-    const T* xr = (sr.shared ? X : Xp) + (size_t)(sr.xrow0 + r0 + i) * d;
-    const float sx = wave_sumsq(xr, d), so = wave_sumsq(dO + o * d, d);
-    const float sh = wave_sumsq(H + o * I, I), sg = wave_sumsq(dAg + o * I, I), su = wave_sumsq(dAu + o * I, I);
-    acc += (double)so * sh + ((double)sg + su) * sx;
+  const int i = threadIdx.x;
+  double v = 0.0;
+  if (i < tile_rows && r0 + i < sr.nrows) {
+    const long row = sr.orow0 + r0 + i;
+    int tok;
+    float g;
+    if (sr.shared) {
+      tok = r0 + i;
+      g = 1.f;
+    } else {
+      tok = perm_token[row];
+      g = perm_gate[row];
+    }
+    const float2 xy = tn[tok];
+    float sa = 0.f, sh = 0.f;
+    for (int p = 0; p < P; ++p) {
+      const float2 q = norms[row * P + p];
+      sa += q.x;
+      sh += q.y;
+    }
+    v = (double)g * g * xy.y * sh + (double)sa * xy.x;
   }
-  if (lane_id() == 0) wsum[wave] = acc;
+  red[i] = v;
   __syncthreads();
-  if (threadIdx.x == 0) part[b] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+#pragma unroll
+  for (int w = UT_THREADS / 2; w > 0; w >>= 1) {
+    if (i < w) red[i] += red[i + w];
+    __syncthreads();
+  }
+  if (i == 0) part[b] = red[0];
 }
 
 // Second pass: thread s adds its slot's tile sums in tile order.
@@ -1114,18 +1188,50 @@ extern "C" size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int 
   return sched_bytes(n_slots(L));
 }
 
-// Upper bound of the utility pass's row tiles at tile height `rows`: sum_s ceil(n_s / rows).
-static size_t utility_tiles(const moe_layer* L, int T, int k, int rows = UT_ROWS_MIN) {
-  return rows_total(L, T, k) / rows + n_slots(L) + 1;
+// Rows per row tile of the backward (bf16 or fp32 core), and an upper bound of
+// the row tiles: sum_s ceil(n_s / rows).
+static int bwd_tile_rows(const moe_layer* L) { return L->dtype == MOE_BF16 ? B16_ROWS : G_BM; }
+static size_t utility_tiles(const moe_layer* L, int T, int k) {
+  return rows_total(L, T, k) / bwd_tile_rows(L) + n_slots(L) + 1;
 }
-static int utility_tile_rows(const moe_layer* L, int T, int k) {
-  return rows_total(L, T, k) / UT_ROWS >= 2 * (size_t)persistent_blocks() ? UT_ROWS : UT_ROWS_MIN;
+// Partials of the utility's row norms per row: one per dH column tile (bf16),
+// two per column tile (fp32, one per wave column).
+static int norm_parts(const moe_layer* L) {
+  return L->dtype == MOE_BF16 ? (L->I + CB::RB - 1) / CB::RB : 2 * ((L->I + G_BN - 1) / G_BN);
+}
+
+// Backward workspace: schedule | dA_g | dA_u | per-row norm partials (float2) |
+// per-token norms (float2) | utility tile sums (double).
+struct BwdWs {
+  char* dAg;
+  char* dAu;
+  float2* norms;
+  float2* tnorm;
+  double* part;
+};
+static size_t bwd_act_bytes(const moe_layer* L, int T, int k) {
+  return round256(rows_total(L, T, k) * L->I * esize(L->dtype));
+}
+static BwdWs bwd_ws_at(void* ws, const moe_layer* L, int T, int k) {
+  BwdWs w;
+  const size_t act = bwd_act_bytes(L, T, k);
+  char* p = (char*)ws + sched_bytes(n_slots(L));
+  w.dAg = p;
+  w.dAu = p + act;
+  p += 2 * act;
+  w.norms = (float2*)p;
+  p += round256(sizeof(float2) * rows_total(L, T, k) * norm_parts(L));
+  w.tnorm = (float2*)p;
+  p += round256(sizeof(float2) * (size_t)T);
+  w.part = (double*)p;
+  return w;
 }
 
 extern "C" size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k) {
   if (!L || T < 0 || k <= 0) return 0;
-  const size_t act = round256(rows_total(L, T, k) * L->I * esize(L->dtype));
-  return sched_bytes(n_slots(L)) + 2 * act + round256(sizeof(double) * utility_tiles(L, T, k));
+  return sched_bytes(n_slots(L)) + 2 * bwd_act_bytes(L, T, k) +
+         round256(sizeof(float2) * rows_total(L, T, k) * norm_parts(L)) + round256(sizeof(float2) * (size_t)T) +
+         round256(sizeof(double) * utility_tiles(L, T, k));
 }
 
 extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const void* X_perm,
@@ -1147,7 +1253,7 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
   hipStream_t st = as_stream(stream);
   const int S = n_slots(L);
   const Sched sc = sched_at(ws, S);
-  const int tile_rows = L->dtype == MOE_BF16 ? B16_ROWS : G_BM;
+  const int tile_rows = bwd_tile_rows(L);
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, tile_rows,
                      (float* const*)nullptr, sc.mbase, sc.wbase, sc.dorder, sc.queues);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
@@ -1237,11 +1343,11 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   hipStream_t st = as_stream(stream);
   const int S = n_slots(L);
   const Sched sc = sched_at(ws, S);
-  const size_t act = round256(rows_total(L, T, k) * L->I * esize(L->dtype));
-  char* dAg = (char*)ws + sched_bytes(S);
-  char* dAu = dAg + act;
+  const BwdWs bw = bwd_ws_at(ws, L, T, k);
+  char* dAg = bw.dAg;
+  char* dAu = bw.dAu;
   const int d = L->d, I = L->I;
-  const int tile_rows = L->dtype == MOE_BF16 ? B16_ROWS : G_BM;
+  const int tile_rows = bwd_tile_rows(L);
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, tile_rows,
                      L->dw_gate, sc.mbase, sc.wbase, sc.dorder, sc.queues);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, d, I};
@@ -1252,7 +1358,7 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
 #define FM_BWD(TT)                                                                                        \
   if (T > 0) {                                                                                            \
     hipLaunchKernelGGL(kf_dh<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dO, (const TT*)A_g,   \
-                       (const TT*)A_u, ra, (TT*)dAg, (TT*)dAu);                                          \
+                       (const TT*)A_u, ra, (TT*)dAg, (TT*)dAu, bw.norms);                                \
     hipLaunchKernelGGL(kf_dx<TT>, grid, block, 0, st, layer_ptrs<TT>(L), (const TT*)dAg, (const TT*)dAu, \
                        ra, (TT*)dX_perm);                                                                \
   }                                                                                                       \
@@ -1263,7 +1369,7 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
     const dim3 b8(CB::THREADS);
     if (T > 0) {
       hipLaunchKernelGGL(kb_dh, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dO, (cbp)A_g, (cbp)A_u, ra,
-                         (bf16*)dAg, (bf16*)dAu);
+                         (bf16*)dAg, (bf16*)dAu, bw.norms);
       hipLaunchKernelGGL(kb_dx, grid, b8, 0, st, layer_ptrs<bf16>(L), (cbp)dAg, (cbp)dAu, ra, (bf16*)dX_perm);
     }
     if (accumulate_dw) {
@@ -1282,9 +1388,9 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   return check_launch("moe_grouped_swiglu_bwd");
 }
 
-extern "C" int moe_expert_utility(const moe_layer* L, const void* X, const void* X_perm, const int32_t* offsets,
-                                  int T, int k, const void* H, const void* dO, void* ws, size_t ws_bytes,
-                                  float* utility, void* stream) {
+extern "C" int moe_expert_utility(const moe_layer* L, const void* X, const void* dY, const int32_t* perm_token,
+                                  const float* perm_gate, const int32_t* offsets, int T, int k, void* ws,
+                                  size_t ws_bytes, float* utility, void* stream) {
   clear_error();
   FM_TRY(check_layer_ffn(L));
   if (T < 0 || k <= 0 || k > 16) return fail(MOE_ERR_ARG, "T=%d k=%d", T, k);
@@ -1295,30 +1401,27 @@ extern "C" int moe_expert_utility(const moe_layer* L, const void* X, const void*
     hipLaunchKernelGGL(k_zero_f32, dim3(cdiv(S, 256)), dim3(256), 0, st, utility, S);
     return check_launch("moe_expert_utility");
   }
-  FM_TRY(need(X, "X")); FM_TRY(need(offsets, "offsets")); FM_TRY(need(H, "H")); FM_TRY(need(dO, "dO"));
-  FM_TRY(need(ws, "ws"));
-  if (L->S_routed > 0) FM_TRY(need(X_perm, "X_perm"));
-  FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(X_perm, "X_perm")); FM_TRY(need_aligned(H, "H"));
-  FM_TRY(need_aligned(dO, "dO")); FM_TRY(need_aligned(ws, "ws"));
+  FM_TRY(need(X, "X")); FM_TRY(need(dY, "dY")); FM_TRY(need(offsets, "offsets")); FM_TRY(need(ws, "ws"));
+  if (L->S_routed > 0) {
+    FM_TRY(need(perm_token, "perm_token")); FM_TRY(need(perm_gate, "perm_gate"));
+  }
+  FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(dY, "dY")); FM_TRY(need_aligned(ws, "ws"));
   if (ws_bytes < moe_grouped_swiglu_bwd_workspace_size(L, T, k))
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_bwd_workspace_size(L, T, k));
+  // the backward's row-tile schedule (same offsets) is still in the workspace
   const Sched sc = sched_at(ws, S);
-  const size_t act = round256(rows_total(L, T, k) * L->I * esize(L->dtype));
-  const char* dAg = (const char*)ws + sched_bytes(S);
-  const char* dAu = dAg + act;
-  double* part = (double*)((char*)ws + sched_bytes(S) + 2 * act);
-  const int ut_rows = utility_tile_rows(L, T, k);
-  hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, ut_rows,
-                     (float* const*)nullptr, sc.mbase, sc.wbase, sc.dorder, sc.queues);
+  const BwdWs bw = bwd_ws_at(ws, L, T, k);
+  const dim3 tg(cdiv(T, 4));
+  if (L->dtype == MOE_BF16)
+    hipLaunchKernelGGL(k_token_norms<bf16>, tg, dim3(256), 0, st, (const bf16*)X, (const bf16*)dY, T, L->d, bw.tnorm);
+  else
+    hipLaunchKernelGGL(k_token_norms<float>, tg, dim3(256), 0, st, (const float*)X, (const float*)dY, T, L->d,
+                       bw.tnorm);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
-  const dim3 grid((unsigned)utility_tiles(L, T, k, ut_rows));
-#define FM_UT(TT)                                                                                            \
-  hipLaunchKernelGGL(k_utility_rows<TT>, grid, dim3(256), 0, st, (const TT*)X, (const TT*)X_perm, (const TT*)dO, \
-                     (const TT*)H, (const TT*)dAg, (const TT*)dAu, ra, ut_rows, part)
-  if (L->dtype == MOE_BF16) FM_UT(bf16);
-  else FM_UT(float);
-#undef FM_UT
-  hipLaunchKernelGGL(k_utility_slots, dim3(1), dim3(1024), 0, st, ra, (const double*)part, utility);
+  hipLaunchKernelGGL(k_utility_rows, dim3((unsigned)utility_tiles(L, T, k)), dim3(UT_THREADS), 0, st, ra,
+                     bwd_tile_rows(L), perm_token, perm_gate, (const float2*)bw.tnorm, (const float2*)bw.norms,
+                     norm_parts(L), bw.part);
+  hipLaunchKernelGGL(k_utility_slots, dim3(1), dim3(1024), 0, st, ra, (const double*)bw.part, utility);
   return check_launch("moe_expert_utility");
 }

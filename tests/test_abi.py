@@ -33,7 +33,7 @@ def test_every_declared_function_is_exported_and_bound(L):
     for n in names:
         assert hasattr(L, n), n
         assert n in api.exported_names(), n
-    assert L.moe_abi_version() == 1
+    assert L.moe_abi_version() == 2
 
 
 FAKE = 0x100000          # aligned, never dereferenced: validation fails first
@@ -143,12 +143,15 @@ def test_permute_workspace_and_layer_rejections(L):
                        FAKE, MIS, FAKE, 0, FAKE, ctypes.c_size_t(bneed), None)
     assert rc == api.MOE_ERR_ALIGN
     # the utility pass reads the backward's workspace: same size required
-    rc, msg = rc_and_msg(L, "moe_expert_utility", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
-                         FAKE, ctypes.c_size_t(bneed - 1), FAKE, None)
+    rc, msg = rc_and_msg(L, "moe_expert_utility", ctypes.byref(lay), FAKE, FAKE, FAKE, FAKE, FAKE, 8192, 6, FAKE,
+                         ctypes.c_size_t(bneed - 1), FAKE, None)
     assert rc == api.MOE_ERR_WORKSPACE and "workspace" in msg
-    rc, msg = rc_and_msg(L, "moe_expert_utility", ctypes.byref(lay), FAKE, FAKE, FAKE, 8192, 6, FAKE, FAKE,
-                         FAKE, ctypes.c_size_t(bneed), None, None)
+    rc, msg = rc_and_msg(L, "moe_expert_utility", ctypes.byref(lay), FAKE, FAKE, FAKE, FAKE, FAKE, 8192, 6, FAKE,
+                         ctypes.c_size_t(bneed), None, None)
     assert rc == api.MOE_ERR_ARG and "utility" in msg
+    rc, msg = rc_and_msg(L, "moe_expert_utility", ctypes.byref(lay), FAKE, FAKE, None, FAKE, FAKE, 8192, 6, FAKE,
+                         ctypes.c_size_t(bneed), FAKE, None)
+    assert rc == api.MOE_ERR_ARG and "perm_token" in msg        # routed slots need the maps
     rc, _ = rc_and_msg(L, "moe_unpermute", None, FAKE, FAKE, FAKE, 8, 2, FAKE, None)
     assert rc == api.MOE_ERR_ARG
     rc, _ = rc_and_msg(L, "moe_permute_bwd", ctypes.byref(lay), FAKE, FAKE, 8, 17, FAKE, None)
