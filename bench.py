@@ -77,6 +77,16 @@ def ffn_flops(r, offsets):
     return fwd, bwd
 
 
+def ffn_rows(r, offsets):
+    """Row and slot counts of the step's grouped SwiGLU (the operand sizes of its
+    kernels): rows of all slots and of tuning slots, slots with rows."""
+    w = r.w
+    rows = [int(offsets[s + 1] - offsets[s]) for s in range(r.S_r)] + [w.T] * w.n_shared
+    return {"total": sum(rows), "tuning": sum(n for s, n in enumerate(rows) if r.tuning[s]),
+            "slots": sum(1 for n in rows if n), "tuning_slots": sum(1 for s in range(len(rows)) if r.tuning[s]),
+            "d": w.d, "I": w.I, "bytes": w.x_bytes}
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -481,7 +491,8 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "grouped SwiGLU fwd+bwd (moe_grouped_swiglu_fwd + _bwd)",
                      "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": measured_traffic(a.workload),
-                     "flops_per_step": fl_fwd + fl_bwd, "ms": round(ffn_ms, 4)},
+                     "flops_per_step": fl_fwd + fl_bwd, "ms": round(ffn_ms, 4),
+                     "rows": ffn_rows(r, offsets)},
         "stages_ms": {k: round(v, 4) for k, v in per.items()},
         "hbm_kernels_GBps": {"route": gbs(route_bytes, per["route"]), "profile": gbs(hist_bytes, per["profile"]),
                              "merge": gbs(merge_bytes, per["merge"]), "permute": gbs(permute_bytes, per["permute"])},

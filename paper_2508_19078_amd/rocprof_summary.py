@@ -83,6 +83,23 @@ def counter_per_kernel(path: str, counter: str):
     return {k: list(v.values()) for k, v in per.items()}
 
 
+def operand_bytes(rows: dict):
+    """Distinct bytes each grouped-SwiGLU kernel must read and write in one step
+    (every operand once, no padding): rows['total'] rows over rows['slots']
+    slots with rows, rows['tuning'] rows of rows['tuning_slots'] tuning slots."""
+    n, nt, s, st = rows["total"], rows["tuning"], rows["slots"], rows["tuning_slots"]
+    d, I, b = rows["d"], rows["I"], rows["bytes"]
+    w = d * I * b                      # one matrix of one slot
+    return {
+        "kb_gate_up": (n * d * b + 2 * s * w, 3 * n * I * b),
+        "kb_down": (n * I * b + s * w, n * d * b),
+        "kb_dh": (n * d * b + s * w + 2 * n * I * b, 2 * n * I * b),
+        "kb_dx": (2 * n * I * b + 2 * s * w, n * d * b),
+        "kb_dw_gu": (2 * nt * I * b + nt * d * b, 2 * st * d * I * 4),
+        "kb_dw_d": (nt * (d + I) * b, st * d * I * 4),
+    }
+
+
 def traffic(fetch_csv: str, write_csv: str, calib_bytes: int):
     res = {}
     for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
@@ -116,6 +133,7 @@ def main():
     t.add_argument("--cmd-fetch", required=True)
     t.add_argument("--cmd-write", required=True)
     t.add_argument("--calib-bytes", type=int, default=256 << 20)
+    t.add_argument("--bench-json", help="the bench's JSON line (roofline.rows: operand sizes of the step)")
     a = ap.parse_args()
     if a.what == "stats":
         print(f"command: `{a.cmd}`\n")
@@ -127,10 +145,27 @@ def main():
     print(f"Calibration: a device-to-device copy of {a.calib_bytes} bytes reads FETCH_SIZE "
           f"{f['calib_kib']:.0f} KiB (factor {f['factor']:.4f}) and WRITE_SIZE {w['calib_kib']:.0f} KiB "
           f"(factor {w['factor']:.4f}).\n")
-    print("| kernel | FETCH KiB/step | WRITE KiB/step |")
-    print("|---|---|---|")
+    ops = None
+    if a.bench_json:
+        import json
+        for line in open(a.bench_json):
+            if line.startswith("{"):
+                ops = operand_bytes(json.loads(line)["roofline"]["rows"])
+    print("Per step.  Raw = the counter as read (KiB); scaled = raw x the copy's factor (bytes);"
+          " operand = the distinct bytes the kernel must read or write (every operand once);"
+          " ratio = scaled / operand.\n")
+    print("| kernel | FETCH raw KiB | fetch scaled MB | operand read MB | read ratio | WRITE raw KiB | "
+          "write scaled MB | operand write MB | write ratio |")
+    print("|---|---|---|---|---|---|---|---|---|")
     for k in FFN_KERNELS:
-        print(f"| {k} | {f['per_kernel_kib'][k]:.0f} | {w['per_kernel_kib'][k]:.0f} |")
+        fr, wr = f["per_kernel_kib"][k], w["per_kernel_kib"][k]
+        fs, ws_ = fr * 1024 * f["factor"], wr * 1024 * w["factor"]
+        if ops and k in ops:
+            ro, wo = ops[k]
+            print(f"| {k} | {fr:.0f} | {fs / 1e6:.1f} | {ro / 1e6:.1f} | {fs / ro:.2f} | {wr:.0f} | {ws_ / 1e6:.1f} | "
+                  f"{wo / 1e6:.1f} | {ws_ / wo:.2f} |")
+        else:
+            print(f"| {k} | {fr:.0f} | {fs / 1e6:.1f} | | | {wr:.0f} | {ws_ / 1e6:.1f} | | |")
     others = sorted(set(f["other_bytes"]) | set(w["other_bytes"]))
     if others:
         print("\nOther kernels of the library, scaled HBM bytes per dispatch (mean over dispatches):\n")
@@ -140,7 +175,13 @@ def main():
             print(f"| {k} | {f['other_bytes'].get(k, 0) / 1e6:.2f} | {w['other_bytes'].get(k, 0) / 1e6:.2f} |")
     total = f["bytes_per_step"] + w["bytes_per_step"]
     print(f"\nHBM traffic of the grouped SwiGLU fwd+bwd per step (scaled): fetch {f['bytes_per_step']:.4g} B, "
-          f"write {w['bytes_per_step']:.4g} B, total {total:.4g} B.\n")
+          f"write {w['bytes_per_step']:.4g} B, total {total:.4g} B", end="")
+    if ops:
+        ro = sum(ops[k][0] for k in ops)
+        wo = sum(ops[k][1] for k in ops)
+        print(f"; operands {ro:.4g} B read and {wo:.4g} B written ({total / (ro + wo):.2f}x).\n")
+    else:
+        print(".\n")
     print("```")
     print(f"source_sha256: {ffn_source_hash()}")
     print(f"traffic_bytes: {total:.0f}")
