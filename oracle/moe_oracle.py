@@ -128,11 +128,14 @@ def topk_gap(logits, k: int) -> np.ndarray:
 def quantize_int8_rows(W):
     """Per-row symmetric int8 quantisation of a router weight (Section 4.1).
 
-    s_e = max_i |W[e,i]| / 127 and q = clamp(round_half_even(W / s_e), -127, 127);
-    a zero row gets s_e = 0 and q = 0.  The division and the rounding decide an
-    integer, so they are done in float32, the precision of the kernel (W is a
-    bf16 or fp32 value, so max|W| is exact in float32 and the float32 quotient is
-    the correctly rounded one).
+    The section does not say how the low-bit copy is made; this is the
+    definition of the int8 copy used throughout: s_e = max_i |W[e,i]| / 127 and
+    q = clamp(round_half_even(W / s_e), -127, 127), a zero row getting s_e = 0
+    and q = 0, with s_e, the division and the rounding in float32, the precision
+    the copy's scales are stored in.  The division and the rounding decide an
+    integer, so their precision is part of the definition, not an implementation
+    detail (W is a bf16 or fp32 value, so max|W| is exact in float32 and the
+    float32 quotient is the correctly rounded one).
     """
     W32 = np.asarray(W, dtype=np.float32)
     amax = np.max(np.abs(W32), axis=1)

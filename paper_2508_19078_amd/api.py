@@ -85,6 +85,7 @@ _SIGS = {
 }
 
 _lib = None
+ABI_VERSION = 2   # FLUXMOE_ABI_VERSION of the header these signatures follow
 
 
 def lib() -> ctypes.CDLL:
@@ -98,6 +99,10 @@ def lib() -> ctypes.CDLL:
         for name, (res, args) in _SIGS.items():
             fn = getattr(L, name)
             fn.restype, fn.argtypes = res, args
+        v = L.moe_abi_version()
+        if v != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {v}, this binding marshals version {ABI_VERSION}: "
+                               "rebuild it with `python -m paper_2508_19078_amd.build`")
         _lib = L
     return _lib
 

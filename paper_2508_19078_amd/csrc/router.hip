@@ -1,17 +1,21 @@
 // Router (softmax top-k gate), int8 router quantiser and the activation
 // histogram of the int8 profiling router.
 //
-// One kernel serves both the full-precision router and the int8 profiling
-// router: a block owns 32 tokens and accumulates the token x expert logits on
-// MFMA.  For bf16 activations with at most 64 experts and d a multiple of 256
-// (every bf16 workload here) the operands stream through an LDS ring
-// (k_route_lds); otherwise (fp32, wider routers) the waves split the hidden
-// dimension into 16-byte-per-lane register chunks (k_route).  The waves'
-// partial sums are added in a fixed order, so the logits do not depend on
-// scheduling.  Then 16 lanes per token select the top k by (logit desc, index
-// asc) with branch-free 64-bit key reductions, and either write idx/gate or
-// add the selection to an LDS histogram that is flushed to the global counts
-// with one integer atomic per expert and block.
+// One kernel family serves both the full-precision router and the int8
+// profiling router: a block accumulates the logits of a tile of tokens against
+// every expert on MFMA.  For bf16 activations with at most 64 experts and d a
+// multiple of 256 the operands stream through an LDS ring: k_route_p keeps one
+// persistent block per compute unit walking 32-token tiles (64-token tiles once
+// every compute unit gets one) and issues the next tile's first slabs before
+// the current tile's selection; k_route_lds, one 32-token tile per block, is
+// kept for the int8 histogram at smaller T, where it measured faster.
+// Otherwise (fp32, wider routers) the waves split the hidden dimension into
+// 16-byte-per-lane register chunks (k_route).  The waves' partial sums are
+// added in a fixed order, so the logits do not depend on scheduling.  Then 16
+// lanes per token select the top k by (logit desc, index asc) with branch-free
+// 64-bit key reductions, and either write idx/gate or add the selection to an
+// LDS histogram that is flushed to the global counts with one integer atomic
+// per expert and block.
 #include "common.hpp"
 #include "gemm_bf16.hpp"
 

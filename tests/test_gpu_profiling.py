@@ -34,9 +34,11 @@ pytestmark = pytest.mark.gpu
 TOL_X = 2e-2
 WIN = 1e-6          # the near-tie window of the routing bar
 # Share of tokens a chained layer may exclude: its window grows with the
-# difference between the GPU's bf16 stream and the oracle's fp64 one.  Measured:
-# 7.6 % at the second full-size DeepSeek-stack layer, 4.1-4.3 % on the small
-# stacks; the bound leaves half as much again.
+# difference between the GPU's bf16 stream and the oracle's fp64 one, starting
+# with the bf16 rounding of the normalised input of the first layer.  Measured
+# (the kernels are deterministic, so every run gives the same counts): 6.2 % and
+# 11.4 % at the two full-size DeepSeek-stack layers, 0-7 % on the small stacks.
+# The teacher-forced test below has no such window: zero exclusions there.
 MAX_EXCLUDED = 0.12
 
 
