@@ -389,6 +389,11 @@ __global__ __launch_bounds__(256) void k_combine(const T* __restrict__ O, const 
 }
 
 // dO[p] = perm_gate[p] dY[t]; shared rows get dY[t]; dgate[t,j] = <dY[t], O[row]>.
+// A lane loads CB_PF chunks of dY[t] before it stores any of them, so a wave
+// waits for one load latency per CB_PF chunks (one for a whole 2048-wide bf16
+// row) instead of one per chunk.
+constexpr int CB_PF = 4;
+
 template <typename T, int KMAX>
 __global__ __launch_bounds__(256) void k_combine_bwd(const T* __restrict__ dY, const T* __restrict__ O,
                                                      const int32_t* __restrict__ inv,
@@ -407,27 +412,36 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const T* __restrict__ dY, c
     g[j] = p[j] >= 0 ? pg[p[j]] : 0.f;
     dot[j] = 0.f;
   }
-  for (int c = lane_id() * V; c < d; c += 64 * V) {
-    const u32x4_t raw = ld16(dY + (size_t)t * d + c);
-    float f[V];
-    unpack16(raw, f, (T*)nullptr);
+  for (int c0 = lane_id() * V; c0 < d; c0 += CB_PF * 64 * V) {
+    u32x4_t rawp[CB_PF];
 #pragma unroll
-    for (int j = 0; j < KMAX; ++j) {
-      if (j >= k) continue;
-      if (p[j] >= 0) {
-        float o[V];
+    for (int u = 0; u < CB_PF; ++u)
+      if (c0 + u * 64 * V < d) rawp[u] = ld16(dY + (size_t)t * d + c0 + u * 64 * V);
 #pragma unroll
-        for (int i = 0; i < V; ++i) o[i] = g[j] * f[i];
-        st16(dO + (size_t)p[j] * d + c, pack16(o, (T*)nullptr));
+    for (int u = 0; u < CB_PF; ++u) {
+      const int c = c0 + u * 64 * V;
+      if (c >= d) break;
+      const u32x4_t raw = rawp[u];
+      float f[V];
+      unpack16(raw, f, (T*)nullptr);
+#pragma unroll
+      for (int j = 0; j < KMAX; ++j) {
+        if (j >= k) continue;
+        if (p[j] >= 0) {
+          float o[V];
+#pragma unroll
+          for (int i = 0; i < V; ++i) o[i] = g[j] * f[i];
+          st16(dO + (size_t)p[j] * d + c, pack16(o, (T*)nullptr));
+        }
+        if (dgate) {
+          float o[V];
+          unpack16(ld16(O + (size_t)row_of(p[j]) * d + c), o, (T*)nullptr);
+#pragma unroll
+          for (int i = 0; i < V; ++i) dot[j] = fmaf(f[i], o[i], dot[j]);
+        }
       }
-      if (dgate) {
-        float o[V];
-        unpack16(ld16(O + (size_t)row_of(p[j]) * d + c), o, (T*)nullptr);
-#pragma unroll
-        for (int i = 0; i < V; ++i) dot[j] = fmaf(f[i], o[i], dot[j]);
-      }
+      for (int sh = 0; sh < S_sh; ++sh) st16(dO + (R + (size_t)sh * Tn + t) * d + c, raw);
     }
-    for (int sh = 0; sh < S_sh; ++sh) st16(dO + (R + (size_t)sh * Tn + t) * d + c, raw);
   }
   if (dgate) {
 #pragma unroll
@@ -478,6 +492,15 @@ int check_tk(int T, int k) {
   if ((k) <= 2) { MACRO(2); }      \
   else if ((k) <= 4) { MACRO(4); } \
   else if ((k) <= 8) { MACRO(8); } \
+  else { MACRO(16); }
+// The combine holds a register set per possible choice (KMAX + 2 rows of two
+// chunks); an instance for k <= 6 keeps k = 6 layers at 114 instead of 137
+// VGPRs (measured 65 -> 63 us cold at T = 8192, d = 2048).
+#define FM_KSWITCH_COMBINE(k, MACRO) \
+  if ((k) <= 2) { MACRO(2); }        \
+  else if ((k) <= 4) { MACRO(4); }   \
+  else if ((k) <= 6) { MACRO(6); }   \
+  else if ((k) <= 8) { MACRO(8); }   \
   else { MACRO(16); }
 
 // Compute units of the current device (256 on MI355X when the query fails).
@@ -708,7 +731,7 @@ extern "C" int moe_unpermute(const moe_layer* L, const void* O, const int32_t* i
   else                                                                                            \
     hipLaunchKernelGGL((k_combine<float, KM>), grid, block, 0, st, (const float*)O, inv,          \
                        perm_gate, T, k, L->d, L->S_shared, (float*)Y);
-  FM_KSWITCH(k, FM_CB)
+  FM_KSWITCH_COMBINE(k, FM_CB)
 #undef FM_CB
   return check_launch("moe_unpermute");
 }
