@@ -375,12 +375,30 @@ def profiling_stack(reps=3):
         passes.append((evs[0].elapsed_time(evs[-1]), stages))
     total = float(np.median([p[0] for p in passes[1:]]))
     stages = {nm: round(float(np.median([p[1][nm] for p in passes[1:]])), 3) for nm in passes[1][1]}
+    # the whole pass captured once into a HIP graph and replayed (same kernels)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        qs.run(X0)
+    graph.replay()
+    torch.cuda.synchronize()
+    gts = []
+    for _ in range(reps):
+        e0.record(st)
+        graph.replay()
+        e1.record(st)
+        torch.cuda.synchronize()
+        gts.append(e0.elapsed_time(e1))
+    graph_ms = float(np.median(gts))
+    del graph
+    Xout = qs.run(X0)
+    torch.cuda.synchronize()
     counts = qs.counts.cpu().numpy()
     # the grouped forward's algorithmic flops: 6 d I per routed row (T k rows per layer; no shared experts)
     ffn_flops = 6.0 * d * I * T * k * L
     out = {"workload": f"deepseek_stack: {L} layers x {E} experts, d={d} I={I}, T={T}, top-{k}, int8 router "
                        "and experts (per-row scales), RMS-normalised layer inputs, residual stream",
            "pass_ms": round(total, 3), "tokens_per_s": round(T / (total * 1e-3), 1),
+           "graph_pass_ms": round(graph_ms, 3),
            "stages_ms": stages, "quantise_ms": round(quant_ms, 3),
            "ffn_fwd_TFLOPs": round(ffn_flops / (stages["ffn_fwd"] * 1e-3) / 1e12, 1),
            "ffn_fwd_frac_bf16_peak": round(ffn_flops / (stages["ffn_fwd"] * 1e-3) / 2.5e15, 4),
@@ -460,6 +478,20 @@ def main():
     ms_step = wall * 1e3 / a.steps
     tok_s = w.T / (ms_step / 1e3)
 
+    # the same step captured once into a HIP graph and replayed (no per-call
+    # host work; the replays run the same kernels on the same buffers)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        r.step()
+    graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms_graph = (time.perf_counter() - t0) * 1e3 / a.steps
+    del graph
+
     offsets = r.offsets.cpu().numpy()
     fl_fwd, fl_bwd = ffn_flops(r, offsets)
     ffn_ms = per["ffn_fwd"] + per["ffn_bwd"]
@@ -494,6 +526,7 @@ def main():
                      "flops_per_step": fl_fwd + fl_bwd, "ms": round(ffn_ms, 4),
                      "rows": ffn_rows(r, offsets)},
         "stages_ms": {k: round(v, 4) for k, v in per.items()},
+        "graph_ms_per_step": round(ms_graph, 4),
         "hbm_kernels_GBps": {"route": gbs(route_bytes, per["route"]), "profile": gbs(hist_bytes, per["profile"]),
                              "merge": gbs(merge_bytes, per["merge"]), "permute": gbs(permute_bytes, per["permute"])},
     }
