@@ -1,7 +1,10 @@
 """HIP path vs the fp64 oracle, element by element, on shapes the oracle
 finishes in seconds: several row tiles per slot, ragged row counts, N and K
 tails (I = 200, 384 and 688), merged and frozen slots, a shared expert, and the
-fp32 workload.  Everything goes through the C ABI."""
+fp32 workload; then eight seeded irregular layers (d and I multiples of 8 but
+not of 16 or of a tile, tens of tokens to a thousand, one to 79 experts, up to
+two shared experts, everything but a few experts merged, both storage types).
+Everything goes through the C ABI."""
 import numpy as np
 import pytest
 import torch
@@ -24,6 +27,39 @@ CASES = {
     "small_deepseek": W.scaled(W.WORKLOADS["deepseek_moe"], name="small_deepseek", cid=103, T=1030, d=256,
                                I=384),
 }
+
+
+def _irregular(n, seed=25081907):
+    """Seeded layers off every tile grid: d, I multiples of 8 in [24, 1032] and
+    [24, 792], T in [1, 1100], E in [1, 79], k up to min(E, 8), 0-2 shared
+    experts, the frequency merge of n_merge = g * j experts in groups of g, a
+    zero, normal or Zipf router bias; cases 2 and 6 in fp32."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    out = {}
+    for i in range(n):
+        f32 = i in (2, 6)
+        d = 8 * int(rng.integers(3, 130))
+        I = 8 * int(rng.integers(3, 100))
+        E = int(rng.integers(1, 80))
+        k = int(rng.integers(1, min(E, 8) + 1))
+        T = int(rng.integers(1, 1100))
+        ns = int(rng.integers(0, 3))
+        merge, n_tune = None, None
+        if E >= 4 and rng.random() < 0.7:
+            g = int(rng.integers(2, 5))
+            m = g * int(rng.integers(1, E // g + 1))
+            merge, n_tune = ("frequency", m, g), int(rng.integers(0, E - m + 1))
+        bias = ["zero", "normal", "zipf"][int(rng.integers(0, 3))]
+        name = f"irregular{i}"
+        out[name] = W.LayerWorkload(name=name, cid=300 + i, T=T, d=d, E=E, k=k, I=I,
+                                    dtype="f32" if f32 else "bf16", n_shared=ns, bias_kind=bias,
+                                    bias_var=1.0 if bias == "normal" else 0.0,
+                                    zipf_s=1.2 if bias == "zipf" else 0.0, merge=merge, n_tune=n_tune)
+    return out
+
+
+CASES.update(_irregular(8))
 
 
 class Run:
