@@ -227,6 +227,144 @@ __device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int
   }
 }
 
+// Selection in small lane groups, for the logits of TT tokens in LDS (the sum,
+// in order, of NPART partials stage[p * PSTRIDE + token * EP + expert], times
+// scale and plus bias as in route_select): LPT = 4 or 8 lanes per token, lane q of the group
+// holding experts [q NQ, (q+1) NQ) as 64-bit keys (ordered fp32 value,
+// 0xFFFF - expert; -0.0 == +0.0), so that a selection round is a local maximum
+// over the lane's NQ keys (a tree of independent compares) and log2(LPT) lane
+// exchanges (DPP quad permutations, then a swizzle across quads), and the k
+// rounds of a token run in one lane group with no loop over tokens (16 lanes
+// per token and one token after another left each round a chain of dependent
+// row rotations that one wave per SIMD could not hide).  Rank j of a token
+// lands in lane j % LPT of its group.  Same outputs and order as
+// route_select; the softmax denominator adds each lane's ranks in order, then
+// the group's lanes by the same exchanges.
+template <int CTRL> __device__ __forceinline__ uint64_t quad_perm64(uint64_t x) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, 0xF, 0xF, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+template <int CTRL> __device__ __forceinline__ float quad_perm_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+constexpr int QP_SWAP1 = 0xB1;   // quad_perm [1, 0, 3, 2]
+constexpr int QP_SWAP2 = 0x4E;   // quad_perm [2, 3, 0, 1]
+
+template <int LPT> __device__ __forceinline__ uint64_t group_max64(uint64_t b) {
+  uint64_t o = quad_perm64<QP_SWAP1>(b);
+  b = o > b ? o : b;
+  o = quad_perm64<QP_SWAP2>(b);
+  b = o > b ? o : b;
+  if (LPT == 8) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)b, 4);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(b >> 32), 4);
+    o = ((uint64_t)hi << 32) | lo;
+    b = o > b ? o : b;
+  }
+  return b;
+}
+template <int LPT> __device__ __forceinline__ float group_sum(float x) {
+  x += quad_perm_f<QP_SWAP1>(x);
+  x += quad_perm_f<QP_SWAP2>(x);
+  if (LPT == 8) x += __shfl_xor(x, 4);
+  return x;
+}
+
+template <int LPT, int NQ, int KMAX, int MODE, int WAVES, int TT, int NPART = 1>
+__device__ __forceinline__ void route_select_q(const float* stage, int PSTRIDE, int EP, const float* scale,
+                                               const float* bias,
+                                               int t0, int T, int E, int k, int32_t* __restrict__ idx,
+                                               float* __restrict__ gate, float* __restrict__ logits,
+                                               int* hist) {
+  static_assert(LPT == 4 || LPT == 8, "4 or 8 lanes per token");
+  constexpr int GPW = 64 / LPT;                                 // lane groups per wave
+  constexpr int TPL = (TT + WAVES * GPW - 1) / (WAVES * GPW);   // tokens per lane group
+  constexpr int RPL = (KMAX + LPT - 1) / LPT;                   // ranks held per lane
+  const int lane = lane_id(), wave = threadIdx.x >> 6;
+  const int grp = lane / LPT, q = lane % LPT;
+#pragma unroll
+  for (int u = 0; u < TPL; ++u) {
+    const int tl = u * WAVES * GPW + wave * GPW + grp;
+    const bool on = tl < TT;
+    const int tc = on ? tl : 0;
+    uint64_t key[NQ];
+#pragma unroll
+    for (int i = 0; i < NQ; ++i) {
+      const int e = q * NQ + i;
+      float v = 0.f;
+      if (e < E) {
+        v = stage[tc * EP + e];
+#pragma unroll
+        for (int p = 1; p < NPART; ++p) v += stage[p * PSTRIDE + tc * EP + e];
+        if (scale) v *= scale[e];
+        if (bias) v += bias[e];
+        if (MODE == 0 && logits && on && t0 + tc < T) logits[(size_t)(t0 + tc) * E + e] = v;
+      }
+      v += 0.0f;
+      key[i] = (on && e < E) ? (((uint64_t)ordered_key(v) << 32) | (uint64_t)(0xFFFFu - (uint32_t)e)) : 0ull;
+    }
+    float rv[RPL], v0 = 0.f;
+    int re[RPL];
+#pragma unroll
+    for (int r = 0; r < RPL; ++r) {
+      rv[r] = 0.f;
+      re[r] = 0;
+    }
+#pragma unroll
+    for (int j = 0; j < KMAX; ++j) {
+      if (j < k) {
+        uint64_t m[NQ];
+#pragma unroll
+        for (int i = 0; i < NQ; ++i) m[i] = key[i];
+#pragma unroll
+        for (int w = NQ / 2; w > 0; w >>= 1)
+#pragma unroll
+          for (int i = 0; i < w; ++i) m[i] = m[i + w] > m[i] ? m[i + w] : m[i];
+        const uint64_t b = group_max64<LPT>(m[0]);
+        const int e = 0xFFFF - (int)(uint32_t)(b & 0xFFFFu);
+        const float v = key_value((uint32_t)(b >> 32));
+        if (j == 0) v0 = v;
+        if (q == j % LPT) {
+          rv[j / LPT] = v;
+          re[j / LPT] = e;
+        }
+#pragma unroll
+        for (int i = 0; i < NQ; ++i)
+          if (q * NQ + i == e) key[i] = 0ull;
+      }
+    }
+    const int t = t0 + tl;
+    if (MODE != 1) {                 // idx and the softmax gate over the k selected
+      float g[RPL], sum = 0.f;
+#pragma unroll
+      for (int r = 0; r < RPL; ++r) {
+        g[r] = LPT * r + q < k ? expf(rv[r] - v0) : 0.f;
+        sum += g[r];
+      }
+      sum = group_sum<LPT>(sum);
+#pragma unroll
+      for (int r = 0; r < RPL; ++r) {
+        const int j = LPT * r + q;
+        if (j < k && on && t < T) {
+          idx[(size_t)t * k + j] = re[r];
+          gate[(size_t)t * k + j] = g[r] / sum;
+        }
+      }
+    }
+    if (MODE != 0) {                 // histogram (+ idx alone in MODE 1)
+#pragma unroll
+      for (int r = 0; r < RPL; ++r) {
+        const int j = LPT * r + q;
+        if (j < k && on && t < T) {
+          atomicAdd(&hist[re[r]], 1);
+          if (MODE == 1 && idx) idx[(size_t)t * k + j] = re[r];
+        }
+      }
+    }
+  }
+}
+
 // MODE 0: write idx/gate (+logits).  MODE 1: histogram (+idx).  MODE 2:
 // histogram, idx and gate.
 template <typename TX, typename TW, int NE, int KMAX, int MODE>
@@ -511,9 +649,15 @@ __global__ __launch_bounds__(256) void k_route_lds(const bf16* __restrict__ X, c
         red[(wave * RT_TOK + 8 * (r >> 2) + 4 * (L >> 5) + (r & 3)) * EP + 32 * b + (L & 31)] = acc[b][r];
   }
   __syncthreads();
-  route_select<(NB * 32 + 15) / 16, KMAX, MODE, 4, 4>(red, RT_TOK * EP, EP, wscale ? s_scale : nullptr,
-                                                     bias ? s_bias : nullptr, t0, T, E, k, idx, gate, logits,
-                                                     counts, hist);
+  // 8 lanes per token: the block's 256 lanes hold its 32 tokens
+  route_select_q<8, NB * 32 / 8, KMAX, MODE, 4, RT_TOK, 4>(red, RT_TOK * EP, EP, wscale ? s_scale : nullptr,
+                                                           bias ? s_bias : nullptr, t0, T, E, k, idx, gate, logits,
+                                                           hist);
+  if (MODE != 0) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x)
+      if (hist[e]) atomicAdd(&counts[e], hist[e]);
+  }
 }
 
 // Persistent router for bf16 activations, E <= 64 and d a multiple of the slab
@@ -741,9 +885,11 @@ __global__ __launch_bounds__(256) void k_route_p(const bf16* __restrict__ X, con
       }
       __syncthreads();
     }
-    route_select<(NEG * 32 + 15) / 16, KMAX, MODE, 4, 1, TT, false>(
-        stage, 0, EP, wscale ? s_scale : nullptr, bias ? s_bias : nullptr, t0, T, E, k, idx, gate, logits,
-        counts, hist);
+    // lanes per token: every lane of the block has a token (TT = 32: 8, TT = 64: 4)
+    constexpr int LPT = 256 / TT;
+    route_select_q<LPT, NEG * 32 / LPT, KMAX, MODE, 4, TT>(stage, 0, EP, wscale ? s_scale : nullptr,
+                                                           bias ? s_bias : nullptr, t0, T, E, k, idx, gate,
+                                                           logits, hist);
     __syncthreads();   // the stage is free again
     tile = next;
   }
