@@ -229,7 +229,7 @@ __device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int
 
 // Selection in small lane groups, for the logits of TT tokens in LDS (the sum,
 // in order, of NPART partials stage[p * PSTRIDE + token * EP + expert], times
-// scale and plus bias as in route_select): LPT = 4 or 8 lanes per token, lane q of the group
+// scale and plus bias as in route_select): LPT = 2, 4 or 8 lanes per token, lane q of the group
 // holding experts [q NQ, (q+1) NQ) as 64-bit keys (ordered fp32 value,
 // 0xFFFF - expert; -0.0 == +0.0), so that a selection round is a local maximum
 // over the lane's NQ keys (a tree of independent compares) and log2(LPT) lane
@@ -254,6 +254,7 @@ constexpr int QP_SWAP2 = 0x4E;   // quad_perm [2, 3, 0, 1]
 template <int LPT> __device__ __forceinline__ uint64_t group_max64(uint64_t b) {
   uint64_t o = quad_perm64<QP_SWAP1>(b);
   b = o > b ? o : b;
+  if (LPT == 2) return b;
   o = quad_perm64<QP_SWAP2>(b);
   b = o > b ? o : b;
   if (LPT == 8) {
@@ -266,6 +267,7 @@ template <int LPT> __device__ __forceinline__ uint64_t group_max64(uint64_t b) {
 }
 template <int LPT> __device__ __forceinline__ float group_sum(float x) {
   x += quad_perm_f<QP_SWAP1>(x);
+  if (LPT == 2) return x;
   x += quad_perm_f<QP_SWAP2>(x);
   if (LPT == 8) x += __shfl_xor(x, 4);
   return x;
@@ -277,7 +279,7 @@ __device__ __forceinline__ void route_select_q(const float* stage, int PSTRIDE, 
                                                int t0, int T, int E, int k, int32_t* __restrict__ idx,
                                                float* __restrict__ gate, float* __restrict__ logits,
                                                int* hist) {
-  static_assert(LPT == 4 || LPT == 8, "4 or 8 lanes per token");
+  static_assert(LPT == 2 || LPT == 4 || LPT == 8, "2, 4 or 8 lanes per token");
   constexpr int GPW = 64 / LPT;                                 // lane groups per wave
   constexpr int TPL = (TT + WAVES * GPW - 1) / (WAVES * GPW);   // tokens per lane group
   constexpr int RPL = (KMAX + LPT - 1) / LPT;                   // ranks held per lane
@@ -885,7 +887,7 @@ __global__ __launch_bounds__(256) void k_route_p(const bf16* __restrict__ X, con
       }
       __syncthreads();
     }
-    // lanes per token: every lane of the block has a token (TT = 32: 8, TT = 64: 4)
+    // lanes per token: every lane of the block has a token (TT = 32: 8, 64: 4, 128: 2)
     constexpr int LPT = 256 / TT;
     route_select_q<LPT, NEG * 32 / LPT, KMAX, MODE, 4, TT>(stage, 0, EP, wscale ? s_scale : nullptr,
                                                            bias ? s_bias : nullptr, t0, T, E, k, idx, gate,
@@ -955,11 +957,13 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
   if constexpr (std::is_same<TX, bf16>::value) {
     const int ncu = route_cu_count();
     const bool wide = T >= 64 * ncu;
+    const bool wider = T >= 128 * ncu;
     // the int8 profiling router keeps the 32-token kernel below when tiles are
     // 32 tokens (measured faster there: 20.3 against 22.7 us at T = 8192, d = 2048)
     if (E <= 64 && d % (wide ? 128 : 256) == 0 && (MODE == 0 || wide)) {
-      // 64-token tiles once every compute unit gets one, else 32; one block per CU
-      const int tiles = wide ? cdiv(T, 64) : cdiv(T, 32);
+      // 128-token tiles once every compute unit gets one (the router is read
+      // once per CU), else 64-token ones, else 32; one block per CU
+      const int tiles = wider ? cdiv(T, 128) : wide ? cdiv(T, 64) : cdiv(T, 32);
       const dim3 pg(tiles < ncu ? tiles : ncu);
 #define FM_RP(TT, NEG, KM)                                                                                \
   hipLaunchKernelGGL((k_route_p<TW, TT, NEG, KM, MODE>), pg, dim3(256), 0, st, X, W, ws, bias, T, d, E, k, \
@@ -969,7 +973,9 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
   else if (k <= 4) FM_RP(TT, NEG, 4); \
   else if (k <= 8) FM_RP(TT, NEG, 8); \
   else FM_RP(TT, NEG, 16);
-      if (wide) {
+      if (wider) {
+        if (E <= 32) { FM_RP_K(128, 1) } else { FM_RP_K(128, 2) }
+      } else if (wide) {
         if (E <= 32) { FM_RP_K(64, 1) } else { FM_RP_K(64, 2) }
       } else {
         if (E <= 32) { FM_RP_K(32, 1) } else { FM_RP_K(32, 2) }

@@ -144,6 +144,59 @@ def test_edge_route_backward(run):
     assert e_alone <= TOL_FFN and e_acc <= TOL_FFN
 
 
+# Token counts that reach each tile size of the persistent router on a
+# 256-CU MI355X: 32-token tiles below 64 tokens per CU, 64-token tiles from
+# there, 128-token tiles from 128 per CU (ragged last tiles), each with a
+# router of one or two 32-expert groups and k from 1 to 16.
+PERSISTENT_ROUTER = {
+    "tile32_E20_k16": (1000, 256, 20, 16),
+    "tile64_E64_k1": (20000, 384, 64, 1),
+    "tile128_E20_k5": (33000, 256, 20, 5),
+    "tile128_E64_k16": (32845, 128, 64, 16),
+}
+
+
+@pytest.mark.parametrize("name", list(PERSISTENT_ROUTER))
+def test_router_tile_sizes(name):
+    """Routing (idx, gate, logits), the int8 histogram with its top-k sets, and
+    the profiling route (histogram, idx and gate) against the oracle at every
+    tile size of the persistent router."""
+    T, d, E, k = PERSISTENT_ROUTER[name]
+    w = W.LayerWorkload(name=name, cid=211, T=T, d=d, E=E, k=k, I=64, dtype="bf16", bias_kind="normal",
+                        bias_var=1.0)
+    inp = LayerInputs(w, with_experts=False)
+    ref = OracleLayer(w, inp, with_ffn_weights=False)
+    log(f"persistent router {name}: T={T} d={d} E={E} k={k}")
+    X, Wr = W.to_torch(inp.X, "cuda"), W.to_torch(inp.Wr, "cuda")
+    bias = torch.from_numpy(inp.bias).cuda()
+    i32 = lambda *s: torch.full(s, -1, dtype=torch.int32, device="cuda")
+    f32 = lambda *s: torch.full(s, float("nan"), dtype=torch.float32, device="cuda")
+    idx, gate, logits = i32(T, k), f32(T, k), f32(T, E)
+    api.moe_route_topk(X, Wr, bias, k, idx, gate, logits)
+    Wq = torch.empty(E, d, dtype=torch.int8, device="cuda")
+    sc = torch.empty(E, dtype=torch.float32, device="cuda")
+    api.moe_quantize_int8(Wr, Wq, sc)
+    counts, idx8 = torch.zeros(E, dtype=torch.int32, device="cuda"), i32(T, k)
+    api.moe_profile_hist(X, Wq, sc, bias, k, counts, idx8)
+    counts2, idx8b, gate8 = torch.zeros(E, dtype=torch.int32, device="cuda"), i32(T, k), f32(T, k)
+    api.moe_profile_route(X, Wq, sc, bias, k, counts2, idx8b, gate8)
+    torch.cuda.synchronize()
+    excl, bad = compare_topk(host(idx), host(logits), ref.idx, ref.logits, k)
+    log(f"  route: {excl} of {T} tokens in the tie window, {bad} mismatched")
+    assert bad == 0 and excl <= max(2, T // 1000)
+    np.testing.assert_allclose(host(logits), ref.logits, rtol=0, atol=2e-5 * max(1.0, np.abs(ref.logits).max()))
+    keep = O.topk_gap(ref.logits, k) >= GAP
+    np.testing.assert_allclose(host(gate)[keep], ref.gate[keep], rtol=1e-5, atol=1e-7)
+    excl8 = compare_hist(host(counts), host(idx8), ref, k, E)
+    log(f"  histogram: {excl8} tokens in the tie window, the rest bit-exact")
+    # the profiling route: same histogram and sets, gates of the int8 logits
+    np.testing.assert_array_equal(host(counts2), host(counts))
+    np.testing.assert_array_equal(host(idx8b), host(idx8))
+    keep8 = O.topk_gap(ref.logits8, k) >= GAP
+    g8 = O.softmax_rows(np.take_along_axis(ref.logits8, np.asarray(ref.idx8), axis=1))
+    np.testing.assert_allclose(host(gate8)[keep8], g8[keep8], rtol=1e-5, atol=1e-7)
+
+
 def test_router_limits():
     """E = 256 experts, k = 16: the largest router the ABI accepts."""
     w = W.LayerWorkload(name="router_max", cid=207, T=777, d=256, E=256, k=16, I=64, dtype="bf16",
