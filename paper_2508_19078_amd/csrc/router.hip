@@ -229,17 +229,18 @@ __device__ __forceinline__ void route_select(const float* part, int PSTRIDE, int
 
 // Selection in small lane groups, for the logits of TT tokens in LDS (the sum,
 // in order, of NPART partials stage[p * PSTRIDE + token * EP + expert], times
-// scale and plus bias as in route_select): LPT = 2, 4 or 8 lanes per token, lane q of the group
-// holding experts [q NQ, (q+1) NQ) as 64-bit keys (ordered fp32 value,
-// 0xFFFF - expert; -0.0 == +0.0), so that a selection round is a local maximum
-// over the lane's NQ keys (a tree of independent compares) and log2(LPT) lane
-// exchanges (DPP quad permutations, then a swizzle across quads), and the k
-// rounds of a token run in one lane group with no loop over tokens (16 lanes
-// per token and one token after another left each round a chain of dependent
-// row rotations that one wave per SIMD could not hide).  Rank j of a token
-// lands in lane j % LPT of its group.  Same outputs and order as
-// route_select; the softmax denominator adds each lane's ranks in order, then
-// the group's lanes by the same exchanges.
+// scale and plus bias as in route_select).  LPT = 2, 4 or 8 lanes per token;
+// lane q of a group holds experts [q NQ, (q+1) NQ) as 64-bit keys (ordered
+// fp32 value, 0xFFFF - expert; -0.0 == +0.0), so that a selection round is a
+// local maximum over the lane's NQ keys (a tree of independent compares) and
+// log2(LPT) lane exchanges (DPP quad permutations, then a swizzle across
+// quads), and the k rounds of a token run in one lane group with no loop over
+// tokens (16 lanes per token and one token after another left each round a
+// chain of dependent row rotations that one wave per SIMD could not hide).
+// Rank j of a token lands in lane j % LPT of its group.  The selected experts
+// and their order are those of route_select; the softmax denominator adds
+// each lane's ranks in order, then the group's lanes by the same exchanges
+// (so a gate may differ from route_select's in its last bit).
 template <int CTRL> __device__ __forceinline__ uint64_t quad_perm64(uint64_t x) {
   const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, CTRL, 0xF, 0xF, false);
   const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), CTRL, 0xF, 0xF, false);
