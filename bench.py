@@ -114,23 +114,24 @@ def cold_hbm(r, w, st, N, reps=5):
         "profile_hist": (lambda: api.moe_profile_hist(r.X, r.Wq, r.wscale, r.bias, w.k, r.counts),
                          w.T * w.d * b + w.E * w.d + 12 * w.E),
         "permute": (lambda: api.moe_permute(r.X, r.idx, r.gate, r.expert_map, r.S_r, r.offsets, r.perm_token,
-                                            r.perm_gate, r.inv, r.X_perm, r.ws_perm, E=w.E),
-                    w.T * w.d * b + N * w.d * b + w.T * w.k * 8 + N * 12 + 4 * (r.S_r + 1)),
+                                            r.perm_gate, r.inv, r.X_perm, r.ws_perm, E=w.E, x_sq=r.x_sq),
+                    w.T * w.d * b + N * w.d * b + w.T * w.k * 8 + N * 12 + 4 * (r.S_r + 1) + 4 * w.T),
         "combine": (lambda: api.moe_unpermute(r.layer_tables, r.O, r.inv, r.perm_gate, w.T, w.k, r.Y),
                     Ntot * w.d * b + w.T * w.d * b + w.T * w.k * 8),
         "combine_bwd": (lambda: api.moe_unpermute_bwd(r.layer_tables, r.dY, r.O, r.inv, r.offsets, r.perm_gate,
-                                                      w.T, w.k, r.dO, None),
-                        Ntot * w.d * b + w.T * w.d * b),
+                                                      w.T, w.k, r.dO, None, dy_sq=r.dy_sq),
+                        Ntot * w.d * b + w.T * w.d * b + 4 * w.T),
         "permute_bwd": (lambda: api.moe_permute_bwd(r.layer_tables, r.dX_perm, r.inv, w.T, w.k, r.dX),
                         Ntot * w.d * b + w.T * w.d * b + w.T * w.k * 4),
         # router backward (selection fixed), added to the layer's dX
         "route_bwd": (lambda: api.moe_route_bwd(r.gate, r.idx, r.dgate, r.Wr, r.dX, accumulate=True),
                       w.T * w.k * 12 + 2 * w.T * w.d * b + w.E * w.d * b),
-        # expert utility (Eq. 3): the tokens' X and dY rows, the rows' maps and the
-        # per-row norm partials the backward left (8 bytes per row and dH column tile)
-        "expert_utility": (lambda: api.moe_expert_utility(r.layer_tables, r.X, r.dY, r.perm_token, r.perm_gate,
-                                                          r.offsets, w.T, w.k, r.ws_bwd, util),
-                           2 * w.T * w.d * b + N * 8 + Ntot * 8 * -(-w.I // 256)),
+        # expert utility (Eq. 3): the tokens' squared norms (from the permutation and
+        # the combine backward), the rows' maps and the per-row norm partials the
+        # backward left (8 bytes per row and dH column tile)
+        "expert_utility": (lambda: api.moe_expert_utility(r.layer_tables, r.x_sq, r.dy_sq, r.perm_token,
+                                                          r.perm_gate, r.offsets, w.T, w.k, r.ws_bwd, util),
+                           2 * w.T * 4 + N * 8 + Ntot * 8 * -(-w.I // 256)),
     }
     util = torch.empty(r.S_r + w.n_shared, dtype=torch.float32, device="cuda")
     if r.G:
@@ -448,14 +449,15 @@ def main():
         mark(2); r.route()
         mark(3)
         api.moe_permute(r.X, r.idx, r.gate, r.expert_map, r.S_r, r.offsets, r.perm_token, r.perm_gate, r.inv,
-                        r.X_perm, r.ws_perm, E=w.E)
+                        r.X_perm, r.ws_perm, E=w.E, x_sq=r.x_sq)
         mark(4)
         api.moe_grouped_swiglu_fwd(r.layer_tables, r.X, r.X_perm, r.offsets, w.T, w.k, r.A_g, r.A_u, r.H, r.O,
                                    r.ws_fwd)
         mark(5)
         api.moe_unpermute(r.layer_tables, r.O, r.inv, r.perm_gate, w.T, w.k, r.Y)
         mark(6)
-        api.moe_unpermute_bwd(r.layer_tables, r.dY, r.O, r.inv, r.offsets, r.perm_gate, w.T, w.k, r.dO, None)
+        api.moe_unpermute_bwd(r.layer_tables, r.dY, r.O, r.inv, r.offsets, r.perm_gate, w.T, w.k, r.dO, None,
+                              dy_sq=r.dy_sq)
         mark(7)
         api.moe_grouped_swiglu_bwd(r.layer_tables, r.X, r.X_perm, r.offsets, w.T, w.k, r.A_g, r.A_u, r.H, r.dO,
                                    r.dX_perm, 0, r.ws_bwd)
@@ -500,7 +502,7 @@ def main():
     N = int(offsets[-1])
     b = w.x_bytes
     route_bytes = w.T * w.d * b + w.E * w.d * b + w.T * w.k * 8
-    permute_bytes = w.T * w.d * b + N * w.d * b + w.T * w.k * 8 + N * 12 + 4 * (r.S_r + 1)
+    permute_bytes = w.T * w.d * b + N * w.d * b + w.T * w.k * 8 + N * 12 + 4 * (r.S_r + 1) + 4 * w.T
     merge_bytes = (w.E - r.K + r.G) * 3 * w.d * w.I * b if r.G else 0
     hist_bytes = w.T * w.d * b + w.E * w.d + 12 * w.E
     gbs = lambda by, ms: round(by / (ms * 1e-3) / 1e9, 1) if ms > 0 else None

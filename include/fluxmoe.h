@@ -60,7 +60,7 @@ enum { MOE_F32 = 0, MOE_BF16 = 1, MOE_I8 = 2 };
 const char* moe_last_error(void);
 /* ABI revision of this header. */
 int moe_abi_version(void);
-#define FLUXMOE_ABI_VERSION 2
+#define FLUXMOE_ABI_VERSION 3
 
 /* ---------------------------------------------------------------- routing --
  * moe_route_topk: the gating network of an MoE layer (Section 2.1, "MoE":
@@ -318,14 +318,17 @@ typedef struct moe_layer {
  * Outputs: offsets[S_routed+1]; perm_token[T*k] (row -> token); perm_gate[T*k]
  * fp32; inv[T,k]: p for the choice that opened row p, -2-p for a choice folded
  * into row p; X_perm[T*k, d] with X_perm[p] = X[perm_token[p]].  Entries at or
- * beyond offsets[S_routed] are left untouched.  idx values must be in [0, E)
- * and expert_map values in [0, S_routed) (not checked on the device; see
- * moe_validate_routing and FLUXMOE_DEBUG_CHECKS).
+ * beyond offsets[S_routed] are left untouched.  x_sq [T] fp32 (optional, NULL
+ * = not written): ||X[t]||^2, the squares of X's elements summed in fp32 in a
+ * fixed order, the per-token input norms the expert utility (Eq. 3,
+ * moe_expert_utility) needs, formed while the rows are read anyway.  idx
+ * values must be in [0, E) and expert_map values in [0, S_routed) (not checked
+ * on the device; see moe_validate_routing and FLUXMOE_DEBUG_CHECKS).
  */
 int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
                 const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
                 int32_t* offsets, int32_t* perm_token, float* perm_gate,
-                int32_t* inv, void* X_perm, void* ws, size_t ws_bytes, void* stream);
+                int32_t* inv, void* X_perm, void* ws, size_t ws_bytes, float* x_sq, void* stream);
 size_t moe_permute_workspace_size(int T, int k, int S_routed);
 
 /* moe_permute_noalloc: moe_permute for callers that cannot allocate device
@@ -345,7 +348,7 @@ size_t moe_permute_workspace_size(int T, int k, int S_routed);
 int moe_permute_noalloc(const void* X, int dtype, const int32_t* idx, const float* gate,
                         const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
                         int32_t* offsets, int32_t* perm_token, float* perm_gate,
-                        int32_t* inv, void* X_perm, void* stream);
+                        int32_t* inv, void* X_perm, float* x_sq, void* stream);
 size_t moe_permute_noalloc_max_bytes(void);
 
 /* moe_validate_routing: range check of moe_permute's index inputs, for
@@ -426,11 +429,14 @@ int moe_unpermute(const moe_layer* L, const void* O, const int32_t* inv,
  *   dO[T*k + i*T + t] = dY[t]                  for shared slot i
  *   dgate[t,j] = <dY[t], O[row of (t,j)]>      (optional, fp32, when dgate != NULL;
  *                folded choices read the row they were folded into)
+ *   dy_sq[t] = ||dY[t]||^2                     (optional, fp32 [T], when dy_sq != NULL:
+ *                the squares summed in fp32 in a fixed order; the per-token
+ *                output-gradient norms of moe_expert_utility, Eq. 3)
  */
 int moe_unpermute_bwd(const moe_layer* L, const void* dY, const void* O,
                       const int32_t* inv, const int32_t* offsets,
                       const float* perm_gate, int T, int k,
-                      void* dO, float* dgate, void* stream);
+                      void* dO, float* dgate, float* dy_sq, void* stream);
 
 /* moe_grouped_swiglu_bwd: backward of every slot's SwiGLU FFN.  Only tuning
  * experts are updated during local fine-tuning; non-tuning experts are merged
@@ -465,16 +471,18 @@ size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k);
  * with x_r = X[t] and dO_r = gate_r dY[t] for the row's token t (gate 1 on a
  * shared slot).  The sums of squares of dA_g, dA_u and h = silu(a_g) a_u over
  * each row are left in the workspace by moe_grouped_swiglu_bwd (its dH step,
- * h recomputed from the saved A_g, A_u); this call adds ||X[t]||^2 and
- * ||dY[t]||^2 per token and reduces per slot (per-row and per-token sums in
- * fp32, per-slot sums in fp64, fixed order); an empty slot gets 0.  Every slot
- * gets a utility, frozen ones included.  Call it after moe_grouped_swiglu_bwd
- * on the same stream with that call's workspace and the same layer, offsets,
- * T and k; nothing else may use the workspace in between.
- * X, dY [T,d] in L->dtype; perm_token, perm_gate: moe_permute's maps (may be
- * NULL when S_routed == 0); utility [S] fp32.
+ * h recomputed from the saved A_g, A_u); the per-token ||X[t]||^2 and
+ * ||dY[t]||^2 come from moe_permute (x_sq) and moe_unpermute_bwd (dy_sq),
+ * which form them as they read X and dY; this call combines them per row and
+ * reduces per slot (per-row and per-token sums in fp32, per-slot sums in fp64,
+ * fixed order); an empty slot gets 0.  Every slot gets a utility, frozen ones
+ * included.  Call it after moe_grouped_swiglu_bwd on the same stream with that
+ * call's workspace and the same layer, offsets, T and k; nothing else may use
+ * the workspace in between.
+ * x_sq, dy_sq [T] fp32; perm_token, perm_gate: moe_permute's maps (may be NULL
+ * when S_routed == 0); utility [S] fp32.
  */
-int moe_expert_utility(const moe_layer* L, const void* X, const void* dY,
+int moe_expert_utility(const moe_layer* L, const float* x_sq, const float* dy_sq,
                        const int32_t* perm_token, const float* perm_gate,
                        const int32_t* offsets, int T, int k, void* ws, size_t ws_bytes,
                        float* utility, void* stream);

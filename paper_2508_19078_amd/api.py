@@ -55,11 +55,11 @@ _SIGS = {
     "moe_slot_pointers": (_c_int, [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
                                    _vp, _vp, _vp, _vp, _vp]),
     "moe_permute": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp,
-                             _vp, _vp, _vp, _vp, _c_size, _vp]),
+                             _vp, _vp, _vp, _vp, _c_size, _vp, _vp]),
     "moe_permute_workspace_size": (_c_size, [_c_int, _c_int, _c_int]),
     "moe_validate_routing": (_c_int, [_vp, _vp, _c_int, _c_int, _c_int, _c_int]),
     "moe_permute_noalloc": (_c_int, [_vp, _c_int, _vp, _vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp,
-                                     _vp, _vp, _vp, _vp, _vp]),
+                                     _vp, _vp, _vp, _vp, _vp, _vp]),
     "moe_permute_noalloc_max_bytes": (_c_size, []),
     "moe_grouped_swiglu_fwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
                                         _c_size, _vp]),
@@ -67,7 +67,7 @@ _SIGS = {
     "moe_grouped_swiglu_fwd_q8": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _c_size, _vp]),
     "moe_grouped_swiglu_fwd_q8_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
     "moe_unpermute": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp]),
-    "moe_unpermute_bwd": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp]),
+    "moe_unpermute_bwd": (_c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp]),
     "moe_grouped_swiglu_bwd": (_c_int, [_vp, _vp, _vp, _vp, _c_int, _c_int, _vp, _vp, _vp, _vp, _vp,
                                         _c_int, _vp, _c_size, _vp]),
     "moe_grouped_swiglu_bwd_workspace_size": (_c_size, [_vp, _c_int, _c_int]),
@@ -85,7 +85,7 @@ _SIGS = {
 }
 
 _lib = None
-ABI_VERSION = 2   # FLUXMOE_ABI_VERSION of the header these signatures follow
+ABI_VERSION = 3   # FLUXMOE_ABI_VERSION of the header these signatures follow
 
 
 def lib() -> ctypes.CDLL:
@@ -307,25 +307,26 @@ def moe_permute_workspace_size(T, k, S_routed) -> int:
 
 
 def moe_permute(X, idx, gate, expert_map, S_routed, offsets, perm_token, perm_gate, inv, X_perm, ws,
-                E=None, stream=None):
+                E=None, x_sq=None, stream=None):
+    """x_sq [T] fp32, if given, receives ||X[t]||^2 (for moe_expert_utility)."""
     T, d = X.shape
     k = idx.shape[1]
     E = E if E is not None else (expert_map.shape[0] if expert_map is not None else S_routed)
     return _call("moe_permute", ptr(X, FLOAT), dtype_code(X.dtype), ptr(idx, I32), ptr(gate, F32),
                  ptr(expert_map, I32), T, d, E, k, S_routed, ptr(offsets, I32), ptr(perm_token, I32),
                  ptr(perm_gate, F32), ptr(inv, I32), ptr(X_perm, X.dtype), ptr(ws),
-                 ws.numel() * ws.element_size() if ws is not None else 0, stream_ptr(stream))
+                 ws.numel() * ws.element_size() if ws is not None else 0, ptr(x_sq, F32), stream_ptr(stream))
 
 
 def moe_permute_noalloc(X, idx, gate, expert_map, S_routed, offsets, perm_token, perm_gate, inv, X_perm, E=None,
-                        stream=None):
+                        x_sq=None, stream=None):
     """moe_permute without a workspace (the library's own device scratch)."""
     T, d = X.shape
     k = idx.shape[1]
     E = E if E is not None else (expert_map.shape[0] if expert_map is not None else S_routed)
     return _call("moe_permute_noalloc", ptr(X, FLOAT), dtype_code(X.dtype), ptr(idx, I32), ptr(gate, F32),
                  ptr(expert_map, I32), T, d, E, k, S_routed, ptr(offsets, I32), ptr(perm_token, I32),
-                 ptr(perm_gate, F32), ptr(inv, I32), ptr(X_perm, X.dtype), stream_ptr(stream))
+                 ptr(perm_gate, F32), ptr(inv, I32), ptr(X_perm, X.dtype), ptr(x_sq, F32), stream_ptr(stream))
 
 
 def moe_permute_noalloc_max_bytes() -> int:
@@ -375,9 +376,10 @@ def moe_unpermute(layer, O, inv, perm_gate, T, k, Y, stream=None):
                  ptr(Y, FLOAT), stream_ptr(stream))
 
 
-def moe_unpermute_bwd(layer, dY, O, inv, offsets, perm_gate, T, k, dO, dgate=None, stream=None):
+def moe_unpermute_bwd(layer, dY, O, inv, offsets, perm_gate, T, k, dO, dgate=None, dy_sq=None, stream=None):
+    """dy_sq [T] fp32, if given, receives ||dY[t]||^2 (for moe_expert_utility)."""
     return _call("moe_unpermute_bwd", ptr(layer), ptr(dY, FLOAT), ptr(O, FLOAT), ptr(inv, I32), ptr(offsets, I32),
-                 ptr(perm_gate, F32), T, k, ptr(dO, FLOAT), ptr(dgate, F32), stream_ptr(stream))
+                 ptr(perm_gate, F32), T, k, ptr(dO, FLOAT), ptr(dgate, F32), ptr(dy_sq, F32), stream_ptr(stream))
 
 
 def moe_grouped_swiglu_bwd(layer, X, X_perm, offsets, T, k, A_g, A_u, H, dO, dX_perm, accumulate_dw, ws,
@@ -392,9 +394,10 @@ def moe_permute_bwd(layer, dX_perm, inv, T, k, dX, stream=None):
                  stream_ptr(stream))
 
 
-def moe_expert_utility(layer, X, dY, perm_token, perm_gate, offsets, T, k, ws, utility, stream=None):
-    """After moe_grouped_swiglu_bwd with the same workspace `ws`."""
-    return _call("moe_expert_utility", ptr(layer), ptr(X, FLOAT), ptr(dY, FLOAT), ptr(perm_token, I32),
+def moe_expert_utility(layer, x_sq, dy_sq, perm_token, perm_gate, offsets, T, k, ws, utility, stream=None):
+    """After moe_grouped_swiglu_bwd with the same workspace `ws`; x_sq and dy_sq
+    as written by moe_permute and moe_unpermute_bwd."""
+    return _call("moe_expert_utility", ptr(layer), ptr(x_sq, F32), ptr(dy_sq, F32), ptr(perm_token, I32),
                  ptr(perm_gate, F32), ptr(offsets, I32), T, k, ptr(ws), ws.numel() * ws.element_size(),
                  ptr(utility, F32), stream_ptr(stream))
 

@@ -1049,40 +1049,12 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
 // slot is one row with the summed gate), so |D_s| is the slot's row count.
 // The backward's dH epilogue leaves per row the partial sums of dA_g^2 + dA_u^2
 // and h^2 over its column tiles; a row's x is its token's input and its dO the
-// token's output gradient times the row's gate, so the rest needs only one
-// pass over the tokens: ||x_t||^2 and ||dY_t||^2.
+// token's output gradient times the row's gate, so the rest needs only the
+// tokens' ||x_t||^2 and ||dY_t||^2, which the permutation and the combine
+// backward write as they read X and dY.
 
 constexpr int UT_THREADS = 256;   // threads of the per-row pass: one row each (tiles of up to 256 rows)
 static_assert(B16_ROWS <= UT_THREADS && G_BM <= UT_THREADS, "a row tile per block of the utility pass");
-
-// ||X_t||^2 and ||dY_t||^2, one wave per token (fp32 lane sums, fixed butterfly).
-template <typename T>
-__global__ __launch_bounds__(256) void k_token_norms(const T* __restrict__ X, const T* __restrict__ dY, int Tn,
-                                                     int d, float2* __restrict__ tn) {
-  constexpr int V = 16 / sizeof(T);
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= Tn) return;
-  float sx = 0.f, sy = 0.f;
-  const T* xr = X + (size_t)t * d;
-  const T* yr = dY + (size_t)t * d;
-#pragma unroll 4
-  for (int c = lane_id() * V; c < d; c += 64 * V) {
-    float a[V], b[V];
-    unpack16(ld16(xr + c), a, (T*)nullptr);
-    unpack16(ld16(yr + c), b, (T*)nullptr);
-#pragma unroll
-    for (int i = 0; i < V; ++i) {
-      sx = fmaf(a[i], a[i], sx);
-      sy = fmaf(b[i], b[i], sy);
-    }
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    sx += __shfl_xor(sx, off);
-    sy += __shfl_xor(sy, off);
-  }
-  if (lane_id() == 0) tn[t] = make_float2(sx, sy);
-}
 
 // One block per row tile of a slot, the backward's own row tiles (its
 // schedule, tile_rows <= UT_THREADS rows, is still in the workspace): a thread
@@ -1091,7 +1063,8 @@ __global__ __launch_bounds__(256) void k_token_norms(const T* __restrict__ X, co
 __global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, int tile_rows,
                                                              const int32_t* __restrict__ perm_token,
                                                              const float* __restrict__ perm_gate,
-                                                             const float2* __restrict__ tn,
+                                                             const float* __restrict__ x_sq,
+                                                             const float* __restrict__ dy_sq,
                                                              const float2* __restrict__ norms, int P,
                                                              double* __restrict__ part) {
   __shared__ double red[UT_THREADS];
@@ -1113,14 +1086,14 @@ __global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, int til
       tok = perm_token[row];
       g = perm_gate[row];
     }
-    const float2 xy = tn[tok];
+    const float xx = x_sq[tok], yy = dy_sq[tok];
     float sa = 0.f, sh = 0.f;
     for (int p = 0; p < P; ++p) {
       const float2 q = norms[row * P + p];
       sa += q.x;
       sh += q.y;
     }
-    v = (double)g * g * xy.y * sh + (double)sa * xy.x;
+    v = (double)g * g * yy * sh + (double)sa * xx;
   }
   red[i] = v;
   __syncthreads();
@@ -1201,12 +1174,11 @@ static int norm_parts(const moe_layer* L) {
 }
 
 // Backward workspace: schedule | dA_g | dA_u | per-row norm partials (float2) |
-// per-token norms (float2) | utility tile sums (double).
+// utility tile sums (double).
 struct BwdWs {
   char* dAg;
   char* dAu;
   float2* norms;
-  float2* tnorm;
   double* part;
 };
 static size_t bwd_act_bytes(const moe_layer* L, int T, int k) {
@@ -1221,8 +1193,6 @@ static BwdWs bwd_ws_at(void* ws, const moe_layer* L, int T, int k) {
   p += 2 * act;
   w.norms = (float2*)p;
   p += round256(sizeof(float2) * rows_total(L, T, k) * norm_parts(L));
-  w.tnorm = (float2*)p;
-  p += round256(sizeof(float2) * (size_t)T);
   w.part = (double*)p;
   return w;
 }
@@ -1230,7 +1200,7 @@ static BwdWs bwd_ws_at(void* ws, const moe_layer* L, int T, int k) {
 extern "C" size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int T, int k) {
   if (!L || T < 0 || k <= 0) return 0;
   return sched_bytes(n_slots(L)) + 2 * bwd_act_bytes(L, T, k) +
-         round256(sizeof(float2) * rows_total(L, T, k) * norm_parts(L)) + round256(sizeof(float2) * (size_t)T) +
+         round256(sizeof(float2) * rows_total(L, T, k) * norm_parts(L)) +
          round256(sizeof(double) * utility_tiles(L, T, k));
 }
 
@@ -1388,9 +1358,9 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
   return check_launch("moe_grouped_swiglu_bwd");
 }
 
-extern "C" int moe_expert_utility(const moe_layer* L, const void* X, const void* dY, const int32_t* perm_token,
-                                  const float* perm_gate, const int32_t* offsets, int T, int k, void* ws,
-                                  size_t ws_bytes, float* utility, void* stream) {
+extern "C" int moe_expert_utility(const moe_layer* L, const float* x_sq, const float* dy_sq,
+                                  const int32_t* perm_token, const float* perm_gate, const int32_t* offsets, int T,
+                                  int k, void* ws, size_t ws_bytes, float* utility, void* stream) {
   clear_error();
   FM_TRY(check_layer_ffn(L));
   if (T < 0 || k <= 0 || k > 16) return fail(MOE_ERR_ARG, "T=%d k=%d", T, k);
@@ -1401,27 +1371,22 @@ extern "C" int moe_expert_utility(const moe_layer* L, const void* X, const void*
     hipLaunchKernelGGL(k_zero_f32, dim3(cdiv(S, 256)), dim3(256), 0, st, utility, S);
     return check_launch("moe_expert_utility");
   }
-  FM_TRY(need(X, "X")); FM_TRY(need(dY, "dY")); FM_TRY(need(offsets, "offsets")); FM_TRY(need(ws, "ws"));
+  FM_TRY(need(x_sq, "x_sq")); FM_TRY(need(dy_sq, "dy_sq")); FM_TRY(need(offsets, "offsets"));
+  FM_TRY(need(ws, "ws"));
   if (L->S_routed > 0) {
     FM_TRY(need(perm_token, "perm_token")); FM_TRY(need(perm_gate, "perm_gate"));
   }
-  FM_TRY(need_aligned(X, "X")); FM_TRY(need_aligned(dY, "dY")); FM_TRY(need_aligned(ws, "ws"));
+  FM_TRY(need_aligned(x_sq, "x_sq")); FM_TRY(need_aligned(dy_sq, "dy_sq")); FM_TRY(need_aligned(ws, "ws"));
   if (ws_bytes < moe_grouped_swiglu_bwd_workspace_size(L, T, k))
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_bwd_workspace_size(L, T, k));
   // the backward's row-tile schedule (same offsets) is still in the workspace
   const Sched sc = sched_at(ws, S);
   const BwdWs bw = bwd_ws_at(ws, L, T, k);
-  const dim3 tg(cdiv(T, 4));
-  if (L->dtype == MOE_BF16)
-    hipLaunchKernelGGL(k_token_norms<bf16>, tg, dim3(256), 0, st, (const bf16*)X, (const bf16*)dY, T, L->d, bw.tnorm);
-  else
-    hipLaunchKernelGGL(k_token_norms<float>, tg, dim3(256), 0, st, (const float*)X, (const float*)dY, T, L->d,
-                       bw.tnorm);
   const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
   hipLaunchKernelGGL(k_utility_rows, dim3((unsigned)utility_tiles(L, T, k)), dim3(UT_THREADS), 0, st, ra,
-                     bwd_tile_rows(L), perm_token, perm_gate, (const float2*)bw.tnorm, (const float2*)bw.norms,
-                     norm_parts(L), bw.part);
+                     bwd_tile_rows(L), perm_token, perm_gate, x_sq, dy_sq, (const float2*)bw.norms, norm_parts(L),
+                     bw.part);
   hipLaunchKernelGGL(k_utility_slots, dim3(1), dim3(1024), 0, st, ra, (const double*)bw.part, utility);
   return check_launch("moe_expert_utility");
 }

@@ -132,12 +132,28 @@ __global__ __launch_bounds__(1024) void k_perm_scan(int32_t* __restrict__ bc, in
 //      bucket offsets), otherwise bc already holds those positions;
 //   3. the maps are written and each row is stored at every position its token
 //      opens.
+// s + the squares of the 16 bytes' elements (bf16, or fp32 when f32), in order.
+__device__ __forceinline__ float sq_acc(const u32x4_t& v, bool f32, float s) {
+  if (f32) {
+    float f[4];
+    unpack16(v, f, (float*)nullptr);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s = fmaf(f[i], f[i], s);
+  } else {
+    float f[8];
+    unpack16(v, f, (bf16*)nullptr);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s = fmaf(f[i], f[i], s);
+  }
+  return s;
+}
+
 template <int KMAX, bool SCAN, int PS_TOK>
 __global__ __launch_bounds__(PS_THREADS) void k_place_scatter(
     const int32_t* __restrict__ idx, const float* __restrict__ gate, const int32_t* __restrict__ emap,
     int T, int k, int S, const int32_t* __restrict__ bc, int nblk, int32_t* __restrict__ offsets,
     int32_t* __restrict__ perm_token, float* __restrict__ perm_gate, int32_t* __restrict__ inv,
-    const char* __restrict__ X, int row_bytes, char* __restrict__ Xp) {
+    const char* __restrict__ X, int row_bytes, char* __restrict__ Xp, bool xf32, float* __restrict__ x_sq) {
   constexpr int NTW = PS_TOK / (PS_THREADS / 64);   // tokens per wave
   constexpr int U = 4;                              // 16-byte chunks per lane and row per pass
   __shared__ unsigned long long msk[PM_SMAX];       // this block's tokens, one bit each, per slot
@@ -273,6 +289,7 @@ __global__ __launch_bounds__(PS_THREADS) void k_place_scatter(
   for (int x = 0; x < NTW; ++x) {
     const int tl = wave * NTW + x, t = t0 + tl;
     if (t >= T) break;
+    float ss = 0.f;                  // ||X[t]||^2: the lane's chunks in order, then the wave
     for (int j = 0; j < k; ++j) {
       const int p = posl[tl][j];
       if (p < 0) continue;
@@ -282,6 +299,11 @@ __global__ __launch_bounds__(PS_THREADS) void k_place_scatter(
         const int c = (lane + 64 * u) * 16;
         if (c < row_bytes) st16(dst + c, v[x][u]);
       }
+    }
+    if (x_sq) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if ((lane + 64 * u) * 16 < row_bytes) ss = sq_acc(v[x][u], xf32, ss);
     }
     // rows longer than one pass
     const char* src = X + (size_t)t * row_bytes;
@@ -302,6 +324,16 @@ __global__ __launch_bounds__(PS_THREADS) void k_place_scatter(
           if (c < row_bytes) st16(dst + c, w[u]);
         }
       }
+      if (x_sq) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (c0 + (lane + 64 * u) * 16 < row_bytes) ss = sq_acc(w[u], xf32, ss);
+      }
+    }
+    if (x_sq) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      if (lane == 0) x_sq[t] = ss;
     }
   }
 }
@@ -399,7 +431,7 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const T* __restrict__ dY, c
                                                      const int32_t* __restrict__ inv,
                                                      const float* __restrict__ pg, int Tn, int k,
                                                      int d, int S_sh, T* __restrict__ dO,
-                                                     float* __restrict__ dgate) {
+                                                     float* __restrict__ dgate, float* __restrict__ dy_sq) {
   constexpr int V = 16 / sizeof(T);
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= Tn) return;
@@ -412,6 +444,7 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const T* __restrict__ dY, c
     g[j] = p[j] >= 0 ? pg[p[j]] : 0.f;
     dot[j] = 0.f;
   }
+  float ss = 0.f;                    // ||dY[t]||^2: the lane's chunks in order, then the wave
   for (int c0 = lane_id() * V; c0 < d; c0 += CB_PF * 64 * V) {
     u32x4_t rawp[CB_PF];
 #pragma unroll
@@ -424,6 +457,10 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const T* __restrict__ dY, c
       const u32x4_t raw = rawp[u];
       float f[V];
       unpack16(raw, f, (T*)nullptr);
+      if (dy_sq) {
+#pragma unroll
+        for (int i = 0; i < V; ++i) ss = fmaf(f[i], f[i], ss);
+      }
 #pragma unroll
       for (int j = 0; j < KMAX; ++j) {
         if (j >= k) continue;
@@ -452,6 +489,11 @@ __global__ __launch_bounds__(256) void k_combine_bwd(const T* __restrict__ dY, c
       for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
       if (lane_id() == 0) dgate[(size_t)t * k + j] = v;
     }
+  }
+  if (dy_sq) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    if (lane_id() == 0) dy_sq[t] = ss;
   }
 }
 
@@ -595,8 +637,8 @@ int permute_check(const void* X, int dtype, const int32_t* idx, const float* gat
 // The launches of a validated permute; bc = the count table (workspace).
 int permute_launch(const void* X, int dtype, const int32_t* idx, const float* gate, const int32_t* expert_map,
                    int T, int d, int E, int k, int S_routed, int32_t* offsets, int32_t* perm_token,
-                   float* perm_gate, int32_t* inv, void* X_perm, int32_t* bc, hipStream_t st, const char* what,
-                   bool allow_debug) {
+                   float* perm_gate, int32_t* inv, void* X_perm, float* x_sq, int32_t* bc, hipStream_t st,
+                   const char* what, bool allow_debug) {
   if (T == 0) {
     hipLaunchKernelGGL(k_zero_i32, dim3(cdiv(S_routed + 1, 256)), dim3(256), 0, st, offsets,
                        S_routed + 1);
@@ -617,7 +659,7 @@ int permute_launch(const void* X, int dtype, const int32_t* idx, const float* ga
 #define FM_PS(KM, SC, TOK)                                                                                  \
   hipLaunchKernelGGL((k_place_scatter<KM, SC, TOK>), dim3(cdiv(T, TOK)), dim3(PS_THREADS), 0, st, idx, gate, \
                      expert_map, T, k, S_routed, bc, nblk, offsets, perm_token, perm_gate, inv,             \
-                     (const char*)X, row_bytes, (char*)X_perm)
+                     (const char*)X, row_bytes, (char*)X_perm, dtype == MOE_F32, x_sq)
 #define FM_PP(KM)                       \
   if (fuse && wide) FM_PS(KM, true, 32);  \
   else if (fuse) FM_PS(KM, true, 16);     \
@@ -635,7 +677,7 @@ int permute_launch(const void* X, int dtype, const int32_t* idx, const float* ga
 extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const float* gate,
                            const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
                            int32_t* offsets, int32_t* perm_token, float* perm_gate, int32_t* inv,
-                           void* X_perm, void* ws, size_t ws_bytes, void* stream) {
+                           void* X_perm, void* ws, size_t ws_bytes, float* x_sq, void* stream) {
   clear_error();
   FM_TRY(permute_check(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
                        X_perm));
@@ -644,8 +686,9 @@ extern "C" int moe_permute(const void* X, int dtype, const int32_t* idx, const f
   if (ws_bytes < moe_permute_workspace_size(T, k, S_routed))
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_permute_workspace_size(T, k, S_routed));
+  FM_TRY(need_aligned(x_sq, "x_sq"));
   return permute_launch(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
-                        X_perm, (int32_t*)ws, as_stream(stream), "moe_permute", true);
+                        X_perm, x_sq, (int32_t*)ws, as_stream(stream), "moe_permute", true);
 }
 
 // ------------------------------------------------- no-allocation variant ----
@@ -698,7 +741,7 @@ extern "C" size_t moe_permute_noalloc_max_bytes(void) { return PERM_SCRATCH_BYTE
 extern "C" int moe_permute_noalloc(const void* X, int dtype, const int32_t* idx, const float* gate,
                                    const int32_t* expert_map, int T, int d, int E, int k, int S_routed,
                                    int32_t* offsets, int32_t* perm_token, float* perm_gate, int32_t* inv,
-                                   void* X_perm, void* stream) {
+                                   void* X_perm, float* x_sq, void* stream) {
   clear_error();
   FM_TRY(permute_check(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
                        X_perm));
@@ -708,10 +751,11 @@ extern "C" int moe_permute_noalloc(const void* X, int dtype, const int32_t* idx,
                 "moe_permute_noalloc: T=%d tokens over S_routed=%d slots need a %zu-byte count table, above its "
                 "%zu-byte scratch; use moe_permute with a workspace",
                 T, S_routed, need, PERM_SCRATCH_BYTES);
+  FM_TRY(need_aligned(x_sq, "x_sq"));
   void* p = nullptr;
   FM_TRY(scratch_address(&p));
   return permute_launch(X, dtype, idx, gate, expert_map, T, d, E, k, S_routed, offsets, perm_token, perm_gate, inv,
-                        X_perm, (int32_t*)p, as_stream(stream), "moe_permute_noalloc", false);
+                        X_perm, x_sq, (int32_t*)p, as_stream(stream), "moe_permute_noalloc", false);
 }
 
 extern "C" int moe_unpermute(const moe_layer* L, const void* O, const int32_t* inv,
@@ -738,7 +782,7 @@ extern "C" int moe_unpermute(const moe_layer* L, const void* O, const int32_t* i
 
 extern "C" int moe_unpermute_bwd(const moe_layer* L, const void* dY, const void* O,
                                  const int32_t* inv, const int32_t* offsets, const float* perm_gate,
-                                 int T, int k, void* dO, float* dgate, void* stream) {
+                                 int T, int k, void* dO, float* dgate, float* dy_sq, void* stream) {
   clear_error();
   FM_TRY(check_layer(L));
   FM_TRY(check_tk(T, k));
@@ -748,16 +792,17 @@ extern "C" int moe_unpermute_bwd(const moe_layer* L, const void* dY, const void*
   if (dgate) FM_TRY(need(O, "O"));
   (void)offsets;  // rows are addressed through inv; every routed row has one owner token
   FM_TRY(need_aligned(dY, "dY")); FM_TRY(need_aligned(O, "O")); FM_TRY(need_aligned(dO, "dO"));
+  FM_TRY(need_aligned(dy_sq, "dy_sq"));
   hipStream_t st = as_stream(stream);
   dim3 grid(cdiv(T, 4)), block(256);
 #define FM_CBB(KM)                                                                                  \
   if (L->dtype == MOE_BF16)                                                                         \
     hipLaunchKernelGGL((k_combine_bwd<bf16, KM>), grid, block, 0, st, (const bf16*)dY,              \
-                       (const bf16*)O, inv, perm_gate, T, k, L->d, L->S_shared, (bf16*)dO, dgate); \
+                       (const bf16*)O, inv, perm_gate, T, k, L->d, L->S_shared, (bf16*)dO, dgate, dy_sq); \
   else                                                                                              \
     hipLaunchKernelGGL((k_combine_bwd<float, KM>), grid, block, 0, st, (const float*)dY,            \
                        (const float*)O, inv, perm_gate, T, k, L->d, L->S_shared, (float*)dO,       \
-                       dgate);
+                       dgate, dy_sq);
   FM_KSWITCH(k, FM_CBB)
 #undef FM_CBB
   return check_launch("moe_unpermute_bwd");

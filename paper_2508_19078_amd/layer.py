@@ -147,6 +147,10 @@ class MoELayerRunner:
         self.perm_gate = z(R, dtype=torch.float32)
         self.inv = zi(T, k)
         self.X_perm = z(R, d)
+        # per-token ||X||^2 and ||dY||^2 (written by the permutation and the
+        # combine backward; the expert utility reads them)
+        self.x_sq = z(T, dtype=torch.float32)
+        self.dy_sq = z(T, dtype=torch.float32)
         self.ws_perm = torch.empty(api.moe_permute_workspace_size(T, k, self.S_r), dtype=torch.uint8,
                                    device=device)
         # forward / backward activations
@@ -194,7 +198,7 @@ class MoELayerRunner:
         idx = self.idx if idx is None else idx
         gate = self.gate if gate is None else gate
         api.moe_permute(self.X, idx, gate, self.expert_map, self.S_r, self.offsets, self.perm_token,
-                        self.perm_gate, self.inv, self.X_perm, self.ws_perm, E=w.E)
+                        self.perm_gate, self.inv, self.X_perm, self.ws_perm, E=w.E, x_sq=self.x_sq)
         api.moe_grouped_swiglu_fwd(self.layer_tables, self.X, self.X_perm, self.offsets, w.T, w.k, self.A_g,
                                    self.A_u, self.H, self.O, self.ws_fwd)
         api.moe_unpermute(self.layer_tables, self.O, self.inv, self.perm_gate, w.T, w.k, self.Y)
@@ -202,7 +206,7 @@ class MoELayerRunner:
     def backward(self, dgate: bool = False, accumulate_dw: bool = False):
         w = self.w
         api.moe_unpermute_bwd(self.layer_tables, self.dY, self.O, self.inv, self.offsets, self.perm_gate,
-                              w.T, w.k, self.dO, self.dgate if dgate else None)
+                              w.T, w.k, self.dO, self.dgate if dgate else None, dy_sq=self.dy_sq)
         api.moe_grouped_swiglu_bwd(self.layer_tables, self.X, self.X_perm, self.offsets, w.T, w.k, self.A_g,
                                    self.A_u, self.H, self.dO, self.dX_perm, accumulate_dw, self.ws_bwd)
         api.moe_permute_bwd(self.layer_tables, self.dX_perm, self.inv, w.T, w.k, self.dX)

@@ -33,7 +33,7 @@ def test_every_declared_function_is_exported_and_bound(L):
     for n in names:
         assert hasattr(L, n), n
         assert n in api.exported_names(), n
-    assert L.moe_abi_version() == 2
+    assert L.moe_abi_version() == api.ABI_VERSION == 3
 
 
 FAKE = 0x100000          # aligned, never dereferenced: validation fails first
@@ -121,10 +121,10 @@ def test_permute_workspace_and_layer_rejections(L):
     need = L.moe_permute_workspace_size(4096, 4, 16)
     assert need >= (4096 // 256) * 16 * 4
     rc, msg = rc_and_msg(L, "moe_permute", FAKE, api.MOE_BF16, FAKE, FAKE, None, 4096, 4096, 16, 4, 16,
-                         FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_size_t(need - 1), None)
+                         FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_size_t(need - 1), None, None)
     assert rc == api.MOE_ERR_WORKSPACE and "workspace" in msg
     rc, _ = rc_and_msg(L, "moe_permute", FAKE, api.MOE_BF16, FAKE, FAKE, None, 4096, 4096, 16, 4, 8,
-                       FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_size_t(need), None)
+                       FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, ctypes.c_size_t(need), None, None)
     assert rc == api.MOE_ERR_ARG                                    # identity map needs S >= E
     # a layer with an unsupported intermediate size
     lay = api.moe_layer(2048, 1404, api.MOE_BF16, 40, 2, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
@@ -323,8 +323,8 @@ def test_noalloc_permute_rejects_tables_above_its_scratch(L):
     T, S = 140000, 512
     assert L.moe_permute_workspace_size(T, 8, S) > 1 << 20
     rc, msg = rc_and_msg(L, "moe_permute_noalloc", FAKE, api.MOE_BF16, FAKE, FAKE, FAKE, T, 256, 256, 8, S, FAKE,
-                         FAKE, FAKE, FAKE, FAKE, None)
+                         FAKE, FAKE, FAKE, FAKE, None, None)
     assert rc == api.MOE_ERR_UNSUPPORTED and "scratch" in msg
     rc, msg = rc_and_msg(L, "moe_permute_noalloc", FAKE, api.MOE_BF16, FAKE, FAKE, FAKE, 64, 256, 256, 17, S, FAKE,
-                         FAKE, FAKE, FAKE, FAKE, None)
+                         FAKE, FAKE, FAKE, FAKE, None, None)
     assert rc == api.MOE_ERR_UNSUPPORTED                             # k > 16: validated as moe_permute does

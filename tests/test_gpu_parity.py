@@ -239,7 +239,7 @@ def utility_check(w, r, ref, only=None):
     slots, or `only`).  Returns (GPU utilities, oracle utilities)."""
     from paper_2508_19078_amd import api
     u = torch.full((r.S_r + w.n_shared,), -1.0, dtype=torch.float32, device="cuda")
-    assert api.moe_expert_utility(r.layer_tables, r.X, r.dY, r.perm_token, r.perm_gate, r.offsets, w.T, w.k,
+    assert api.moe_expert_utility(r.layer_tables, r.x_sq, r.dy_sq, r.perm_token, r.perm_gate, r.offsets, w.T, w.k,
                                   r.ws_bwd, u) == 0
     torch.cuda.synchronize()
     exp = O.expert_utility(ref.X, ref.dY, ref.idx, ref.gate, ref.plan.expert_map, ref.slots, only=only)

@@ -183,7 +183,7 @@ def test_full_expert_utility(run):
     linear in dY (a second backward with 2 dY doubles every utility)."""
     w, r, ref = run.w, run.r, run.ref
     u = torch.full((r.S_r + w.n_shared,), -1.0, dtype=torch.float32, device="cuda")
-    api.moe_expert_utility(r.layer_tables, r.X, r.dY, r.perm_token, r.perm_gate, r.offsets, w.T, w.k, r.ws_bwd, u)
+    api.moe_expert_utility(r.layer_tables, r.x_sq, r.dy_sq, r.perm_token, r.perm_gate, r.offsets, w.T, w.k, r.ws_bwd, u)
     torch.cuda.synchronize()
     got = host(u)
     exp = O.expert_utility_rank_one(ref.X, ref.dY, ref.idx, ref.gate, ref.plan.expert_map, ref.slots)
@@ -193,7 +193,7 @@ def test_full_expert_utility(run):
     assert rel_fro(got, exp) <= TOL_FFN and np.all(rel[exp > 0] <= TOL_FFN)
     r.dY.mul_(2)
     r.backward()
-    api.moe_expert_utility(r.layer_tables, r.X, r.dY, r.perm_token, r.perm_gate, r.offsets, w.T, w.k, r.ws_bwd, u)
+    api.moe_expert_utility(r.layer_tables, r.x_sq, r.dy_sq, r.perm_token, r.perm_gate, r.offsets, w.T, w.k, r.ws_bwd, u)
     torch.cuda.synchronize()
     got2 = host(u)
     r.dY.div_(2)

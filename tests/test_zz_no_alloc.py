@@ -39,7 +39,8 @@ def outputs(T, d, k, S, dev="cuda"):
                 perm_token=torch.full((R,), -5, dtype=torch.int32, device=dev),
                 perm_gate=torch.full((R,), -5.0, dtype=torch.float32, device=dev),
                 inv=torch.full((T, k), -5, dtype=torch.int32, device=dev),
-                X_perm=torch.zeros((R, d), dtype=torch.bfloat16, device=dev))
+                X_perm=torch.zeros((R, d), dtype=torch.bfloat16, device=dev),
+                x_sq=torch.full((T,), -5.0, dtype=torch.float32, device=dev))
 
 
 def one_pair(T, d, E, k, S, seed):
@@ -49,9 +50,9 @@ def one_pair(T, d, E, k, S, seed):
     a, b = outputs(T, d, k, S), outputs(T, d, k, S)
     ws = torch.empty(api.moe_permute_workspace_size(T, k, S), dtype=torch.uint8, device="cuda")
     assert api.moe_permute(Xd, idd, gd, emd, S, a["offsets"], a["perm_token"], a["perm_gate"], a["inv"],
-                           a["X_perm"], ws, E=E) == 0
+                           a["X_perm"], ws, E=E, x_sq=a["x_sq"]) == 0
     assert api.moe_permute_noalloc(Xd, idd, gd, emd, S, b["offsets"], b["perm_token"], b["perm_gate"], b["inv"],
-                                   b["X_perm"], E=E) == 0
+                                   b["X_perm"], E=E, x_sq=b["x_sq"]) == 0
     torch.cuda.synchronize()
     offsets = host(a["offsets"])
     N = int(offsets[-1])
@@ -63,6 +64,9 @@ def one_pair(T, d, E, k, S, seed):
     np.testing.assert_array_equal(host(b["perm_token"])[:N], host(a["perm_token"])[:N])
     np.testing.assert_array_equal(host(b["perm_gate"])[:N], host(a["perm_gate"])[:N])
     assert torch.equal(b["X_perm"][:N].view(torch.int16), a["X_perm"][:N].view(torch.int16))
+    assert torch.equal(b["x_sq"].view(torch.int32), a["x_sq"].view(torch.int32))
+    xs = np.sum(host(Xd).astype(np.float64) ** 2, axis=1)
+    np.testing.assert_allclose(host(b["x_sq"]), xs, rtol=1e-5)
     # and both are the oracle's maps
     o_off, o_tok, o_gate, o_inv = O.permute_maps(idx, gate, emap, S)
     np.testing.assert_array_equal(offsets, o_off)
@@ -85,5 +89,5 @@ def test_noalloc_permute_rejects_tables_above_its_scratch():
     assert api.moe_permute_workspace_size(T, 8, S) > cap
     fake = 0x100000                           # never dereferenced: rejected on the host
     rc = L.moe_permute_noalloc(fake, api.MOE_BF16, fake, fake, fake, T, 256, 256, 8, S, fake, fake, fake, fake,
-                               fake, None)
+                               fake, None, None)
     assert rc == api.MOE_ERR_UNSUPPORTED and b"scratch" in L.moe_last_error()
