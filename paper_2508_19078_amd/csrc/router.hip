@@ -960,7 +960,7 @@ int launch_route(const TX* X, const TW* W, const float* ws, const float* bias, i
     const bool wide = T >= 64 * ncu;
     const bool wider = T >= 128 * ncu;
     // the int8 profiling router keeps the 32-token kernel below when tiles are
-    // 32 tokens (measured faster there: 19.6 against 21.7 us at T = 8192, d = 2048)
+    // 32 tokens (measured faster there: 19.2 against 21.7 us at T = 8192, d = 2048)
     if (E <= 64 && d % (wide ? 128 : 256) == 0 && (MODE == 0 || wide)) {
       // 128-token tiles once every compute unit gets one (the router is read
       // once per CU), else 64-token ones, else 32; one block per CU
