@@ -359,7 +359,15 @@ size_t moe_permute_noalloc_max_bytes(void);
  * [0, E) resp. [0, S_routed).  With the environment variable
  * FLUXMOE_DEBUG_CHECKS set (to anything but "0"), moe_permute itself copies
  * idx and expert_map to the host, waits for `stream`, and runs this check
- * before it enqueues anything (slow: debugging only).
+ * before it enqueues anything (slow: debugging only).  The same switch makes
+ * the later entry points check the maps they index memory through, the same
+ * way, before they enqueue anything: inv (every entry decodes to a row in
+ * [0, T*k)) in moe_unpermute, moe_unpermute_bwd and moe_permute_bwd; offsets
+ * (0 first, non-decreasing, at most T*k) in moe_unpermute_bwd, the grouped
+ * SwiGLU forward (both) and backward, and moe_expert_utility; perm_token
+ * (tokens in [0, T) over the routed rows) in moe_expert_utility.  A failed
+ * check returns MOE_ERR_ARG naming the map and the entry.  A checking call
+ * synchronises the stream, so it cannot be captured into a HIP graph.
  */
 int moe_validate_routing(const int32_t* idx, const int32_t* expert_map, int T, int E, int k, int S_routed);
 

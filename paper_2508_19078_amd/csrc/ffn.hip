@@ -25,6 +25,7 @@
 // round-robin (every XCD gets an eighth of every slot), and the blocks of an XCD
 // draw its tiles from a counter, so that blocks that drew cheap tiles take more
 // (see DwQueue).
+#include "debug.hpp"
 #include "gemm_bf16.hpp"
 
 namespace fm {
@@ -1221,6 +1222,7 @@ extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const v
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_fwd_workspace_size(L, T, k));
   hipStream_t st = as_stream(stream);
+  if (debug_checks() && L->S_routed > 0) FM_TRY(debug_check_offsets(offsets, L->S_routed, T, k, st));
   const int S = n_slots(L);
   const Sched sc = sched_at(ws, S);
   const int tile_rows = bwd_tile_rows(L);
@@ -1274,6 +1276,7 @@ extern "C" int moe_grouped_swiglu_fwd_q8(const moe_layer_q8* L, const void* X, c
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_fwd_q8_workspace_size(L, T, k));
   hipStream_t st = as_stream(stream);
+  if (debug_checks() && L->S_routed > 0) FM_TRY(debug_check_offsets(offsets, L->S_routed, T, k, st));
   const int S = L->S_routed + L->S_shared;
   const Sched sc = sched_at(ws, S);
   hipLaunchKernelGGL(k_build_sched, dim3(1), dim3(1024), 0, st, offsets, L->S_routed, L->S_shared, T, CQ::RA,
@@ -1311,6 +1314,7 @@ extern "C" int moe_grouped_swiglu_bwd(const moe_layer* L, const void* X, const v
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_bwd_workspace_size(L, T, k));
   hipStream_t st = as_stream(stream);
+  if (debug_checks() && T > 0 && L->S_routed > 0) FM_TRY(debug_check_offsets(offsets, L->S_routed, T, k, st));
   const int S = n_slots(L);
   const Sched sc = sched_at(ws, S);
   const BwdWs bw = bwd_ws_at(ws, L, T, k);
@@ -1380,6 +1384,12 @@ extern "C" int moe_expert_utility(const moe_layer* L, const float* x_sq, const f
   if (ws_bytes < moe_grouped_swiglu_bwd_workspace_size(L, T, k))
     return fail(MOE_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes,
                 moe_grouped_swiglu_bwd_workspace_size(L, T, k));
+  if (debug_checks() && L->S_routed > 0) {
+    FM_TRY(debug_check_offsets(offsets, L->S_routed, T, k, st));
+    int rows = 0;
+    FM_TRY(debug_rows(offsets, L->S_routed, st, &rows));
+    FM_TRY(debug_check_tokens(perm_token, rows, T, st));
+  }
   // the backward's row-tile schedule (same offsets) is still in the workspace
   const Sched sc = sched_at(ws, S);
   const BwdWs bw = bwd_ws_at(ws, L, T, k);

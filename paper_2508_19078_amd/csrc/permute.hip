@@ -19,6 +19,7 @@
 #include <vector>
 
 #include "common.hpp"
+#include "debug.hpp"
 
 namespace fm {
 namespace {
@@ -583,11 +584,6 @@ namespace {
 // FLUXMOE_DEBUG_CHECKS set (and not "0"): moe_permute copies idx and
 // expert_map to the host, waits for the stream, and range-checks them before
 // launching anything.  Slow; for debugging callers.
-bool debug_checks() {
-  const char* v = getenv("FLUXMOE_DEBUG_CHECKS");
-  return v && v[0] && !(v[0] == '0' && v[1] == '\0');
-}
-
 int debug_check_routing(const int32_t* idx, const int32_t* expert_map, int T, int E, int k, int S_routed,
                         hipStream_t st) {
   std::vector<int32_t> hi((size_t)T * k), hm(expert_map ? E : 0);
@@ -767,6 +763,7 @@ extern "C" int moe_unpermute(const moe_layer* L, const void* O, const int32_t* i
   FM_TRY(need(O, "O")); FM_TRY(need(inv, "inv")); FM_TRY(need(perm_gate, "perm_gate")); FM_TRY(need(Y, "Y"));
   FM_TRY(need_aligned(O, "O")); FM_TRY(need_aligned(Y, "Y"));
   hipStream_t st = as_stream(stream);
+  if (debug_checks()) FM_TRY(debug_check_inv(inv, T, k, st));
   dim3 grid(cdiv(T, 4)), block(256);
 #define FM_CB(KM)                                                                                 \
   if (L->dtype == MOE_BF16)                                                                       \
@@ -794,6 +791,10 @@ extern "C" int moe_unpermute_bwd(const moe_layer* L, const void* dY, const void*
   FM_TRY(need_aligned(dY, "dY")); FM_TRY(need_aligned(O, "O")); FM_TRY(need_aligned(dO, "dO"));
   FM_TRY(need_aligned(dy_sq, "dy_sq"));
   hipStream_t st = as_stream(stream);
+  if (debug_checks()) {
+    FM_TRY(debug_check_inv(inv, T, k, st));
+    if (offsets && L->S_routed > 0) FM_TRY(debug_check_offsets(offsets, L->S_routed, T, k, st));
+  }
   dim3 grid(cdiv(T, 4)), block(256);
 #define FM_CBB(KM)                                                                                  \
   if (L->dtype == MOE_BF16)                                                                         \
@@ -817,6 +818,7 @@ extern "C" int moe_permute_bwd(const moe_layer* L, const void* dX_perm, const in
   FM_TRY(need(dX_perm, "dX_perm")); FM_TRY(need(inv, "inv")); FM_TRY(need(dX, "dX"));
   FM_TRY(need_aligned(dX_perm, "dX_perm")); FM_TRY(need_aligned(dX, "dX"));
   hipStream_t st = as_stream(stream);
+  if (debug_checks()) FM_TRY(debug_check_inv(inv, T, k, st));
   dim3 grid(cdiv(T, 4)), block(256);
 #define FM_PB(KM)                                                                                  \
   if (L->dtype == MOE_BF16)                                                                        \

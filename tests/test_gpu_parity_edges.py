@@ -288,6 +288,60 @@ def test_permute_with_debug_range_checks(monkeypatch):
         np.testing.assert_array_equal(a, host(t))
 
 
+def test_step_with_debug_range_checks(monkeypatch):
+    """FLUXMOE_DEBUG_CHECKS over the whole step and the utility: with valid maps
+    every output equals the run without the checks; maps with an entry out of
+    range are refused with MOE_ERR_ARG before anything is launched.  Each bad
+    entry still lies inside its buffer's allocation (a row just past the routed
+    rows, offsets[0] = 1, the token index T), so nothing could read outside
+    device memory even if a check were missing."""
+    w = W.scaled(W.WORKLOADS["deepseek_moe"], name="dbg2", cid=210, T=700, d=128, I=128)
+    inp = LayerInputs(w)
+    r = MoELayerRunner(w, inp)
+    util = torch.empty(r.S_r + w.n_shared, dtype=torch.float32, device="cuda")
+
+    def run():
+        r.step()
+        r.backward(dgate=True)
+        assert api.moe_expert_utility(r.layer_tables, r.x_sq, r.dy_sq, r.perm_token, r.perm_gate, r.offsets, w.T,
+                                      w.k, r.ws_bwd, util) == 0
+        torch.cuda.synchronize()
+        return [host(t).copy() for t in (r.counts, r.idx, r.offsets, r.inv, r.Y, r.dX, r.dgate, r.dWg, util,
+                                         r.x_sq, r.dy_sq)]
+
+    plain = run()
+    monkeypatch.setenv("FLUXMOE_DEBUG_CHECKS", "1")
+    for a, b in zip(plain, run()):
+        np.testing.assert_array_equal(a, b)
+    R = w.T * w.k
+    bad_inv = r.inv.clone()
+    bad_inv[3, 1] = R + 3                  # a shared row of the same buffers, past the routed ones
+    L = api.lib()
+    for name, call in (
+            ("moe_unpermute", lambda: api.moe_unpermute(r.layer_tables, r.O, bad_inv, r.perm_gate, w.T, w.k, r.Y)),
+            ("moe_unpermute_bwd", lambda: api.moe_unpermute_bwd(r.layer_tables, r.dY, r.O, bad_inv, r.offsets,
+                                                                r.perm_gate, w.T, w.k, r.dO, None)),
+            ("moe_permute_bwd", lambda: api.moe_permute_bwd(r.layer_tables, r.dX_perm, bad_inv, w.T, w.k, r.dX))):
+        with pytest.raises(RuntimeError, match="inv"):
+            call()
+        log(f"debug check refused a bad inv in {name}")
+    bad_off = r.offsets.clone()
+    bad_off[0] = 1
+    with pytest.raises(RuntimeError, match="offsets"):
+        api.moe_grouped_swiglu_fwd(r.layer_tables, r.X, r.X_perm, bad_off, w.T, w.k, r.A_g, r.A_u, r.H, r.O,
+                                   r.ws_fwd)
+    with pytest.raises(RuntimeError, match="offsets"):
+        api.moe_grouped_swiglu_bwd(r.layer_tables, r.X, r.X_perm, bad_off, w.T, w.k, r.A_g, r.A_u, r.H, r.dO,
+                                   r.dX_perm, False, r.ws_bwd)
+    bad_tok = r.perm_token.clone()
+    bad_tok[0] = w.T
+    with pytest.raises(RuntimeError, match="perm_token"):
+        api.moe_expert_utility(r.layer_tables, r.x_sq, r.dy_sq, bad_tok, r.perm_gate, r.offsets, w.T, w.k,
+                               r.ws_bwd, util)
+    torch.cuda.synchronize()
+    assert L.moe_last_error()
+
+
 def test_step_is_deterministic():
     """Two runs of the whole step on the same inputs agree bit for bit."""
     w = W.scaled(W.WORKLOADS["deepseek_moe"], name="det", cid=208, T=1500, d=256, I=320)
