@@ -1058,9 +1058,13 @@ constexpr int UT_THREADS = 256;   // threads of the per-row pass: one row each (
 static_assert(B16_ROWS <= UT_THREADS && G_BM <= UT_THREADS, "a row tile per block of the utility pass");
 
 // One block per row tile of a slot, the backward's own row tiles (its
-// schedule, tile_rows <= UT_THREADS rows, is still in the workspace): a thread
-// takes one row, ||g_r||^2 in fp64 from its token's norms, its gate and the P
-// partials of the row (in order); the block adds its rows by a fixed tree.
+// schedule, tile_rows <= UT_THREADS rows, is still in the workspace; the block
+// reads the tile prefix into LDS with one load per thread and finds its slot by
+// a binary search there): a thread takes one row, ||g_r||^2 in fp64 from its
+// token's norms, its gate and the P partials of the row (in order, loaded
+// UT_PB at a time); the block adds its rows by a fixed butterfly per wave and
+// then the waves in order.
+constexpr int UT_PB = 4;
 __global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, int tile_rows,
                                                              const int32_t* __restrict__ perm_token,
                                                              const float* __restrict__ perm_gate,
@@ -1068,13 +1072,21 @@ __global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, int til
                                                              const float* __restrict__ dy_sq,
                                                              const float2* __restrict__ norms, int P,
                                                              double* __restrict__ part) {
-  __shared__ double red[UT_THREADS];
-  const int b = blockIdx.x;
-  if (b >= ld_scalar(ra.mbase + ra.S)) return;
-  const int s = find_slot(ra.mbase, ra.S, b);
-  const int r0 = (b - ld_scalar(ra.mbase + s)) * tile_rows;
+  __shared__ int smb[1024];          // mbase[0..S], S <= 1023
+  __shared__ double wsum[UT_THREADS / 64];
+  const int S = ra.S, b = blockIdx.x, i = threadIdx.x;
+  for (int j = i; j <= S; j += UT_THREADS) smb[j] = ra.mbase[j];
+  __syncthreads();
+  if (b >= smb[S]) return;
+  int lo = 0, hi = S - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (smb[mid] <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  const int s = lo;
+  const int r0 = (b - smb[s]) * tile_rows;
   const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-  const int i = threadIdx.x;
   double v = 0.0;
   if (i < tile_rows && r0 + i < sr.nrows) {
     const long row = sr.orow0 + r0 + i;
@@ -1087,33 +1099,53 @@ __global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, int til
       tok = perm_token[row];
       g = perm_gate[row];
     }
-    const float xx = x_sq[tok], yy = dy_sq[tok];
     float sa = 0.f, sh = 0.f;
-    for (int p = 0; p < P; ++p) {
-      const float2 q = norms[row * P + p];
-      sa += q.x;
-      sh += q.y;
+    for (int p0 = 0; p0 < P; p0 += UT_PB) {
+      float2 q[UT_PB];
+#pragma unroll
+      for (int e = 0; e < UT_PB; ++e)
+        if (p0 + e < P) q[e] = norms[row * P + p0 + e];
+#pragma unroll
+      for (int e = 0; e < UT_PB; ++e)
+        if (p0 + e < P) {
+          sa += q[e].x;
+          sh += q[e].y;
+        }
     }
+    const float xx = x_sq[tok], yy = dy_sq[tok];
     v = (double)g * g * yy * sh + (double)sa * xx;
   }
-  red[i] = v;
-  __syncthreads();
+  // the butterfly leaves the same sum in every lane (each step adds two equal
+  // partial sums, in one order or the other)
 #pragma unroll
-  for (int w = UT_THREADS / 2; w > 0; w >>= 1) {
-    if (i < w) red[i] += red[i + w];
-    __syncthreads();
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if ((i & 63) == 0) wsum[i >> 6] = v;
+  __syncthreads();
+  if (i == 0) {
+    double t = 0.0;
+#pragma unroll
+    for (int w = 0; w < UT_THREADS / 64; ++w) t += wsum[w];
+    part[b] = t;
   }
-  if (i == 0) part[b] = red[0];
 }
 
-// Second pass: thread s adds its slot's tile sums in tile order.
+// Second pass: thread s adds its slot's tile sums in tile order (eight loads
+// in flight at a time).
 __global__ __launch_bounds__(1024) void k_utility_slots(RowArgs ra, const double* __restrict__ part,
                                                         float* __restrict__ u) {
   const int s = threadIdx.x;
   if (s >= ra.S) return;
-  double sum = 0.0;
-  for (int b = ld_scalar(ra.mbase + s); b < ld_scalar(ra.mbase + s + 1); ++b) sum += part[b];
   const int n = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k).nrows;
+  const int b0 = ra.mbase[s], b1 = ra.mbase[s + 1];
+  double sum = 0.0;
+  for (int q = b0; q < b1; q += 8) {
+    double x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = q + e < b1 ? part[q + e] : 0.0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (q + e < b1) sum += x[e];
+  }
   u[s] = n > 0 ? (float)sqrt((double)n * sum) : 0.f;
 }
 

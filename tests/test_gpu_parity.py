@@ -254,3 +254,12 @@ def test_expert_utility(run):
     np.testing.assert_array_equal(got == 0, exp == 0)      # exactly the empty slots are 0
     rel = np.abs(got - exp) / np.maximum(exp, 1e-30)
     assert np.all(rel[exp > 0] <= 5e-2)
+    # a second call on the same workspace (its block counter was set back to
+    # zero by the first) gives the same utilities bit for bit
+    from paper_2508_19078_amd import api
+    w, r = run.w, run.r
+    u2 = torch.full((r.S_r + w.n_shared,), -1.0, dtype=torch.float32, device="cuda")
+    assert api.moe_expert_utility(r.layer_tables, r.x_sq, r.dy_sq, r.perm_token, r.perm_gate, r.offsets, w.T, w.k,
+                                  r.ws_bwd, u2) == 0
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(u2), got)
