@@ -1054,99 +1054,88 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
 // tokens' ||x_t||^2 and ||dY_t||^2, which the permutation and the combine
 // backward write as they read X and dY.
 
-constexpr int UT_THREADS = 256;   // threads of the per-row pass: one row each (tiles of up to 256 rows)
-static_assert(B16_ROWS <= UT_THREADS && G_BM <= UT_THREADS, "a row tile per block of the utility pass");
+constexpr int UT_THREADS = 256;    // threads of the per-row pass: one row each
+constexpr int UT_PB = 4;           // norm partials of a row loaded together
+constexpr int US_THREADS = 1024;   // threads of the per-slot pass: one block per slot
+constexpr int US_BATCH = 8;        // row values per thread loaded together
 
-// One block per row tile of a slot, the backward's own row tiles (its
-// schedule, tile_rows <= UT_THREADS rows, is still in the workspace; the block
-// reads the tile prefix into LDS with one load per thread and finds its slot by
-// a binary search there): a thread takes one row, ||g_r||^2 in fp64 from its
-// token's norms, its gate and the P partials of the row (in order, loaded
-// UT_PB at a time); the block adds its rows by a fixed butterfly per wave and
-// then the waves in order.
-constexpr int UT_PB = 4;
-__global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, int tile_rows,
-                                                             const int32_t* __restrict__ perm_token,
+// Per-row pass over the whole row space (routed rows [0, T*k), of which the
+// first offsets[S_r] are used, then T rows per shared expert): a thread forms
+// its row's ||g_r||^2 in fp64 from the row's token norms, its gate and its P
+// partials (in order) and stores it at vrow[row].  The token of a routed row
+// is read before it is known whether the row is used (the row count is read in
+// parallel); an unused row's token is clamped into [0, T) so that its norm
+// loads stay in bounds, and its value is not stored.  With no routed slot the
+// routed rows are skipped (the maps may then be NULL).
+__global__ __launch_bounds__(UT_THREADS) void k_utility_rows(RowArgs ra, const int32_t* __restrict__ perm_token,
                                                              const float* __restrict__ perm_gate,
                                                              const float* __restrict__ x_sq,
                                                              const float* __restrict__ dy_sq,
                                                              const float2* __restrict__ norms, int P,
-                                                             double* __restrict__ part) {
-  __shared__ int smb[1024];          // mbase[0..S], S <= 1023
-  __shared__ double wsum[UT_THREADS / 64];
-  const int S = ra.S, b = blockIdx.x, i = threadIdx.x;
-  for (int j = i; j <= S; j += UT_THREADS) smb[j] = ra.mbase[j];
-  __syncthreads();
-  if (b >= smb[S]) return;
-  int lo = 0, hi = S - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (smb[mid] <= b) lo = mid;
-    else hi = mid - 1;
+                                                             double* __restrict__ vrow) {
+  const long R = (long)ra.Tn * ra.k;
+  const long r = (long)blockIdx.x * UT_THREADS + threadIdx.x;
+  if (r >= R + (long)ra.Tn * (ra.S - ra.S_r)) return;
+  const bool routed = r < R;
+  if (routed && ra.S_r == 0) return;   // no routed slot: the maps may be NULL
+  const int used = ra.S_r > 0 ? ld_scalar(ra.offsets + ra.S_r) : 0;
+  int tok;
+  float g = 1.f;
+  if (routed) {
+    tok = min(max(perm_token[r], 0), ra.Tn - 1);
+    g = perm_gate[r];
+  } else {
+    tok = (int)((r - R) % ra.Tn);
   }
-  const int s = lo;
-  const int r0 = (b - smb[s]) * tile_rows;
+  float sa = 0.f, sh = 0.f;
+  for (int p0 = 0; p0 < P; p0 += UT_PB) {
+    float2 q[UT_PB];
+#pragma unroll
+    for (int c = 0; c < UT_PB; ++c) q[c] = norms[r * P + min(p0 + c, P - 1)];
+#pragma unroll
+    for (int c = 0; c < UT_PB; ++c)
+      if (p0 + c < P) {
+        sa += q[c].x;
+        sh += q[c].y;
+      }
+  }
+  const float xx = x_sq[tok], yy = dy_sq[tok];
+  if (!routed || r < used) vrow[r] = (double)g * g * yy * sh + (double)sa * xx;
+}
+
+// Per-slot pass, one block per slot: a thread adds the row values i, i + 1024,
+// ... of the slot (US_BATCH loads in flight, added in row order); the block
+// adds its threads by a fixed butterfly per wave, then the waves in order.
+__global__ __launch_bounds__(US_THREADS) void k_utility_slots(RowArgs ra, const double* __restrict__ vrow,
+                                                              float* __restrict__ u) {
+  __shared__ double wsum[US_THREADS / 64];
+  const int s = blockIdx.x, i = threadIdx.x;
   const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-  double v = 0.0;
-  if (i < tile_rows && r0 + i < sr.nrows) {
-    const long row = sr.orow0 + r0 + i;
-    int tok;
-    float g;
-    if (sr.shared) {
-      tok = r0 + i;
-      g = 1.f;
-    } else {
-      tok = perm_token[row];
-      g = perm_gate[row];
-    }
-    float sa = 0.f, sh = 0.f;
-    for (int p0 = 0; p0 < P; p0 += UT_PB) {
-      float2 q[UT_PB];
+  const double* v = vrow + sr.orow0;
+  double sum = 0.0;
+  for (int r0 = 0; r0 < sr.nrows; r0 += US_BATCH * US_THREADS) {
+    double x[US_BATCH];
 #pragma unroll
-      for (int e = 0; e < UT_PB; ++e)
-        if (p0 + e < P) q[e] = norms[row * P + p0 + e];
-#pragma unroll
-      for (int e = 0; e < UT_PB; ++e)
-        if (p0 + e < P) {
-          sa += q[e].x;
-          sh += q[e].y;
-        }
+    for (int e = 0; e < US_BATCH; ++e) {
+      const int r = r0 + e * US_THREADS + i;
+      x[e] = r < sr.nrows ? v[r] : 0.0;
     }
-    const float xx = x_sq[tok], yy = dy_sq[tok];
-    v = (double)g * g * yy * sh + (double)sa * xx;
+#pragma unroll
+    for (int e = 0; e < US_BATCH; ++e)
+      if (r0 + e * US_THREADS + i < sr.nrows) sum += x[e];
   }
   // the butterfly leaves the same sum in every lane (each step adds two equal
   // partial sums, in one order or the other)
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-  if ((i & 63) == 0) wsum[i >> 6] = v;
+  for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
+  if ((i & 63) == 0) wsum[i >> 6] = sum;
   __syncthreads();
   if (i == 0) {
     double t = 0.0;
 #pragma unroll
-    for (int w = 0; w < UT_THREADS / 64; ++w) t += wsum[w];
-    part[b] = t;
+    for (int w = 0; w < US_THREADS / 64; ++w) t += wsum[w];
+    u[s] = sr.nrows > 0 ? (float)sqrt((double)sr.nrows * t) : 0.f;
   }
-}
-
-// Second pass: thread s adds its slot's tile sums in tile order (eight loads
-// in flight at a time).
-__global__ __launch_bounds__(1024) void k_utility_slots(RowArgs ra, const double* __restrict__ part,
-                                                        float* __restrict__ u) {
-  const int s = threadIdx.x;
-  if (s >= ra.S) return;
-  const int n = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k).nrows;
-  const int b0 = ra.mbase[s], b1 = ra.mbase[s + 1];
-  double sum = 0.0;
-  for (int q = b0; q < b1; q += 8) {
-    double x[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) x[e] = q + e < b1 ? part[q + e] : 0.0;
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-      if (q + e < b1) sum += x[e];
-  }
-  u[s] = n > 0 ? (float)sqrt((double)n * sum) : 0.f;
 }
 
 __global__ void k_zero_f32(float* p, int n) {
@@ -1194,12 +1183,8 @@ extern "C" size_t moe_grouped_swiglu_fwd_workspace_size(const moe_layer* L, int 
   return sched_bytes(n_slots(L));
 }
 
-// Rows per row tile of the backward (bf16 or fp32 core), and an upper bound of
-// the row tiles: sum_s ceil(n_s / rows).
+// Rows per row tile of the backward (bf16 or fp32 core).
 static int bwd_tile_rows(const moe_layer* L) { return L->dtype == MOE_BF16 ? B16_ROWS : G_BM; }
-static size_t utility_tiles(const moe_layer* L, int T, int k) {
-  return rows_total(L, T, k) / bwd_tile_rows(L) + n_slots(L) + 1;
-}
 // Partials of the utility's row norms per row: one per dH column tile (bf16),
 // two per column tile (fp32, one per wave column).
 static int norm_parts(const moe_layer* L) {
@@ -1207,12 +1192,12 @@ static int norm_parts(const moe_layer* L) {
 }
 
 // Backward workspace: schedule | dA_g | dA_u | per-row norm partials (float2) |
-// utility tile sums (double).
+// the utility's per-row values (double).
 struct BwdWs {
   char* dAg;
   char* dAu;
   float2* norms;
-  double* part;
+  double* vrow;
 };
 static size_t bwd_act_bytes(const moe_layer* L, int T, int k) {
   return round256(rows_total(L, T, k) * L->I * esize(L->dtype));
@@ -1226,7 +1211,7 @@ static BwdWs bwd_ws_at(void* ws, const moe_layer* L, int T, int k) {
   p += 2 * act;
   w.norms = (float2*)p;
   p += round256(sizeof(float2) * rows_total(L, T, k) * norm_parts(L));
-  w.part = (double*)p;
+  w.vrow = (double*)p;
   return w;
 }
 
@@ -1234,7 +1219,7 @@ extern "C" size_t moe_grouped_swiglu_bwd_workspace_size(const moe_layer* L, int 
   if (!L || T < 0 || k <= 0) return 0;
   return sched_bytes(n_slots(L)) + 2 * bwd_act_bytes(L, T, k) +
          round256(sizeof(float2) * rows_total(L, T, k) * norm_parts(L)) +
-         round256(sizeof(double) * utility_tiles(L, T, k));
+         round256(sizeof(double) * rows_total(L, T, k));
 }
 
 extern "C" int moe_grouped_swiglu_fwd(const moe_layer* L, const void* X, const void* X_perm,
@@ -1422,13 +1407,14 @@ extern "C" int moe_expert_utility(const moe_layer* L, const float* x_sq, const f
     FM_TRY(debug_rows(offsets, L->S_routed, st, &rows));
     FM_TRY(debug_check_tokens(perm_token, rows, T, st));
   }
-  // the backward's row-tile schedule (same offsets) is still in the workspace
-  const Sched sc = sched_at(ws, S);
+  // the per-row partials the backward left in the workspace; the row values
+  // go to the space after them
   const BwdWs bw = bwd_ws_at(ws, L, T, k);
-  const RowArgs ra{offsets, sc.mbase, L->S_routed, S, T, k, L->d, L->I};
-  hipLaunchKernelGGL(k_utility_rows, dim3((unsigned)utility_tiles(L, T, k)), dim3(UT_THREADS), 0, st, ra,
-                     bwd_tile_rows(L), perm_token, perm_gate, x_sq, dy_sq, (const float2*)bw.norms, norm_parts(L),
-                     bw.part);
-  hipLaunchKernelGGL(k_utility_slots, dim3(1), dim3(1024), 0, st, ra, (const double*)bw.part, utility);
+  const RowArgs ra{offsets, nullptr, L->S_routed, S, T, k, L->d, L->I};
+  hipLaunchKernelGGL(k_utility_rows, dim3((unsigned)cdiv((long long)rows_total(L, T, k), UT_THREADS)),
+                     dim3(UT_THREADS), 0, st, ra, perm_token, perm_gate, x_sq, dy_sq, (const float2*)bw.norms,
+                     norm_parts(L), bw.vrow);
+  hipLaunchKernelGGL(k_utility_slots, dim3((unsigned)S), dim3(US_THREADS), 0, st, ra, (const double*)bw.vrow,
+                     utility);
   return check_launch("moe_expert_utility");
 }
