@@ -268,6 +268,47 @@ def test_backward_without_tokens_zeroes_weight_gradients():
         assert bool((t[1] == 3).all())
 
 
+def test_utility_of_a_layer_without_routed_slots():
+    """A layer of shared experts only (S_routed = 0): forward, backward and the
+    expert utility with the permutation maps NULL (the routed part of the row
+    space is never read), against the fp64 oracle."""
+    T, d, I, k, n_sh = 300, 128, 192, 2, 2
+    dt = torch.bfloat16
+    g = torch.Generator(device="cpu").manual_seed(611)
+    X = (torch.randn(T, d, generator=g)).to(dt).cuda()
+    dY = (torch.randn(T, d, generator=g) * 0.1).to(dt).cuda()
+    Wg = (torch.randn(n_sh, I, d, generator=g) / d ** 0.5).to(dt).cuda()
+    Wu = (torch.randn(n_sh, I, d, generator=g) / d ** 0.5).to(dt).cuda()
+    Wd = (torch.randn(n_sh, d, I, generator=g) / I ** 0.5).to(dt).cuda()
+    dWg, dWu, dWd = (torch.zeros(n_sh, *t.shape[1:], device="cuda") for t in (Wg, Wu, Wd))
+    lay = api.LayerTables(d, I, dt, 0, n_sh, list(Wg), list(Wu), list(Wd), list(dWg), list(dWu), list(dWd))
+    Rt = T * (k + n_sh)
+    A_g, A_u, H = (torch.zeros(Rt, I, dtype=dt, device="cuda") for _ in range(3))
+    Ob = torch.zeros(Rt, d, dtype=dt, device="cuda")
+    dO = torch.zeros(Rt, d, dtype=dt, device="cuda")
+    for i in range(n_sh):
+        dO[T * k + i * T:T * k + (i + 1) * T] = dY
+    dXp = torch.zeros(Rt, d, dtype=dt, device="cuda")
+    offsets = torch.zeros(1, dtype=torch.int32, device="cuda")
+    wsf = torch.empty(api.moe_grouped_swiglu_fwd_workspace_size(lay, T, k), dtype=torch.uint8, device="cuda")
+    wsb = torch.empty(api.moe_grouped_swiglu_bwd_workspace_size(lay, T, k), dtype=torch.uint8, device="cuda")
+    assert api.moe_grouped_swiglu_fwd(lay, X, None, offsets, T, k, A_g, A_u, H, Ob, wsf) == 0
+    assert api.moe_grouped_swiglu_bwd(lay, X, None, offsets, T, k, A_g, A_u, H, dO, dXp, False, wsb) == 0
+    x_sq = X.float().pow(2).sum(1).contiguous()
+    dy_sq = dY.float().pow(2).sum(1).contiguous()
+    u = torch.full((n_sh,), -1.0, dtype=torch.float32, device="cuda")
+    assert api.moe_expert_utility(lay, x_sq, dy_sq, None, None, offsets, T, k, wsb, u) == 0
+    torch.cuda.synchronize()
+    f64 = lambda t: host(t.float()).astype(np.float64)
+    slots = O.SlotWeights([f64(w) for w in Wg], [f64(w) for w in Wu], [f64(w) for w in Wd], [True] * n_sh,
+                          n_shared=n_sh)
+    exp = O.expert_utility(f64(X), f64(dY), np.zeros((T, k), dtype=np.int64), np.ones((T, k)),
+                           np.zeros(1, dtype=np.int64), slots)
+    got = host(u)
+    log(f"shared-only utility: got {got}, oracle {exp}")
+    assert rel_fro(got, exp) <= TOL_FFN and bool(np.all(got > 0))
+
+
 def test_permute_with_debug_range_checks(monkeypatch):
     """FLUXMOE_DEBUG_CHECKS: moe_permute copies idx and expert_map to the host
     and range-checks them before launching; valid maps give the same result as
