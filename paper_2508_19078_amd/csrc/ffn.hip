@@ -535,6 +535,30 @@ typedef const bf16* cbp;
 // lone wave cannot hide its own LDS-read and DMA-issue stalls.)
 using CB = B16Cfg<256, 256, 2, 4, 64, 3, 2>;
 constexpr int B16_ROWS = CB::RA;   // rows per row tile of the bf16 kernels
+// Pieces of a full tile for the last round of a row-tile product: a row half
+// (128 x 256) and a quarter (128 x 128), same waves and slab depth.
+using CBH = B16Cfg<128, 256, 2, 4, 64, 3, 2>;
+using CBQ = B16Cfg<128, 128, 2, 4, 64, 3, 2>;
+
+// The XCD's share of a row-tile product (row_range) goes in rounds of one full
+// tile per block.  When the last round would leave at least half of the XCD's
+// blocks idle, its tiles are cut into `parts` pieces (2: row halves; 4: row and
+// column halves, where the product allows them), one piece per block, so that
+// the round takes about a piece's time (a slab of a piece moves 3/4 or 1/2 of a
+// full tile's bytes).  cut = the first tile of that round, or tr.hi.
+struct LastRound {
+  long long cut;
+  int parts;
+};
+__device__ __forceinline__ LastRound last_round(const TileRange& tr, bool quarters) {
+  const long long rem = (tr.hi - tr.lo) % tr.step;
+  LastRound lr{tr.hi, 0};
+  if (rem > 0 && rem * 2 <= tr.step) {
+    lr.cut = tr.hi - rem;
+    lr.parts = quarters && rem * 4 <= tr.step ? 4 : 2;
+  }
+  return lr;
+}
 
 // Physical index of logical row / column c of an operand that interleaves two
 // matrices in 32-blocks (the matrix is (c >> 5) & 1).
@@ -648,59 +672,74 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
 }
 
 // [A_g | A_u] = X_s [W_gate | W_up]^T, H = silu(A_g) A_u.  The B tile
-// interleaves 32-row blocks of W_gate and W_up (128 intermediate columns per
-// 256-row tile): tile j = 2jj of a wave holds gate and j = 2jj + 1 up of the
-// same columns.
+// interleaves 32-row blocks of W_gate and W_up (RB / 2 intermediate columns per
+// tile): tile j = 2jj of a wave holds gate and j = 2jj + 1 up of the same
+// columns.  One tile of shape C at rows m0 of slot s, intermediate columns n0.
+template <class C>
+__device__ __forceinline__ void gate_up_tile(const LayerPtrs<bf16>& W, cbp X, cbp Xp, const RowArgs& ra,
+                                             FM_LDS char* lds, int s, int m0, int n0, bf16* Ag, bf16* Au,
+                                             bf16* H) {
+  const int d = ra.d, I = ra.I;
+  const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+  const int rows = sr.nrows - m0, cols = I - n0;
+  if (rows <= 0 || cols <= 0) return;
+  const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, rows, d};
+  const B16Src B{ld_scalar(W.wg + s) + (size_t)n0 * d, ld_scalar(W.wu + s) + (size_t)n0 * d, d, cols, d};
+  B16Acc<C::MI, C::NJ> acc;
+  acc.zero();
+  b16_gemm<C, true, true, false, true>(A, B, d, lds, acc);
+  // A_g and A_u staged side by side, then H in the first half.
+  using SG = Stage<bf16, C::RB / 2>;
+  FM_LDS char* sg = lds;
+  FM_LDS char* su = sg + C::RA * (C::RB / 2) * 2;
+  const size_t ob = (size_t)(sr.orow0 + m0);
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int jj = 0; jj < C::NJ / 2; ++jj)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const AccCoord c = b16_coord<C>(i, 2 * jj, q);
+        SG::put4(sg, c.row, deinter(c.col4), acc.quad(i, 2 * jj, q));
+        SG::put4(su, c.row, deinter(c.col4), acc.quad(i, 2 * jj + 1, q));
+      }
+  barrier_lds_writes();
+  SG::template copy_out<C::RA, C::THREADS>(sg, Ag + ob * I + n0, I, rows, cols);
+  SG::template copy_out<C::RA, C::THREADS>(su, Au + ob * I + n0, I, rows, cols);
+  barrier_lds();
+#pragma unroll
+  for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+    for (int jj = 0; jj < C::NJ / 2; ++jj)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const AccCoord c = b16_coord<C>(i, 2 * jj, q);
+        const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
+        f32x4_t h;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm_fast(ag[r]) * u[r];
+        SG::put4(sg, c.row, deinter(c.col4), h);
+      }
+  barrier_lds_writes();
+  SG::template copy_out<C::RA, C::THREADS>(sg, H + ob * I + n0, I, rows, cols);
+  barrier_lds();
+}
+
 __global__ __launch_bounds__(CB::THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp X, cbp Xp, RowArgs ra,
                                                           bf16* Ag, bf16* Au, bf16* H) {
   __shared__ __align__(16) char lds[CB::LDS];
-  const int d = ra.d, I = ra.I, NT = (I + CB::RB / 2 - 1) / (CB::RB / 2);
+  FM_LDS char* const l = (FM_LDS char*)lds;
+  const int NT = (ra.I + CB::RB / 2 - 1) / (CB::RB / 2);
   const TileRange tr = row_range(ra, NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+  const LastRound lr = last_round(tr, false);
+  for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * CB::RA, n0 = rt.n * (CB::RB / 2);
-    const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, sr.nrows - m0, d};
-    const B16Src B{ld_scalar(W.wg + rt.s) + (size_t)n0 * d, ld_scalar(W.wu + rt.s) + (size_t)n0 * d, d, I - n0, d};
-    B16Acc<CB::MI, CB::NJ> acc;
-    acc.zero();
-    b16_gemm<CB, true, true, false, true>(A, B, d, (FM_LDS char*)lds, acc);
-    // A_g and A_u staged side by side (64 KB each), then H in the first half.
-    using SG = Stage<bf16, CB::RB / 2>;
-    FM_LDS char* sg = (FM_LDS char*)lds;
-    FM_LDS char* su = sg + CB::RA * (CB::RB / 2) * 2;
-    const size_t ob = (size_t)(sr.orow0 + m0);
-    const int rows = sr.nrows - m0, cols = I - n0;
-#pragma unroll
-    for (int i = 0; i < CB::MI; ++i)
-#pragma unroll
-      for (int jj = 0; jj < CB::NJ / 2; ++jj)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const AccCoord c = b16_coord<CB>(i, 2 * jj, q);
-          SG::put4(sg, c.row, deinter(c.col4), acc.quad(i, 2 * jj, q));
-          SG::put4(su, c.row, deinter(c.col4), acc.quad(i, 2 * jj + 1, q));
-        }
-    barrier_lds_writes();
-    SG::template copy_out<CB::RA, CB::THREADS>(sg, Ag + ob * I + n0, I, rows, cols);
-    SG::template copy_out<CB::RA, CB::THREADS>(su, Au + ob * I + n0, I, rows, cols);
-    barrier_lds();
-#pragma unroll
-    for (int i = 0; i < CB::MI; ++i)
-#pragma unroll
-      for (int jj = 0; jj < CB::NJ / 2; ++jj)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const AccCoord c = b16_coord<CB>(i, 2 * jj, q);
-          const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
-          f32x4_t h;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm_fast(ag[r]) * u[r];
-          SG::put4(sg, c.row, deinter(c.col4), h);
-        }
-    barrier_lds_writes();
-    SG::template copy_out<CB::RA, CB::THREADS>(sg, H + ob * I + n0, I, rows, cols);
-    barrier_lds();
+    gate_up_tile<CB>(W, X, Xp, ra, l, rt.s, rt.m * CB::RA, rt.n * (CB::RB / 2), Ag, Au, H);
+  }
+  if (lr.parts && tr.first < (tr.hi - lr.cut) * 2) {   // a row half of the last round
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / 2);
+    gate_up_tile<CBH>(W, X, Xp, ra, l, rt.s, rt.m * CB::RA + (tr.first % 2) * CBH::RA, rt.n * (CB::RB / 2), Ag,
+                      Au, H);
   }
 }
 
@@ -804,66 +843,123 @@ __global__ __launch_bounds__(CQ::THREADS) void kq_down(Q8Ptrs W, cbp H, RowArgs 
   }
 }
 
-// O = H W_down^T
+// O = H W_down^T, one tile of shape C at rows m0 of slot s, columns n0.
+template <class C>
+__device__ __forceinline__ void down_tile(const LayerPtrs<bf16>& W, cbp H, const RowArgs& ra, FM_LDS char* lds,
+                                          int s, int m0, int n0, bf16* O) {
+  const int d = ra.d, I = ra.I;
+  const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+  const int rows = sr.nrows - m0, cols = d - n0;
+  if (rows <= 0 || cols <= 0) return;
+  const size_t ob = (size_t)(sr.orow0 + m0);
+  const B16Src A{H + ob * I, nullptr, I, rows, I};
+  const B16Src B{ld_scalar(W.wd + s) + (size_t)n0 * I, nullptr, I, cols, I};
+  B16Acc<C::MI, C::NJ> acc;
+  acc.zero();
+  b16_gemm<C, true, true>(A, B, I, lds, acc);
+  b16_store_staged<C>(acc, lds, O + ob * d + n0, d, rows, cols);
+}
+
 __global__ __launch_bounds__(CB::THREADS) void kb_down(LayerPtrs<bf16> W, cbp H, RowArgs ra, bf16* O) {
   __shared__ __align__(16) char lds[CB::LDS];
-  const int d = ra.d, I = ra.I, NT = (d + CB::RB - 1) / CB::RB;
+  FM_LDS char* const l = (FM_LDS char*)lds;
+  const int NT = (ra.d + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+  const LastRound lr = last_round(tr, true);
+  for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
-    const size_t ob = (size_t)(sr.orow0 + m0);
-    const B16Src A{H + ob * I, nullptr, I, sr.nrows - m0, I};
-    const B16Src B{ld_scalar(W.wd + rt.s) + (size_t)n0 * I, nullptr, I, d - n0, I};
-    B16Acc<CB::MI, CB::NJ> acc;
-    acc.zero();
-    b16_gemm<CB, true, true>(A, B, I, (FM_LDS char*)lds, acc);
-    b16_store_staged<CB>(acc, (FM_LDS char*)lds, O + ob * d + n0, d, sr.nrows - m0, d - n0);
+    down_tile<CB>(W, H, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, O);
+  }
+  if (lr.parts && tr.first < (tr.hi - lr.cut) * lr.parts) {   // a piece of the last round
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / lr.parts);
+    const int p = tr.first % lr.parts;
+    if (lr.parts == 4)
+      down_tile<CBQ>(W, H, ra, l, rt.s, rt.m * CB::RA + (p >> 1) * CBQ::RA, rt.n * CB::RB + (p & 1) * CBQ::RB, O);
+    else
+      down_tile<CBH>(W, H, ra, l, rt.s, rt.m * CB::RA + p * CBH::RA, rt.n * CB::RB, O);
   }
 }
 
-// dH = dO W_down (B = W_down read k-major), epilogue dA_g, dA_u.
+// dH = dO W_down (B = W_down read k-major), epilogue dA_g, dA_u; one tile of
+// shape C (C::RB = 256: the epilogue takes whole 256-column rows) at rows m0
+// of slot s, column tile n.
+template <class C>
+__device__ __forceinline__ void dh_tile(const LayerPtrs<bf16>& W, cbp dO, cbp Ag, cbp Au, const RowArgs& ra,
+                                        FM_LDS char* lds, int s, int m0, int n, int NT, bf16* dAg, bf16* dAu,
+                                        float2* norms) {
+  static_assert(C::RB == CB::RB, "whole column tiles");
+  const int d = ra.d, I = ra.I, n0 = n * C::RB;
+  const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+  const int rows = sr.nrows - m0;
+  if (rows <= 0) return;
+  const size_t ob = (size_t)(sr.orow0 + m0);
+  // B(n = intermediate index, k = hidden index) = W_down[k][n]
+  const B16Src A{dO + ob * d, nullptr, d, rows, d};
+  const B16Src B{ld_scalar(W.wd + s) + n0, nullptr, I, I - n0, d};
+  B16Acc<C::MI, C::NJ> acc;
+  acc.zero();
+  b16_gemm<C, true, false>(A, B, d, lds, acc);
+  b16_dswiglu_staged<C>(acc, lds, Ag + ob * I + n0, Au + ob * I + n0, dAg + ob * I + n0, dAu + ob * I + n0, I,
+                        rows, I - n0, norms + ob * NT + n, NT);
+}
+
 __global__ __launch_bounds__(CB::THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, cbp Ag, cbp Au, RowArgs ra,
                                                      bf16* dAg, bf16* dAu, float2* norms) {
   __shared__ __align__(16) char lds[CB::LDS];
-  const int d = ra.d, I = ra.I, NT = (I + CB::RB - 1) / CB::RB;
+  FM_LDS char* const l = (FM_LDS char*)lds;
+  const int NT = (ra.I + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+  const LastRound lr = last_round(tr, false);
+  for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
-    const size_t ob = (size_t)(sr.orow0 + m0);
-    // B(n = intermediate index, k = hidden index) = W_down[k][n]
-    const B16Src A{dO + ob * d, nullptr, d, sr.nrows - m0, d};
-    const B16Src B{ld_scalar(W.wd + rt.s) + n0, nullptr, I, I - n0, d};
-    B16Acc<CB::MI, CB::NJ> acc;
-    acc.zero();
-    b16_gemm<CB, true, false>(A, B, d, (FM_LDS char*)lds, acc);
-    b16_dswiglu_staged<CB>(acc, (FM_LDS char*)lds, Ag + ob * I + n0, Au + ob * I + n0, dAg + ob * I + n0,
-                           dAu + ob * I + n0, I, sr.nrows - m0, I - n0, norms + ob * NT + rt.n, NT);
+    dh_tile<CB>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA, rt.n, NT, dAg, dAu, norms);
+  }
+  if (lr.parts && tr.first < (tr.hi - lr.cut) * 2) {   // a row half of the last round
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / 2);
+    dh_tile<CBH>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA + (tr.first % 2) * CBH::RA, rt.n, NT, dAg, dAu,
+                 norms);
   }
 }
 
-// dX_s = dA_g W_gate + dA_u W_up (two K passes, B read k-major).
+// dX_s = dA_g W_gate + dA_u W_up (two K passes, B read k-major), one tile of
+// shape C at rows m0 of slot s, columns n0.
+template <class C>
+__device__ __forceinline__ void dx_tile(const LayerPtrs<bf16>& W, cbp dAg, cbp dAu, const RowArgs& ra,
+                                        FM_LDS char* lds, int s, int m0, int n0, bf16* dXp) {
+  const int d = ra.d, I = ra.I;
+  const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+  const int rows = sr.nrows - m0, cols = d - n0;
+  if (rows <= 0 || cols <= 0) return;
+  const size_t ob = (size_t)(sr.orow0 + m0);
+  B16Acc<C::MI, C::NJ> acc;
+  acc.zero();
+  // B(n = hidden index, k = intermediate index) = W_gate[k][n], then W_up
+  b16_gemm<C, true, false>(B16Src{dAg + ob * I, nullptr, I, rows, I},
+                           B16Src{ld_scalar(W.wg + s) + n0, nullptr, d, cols, I}, I, lds, acc);
+  b16_gemm<C, true, false>(B16Src{dAu + ob * I, nullptr, I, rows, I},
+                           B16Src{ld_scalar(W.wu + s) + n0, nullptr, d, cols, I}, I, lds, acc);
+  b16_store_staged<C>(acc, lds, dXp + ob * d + n0, d, rows, cols);
+}
+
 __global__ __launch_bounds__(CB::THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg, cbp dAu, RowArgs ra,
                                                      bf16* dXp) {
   __shared__ __align__(16) char lds[CB::LDS];
-  const int d = ra.d, I = ra.I, NT = (d + CB::RB - 1) / CB::RB;
+  FM_LDS char* const l = (FM_LDS char*)lds;
+  const int NT = (ra.d + CB::RB - 1) / CB::RB;
   const TileRange tr = row_range(ra, NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+  const LastRound lr = last_round(tr, true);
+  for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
-    const int m0 = rt.m * CB::RA, n0 = rt.n * CB::RB;
-    const size_t ob = (size_t)(sr.orow0 + m0);
-    B16Acc<CB::MI, CB::NJ> acc;
-    acc.zero();
-    // B(n = hidden index, k = intermediate index) = W_gate[k][n], then W_up
-    b16_gemm<CB, true, false>(B16Src{dAg + ob * I, nullptr, I, sr.nrows - m0, I},
-                              B16Src{ld_scalar(W.wg + rt.s) + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
-    b16_gemm<CB, true, false>(B16Src{dAu + ob * I, nullptr, I, sr.nrows - m0, I},
-                              B16Src{ld_scalar(W.wu + rt.s) + n0, nullptr, d, d - n0, I}, I, (FM_LDS char*)lds, acc);
-    b16_store_staged<CB>(acc, (FM_LDS char*)lds, dXp + ob * d + n0, d, sr.nrows - m0, d - n0);
+    dx_tile<CB>(W, dAg, dAu, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, dXp);
+  }
+  if (lr.parts && tr.first < (tr.hi - lr.cut) * lr.parts) {   // a piece of the last round
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / lr.parts);
+    const int p = tr.first % lr.parts;
+    if (lr.parts == 4)
+      dx_tile<CBQ>(W, dAg, dAu, ra, l, rt.s, rt.m * CB::RA + (p >> 1) * CBQ::RA, rt.n * CB::RB + (p & 1) * CBQ::RB,
+                   dXp);
+    else
+      dx_tile<CBH>(W, dAg, dAu, ra, l, rt.s, rt.m * CB::RA + p * CBH::RA, rt.n * CB::RB, dXp);
   }
 }
 
