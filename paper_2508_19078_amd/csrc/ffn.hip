@@ -180,11 +180,11 @@ __device__ __forceinline__ Tile row_tile(const int32_t* mbase, int S, int NT, lo
   return r;
 }
 
-// Weight-gradient tile t: tps = MT * NT tiles per slot.
-__device__ __forceinline__ Tile dw_tile(long long t, int tps, int MT) {
+// Weight-gradient tile t: tps = MT * NT tiles per slot, bands of gm row tiles.
+__device__ __forceinline__ Tile dw_tile(long long t, int tps, int MT, int gm = GM_DW) {
   Tile r;
   r.s = (int)(t / tps);
-  band_order((int)(t - (long long)r.s * tps), MT, tps / MT, GM_DW, r.m, r.n);
+  band_order((int)(t - (long long)r.s * tps), MT, tps / MT, gm, r.m, r.n);
   return r;
 }
 
@@ -1065,15 +1065,25 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X
   }
 }
 
-// dW_down = dO^T H (both read k-major).
+// dW_down = dO^T H (both read k-major).  Rows over d, columns over I.  A last
+// column tile with at most 128 columns left (I = 1408: 1280..1407) is computed
+// as a 256 x 128 tile (CBN): its slabs move 3/4 of a full tile's bytes and it
+// stores half the output, where a full tile would multiply and store a half
+// that is never written back.
+using CBN = B16Cfg<256, 128, 2, 4, 64, 3, 2>;
+// Band height of the dW_down tile order: the XCDs are dealt tiles t = 8 j + x,
+// so with 8 row tiles per band (d = 2048: the whole slot) the last column's 8
+// tiles of a band land on 8 different XCDs, one narrow tile each.
+constexpr int GM_DWD = 8;
+
 struct DwDTile {
   float* dwd;
   int m0, n0, K;
-  bool run;
+  bool run, narrow;
   B16Src A, B;
   __device__ __forceinline__ void init(const LayerPtrs<bf16>& W, cbp dO, cbp H, const DwArgs& da, long long t, int MT,
                                       int NT) {
-    Tile rt = dw_tile(t, MT * NT, MT);
+    Tile rt = dw_tile(t, MT * NT, MT, GM_DWD);
     rt.s = ld_scalar(da.dorder + rt.s);
     dwd = ld_scalar(W.dwd + rt.s);
     run = dwd != nullptr;
@@ -1081,11 +1091,62 @@ struct DwDTile {
     const int d = da.d, I = da.I;
     m0 = rt.m * CB::RA;
     n0 = rt.n * CB::RB;
+    narrow = I - n0 <= CBN::RB;
     K = sr.nrows;
     A = B16Src{dO + (size_t)sr.orow0 * d + m0, nullptr, d, d - m0, sr.nrows};
     B = B16Src{H + (size_t)sr.orow0 * I + n0, nullptr, I, I - n0, sr.nrows};
   }
+  __device__ __forceinline__ void prologue(FM_LDS char* l) const {
+    if (!run) return;
+    if (narrow) b16_prologue<CBN, false, false>(A, B, K, l);
+    else b16_prologue<CB, false, false>(A, B, K, l);
+  }
 };
+
+// One dW_down tile of shape C: the product (its prologue was issued with the
+// same shape), the hand-over of the next draw, the next tile's prologue, then
+// this tile's stores.  Every wave issues exactly DwEpi's store count (a 256 x 128
+// tile has half as many outputs; its other stores go to the sink), the number
+// the next product's first wait lets stay in flight.
+template <class C, bool ACCUM>
+__device__ __forceinline__ long long dwd_step(const LayerPtrs<bf16>& W, cbp dO, cbp H, const DwArgs& da,
+                                              const DwQueue& qu, FM_LDS char* l, const DwDTile& o, int next,
+                                              bool stored, int MT, int NT, float* sink) {
+  static_assert(C::MI * C::NJ * 4 <= DwEpi<ACCUM>::STORES || ACCUM, "store count");
+  const int d = da.d, I = da.I;
+  B16Acc<C::MI, C::NJ> acc;
+  if (o.run) {
+    acc.zero();
+    b16_gemm<C, false, false, false, false, DwEpi<ACCUM>::EXTRA>(o.A, o.B, o.K, l, acc, stored);
+  }
+  const int j = DwQueue::share(l, next);
+  barrier_lds();
+  const long long t = qu.tile(j);
+  if (t < qu.total) {
+    DwDTile on;
+    on.init(W, dO, H, da, t, MT, NT);
+    on.prologue(l);
+  }
+  if (o.run) {
+#pragma unroll
+    for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+      for (int jj = 0; jj < C::NJ; ++jj)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const AccCoord c = b16_coord<C>(i, jj, q);
+          const int m = o.m0 + c.row, n = o.n0 + c.col4;
+          float* dst = (m < d && n < I) ? o.dwd + (size_t)m * I + n : sink;
+          store_dw(dst, acc.quad(i, jj, q), ACCUM);
+        }
+    if (!ACCUM) {   // volatile: stores to one address must not be merged away
+      const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = C::MI * C::NJ * 4; u < DwEpi<ACCUM>::STORES; ++u) *(volatile FM_GLOBAL f32x4_t*)sink = z;
+    }
+  }
+  return t;
+}
 
 template <bool ACCUM>
 __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO, cbp H, DwArgs da) {
@@ -1101,7 +1162,7 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
   if (t < qu.total) {
     DwDTile o;
     o.init(W, dO, H, da, t, MT, NT);
-    if (o.run) b16_prologue<CB, false, false>(o.A, o.B, o.K, l);
+    o.prologue(l);
   }
   bool stored = false;
   while (t < qu.total) {
@@ -1112,33 +1173,10 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_d(LayerPtrs<bf16> W, cbp dO
 #pragma clang diagnostic pop
     DwDTile o;
     o.init(W, dO, H, da, t, MT, NT);
-    B16Acc<CB::MI, CB::NJ> acc;
-    if (o.run) {
-      acc.zero();
-      b16_gemm<CB, false, false, false, false, DwEpi<ACCUM>::EXTRA>(o.A, o.B, o.K, l, acc, stored);
-    }
-    j = DwQueue::share(l, next);
-    barrier_lds();
-    t = qu.tile(j);
-    if (t < qu.total) {
-      DwDTile on;
-      on.init(W, dO, H, da, t, MT, NT);
-      if (on.run) b16_prologue<CB, false, false>(on.A, on.B, on.K, l);
-    }
+    const long long tn = o.narrow ? dwd_step<CBN, ACCUM>(W, dO, H, da, qu, l, o, next, stored, MT, NT, sink)
+                                  : dwd_step<CB, ACCUM>(W, dO, H, da, qu, l, o, next, stored, MT, NT, sink);
     stored = o.run;
-    if (o.run) {
-#pragma unroll
-      for (int i = 0; i < CB::MI; ++i)
-#pragma unroll
-        for (int jj = 0; jj < CB::NJ; ++jj)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const AccCoord c = b16_coord<CB>(i, jj, q);
-            const int m = o.m0 + c.row, n = o.n0 + c.col4;
-            float* dst = (m < d && n < I) ? o.dwd + (size_t)m * I + n : sink;
-            store_dw(dst, acc.quad(i, jj, q), ACCUM);
-          }
-    }
+    t = tn;
   }
 }
 
