@@ -322,21 +322,23 @@ def layer_merging(reps=3, B_non=840, r=16, n_classes=32, mix=0.6, max_iter=100):
     return out
 
 
-def profiling_stack(reps=3):
-    """The quantised profiling pass of Section 4.1 over the 28-layer
-    DeepSeek-MoE stack (64 experts, d = 2048, I = 1408, top-6, T = 4096 tokens):
-    per layer int8 routing with the histogram on the RMS-normalised stream,
-    permute, the grouped SwiGLU forward straight from the int8 expert codes,
-    combine, and the residual add fused with the next layer's normalisation.  The
-    weights are drawn on the GPU (torch's seeded generator, the workload's
-    distributions) and quantised once; the pass is timed with HIP events per
-    stage, median over `reps` passes after one warm-up."""
+def profiling_stack(reps=3, workload="deepseek_stack"):
+    """The quantised profiling pass of Section 4.1 over a stack of layers: the
+    28-layer DeepSeek-MoE stack (64 experts, d = 2048, I = 1408, top-6, T = 4096
+    tokens), or the one LLaMA-MoE layer whose profiling pass uses int8 router and
+    expert weights (16 experts, d = 4096, I = 688, top-4, T = 4096): per layer
+    int8 routing with the histogram on the RMS-normalised stream, permute, the
+    grouped SwiGLU forward straight from the int8 expert codes, combine, and the
+    residual add fused with the next layer's normalisation.  The weights are
+    drawn on the GPU (torch's seeded generator, the workload's distributions)
+    and quantised once; the pass is timed with HIP events per stage, median over
+    `reps` passes after one warm-up."""
     import numpy as np
     import torch
     from paper_2508_19078_amd import workloads as W
     from paper_2508_19078_amd.profiling import QuantizedStack
 
-    w = W.WORKLOADS["deepseek_stack"]
+    w = W.WORKLOADS[workload]
     dev = torch.device("cuda")
     L, E, d, I, T, k = w.n_layers, w.E, w.d, w.I, w.T, w.k
     g = torch.Generator(device=dev)
@@ -396,8 +398,8 @@ def profiling_stack(reps=3):
     counts = qs.counts.cpu().numpy()
     # the grouped forward's algorithmic flops: 6 d I per routed row (T k rows per layer; no shared experts)
     ffn_flops = 6.0 * d * I * T * k * L
-    out = {"workload": f"deepseek_stack: {L} layers x {E} experts, d={d} I={I}, T={T}, top-{k}, int8 router "
-                       "and experts (per-row scales), RMS-normalised layer inputs, residual stream",
+    out = {"workload": f"{w.name}: {L} layer{'s' if L > 1 else ''} x {E} experts, d={d} I={I}, T={T}, top-{k}, "
+                       "int8 router and experts (per-row scales), RMS-normalised layer inputs, residual stream",
            "pass_ms": round(total, 3), "tokens_per_s": round(T / (total * 1e-3), 1),
            "graph_pass_ms": round(graph_ms, 3),
            "stages_ms": stages, "quantise_ms": round(quant_ms, 3),
@@ -539,8 +541,10 @@ def main():
         print("# layer-aware merging over the 28-layer stack", file=sys.stderr, flush=True)
         out["layer_merging"] = layer_merging()
     if not a.no_profiling:
-        print("# quantised profiling pass over the 28-layer stack", file=sys.stderr, flush=True)
-        out["profiling_stack"] = profiling_stack()
+        # the LLaMA-MoE layer's own int8 profiling pass; the 28-layer DeepSeek-MoE stack otherwise
+        pw = "llama_moe" if a.workload == "llama_moe" else "deepseek_stack"
+        print(f"# quantised profiling pass ({pw})", file=sys.stderr, flush=True)
+        out["profiling_stack"] = profiling_stack(workload=pw)
     if a.calib_copy:
         src = torch.ones(128 << 20, dtype=torch.bfloat16, device="cuda")
         dst = torch.empty_like(src)
