@@ -26,9 +26,9 @@
 //   transposed on the way in.  A 32-lane read touches four 64-byte k-rows, 32
 //   bytes of each, which already covers the 64 banks once.
 // * Fragments are read one 16-k step ahead of the MFMAs that use them, into a
-//   second register set; at the end of a slab the read-ahead crosses into the
-//   next slab right after the barrier that publishes it.  LDS reads thus
-//   overlap the MFMAs of the same wave, not only those of the other wave.
+//   second register set.  In the steady state the two waves of each SIMD take
+//   turns: one issues a k-step's MFMAs while the other reads its next
+//   fragments and issues refills, a block barrier between turns (see b16_gemm).
 // * An operand may interleave two matrices in 32-row blocks (gate and up
 //   weights; the two dSwiGLU gradients), so that the pairs the epilogue needs sit
 //   in one lane.  A DMA instruction always stays inside one 32-row block.
@@ -499,14 +499,22 @@ __device__ __forceinline__ void barrier_lds_writes() {
 // DMA instruction issued before A(kt + NSA - 1) has landed: the waits count the
 // A instructions issued after B(kt + 1) (s_waitcnt vmcnt is in issue order).
 //
-// Steady state (slab kt, while both refills are whole slabs): every k-step but
-// the last reads the next k-step's fragments, then multiplies.  The last k-step
-// multiplies half of its tiles, waits for its own LDS reads and for slab kt + 1,
-// crosses the barrier that publishes slab kt + 1 and frees slab kt's buffers,
-// issues the refills, reads the first fragments of slab kt + 1 and multiplies
-// the other half, which hides the read latency.  The loop body is straight-line
-// code, so the LDS-read wait counts stay exact.  The last slabs (and the partial
-// one) drain through a general version of the same step.
+// Steady state (slab kt, while both refills are whole slabs): the two waves of
+// each SIMD take turns on its matrix pipe.  Group P (waves 0 .. NW/2-1) and
+// group Q (the others, one per SIMD) run the same straight-line loop one
+// block barrier apart: Q passes one extra barrier before the loop, P one after
+// it.  The loop alternates an MFMA burst (the 8 products of one k-step) with
+// the next k-step's fragment reads plus a share of the refills, a barrier
+// after each, so while P multiplies Q reads and the other way round, and
+// neither wave runs a slab's last k-steps alone.  (Left to the hardware, the
+// first wave of a SIMD took the pipe for whole bursts and finished its k-steps
+// about 800 clocks per slab before the second, which then could not keep the
+// pipe busy by itself.)  Each wave's reads, MFMAs and refills keep their order
+// (accumulation order and vmcnt counting as before).  The slab's buffers are
+// released by the barrier after P's last burst, which is the barrier after Q's
+// last reads: both of those phases end with the wave's reads of the slab and
+// its DMA of the next slab complete.  The last slabs (and the partial one)
+// drain through a general version of the step with every wave in step.
 // The DMA side of one product: slab issue into the two rings.
 template <class C, bool AKC, bool BKC, bool AI, bool BI> struct B16Pipe {
   static constexpr int BK = C::BK, NSA = C::NSA, NSB = C::NSB;
@@ -605,7 +613,6 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
     }
   };
   constexpr int LAST = (KS - 1) & 1;           // register set of the last k-step
-  constexpr int HALF = MI / 2;
 
   if (EXTRA < 0) pp.prologue();
   // slab 0 is complete once everything issued after A(0) is at most in flight
@@ -624,38 +631,45 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
 
   int kt = 0;
   const int nsteady = nfull - NSA;             // refills A(kt + NSA), B(kt + NSB) whole
-  // The refills issued at the end of slab kt are spread over slab kt + 1: all
-  // eight waves issuing 64 KB at once stall on the address unit for about a
-  // thousand cycles.  B(kt + 2) goes out in the first half of the next slab
-  // (it is needed at its end), A(kt + 3) in the second half.
-  static_assert(KS == 4 && PA % 2 == 0 && PB % 2 == 0, "refill spread over four k-steps");
+  // Per slab each wave issues B(kt + 1)'s second half, A(kt + 2) in two
+  // halves, and after the slab barrier B(kt + 2)'s first half, the order the
+  // slab-end wait (at most A(kt + 2) in flight) counts on.  Spreading them over
+  // the read phases keeps all eight waves from stalling on the address unit at
+  // once.
+  static_assert(KS == 4 && PA % 2 == 0 && PB % 2 == 0, "refills spread over the read phases");
+  const bool P = wave < C::NW / 2;
+  auto bar = [&]() { sched_fence(); barrier_lds(); sched_fence(); };
+  if (nsteady > 0 && !P) bar();
   for (; kt < nsteady; ++kt) {
-    if (kt > 0) {
-      db.template issue_part<PB / 2, PB>(kt + NSB - 1, bbuf(kt + NSB - 1));
-    }
-#pragma unroll
-    for (int ks = 0; ks + 1 < KS; ++ks) {
-      read((ks & 1) ^ 1, kt, ks + 1);
-      sched_fence();
-      if (kt > 0) {
-        if (ks == 0) da.template issue_part<0, PA / 2>(kt + NSA - 1, abuf(kt + NSA - 1));
-        if (ks == 1) da.template issue_part<PA / 2, PA>(kt + NSA - 1, abuf(kt + NSA - 1));
-      }
-      sched_fence();
-      mma(ks & 1, 0, MI, false, 0, 0);
-      sched_fence();
-    }
-    mma(LAST, 0, HALF, false, 0, 0);
+    const bool ref = kt > 0;
+    mma(0, 0, MI, false, 0, 0);
+    bar();
+    read(1, kt, 1);
+    if (ref) db.template issue_part<PB / 2, PB>(kt + NSB - 1, bbuf(kt + NSB - 1));
+    bar();
+    mma(1, 0, MI, false, 0, 0);
+    bar();
+    read(0, kt, 2);
+    if (ref) da.template issue_part<0, PA / 2>(kt + NSA - 1, abuf(kt + NSA - 1));
+    bar();
+    mma(0, 0, MI, false, 0, 0);
+    bar();
+    read(1, kt, 3);
+    if (ref) da.template issue_part<PA / 2, PA>(kt + NSA - 1, abuf(kt + NSA - 1));
     sched_fence();
     wait_lgkm0();
     wait_vmcnt<PA>();                          // A(kt + NSA - 1) may still be in flight
-    barrier_lds();
+    bar();                                     // Q: the slab barrier
+    mma(1, 0, MI, false, 0, 0);
+    sched_fence();
+    wait_lgkm0();
+    wait_vmcnt<PA>();
+    bar();                                     // P: the slab barrier
     db.template issue_part<0, PB / 2>(kt + NSB, bbuf(kt + NSB));
-    read(LAST ^ 1, kt + 1, 0);
-    sched_fence();
-    mma(LAST, HALF, MI, false, 0, 0);
-    sched_fence();
+    read(0, kt + 1, 0);
+    bar();
   }
+  if (nsteady > 0 && P) bar();
   // Refills still owed by the last steady slab.
   if (kt > 0 && kt == nsteady) {
     db.template issue_part<PB / 2, PB>(kt + NSB - 1, bbuf(kt + NSB - 1));
