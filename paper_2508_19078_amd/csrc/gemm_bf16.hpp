@@ -503,9 +503,9 @@ __device__ __forceinline__ void barrier_lds_writes() {
 // each SIMD take turns on its matrix pipe.  Group P (waves 0 .. NW/2-1) and
 // group Q (the others, one per SIMD) run the same straight-line loop one
 // block barrier apart: Q passes one extra barrier before the loop, P one after
-// it.  The loop alternates an MFMA burst (the 8 products of one k-step) with
-// the next k-step's fragment reads plus a share of the refills, a barrier
-// after each, so while P multiplies Q reads and the other way round, and
+// it.  The loop alternates an MFMA burst (the 16 products of two k-steps) with
+// the next two k-steps' fragment reads plus the refills, a barrier after each
+// (four per slab), so while P multiplies Q reads and the other way round, and
 // neither wave runs a slab's last k-steps alone.  (Left to the hardware, the
 // first wave of a SIMD took the pipe for whole bursts and finished its k-steps
 // about 800 clocks per slab before the second, which then could not keep the
@@ -631,50 +631,44 @@ __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K
 
   int kt = 0;
   const int nsteady = nfull - NSA;             // refills A(kt + NSA), B(kt + NSB) whole
-  // Per slab each wave issues B(kt + 1)'s second half, A(kt + 2) in two
-  // halves, and after the slab barrier B(kt + 2)'s first half, the order the
-  // slab-end wait (at most A(kt + 2) in flight) counts on.  Spreading them over
-  // the read phases keeps all eight waves from stalling on the address unit at
-  // once.
-  static_assert(KS == 4 && PA % 2 == 0 && PB % 2 == 0, "refills spread over the read phases");
+  // Per slab each wave issues A(kt + 2) with its reads of k-steps 2 and 3, and
+  // B(kt + 2) right after the slab barrier that frees B's buffer, so that the
+  // slab-end wait (at most A(kt + 2) in flight) finds B(kt + 1) issued a whole
+  // read phase and burst earlier.
+  static_assert(KS == 4, "two k-steps per burst");
   const bool P = wave < C::NW / 2;
   auto bar = [&]() { sched_fence(); barrier_lds(); sched_fence(); };
+  if (nsteady > 0) read(1, 0, 1);              // the first burst multiplies k-steps 0 and 1
   if (nsteady > 0 && !P) bar();
   for (; kt < nsteady; ++kt) {
-    const bool ref = kt > 0;
+    // 1: k-steps 0 and 1
     mma(0, 0, MI, false, 0, 0);
-    bar();
-    read(1, kt, 1);
-    if (ref) db.template issue_part<PB / 2, PB>(kt + NSB - 1, bbuf(kt + NSB - 1));
-    bar();
     mma(1, 0, MI, false, 0, 0);
     bar();
+    // 2: read k-steps 2 and 3; A(kt + 2); this slab's reads and the next slab's DMA done
     read(0, kt, 2);
-    if (ref) da.template issue_part<0, PA / 2>(kt + NSA - 1, abuf(kt + NSA - 1));
-    bar();
-    mma(0, 0, MI, false, 0, 0);
-    bar();
     read(1, kt, 3);
-    if (ref) da.template issue_part<PA / 2, PA>(kt + NSA - 1, abuf(kt + NSA - 1));
+    if (kt > 0) da.issue_full(kt + NSA - 1, abuf(kt + NSA - 1));
     sched_fence();
     wait_lgkm0();
     wait_vmcnt<PA>();                          // A(kt + NSA - 1) may still be in flight
     bar();                                     // Q: the slab barrier
+    // 3: k-steps 2 and 3
+    mma(0, 0, MI, false, 0, 0);
     mma(1, 0, MI, false, 0, 0);
     sched_fence();
     wait_lgkm0();
     wait_vmcnt<PA>();
     bar();                                     // P: the slab barrier
-    db.template issue_part<0, PB / 2>(kt + NSB, bbuf(kt + NSB));
+    // 4: B(kt + 2) into this slab's B buffer; the next slab's k-steps 0 and 1
+    db.issue_full(kt + NSB, bbuf(kt + NSB));
     read(0, kt + 1, 0);
+    read(1, kt + 1, 1);
     bar();
   }
   if (nsteady > 0 && P) bar();
   // Refills still owed by the last steady slab.
-  if (kt > 0 && kt == nsteady) {
-    db.template issue_part<PB / 2, PB>(kt + NSB - 1, bbuf(kt + NSB - 1));
-    da.issue_full(kt + NSA - 1, abuf(kt + NSA - 1));
-  }
+  if (kt > 0 && kt == nsteady) da.issue_full(kt + NSA - 1, abuf(kt + NSA - 1));
   // Drain: the slabs whose refills pass the end, and the partial slab.
   for (; kt < nk; ++kt) {
     const bool tail = kt >= nfull;
