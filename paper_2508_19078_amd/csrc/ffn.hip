@@ -925,8 +925,10 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
   }
 }
 
-// dX_s = dA_g W_gate + dA_u W_up (two K passes, B read k-major), one tile of
-// shape C at rows m0 of slot s, columns n0.
+// dX_s = dA_g W_gate + dA_u W_up (B read k-major), one tile of shape C at rows
+// m0 of slot s, columns n0.  With I a whole number of slabs the two products
+// run as one K loop of 2I (one prologue and one drain per tile); otherwise as
+// two K passes.  Either way k runs over dA_g W_gate first: the same sums.
 template <class C>
 __device__ __forceinline__ void dx_tile(const LayerPtrs<bf16>& W, cbp dAg, cbp dAu, const RowArgs& ra,
                                         FM_LDS char* lds, int s, int m0, int n0, bf16* dXp) {
@@ -938,10 +940,17 @@ __device__ __forceinline__ void dx_tile(const LayerPtrs<bf16>& W, cbp dAg, cbp d
   B16Acc<C::MI, C::NJ> acc;
   acc.zero();
   // B(n = hidden index, k = intermediate index) = W_gate[k][n], then W_up
-  b16_gemm<C, true, false>(B16Src{dAg + ob * ra.ldA, nullptr, ra.ldA, rows, I},
-                           B16Src{ld_scalar(W.wg + s) + n0, nullptr, d, cols, I}, I, lds, acc);
-  b16_gemm<C, true, false>(B16Src{dAu + ob * ra.ldA, nullptr, ra.ldA, rows, I},
-                           B16Src{ld_scalar(W.wu + s) + n0, nullptr, d, cols, I}, I, lds, acc);
+  cbp wg = ld_scalar(W.wg + s) + n0, wu = ld_scalar(W.wu + s) + n0;
+  if (I % C::BK == 0) {
+    b16_gemm<C, true, false, false, false, -1, true>(
+        B16Src{dAg + ob * ra.ldA, nullptr, ra.ldA, rows, 2 * I, dAu + ob * ra.ldA, I},
+        B16Src{wg, nullptr, d, cols, 2 * I, wu, I}, 2 * I, lds, acc);
+  } else {
+    b16_gemm<C, true, false>(B16Src{dAg + ob * ra.ldA, nullptr, ra.ldA, rows, I},
+                             B16Src{wg, nullptr, d, cols, I}, I, lds, acc);
+    b16_gemm<C, true, false>(B16Src{dAu + ob * ra.ldA, nullptr, ra.ldA, rows, I},
+                             B16Src{wu, nullptr, d, cols, I}, I, lds, acc);
+  }
   b16_store_staged<C>(acc, lds, dXp + ob * d + n0, d, rows, cols);
 }
 

@@ -153,13 +153,17 @@ __device__ __forceinline__ int swz_kc(int row) { return (row >> 2) & 3; }
 // the tile origin.  With p2 set, the logical rows alternate in blocks of 32
 // between p (even blocks) and p2 (odd blocks): logical row r is physical row
 // 32 (r / 64) + r % 32 of matrix (r / 32) % 2.  rows = physical rows valid from
-// the origin (per matrix).
+// the origin (per matrix).  With pk set (a product run with KJ), k >= kj reads
+// the matrix at pk (same layout and ld) at k - kj: two products summed into one
+// accumulator as a single K loop; kj is a whole number of slabs.
 struct B16Src {
   const bf16* p;
   const bf16* p2;
   int ld;
   int rows;
   int K;
+  const bf16* pk;
+  int kj;
 };
 
 __device__ __forceinline__ const bf16* b16_row(const B16Src& s, int r, int& pr) {
@@ -179,11 +183,14 @@ __device__ __forceinline__ const bf16* b16_row(const B16Src& s, int r, int& pr) 
 //       block's k-rows; CB = R / 32 column blocks.
 // Consecutive instructions of a wave cover the two 64-byte halves of the same
 // 16 lines.  Each takes a uniform 64-bit base plus a 32-bit per-lane offset.
-template <bool KC, int R, int NI, bool INTER> struct B16Dma {
+template <bool KC, int R, int NI, bool INTER, bool KJ = false> struct B16Dma {
   static constexpr int CB = R / 32;
+  static_assert(!(KJ && INTER), "one second matrix");
   const char* base[NI];      // uniform
   uint32_t off[NI];          // per lane
   size_t step;
+  size_t jump;               // KJ: added to the address of slabs nj and later
+  int nj;
 
   // Column block of an MN instruction.  With two interleaved matrices the
   // blocks of one matrix alternate, so consecutive instructions take blocks
@@ -229,6 +236,10 @@ template <bool KC, int R, int NI, bool INTER> struct B16Dma {
       off[u] = lane_off(s, ins, lane, 0);
     }
     step = KC ? (size_t)64 * 2 : (size_t)64 * s.ld * 2;
+    if (KJ) {
+      nj = s.kj / 64;
+      jump = (size_t)((uintptr_t)s.pk - (uintptr_t)s.p) - step * (size_t)nj;
+    }
   }
 
   __device__ __forceinline__ static int lds_block(int ins) {
@@ -240,7 +251,7 @@ template <bool KC, int R, int NI, bool INTER> struct B16Dma {
   template <int U0, int U1>
   __device__ __forceinline__ void issue_part(int slab, FM_LDS char* tile) const {
     const int wave = wave_id();
-    const size_t adv = step * (size_t)slab;
+    const size_t adv = step * (size_t)slab + (KJ && slab >= nj ? jump : 0);
 #pragma unroll
     for (int u = U0; u < U1; ++u) dma16s(base[u] + adv, off[u], tile + lds_block(wave * NI + u) * 1024);
   }
@@ -253,8 +264,10 @@ template <bool KC, int R, int NI, bool INTER> struct B16Dma {
 #pragma unroll
     for (int u = 0; u < NI; ++u) {
       const int ins = wave * NI + u;
-      const bf16* m = matrix(s, ins);
-      const char* bt = (const char*)(KC ? m + k0 : m + (size_t)k0 * s.ld);
+      const bool second = KJ && k0 >= s.kj;
+      const bf16* m = second ? s.pk : matrix(s, ins);
+      const int km = second ? k0 - s.kj : k0;
+      const char* bt = (const char*)(KC ? m + km : m + (size_t)km * s.ld);
       dma16s(bt, lane_off(s, ins, lane, k0), tile + lds_block(ins) * 1024);
     }
   }
@@ -516,11 +529,12 @@ __device__ __forceinline__ void barrier_lds_writes() {
 // its DMA of the next slab complete.  The last slabs (and the partial one)
 // drain through a general version of the step with every wave in step.
 // The DMA side of one product: slab issue into the two rings.
-template <class C, bool AKC, bool BKC, bool AI, bool BI> struct B16Pipe {
+template <class C, bool AKC, bool BKC, bool AI, bool BI, bool KJ = false> struct B16Pipe {
   static constexpr int BK = C::BK, NSA = C::NSA, NSB = C::NSB;
   static_assert(C::BE == 2 || BKC, "int8 B is K-contiguous");
-  using DmaB = std::conditional_t<C::BE == 1, I8Dma<C::RB, C::B_INS, BI>, B16Dma<BKC, C::RB, C::B_INS, BI>>;
-  B16Dma<AKC, C::RA, C::A_INS, AI> da;
+  static_assert(C::BE == 2 || !KJ, "bf16 operands only");
+  using DmaB = std::conditional_t<C::BE == 1, I8Dma<C::RB, C::B_INS, BI>, B16Dma<BKC, C::RB, C::B_INS, BI, KJ>>;
+  B16Dma<AKC, C::RA, C::A_INS, AI, KJ> da;
   DmaB db;
   const B16Src& A;
   const B16Src& B;
@@ -569,15 +583,15 @@ __device__ __forceinline__ void b16_prologue(const B16Src& A, const B16Src& B, i
 // EXTRA < 0: the product issues its own prologue.  EXTRA >= 0: b16_prologue
 // issued it already (same A, B, K); with extra_issued the wave has issued at
 // least EXTRA more vector-memory instructions since, which may stay in flight
-// at the first wait.
-template <class C, bool AKC, bool BKC, bool AI = false, bool BI = false, int EXTRA = -1>
+// at the first wait.  KJ: A and B switch to their second matrices (pk) at k = kj.
+template <class C, bool AKC, bool BKC, bool AI = false, bool BI = false, int EXTRA = -1, bool KJ = false>
 __device__ __forceinline__ void b16_gemm(const B16Src& A, const B16Src& B, int K, FM_LDS char* lds,
                                          B16Acc<C::MI, C::NJ>& acc, bool extra_issued = true) {
   constexpr int BK = C::BK, NSA = C::NSA, NSB = C::NSB, KS = C::KS, MI = C::MI, NJ = C::NJ;
   constexpr int PA = C::A_INS, PB = C::B_INS;   // DMA instructions per wave and slab
   constexpr int XW = EXTRA < 0 ? 0 : EXTRA;
   static_assert((NSB - 1) * (PA + PB) + PA + XW < 64, "vmcnt range");
-  const B16Pipe<C, AKC, BKC, AI, BI> pp(A, B, K, lds);
+  const B16Pipe<C, AKC, BKC, AI, BI, KJ> pp(A, B, K, lds);
   const int nk = pp.nk;
   if (nk <= 0) return;
   const int nfull = pp.nfull;
