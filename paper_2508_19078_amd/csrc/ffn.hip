@@ -771,79 +771,122 @@ __device__ __forceinline__ f32x4_t scale4(const float* s, int col, int n) {
 // H = silu(s_g (X_s Q_g^T)) (s_u (X_s Q_u^T)) with int8 Q_g, Q_u interleaved
 // in 32-row blocks as in kb_gate_up; the row scales of the weights scale the
 // output columns.  Only H is written (no backward follows this forward).
+// One such tile of shape C at rows m0 of slot s, intermediate columns n0.
+template <class C>
+__device__ __forceinline__ void q8_gate_up_tile(const Q8Ptrs& W, cbp X, cbp Xp, const RowArgs& ra, FM_LDS char* lds,
+                                                int s, int m0, int n0, bf16* H) {
+  const int d = ra.d, I = ra.I;
+  const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+  const int rows = sr.nrows - m0, cols = I - n0;
+  if (rows <= 0 || cols <= 0) return;
+  const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, rows, d};
+  // byte pointers in the B16Src fields: ld and K count bytes
+  const B16Src B{(cbp)(ld_scalar(W.qg + s) + (size_t)n0 * d), (cbp)(ld_scalar(W.qu + s) + (size_t)n0 * d), d, cols,
+                 d};
+  B16Acc<C::MI, C::NJ> acc;
+  acc.zero();
+  b16_gemm<C, true, true, false, true>(A, B, d, lds, acc);
+  const float* sgp = ld_scalar(W.sg + s) + n0;
+  const float* sup = ld_scalar(W.su + s) + n0;
+  using SG = Stage<bf16, C::RB / 2>;
+  const size_t ob = (size_t)(sr.orow0 + m0);
+#pragma unroll
+  for (int jj = 0; jj < C::NJ / 2; ++jj)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int col = deinter(b16_coord<C>(0, 2 * jj, q).col4);
+      const f32x4_t cg = scale4(sgp, col, cols), cu = scale4(sup, col, cols);
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i) {
+        const AccCoord c = b16_coord<C>(i, 2 * jj, q);
+        const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
+        f32x4_t h;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float a = ag[r] * cg[r];
+          h[r] = a * sigm_fast(a) * (u[r] * cu[r]);
+        }
+        SG::put4(lds, c.row, col, h);
+      }
+    }
+  barrier_lds_writes();
+  SG::template copy_out<C::RA, C::THREADS>(lds, H + ob * I + n0, I, rows, cols);
+  barrier_lds();
+}
+
+// A 128-row int8 tile (same waves and slab depth): the last row tile of a slot
+// with at most 128 rows left, and the row halves of a last round.
+using CQH = B16Cfg<128, 256, 2, 4, 64, 3, 2, 1>;
+
+// Rows of slot s from row m0 on.
+__device__ __forceinline__ int rows_left(const RowArgs& ra, int s, int m0) {
+  return slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k).nrows - m0;
+}
+
+// The int8 gate-up product: rounds of whole tiles per XCD as in kb_gate_up, a
+// tile with at most 128 rows left taken as a 128-row tile.
 __global__ __launch_bounds__(CQ::THREADS) void kq_gate_up(Q8Ptrs W, cbp X, cbp Xp, RowArgs ra, bf16* H) {
   __shared__ __align__(16) char lds[CQ::LDS];
-  const int d = ra.d, I = ra.I, NT = (I + CQ::RB / 2 - 1) / (CQ::RB / 2);
+  FM_LDS char* const l = (FM_LDS char*)lds;
+  const int NT = (ra.I + CQ::RB / 2 - 1) / (CQ::RB / 2);
   const TileRange tr = row_range(ra, NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+  const LastRound lr = last_round(tr, false);
+  for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
     const int m0 = rt.m * CQ::RA, n0 = rt.n * (CQ::RB / 2);
-    const B16Src A{(sr.shared ? X : Xp) + (size_t)(sr.xrow0 + m0) * d, nullptr, d, sr.nrows - m0, d};
-    // byte pointers in the B16Src fields: ld and K count bytes
-    const B16Src B{(cbp)(ld_scalar(W.qg + rt.s) + (size_t)n0 * d), (cbp)(ld_scalar(W.qu + rt.s) + (size_t)n0 * d),
-                   d, I - n0, d};
-    B16Acc<CQ::MI, CQ::NJ> acc;
-    acc.zero();
-    b16_gemm<CQ, true, true, false, true>(A, B, d, (FM_LDS char*)lds, acc);
-    const float* sgp = ld_scalar(W.sg + rt.s) + n0;
-    const float* sup = ld_scalar(W.su + rt.s) + n0;
-    using SG = Stage<bf16, CQ::RB / 2>;
-    FM_LDS char* sg = (FM_LDS char*)lds;
-    const size_t ob = (size_t)(sr.orow0 + m0);
-    const int rows = sr.nrows - m0, cols = I - n0;
-#pragma unroll
-    for (int jj = 0; jj < CQ::NJ / 2; ++jj)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int col = deinter(b16_coord<CQ>(0, 2 * jj, q).col4);
-        const f32x4_t cg = scale4(sgp, col, cols), cu = scale4(sup, col, cols);
-#pragma unroll
-        for (int i = 0; i < CQ::MI; ++i) {
-          const AccCoord c = b16_coord<CQ>(i, 2 * jj, q);
-          const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
-          f32x4_t h;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float a = ag[r] * cg[r];
-            h[r] = a * sigm_fast(a) * (u[r] * cu[r]);
-          }
-          SG::put4(sg, c.row, col, h);
-        }
-      }
-    barrier_lds_writes();
-    SG::template copy_out<CQ::RA, CQ::THREADS>(sg, H + ob * I + n0, I, rows, cols);
-    barrier_lds();
+    if (rows_left(ra, rt.s, m0) <= CQH::RA) q8_gate_up_tile<CQH>(W, X, Xp, ra, l, rt.s, m0, n0, H);
+    else q8_gate_up_tile<CQ>(W, X, Xp, ra, l, rt.s, m0, n0, H);
+  }
+  if (lr.parts && tr.first < (tr.hi - lr.cut) * 2) {   // a row half of the last round
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / 2);
+    q8_gate_up_tile<CQH>(W, X, Xp, ra, l, rt.s, rt.m * CQ::RA + (tr.first % 2) * CQH::RA, rt.n * (CQ::RB / 2), H);
   }
 }
 
-// O = s_d (H Q_d^T) with int8 Q_d.
+// One int8-weight down tile of shape C: O = s_d (H Q_d^T).
+template <class C>
+__device__ __forceinline__ void q8_down_tile(const Q8Ptrs& W, cbp H, const RowArgs& ra, FM_LDS char* lds, int s,
+                                             int m0, int n0, bf16* O) {
+  const int d = ra.d, I = ra.I;
+  const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
+  const int rows = sr.nrows - m0, cols = d - n0;
+  if (rows <= 0 || cols <= 0) return;
+  const size_t ob = (size_t)(sr.orow0 + m0);
+  const B16Src A{H + ob * I, nullptr, I, rows, I};
+  const B16Src B{(cbp)(ld_scalar(W.qd + s) + (size_t)n0 * I), nullptr, I, cols, I};
+  B16Acc<C::MI, C::NJ> acc;
+  acc.zero();
+  b16_gemm<C, true, true>(A, B, I, lds, acc);
+  const float* sdp = ld_scalar(W.sd + s) + n0;
+#pragma unroll
+  for (int j = 0; j < C::NJ; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const f32x4_t c4 = scale4(sdp, b16_coord<C>(0, j, q).col4, cols);
+#pragma unroll
+      for (int i = 0; i < C::MI; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc.v[i][j][4 * q + r] *= c4[r];
+    }
+  b16_store_staged<C>(acc, lds, O + ob * d + n0, d, rows, cols);
+}
+
+// O = s_d (H Q_d^T) with int8 Q_d; tiles as in kq_gate_up.
 __global__ __launch_bounds__(CQ::THREADS) void kq_down(Q8Ptrs W, cbp H, RowArgs ra, bf16* O) {
   __shared__ __align__(16) char lds[CQ::LDS];
-  const int d = ra.d, I = ra.I, NT = (d + CQ::RB - 1) / CQ::RB;
+  FM_LDS char* const l = (FM_LDS char*)lds;
+  const int NT = (ra.d + CQ::RB - 1) / CQ::RB;
   const TileRange tr = row_range(ra, NT);
-  for (long long t = tr.lo + tr.first; t < tr.hi; t += tr.step) {
+  const LastRound lr = last_round(tr, false);
+  for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    const SlotRows sr = slot_rows(rt.s, ra.offsets, ra.S_r, ra.Tn, ra.k);
     const int m0 = rt.m * CQ::RA, n0 = rt.n * CQ::RB;
-    const size_t ob = (size_t)(sr.orow0 + m0);
-    const B16Src A{H + ob * I, nullptr, I, sr.nrows - m0, I};
-    const B16Src B{(cbp)(ld_scalar(W.qd + rt.s) + (size_t)n0 * I), nullptr, I, d - n0, I};
-    B16Acc<CQ::MI, CQ::NJ> acc;
-    acc.zero();
-    b16_gemm<CQ, true, true>(A, B, I, (FM_LDS char*)lds, acc);
-    const float* sdp = ld_scalar(W.sd + rt.s) + n0;
-#pragma unroll
-    for (int j = 0; j < CQ::NJ; ++j)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const f32x4_t c4 = scale4(sdp, b16_coord<CQ>(0, j, q).col4, d - n0);
-#pragma unroll
-        for (int i = 0; i < CQ::MI; ++i)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc.v[i][j][4 * q + r] *= c4[r];
-      }
-    b16_store_staged<CQ>(acc, (FM_LDS char*)lds, O + ob * d + n0, d, sr.nrows - m0, d - n0);
+    if (rows_left(ra, rt.s, m0) <= CQH::RA) q8_down_tile<CQH>(W, H, ra, l, rt.s, m0, n0, O);
+    else q8_down_tile<CQ>(W, H, ra, l, rt.s, m0, n0, O);
+  }
+  if (lr.parts && tr.first < (tr.hi - lr.cut) * 2) {   // a row half of the last round
+    const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / 2);
+    q8_down_tile<CQH>(W, H, ra, l, rt.s, rt.m * CQ::RA + (tr.first % 2) * CQH::RA, rt.n * CQ::RB, O);
   }
 }
 
