@@ -240,6 +240,12 @@ struct DwArgs {
 
 // The range of the tile space handled by this block's XCD, and the block's
 // first tile and stride inside it.
+// Rows of slot s from row m0 on (a row tile with at most half a tile's rows
+// left runs as a half-height tile).
+__device__ __forceinline__ int rows_left(const RowArgs& ra, int s, int m0) {
+  return slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k).nrows - m0;
+}
+
 struct TileRange {
   long long lo, hi;
   int first, step;
@@ -738,7 +744,10 @@ __global__ __launch_bounds__(CB::THREADS) void kb_gate_up(LayerPtrs<bf16> W, cbp
   const LastRound lr = last_round(tr, false);
   for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    gate_up_tile<CB>(W, X, Xp, ra, l, rt.s, rt.m * CB::RA, rt.n * (CB::RB / 2), Ag, Au, H);
+    if (rows_left(ra, rt.s, rt.m * CB::RA) <= CBH::RA)
+      gate_up_tile<CBH>(W, X, Xp, ra, l, rt.s, rt.m * CB::RA, rt.n * (CB::RB / 2), Ag, Au, H);
+    else
+      gate_up_tile<CB>(W, X, Xp, ra, l, rt.s, rt.m * CB::RA, rt.n * (CB::RB / 2), Ag, Au, H);
   }
   if (lr.parts && tr.first < (tr.hi - lr.cut) * 2) {   // a row half of the last round
     const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / 2);
@@ -817,11 +826,6 @@ __device__ __forceinline__ void q8_gate_up_tile(const Q8Ptrs& W, cbp X, cbp Xp, 
 // A 128-row int8 tile (same waves and slab depth): the last row tile of a slot
 // with at most 128 rows left, and the row halves of a last round.
 using CQH = B16Cfg<128, 256, 2, 4, 64, 3, 2, 1>;
-
-// Rows of slot s from row m0 on.
-__device__ __forceinline__ int rows_left(const RowArgs& ra, int s, int m0) {
-  return slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k).nrows - m0;
-}
 
 // The int8 gate-up product: rounds of whole tiles per XCD as in kb_gate_up, a
 // tile with at most 128 rows left taken as a 128-row tile.
@@ -915,7 +919,10 @@ __global__ __launch_bounds__(CB::THREADS) void kb_down(LayerPtrs<bf16> W, cbp H,
   const LastRound lr = last_round(tr, true);
   for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    down_tile<CB>(W, H, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, O);
+    if (rows_left(ra, rt.s, rt.m * CB::RA) <= CBH::RA)
+      down_tile<CBH>(W, H, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, O);
+    else
+      down_tile<CB>(W, H, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, O);
   }
   if (lr.parts && tr.first < (tr.hi - lr.cut) * lr.parts) {   // a piece of the last round
     const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / lr.parts);
@@ -959,7 +966,10 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
   const LastRound lr = last_round(tr, false);
   for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    dh_tile<CB>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA, rt.n, NT, dAg, dAu, norms);
+    if (rows_left(ra, rt.s, rt.m * CB::RA) <= CBH::RA)
+      dh_tile<CBH>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA, rt.n, NT, dAg, dAu, norms);
+    else
+      dh_tile<CB>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA, rt.n, NT, dAg, dAu, norms);
   }
   if (lr.parts && tr.first < (tr.hi - lr.cut) * 2) {   // a row half of the last round
     const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / 2);
@@ -1006,7 +1016,10 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dx(LayerPtrs<bf16> W, cbp dAg,
   const LastRound lr = last_round(tr, true);
   for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    dx_tile<CB>(W, dAg, dAu, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, dXp);
+    if (rows_left(ra, rt.s, rt.m * CB::RA) <= CBH::RA)
+      dx_tile<CBH>(W, dAg, dAu, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, dXp);
+    else
+      dx_tile<CB>(W, dAg, dAu, ra, l, rt.s, rt.m * CB::RA, rt.n * CB::RB, dXp);
   }
   if (lr.parts && tr.first < (tr.hi - lr.cut) * lr.parts) {   // a piece of the last round
     const Tile rt = row_tile(ra.mbase, ra.S, NT, lr.cut + tr.first / lr.parts);
