@@ -61,4 +61,4 @@ def test_permute_maps_and_rows(name):
     np.testing.assert_array_equal(host(ptok)[:N], o_tok)
     np.testing.assert_array_equal(host(inv), o_inv)
     np.testing.assert_allclose(host(pgate)[:N], o_gate, rtol=2e-6)
-    np.testing.assert_array_equal(host(Xp)[:N], host(X)[o_tok])
+    np.testing.assert_array_equal(host(Xp[:N]), host(X)[o_tok])
