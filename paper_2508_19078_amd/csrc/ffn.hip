@@ -547,6 +547,11 @@ constexpr int B16_ROWS = CB::RA;   // rows per row tile of the bf16 kernels
 // (128 x 256) and a quarter (128 x 128), same waves and slab depth.
 using CBH = B16Cfg<128, 256, 2, 4, 64, 3, 2>;
 using CBQ = B16Cfg<128, 128, 2, 4, 64, 3, 2>;
+// A narrow tile for a last column tile over I with at most 128 columns left
+// (I = 1408: 1280..1407) in dH and dW_down: its slabs move 3/4 of a full
+// tile's bytes for half the flops, where a full tile would multiply a half
+// that is never written back.
+using CBN = B16Cfg<256, 128, 2, 4, 64, 3, 2>;
 
 // The XCD's share of a row-tile product (row_range) goes in rounds of one full
 // tile per block.  When the last round would leave at least half of the XCD's
@@ -615,9 +620,10 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
   using S = Stage<bf16, C::RB>;
   constexpr int CH = C::RB / 8;                     // 8-column chunks per row
   constexpr int PER = C::RA * CH / C::THREADS;      // chunks per lane
-  constexpr int G = 8;                              // chunks in flight per lane
-  static_assert(PER % G == 0 && PER * C::THREADS == C::RA * CH && C::RA * C::RB * 2 <= C::LDS && CH == 32,
-                "whole chunks per lane, a row per half-wave");
+  constexpr int G = PER < 8 ? PER : 8;              // chunks in flight per lane
+  static_assert(PER % G == 0 && PER * C::THREADS == C::RA * CH && C::RA * C::RB * 2 <= C::LDS &&
+                    (CH == 32 || CH == 16),
+                "whole chunks per lane, a row per half or quarter wave");
   // thread index re-read here (opaque), so that the per-chunk addresses are
   // not hoisted out of the tile loop and kept live through the main loop
   const int tid = wave_id() * 64 + lane_id_here();
@@ -669,13 +675,14 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
         st16(dAg + (size_t)r * ldo + c, pack16(dg, (bf16*)nullptr));
         st16(dAu + (size_t)r * ldo + c, pack16(du, (bf16*)nullptr));
       }
-      // the 32 lanes of this row (one half of the wave, CH = 32 chunks)
+      // the CH lanes of this row (half or a quarter of the wave); a 128-column
+      // tile gives the same sums as a 256-column tile whose other half is zero
 #pragma unroll
-      for (int off = 16; off > 0; off >>= 1) {
+      for (int off = CH / 2; off > 0; off >>= 1) {
         sa += __shfl_xor(sa, off);
         sh += __shfl_xor(sh, off);
       }
-      if ((tid & 31) == 0 && r < rows) norms[(size_t)r * P] = make_float2(sa, sh);
+      if ((tid & (CH - 1)) == 0 && r < rows) norms[(size_t)r * P] = make_float2(sa, sh);
     }
   }
   barrier_lds();
@@ -935,14 +942,14 @@ __global__ __launch_bounds__(CB::THREADS) void kb_down(LayerPtrs<bf16> W, cbp H,
 }
 
 // dH = dO W_down (B = W_down read k-major), epilogue dA_g, dA_u; one tile of
-// shape C (C::RB = 256: the epilogue takes whole 256-column rows) at rows m0
-// of slot s, column tile n.
+// shape C at rows m0 of slot s, column tile n (of 256 columns; C::RB = 128 for
+// a last column tile with at most 128 columns left).
 template <class C>
 __device__ __forceinline__ void dh_tile(const LayerPtrs<bf16>& W, cbp dO, cbp Ag, cbp Au, const RowArgs& ra,
                                         FM_LDS char* lds, int s, int m0, int n, int NT, bf16* dAg, bf16* dAu,
                                         float2* norms) {
-  static_assert(C::RB == CB::RB, "whole column tiles");
-  const int d = ra.d, I = ra.I, n0 = n * C::RB;
+  static_assert(C::RB == CB::RB || C::RB == CBN::RB, "whole or narrow column tiles");
+  const int d = ra.d, I = ra.I, n0 = n * CB::RB;
   const SlotRows sr = slot_rows(s, ra.offsets, ra.S_r, ra.Tn, ra.k);
   const int rows = sr.nrows - m0;
   if (rows <= 0) return;
@@ -966,7 +973,9 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dh(LayerPtrs<bf16> W, cbp dO, 
   const LastRound lr = last_round(tr, false);
   for (long long t = tr.lo + tr.first; t < lr.cut; t += tr.step) {
     const Tile rt = row_tile(ra.mbase, ra.S, NT, t);
-    if (rows_left(ra, rt.s, rt.m * CB::RA) <= CBH::RA)
+    if (ra.I - rt.n * CB::RB <= CBN::RB)
+      dh_tile<CBN>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA, rt.n, NT, dAg, dAu, norms);
+    else if (rows_left(ra, rt.s, rt.m * CB::RA) <= CBH::RA)
       dh_tile<CBH>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA, rt.n, NT, dAg, dAu, norms);
     else
       dh_tile<CB>(W, dO, Ag, Au, ra, l, rt.s, rt.m * CB::RA, rt.n, NT, dAg, dAu, norms);
@@ -1130,12 +1139,8 @@ __global__ __launch_bounds__(CB::THREADS) void kb_dw_gu(LayerPtrs<bf16> W, cbp X
   }
 }
 
-// dW_down = dO^T H (both read k-major).  Rows over d, columns over I.  A last
-// column tile with at most 128 columns left (I = 1408: 1280..1407) is computed
-// as a 256 x 128 tile (CBN): its slabs move 3/4 of a full tile's bytes and it
-// stores half the output, where a full tile would multiply and store a half
-// that is never written back.
-using CBN = B16Cfg<256, 128, 2, 4, 64, 3, 2>;
+// dW_down = dO^T H (both read k-major).  Rows over d, columns over I; a last
+// column tile with at most 128 columns left runs as a 256 x 128 tile (CBN).
 // Band height of the dW_down tile order: the XCDs are dealt tiles t = 8 j + x,
 // so with 8 row tiles per band (d = 2048: the whole slot) the last column's 8
 // tiles of a band land on 8 different XCDs, one narrow tile each.
