@@ -688,7 +688,8 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
   barrier_lds();
 }
 
-// [A_g | A_u] = X_s [W_gate | W_up]^T, H = silu(A_g) A_u.  The B tile
+// [A_g | A_u] = X_s [W_gate | W_up]^T, H = silu(A_g) A_u (from A_g, A_u as
+// stored in bf16, the values the backward reads).  The B tile
 // interleaves 32-row blocks of W_gate and W_up (RB / 2 intermediate columns per
 // tile): tile j = 2jj of a wave holds gate and j = 2jj + 1 up of the same
 // columns.  One tile of shape C at rows m0 of slot s, intermediate columns n0.
@@ -721,24 +722,28 @@ __device__ __forceinline__ void gate_up_tile(const LayerPtrs<bf16>& W, cbp X, cb
         SG::put4(su, c.row, deinter(c.col4), acc.quad(i, 2 * jj + 1, q));
       }
   barrier_lds_writes();
-  SG::template copy_out<C::RA, C::THREADS>(sg, Ag + ob * I + n0, I, rows, cols);
-  SG::template copy_out<C::RA, C::THREADS>(su, Au + ob * I + n0, I, rows, cols);
-  barrier_lds();
+  // Each lane takes 8-column chunks of A_g and A_u, stores them, and forms H
+  // from the same bf16 values (the ones the backward reads).
+  constexpr int TOTAL = C::RA * SG::CPR;
+  const int tid = wave_id() * 64 + lane_id_here();
+#pragma unroll 4
+  for (int idx = tid; idx < TOTAL; idx += C::THREADS) {
+    const int row = idx / SG::CPR, c = idx % SG::CPR;
+    const uint32_t off = row * SG::ROW_BYTES + ((c ^ (row & (SG::CPR - 1))) << 4);
+    const u32x4_t g = *(const FM_LDS u32x4_t*)(sg + off);
+    const u32x4_t u = *(const FM_LDS u32x4_t*)(su + off);
+    if (row < rows && c * SG::EPC < cols) {
+      const size_t o = (ob + row) * I + n0 + c * SG::EPC;
+      st16(Ag + o, g);
+      st16(Au + o, u);
+      float a[8], v[8], h[8];
+      unpack16(g, a, (bf16*)nullptr);
+      unpack16(u, v, (bf16*)nullptr);
 #pragma unroll
-  for (int i = 0; i < C::MI; ++i)
-#pragma unroll
-    for (int jj = 0; jj < C::NJ / 2; ++jj)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const AccCoord c = b16_coord<C>(i, 2 * jj, q);
-        const f32x4_t ag = acc.quad(i, 2 * jj, q), u = acc.quad(i, 2 * jj + 1, q);
-        f32x4_t h;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) h[r] = ag[r] * sigm_fast(ag[r]) * u[r];
-        SG::put4(sg, c.row, deinter(c.col4), h);
-      }
-  barrier_lds_writes();
-  SG::template copy_out<C::RA, C::THREADS>(sg, H + ob * I + n0, I, rows, cols);
+      for (int e = 0; e < 8; ++e) h[e] = a[e] * sigm_fast(a[e]) * v[e];
+      st16(H + o, pack16(h, (bf16*)nullptr));
+    }
+  }
   barrier_lds();
 }
 
