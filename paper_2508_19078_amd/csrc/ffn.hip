@@ -597,6 +597,27 @@ __device__ __forceinline__ void b16_store_staged(const B16Acc<C::MI, C::NJ>& acc
   barrier_lds();
 }
 
+// x moved between lanes by a DPP control within each 16-lane row.
+template <int CTRL> __device__ __forceinline__ float dpp_f(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+
+// Sum of x over aligned groups of N = 16 or 32 lanes, in every lane of the
+// group: quad permutes (lane ^ 1, lane ^ 2), the half-row mirror (quad pairs)
+// and the row mirror (half-row pairs) inside each row of 16, then one exchange
+// across the two rows for N = 32.  Each step adds a lane's value to a partner
+// holding a sum over the other, equally sized part, so every lane of the group
+// ends with the same bits.
+template <int N> __device__ __forceinline__ float row_lanes_sum(float x) {
+  static_assert(N == 16 || N == 32, "one or two DPP rows");
+  x += dpp_f<0xB1>(x);    // quad_perm [1, 0, 3, 2]
+  x += dpp_f<0x4E>(x);    // quad_perm [2, 3, 0, 1]
+  x += dpp_f<0x141>(x);   // row_half_mirror
+  x += dpp_f<0x140>(x);   // row_mirror
+  if (N == 32) x += __shfl_xor(x, 16);
+  return x;
+}
+
 // SwiGLU backward of a dH tile with s = logistic(a_g): dA_u = dH a_g s,
 // dA_g = dH u s (1 + a_g (1 - s)).  dH is staged through LDS rounded to bf16
 // (the precision a bf16 product would hand to the elementwise step), the
@@ -677,11 +698,8 @@ __device__ __forceinline__ void b16_dswiglu_staged(const B16Acc<C::MI, C::NJ>& a
       }
       // the CH lanes of this row (half or a quarter of the wave); a 128-column
       // tile gives the same sums as a 256-column tile whose other half is zero
-#pragma unroll
-      for (int off = CH / 2; off > 0; off >>= 1) {
-        sa += __shfl_xor(sa, off);
-        sh += __shfl_xor(sh, off);
-      }
+      sa = row_lanes_sum<CH>(sa);
+      sh = row_lanes_sum<CH>(sh);
       if ((tid & (CH - 1)) == 0 && r < rows) norms[(size_t)r * P] = make_float2(sa, sh);
     }
   }
